@@ -1,0 +1,364 @@
+"""Pins for the float64 oracle (CPU only).
+
+Every check here ties the oracle to something other than itself: closed forms
+derived by hand from the paper's definitions, torch's float64
+scaled_dot_product_attention (a library routine the banded softmax reduces to),
+scalar brute-force loops written independently of the vectorised oracle,
+invariants the definitions imply, and the one number the paper prints about
+the band (Sec. 4.2).  A dropped term, a wrong sign or index, or a transposed
+operand in the oracle fails at least one of them.
+"""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import fmm_ref as ref
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def rnd(shape, seed, std=1.0):
+    return np.random.default_rng(seed).standard_normal(shape) * std
+
+
+def sig(x):
+    return 1.0 / (1.0 + math.exp(-x))
+
+
+# ------------------------------------------------------------------ brute force
+# Scalar loops, written from the definitions with the math module only.
+
+def bf_elu(x):
+    return x if x > 0 else math.exp(x) - 1.0
+
+
+def bf_phi(x, l):
+    return bf_elu(x) + 1.0 if l == 1 else bf_elu(-x) + 1.0
+
+
+def bf_near(qs, ks, vs, kw, causal):
+    n, d = len(qs), len(qs[0])
+    out = []
+    for i in range(n):
+        js = [j for j in range(n) if (i - kw <= j <= i if causal else abs(i - j) <= kw)]
+        sc = [sum(qs[i][c] * ks[j][c] for c in range(d)) / math.sqrt(d) for j in js]
+        m = max(sc)
+        w = [math.exp(s - m) for s in sc]
+        tot = sum(w)
+        out.append([sum(w[t] * vs[j][c] for t, j in enumerate(js)) / tot for c in range(d)])
+    return np.array(out)
+
+
+def bf_far(qs, ks, vs, rank, causal):
+    n, d = len(qs), len(qs[0])
+    out = np.zeros((n, d))
+    for l in range(1, rank + 1):
+        for i in range(n):
+            js = range(i + 1) if causal else range(n)
+            a = {j: sum(bf_phi(qs[i][c], l) * bf_phi(ks[j][c], l) for c in range(d)) for j in js}
+            tot = sum(a.values())
+            for c in range(d):
+                out[i, c] += sum(a[j] * vs[j][c] for j in js) / tot
+    return out
+
+
+# ------------------------------------------------------------------ primitives
+
+def test_phi_closed_forms():
+    e = math.exp
+    assert ref.phi(np.array(1.5), 1) == pytest.approx(2.5)
+    assert ref.phi(np.array(-1.0), 1) == pytest.approx(e(-1.0))
+    assert ref.phi(np.array(0.0), 1) == pytest.approx(1.0)
+    assert ref.phi(np.array(1.0), 2) == pytest.approx(e(-1.0))
+    assert ref.phi(np.array(-2.0), 2) == pytest.approx(3.0)
+    assert ref.phi(np.array(0.0), 2) == pytest.approx(1.0)
+    # phi_2(x) = phi_1(-x) and both are strictly positive
+    x = rnd(1000, 0) * 5
+    assert np.array_equal(ref.phi(x, 2), ref.phi(-x, 1))
+    assert (ref.phi(x, 1) > 0).all() and (ref.phi(x, 2) > 0).all()
+    with pytest.raises(ValueError):
+        ref.phi(x, 3)
+
+
+def test_sigmoid_closed_forms():
+    assert ref.sigmoid(0.0) == 0.5
+    assert ref.sigmoid(math.log(3.0)) == pytest.approx(0.75)
+    assert ref.sigmoid(np.inf) == 1.0
+    assert ref.sigmoid(-np.inf) == 0.0
+
+
+def test_band_coverage_matches_paper():
+    g = json.load(open(os.path.join(GOLDEN, "band_coverage.json")))
+    n, k = g["n"], g["half_width_k"]
+    mask = ref.band_mask(n, k, causal=False)
+    assert mask.sum(axis=1).max() == g["paper_bandwidth"]
+    pct = 100.0 * mask.sum() / n ** 2
+    assert round(pct, g["printed_digits"]) == g["fraction_percent"]
+
+
+# ------------------------------------------------------------------ near field
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("form", ["dense", "stream"])
+def test_near_full_band_is_softmax_attention(causal, form):
+    # k >= N-1: the band is the whole (causal) matrix, so Eq. (3) is Eq. (1).
+    b, h, n, d = 2, 3, 37, 8
+    q, k, v = (rnd((b, h, n, d), s) for s in (1, 2, 3))
+    fn = ref.near_dense if form == "dense" else ref.near_stream
+    for kw in (n - 1, n, n + 5):
+        got = fn(q, k, v, kw, causal)
+        want = torch.nn.functional.scaled_dot_product_attention(
+            torch.from_numpy(q), torch.from_numpy(k), torch.from_numpy(v),
+            is_causal=causal).numpy()
+        np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("kw", [0, 1, 3, 6])
+def test_near_band_is_masked_softmax_attention(causal, kw):
+    b, h, n, d = 1, 2, 29, 5
+    q, k, v = (rnd((b, h, n, d), s) for s in (4, 5, 6))
+    allowed = np.zeros((n, n), dtype=bool)
+    for i in range(n):
+        for j in range(n):
+            allowed[i, j] = (i - kw <= j <= i) if causal else (i - kw <= j <= i + kw)
+    want = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q), torch.from_numpy(k), torch.from_numpy(v),
+        attn_mask=torch.from_numpy(allowed)).numpy()
+    for fn in (ref.near_dense, ref.near_stream):
+        np.testing.assert_allclose(fn(q, k, v, kw, causal), want, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_near_brute_force(causal):
+    n, d = 11, 3
+    q, k, v = (rnd((1, 1, n, d), s) for s in (7, 8, 9))
+    for kw in (0, 1, 2, 4, 20):
+        want = bf_near(q[0, 0].tolist(), k[0, 0].tolist(), v[0, 0].tolist(), kw, causal)
+        np.testing.assert_allclose(ref.near_stream(q, k, v, kw, causal)[0, 0], want,
+                                   rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_near_zero_width_is_v(causal):
+    q, k, v = (rnd((2, 2, 17, 4), s) for s in (10, 11, 12))
+    for fn in (ref.near_dense, ref.near_stream):
+        np.testing.assert_array_equal(fn(q, k, v, 0, causal), v)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_near_zero_queries_average_the_band(causal):
+    n, d, kw = 23, 4, 3
+    k, v = rnd((1, 1, n, d), 13), rnd((1, 1, n, d), 14)
+    q = np.zeros_like(k)
+    got = ref.near_stream(q, k, v, kw, causal)[0, 0]
+    for i in range(n):
+        lo, hi = max(0, i - kw), (i if causal else min(n - 1, i + kw))
+        np.testing.assert_allclose(got[i], v[0, 0, lo:hi + 1].mean(axis=0), rtol=1e-12)
+
+
+def test_near_translation_equivariance_interior():
+    # Shifting the whole sequence by one position shifts interior near rows.
+    n, d, kw = 30, 4, 3
+    q, k, v = (rnd((1, 1, n + 1, d), s) for s in (15, 16, 17))
+    a = ref.near_stream(q[:, :, :n], k[:, :, :n], v[:, :, :n], kw, False)
+    b = ref.near_stream(q[:, :, 1:], k[:, :, 1:], v[:, :, 1:], kw, False)
+    np.testing.assert_allclose(a[0, 0, kw + 1:n - kw], b[0, 0, kw:n - kw - 1], rtol=1e-12)
+
+
+# ------------------------------------------------------------------ far field
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("rank", [1, 2])
+def test_far_brute_force(causal, rank):
+    n, d = 9, 3
+    q, k, v = (rnd((1, 1, n, d), s) for s in (20, 21, 22))
+    want = bf_far(q[0, 0].tolist(), k[0, 0].tolist(), v[0, 0].tolist(), rank, causal)
+    for fn in (ref.far_dense, ref.far_stream):
+        np.testing.assert_allclose(fn(q, k, v, rank, causal)[0, 0], want, rtol=1e-12,
+                                   atol=1e-12)
+
+
+def test_far_rank2_closed_form():
+    # d = 1, keys (1, -1), values (1, 0).  phi_1(k) = (2, 1/e), phi_2(k) = (1/e, 2),
+    # and with d = 1 the query factor cancels in each map, so every row is
+    # 2/(2 + 1/e) + (1/e)/(1/e + 2) = 1.  Using elu(x)+1 for both maps, or
+    # dropping a denominator, gives a different value.
+    k = np.array([1.0, -1.0]).reshape(1, 1, 2, 1)
+    v = np.array([1.0, 0.0]).reshape(1, 1, 2, 1)
+    q = np.array([0.3, -2.0]).reshape(1, 1, 2, 1)
+    for fn in (ref.far_dense, ref.far_stream):
+        np.testing.assert_allclose(fn(q, k, v, 2, False)[0, 0, :, 0], [1.0, 1.0], rtol=1e-14)
+        one = fn(q, k, v, 1, False)[0, 0, :, 0]
+        np.testing.assert_allclose(one, [2.0 / (2.0 + math.exp(-1))] * 2, rtol=1e-14)
+    # causal row 0 sees only key 0, row 1 sees both
+    c = ref.far_stream(q, k, v, 2, True)[0, 0, :, 0]
+    np.testing.assert_allclose(c, [2.0, 1.0], rtol=1e-14)
+
+
+def test_far_two_dim_closed_form():
+    # d = 2 so that the query does not cancel: one query (0, 1), keys (0, 0) and
+    # (1, 0), values (1, 0) and (0, 1), rank 1.  phi_1(q) = (1, 2),
+    # phi_1(k_0) = (1, 1), phi_1(k_1) = (2, 1); a_0 = 1 + 2 = 3, a_1 = 2 + 2 = 4;
+    # far = (3 v_0 + 4 v_1) / 7.
+    q = np.array([[0.0, 1.0], [0.0, 1.0]]).reshape(1, 1, 2, 2)
+    k = np.array([[0.0, 0.0], [1.0, 0.0]]).reshape(1, 1, 2, 2)
+    v = np.array([[1.0, 0.0], [0.0, 1.0]]).reshape(1, 1, 2, 2)
+    for fn in (ref.far_dense, ref.far_stream):
+        np.testing.assert_allclose(fn(q, k, v, 1, False)[0, 0, 0], [3 / 7, 4 / 7], rtol=1e-14)
+    np.testing.assert_allclose(ref.far_stream(q, k, v, 1, True)[0, 0, 1], [3 / 7, 4 / 7],
+                               rtol=1e-14)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_far_zero_qk_is_mean(causal):
+    n, d = 19, 3
+    v = rnd((1, 2, n, d), 23)
+    z = np.zeros_like(v)
+    for rank in (1, 2):
+        got = ref.far_stream(z, z, v, rank, causal)
+        if causal:
+            want = np.cumsum(v, axis=2) / np.arange(1, n + 1)[None, None, :, None]
+        else:
+            want = np.broadcast_to(v.mean(axis=2, keepdims=True), v.shape)
+        np.testing.assert_allclose(got, rank * want, rtol=1e-12, atol=1e-14)
+
+
+def test_far_permutation_invariance_noncausal():
+    n, d = 21, 4
+    q, k, v = (rnd((1, 1, n, d), s) for s in (24, 25, 26))
+    p = np.random.default_rng(0).permutation(n)
+    a = ref.far_stream(q, k, v, 2, False)
+    b = ref.far_stream(q, k[:, :, p], v[:, :, p], 2, False)
+    np.testing.assert_allclose(a, b, rtol=1e-12)
+
+
+def test_far_rank_bounded_by_feature_width():
+    # Prop. 1 analogue (Eq. (10)): each phi_l(Q) phi_l(K)^T has rank <= d, so the
+    # row-normalised far map of r feature maps has rank <= r d.
+    n, d = 39, 3
+    q, k = rnd((1, 1, n, d), 27), rnd((1, 1, n, d), 28)
+    eye = np.eye(n)
+    for rank in (1, 2):
+        # far applied to unit value vectors, d columns at a time, exposes the
+        # N x N far matrix itself
+        cols = []
+        for j0 in range(0, n, d):
+            v = eye[:, j0:j0 + d].reshape(1, 1, n, d)
+            cols.append(ref.far_dense(q, k, v, rank, False)[0, 0])
+        m = np.concatenate(cols, axis=1)
+        np.testing.assert_allclose(m.sum(axis=1), rank, rtol=1e-12)
+        s = np.linalg.svd(m, compute_uv=False)
+        assert (s > 1e-10 * s[0]).sum() <= rank * d
+        assert (s > 1e-10 * s[0]).sum() > (rank - 1) * d
+
+
+# ------------------------------------------------------------------ blend / whole op
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_equal_value_rows_give_weighted_sum(causal):
+    b, h, n, d = 1, 3, 16, 4
+    q, k = rnd((b, h, n, d), 29), rnd((b, h, n, d), 30)
+    c = rnd(d, 31)
+    v = np.broadcast_to(c, (b, h, n, d)).copy()
+    wn, wf = rnd(h, 32), rnd(h, 33)
+    for rank in (1, 2):
+        out = ref.fmm_attention_stream(q, k, v, wn, wf, 3, rank, causal)
+        for hh in range(h):
+            coef = sig(wn[hh]) + rank * sig(wf[hh])
+            np.testing.assert_allclose(out[0, hh], np.broadcast_to(coef * c, (n, d)),
+                                       rtol=1e-12)
+
+
+def test_causal_first_row():
+    q, k, v = (rnd((2, 2, 12, 4), s) for s in (34, 35, 36))
+    wn, wf = rnd(2, 37), rnd(2, 38)
+    for rank in (1, 2):
+        out = ref.fmm_attention_stream(q, k, v, wn, wf, 5, rank, True)
+        for hh in range(2):
+            coef = sig(wn[hh]) + rank * sig(wf[hh])
+            np.testing.assert_allclose(out[:, hh, 0], coef * v[:, hh, 0], rtol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_blend_isolates_parts(causal):
+    q, k, v = (rnd((1, 2, 14, 4), s) for s in (39, 40, 41))
+    inf = np.inf
+    near = ref.fmm_attention_stream(q, k, v, np.array([inf, inf]), np.array([-inf, -inf]),
+                                    3, 2, causal)
+    far = ref.fmm_attention_stream(q, k, v, np.array([-inf, -inf]), np.array([inf, inf]),
+                                   3, 2, causal)
+    np.testing.assert_array_equal(near, ref.near_stream(q, k, v, 3, causal))
+    np.testing.assert_array_equal(far, ref.far_stream(q, k, v, 2, causal))
+    half = ref.fmm_attention_stream(q, k, v, np.zeros(2), np.zeros(2), 3, 2, causal)
+    np.testing.assert_allclose(half, 0.5 * near + 0.5 * far, rtol=1e-14)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_each_part_is_convex_combination(causal):
+    n, d, kw = 25, 3, 4
+    q, k, v = (rnd((1, 1, n, d), s, 2.0) for s in (42, 43, 44))
+    near = ref.near_stream(q, k, v, kw, causal)[0, 0]
+    vs = v[0, 0]
+    for i in range(n):
+        lo, hi = max(0, i - kw), (i if causal else min(n - 1, i + kw))
+        assert (near[i] >= vs[lo:hi + 1].min(axis=0) - 1e-12).all()
+        assert (near[i] <= vs[lo:hi + 1].max(axis=0) + 1e-12).all()
+    for rank in (1, 2):
+        far = ref.far_stream(q, k, v, rank, causal)[0, 0] / rank
+        for i in range(n):
+            hi = i if causal else n - 1
+            assert (far[i] >= vs[:hi + 1].min(axis=0) - 1e-12).all()
+            assert (far[i] <= vs[:hi + 1].max(axis=0) + 1e-12).all()
+
+
+def test_linear_in_values():
+    q, k, v1, v2 = (rnd((1, 2, 18, 4), s) for s in (45, 46, 47, 48))
+    wn, wf = rnd(2, 49), rnd(2, 50)
+    for causal in (False, True):
+        f = lambda v: ref.fmm_attention_stream(q, k, v, wn, wf, 2, 2, causal)
+        np.testing.assert_allclose(f(2.0 * v1 - 3.0 * v2), 2.0 * f(v1) - 3.0 * f(v2),
+                                   rtol=1e-10, atol=1e-12)
+
+
+# ------------------------------------------------------------------ forms agree
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 4), (2, 3, 17, 8), (1, 2, 64, 16), (1, 1, 130, 4)])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("rank", [1, 2])
+def test_dense_equals_stream(shape, causal, rank):
+    q, k, v = (rnd(shape, s) for s in (51, 52, 53))
+    wn, wf = rnd(shape[1], 54), rnd(shape[1], 55)
+    for kw in (0, 2, 7, shape[2] + 3):
+        a = ref.fmm_attention_dense(q, k, v, wn, wf, kw, rank, causal)
+        b = ref.fmm_attention_stream(q, k, v, wn, wf, kw, rank, causal)
+        np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-12)
+
+
+def test_stream_chunking_is_invisible():
+    q, k, v = (rnd((1, 2, 300, 4), s) for s in (56, 57, 58))
+    for causal in (False, True):
+        a = ref.far_stream(q, k, v, 2, causal, row_chunk=7)
+        b = ref.far_stream(q, k, v, 2, causal, row_chunk=512)
+        np.testing.assert_allclose(a, b, rtol=1e-12)
+        c = ref.near_stream(q, k, v, 9, causal, row_chunk=13)
+        e = ref.near_stream(q, k, v, 9, causal)
+        np.testing.assert_allclose(c, e, rtol=1e-12)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_rows_form_equals_stream(causal):
+    b, h, n, d = 2, 2, 150, 8
+    q, k, v = (rnd((b, h, n, d), s) for s in (59, 60, 61))
+    wn, wf = rnd(h, 62), rnd(h, 63)
+    full = ref.fmm_attention_stream(q, k, v, wn, wf, 6, 2, causal)
+    rows = [149, 0, 3, 77, 77, 6, 148]
+    for bb in range(b):
+        for hh in range(h):
+            got = ref.fmm_attention_rows(q, k, v, wn, wf, 6, 2, causal, bb, hh, rows)
+            np.testing.assert_allclose(got, full[bb, hh, rows], rtol=1e-12, atol=1e-13)
