@@ -1,0 +1,155 @@
+/*
+ * fmm_attn.h - C ABI of the FMMformer attention forward operator on AMD
+ * MI355X (gfx950).
+ *
+ * The operator (FMMformer, arXiv 2108.02347) blends a banded softmax "near
+ * field" with a kernelized low-rank "far field", per batch b, head h and
+ * query row i, with tau = 1/sqrt(d):
+ *
+ *   near_i = sum_{j in J(i)} exp(tau q_i.k_j) v_j / sum_{j in J(i)} exp(tau q_i.k_j)
+ *            J(i) = [i-k, i+k] clipped to [0, N-1]    (causal: [i-k, i])
+ *            -- Sec. 3.1, Eq. (3); entries outside the band are excluded.
+ *   far_i  = sum_{l=1..rank} phi_l(q_i)^T S_l(i) / phi_l(q_i)^T z_l(i)
+ *            S_l(i) = sum_{j in F(i)} phi_l(k_j) v_j^T,  z_l(i) = sum_{j in F(i)} phi_l(k_j)
+ *            F(i) = [0, N-1]                           (causal: [0, i])
+ *            -- Sec. 3.2.1, Eq. (7)-(9); causal form by truncating the sum at i.
+ *            phi_1(x) = elu(x)+1, phi_2(x) = elu(-x)+1 (elementwise)
+ *            -- Sec. 3.2.1, "Feature map selection".
+ *   out_i  = sigmoid(w_near[h]) * near_i + sigmoid(w_far[h]) * far_i
+ *            -- Sec. 3.3, Eq. (11).
+ *
+ * Each feature map is normalised on its own, as Eq. (9) writes it, so the far
+ * rows carry total weight `rank`.  The far sum runs over all of F(i), the band
+ * included.  There is no epsilon in the far denominator (phi_1, phi_2 > 0).
+ *
+ * Layout: q, k, v and out are contiguous [B, H, N, d] arrays (d innermost) in
+ * device memory, 16-byte aligned.  w_near and w_far are device float[H] raw
+ * logits; the library applies the sigmoid (+inf and -inf select or remove a
+ * part exactly).  All accumulation is in fp32.
+ *
+ * Ownership: the caller owns every pointer passed in.  The library keeps none
+ * of them past the work it enqueues on `stream`.
+ *
+ * Asynchrony: every forward entry point validates its arguments on the host,
+ * then enqueues its kernels on `stream` (a hipStream_t; NULL = the default
+ * stream) and returns without synchronising.  Faults inside kernels surface
+ * at the caller's next synchronisation.
+ *
+ * Errors: functions return an int status.  On any error nothing is enqueued
+ * and `out` is left untouched.  No C++ exception crosses this interface.
+ */
+#ifndef FMM_ATTN_H
+#define FMM_ATTN_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------- */
+#define FMM_OK               0
+#define FMM_ERR_INVALID_ARG (-1) /* null pointer, B/H/N/d < 1, band_k < 0,
+                                    causal not 0/1, misaligned pointer,
+                                    out overlapping q, k or v, or a shape whose
+                                    element count does not fit in int64 */
+#define FMM_ERR_UNSUPPORTED (-2) /* d not in {16, 32, 64}, rank not in {1, 2},
+                                    or dtype code unknown */
+#define FMM_ERR_HIP         (-3) /* a HIP runtime call or kernel launch failed */
+#define FMM_ERR_OOM         (-4) /* workspace allocation failed, or a
+                                    caller-provided workspace is too small */
+
+/* dtype codes for fmm_attn_forward_ws */
+#define FMM_DTYPE_F32  0
+#define FMM_DTYPE_BF16 1
+
+/* kernel ids for the timing interface */
+#define FMM_KERNEL_SEG_STATE     0 /* per-segment phi(K)^T [V | 1] totals      */
+#define FMM_KERNEL_STATE_COMBINE 1 /* sum (non-causal) or exclusive scan       */
+#define FMM_KERNEL_BAND_APPLY    2 /* non-causal near field + far apply + blend */
+#define FMM_KERNEL_CAUSAL_APPLY  3 /* causal near field + prefix far + blend    */
+#define FMM_KERNEL_COUNT         4
+
+/*
+ * fmm_attn_forward - the operator of Eq. (9) blended as in Eq. (11), fp32.
+ *   q, k, v : const float*, [B, H, N, d]; read only.
+ *   out     : float*, [B, H, N, d]; written completely; must not overlap
+ *             q, k or v (the kernels read key windows of neighbouring rows
+ *             while writing out).
+ *   B, H, N : batch, heads, sequence length, each >= 1.
+ *   d       : head width, one of 16, 32, 64 (the 1/sqrt(d) of Eq. (1)).
+ *   band_k  : near-field half-width k >= 0 (2k+1 entries per interior row;
+ *             causal: k+1).  k >= N-1 makes the near field full softmax
+ *             attention.
+ *   rank    : number of feature maps, 1 (phi_1) or 2 (phi_1, phi_2).
+ *   causal  : 0 or 1.
+ *   w_near, w_far : device float[H], raw blend logits.
+ *   stream  : hipStream_t or NULL.
+ * Uses a library-owned workspace per (device, stream), grown on demand
+ * (the first call for a larger shape allocates; see fmm_attn_forward_ws for a
+ * caller-owned workspace).  Two calls on the same stream are ordered by the
+ * stream; calls on different streams use different workspaces.
+ */
+int fmm_attn_forward(const void* q, const void* k, const void* v, void* out,
+                     int B, int H, int N, int d, int band_k, int rank,
+                     int causal, const float* w_near, const float* w_far,
+                     void* stream);
+
+/*
+ * fmm_attn_forward_bf16 - same operator and arguments, with q, k, v and out
+ * holding bf16 values (__hip_bfloat16).  Products that feed the matrix cores
+ * take bf16 operands; every sum is accumulated in fp32; out is rounded to
+ * bf16 (round to nearest even).
+ */
+int fmm_attn_forward_bf16(const void* q, const void* k, const void* v, void* out,
+                          int B, int H, int N, int d, int band_k, int rank,
+                          int causal, const float* w_near, const float* w_far,
+                          void* stream);
+
+/*
+ * fmm_attn_workspace_bytes - device bytes fmm_attn_forward_ws needs for this
+ * shape (the far-field segment states).  Returns 0 for invalid or unsupported
+ * arguments.
+ */
+size_t fmm_attn_workspace_bytes(int B, int H, int N, int d, int rank, int causal);
+
+/*
+ * fmm_attn_forward_ws - the operator with a caller-owned device workspace of
+ * at least fmm_attn_workspace_bytes(...) bytes, 256-byte aligned.  dtype is
+ * FMM_DTYPE_F32 or FMM_DTYPE_BF16.  Allocates nothing.  Calls that overlap in
+ * time must not share a workspace.  FMM_ERR_OOM if ws_bytes is too small.
+ */
+int fmm_attn_forward_ws(const void* q, const void* k, const void* v, void* out,
+                        int B, int H, int N, int d, int band_k, int rank,
+                        int causal, const float* w_near, const float* w_far,
+                        int dtype, void* workspace, size_t ws_bytes, void* stream);
+
+/* Human-readable text for a status code; never NULL, static storage. */
+const char* fmm_attn_status_string(int status);
+
+/*
+ * Frees every library-owned workspace after synchronising the devices that
+ * hold one.  Safe to call at any time from the host when no other thread is
+ * inside the library.
+ */
+void fmm_attn_release_workspace(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int fmm_attn_version(void);
+
+/*
+ * Kernel timing (profiling aid).  fmm_attn_kernel_timing(1) makes every later
+ * forward call record a pair of HIP events around each kernel it launches, on
+ * the launch stream; fmm_attn_kernel_timing(0) stops recording.
+ * fmm_attn_kernel_timing_read waits for the recorded events, writes the total
+ * elapsed milliseconds and the number of launches of kernel `kernel`
+ * (FMM_KERNEL_*) since the last read, and clears that kernel's record.
+ */
+int fmm_attn_kernel_timing(int enable);
+int fmm_attn_kernel_timing_read(int kernel, double* total_ms, long long* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FMM_ATTN_H */

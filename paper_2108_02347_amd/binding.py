@@ -1,0 +1,175 @@
+"""ctypes binding of libfmm_attn.so (the C ABI declared in include/fmm_attn.h).
+
+Argument marshalling only: every step of the operator runs in the HIP library.
+PyTorch supplies device memory and the current stream.  If the library has not
+been built, every call raises; there is no fallback implementation.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfmm_attn.so")
+
+FMM_OK = 0
+FMM_ERR_INVALID_ARG = -1
+FMM_ERR_UNSUPPORTED = -2
+FMM_ERR_HIP = -3
+FMM_ERR_OOM = -4
+
+FMM_DTYPE_F32 = 0
+FMM_DTYPE_BF16 = 1
+
+KERNELS = {"seg_state": 0, "state_combine": 1, "band_apply": 2, "causal_apply": 3}
+
+EXPORTS = (
+    "fmm_attn_forward", "fmm_attn_forward_bf16", "fmm_attn_workspace_bytes",
+    "fmm_attn_forward_ws", "fmm_attn_status_string", "fmm_attn_release_workspace",
+    "fmm_attn_version", "fmm_attn_kernel_timing", "fmm_attn_kernel_timing_read",
+)
+
+_lib = None
+
+
+class FmmError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(msg)
+        self.status = status
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library (once); raises if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is missing: build it with `python -m paper_2108_02347_amd.build_lib` "
+            "(there is no non-HIP fallback)")
+    h = ctypes.CDLL(LIB_PATH)
+    vp, ci, cf = ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p
+    fwd_args = [vp, vp, vp, vp, ci, ci, ci, ci, ci, ci, ci, cf, cf, vp]
+    for name in ("fmm_attn_forward", "fmm_attn_forward_bf16"):
+        fn = getattr(h, name)
+        fn.argtypes = fwd_args
+        fn.restype = ci
+    h.fmm_attn_forward_ws.argtypes = fwd_args[:-1] + [ci, vp, ctypes.c_size_t, vp]
+    h.fmm_attn_forward_ws.restype = ci
+    h.fmm_attn_workspace_bytes.argtypes = [ci] * 6
+    h.fmm_attn_workspace_bytes.restype = ctypes.c_size_t
+    h.fmm_attn_status_string.argtypes = [ci]
+    h.fmm_attn_status_string.restype = ctypes.c_char_p
+    h.fmm_attn_release_workspace.argtypes = []
+    h.fmm_attn_release_workspace.restype = None
+    h.fmm_attn_version.argtypes = []
+    h.fmm_attn_version.restype = ci
+    h.fmm_attn_kernel_timing.argtypes = [ci]
+    h.fmm_attn_kernel_timing.restype = ci
+    h.fmm_attn_kernel_timing_read.argtypes = [ci, ctypes.POINTER(ctypes.c_double),
+                                              ctypes.POINTER(ctypes.c_longlong)]
+    h.fmm_attn_kernel_timing_read.restype = ci
+    _lib = h
+    return h
+
+
+def status_string(status: int) -> str:
+    return lib().fmm_attn_status_string(status).decode()
+
+
+def version() -> int:
+    return lib().fmm_attn_version()
+
+
+def release_workspace() -> None:
+    lib().fmm_attn_release_workspace()
+
+
+def workspace_bytes(B: int, H: int, N: int, d: int, rank: int, causal: int) -> int:
+    return int(lib().fmm_attn_workspace_bytes(B, H, N, d, rank, int(causal)))
+
+
+def _check(status: int) -> None:
+    if status != FMM_OK:
+        raise FmmError(status, status_string(status))
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _stream_of(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _shape(q: torch.Tensor):
+    if q.dim() != 4:
+        raise ValueError("q, k, v must be [B, H, N, d]")
+    return tuple(int(x) for x in q.shape)
+
+
+def _prep(q, k, v, w_near, w_far):
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous CUDA/HIP tensor")
+        if t.dtype != q.dtype or t.shape != q.shape or t.device != q.device:
+            raise ValueError("q, k, v must share dtype, shape and device")
+    if q.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("q, k, v must be float32 or bfloat16")
+    B, H, N, d = _shape(q)
+    ws = []
+    for name, w in (("w_near", w_near), ("w_far", w_far)):
+        if (not w.is_cuda or w.dtype != torch.float32 or w.numel() != H
+                or not w.is_contiguous() or w.device != q.device):
+            raise ValueError(f"{name} must be a contiguous float32 device tensor of H values")
+        ws.append(w)
+    return B, H, N, d
+
+
+def forward(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool, out=None):
+    """FMMformer attention forward; returns out (allocated if not given)."""
+    B, H, N, d = _prep(q, k, v, w_near, w_far)
+    if out is None:
+        out = torch.empty_like(q)
+    fn = lib().fmm_attn_forward_bf16 if q.dtype == torch.bfloat16 else lib().fmm_attn_forward
+    _check(fn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, int(band_k), int(rank),
+              int(bool(causal)), _ptr(w_near), _ptr(w_far), _stream_of(q)))
+    return out
+
+
+def forward_ws(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool, workspace,
+               out=None):
+    """Same operator with a caller-owned workspace (a uint8 device tensor)."""
+    B, H, N, d = _prep(q, k, v, w_near, w_far)
+    if out is None:
+        out = torch.empty_like(q)
+    dt = FMM_DTYPE_BF16 if q.dtype == torch.bfloat16 else FMM_DTYPE_F32
+    _check(lib().fmm_attn_forward_ws(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, int(band_k), int(rank),
+        int(bool(causal)), _ptr(w_near), _ptr(w_far), dt, _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream_of(q)))
+    return out
+
+
+def raw_forward(q_ptr, k_ptr, v_ptr, out_ptr, B, H, N, d, band_k, rank, causal, wn_ptr,
+                wf_ptr, stream_ptr, bf16: bool) -> int:
+    """Direct call of the C entry point with raw pointers; returns the status."""
+    fn = lib().fmm_attn_forward_bf16 if bf16 else lib().fmm_attn_forward
+    v = ctypes.c_void_p
+    return fn(v(q_ptr), v(k_ptr), v(v_ptr), v(out_ptr), B, H, N, d, band_k, rank, causal,
+              v(wn_ptr), v(wf_ptr), v(stream_ptr))
+
+
+def kernel_timing(enable: bool) -> None:
+    _check(lib().fmm_attn_kernel_timing(int(bool(enable))))
+
+
+def kernel_timing_read(kernel: str):
+    """(total_ms, launches) of one kernel since the previous read."""
+    ms = ctypes.c_double(0.0)
+    n = ctypes.c_longlong(0)
+    _check(lib().fmm_attn_kernel_timing_read(KERNELS[kernel], ctypes.byref(ms),
+                                             ctypes.byref(n)))
+    return ms.value, n.value

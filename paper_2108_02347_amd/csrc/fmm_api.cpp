@@ -1,0 +1,297 @@
+// C ABI of the FMMformer attention forward operator: argument validation,
+// segment planning, the per-(device, stream) workspace cache and the optional
+// kernel timer.  Every kernel is launched asynchronously on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+#include <stdlib.h>
+
+#include <map>
+#include <mutex>
+#include <utility>
+#include <vector>
+
+#include "../../include/fmm_attn.h"
+#include "fmm_launch.h"
+
+namespace {
+
+constexpr int kVersion = 1 * 10000 + 0 * 100 + 0;
+
+// ------------------------------------------------------------------ planning
+// Segments split the key axis of every (batch, head) slice for the far-field
+// state: enough segments to give the GPU about 512 workgroups, but long enough
+// that the per-segment state (rank * d * (d+1) floats) stays at most a quarter
+// of the key/value bytes it summarises.
+struct Plan {
+  int nseg;
+  int L;
+  size_t ws_bytes;
+};
+
+Plan make_plan(int B, int H, int N, int d, int rank, int esize) {
+  const int tm = fmm::tile_rows();
+  const long long bh = (long long)B * H;
+  const long long target = bh >= 512 ? 1 : (512 + bh - 1) / bh;
+  long long L = (N + target - 1) / target;
+  const long long lmin = 8LL * rank * (d + 1) / esize;  // state <= 1/4 of K+V bytes
+  if (L < lmin) L = lmin;
+  L = (L + tm - 1) / tm * tm;
+  if (L < tm) L = tm;
+  Plan p;
+  p.L = (int)L;
+  p.nseg = (int)((N + L - 1) / L);
+  const size_t rec = (size_t)rank * d * (d + 1);
+  p.ws_bytes = ((size_t)bh * p.nseg + (size_t)bh) * rec * sizeof(float);
+  p.ws_bytes = (p.ws_bytes + 255) / 256 * 256;
+  return p;
+}
+
+bool supported(int d, int rank) {
+  return (d == 16 || d == 32 || d == 64) && (rank == 1 || rank == 2);
+}
+
+bool overlaps(const void* a, const void* b, size_t n) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + n && y < x + n;
+}
+
+int validate(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
+             int d, int band_k, int rank, int causal, const float* w_near, const float* w_far,
+             int dtype) {
+  if (!q || !k || !v || !out || !w_near || !w_far) return FMM_ERR_INVALID_ARG;
+  if (B < 1 || H < 1 || N < 1 || d < 1 || band_k < 0) return FMM_ERR_INVALID_ARG;
+  if (causal != 0 && causal != 1) return FMM_ERR_INVALID_ARG;
+  if (dtype != FMM_DTYPE_F32 && dtype != FMM_DTYPE_BF16) return FMM_ERR_UNSUPPORTED;
+  if (!supported(d, rank)) return FMM_ERR_UNSUPPORTED;
+  const long long elems = (long long)B * H * N * d;
+  if (elems / d / N / H != B) return FMM_ERR_INVALID_ARG;
+  const size_t es = dtype == FMM_DTYPE_BF16 ? 2 : 4;
+  if (elems > (long long)(INT64_MAX / (long long)es)) return FMM_ERR_INVALID_ARG;
+  for (const void* p : {q, k, v, (const void*)out})
+    if ((uintptr_t)p % 16) return FMM_ERR_INVALID_ARG;
+  if ((uintptr_t)w_near % 4 || (uintptr_t)w_far % 4) return FMM_ERR_INVALID_ARG;
+  const size_t bytes = (size_t)elems * es;
+  if (overlaps(out, q, bytes) || overlaps(out, k, bytes) || overlaps(out, v, bytes))
+    return FMM_ERR_INVALID_ARG;
+  return FMM_OK;
+}
+
+// ------------------------------------------------------------------ timing
+struct EventTimer : fmm::LaunchTimer {
+  std::mutex mu;
+  bool enabled = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> pending[FMM_KERNEL_COUNT];
+  std::vector<hipEvent_t> pool;
+  hipEvent_t cur = nullptr;
+
+  hipEvent_t take() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+  void begin(int, hipStream_t s) override {
+    if (!enabled) return;
+    cur = take();
+    if (cur) hipEventRecord(cur, s);
+  }
+  void end(int kernel, hipStream_t s) override {
+    if (!enabled || !cur) return;
+    hipEvent_t stop = take();
+    if (!stop) return;
+    hipEventRecord(stop, s);
+    pending[kernel].push_back({cur, stop});
+    cur = nullptr;
+  }
+};
+
+EventTimer& timer() {
+  static EventTimer* t = new EventTimer();
+  return *t;
+}
+
+// ------------------------------------------------------------------ workspace
+struct WsEntry {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+
+std::mutex& ws_mutex() {
+  static std::mutex* m = new std::mutex();
+  return *m;
+}
+std::map<std::pair<int, void*>, WsEntry>& ws_map() {
+  static auto* m = new std::map<std::pair<int, void*>, WsEntry>();
+  return *m;
+}
+
+size_t ws_limit() {
+  const char* s = getenv("FMM_ATTN_WS_LIMIT");
+  if (!s || !*s) return (size_t)-1;
+  return (size_t)strtoull(s, nullptr, 10);
+}
+
+// Returns a workspace of at least `bytes` for (current device, stream).
+int acquire_ws(void* stream, size_t bytes, void** out) {
+  if (bytes > ws_limit()) return FMM_ERR_OOM;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return FMM_ERR_HIP;
+  std::lock_guard<std::mutex> g(ws_mutex());
+  WsEntry& e = ws_map()[{dev, stream}];
+  if (e.bytes < bytes) {
+    if (e.ptr) {
+      // kernels enqueued earlier on this stream may still read the old buffer
+      if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return FMM_ERR_HIP;
+      hipFree(e.ptr);
+      e.ptr = nullptr;
+      e.bytes = 0;
+    }
+    void* p = nullptr;
+    if (hipMalloc(&p, bytes) != hipSuccess) {
+      (void)hipGetLastError();
+      return FMM_ERR_OOM;
+    }
+    e.ptr = p;
+    e.bytes = bytes;
+  }
+  *out = e.ptr;
+  return FMM_OK;
+}
+
+int run(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d,
+        int band_k, int rank, int causal, const float* w_near, const float* w_far, int dtype,
+        void* ws, size_t ws_bytes, bool own_ws, void* stream) {
+  int st = validate(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype);
+  if (st != FMM_OK) return st;
+  const Plan p = make_plan(B, H, N, d, rank, dtype == FMM_DTYPE_BF16 ? 2 : 4);
+  if (own_ws) {
+    st = acquire_ws(stream, p.ws_bytes, &ws);
+    if (st != FMM_OK) return st;
+  } else {
+    if (!ws || (uintptr_t)ws % 256) return FMM_ERR_INVALID_ARG;
+    if (ws_bytes < p.ws_bytes) return FMM_ERR_OOM;
+  }
+  fmm::LaunchArgs a;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.out = out;
+  a.w_near = w_near;
+  a.w_far = w_far;
+  a.B = B;
+  a.H = H;
+  a.N = N;
+  a.d = d;
+  // a half-width of N already covers every key; clamping keeps row +/- k in int range
+  a.band_k = band_k < N ? band_k : N;
+  a.rank = rank;
+  a.causal = causal;
+  a.dtype = dtype;
+  a.stream = stream;
+  a.ws = (float*)ws;
+  a.nseg = p.nseg;
+  a.L = p.L;
+  EventTimer& t = timer();
+  std::lock_guard<std::mutex> g(t.mu);
+  return fmm::launch_forward(a, &t) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fmm_attn_forward(const void* q, const void* k, const void* v, void* out, int B, int H,
+                     int N, int d, int band_k, int rank, int causal, const float* w_near,
+                     const float* w_far, void* stream) {
+  return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, FMM_DTYPE_F32,
+             nullptr, 0, true, stream);
+}
+
+int fmm_attn_forward_bf16(const void* q, const void* k, const void* v, void* out, int B, int H,
+                          int N, int d, int band_k, int rank, int causal, const float* w_near,
+                          const float* w_far, void* stream) {
+  return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, FMM_DTYPE_BF16,
+             nullptr, 0, true, stream);
+}
+
+size_t fmm_attn_workspace_bytes(int B, int H, int N, int d, int rank, int causal) {
+  if (B < 1 || H < 1 || N < 1 || (causal != 0 && causal != 1) || !supported(d, rank)) return 0;
+  // the plan depends on the element size only through the segment length
+  // floor; report the larger of the two dtypes' needs
+  const Plan a = make_plan(B, H, N, d, rank, 2), b = make_plan(B, H, N, d, rank, 4);
+  return a.ws_bytes > b.ws_bytes ? a.ws_bytes : b.ws_bytes;
+}
+
+int fmm_attn_forward_ws(const void* q, const void* k, const void* v, void* out, int B, int H,
+                        int N, int d, int band_k, int rank, int causal, const float* w_near,
+                        const float* w_far, int dtype, void* workspace, size_t ws_bytes,
+                        void* stream) {
+  return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype, workspace,
+             ws_bytes, false, stream);
+}
+
+const char* fmm_attn_status_string(int status) {
+  switch (status) {
+    case FMM_OK: return "FMM_OK: success";
+    case FMM_ERR_INVALID_ARG:
+      return "FMM_ERR_INVALID_ARG: null, negative, misaligned or overlapping argument";
+    case FMM_ERR_UNSUPPORTED: return "FMM_ERR_UNSUPPORTED: d must be 16, 32 or 64 and rank 1 or 2";
+    case FMM_ERR_HIP: return "FMM_ERR_HIP: a HIP runtime call or kernel launch failed";
+    case FMM_ERR_OOM: return "FMM_ERR_OOM: workspace allocation failed or workspace too small";
+    default: return "unknown fmm_attn status";
+  }
+}
+
+void fmm_attn_release_workspace(void) {
+  std::lock_guard<std::mutex> g(ws_mutex());
+  int cur = 0;
+  const bool have_cur = hipGetDevice(&cur) == hipSuccess;
+  for (auto& kv : ws_map()) {
+    if (!kv.second.ptr) continue;
+    hipSetDevice(kv.first.first);
+    hipDeviceSynchronize();
+    hipFree(kv.second.ptr);
+  }
+  ws_map().clear();
+  if (have_cur) hipSetDevice(cur);
+}
+
+int fmm_attn_version(void) { return kVersion; }
+
+int fmm_attn_kernel_timing(int enable) {
+  EventTimer& t = timer();
+  std::lock_guard<std::mutex> g(t.mu);
+  t.enabled = enable != 0;
+  return FMM_OK;
+}
+
+int fmm_attn_kernel_timing_read(int kernel, double* total_ms, long long* launches) {
+  if (kernel < 0 || kernel >= FMM_KERNEL_COUNT || !total_ms || !launches)
+    return FMM_ERR_INVALID_ARG;
+  EventTimer& t = timer();
+  std::lock_guard<std::mutex> g(t.mu);
+  double sum = 0.0;
+  long long n = 0;
+  int st = FMM_OK;
+  for (auto& pr : t.pending[kernel]) {
+    float ms = 0.f;
+    if (hipEventSynchronize(pr.second) != hipSuccess ||
+        hipEventElapsedTime(&ms, pr.first, pr.second) != hipSuccess)
+      st = FMM_ERR_HIP;
+    sum += ms;
+    ++n;
+    t.pool.push_back(pr.first);
+    t.pool.push_back(pr.second);
+  }
+  t.pending[kernel].clear();
+  *total_ms = sum;
+  *launches = n;
+  return st;
+}
+
+}  // extern "C"

@@ -1,0 +1,83 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/fmm_attn.h declares, and rejects bad arguments on the
+host before touching the HIP runtime."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2108_02347_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fmm_attn.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fmm_attn_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = binding.lib()
+    names = declared_functions()
+    assert len(names) >= 9
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(binding.EXPORTS)
+
+
+def test_status_strings_and_version():
+    assert binding.version() == 10000
+    for st in (0, -1, -2, -3, -4):
+        assert binding.status_string(st).startswith(
+            {0: "FMM_OK", -1: "FMM_ERR_INVALID_ARG", -2: "FMM_ERR_UNSUPPORTED",
+             -3: "FMM_ERR_HIP", -4: "FMM_ERR_OOM"}[st])
+    assert "unknown" in binding.status_string(17)
+
+
+def test_workspace_bytes():
+    ws = binding.workspace_bytes
+    assert ws(1, 8, 65536, 64, 2, 1) > 0
+    assert ws(1, 8, 65536, 64, 2, 1) % 256 == 0
+    # one state record per segment plus one final record, rank * d * (d+1) floats
+    assert ws(1, 1, 64, 16, 1, 0) >= 2 * 16 * 17 * 4
+    assert ws(1, 1, 64, 48, 1, 0) == 0      # unsupported width
+    assert ws(1, 1, 64, 16, 3, 0) == 0      # unsupported rank
+    assert ws(0, 1, 64, 16, 1, 0) == 0
+
+
+FAKE = 1 << 20  # aligned non-null addresses; never dereferenced on the error paths
+
+
+def call(q=FAKE, k=2 * FAKE, v=3 * FAKE, out=4 * FAKE, B=1, H=2, N=64, d=32, kw=5, r=2, c=0,
+         wn=5 * FAKE, wf=6 * FAKE, bf16=False):
+    return binding.raw_forward(q, k, v, out, B, H, N, d, kw, r, c, wn, wf, 0, bf16)
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(q=0), binding.FMM_ERR_INVALID_ARG),
+    (dict(out=0), binding.FMM_ERR_INVALID_ARG),
+    (dict(wn=0), binding.FMM_ERR_INVALID_ARG),
+    (dict(B=0), binding.FMM_ERR_INVALID_ARG),
+    (dict(N=-3), binding.FMM_ERR_INVALID_ARG),
+    (dict(kw=-1), binding.FMM_ERR_INVALID_ARG),
+    (dict(c=2), binding.FMM_ERR_INVALID_ARG),
+    (dict(q=FAKE + 8), binding.FMM_ERR_INVALID_ARG),          # misaligned
+    (dict(out=FAKE + 64), binding.FMM_ERR_INVALID_ARG),       # overlaps q
+    (dict(d=48), binding.FMM_ERR_UNSUPPORTED),
+    (dict(d=128), binding.FMM_ERR_UNSUPPORTED),
+    (dict(r=3), binding.FMM_ERR_UNSUPPORTED),
+    (dict(r=0), binding.FMM_ERR_UNSUPPORTED),
+    (dict(d=48, bf16=True), binding.FMM_ERR_UNSUPPORTED),
+])
+def test_host_validation(kwargs, status):
+    assert call(**kwargs) == status
+
+
+def test_timing_read_rejects_bad_kernel_id():
+    lib = binding.lib()
+    ms, n = ctypes.c_double(), ctypes.c_longlong()
+    assert lib.fmm_attn_kernel_timing_read(9, ctypes.byref(ms), ctypes.byref(n)) == -1
