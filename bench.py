@@ -1,0 +1,266 @@
+"""Throughput benchmark of the FMMformer attention forward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+Workload (the 2^16-token configuration): B=1, H=8, N=65536, d=64, bf16 storage
+with fp32 accumulation, band half-width k=64, rank 2 (elu(x)+1, elu(-x)+1),
+q, k, v ~ N(0, 1/8^2).  One step = one non-causal and one causal forward over
+the same resident inputs (both forms of the operator), so a step processes
+2 * B * N token-forwards.  Inputs are generated once and stay in HBM.
+
+Printed: one JSON line with the whole-job throughput, the roofline of the
+dominant kernel (algorithmic bytes per launch over its mean duration, timed
+with HIP events recorded by the library on the launch stream during the timed
+steps), the same figures at N=4096 (B=8, H=2, d=32, k=20), and the float64
+CPU oracle timed on a bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+METRIC = "FMM attention fwd tokens/sec at N=4096 & 65536; % of HBM roofline"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--no-cpu-baseline", action="store_true",
+                   help="skip the oracle timing (used when profiling)")
+    p.add_argument("--profile-only", action="store_true",
+                   help="run only warmup + timed steps of the main workload, print nothing else")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="run a plain 256 MiB device copy (for counter calibration) and exit")
+    return p.parse_args()
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2108_02347_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    with the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith("#"):
+            a, b = line.split(":", 1)
+            kv[a.strip()] = b.strip()
+    if kv.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def make_device_inputs(name, dtype, torch):
+    from paper_2108_02347_amd.inputs import workload_inputs
+    dt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    q, k, v, wn, wf = workload_inputs(name, dtype)
+    dev = "cuda:0"
+    tq, tk, tv = (torch.from_numpy(x.astype("float32")).to(dev).to(dt).contiguous()
+                  for x in (q, k, v))
+    twn, twf = (torch.from_numpy(x.astype("float32")).to(dev) for x in (wn, wf))
+    return (q, k, v, wn, wf), (tq, tk, tv, twn, twf)
+
+
+def timed(fn, steps, warmup, torch):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) / steps
+
+
+def cpu_baseline(host_inputs, w):
+    """Oracle (float64 numpy, single BLAS thread) on head 0 of the workload,
+    full sequence, both forms."""
+    import numpy as np
+    from oracle import fmm_ref as ref
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    q, k, v, wn, wf = host_inputs
+    sl = (slice(0, 1), slice(0, 1))
+    qs, ks, vs = (np.ascontiguousarray(x[sl]) for x in (q, k, v))
+    import contextlib
+    ctx = threadpool_limits(limits=1) if threadpool_limits else contextlib.nullcontext()
+    with ctx:
+        t0 = time.perf_counter()
+        for causal in (False, True):
+            ref.fmm_attention_stream(qs, ks, vs, wn[:1], wf[:1], w.band_k, w.rank, causal)
+    dt = time.perf_counter() - t0
+    # one head of H processed in both forms -> 2 * N / H token-forwards
+    tokens = 2.0 * w.B * w.N / w.H
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"head 0 of {w.H}, batch 0, all {w.N} rows, non-causal + causal "
+                      f"forward (float64 numpy, 1 BLAS thread); {dt:.1f} s for "
+                      f"{tokens:.0f} token-forwards"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); the operator "
+              "is single-GPU in this build, see DESIGN.md for how it would shard.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2108_02347_amd import binding
+    from paper_2108_02347_amd.inputs import WORKLOADS
+
+    if args.copy_calibration:
+        n = 256 << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda:0").random_()
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "launches": 5}))
+        return
+
+    w = WORKLOADS["stress64k"]
+    host, (tq, tk, tv, twn, twf) = make_device_inputs("stress64k", "bf16", torch)
+    out_nc = torch.empty_like(tq)
+    out_c = torch.empty_like(tq)
+
+    def step():
+        binding.forward(tq, tk, tv, twn, twf, w.band_k, w.rank, 0, out=out_nc)
+        binding.forward(tq, tk, tv, twn, twf, w.band_k, w.rank, 1, out=out_c)
+
+    if args.profile_only:
+        timed(step, args.steps, args.warmup, torch)
+        return
+
+    for name in binding.KERNELS:
+        binding.kernel_timing_read(name)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    binding.kernel_timing(True)
+    t_step = timed(step, args.steps, 0, torch)
+    binding.kernel_timing(False)
+    kt = {}
+    for name in binding.KERNELS:
+        ms, n = binding.kernel_timing_read(name)
+        kt[name] = ms / n if n else None
+
+    X = w.B * w.H * w.N * w.d * 2  # bytes of one bf16 [B, H, N, d] tensor
+    alg_bytes = {"seg_state": 2 * X, "band_apply": 4 * X, "causal_apply": 4 * X}
+    per_kernel = {
+        name: {"mean_us": round(kt[name] * 1e3, 3),
+               **({"alg_GBps": round(alg_bytes[name] / (kt[name] * 1e-3) / 1e9, 1),
+                   "hbm_frac": round(alg_bytes[name] / (kt[name] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+                  if name in alg_bytes else {})}
+        for name in kt if kt[name]}
+    # dominant kernel: the largest time share per step (seg_state runs twice)
+    share = {"band_apply": kt["band_apply"], "causal_apply": kt["causal_apply"],
+             "seg_state": 2 * kt["seg_state"]}
+    dom = max(share, key=share.get)
+    ach = alg_bytes[dom] / (kt[dom] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(ach, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                "traffic": read_traffic(dom, "stress64k"),
+                "algorithmic_bytes_per_launch": alg_bytes[dom],
+                "mean_launch_us": round(kt[dom] * 1e3, 3)}
+
+    # per-form throughput on the same inputs
+    t_nc = timed(lambda: binding.forward(tq, tk, tv, twn, twf, w.band_k, w.rank, 0, out=out_nc),
+                 args.steps, 2, torch)
+    t_c = timed(lambda: binding.forward(tq, tk, tv, twn, twf, w.band_k, w.rank, 1, out=out_c),
+                args.steps, 2, torch)
+
+    # N = 4096 (long-range retrieval shape), non-causal
+    w4 = WORKLOADS["lra4k"]
+    _, (q4, k4, v4, wn4, wf4) = make_device_inputs("lra4k", "bf16", torch)
+    o4 = torch.empty_like(q4)
+    f4 = lambda: binding.forward(q4, k4, v4, wn4, wf4, w4.band_k, w4.rank, 0, out=o4)
+    for name in binding.KERNELS:
+        binding.kernel_timing_read(name)
+    t4 = timed(f4, args.steps, args.warmup, torch)
+    binding.kernel_timing(True)
+    timed(f4, args.steps, 0, torch)
+    binding.kernel_timing(False)
+    X4 = w4.B * w4.H * w4.N * w4.d * 2
+    kt4 = {}
+    for name in binding.KERNELS:
+        ms, n = binding.kernel_timing_read(name)
+        if n:
+            kt4[name] = ms / n
+    n4096 = {
+        "workload": "lra4k: B=8 H=2 N=4096 d=32 bf16 k=20 rank=2 non-causal",
+        "tokens_per_s": round(w4.B * w4.N / t4, 1), "ms_per_call": round(t4 * 1e3, 4),
+        "op_hbm_frac_4X": round(4 * X4 / t4 / 1e9 / HBM_PEAK_GBS, 4),
+        "kernels": {name: {"mean_us": round(ms * 1e3, 3),
+                           **({"alg_GBps": round(b / (ms * 1e-3) / 1e9, 1)}
+                              if (b := {"seg_state": 2 * X4, "band_apply": 4 * X4}.get(name))
+                              else {})}
+                    for name, ms in kt4.items()},
+    }
+
+    tokens_per_step = 2 * w.B * w.N
+    rec = {
+        "metric": METRIC,
+        "value": round(tokens_per_step / t_step, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_step * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "stress64k: B=1 H=8 N=65536 d=64 bf16 storage, fp32 accumulate, "
+                        "k=64, rank 2, q/k/v ~ N(0, 1/64); step = non-causal + causal forward",
+            "global_batch": w.B, "seq_len": w.N, "heads": w.H, "head_dim": w.d,
+            "band_k": w.band_k, "rank": w.rank, "forward_calls_per_step": 2,
+            "parallelism": "single-gpu",
+        },
+        "roofline": roofline,
+        "forms": {
+            "noncausal": {"tokens_per_s": round(w.B * w.N / t_nc, 1),
+                          "ms_per_call": round(t_nc * 1e3, 4),
+                          "op_hbm_frac_4X": round(4 * X / t_nc / 1e9 / HBM_PEAK_GBS, 4)},
+            "causal": {"tokens_per_s": round(w.B * w.N / t_c, 1),
+                       "ms_per_call": round(t_c * 1e3, 4),
+                       "op_hbm_frac_4X": round(4 * X / t_c / 1e9 / HBM_PEAK_GBS, 4)},
+        },
+        "kernels": per_kernel,
+        "n4096": n4096,
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(host, w)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()
