@@ -26,21 +26,34 @@ constexpr int kVersion = 1 * 10000 + 0 * 100 + 0;
 struct Plan {
   int nseg;
   int L;
+  int nseg_apply;
+  int L_apply;
   size_t ws_bytes;
 };
+
+// Rows per segment so that B*H*segments is about `target_wg` workgroups.
+long long seg_rows(long long bh, int N, long long target_wg, int tm) {
+  const long long per_slice = bh >= target_wg ? 1 : (target_wg + bh - 1) / bh;
+  long long L = (N + per_slice - 1) / per_slice;
+  L = (L + tm - 1) / tm * tm;
+  return L < tm ? tm : L;
+}
 
 Plan make_plan(int B, int H, int N, int d, int rank, int esize) {
   const int tm = fmm::tile_rows();
   const long long bh = (long long)B * H;
-  const long long target = bh >= 512 ? 1 : (512 + bh - 1) / bh;
-  long long L = (N + target - 1) / target;
-  const long long lmin = 8LL * rank * (d + 1) / esize;  // state <= 1/4 of K+V bytes
-  if (L < lmin) L = lmin;
-  L = (L + tm - 1) / tm * tm;
-  if (L < tm) L = tm;
+  // state segments: ~512 workgroups, but each segment's state record
+  // (rank*d*(d+1) floats) at most a quarter of the K+V bytes it summarises
+  long long L = seg_rows(bh, N, 512, tm);
+  const long long lmin = 8LL * rank * (d + 1) / esize;
+  if (L < lmin) L = (lmin + tm - 1) / tm * tm;
+  // non-causal apply walk: ~512 workgroups (two per CU), no state per segment
+  const long long La = seg_rows(bh, N, 512, tm);
   Plan p;
   p.L = (int)L;
   p.nseg = (int)((N + L - 1) / L);
+  p.L_apply = (int)La;
+  p.nseg_apply = (int)((N + La - 1) / La);
   const size_t rec = (size_t)rank * d * (d + 1);
   p.ws_bytes = ((size_t)bh * p.nseg + (size_t)bh) * rec * sizeof(float);
   p.ws_bytes = (p.ws_bytes + 255) / 256 * 256;
@@ -196,6 +209,8 @@ int run(const void* q, const void* k, const void* v, void* out, int B, int H, in
   a.ws = (float*)ws;
   a.nseg = p.nseg;
   a.L = p.L;
+  a.nseg_apply = p.nseg_apply;
+  a.L_apply = p.L_apply;
   EventTimer& t = timer();
   std::lock_guard<std::mutex> g(t.mu);
   return fmm::launch_forward(a, &t) == hipSuccess ? FMM_OK : FMM_ERR_HIP;

@@ -18,8 +18,10 @@ struct LaunchArgs {
   int B, H, N, d, band_k, rank, causal, dtype;
   void* stream;
   float* ws;   // segment states (+ final state for the non-causal form)
-  int nseg;    // segments per (batch, head)
-  int L;       // rows per segment (multiple of the tile height)
+  int nseg;        // state segments per (batch, head)
+  int L;           // rows per state segment (multiple of the tile height)
+  int nseg_apply;  // row segments walked by one non-causal apply workgroup
+  int L_apply;     // rows per apply segment (multiple of the tile height)
 };
 
 // Records HIP events around kernel launches when timing is enabled.

@@ -182,3 +182,16 @@ def test_kernel_timing_counts_launches():
     assert n == 3 and ms > 0
     assert binding.kernel_timing_read("causal_apply")[1] == 1
     assert binding.kernel_timing_read("seg_state")[1] == 4
+
+
+# ------------------------------------------------------------------ ring sizes and wrap-around
+@pytest.mark.parametrize("causal", [0, 1])
+@pytest.mark.parametrize("d,dtype", [(32, "bf16"), (64, "bf16"), (32, "f32")])
+def test_band_widths_across_ring_sizes(d, dtype, causal):
+    # one long slice so every workgroup walks many tiles; half-widths around
+    # the 32-key unit boundaries give odd and even ring sizes, ring wrap-around
+    # of the tile's own keys, and the switch to staged rounds for wide bands
+    worst = 0.0
+    for kw in (1, 31, 32, 33, 64, 65, 100, 250):
+        worst = max(worst, check_full(1, 1, 3000, d, kw, 2, causal, dtype, 700 + kw))
+    log(f"ring sweep d={d} {dtype} causal={causal}: worst {worst:.3e}")
