@@ -8,7 +8,7 @@
 //   k_band_ring      non-causal, band fits the LDS ring: each workgroup walks the
 //                    64-row tiles of a segment; the key/value window slides
 //                    through an LDS ring and the next tile is prefetched into
-//                    registers during compute.  Per tile: banded online softmax
+//                    registers during compute.  Per tile: banded softmax
 //                    (Eq. (3)), far apply phi_l(Q) S_l / phi_l(Q) z_l
 //                    (Eq. (8)-(9)), sigmoid blend (Eq. (11)), store
 //   k_causal_ring    causal, band fits the ring: same walk, with the running
@@ -21,6 +21,11 @@
 // Every workgroup of the apply kernels has NW = 4 wavefronts; wave w owns query
 // rows [16w, 16w+16) of a TM = 64-row tile.  All sums are accumulated in fp32
 // in a fixed order, so results are bit-reproducible run to run.
+//
+// Row sums of the softmax weights and the far-field denominators
+// phi_l(q) . z_l are taken on the matrix cores too: an extra 16-row A block of
+// ones (resp. of z_l broadcast over rows) yields the sum in every lane of the
+// row, so no cross-lane reduction is needed for them.
 //
 // State records (one per segment, and one final record per (batch, head) in
 // the non-causal form) are kept in MFMA tile order: for map l, the d x d block
@@ -35,7 +40,7 @@ namespace fmm {
 constexpr int NW = 4;            // wavefronts per apply workgroup
 constexpr int NT = NW * 64;      // threads per apply workgroup
 constexpr int TM = 16 * NW;      // query rows per tile (= 2 key units)
-constexpr int WK = 192;          // keys staged per round in the rounds kernels
+constexpr int GU = 6;            // key units whose scores are held at once
 
 template <typename T> struct Lay {
   static constexpr int ES = (int)sizeof(T);
@@ -43,16 +48,25 @@ template <typename T> struct Lay {
   static constexpr int PAD = ES == 2 ? 8 : 4;  // row pad (rows stay 16-B aligned)
 };
 
-// Ring capacity limit (in 32-key units) for the apply kernels: the LDS of one
-// workgroup (ring + state fragments) stays within 78 KiB, so two workgroups
-// fit on a CU whatever the band; narrower bands use less and fit more.
+// LDS budgets of the apply kernels.  Ring kernels: ring + state fragments (+
+// the causal tile's feature rows) within 78 KiB, so two workgroups fit on a
+// CU whatever the band (narrower bands use less and fit more); U_NC / U_C is
+// the widest ring, in 32-key units, of the non-causal / causal walk.  Rounds
+// kernels (bands wider than the ring): up to UR units per round within 150 KiB.
 template <typename T, int D, int R> struct Ring {
   static constexpr int ST = D + Lay<T>::PAD;
   static constexpr int UNIT_BYTES = 2 * 32 * ST * (int)sizeof(T);  // K + V
   static constexpr int FRAG_BYTES = R * (D / 16) * (D / 16) * 64 * 4 * (int)sizeof(T) + R * D * 4;
-  static constexpr int BUDGET = 78 * 1024;
-  static constexpr int U = (BUDGET - FRAG_BYTES) / UNIT_BYTES;
-  static size_t bytes(int u) { return (size_t)u * UNIT_BYTES + FRAG_BYTES; }
+  static constexpr int PHI_BYTES = R * TM * ST * (int)sizeof(T);   // causal only
+  static constexpr int BUDGET = 78 * 1024, RBUDGET = 150 * 1024;
+  static constexpr int U_NC = (BUDGET - FRAG_BYTES) / UNIT_BYTES;
+  static constexpr int U_C = (BUDGET - FRAG_BYTES - PHI_BYTES) / UNIT_BYTES;
+  static constexpr int UR_FIT = (RBUDGET - FRAG_BYTES - PHI_BYTES) / UNIT_BYTES;
+  static constexpr int UR = UR_FIT > 6 ? 6 : UR_FIT;
+  static_assert(UR >= 2, "a round must hold one tile of keys");
+  static size_t bytes(int u, bool causal) {
+    return (size_t)u * UNIT_BYTES + FRAG_BYTES + (causal ? PHI_BYTES : 0);
+  }
 };
 
 // ------------------------------------------------------------------ LDS operand reads
@@ -79,10 +93,17 @@ __device__ __forceinline__ float4 ld_tquad(const float* x, int row0, int col0, i
   return make_float4(p[0], p[ld], p[2 * ld], p[3 * ld]);
 }
 
+template <typename T> __device__ __forceinline__ typename QuadOf<T>::type quad_fill(float x) {
+  const float f[4] = {x, x, x, x};
+  return f32_to_quad<T>(f);
+}
+
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
 // ------------------------------------------------------------------ row staging
-// Copy rows [k0, k0 + nrows) of a [N, D] head into LDS rows `dst` (row-major,
-// stride ST); rows outside [0, N) are zero.  `dst_row(i)` gives the LDS row of
-// the i-th copied row.
+// Copy rows [k0, k0 + nrows) of a [N, D] head into LDS (row-major, stride ST);
+// rows outside [0, N) are zero.  `dst_row(i)` gives the LDS row of the i-th
+// copied row.
 template <typename T, int D, int NTHR, int MAXROWS>
 struct RowCopy {
   static constexpr int CPR = D / Lay<T>::EPC;
@@ -109,101 +130,182 @@ struct RowCopy {
   }
 };
 
+// LDS row of the first key of absolute 32-key unit ua.
+struct RingMap {
+  int ua0, U;
+  __device__ __forceinline__ int operator()(int ua) const { return ((ua - ua0) % U) * 32; }
+};
+struct RoundMap {
+  int ks;
+  __device__ __forceinline__ int operator()(int ua) const { return ua * 32 - ks; }
+};
+
 // ------------------------------------------------------------------ near field
-// Online-softmax state of one wavefront's 16-row strip.  Lane (r, g) holds
-// row r; o[nb] holds output columns 16nb + 4g + {0..3}; lsum is this lane's
-// share of the row normaliser (summed over the four lane groups at the end).
+// Softmax state of one wavefront's 16-row strip.  Lane (r, g) holds row r;
+// o[nb] (nb < NB) holds output columns 16nb + 4g + {0..3}; o[NB] holds the
+// row's sum of weights in all four entries; m is the running maximum of the
+// raw scores q.k of the row.
 template <int D> struct NearState {
-  f32x4 o[D / 16];
-  float m, lsum;
+  f32x4 o[D / 16 + 1];
+  float m;
+  bool fresh;
   __device__ __forceinline__ void init() {
 #pragma unroll
-    for (int nb = 0; nb < D / 16; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb <= D / 16; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     m = -INFINITY;
-    lsum = 0.f;
+    fresh = true;
   }
 };
 
-// One 32-key unit of the band for the strip whose lane row is `row`.  kx, vx
-// point at the unit's first K / V row in LDS (row-major, stride ST); j0 is the
-// absolute index of its first key.  Scores use exp2 with tau*log2(e) folded in.
-template <typename T, int D, bool CAUSAL>
-__device__ __forceinline__ void near_unit(NearState<D>& st, const typename QuadOf<T>::type* qq,
-                                          const T* kx, const T* vx, int ST, int j0, int row,
-                                          int N, int band_k, float scale2) {
+// Band units [ua_lo, ua_hi] (32 keys each, in LDS through `map`) for the strip
+// of rows [i0, i0 + 16).  Up to GU units are scored at once, then one row
+// maximum, one exponentiation pass and the P V products; the accumulator is
+// rescaled only between groups.  Exponentials use exp2 with tau*log2(e)
+// folded into the subtraction of the maximum.
+template <typename T, int D, bool CAUSAL, class Map>
+__device__ __forceinline__ void near_units(NearState<D>& st, const typename QuadOf<T>::type* qq,
+                                           const T* kr, const T* vr, int ST, Map map, int ua_lo,
+                                           int ua_hi, int i0, int N, int band_k, float scale2) {
   using Q = typename QuadOf<T>::type;
   constexpr int NB = D / 16;
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
-  f32x4 sc[2];
+  const int row = i0 + r;
+  const Q ones = quad_fill<T>(1.f);
+  for (int u0 = ua_lo; u0 <= ua_hi; u0 += GU) {
+    f32x4 sc[GU][2];
+    float mloc = -INFINITY;
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    Q ka[NB];
+    for (int gi = 0; gi < GU; ++gi) {
+      const int ua = u0 + gi;
+      if (ua > ua_hi) break;
+      const T* kx = kr + map(ua) * ST;
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) ka[cb] = ld_quad(kx, 16 * b + r, 16 * cb + 4 * g, ST);
-    sc[b] = contract<NB>(ka, qq, f32x4{0.f, 0.f, 0.f, 0.f});
-  }
-  float x[2][4];
-  float mloc = -INFINITY;
+      for (int b = 0; b < 2; ++b) {
+        Q ka[NB];
 #pragma unroll
-  for (int b = 0; b < 2; ++b)
+        for (int cb = 0; cb < NB; ++cb) ka[cb] = ld_quad(kx, 16 * b + r, 16 * cb + 4 * g, ST);
+        sc[gi][b] = contract<NB>(ka, qq, f32x4{0.f, 0.f, 0.f, 0.f});
+      }
+      const int j0 = ua * 32;
+      const bool interior = j0 >= 0 && j0 + 31 < N && j0 >= i0 + 15 - band_k &&
+                            (CAUSAL ? j0 + 31 <= i0 : j0 + 31 <= i0 + band_k);
+      if (!interior) {
+        const int dbase = j0 + 4 * g - row;
+        const unsigned span = CAUSAL ? (unsigned)band_k : 2u * (unsigned)band_k;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int j = j0 + 16 * b + 4 * g + i;
-      const bool ok = j >= 0 && j < N && j >= row - band_k &&
-                      (CAUSAL ? j <= row : j <= row + band_k);
-      x[b][i] = ok ? sc[b][i] * scale2 : -INFINITY;
-      mloc = fmaxf(mloc, x[b][i]);
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int dd = dbase + 16 * b + i;
+            const int j = j0 + 16 * b + 4 * g + i;
+            const bool ok = (unsigned)(dd + band_k) <= span && (unsigned)j < (unsigned)N;
+            if (!ok) sc[gi][b][i] = -INFINITY;
+          }
+      }
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) mloc = fmaxf(mloc, sc[gi][b][i]);
     }
-  const float mnew = fmaxf(st.m, col_max(mloc));
-  const float muse = mnew == -INFINITY ? 0.f : mnew;
-  const float alpha = __builtin_amdgcn_exp2f(st.m - muse);
-  st.m = mnew;
-  float p[2][4];
-  float ps = 0.f;
+    const float mnew = fmaxf(st.m, col_max(mloc));
+    const float ms = (mnew == -INFINITY ? 0.f : mnew) * scale2;
+    if (!st.fresh) {
+      const float alpha = __builtin_amdgcn_exp2f(st.m * scale2 - ms);
 #pragma unroll
-  for (int b = 0; b < 2; ++b)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      p[b][i] = round_as<T>(__builtin_amdgcn_exp2f(x[b][i] - muse));
-      ps += p[b][i];
+      for (int nb = 0; nb <= NB; ++nb) st.o[nb] *= alpha;
     }
-  st.lsum = st.lsum * alpha + ps;
-  const Q pq0 = f32_to_quad<T>(p[0]), pq1 = f32_to_quad<T>(p[1]);
+    st.m = mnew;
+    st.fresh = false;
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) {
-    const Q va0 = ld_tquad(vx, 0, 16 * nb, ST);
-    const Q va1 = ld_tquad(vx, 16, 16 * nb, ST);
-    st.o[nb] = mma_step2(va0, va1, pq0, pq1, st.o[nb] * alpha);
+    for (int gi = 0; gi < GU; ++gi) {
+      const int ua = u0 + gi;
+      if (ua > ua_hi) break;
+      float p[2][4];
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[b][i] = __builtin_amdgcn_exp2f(fmaf(sc[gi][b][i], scale2, -ms));
+      const Q pq0 = f32_to_quad<T>(p[0]), pq1 = f32_to_quad<T>(p[1]);
+      const T* vx = vr + map(ua) * ST;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        st.o[nb] = mma_step2(ld_tquad(vx, 0, 16 * nb, ST), ld_tquad(vx, 16, 16 * nb, ST), pq0,
+                             pq1, st.o[nb]);
+      st.o[NB] = mma_step2(ones, ones, pq0, pq1, st.o[NB]);
+    }
   }
 }
 
 // ------------------------------------------------------------------ far field
-// State fragments in LDS: sf[(l*NB + nb)*NB + cb][lane] is the quad
-// S_l[16cb + 4g + {0..3}][16nb + r], the A operand of F^T = S_l^T phi_l(Q)^T;
-// sz[l*D + c] = z_l[c].
-template <typename T, int D>
-__device__ __forceinline__ void far_prefix(const typename QuadOf<T>::type* sf, const float* sz,
-                                           const float* qf, int l, f32x4* num, float& den) {
+// phi_1(q), phi_2(q) of the lane's row as operand quads.
+template <typename T, int D, int R>
+__device__ __forceinline__ void phi_q(const typename QuadOf<T>::type* qq,
+                                      typename QuadOf<T>::type (*pq)[D / 16]) {
+#pragma unroll
+  for (int cb = 0; cb < D / 16; ++cb) {
+    float x[4], p1[4], p2[4];
+    quad_to_f32(qq[cb], x);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) phi12(x[i], p1[i], p2[i]);
+    pq[0][cb] = f32_to_quad<T>(p1);
+    if constexpr (R == 2) pq[1][cb] = f32_to_quad<T>(p2);
+  }
+}
+
+// num[l][nb] += S_l^T phi_l(Q)^T for nb < NB and num[l][NB] += phi_l(q) . z_l
+// (z_l broadcast over the 16 rows of an extra A block).  State fragments:
+// sf[(l*NB + nb)*NB + cb][lane] = S_l[16cb + 4g + {0..3}][16nb + r]; sz = z.
+template <typename T, int D, int R>
+__device__ __forceinline__ void far_terms(const typename QuadOf<T>::type* sf, const float* sz,
+                                          const typename QuadOf<T>::type (*pq)[D / 16],
+                                          f32x4 (*num)[D / 16 + 1]) {
   using Q = typename QuadOf<T>::type;
   constexpr int NB = D / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4;
-  float pf[D / 4];
-  float dpart = 0.f;
 #pragma unroll
-  for (int t = 0; t < D / 4; ++t) {
-    pf[t] = phi_l(qf[t], l);
-    dpart += round_as<T>(pf[t]) * sz[l * D + 16 * (t >> 2) + 4 * g + (t & 3)];
+  for (int l = 0; l < R; ++l) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      Q a[NB];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) a[cb] = sf[((l * NB + nb) * NB + cb) * 64 + lane];
+      num[l][nb] = contract<NB>(a, pq[l], num[l][nb]);
+    }
+    Q zq[NB];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      const float4 z4 = *reinterpret_cast<const float4*>(sz + l * D + 16 * cb + 4 * g);
+      const float f[4] = {z4.x, z4.y, z4.z, z4.w};
+      zq[cb] = f32_to_quad<T>(f);
+    }
+    num[l][NB] = contract<NB>(zq, pq[l], num[l][NB]);
   }
-  den += col_sum(dpart);
-  Q pq[NB];
+}
+
+// out = sigmoid(w_near) near + sigmoid(w_far) sum_l num_l / den_l  (Eq. (11)).
+template <typename T, int D, int R>
+__device__ __forceinline__ void blend_store(T* __restrict__ oh, int row, int N, float sn,
+                                            float sfw, const NearState<D>& st,
+                                            const f32x4 (*num)[D / 16 + 1]) {
+  using Q = typename QuadOf<T>::type;
+  constexpr int NB = D / 16;
+  const int g = (threadIdx.x & 63) >> 4;
+  const float a = sn > 0.f ? sn * fast_rcp(st.o[NB][0]) : 0.f;
+  float f[R];
 #pragma unroll
-  for (int cb = 0; cb < NB; ++cb) pq[cb] = f32_to_quad<T>(pf + 4 * cb);
+  for (int l = 0; l < R; ++l) f[l] = sfw > 0.f ? sfw * fast_rcp(num[l][NB][0]) : 0.f;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    Q a[NB];
+    float o[4];
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) a[cb] = sf[((l * NB + nb) * NB + cb) * 64 + lane];
-    num[nb] = contract<NB>(a, pq, num[nb]);
+    for (int i = 0; i < 4; ++i) {
+      float x = st.o[nb][i] * a;
+#pragma unroll
+      for (int l = 0; l < R; ++l) x = fmaf(num[l][nb][i], f[l], x);
+      o[i] = x;
+    }
+    if (row < N)
+      *reinterpret_cast<Q*>(oh + (size_t)row * D + 16 * nb + 4 * g) = f32_to_quad<T>(o);
   }
 }
 
@@ -236,124 +338,174 @@ __device__ __forceinline__ void load_q(const T* __restrict__ qh, int row, int N,
     qq[cb] = row < N ? *reinterpret_cast<const Q*>(qh + (size_t)row * D + 16 * cb + 4 * g) : Q{};
 }
 
-template <typename T, int D>
-__device__ __forceinline__ void q_floats(const typename QuadOf<T>::type* qq, float* qf) {
+// ------------------------------------------------------------------ causal pieces
+// phi_l of the tile's 64 keys (LDS rows kt0 .. kt0+31 and kt1 .. kt1+31 of the
+// key buffer) into pk[l] (row-major, TM rows); keys at or beyond N give 0.
+template <typename T, int D, int R>
+__device__ __forceinline__ void stage_phi_tile(const T* kbuf, int kt0, int kt1, int ST, int t0,
+                                               int N, T* pk) {
+  using L = Lay<T>;
+  constexpr int CPR = D / L::EPC;
+  for (int t = threadIdx.x; t < TM * CPR; t += NT) {
+    const int key = t / CPR, c = t % CPR;
+    const int src = key < 32 ? kt0 + key : kt1 + key - 32;
+    const uint4 raw = *reinterpret_cast<const uint4*>(kbuf + src * ST + c * L::EPC);
+    float x[L::EPC], p1[L::EPC], p2[L::EPC];
+    if constexpr (sizeof(T) == 2) {
+      const uint16_t* e = reinterpret_cast<const uint16_t*>(&raw);
 #pragma unroll
-  for (int cb = 0; cb < D / 16; ++cb) quad_to_f32(qq[cb], qf + 4 * cb);
-}
-
-// Blend (Eq. (11)) and store one lane's 4 x (D/16) outputs.
-template <typename T, int D>
-__device__ __forceinline__ void blend_store(T* __restrict__ oh, int row, int N, float sn,
-                                            float sfw, const NearState<D>& st, const f32x4* far) {
-  using Q = typename QuadOf<T>::type;
-  const int g = (threadIdx.x & 63) >> 4;
-  const float inv_l = 1.f / col_sum(st.lsum);
+      for (int i = 0; i < L::EPC; ++i) x[i] = bf16_to_f32(e[i]);
+    } else {
+      const float* e = reinterpret_cast<const float*>(&raw);
 #pragma unroll
-  for (int nb = 0; nb < D / 16; ++nb) {
-    float o[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float a = sn > 0.f ? sn * (st.o[nb][i] * inv_l) : 0.f;
-      const float b = sfw > 0.f ? sfw * far[nb][i] : 0.f;
-      o[i] = a + b;
+      for (int i = 0; i < L::EPC; ++i) x[i] = e[i];
     }
-    if (row < N)
-      *reinterpret_cast<Q*>(oh + (size_t)row * D + 16 * nb + 4 * g) = f32_to_quad<T>(o);
+    const bool ok = t0 + key < N;
+#pragma unroll
+    for (int i = 0; i < L::EPC; ++i) {
+      phi12(x[i], p1[i], p2[i]);
+      if (!ok) { p1[i] = 0.f; p2[i] = 0.f; }
+    }
+#pragma unroll
+    for (int l = 0; l < R; ++l) {
+      const float* p = l == 0 ? p1 : p2;
+      uint4 outw;
+      if constexpr (sizeof(T) == 2) {
+        outw = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                          pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+      } else {
+        outw = make_uint4(__float_as_uint(p[0]), __float_as_uint(p[1]), __float_as_uint(p[2]),
+                          __float_as_uint(p[3]));
+      }
+      *reinterpret_cast<uint4*>(pk + l * TM * ST + key * ST + c * L::EPC) = outw;
+    }
   }
 }
 
-// Non-causal far apply for one strip: sum_l phi_l(q) S_l / phi_l(q) z_l.
+// phi_l of the 64 key rows a RowCopy holds in registers (rows k0 .. k0+63 of
+// the head) into pk[l]; rows at or beyond N give 0.  Same chunk-to-thread
+// assignment as RowCopy.
 template <typename T, int D, int R>
-__device__ __forceinline__ void far_apply(const typename QuadOf<T>::type* sf, const float* sz,
-                                          const float* qf, f32x4* far) {
+__device__ __forceinline__ void phi_rows_from_regs(const RowCopy<T, D, NT, 64>& ck, int k0,
+                                                   int N, int ST, T* pk) {
+  using L = Lay<T>;
+  using RC = RowCopy<T, D, NT, 64>;
+#pragma unroll
+  for (int it = 0; it < RC::IT; ++it) {
+    const int t = threadIdx.x + it * NT;
+    if (t >= TM * RC::CPR) continue;
+    const int key = t / RC::CPR, c = t % RC::CPR;
+    const uint4 raw = ck.r[it];
+    float x[L::EPC], p1[L::EPC], p2[L::EPC];
+    if constexpr (sizeof(T) == 2) {
+      const uint16_t* e = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+      for (int i = 0; i < L::EPC; ++i) x[i] = bf16_to_f32(e[i]);
+    } else {
+      const float* e = reinterpret_cast<const float*>(&raw);
+#pragma unroll
+      for (int i = 0; i < L::EPC; ++i) x[i] = e[i];
+    }
+    const bool ok = k0 + key < N;
+#pragma unroll
+    for (int i = 0; i < L::EPC; ++i) {
+      phi12(x[i], p1[i], p2[i]);
+      if (!ok) { p1[i] = 0.f; p2[i] = 0.f; }
+    }
+#pragma unroll
+    for (int l = 0; l < R; ++l) {
+      const float* p = l == 0 ? p1 : p2;
+      uint4 outw;
+      if constexpr (sizeof(T) == 2) {
+        outw = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                          pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+      } else {
+        outw = make_uint4(__float_as_uint(p[0]), __float_as_uint(p[1]), __float_as_uint(p[2]),
+                          __float_as_uint(p[3]));
+      }
+      *reinterpret_cast<uint4*>(pk + l * TM * ST + key * ST + c * L::EPC) = outw;
+    }
+  }
+}
+
+// Intra-tile far part of the strip of wave w: keys [t0, row] of the tile, per
+// map: A = tril(phi_l(K_t) phi_l(q)^T) from pk, num[l][nb] += V^T A and the
+// row sums of A into num[l][NB].  vt0 / vt1: LDS rows of the tile's two V units.
+template <typename T, int D, int R>
+__device__ __forceinline__ void causal_intra(const T* pk, const T* vt0, const T* vt1, int ST,
+                                             int t0, int w,
+                                             const typename QuadOf<T>::type (*pq)[D / 16],
+                                             f32x4 (*num)[D / 16 + 1]) {
+  using Q = typename QuadOf<T>::type;
   constexpr int NB = D / 16;
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const int row = t0 + 16 * w + r;
+  const Q ones = quad_fill<T>(1.f);
+  for (int u = 0; u <= (w >> 1); ++u) {
+    const T* vx = u == 0 ? vt0 : vt1;
+    const bool diag = u == (w >> 1);
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb) far[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int l = 0; l < R; ++l) {
+      const T* pkl = pk + l * TM * ST;
+      float a[2][4];
 #pragma unroll
-  for (int l = 0; l < R; ++l) {
-    f32x4 num[NB];
+      for (int b = 0; b < 2; ++b) {
+        Q ka[NB];
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) num[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float den = 0.f;
-    far_prefix<T, D>(sf, sz, qf, l, num, den);
-    const float inv = 1.f / den;
+        for (int cb = 0; cb < NB; ++cb) ka[cb] = ld_quad(pkl, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
+        const f32x4 at = contract<NB>(ka, pq[l], f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb) far[nb] += num[nb] * inv;
+        for (int i = 0; i < 4; ++i) {
+          const int j = t0 + 32 * u + 16 * b + 4 * g + i;
+          a[b][i] = (!diag || j <= row) ? at[i] : 0.f;
+        }
+      }
+      const Q p0 = f32_to_quad<T>(a[0]), p1 = f32_to_quad<T>(a[1]);
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+        num[l][nb] = mma_step2(ld_tquad(vx, 0, 16 * nb, ST), ld_tquad(vx, 16, 16 * nb, ST), p0,
+                               p1, num[l][nb]);
+      num[l][NB] = mma_step2(ones, ones, p0, p1, num[l][NB]);
+    }
   }
 }
 
 // ------------------------------------------------------------------ state tiles
-// A wave's share of the state T_l = phi_l(K)^T [V | 1]: the (map, feature
-// block) groups ag = w + NW2*a (l = ag / NB, cb = ag % NB), every value block
+// A wave's share of the running state T_l = phi_l(K)^T [V | 1] in the causal
+// walk: groups ag = w + NW*a (l = ag / NB, cb = ag % NB), every value block
 // eb < NB plus the ones column eb = NB that yields z_l.
-template <typename T, int D, int R, int NW2>
+template <typename T, int D, int R>
 struct StateTiles {
   using Q = typename QuadOf<T>::type;
   static constexpr int NB = D / 16;
   static constexpr int AG = R * NB;
-  static constexpr int AGPW = AG >= NW2 ? AG / NW2 : 1;
+  static constexpr int AGPW = AG >= NW ? AG / NW : 1;
+  static_assert(AG < NW || AG % NW == 0, "group split");
   f32x4 acc[AGPW][NB + 1];
 
   __device__ __forceinline__ static bool active(int w) { return w < AG; }
-  __device__ __forceinline__ static int group(int w, int a) { return w + NW2 * a; }
+  __device__ __forceinline__ static int group(int w, int a) { return w + NW * a; }
 
-  __device__ __forceinline__ void zero() {
-#pragma unroll
-    for (int a = 0; a < AGPW; ++a)
-#pragma unroll
-      for (int eb = 0; eb <= NB; ++eb) acc[a][eb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-  // acc += phi_l(K)^T [V | 1] over one 32-key unit at LDS rows kx / vx.
-  // Keys with index >= kvalid (relative to the unit) contribute nothing.
-  __device__ __forceinline__ void add_unit(int w, const T* kx, const T* vx, int ST, int kvalid) {
-    const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  // acc += phi_l(K)^T [V | 1] over one 32-key unit: phi rows from pk (rows
+  // pr .. pr+31 of map l's buffer), V rows at vx.
+  __device__ __forceinline__ void add_unit(int w, const T* pk, int pr, const T* vx, int ST) {
+    const int lane = threadIdx.x & 63, r = lane & 15;
     Q vb0[NB + 1], vb1[NB + 1];
 #pragma unroll
     for (int eb = 0; eb < NB; ++eb) {
       vb0[eb] = ld_tquad(vx, 0, 16 * eb, ST);
       vb1[eb] = ld_tquad(vx, 16, 16 * eb, ST);
     }
-    {
-      float f[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) f[i] = r == 0 ? 1.f : 0.f;
-      vb0[NB] = f32_to_quad<T>(f);
-      vb1[NB] = vb0[NB];
-    }
+    vb0[NB] = quad_fill<T>(r == 0 ? 1.f : 0.f);
+    vb1[NB] = vb0[NB];
 #pragma unroll
     for (int a = 0; a < AGPW; ++a) {
       const int ag = group(w, a);
       const int l = ag / NB, cb = ag % NB;
-      Q aq[2];
+      const T* pkl = pk + l * TM * ST;
+      const Q a0 = ld_tquad(pkl, pr, 16 * cb, ST), a1 = ld_tquad(pkl, pr + 16, 16 * cb, ST);
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        float kf[4], p1[4], p2[4];
-        quad_to_f32(ld_tquad(kx, 16 * b, 16 * cb, ST), kf);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          phi12(kf[i], p1[i], p2[i]);
-          if (16 * b + 4 * g + i >= kvalid) { p1[i] = 0.f; p2[i] = 0.f; }
-        }
-        aq[b] = f32_to_quad<T>(l == 0 ? p1 : p2);
-      }
-#pragma unroll
-      for (int eb = 0; eb <= NB; ++eb)
-        acc[a][eb] = mma_step2(aq[0], aq[1], vb0[eb], vb1[eb], acc[a][eb]);
-    }
-  }
-  // Tile-order record I/O (see the file header).
-  __device__ __forceinline__ void store(int w, float* rec) const {
-    const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
-#pragma unroll
-    for (int a = 0; a < AGPW; ++a) {
-      const int ag = group(w, a);
-      const int l = ag / NB, cb = ag % NB;
-      float* sl = rec + (size_t)l * D * (D + 1);
-#pragma unroll
-      for (int eb = 0; eb < NB; ++eb)
-        *reinterpret_cast<f32x4*>(sl + ((cb * NB + eb) * 64 + lane) * 4) = acc[a][eb];
-      if (r == 0) *reinterpret_cast<f32x4*>(sl + D * D + 16 * cb + 4 * g) = acc[a][NB];
+      for (int eb = 0; eb <= NB; ++eb) acc[a][eb] = mma_step2(a0, a1, vb0[eb], vb1[eb], acc[a][eb]);
     }
   }
   __device__ __forceinline__ void load(int w, const float* rec) {
@@ -383,8 +535,7 @@ struct StateTiles {
         sf[((l * NB + eb) * NB + cb) * 64 + lane] = f32_to_quad<T>(f);
       }
       if (r == 0)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) sz[l * D + 16 * cb + 4 * g + i] = acc[a][NB][i];
+        *reinterpret_cast<f32x4*>(sz + l * D + 16 * cb + 4 * g) = acc[a][NB];
     }
   }
 };
@@ -561,36 +712,38 @@ __global__ __launch_bounds__(256) void k_state_combine(float* __restrict__ part,
   }
 }
 
-// ------------------------------------------------------------------ ring helpers
-// LDS ring of U 32-key units; window of tile t of a segment = absolute units
-// [ua0 + 2t, ua0 + 2t + U), unit ua lives at ring rows ((ua - ua0) % U) * 32.
+// ------------------------------------------------------------------ apply LDS
+// One workgroup's LDS: key and value rows (ring or round), state fragments,
+// z, and for the causal form the tile's phi_l(K) rows.
 template <typename T, int D, int R>
-struct RingSmem {
+struct ApplyLds {
   using Q = typename QuadOf<T>::type;
-  static constexpr int ST = Ring<T, D, R>::ST, NB = D / 16;
+  static constexpr int ST = D + Lay<T>::PAD, NB = D / 16;
   T* k;
   T* v;
   Q* sf;
   float* sz;
-  __device__ __forceinline__ RingSmem(unsigned char* base, int U) {
+  T* pk;
+  __device__ __forceinline__ ApplyLds(unsigned char* base, int rows) {
     k = reinterpret_cast<T*>(base);
-    v = k + U * 32 * ST;
-    sf = reinterpret_cast<Q*>(v + U * 32 * ST);
+    v = k + rows * ST;
+    sf = reinterpret_cast<Q*>(v + rows * ST);
     sz = reinterpret_cast<float*>(sf + R * NB * NB * 64);
+    pk = reinterpret_cast<T*>(sz + R * D);
   }
 };
 
 // Copy absolute units [ua, ua + n) of K and V into the ring (synchronously).
 template <typename T, int D, int R>
-__device__ __forceinline__ void ring_fill(const RingSmem<T, D, R>& sm, const T* kh, const T* vh,
-                                          int ua, int n, int ua0, int U, int N) {
-  constexpr int ST = RingSmem<T, D, R>::ST;
+__device__ __forceinline__ void ring_fill(const ApplyLds<T, D, R>& sm, const T* kh, const T* vh,
+                                          int ua, int n, RingMap map, int N) {
+  constexpr int ST = ApplyLds<T, D, R>::ST;
   for (int x = 0; x < n; x += 2) {
     const int m = min(2, n - x);
     RowCopy<T, D, NT, 64> ck, cv;
     ck.load(kh, (ua + x) * 32, 32 * m, N);
     cv.load(vh, (ua + x) * 32, 32 * m, N);
-    auto row = [&](int i) { return ((ua + x + (i >> 5) - ua0) % U) * 32 + (i & 31); };
+    auto row = [&](int i) { return map(ua + x + (i >> 5)) + (i & 31); };
     ck.store(sm.k, ST, 32 * m, row);
     cv.store(sm.v, ST, 32 * m, row);
   }
@@ -599,7 +752,8 @@ __device__ __forceinline__ void ring_fill(const RingSmem<T, D, R>& sm, const T* 
 // ------------------------------------------------------------------ k_band_ring
 // Non-causal.  grid.x = BH * nseg (XCD-aware remap); the workgroup walks the
 // 64-row tiles of rows [s*L, min(N, s*L + L)).  Window of a tile starting at
-// t0: keys [t0 - 32*ceil(k/32), t0 + 64 + 32*ceil(k/32)) = U = 2 + 2*ceil(k/32) units.
+// t0: keys [t0 - 32*ceil(k/32), t0 + 64 + 32*ceil(k/32)) = U = 2 + 2*ceil(k/32)
+// units; it slides by two units per tile.
 template <typename T, int D, int R>
 __global__ __launch_bounds__(NT) void k_band_ring(const T* __restrict__ q,
                                                   const T* __restrict__ k,
@@ -609,12 +763,12 @@ __global__ __launch_bounds__(NT) void k_band_ring(const T* __restrict__ q,
                                                   const float* __restrict__ w_far, int H, int N,
                                                   int band_k, int L, int nseg, float scale2) {
   using Q = typename QuadOf<T>::type;
-  using SM = RingSmem<T, D, R>;
+  using SM = ApplyLds<T, D, R>;
   constexpr int NB = D / 16, ST = SM::ST;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
-  const int kc = (band_k + 31) >> 5;        // band half-width in units (rounded up)
+  const int kc = (band_k + 31) >> 5;  // band half-width in units (rounded up)
   const int U = 2 + 2 * kc;
-  const SM sm(dyn_smem, U);
+  const SM sm(dyn_smem, U * 32);
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = lin / nseg, seg = lin % nseg, h = bh % H;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, r = lane & 15;
@@ -625,16 +779,16 @@ __global__ __launch_bounds__(NT) void k_band_ring(const T* __restrict__ q,
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const int s0 = seg * L, s1 = min(N, s0 + L);
   const int ntile = (s1 - s0 + TM - 1) / TM;
-  const int ua0 = (s0 >> 5) - kc;
+  const RingMap map{(s0 >> 5) - kc, U};
 
   load_state_frags<T, D, R, NT>(fin + (size_t)bh * R * D * (D + 1), sm.sf, sm.sz);
-  ring_fill<T, D, R>(sm, kh, vh, ua0, U, ua0, U, N);
+  ring_fill<T, D, R>(sm, kh, vh, map.ua0, U, map, N);
   Q qq[NB], qn[NB];
   load_q<T, D>(qh, s0 + 16 * w + r, N, qq);
   RowCopy<T, D, NT, 64> pk, pv;
   if (ntile > 1) {
-    pk.load(kh, (ua0 + U) * 32, 64, N);
-    pv.load(vh, (ua0 + U) * 32, 64, N);
+    pk.load(kh, (map.ua0 + U) * 32, 64, N);
+    pv.load(vh, (map.ua0 + U) * 32, 64, N);
     load_q<T, D>(qh, s0 + TM + 16 * w + r, N, qn);
   }
   for (int t = 0; t < ntile; ++t) {
@@ -643,20 +797,21 @@ __global__ __launch_bounds__(NT) void k_band_ring(const T* __restrict__ q,
     NearState<D> st;
     st.init();
     const int lo = max(0, i0 - band_k), hi = min(N - 1, i0 + 15 + band_k);
-    for (int ua = lo >> 5; ua <= hi >> 5; ++ua) {
-      const int rr = ((ua - ua0) % U) * 32;
-      near_unit<T, D, false>(st, qq, sm.k + rr * ST, sm.v + rr * ST, ST, ua * 32, row, N,
-                             band_k, scale2);
-    }
-    float qf[D / 4];
-    q_floats<T, D>(qq, qf);
-    f32x4 far[NB];
-    far_apply<T, D, R>(sm.sf, sm.sz, qf, far);
-    blend_store<T, D>(out + base, row, N, sn, sfw, st, far);
+    near_units<T, D, false>(st, qq, sm.k, sm.v, ST, map, lo >> 5, hi >> 5, i0, N, band_k,
+                            scale2);
+    Q pq[R][NB];
+    phi_q<T, D, R>(qq, pq);
+    f32x4 num[R][NB + 1];
+#pragma unroll
+    for (int l = 0; l < R; ++l)
+#pragma unroll
+      for (int nb = 0; nb <= NB; ++nb) num[l][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    far_terms<T, D, R>(sm.sf, sm.sz, pq, num);
+    blend_store<T, D, R>(out + base, row, N, sn, sfw, st, num);
     if (t + 1 < ntile) {
       __syncthreads();  // every wave is done with the window of tile t
-      const int ua_new = ua0 + 2 * t + U;  // the two units tile t+1 adds
-      auto rowmap = [&](int i) { return ((ua_new + (i >> 5) - ua0) % U) * 32 + (i & 31); };
+      const int ua_new = map.ua0 + 2 * t + U;  // the two units tile t+1 adds
+      auto rowmap = [&](int i) { return map(ua_new + (i >> 5)) + (i & 31); };
       pk.store(sm.k, ST, 64, rowmap);
       pv.store(sm.v, ST, 64, rowmap);
 #pragma unroll
@@ -667,93 +822,6 @@ __global__ __launch_bounds__(NT) void k_band_ring(const T* __restrict__ q,
         load_q<T, D>(qh, t0 + 2 * TM + 16 * w + r, N, qn);
       }
     }
-  }
-}
-
-// ------------------------------------------------------------------ causal tile body
-// Intra-tile far part of one strip: keys [t0, row] of the tile, per map,
-// accumulated into fnum / fden.  kt, vt: LDS rows of the tile's first key.
-template <typename T, int D, int R>
-__device__ __forceinline__ void causal_intra(const T* kt, const T* vt, int ST, int t0, int row,
-                                             int w, const typename QuadOf<T>::type (*pq)[D / 16],
-                                             f32x4 (*fnum)[D / 16], float* fden) {
-  using Q = typename QuadOf<T>::type;
-  constexpr int NB = D / 16;
-  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
-  for (int u = 0; u <= (w >> 1); ++u) {
-    float kf[2][D / 4];
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int cb = 0; cb < NB; ++cb)
-        quad_to_f32(ld_quad(kt, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST), kf[b] + 4 * cb);
-    float pk[2][2][D / 4];  // [b][map][t]
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int t = 0; t < D / 4; ++t) phi12(kf[b][t], pk[b][0][t], pk[b][1][t]);
-#pragma unroll
-    for (int l = 0; l < R; ++l) {
-      f32x4 at[2];
-#pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        Q ka[NB];
-#pragma unroll
-        for (int cb = 0; cb < NB; ++cb) ka[cb] = f32_to_quad<T>(pk[b][l] + 4 * cb);
-        at[b] = contract<NB>(ka, pq[l], f32x4{0.f, 0.f, 0.f, 0.f});
-      }
-      float pa[2][4];
-      float dp = 0.f;
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int j = t0 + 32 * u + 16 * b + 4 * g + i;
-          pa[b][i] = j <= row ? round_as<T>(at[b][i]) : 0.f;
-          dp += pa[b][i];
-        }
-      fden[l] += col_sum(dp);
-      const Q p0 = f32_to_quad<T>(pa[0]), p1 = f32_to_quad<T>(pa[1]);
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const Q va0 = ld_tquad(vt, 32 * u, 16 * nb, ST);
-        const Q va1 = ld_tquad(vt, 32 * u + 16, 16 * nb, ST);
-        fnum[l][nb] = mma_step2(va0, va1, p0, p1, fnum[l][nb]);
-      }
-    }
-  }
-}
-
-template <typename T, int D, int R>
-__device__ __forceinline__ void causal_finish(T* __restrict__ oh, int row, int N, float sn,
-                                              float sfw, const NearState<D>& st,
-                                              const typename QuadOf<T>::type* sf,
-                                              const float* sz, const float* qf,
-                                              f32x4 (*fnum)[D / 16], float* fden) {
-  constexpr int NB = D / 16;
-  f32x4 far[NB];
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb) far[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int l = 0; l < R; ++l) {
-    far_prefix<T, D>(sf, sz, qf, l, fnum[l], fden[l]);
-    const float inv = 1.f / fden[l];
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) far[nb] += fnum[l][nb] * inv;
-  }
-  blend_store<T, D>(oh, row, N, sn, sfw, st, far);
-}
-
-template <typename T, int D, int R>
-__device__ __forceinline__ void phi_q_quads(const float* qf,
-                                            typename QuadOf<T>::type (*pq)[D / 16]) {
-#pragma unroll
-  for (int cb = 0; cb < D / 16; ++cb) {
-    float p1[4], p2[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) phi12(qf[4 * cb + i], p1[i], p2[i]);
-    pq[0][cb] = f32_to_quad<T>(p1);
-    if constexpr (R == 2) pq[1][cb] = f32_to_quad<T>(p2);
   }
 }
 
@@ -772,13 +840,13 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
                                                     int N, int band_k, int L, int nseg,
                                                     float scale2) {
   using Q = typename QuadOf<T>::type;
-  using SM = RingSmem<T, D, R>;
-  using Tiles = StateTiles<T, D, R, NW>;
+  using SM = ApplyLds<T, D, R>;
+  using Tiles = StateTiles<T, D, R>;
   constexpr int NB = D / 16, ST = SM::ST;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
   const int kc = (band_k + 31) >> 5;
   const int U = 2 + kc;
-  const SM sm(dyn_smem, U);
+  const SM sm(dyn_smem, U * 32);
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = lin / nseg, seg = lin % nseg, h = bh % H;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, r = lane & 15;
@@ -789,67 +857,53 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const int s0 = seg * L, s1 = min(N, s0 + L);
   const int ntile = (s1 - s0 + TM - 1) / TM;
-  const int ua0 = (s0 >> 5) - kc;
+  const RingMap map{(s0 >> 5) - kc, U};
   const bool has_ag = Tiles::active(w);
 
   Tiles tiles;
   if (has_ag) tiles.load(w, prefix + ((size_t)bh * nseg + seg) * R * D * (D + 1));
-  ring_fill<T, D, R>(sm, kh, vh, ua0, U, ua0, U, N);
+  ring_fill<T, D, R>(sm, kh, vh, map.ua0, U, map, N);
   Q qq[NB], qn[NB];
   load_q<T, D>(qh, s0 + 16 * w + r, N, qq);
   RowCopy<T, D, NT, 64> pk, pv;
   if (ntile > 1) {
-    pk.load(kh, (ua0 + U) * 32, 64, N);
-    pv.load(vh, (ua0 + U) * 32, 64, N);
+    pk.load(kh, (map.ua0 + U) * 32, 64, N);
+    pv.load(vh, (map.ua0 + U) * 32, 64, N);
     load_q<T, D>(qh, s0 + TM + 16 * w + r, N, qn);
   }
+  __syncthreads();  // ring filled
+  stage_phi_tile<T, D, R>(sm.k, map(s0 >> 5), map((s0 >> 5) + 1), ST, s0, N, sm.pk);
   for (int t = 0; t < ntile; ++t) {
     const int t0 = s0 + t * TM, i0 = t0 + 16 * w, row = i0 + r;
+    const int rt0 = map(t0 >> 5), rt1 = map((t0 >> 5) + 1);  // ring rows of the tile
     if (has_ag) tiles.to_frags(w, sm.sf, sm.sz);
-    __syncthreads();  // ring window and prefix fragments of tile t are in LDS
+    __syncthreads();  // window, phi rows and prefix fragments of tile t are in LDS
     NearState<D> st;
     st.init();
     const int lo = max(0, i0 - band_k), hi = min(N - 1, i0 + 15);
-    for (int ua = lo >> 5; ua <= hi >> 5; ++ua) {
-      const int rr = ((ua - ua0) % U) * 32;
-      near_unit<T, D, true>(st, qq, sm.k + rr * ST, sm.v + rr * ST, ST, ua * 32, row, N,
-                            band_k, scale2);
-    }
-    float qf[D / 4];
-    q_floats<T, D>(qq, qf);
+    near_units<T, D, true>(st, qq, sm.k, sm.v, ST, map, lo >> 5, hi >> 5, i0, N, band_k,
+                           scale2);
     Q pq[R][NB];
-    phi_q_quads<T, D, R>(qf, pq);
-    f32x4 fnum[R][NB];
-    float fden[R];
+    phi_q<T, D, R>(qq, pq);
+    f32x4 num[R][NB + 1];
 #pragma unroll
-    for (int l = 0; l < R; ++l) {
-      fden[l] = 0.f;
+    for (int l = 0; l < R; ++l)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) fnum[l][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    const int rt = (((t0 >> 5) - ua0) % U) * 32;  // ring row of the tile's first key
-    // the tile's two units are consecutive ring units unless the ring wraps
-    const int rt2 = (((t0 >> 5) + 1 - ua0) % U) * 32;
-    if (rt2 == rt + 32) {
-      causal_intra<T, D, R>(sm.k + rt * ST, sm.v + rt * ST, ST, t0, row, w, pq, fnum, fden);
-    } else {
-      // wrapped: handle the two units separately (unit 1 only matters for w >= 2)
-      causal_intra<T, D, R>(sm.k + rt * ST, sm.v + rt * ST, ST, t0, row, 0, pq, fnum, fden);
-      if (w >= 2)
-        causal_intra<T, D, R>(sm.k + rt2 * ST, sm.v + rt2 * ST, ST, t0 + 32, row, 0, pq, fnum,
-                              fden);
-    }
-    causal_finish<T, D, R>(out + base, row, N, sn, sfw, st, sm.sf, sm.sz, qf, fnum, fden);
-    if (has_ag && t + 1 < ntile) {
-      tiles.add_unit(w, sm.k + rt * ST, sm.v + rt * ST, ST, N - t0);
-      tiles.add_unit(w, sm.k + rt2 * ST, sm.v + rt2 * ST, ST, N - t0 - 32);
-    }
+      for (int nb = 0; nb <= NB; ++nb) num[l][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    causal_intra<T, D, R>(sm.pk, sm.v + rt0 * ST, sm.v + rt1 * ST, ST, t0, w, pq, num);
+    far_terms<T, D, R>(sm.sf, sm.sz, pq, num);
+    blend_store<T, D, R>(out + base, row, N, sn, sfw, st, num);
     if (t + 1 < ntile) {
-      __syncthreads();  // every wave is done with the window and fragments of tile t
-      const int ua_new = ua0 + 2 * t + U;
-      auto rowmap = [&](int i) { return ((ua_new + (i >> 5) - ua0) % U) * 32 + (i & 31); };
+      if (has_ag) {
+        tiles.add_unit(w, sm.pk, 0, sm.v + rt0 * ST, ST);
+        tiles.add_unit(w, sm.pk, 32, sm.v + rt1 * ST, ST);
+      }
+      __syncthreads();  // every wave is done with tile t's LDS
+      const int ua_new = map.ua0 + 2 * t + U;  // = the keys of tile t+1
+      auto rowmap = [&](int i) { return map(ua_new + (i >> 5)) + (i & 31); };
       pk.store(sm.k, ST, 64, rowmap);
       pv.store(sm.v, ST, 64, rowmap);
+      phi_rows_from_regs<T, D, R>(pk, t0 + TM, N, ST, sm.pk);
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) qq[cb] = qn[cb];
       if (t + 2 < ntile) {
@@ -863,20 +917,11 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
 
 // ------------------------------------------------------------------ rounds variants
 // Bands too wide for the ring: every tile stages its window in rounds of up to
-// WK keys (row-major K and V, like the ring).
-template <typename T, int D, int R> struct RoundSmem {
-  using Q = typename QuadOf<T>::type;
-  static constexpr int ST = D + Lay<T>::PAD, NB = D / 16;
-  T k[WK * ST];
-  T v[WK * ST];
-  Q sf[R * NB * NB * 64];
-  float sz[R * D];
-};
-
+// 32 * Ring::UR keys (row-major K and V, like the ring).
 template <typename T, int D, int R>
-__device__ __forceinline__ void round_stage(RoundSmem<T, D, R>& sm, const T* kh, const T* vh,
-                                            int ks, int nk, int kend) {
-  constexpr int ST = RoundSmem<T, D, R>::ST;
+__device__ __forceinline__ void round_stage(const ApplyLds<T, D, R>& sm, const T* kh,
+                                            const T* vh, int ks, int nk, int kend) {
+  constexpr int ST = ApplyLds<T, D, R>::ST;
   auto ident = [](int i) { return i; };
   for (int x = 0; x < nk; x += 64) {
     const int m = min(64, nk - x);
@@ -898,9 +943,11 @@ __global__ __launch_bounds__(NT) void k_band_rounds(const T* __restrict__ q,
                                                     const float* __restrict__ w_far, int H,
                                                     int N, int band_k, int ntile, float scale2) {
   using Q = typename QuadOf<T>::type;
-  using SM = RoundSmem<T, D, R>;
+  using SM = ApplyLds<T, D, R>;
   constexpr int NB = D / 16, ST = SM::ST;
-  __shared__ __attribute__((aligned(16))) SM sm;
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
+  constexpr int WK = 32 * Ring<T, D, R>::UR;
+  const SM sm(dyn_smem, WK);
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = lin / ntile, tile = lin % ntile, h = bh % H;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, r = lane & 15;
@@ -920,15 +967,19 @@ __global__ __launch_bounds__(NT) void k_band_rounds(const T* __restrict__ q,
     round_stage<T, D, R>(sm, k + base, v + base, ks, nk, kend);
     __syncthreads();
     const int lo = max(max(0, i0 - band_k), ks), hi = min(min(N - 1, i0 + 15 + band_k), ks + nk - 1);
-    for (int j = lo & ~31; j <= hi; j += 32)
-      near_unit<T, D, false>(st, qq, sm.k + (j - ks) * ST, sm.v + (j - ks) * ST, ST, j, row, N,
-                             band_k, scale2);
+    if (lo <= hi)
+      near_units<T, D, false>(st, qq, sm.k, sm.v, ST, RoundMap{ks}, lo >> 5, hi >> 5, i0, N,
+                              band_k, scale2);
   }
-  float qf[D / 4];
-  q_floats<T, D>(qq, qf);
-  f32x4 far[NB];
-  far_apply<T, D, R>(sm.sf, sm.sz, qf, far);
-  blend_store<T, D>(out + base, row, N, sn, sfw, st, far);
+  Q pq[R][NB];
+  phi_q<T, D, R>(qq, pq);
+  f32x4 num[R][NB + 1];
+#pragma unroll
+  for (int l = 0; l < R; ++l)
+#pragma unroll
+    for (int nb = 0; nb <= NB; ++nb) num[l][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  far_terms<T, D, R>(sm.sf, sm.sz, pq, num);
+  blend_store<T, D, R>(out + base, row, N, sn, sfw, st, num);
 }
 
 // Causal, walks the tiles of a segment; per tile the window [t0 - k, t0 + 64)
@@ -944,11 +995,12 @@ __global__ __launch_bounds__(NT) void k_causal_rounds(const T* __restrict__ q,
                                                       int N, int band_k, int L, int nseg,
                                                       float scale2) {
   using Q = typename QuadOf<T>::type;
-  using SM = RoundSmem<T, D, R>;
-  using Tiles = StateTiles<T, D, R, NW>;
+  using SM = ApplyLds<T, D, R>;
+  using Tiles = StateTiles<T, D, R>;
   constexpr int NB = D / 16, ST = SM::ST;
-  static_assert(WK >= TM, "round 0 must hold the whole tile");
-  __shared__ __attribute__((aligned(16))) SM sm;
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
+  constexpr int WK = 32 * Ring<T, D, R>::UR;
+  const SM sm(dyn_smem, WK);
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = lin / nseg, seg = lin % nseg, h = bh % H;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, r = lane & 15;
@@ -960,50 +1012,50 @@ __global__ __launch_bounds__(NT) void k_causal_rounds(const T* __restrict__ q,
   const int s0 = seg * L, s1 = min(N, s0 + L);
   for (int t0 = s0; t0 < s1; t0 += TM) {
     const int i0 = t0 + 16 * w, row = i0 + r;
-    __syncthreads();  // every wave is done with the previous tile's LDS
-    if (has_ag) tiles.to_frags(w, sm.sf, sm.sz);
     Q qq[NB];
     load_q<T, D>(q + base, row, N, qq);
-    float qf[D / 4];
-    q_floats<T, D>(qq, qf);
     Q pq[R][NB];
-    phi_q_quads<T, D, R>(qf, pq);
+    phi_q<T, D, R>(qq, pq);
     NearState<D> st;
     st.init();
-    f32x4 fnum[R][NB];
-    float fden[R];
+    f32x4 num[R][NB + 1];
 #pragma unroll
-    for (int l = 0; l < R; ++l) {
-      fden[l] = 0.f;
+    for (int l = 0; l < R; ++l)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) fnum[l][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
+      for (int nb = 0; nb <= NB; ++nb) num[l][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int ka = (max(0, t0 - band_k) >> 5) << 5;
     const int hi = t0 + TM;
     for (int ke = hi; ke > ka; ke -= WK) {
       const int ks = max(ka, ke - WK), nk = ke - ks;
-      __syncthreads();
+      __syncthreads();  // every wave is done with the previous round / tile
       round_stage<T, D, R>(sm, k + base, v + base, ks, nk, min(N, ke));
+      if (ke == hi) {
+        if (has_ag) tiles.to_frags(w, sm.sf, sm.sz);
+        __syncthreads();  // the tile's keys are staged
+        stage_phi_tile<T, D, R>(sm.k, t0 - ks, t0 - ks + 32, ST, t0, N, sm.pk);
+      }
       __syncthreads();
       const int lo = max(max(0, i0 - band_k), ks), hj = min(min(N - 1, i0 + 15), ks + nk - 1);
-      for (int j = lo & ~31; j <= hj; j += 32)
-        near_unit<T, D, true>(st, qq, sm.k + (j - ks) * ST, sm.v + (j - ks) * ST, ST, j, row, N,
-                              band_k, scale2);
+      if (lo <= hj)
+        near_units<T, D, true>(st, qq, sm.k, sm.v, ST, RoundMap{ks}, lo >> 5, hj >> 5, i0, N,
+                               band_k, scale2);
       if (ke != hi) continue;
       const int tk = t0 - ks;
-      causal_intra<T, D, R>(sm.k + tk * ST, sm.v + tk * ST, ST, t0, row, w, pq, fnum, fden);
+      causal_intra<T, D, R>(sm.pk, sm.v + tk * ST, sm.v + (tk + 32) * ST, ST, t0, w, pq, num);
       if (has_ag && t0 + TM < s1) {
-        tiles.add_unit(w, sm.k + tk * ST, sm.v + tk * ST, ST, N - t0);
-        tiles.add_unit(w, sm.k + (tk + 32) * ST, sm.v + (tk + 32) * ST, ST, N - t0 - 32);
+        tiles.add_unit(w, sm.pk, 0, sm.v + tk * ST, ST);
+        tiles.add_unit(w, sm.pk, 32, sm.v + (tk + 32) * ST, ST);
       }
     }
-    causal_finish<T, D, R>(out + base, row, N, sn, sfw, st, sm.sf, sm.sz, qf, fnum, fden);
+    far_terms<T, D, R>(sm.sf, sm.sz, pq, num);
+    blend_store<T, D, R>(out + base, row, N, sn, sfw, st, num);
   }
 }
 
 // ------------------------------------------------------------------ launchers
 template <typename T, int D, int R>
 static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
+  using RG = Ring<T, D, R>;
   const int BH = a.B * a.H;
   const float scale2 = 1.4426950408889634f / sqrtf((float)D);
   const int REC = R * D * (D + 1);
@@ -1016,17 +1068,26 @@ static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
   float* fin = a.ws + (size_t)BH * a.nseg * REC;
   const int kc = (a.band_k + 31) / 32;
   const int U = a.causal ? 2 + kc : 2 + 2 * kc;
-  const bool ring = U <= Ring<T, D, R>::U;
-  const size_t ring_lds = Ring<T, D, R>::bytes(U);
-  static const bool lds_attr = [] {
-    const int mx = (int)Ring<T, D, R>::bytes(Ring<T, D, R>::U);
-    hipFuncSetAttribute((const void*)k_band_ring<T, D, R>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, mx);
-    hipFuncSetAttribute((const void*)k_causal_ring<T, D, R>,
-                        hipFuncAttributeMaxDynamicSharedMemorySize, mx);
-    return true;
+  const bool ring = U <= (a.causal ? RG::U_C : RG::U_NC);
+  const size_t lds = RG::bytes(ring ? U : RG::UR, a.causal != 0);
+  static const hipError_t lds_attr = [] {
+    hipError_t e = hipSuccess, x;
+    if ((x = hipFuncSetAttribute((const void*)k_band_ring<T, D, R>,
+                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)RG::bytes(RG::U_NC, false))) != hipSuccess) e = x;
+    if ((x = hipFuncSetAttribute((const void*)k_causal_ring<T, D, R>,
+                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)RG::bytes(RG::U_C, true))) != hipSuccess) e = x;
+    if ((x = hipFuncSetAttribute((const void*)k_band_rounds<T, D, R>,
+                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)RG::bytes(RG::UR, false))) != hipSuccess) e = x;
+    if ((x = hipFuncSetAttribute((const void*)k_causal_rounds<T, D, R>,
+                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)RG::bytes(RG::UR, true))) != hipSuccess) e = x;
+    (void)hipGetLastError();
+    return e;
   }();
-  (void)lds_attr;
+  if (lds_attr != hipSuccess) return lds_attr;
 
   timer->begin(FMM_KERNEL_SEG_STATE, s);
   hipLaunchKernelGGL((k_seg_state<T, D, R>), dim3(a.nseg * BH), dim3(SNT), 0, s, k, v, part,
@@ -1046,22 +1107,22 @@ static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
   if (a.causal) {
     timer->begin(FMM_KERNEL_CAUSAL_APPLY, s);
     if (ring)
-      hipLaunchKernelGGL((k_causal_ring<T, D, R>), dim3(BH * a.nseg), dim3(NT), ring_lds, s, q, k, v,
-                         o, part, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L, a.nseg, scale2);
+      hipLaunchKernelGGL((k_causal_ring<T, D, R>), dim3(BH * a.nseg), dim3(NT), lds, s, q, k,
+                         v, o, part, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L, a.nseg, scale2);
     else
-      hipLaunchKernelGGL((k_causal_rounds<T, D, R>), dim3(BH * a.nseg), dim3(NT), 0, s, q, k,
+      hipLaunchKernelGGL((k_causal_rounds<T, D, R>), dim3(BH * a.nseg), dim3(NT), lds, s, q, k,
                          v, o, part, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L, a.nseg,
                          scale2);
     timer->end(FMM_KERNEL_CAUSAL_APPLY, s);
   } else {
     timer->begin(FMM_KERNEL_BAND_APPLY, s);
     if (ring) {
-      hipLaunchKernelGGL((k_band_ring<T, D, R>), dim3(BH * a.nseg_apply), dim3(NT), ring_lds, s, q, k,
-                         v, o, fin, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L_apply,
+      hipLaunchKernelGGL((k_band_ring<T, D, R>), dim3(BH * a.nseg_apply), dim3(NT), lds, s, q,
+                         k, v, o, fin, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L_apply,
                          a.nseg_apply, scale2);
     } else {
       const int ntile = (a.N + TM - 1) / TM;
-      hipLaunchKernelGGL((k_band_rounds<T, D, R>), dim3(BH * ntile), dim3(NT), 0, s, q, k, v,
+      hipLaunchKernelGGL((k_band_rounds<T, D, R>), dim3(BH * ntile), dim3(NT), lds, s, q, k, v,
                          o, fin, a.w_near, a.w_far, a.H, a.N, a.band_k, ntile, scale2);
     }
     timer->end(FMM_KERNEL_BAND_APPLY, s);
