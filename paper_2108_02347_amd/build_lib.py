@@ -31,6 +31,10 @@ def build(verbose: bool = False) -> str:
         hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
         # keep the compiler from forming packed fp32 instructions
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+        # keep MFMA accumulators in ordinary VGPRs: the kernels scale and
+        # blend them with VALU code, which would otherwise copy them out of
+        # and back into AGPRs
+        "-mllvm", "-amdgpu-mfma-vgpr-form=1",
         "-Wno-unused-result",
         "-I", os.path.join(ROOT, "include"),
     ] + [os.path.join(CSRC, s) for s in SOURCES] + ["-o", LIB + ".tmp"]

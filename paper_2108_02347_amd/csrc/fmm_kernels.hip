@@ -561,7 +561,8 @@ __global__ __launch_bounds__(SNT) void k_seg_state(const T* __restrict__ k,
   __shared__ __attribute__((aligned(16))) T s_kv[2][2][TK * ST];  // [buffer][K, V]
 
   const int seg = blockIdx.x % nseg, bh = blockIdx.x / nseg;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   const int cbw = w % NB, rs = w / NB;
   const int r0 = seg * L, r1 = min(N, r0 + L);
   const T* kh = k + (size_t)bh * N * D;
@@ -771,7 +772,8 @@ __global__ __launch_bounds__(NT) void k_band_ring(const T* __restrict__ q,
   const SM sm(dyn_smem, U * 32);
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = lin / nseg, seg = lin % nseg, h = bh % H;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, r = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, r = lane & 15;
   const size_t base = (size_t)bh * N * D;
   const T* qh = q + base;
   const T* kh = k + base;
@@ -849,7 +851,8 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
   const SM sm(dyn_smem, U * 32);
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = lin / nseg, seg = lin % nseg, h = bh % H;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, r = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, r = lane & 15;
   const size_t base = (size_t)bh * N * D;
   const T* qh = q + base;
   const T* kh = k + base;
@@ -950,7 +953,8 @@ __global__ __launch_bounds__(NT) void k_band_rounds(const T* __restrict__ q,
   const SM sm(dyn_smem, WK);
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = lin / ntile, tile = lin % ntile, h = bh % H;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, r = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, r = lane & 15;
   const int t0 = tile * TM, i0 = t0 + 16 * w, row = i0 + r;
   const size_t base = (size_t)bh * N * D;
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
@@ -1003,7 +1007,8 @@ __global__ __launch_bounds__(NT) void k_causal_rounds(const T* __restrict__ q,
   const SM sm(dyn_smem, WK);
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int bh = lin / nseg, seg = lin % nseg, h = bh % H;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, r = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, r = lane & 15;
   const size_t base = (size_t)bh * N * D;
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const bool has_ag = Tiles::active(w);
