@@ -148,12 +148,12 @@ struct RoundMap {
 template <int D> struct NearState {
   f32x4 o[D / 16 + 1];
   float m;
-  bool fresh;
+  int fresh;  // wave-uniform: nothing accumulated yet
   __device__ __forceinline__ void init() {
 #pragma unroll
     for (int nb = 0; nb <= D / 16; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     m = -INFINITY;
-    fresh = true;
+    fresh = 1;
   }
 };
 
@@ -190,17 +190,16 @@ __device__ __forceinline__ void near_units(NearState<D>& st, const typename Quad
       const bool interior = j0 >= 0 && j0 + 31 < N && j0 >= i0 + 15 - band_k &&
                             (CAUSAL ? j0 + 31 <= i0 : j0 + 31 <= i0 + band_k);
       if (!interior) {
-        const int dbase = j0 + 4 * g - row;
-        const unsigned span = CAUSAL ? (unsigned)band_k : 2u * (unsigned)band_k;
+        // valid keys of this lane's row form one interval; in unit-local
+        // offsets c = 16b + i (lane group g adds 4g) it is [lo, lo + span]
+        int lo = max(row - band_k, 0) - j0 - 4 * g;
+        int span = min(CAUSAL ? row : row + band_k, N - 1) - j0 - 4 * g - lo;
+        if (span < 0) { lo = 64; span = 0; }
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int dd = dbase + 16 * b + i;
-            const int j = j0 + 16 * b + 4 * g + i;
-            const bool ok = (unsigned)(dd + band_k) <= span && (unsigned)j < (unsigned)N;
-            if (!ok) sc[gi][b][i] = -INFINITY;
-          }
+          for (int i = 0; i < 4; ++i)
+            if ((unsigned)(16 * b + i - lo) > (unsigned)span) sc[gi][b][i] = -INFINITY;
       }
 #pragma unroll
       for (int b = 0; b < 2; ++b)
@@ -209,13 +208,13 @@ __device__ __forceinline__ void near_units(NearState<D>& st, const typename Quad
     }
     const float mnew = fmaxf(st.m, col_max(mloc));
     const float ms = (mnew == -INFINITY ? 0.f : mnew) * scale2;
-    if (!st.fresh) {
+    if (!__builtin_amdgcn_readfirstlane(st.fresh)) {
       const float alpha = __builtin_amdgcn_exp2f(st.m * scale2 - ms);
 #pragma unroll
       for (int nb = 0; nb <= NB; ++nb) st.o[nb] *= alpha;
     }
     st.m = mnew;
-    st.fresh = false;
+    st.fresh = 0;
 #pragma unroll
     for (int gi = 0; gi < GU; ++gi) {
       const int ua = u0 + gi;
