@@ -118,11 +118,14 @@ __device__ __forceinline__ f32x4 contract(const Q* a, const Q* b, f32x4 c) {
 }
 
 // ---------------------------------------------------------------- maps
-// phi_1(x) = elu(x) + 1 and phi_2(x) = elu(-x) + 1 share exp(-|x|).
+// phi_1(x) = elu(x) + 1 and phi_2(x) = elu(-x) + 1 share e = exp(-|x|).
+// Since exp(y) >= 1 + y for every y, phi_1(x) = max(1 + x, e) (for x > 0, e <
+// 1 < 1 + x; for x <= 0, e = exp(x) >= 1 + x) and likewise phi_2(x) =
+// max(1 - x, e): one exponential, two adds, two max.
 __device__ __forceinline__ void phi12(float x, float& p1, float& p2) {
-  float e = __expf(-fabsf(x));
-  p1 = x > 0.f ? 1.f + x : e;
-  p2 = x < 0.f ? 1.f - x : e;
+  const float e = __expf(-fabsf(x));
+  p1 = fmaxf(1.f + x, e);
+  p2 = fmaxf(1.f - x, e);
 }
 __device__ __forceinline__ float phi_l(float x, int l) {
   float p1, p2;

@@ -251,16 +251,20 @@ __device__ __forceinline__ void phi_q(const typename QuadOf<T>::type* qq,
   }
 }
 
-// num[l][nb] += S_l^T phi_l(Q)^T for nb < NB and num[l][NB] += phi_l(q) . z_l
+// num[l][nb] (+)= S_l^T phi_l(Q)^T for nb < NB and num[l][NB] (+)= phi_l(q) . z_l
 // (z_l broadcast over the 16 rows of an extra A block).  State fragments:
-// sf[(l*NB + nb)*NB + cb][lane] = S_l[16cb + 4g + {0..3}][16nb + r]; sz = z.
-template <typename T, int D, int R>
-__device__ __forceinline__ void far_terms(const typename QuadOf<T>::type* sf, const float* sz,
+// sf[(l*NB + nb)*NB + cb][lane] = S_l[16cb + 4g + {0..3}][16nb + r];
+// szq[(l*NB + cb)*4 + g] = z_l[16cb + 4g + {0..3}].  ACC = false starts the
+// sums from zero.
+template <typename T, int D, int R, bool ACC>
+__device__ __forceinline__ void far_terms(const typename QuadOf<T>::type* sf,
+                                          const typename QuadOf<T>::type* szq,
                                           const typename QuadOf<T>::type (*pq)[D / 16],
                                           f32x4 (*num)[D / 16 + 1]) {
   using Q = typename QuadOf<T>::type;
   constexpr int NB = D / 16;
   const int lane = threadIdx.x & 63, g = lane >> 4;
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int l = 0; l < R; ++l) {
 #pragma unroll
@@ -268,16 +272,12 @@ __device__ __forceinline__ void far_terms(const typename QuadOf<T>::type* sf, co
       Q a[NB];
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) a[cb] = sf[((l * NB + nb) * NB + cb) * 64 + lane];
-      num[l][nb] = contract<NB>(a, pq[l], num[l][nb]);
+      num[l][nb] = contract<NB>(a, pq[l], ACC ? num[l][nb] : zero);
     }
     Q zq[NB];
 #pragma unroll
-    for (int cb = 0; cb < NB; ++cb) {
-      const float4 z4 = *reinterpret_cast<const float4*>(sz + l * D + 16 * cb + 4 * g);
-      const float f[4] = {z4.x, z4.y, z4.z, z4.w};
-      zq[cb] = f32_to_quad<T>(f);
-    }
-    num[l][NB] = contract<NB>(zq, pq[l], num[l][NB]);
+    for (int cb = 0; cb < NB; ++cb) zq[cb] = szq[(l * NB + cb) * 4 + g];
+    num[l][NB] = contract<NB>(zq, pq[l], ACC ? num[l][NB] : zero);
   }
 }
 
@@ -311,7 +311,8 @@ __device__ __forceinline__ void blend_store(T* __restrict__ oh, int row, int N, 
 // Fill state fragments from a tile-order record (non-causal final state).
 template <typename T, int D, int R, int NTHR>
 __device__ __forceinline__ void load_state_frags(const float* __restrict__ rec,
-                                                 typename QuadOf<T>::type* sf, float* sz) {
+                                                 typename QuadOf<T>::type* sf,
+                                                 typename QuadOf<T>::type* szq) {
   constexpr int NB = D / 16;
   constexpr int E = R * NB * NB * 64;
   for (int t = threadIdx.x; t < E; t += NTHR) {
@@ -322,8 +323,12 @@ __device__ __forceinline__ void load_state_frags(const float* __restrict__ rec,
     const float f[4] = {v.x, v.y, v.z, v.w};
     sf[t] = f32_to_quad<T>(f);
   }
-  for (int t = threadIdx.x; t < R * D; t += NTHR)
-    sz[t] = rec[(size_t)(t / D) * D * (D + 1) + D * D + t % D];
+  for (int t = threadIdx.x; t < R * NB * 4; t += NTHR) {
+    const int l = t / (NB * 4), c0 = 4 * (t % (NB * 4));
+    const float* z = rec + (size_t)l * D * (D + 1) + D * D + c0;
+    const float f[4] = {z[0], z[1], z[2], z[3]};
+    szq[t] = f32_to_quad<T>(f);
+  }
 }
 
 // Query quads of one row: lane (r, g) gets q[row][16cb + 4g + {0..3}].
@@ -521,8 +526,8 @@ struct StateTiles {
                           : f32x4{0.f, 0.f, 0.f, 0.f};
     }
   }
-  // Write this wave's tiles as apply fragments (sf, sz) for the prefix far part.
-  __device__ __forceinline__ void to_frags(int w, Q* sf, float* sz) const {
+  // Write this wave's tiles as apply fragments (sf, szq) for the prefix far part.
+  __device__ __forceinline__ void to_frags(int w, Q* sf, Q* szq) const {
     const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
 #pragma unroll
     for (int a = 0; a < AGPW; ++a) {
@@ -533,8 +538,10 @@ struct StateTiles {
         const float f[4] = {acc[a][eb][0], acc[a][eb][1], acc[a][eb][2], acc[a][eb][3]};
         sf[((l * NB + eb) * NB + cb) * 64 + lane] = f32_to_quad<T>(f);
       }
-      if (r == 0)
-        *reinterpret_cast<f32x4*>(sz + l * D + 16 * cb + 4 * g) = acc[a][NB];
+      if (r == 0) {
+        const float f[4] = {acc[a][NB][0], acc[a][NB][1], acc[a][NB][2], acc[a][NB][3]};
+        szq[(l * NB + cb) * 4 + g] = f32_to_quad<T>(f);
+      }
     }
   }
 };
@@ -722,14 +729,14 @@ struct ApplyLds {
   T* k;
   T* v;
   Q* sf;
-  float* sz;
+  Q* sz;  // z quads, see far_terms
   T* pk;
   __device__ __forceinline__ ApplyLds(unsigned char* base, int rows) {
     k = reinterpret_cast<T*>(base);
     v = k + rows * ST;
     sf = reinterpret_cast<Q*>(v + rows * ST);
-    sz = reinterpret_cast<float*>(sf + R * NB * NB * 64);
-    pk = reinterpret_cast<T*>(sz + R * D);
+    sz = sf + R * NB * NB * 64;
+    pk = reinterpret_cast<T*>(sz + R * NB * 4);
   }
 };
 
@@ -803,16 +810,13 @@ __global__ __launch_bounds__(NT) void k_band_ring(const T* __restrict__ q,
     Q pq[R][NB];
     phi_q<T, D, R>(qq, pq);
     f32x4 num[R][NB + 1];
-#pragma unroll
-    for (int l = 0; l < R; ++l)
-#pragma unroll
-      for (int nb = 0; nb <= NB; ++nb) num[l][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    far_terms<T, D, R>(sm.sf, sm.sz, pq, num);
+    far_terms<T, D, R, false>(sm.sf, sm.sz, pq, num);
     blend_store<T, D, R>(out + base, row, N, sn, sfw, st, num);
     if (t + 1 < ntile) {
       __syncthreads();  // every wave is done with the window of tile t
       const int ua_new = map.ua0 + 2 * t + U;  // the two units tile t+1 adds
-      auto rowmap = [&](int i) { return map(ua_new + (i >> 5)) + (i & 31); };
+      const int ra = map(ua_new), rb = map(ua_new + 1);
+      auto rowmap = [=](int i) { return (i < 32 ? ra : rb) + (i & 31); };
       pk.store(sm.k, ST, 64, rowmap);
       pv.store(sm.v, ST, 64, rowmap);
 #pragma unroll
@@ -893,7 +897,7 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
 #pragma unroll
       for (int nb = 0; nb <= NB; ++nb) num[l][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     causal_intra<T, D, R>(sm.pk, sm.v + rt0 * ST, sm.v + rt1 * ST, ST, t0, w, pq, num);
-    far_terms<T, D, R>(sm.sf, sm.sz, pq, num);
+    far_terms<T, D, R, true>(sm.sf, sm.sz, pq, num);
     blend_store<T, D, R>(out + base, row, N, sn, sfw, st, num);
     if (t + 1 < ntile) {
       if (has_ag) {
@@ -902,7 +906,8 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
       }
       __syncthreads();  // every wave is done with tile t's LDS
       const int ua_new = map.ua0 + 2 * t + U;  // = the keys of tile t+1
-      auto rowmap = [&](int i) { return map(ua_new + (i >> 5)) + (i & 31); };
+      const int ra = map(ua_new), rb = map(ua_new + 1);
+      auto rowmap = [=](int i) { return (i < 32 ? ra : rb) + (i & 31); };
       pk.store(sm.k, ST, 64, rowmap);
       pv.store(sm.v, ST, 64, rowmap);
       phi_rows_from_regs<T, D, R>(pk, t0 + TM, N, ST, sm.pk);
@@ -977,11 +982,7 @@ __global__ __launch_bounds__(NT) void k_band_rounds(const T* __restrict__ q,
   Q pq[R][NB];
   phi_q<T, D, R>(qq, pq);
   f32x4 num[R][NB + 1];
-#pragma unroll
-  for (int l = 0; l < R; ++l)
-#pragma unroll
-    for (int nb = 0; nb <= NB; ++nb) num[l][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  far_terms<T, D, R>(sm.sf, sm.sz, pq, num);
+  far_terms<T, D, R, false>(sm.sf, sm.sz, pq, num);
   blend_store<T, D, R>(out + base, row, N, sn, sfw, st, num);
 }
 
@@ -1051,7 +1052,7 @@ __global__ __launch_bounds__(NT) void k_causal_rounds(const T* __restrict__ q,
         tiles.add_unit(w, sm.pk, 32, sm.v + (tk + 32) * ST, ST);
       }
     }
-    far_terms<T, D, R>(sm.sf, sm.sz, pq, num);
+    far_terms<T, D, R, true>(sm.sf, sm.sz, pq, num);
     blend_store<T, D, R>(out + base, row, N, sn, sfw, st, num);
   }
 }
