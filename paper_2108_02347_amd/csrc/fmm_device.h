@@ -138,16 +138,26 @@ __device__ __forceinline__ float sigmoidf_exact(float w) {
   return 1.0f / (1.0f + expf(-w));
 }
 
-// Sum / max over the four lanes that share a column (lanes r, r+16, r+32, r+48).
-__device__ __forceinline__ float col_sum(float x) {
-  x += __shfl_xor(x, 16);
-  x += __shfl_xor(x, 32);
-  return x;
-}
+// Sum / max over the four lanes that share a column (lanes r, r+16, r+32,
+// r+48), with the gfx950 lane-swap instructions: permlane32_swap exchanges
+// the upper half of one register with the lower half of another, so (a, b)
+// = swap(x, x) holds x's two halves in opposite order; permlane16_swap does
+// the same for odd and even 16-lane rows.  Plain VALU, no LDS round trip.
 __device__ __forceinline__ float col_max(float x) {
-  x = fmaxf(x, __shfl_xor(x, 16));
-  x = fmaxf(x, __shfl_xor(x, 32));
-  return x;
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  const float y = fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+  const auto q = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false,
+                                                  false);
+  return fmaxf(__uint_as_float(q[0]), __uint_as_float(q[1]));
+}
+__device__ __forceinline__ float col_sum(float x) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  const float y = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  const auto q = __builtin_amdgcn_permlane16_swap(__float_as_uint(y), __float_as_uint(y), false,
+                                                  false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
 }
 
 // Workgroup index remap so that consecutive logical tiles land on the same

@@ -40,7 +40,6 @@ namespace fmm {
 constexpr int NW = 4;            // wavefronts per apply workgroup
 constexpr int NT = NW * 64;      // threads per apply workgroup
 constexpr int TM = 16 * NW;      // query rows per tile (= 2 key units)
-constexpr int GU = 6;            // key units whose scores are held at once
 
 template <typename T> struct Lay {
   static constexpr int ES = (int)sizeof(T);
@@ -162,7 +161,7 @@ template <int D> struct NearState {
 // maximum, one exponentiation pass and the P V products; the accumulator is
 // rescaled only between groups.  Exponentials use exp2 with tau*log2(e)
 // folded into the subtraction of the maximum.
-template <typename T, int D, bool CAUSAL, class Map>
+template <typename T, int D, bool CAUSAL, int GU, class Map>
 __device__ __forceinline__ void near_units(NearState<D>& st, const typename QuadOf<T>::type* qq,
                                            const T* kr, const T* vr, int ST, Map map, int ua_lo,
                                            int ua_hi, int i0, int N, int band_k, float scale2) {
@@ -281,6 +280,57 @@ __device__ __forceinline__ void far_terms(const typename QuadOf<T>::type* sf,
   }
 }
 
+// The same terms for one map l, accumulated into num (NB + 1 tiles).
+template <typename T, int D>
+__device__ __forceinline__ void far_terms_map(const typename QuadOf<T>::type* sf,
+                                              const typename QuadOf<T>::type* szq, int l,
+                                              const typename QuadOf<T>::type* pql, f32x4* num) {
+  using Q = typename QuadOf<T>::type;
+  constexpr int NB = D / 16;
+  const int lane = threadIdx.x & 63, g = lane >> 4;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    Q a[NB];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) a[cb] = sf[((l * NB + nb) * NB + cb) * 64 + lane];
+    num[nb] = contract<NB>(a, pql, num[nb]);
+  }
+  Q zq[NB];
+#pragma unroll
+  for (int cb = 0; cb < NB; ++cb) zq[cb] = szq[(l * NB + cb) * 4 + g];
+  num[NB] = contract<NB>(zq, pql, num[NB]);
+}
+
+// Near part of the output, sigmoid(w_near) * near, in the lane's output layout.
+template <int D>
+__device__ __forceinline__ void near_out(const NearState<D>& st, float sn, f32x4* fo) {
+  constexpr int NB = D / 16;
+  const float a = sn > 0.f ? sn * fast_rcp(st.o[NB][0]) : 0.f;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) fo[nb] = st.o[nb] * a;
+}
+
+// fo += sigmoid(w_far) * num / den for one map (den in num[NB]).
+template <int D>
+__device__ __forceinline__ void add_far_map(const f32x4* num, float sfw, f32x4* fo) {
+  constexpr int NB = D / 16;
+  const float f = sfw > 0.f ? sfw * fast_rcp(num[NB][0]) : 0.f;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) fo[nb] += num[nb] * f;
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void store_row(T* __restrict__ oh, int row, int N, const f32x4* fo) {
+  using Q = typename QuadOf<T>::type;
+  const int g = (threadIdx.x & 63) >> 4;
+  if (row >= N) return;
+#pragma unroll
+  for (int nb = 0; nb < D / 16; ++nb) {
+    const float o[4] = {fo[nb][0], fo[nb][1], fo[nb][2], fo[nb][3]};
+    *reinterpret_cast<Q*>(oh + (size_t)row * D + 16 * nb + 4 * g) = f32_to_quad<T>(o);
+  }
+}
+
 // out = sigmoid(w_near) near + sigmoid(w_far) sum_l num_l / den_l  (Eq. (11)).
 template <typename T, int D, int R>
 __device__ __forceinline__ void blend_store(T* __restrict__ oh, int row, int N, float sn,
@@ -387,90 +437,97 @@ __device__ __forceinline__ void stage_phi_tile(const T* kbuf, int kt0, int kt1, 
 }
 
 // phi_l of the 64 key rows a RowCopy holds in registers (rows k0 .. k0+63 of
-// the head) into pk[l]; rows at or beyond N give 0.  Same chunk-to-thread
-// assignment as RowCopy.
+// the head), computed into registers (same chunk-to-thread assignment as
+// RowCopy) and later stored as pk[l]; rows at or beyond N give 0.
 template <typename T, int D, int R>
-__device__ __forceinline__ void phi_rows_from_regs(const RowCopy<T, D, NT, 64>& ck, int k0,
-                                                   int N, int ST, T* pk) {
+struct PhiRows {
   using L = Lay<T>;
   using RC = RowCopy<T, D, NT, 64>;
+  uint4 v[R][RC::IT];
+  __device__ __forceinline__ void compute(const RC& ck, int k0, int N) {
 #pragma unroll
-  for (int it = 0; it < RC::IT; ++it) {
-    const int t = threadIdx.x + it * NT;
-    if (t >= TM * RC::CPR) continue;
-    const int key = t / RC::CPR, c = t % RC::CPR;
-    const uint4 raw = ck.r[it];
-    float x[L::EPC], p1[L::EPC], p2[L::EPC];
-    if constexpr (sizeof(T) == 2) {
-      const uint16_t* e = reinterpret_cast<const uint16_t*>(&raw);
-#pragma unroll
-      for (int i = 0; i < L::EPC; ++i) x[i] = bf16_to_f32(e[i]);
-    } else {
-      const float* e = reinterpret_cast<const float*>(&raw);
-#pragma unroll
-      for (int i = 0; i < L::EPC; ++i) x[i] = e[i];
-    }
-    const bool ok = k0 + key < N;
-#pragma unroll
-    for (int i = 0; i < L::EPC; ++i) {
-      phi12(x[i], p1[i], p2[i]);
-      if (!ok) { p1[i] = 0.f; p2[i] = 0.f; }
-    }
-#pragma unroll
-    for (int l = 0; l < R; ++l) {
-      const float* p = l == 0 ? p1 : p2;
-      uint4 outw;
+    for (int it = 0; it < RC::IT; ++it) {
+      const int t = threadIdx.x + it * NT;
+      const int key = t / RC::CPR;
+      const uint4 raw = ck.r[it];
+      float x[L::EPC], p1[L::EPC], p2[L::EPC];
       if constexpr (sizeof(T) == 2) {
-        outw = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
-                          pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+        const uint16_t* e = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+        for (int i = 0; i < L::EPC; ++i) x[i] = bf16_to_f32(e[i]);
       } else {
-        outw = make_uint4(__float_as_uint(p[0]), __float_as_uint(p[1]), __float_as_uint(p[2]),
-                          __float_as_uint(p[3]));
+        const float* e = reinterpret_cast<const float*>(&raw);
+#pragma unroll
+        for (int i = 0; i < L::EPC; ++i) x[i] = e[i];
       }
-      *reinterpret_cast<uint4*>(pk + l * TM * ST + key * ST + c * L::EPC) = outw;
+      const bool ok = k0 + key < N;
+#pragma unroll
+      for (int i = 0; i < L::EPC; ++i) {
+        phi12(x[i], p1[i], p2[i]);
+        if (!ok) { p1[i] = 0.f; p2[i] = 0.f; }
+      }
+#pragma unroll
+      for (int l = 0; l < R; ++l) {
+        const float* p = l == 0 ? p1 : p2;
+        if constexpr (sizeof(T) == 2) {
+          v[l][it] = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                                pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+        } else {
+          v[l][it] = make_uint4(__float_as_uint(p[0]), __float_as_uint(p[1]),
+                                __float_as_uint(p[2]), __float_as_uint(p[3]));
+        }
+      }
     }
   }
-}
+  __device__ __forceinline__ void store(T* pk, int ST) const {
+#pragma unroll
+    for (int it = 0; it < RC::IT; ++it) {
+      const int t = threadIdx.x + it * NT;
+      if (t >= TM * RC::CPR) continue;
+      const int key = t / RC::CPR, c = t % RC::CPR;
+#pragma unroll
+      for (int l = 0; l < R; ++l)
+        *reinterpret_cast<uint4*>(pk + l * TM * ST + key * ST + c * L::EPC) = v[l][it];
+    }
+  }
+};
 
-// Intra-tile far part of the strip of wave w: keys [t0, row] of the tile, per
-// map: A = tril(phi_l(K_t) phi_l(q)^T) from pk, num[l][nb] += V^T A and the
-// row sums of A into num[l][NB].  vt0 / vt1: LDS rows of the tile's two V units.
+// Intra-tile far part of the strip of wave w for map l: keys [t0, row] of the
+// tile, A = tril(phi_l(K_t) phi_l(q)^T) from pk, num[nb] += V^T A and the row
+// sums of A into num[NB].  vt0 / vt1: LDS rows of the tile's two V units.
 template <typename T, int D, int R>
 __device__ __forceinline__ void causal_intra(const T* pk, const T* vt0, const T* vt1, int ST,
-                                             int t0, int w,
-                                             const typename QuadOf<T>::type (*pq)[D / 16],
-                                             f32x4 (*num)[D / 16 + 1]) {
+                                             int t0, int w, int l,
+                                             const typename QuadOf<T>::type* pql,
+                                             f32x4* num) {
   using Q = typename QuadOf<T>::type;
   constexpr int NB = D / 16;
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
   const int row = t0 + 16 * w + r;
   const Q ones = quad_fill<T>(1.f);
+  const T* pkl = pk + l * TM * ST;
   for (int u = 0; u <= (w >> 1); ++u) {
     const T* vx = u == 0 ? vt0 : vt1;
     const bool diag = u == (w >> 1);
+    float a[2][4];
 #pragma unroll
-    for (int l = 0; l < R; ++l) {
-      const T* pkl = pk + l * TM * ST;
-      float a[2][4];
+    for (int b = 0; b < 2; ++b) {
+      Q ka[NB];
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        Q ka[NB];
+      for (int cb = 0; cb < NB; ++cb) ka[cb] = ld_quad(pkl, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
+      const f32x4 at = contract<NB>(ka, pql, f32x4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
-        for (int cb = 0; cb < NB; ++cb) ka[cb] = ld_quad(pkl, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
-        const f32x4 at = contract<NB>(ka, pq[l], f32x4{0.f, 0.f, 0.f, 0.f});
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int j = t0 + 32 * u + 16 * b + 4 * g + i;
-          a[b][i] = (!diag || j <= row) ? at[i] : 0.f;
-        }
+      for (int i = 0; i < 4; ++i) {
+        const int j = t0 + 32 * u + 16 * b + 4 * g + i;
+        a[b][i] = (!diag || j <= row) ? at[i] : 0.f;
       }
-      const Q p0 = f32_to_quad<T>(a[0]), p1 = f32_to_quad<T>(a[1]);
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        num[l][nb] = mma_step2(ld_tquad(vx, 0, 16 * nb, ST), ld_tquad(vx, 16, 16 * nb, ST), p0,
-                               p1, num[l][nb]);
-      num[l][NB] = mma_step2(ones, ones, p0, p1, num[l][NB]);
     }
+    const Q p0 = f32_to_quad<T>(a[0]), p1 = f32_to_quad<T>(a[1]);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+      num[nb] = mma_step2(ld_tquad(vx, 0, 16 * nb, ST), ld_tquad(vx, 16, 16 * nb, ST), p0, p1,
+                          num[nb]);
+    num[NB] = mma_step2(ones, ones, p0, p1, num[NB]);
   }
 }
 
@@ -524,6 +581,35 @@ struct StateTiles {
         acc[a][eb] = *reinterpret_cast<const f32x4*>(sl + ((cb * NB + eb) * 64 + lane) * 4);
       acc[a][NB] = r == 0 ? *reinterpret_cast<const f32x4*>(sl + D * D + 16 * cb + 4 * g)
                           : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+  // This wave's tiles as operand quads, ready to store with store_frags.
+  struct Frags {
+    Q s[AGPW][NB];
+    Q z[AGPW];
+  };
+  __device__ __forceinline__ Frags pack() const {
+    Frags f;
+#pragma unroll
+    for (int a = 0; a < AGPW; ++a) {
+#pragma unroll
+      for (int eb = 0; eb <= NB; ++eb) {
+        const float x[4] = {acc[a][eb][0], acc[a][eb][1], acc[a][eb][2], acc[a][eb][3]};
+        if (eb < NB) f.s[a][eb] = f32_to_quad<T>(x);
+        else f.z[a] = f32_to_quad<T>(x);
+      }
+    }
+    return f;
+  }
+  __device__ __forceinline__ static void store_frags(int w, const Frags& f, Q* sf, Q* szq) {
+    const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+#pragma unroll
+    for (int a = 0; a < AGPW; ++a) {
+      const int ag = group(w, a);
+      const int l = ag / NB, cb = ag % NB;
+#pragma unroll
+      for (int eb = 0; eb < NB; ++eb) sf[((l * NB + eb) * NB + cb) * 64 + lane] = f.s[a][eb];
+      if (r == 0) szq[(l * NB + cb) * 4 + g] = f.z[a];
     }
   }
   // Write this wave's tiles as apply fragments (sf, szq) for the prefix far part.
@@ -805,7 +891,7 @@ __global__ __launch_bounds__(NT) void k_band_ring(const T* __restrict__ q,
     NearState<D> st;
     st.init();
     const int lo = max(0, i0 - band_k), hi = min(N - 1, i0 + 15 + band_k);
-    near_units<T, D, false>(st, qq, sm.k, sm.v, ST, map, lo >> 5, hi >> 5, i0, N, band_k,
+    near_units<T, D, false, 6>(st, qq, sm.k, sm.v, ST, map, lo >> 5, hi >> 5, i0, N, band_k,
                             scale2);
     Q pq[R][NB];
     phi_q<T, D, R>(qq, pq);
@@ -869,6 +955,7 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
   Tiles tiles;
   if (has_ag) tiles.load(w, prefix + ((size_t)bh * nseg + seg) * R * D * (D + 1));
   ring_fill<T, D, R>(sm, kh, vh, map.ua0, U, map, N);
+  if (has_ag) tiles.to_frags(w, sm.sf, sm.sz);
   Q qq[NB], qn[NB];
   load_q<T, D>(qh, s0 + 16 * w + r, N, qq);
   RowCopy<T, D, NT, 64> pk, pv;
@@ -882,35 +969,48 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
   for (int t = 0; t < ntile; ++t) {
     const int t0 = s0 + t * TM, i0 = t0 + 16 * w, row = i0 + r;
     const int rt0 = map(t0 >> 5), rt1 = map((t0 >> 5) + 1);  // ring rows of the tile
-    if (has_ag) tiles.to_frags(w, sm.sf, sm.sz);
     __syncthreads();  // window, phi rows and prefix fragments of tile t are in LDS
     NearState<D> st;
     st.init();
     const int lo = max(0, i0 - band_k), hi = min(N - 1, i0 + 15);
-    near_units<T, D, true>(st, qq, sm.k, sm.v, ST, map, lo >> 5, hi >> 5, i0, N, band_k,
-                           scale2);
+    near_units<T, D, true, 4>(st, qq, sm.k, sm.v, ST, map, lo >> 5, hi >> 5, i0, N, band_k,
+                              scale2);
+    f32x4 fo[NB];
+    near_out<D>(st, sn, fo);
     Q pq[R][NB];
     phi_q<T, D, R>(qq, pq);
-    f32x4 num[R][NB + 1];
 #pragma unroll
-    for (int l = 0; l < R; ++l)
+    for (int l = 0; l < R; ++l) {
+      f32x4 num[NB + 1];
 #pragma unroll
-      for (int nb = 0; nb <= NB; ++nb) num[l][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    causal_intra<T, D, R>(sm.pk, sm.v + rt0 * ST, sm.v + rt1 * ST, ST, t0, w, pq, num);
-    far_terms<T, D, R, true>(sm.sf, sm.sz, pq, num);
-    blend_store<T, D, R>(out + base, row, N, sn, sfw, st, num);
+      for (int nb = 0; nb <= NB; ++nb) num[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      causal_intra<T, D, R>(sm.pk, sm.v + rt0 * ST, sm.v + rt1 * ST, ST, t0, w, l, pq[l], num);
+      far_terms_map<T, D>(sm.sf, sm.sz, l, pq[l], num);
+      add_far_map<D>(num, sfw, fo);
+    }
+    store_row<T, D>(out + base, row, N, fo);
     if (t + 1 < ntile) {
+      // everything tile t+1 needs in LDS is prepared in registers first, so
+      // that only plain stores sit between the two barriers (the scheduling
+      // fence keeps this work from being hoisted into the compute above,
+      // where it would raise register pressure)
+      __builtin_amdgcn_sched_barrier(0);
       if (has_ag) {
         tiles.add_unit(w, sm.pk, 0, sm.v + rt0 * ST, ST);
         tiles.add_unit(w, sm.pk, 32, sm.v + rt1 * ST, ST);
       }
+      typename Tiles::Frags fr;
+      if (has_ag) fr = tiles.pack();
+      PhiRows<T, D, R> ph;
+      ph.compute(pk, t0 + TM, N);  // the prefetched rows are the keys of tile t+1
       __syncthreads();  // every wave is done with tile t's LDS
-      const int ua_new = map.ua0 + 2 * t + U;  // = the keys of tile t+1
+      const int ua_new = map.ua0 + 2 * t + U;
       const int ra = map(ua_new), rb = map(ua_new + 1);
       auto rowmap = [=](int i) { return (i < 32 ? ra : rb) + (i & 31); };
       pk.store(sm.k, ST, 64, rowmap);
       pv.store(sm.v, ST, 64, rowmap);
-      phi_rows_from_regs<T, D, R>(pk, t0 + TM, N, ST, sm.pk);
+      ph.store(sm.pk, ST);
+      if (has_ag) Tiles::store_frags(w, fr, sm.sf, sm.sz);
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) qq[cb] = qn[cb];
       if (t + 2 < ntile) {
@@ -976,7 +1076,7 @@ __global__ __launch_bounds__(NT) void k_band_rounds(const T* __restrict__ q,
     __syncthreads();
     const int lo = max(max(0, i0 - band_k), ks), hi = min(min(N - 1, i0 + 15 + band_k), ks + nk - 1);
     if (lo <= hi)
-      near_units<T, D, false>(st, qq, sm.k, sm.v, ST, RoundMap{ks}, lo >> 5, hi >> 5, i0, N,
+      near_units<T, D, false, 6>(st, qq, sm.k, sm.v, ST, RoundMap{ks}, lo >> 5, hi >> 5, i0, N,
                               band_k, scale2);
   }
   Q pq[R][NB];
@@ -1042,11 +1142,14 @@ __global__ __launch_bounds__(NT) void k_causal_rounds(const T* __restrict__ q,
       __syncthreads();
       const int lo = max(max(0, i0 - band_k), ks), hj = min(min(N - 1, i0 + 15), ks + nk - 1);
       if (lo <= hj)
-        near_units<T, D, true>(st, qq, sm.k, sm.v, ST, RoundMap{ks}, lo >> 5, hj >> 5, i0, N,
+        near_units<T, D, true, 4>(st, qq, sm.k, sm.v, ST, RoundMap{ks}, lo >> 5, hj >> 5, i0, N,
                                band_k, scale2);
       if (ke != hi) continue;
       const int tk = t0 - ks;
-      causal_intra<T, D, R>(sm.pk, sm.v + tk * ST, sm.v + (tk + 32) * ST, ST, t0, w, pq, num);
+#pragma unroll
+      for (int l = 0; l < R; ++l)
+        causal_intra<T, D, R>(sm.pk, sm.v + tk * ST, sm.v + (tk + 32) * ST, ST, t0, w, l, pq[l],
+                              num[l]);
       if (has_ag && t0 + TM < s1) {
         tiles.add_unit(w, sm.pk, 0, sm.v + tk * ST, ST);
         tiles.add_unit(w, sm.pk, 32, sm.v + (tk + 32) * ST, ST);
