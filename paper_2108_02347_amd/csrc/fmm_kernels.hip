@@ -234,6 +234,90 @@ __device__ __forceinline__ void near_units(NearState<D>& st, const typename Quad
   }
 }
 
+// Straight-line form of near_units for a strip whose band is exactly the NU
+// units [ua_lo, ua_lo + NU) with units 1 .. NU-2 inside the band for every
+// row of the strip (and inside [0, N)): no per-unit branches, so the
+// compiler can overlap one unit's score products with another's softmax
+// arithmetic; only the two end units are masked.  Fresh state only.
+template <typename T, int D, bool CAUSAL, int NU, class Map>
+__device__ __forceinline__ void near_fixed(NearState<D>& st, const typename QuadOf<T>::type* qq,
+                                           const T* kr, const T* vr, int ST, Map map, int ua_lo,
+                                           int i0, int N, int band_k, float scale2) {
+  using Q = typename QuadOf<T>::type;
+  constexpr int NB = D / 16;
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const int row = i0 + r;
+  const Q ones = quad_fill<T>(1.f);
+  f32x4 sc[NU][2];
+  int urow[NU];
+#pragma unroll
+  for (int gi = 0; gi < NU; ++gi) urow[gi] = map(ua_lo + gi);
+#pragma unroll
+  for (int gi = 0; gi < NU; ++gi) {
+    const T* kx = kr + urow[gi] * ST;
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      Q ka[NB];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) ka[cb] = ld_quad(kx, 16 * b + r, 16 * cb + 4 * g, ST);
+      sc[gi][b] = contract<NB>(ka, qq, f32x4{0.f, 0.f, 0.f, 0.f});
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 2; ++e) {
+    const int gi = e == 0 ? 0 : NU - 1;
+    const int j0 = (ua_lo + gi) * 32;
+    int lo = max(row - band_k, 0) - j0 - 4 * g;
+    int span = min(CAUSAL ? row : row + band_k, N - 1) - j0 - 4 * g - lo;
+    if (span < 0) { lo = 64; span = 0; }
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if ((unsigned)(16 * b + i - lo) > (unsigned)span) sc[gi][b][i] = -INFINITY;
+  }
+  float mloc = -INFINITY;
+#pragma unroll
+  for (int gi = 0; gi < NU; ++gi)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mloc = fmaxf(mloc, sc[gi][b][i]);
+  const float mnew = col_max(mloc);
+  const float ms = mnew * scale2;
+  st.m = mnew;
+  st.fresh = 0;
+#pragma unroll
+  for (int gi = 0; gi < NU; ++gi) {
+    float p[2][4];
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p[b][i] = __builtin_amdgcn_exp2f(fmaf(sc[gi][b][i], scale2, -ms));
+    const Q pq0 = f32_to_quad<T>(p[0]), pq1 = f32_to_quad<T>(p[1]);
+    const T* vx = vr + urow[gi] * ST;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+      st.o[nb] = mma_step2(ld_tquad(vx, 0, 16 * nb, ST), ld_tquad(vx, 16, 16 * nb, ST), pq0, pq1,
+                           st.o[nb]);
+    st.o[NB] = mma_step2(ones, ones, pq0, pq1, st.o[NB]);
+  }
+}
+
+// True when the strip [i0, i0 + 16) takes the near_fixed<NU> path: its band
+// spans exactly NU units, the middle ones inside the band for all its rows
+// and the whole span inside [0, N).
+template <bool CAUSAL, int NU>
+__device__ __forceinline__ bool fixed_strip(int i0, int N, int band_k) {
+  const int lo = i0 - band_k, hi = CAUSAL ? i0 + 15 : i0 + 15 + band_k;
+  if (lo < 0 || hi >= N) return false;
+  const int ul = lo >> 5;
+  if ((hi >> 5) - ul != NU - 1) return false;
+  if (NU < 3) return true;
+  const int first_mid = (ul + 1) * 32, last_mid_end = (ul + NU - 2) * 32 + 31;
+  return first_mid >= i0 + 15 - band_k && last_mid_end <= (CAUSAL ? i0 : i0 + band_k);
+}
+
 // ------------------------------------------------------------------ far field
 // phi_1(q), phi_2(q) of the lane's row as operand quads.
 template <typename T, int D, int R>
@@ -891,8 +975,12 @@ __global__ __launch_bounds__(NT) void k_band_ring(const T* __restrict__ q,
     NearState<D> st;
     st.init();
     const int lo = max(0, i0 - band_k), hi = min(N - 1, i0 + 15 + band_k);
-    near_units<T, D, false, 6>(st, qq, sm.k, sm.v, ST, map, lo >> 5, hi >> 5, i0, N, band_k,
-                            scale2);
+    if (fixed_strip<false, 5>(i0, N, band_k))
+      near_fixed<T, D, false, 5>(st, qq, sm.k, sm.v, ST, map, (i0 - band_k) >> 5, i0, N, band_k,
+                                 scale2);
+    else
+      near_units<T, D, false, 6>(st, qq, sm.k, sm.v, ST, map, lo >> 5, hi >> 5, i0, N, band_k,
+                                 scale2);
     Q pq[R][NB];
     phi_q<T, D, R>(qq, pq);
     f32x4 num[R][NB + 1];
@@ -973,8 +1061,12 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
     NearState<D> st;
     st.init();
     const int lo = max(0, i0 - band_k), hi = min(N - 1, i0 + 15);
-    near_units<T, D, true, 4>(st, qq, sm.k, sm.v, ST, map, lo >> 5, hi >> 5, i0, N, band_k,
-                              scale2);
+    if (fixed_strip<true, 3>(i0, N, band_k))
+      near_fixed<T, D, true, 3>(st, qq, sm.k, sm.v, ST, map, (i0 - band_k) >> 5, i0, N, band_k,
+                                scale2);
+    else
+      near_units<T, D, true, 4>(st, qq, sm.k, sm.v, ST, map, lo >> 5, hi >> 5, i0, N, band_k,
+                                scale2);
     f32x4 fo[NB];
     near_out<D>(st, sn, fo);
     Q pq[R][NB];
