@@ -42,7 +42,102 @@ def parse():
                    help="run only warmup + timed steps of the main workload, print nothing else")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run a plain 256 MiB device copy (for counter calibration) and exit")
+    p.add_argument("--traffic-summary", nargs=5, metavar=("KERNEL", "FETCH_CSV", "WRITE_CSV",
+                                                          "COPY_FETCH_CSV", "COPY_WRITE_CSV"),
+                   help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE counter CSVs of the "
+                        "profile-only run and of the copy calibration into the traffic "
+                        "summary under profiles/ (no GPU needed)")
+    p.add_argument("--trace-summary", metavar="KERNEL_STATS_CSV",
+                   help="turn the kernel_stats.csv of a rocprofv3 --kernel-trace --stats run "
+                        "of this benchmark into profiles/kernel_trace_stress64k.md")
     return p.parse_args()
+
+
+# library kernel id -> gfx950 kernel of the stress64k workload (bf16, d=64, rank 2)
+STRESS_KERNELS = {
+    "seg_state": "k_seg_state<unsigned short, 64, 2>",
+    "band_apply": "k_band_ring<unsigned short, 64, 2>",
+    "causal_apply": "k_causal_ring<unsigned short, 64, 2>",
+}
+
+
+def trace_summary(stats_csv):
+    import csv
+    import re
+    rows = list(csv.DictReader(open(stats_csv)))
+    path = os.path.join(ROOT, "profiles", "kernel_trace_stress64k.md")
+    with open(path, "w") as f:
+        f.write("# rocprofv3 kernel trace of bench.py (stress64k + lra4k)\n\n")
+        f.write("Command, from the repository root on one MI355X:\n\n")
+        f.write("    cd /tmp && export TMPDIR=/tmp && rocprofv3 --kernel-trace --stats -f csv "
+                "-d <out> -o trace -- python3 <repo>/bench.py --no-cpu-baseline\n\n")
+        f.write("Rows: rocprofv3's own kernel_stats.csv (durations in microseconds), names "
+                "shortened to the kernel template.  The run times 50 steps (+5 warm-up) of "
+                "one non-causal and one causal forward of B=1 H=8 N=65536 d=64 bf16 k=64 "
+                "rank 2, then 52 calls of each form alone, then 105 calls of the N=4096 "
+                "shape (B=8 H=2 d=32 bf16 k=20 rank 2, non-causal).\n\n")
+        f.write(f"kernel source hash: {kernel_source_hash()}\n\n")
+        f.write("| kernel | calls | avg us | min us | max us | share % |\n|---|---|---|---|---|---|\n")
+        for r in rows:
+            name = re.sub(r"\(.*", "", r["Name"]).replace("void ", "")
+            if len(name) > 70:
+                name = name[:67] + "..."
+            f.write(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                    f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                    f"{float(r['Percentage']):.1f} |\n")
+    print(path)
+
+
+def traffic_summary(kernel, fetch_csv, write_csv, cfetch_csv, cwrite_csv):
+    """HBM bytes per launch of `kernel` from FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch), each scaled by what the same counter reads for the plain 256 MiB
+    device copy of the calibration run."""
+    import csv
+    import statistics
+
+    def per_kernel(path, counter):
+        vals = {}
+        for row in csv.DictReader(open(path)):
+            if row["Counter_Name"] != counter:
+                continue
+            vals.setdefault(row["Kernel_Name"], []).append(float(row["Counter_Value"]))
+        return vals
+
+    def pick(vals, needle):
+        hits = [v for k, v in vals.items() if needle in k]
+        if not hits:
+            raise SystemExit(f"no dispatch of {needle} in the counter file")
+        return statistics.median(hits[0]), len(hits[0])
+
+    copy_bytes = 256 << 20
+    f_copy, _ = pick(per_kernel(cfetch_csv, "FETCH_SIZE"), "copyBuffer")
+    w_copy, _ = pick(per_kernel(cwrite_csv, "WRITE_SIZE"), "copyBuffer")
+    f_scale = copy_bytes / (f_copy * 1024.0)
+    w_scale = copy_bytes / (w_copy * 1024.0)
+    needle = STRESS_KERNELS[kernel]
+    f_kib, n_f = pick(per_kernel(fetch_csv, "FETCH_SIZE"), needle)
+    w_kib, n_w = pick(per_kernel(write_csv, "WRITE_SIZE"), needle)
+    hbm = f_kib * 1024.0 * f_scale + w_kib * 1024.0 * w_scale
+    path = os.path.join(ROOT, "profiles", f"{kernel}_stress64k_traffic.txt")
+    with open(path, "w") as f:
+        f.write(f"# HBM traffic of {kernel} on the stress64k workload (B=1 H=8 N=65536 d=64 "
+                "bf16, k=64, rank 2)\n")
+        f.write("# commands (repo root on one MI355X, cd /tmp && export TMPDIR=/tmp first):\n")
+        for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
+            f.write(f"#   rocprofv3 --pmc {ctr} -f csv -d <out> -o p -- python3 <repo>/bench.py "
+                    "--profile-only --steps 5 --warmup 1\n")
+            f.write(f"#   rocprofv3 --pmc {ctr} -f csv -d <out> -o p -- python3 <repo>/bench.py "
+                    "--copy-calibration\n")
+        f.write("# scale = 256 MiB / counter bytes of the plain device copy "
+                "(__amd_rocclr_copyBuffer), per counter\n")
+        f.write(f"kernel: {kernel} ({needle})\n")
+        f.write(f"dispatches_fetch: {n_f}\ndispatches_write: {n_w}\n")
+        f.write(f"fetch_kib_per_launch_raw: {f_kib:.1f}\nwrite_kib_per_launch_raw: {w_kib:.1f}\n")
+        f.write(f"copy_fetch_kib_raw: {f_copy:.1f}\ncopy_write_kib_raw: {w_copy:.1f}\n")
+        f.write(f"fetch_scale: {f_scale:.4f}\nwrite_scale: {w_scale:.4f}\n")
+        f.write(f"hbm_bytes_per_launch: {hbm:.0f}\n")
+        f.write(f"kernel_source_hash: {kernel_source_hash()}\n")
+    print(path)
 
 
 def kernel_source_hash() -> str:
@@ -125,6 +220,12 @@ def cpu_baseline(host_inputs, w):
 
 def main():
     args = parse()
+    if args.traffic_summary:
+        traffic_summary(*args.traffic_summary)
+        return
+    if args.trace_summary:
+        trace_summary(args.trace_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); the operator "
               "is single-GPU in this build, see DESIGN.md for how it would shard.",

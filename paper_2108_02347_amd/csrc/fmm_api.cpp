@@ -96,9 +96,8 @@ struct EventTimer : fmm::LaunchTimer {
   bool enabled = false;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> pending[FMM_KERNEL_COUNT];
   std::vector<hipEvent_t> pool;
-  hipEvent_t cur = nullptr;
 
-  hipEvent_t take() {
+  hipEvent_t take_one() {
     if (!pool.empty()) {
       hipEvent_t e = pool.back();
       pool.pop_back();
@@ -108,18 +107,17 @@ struct EventTimer : fmm::LaunchTimer {
     if (hipEventCreate(&e) != hipSuccess) return nullptr;
     return e;
   }
-  void begin(int, hipStream_t s) override {
-    if (!enabled) return;
-    cur = take();
-    if (cur) hipEventRecord(cur, s);
+  bool take(int, hipEvent_t* start, hipEvent_t* stop) override {
+    if (!enabled) return false;
+    *start = take_one();
+    *stop = take_one();
+    if (*start && *stop) return true;
+    if (*start) pool.push_back(*start);
+    if (*stop) pool.push_back(*stop);
+    return false;
   }
-  void end(int kernel, hipStream_t s) override {
-    if (!enabled || !cur) return;
-    hipEvent_t stop = take();
-    if (!stop) return;
-    hipEventRecord(stop, s);
-    pending[kernel].push_back({cur, stop});
-    cur = nullptr;
+  void commit(int kernel, hipEvent_t start, hipEvent_t stop) override {
+    pending[kernel].push_back({start, stop});
   }
 };
 

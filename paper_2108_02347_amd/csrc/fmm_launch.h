@@ -24,10 +24,12 @@ struct LaunchArgs {
   int L_apply;     // rows per apply segment (multiple of the tile height)
 };
 
-// Records HIP events around kernel launches when timing is enabled.
+// Supplies a start/stop HIP event pair per kernel launch when timing is
+// enabled; the events are attached to the kernel's own dispatch
+// (hipExtLaunchKernel), so they bracket exactly the kernel's execution.
 struct LaunchTimer {
-  virtual void begin(int kernel, hipStream_t s) = 0;
-  virtual void end(int kernel, hipStream_t s) = 0;
+  virtual bool take(int kernel, hipEvent_t* start, hipEvent_t* stop) = 0;
+  virtual void commit(int kernel, hipEvent_t start, hipEvent_t stop) = 0;
   virtual ~LaunchTimer() {}
 };
 
