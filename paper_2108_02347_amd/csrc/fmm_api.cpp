@@ -39,7 +39,7 @@ long long seg_rows(long long bh, int N, long long target_wg, int tm) {
   return L < tm ? tm : L;
 }
 
-Plan make_plan(int B, int H, int N, int d, int rank, int esize) {
+Plan make_plan(int B, int H, int N, int d, int rank, int esize, int apply_tm) {
   const int tm = fmm::tile_rows();
   const long long bh = (long long)B * H;
   // state segments: ~512 workgroups, but each segment's state record
@@ -48,7 +48,7 @@ Plan make_plan(int B, int H, int N, int d, int rank, int esize) {
   const long long lmin = 8LL * rank * (d + 1) / esize;
   if (L < lmin) L = (lmin + tm - 1) / tm * tm;
   // non-causal apply walk: ~512 workgroups (two per CU), no state per segment
-  const long long La = seg_rows(bh, N, 512, tm);
+  const long long La = seg_rows(bh, N, 512, apply_tm);
   Plan p;
   p.L = (int)L;
   p.nseg = (int)((N + L - 1) / L);
@@ -179,7 +179,10 @@ int run(const void* q, const void* k, const void* v, void* out, int B, int H, in
         void* ws, size_t ws_bytes, bool own_ws, void* stream) {
   int st = validate(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype);
   if (st != FMM_OK) return st;
-  const Plan p = make_plan(B, H, N, d, rank, dtype == FMM_DTYPE_BF16 ? 2 : 4);
+  const int kc = band_k < N ? band_k : N;
+  const int apply_tm = fmm::band_pair_applies(dtype, d, kc, causal) ? fmm::pair_tile_rows()
+                                                                    : fmm::tile_rows();
+  const Plan p = make_plan(B, H, N, d, rank, dtype == FMM_DTYPE_BF16 ? 2 : 4, apply_tm);
   if (own_ws) {
     st = acquire_ws(stream, p.ws_bytes, &ws);
     if (st != FMM_OK) return st;
@@ -236,7 +239,8 @@ size_t fmm_attn_workspace_bytes(int B, int H, int N, int d, int rank, int causal
   if (B < 1 || H < 1 || N < 1 || (causal != 0 && causal != 1) || !supported(d, rank)) return 0;
   // the plan depends on the element size only through the segment length
   // floor; report the larger of the two dtypes' needs
-  const Plan a = make_plan(B, H, N, d, rank, 2), b = make_plan(B, H, N, d, rank, 4);
+  const int tm = fmm::tile_rows();
+  const Plan a = make_plan(B, H, N, d, rank, 2, tm), b = make_plan(B, H, N, d, rank, 4, tm);
   return a.ws_bytes > b.ws_bytes ? a.ws_bytes : b.ws_bytes;
 }
 

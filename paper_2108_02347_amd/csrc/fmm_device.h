@@ -133,6 +133,8 @@ __device__ __forceinline__ float phi_l(float x, int l) {
   return l == 0 ? p1 : p2;
 }
 
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
 __device__ __forceinline__ float sigmoidf_exact(float w) {
   // 1/(1+exp(-w)); w = +inf -> 1, w = -inf -> 0
   return 1.0f / (1.0f + expf(-w));

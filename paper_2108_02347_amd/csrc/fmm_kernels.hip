@@ -32,8 +32,6 @@
 // S_l is stored as tiles (cb, eb) of 16 x 16, each as 64 lanes x 4 floats with
 // lane 16g + r holding S_l[16cb + 4g + i][16eb + r], i = 0..3; z_l (d floats)
 // follows.  A wave's accumulator tile is then one coalesced float4 per lane.
-#include <hip/hip_ext.h>
-
 #include "fmm_device.h"
 #include "fmm_launch.h"
 
@@ -98,8 +96,6 @@ template <typename T> __device__ __forceinline__ typename QuadOf<T>::type quad_f
   const float f[4] = {x, x, x, x};
   return f32_to_quad<T>(f);
 }
-
-__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
 // ------------------------------------------------------------------ row staging
 // Copy rows [k0, k0 + nrows) of a [N, D] head into LDS (row-major, stride ST);
@@ -1255,20 +1251,6 @@ __global__ __launch_bounds__(NT) void k_causal_rounds(const T* __restrict__ q,
 }
 
 // ------------------------------------------------------------------ launchers
-// Launch on stream s; with timing enabled, the timer's events are attached to
-// this dispatch.
-template <typename F, typename... Args>
-static void launch(LaunchTimer* t, int id, F kern, dim3 grid, dim3 block, size_t shm,
-                   hipStream_t s, Args... args) {
-  hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (t->take(id, &e0, &e1)) {
-    hipExtLaunchKernelGGL(kern, grid, block, (uint32_t)shm, s, e0, e1, 0, args...);
-    t->commit(id, e0, e1);
-  } else {
-    hipLaunchKernelGGL(kern, grid, block, shm, s, args...);
-  }
-}
-
 template <typename T, int D, int R>
 static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
   using RG = Ring<T, D, R>;
@@ -1305,36 +1287,38 @@ static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
   }();
   if (lds_attr != hipSuccess) return lds_attr;
 
-  launch(timer, FMM_KERNEL_SEG_STATE, k_seg_state<T, D, R>, dim3(a.nseg * BH), dim3(SNT), 0, s,
+  launch_timed(timer, FMM_KERNEL_SEG_STATE, k_seg_state<T, D, R>, dim3(a.nseg * BH), dim3(SNT), 0, s,
          k, v, part, a.N, a.L, a.nseg);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
 
   const dim3 cgrid((REC + 63) / 64, BH);
   if (a.causal)
-    launch(timer, FMM_KERNEL_STATE_COMBINE, k_state_combine<true>, cgrid, dim3(256), 0, s, part,
+    launch_timed(timer, FMM_KERNEL_STATE_COMBINE, k_state_combine<true>, cgrid, dim3(256), 0, s, part,
            fin, a.nseg, REC);
   else
-    launch(timer, FMM_KERNEL_STATE_COMBINE, k_state_combine<false>, cgrid, dim3(256), 0, s, part,
+    launch_timed(timer, FMM_KERNEL_STATE_COMBINE, k_state_combine<false>, cgrid, dim3(256), 0, s, part,
            fin, a.nseg, REC);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
 
   if (a.causal) {
     if (ring)
-      launch(timer, FMM_KERNEL_CAUSAL_APPLY, k_causal_ring<T, D, R>, dim3(BH * a.nseg), dim3(NT),
+      launch_timed(timer, FMM_KERNEL_CAUSAL_APPLY, k_causal_ring<T, D, R>, dim3(BH * a.nseg), dim3(NT),
              lds, s, q, k, v, o, (const float*)part, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L,
              a.nseg, scale2);
     else
-      launch(timer, FMM_KERNEL_CAUSAL_APPLY, k_causal_rounds<T, D, R>, dim3(BH * a.nseg),
+      launch_timed(timer, FMM_KERNEL_CAUSAL_APPLY, k_causal_rounds<T, D, R>, dim3(BH * a.nseg),
              dim3(NT), lds, s, q, k, v, o, (const float*)part, a.w_near, a.w_far, a.H, a.N,
              a.band_k, a.L, a.nseg, scale2);
   } else {
-    if (ring) {
-      launch(timer, FMM_KERNEL_BAND_APPLY, k_band_ring<T, D, R>, dim3(BH * a.nseg_apply),
+    if (band_pair_applies(a.dtype, a.d, a.band_k, a.causal)) {
+      return launch_band_pair(a, timer, fin);
+    } else if (ring) {
+      launch_timed(timer, FMM_KERNEL_BAND_APPLY, k_band_ring<T, D, R>, dim3(BH * a.nseg_apply),
              dim3(NT), lds, s, q, k, v, o, (const float*)fin, a.w_near, a.w_far, a.H, a.N,
              a.band_k, a.L_apply, a.nseg_apply, scale2);
     } else {
       const int ntile = (a.N + TM - 1) / TM;
-      launch(timer, FMM_KERNEL_BAND_APPLY, k_band_rounds<T, D, R>, dim3(BH * ntile), dim3(NT),
+      launch_timed(timer, FMM_KERNEL_BAND_APPLY, k_band_rounds<T, D, R>, dim3(BH * ntile), dim3(NT),
              lds, s, q, k, v, o, (const float*)fin, a.w_near, a.w_far, a.H, a.N, a.band_k, ntile,
              scale2);
     }

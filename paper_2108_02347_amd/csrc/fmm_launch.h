@@ -1,6 +1,7 @@
 // Host-side interface between the C ABI and the kernel launchers.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 
@@ -33,7 +34,28 @@ struct LaunchTimer {
   virtual ~LaunchTimer() {}
 };
 
+// Launch `kern` on stream s; with timing enabled, the timer's events are
+// attached to this dispatch.
+template <typename F, typename... Args>
+inline void launch_timed(LaunchTimer* t, int id, F kern, dim3 grid, dim3 block, size_t shm,
+                         hipStream_t s, Args... args) {
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (t->take(id, &e0, &e1)) {
+    hipExtLaunchKernelGGL(kern, grid, block, (uint32_t)shm, s, e0, e1, 0, args...);
+    t->commit(id, e0, e1);
+  } else {
+    hipLaunchKernelGGL(kern, grid, block, shm, s, args...);
+  }
+}
+
 hipError_t launch_forward(const LaunchArgs& a, LaunchTimer* timer);
 int tile_rows();
+
+// Non-causal apply with two 16-row strips per wavefront (fmm_pair.hip): bf16,
+// d = 32 or 64, band half-width <= 64.  Its row segments are multiples of
+// pair_tile_rows().
+bool band_pair_applies(int dtype, int d, int band_k, int causal);
+int pair_tile_rows();
+hipError_t launch_band_pair(const LaunchArgs& a, LaunchTimer* timer, const float* fin);
 
 }  // namespace fmm
