@@ -180,7 +180,7 @@ int run(const void* q, const void* k, const void* v, void* out, int B, int H, in
   int st = validate(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype);
   if (st != FMM_OK) return st;
   const int kc = band_k < N ? band_k : N;
-  const int apply_tm = fmm::band_pair_applies(dtype, d, kc, causal) ? fmm::pair_tile_rows()
+  const int apply_tm = fmm::band_pair_applies(dtype, d, kc, causal, N) ? fmm::pair_tile_rows()
                                                                     : fmm::tile_rows();
   const Plan p = make_plan(B, H, N, d, rank, dtype == FMM_DTYPE_BF16 ? 2 : 4, apply_tm);
   if (own_ws) {

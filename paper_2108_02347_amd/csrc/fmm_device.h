@@ -6,13 +6,13 @@
 // ---------------------------------------------------------------
 // A 16x16 MFMA tile is held by one wavefront: lane L has column r = L % 16 and
 // lane group g = L / 16 (0..3).  The output (C/D) of
-// v_mfma_f32_16x16x{4f32,16bf16_1k,32_bf16} holds rows 4g..4g+3 of column r.
+// v_mfma_f32_16x16x{4f32,32_bf16} holds rows 4g..4g+3 of column r.
 // For the operands, the contraction index runs over 16-wide blocks, and in
 // every block lane group g supplies the four consecutive indices 4g..4g+3
 // (a "quad").  One MFMA step consumes:
 //   fp32 16x16x4   : one element of one quad      (4 steps per block)
-//   bf16 16x16x16  : one quad                     (1 step per block)
-//   bf16 16x16x32  : two quads of two blocks      (1 step per 2 blocks)
+//   bf16 16x16x32  : two quads of two blocks      (1 step per 2 blocks; a
+//                    single quad is padded with a zero quad)
 // A and B use the same index for the same (lane group, element) slot, so any
 // such assignment contracts correctly; the quad assignment is chosen because
 // the MFMA output already has it (rows 4g..4g+3), so a score tile can be fed
@@ -85,11 +85,14 @@ __device__ __forceinline__ f32x4 mma_step(const float4& a, const float4& b, f32x
   c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, c, 0, 0, 0);
   return c;
 }
+// One bf16 quad: issued as v_mfma_f32_16x16x32_bf16 with the second quad of
+// both operands zero.  (The 16x16x16 bf16 instruction gave wrong sums in some
+// instruction schedules of the causal kernel at d = 16 with this toolchain;
+// the zero-padded 32-wide form is exact and only d = 16 contractions use it.)
 __device__ __forceinline__ f32x4 mma_step(const uint2& a, const uint2& b, f32x4 c) {
-  s16x4 av, bv;
-  av = __builtin_bit_cast(s16x4, a);
-  bv = __builtin_bit_cast(s16x4, b);
-  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, bv, c, 0, 0, 0);
+  const uint4 ua = make_uint4(a.x, a.y, 0u, 0u), ub = make_uint4(b.x, b.y, 0u, 0u);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ua),
+                                                 __builtin_bit_cast(bf16x8, ub), c, 0, 0, 0);
 }
 __device__ __forceinline__ f32x4 mma_step2(const uint2& a0, const uint2& a1,
                                            const uint2& b0, const uint2& b1, f32x4 c) {

@@ -68,6 +68,43 @@ template <typename T, int D, int R> struct Ring {
   }
 };
 
+// ------------------------------------------------------------------ global access
+// Rows [r0, r0 + nrows) of a [N, D] head, clipped to [0, N), as a raw buffer
+// whose offsets count from row max(r0, 0).  Buffer loads outside it (rows
+// before 0 give negative, i.e. huge unsigned, offsets; rows at or beyond the
+// clip give offsets past its size) return zeros without touching memory and
+// stores there are dropped, so row-range checks need no branches and the
+// compiler's memory-counter waits stay exact across the prefetch pipeline.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+template <typename T, int D>
+__device__ __forceinline__ Rsrc rows_rsrc(const T* head, int r0, int nrows, int N) {
+  const int b = max(r0, 0);
+  const int n = max(0, min(r0 + nrows, N) - b);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(head + (size_t)b * D), 0,
+                                           n * D * (int)sizeof(T), 0x00020000);
+}
+__device__ __forceinline__ uint4 buf_ld(Rsrc rs, int off, uint4*) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+}
+__device__ __forceinline__ float4 buf_ld(Rsrc rs, int off, float4*) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+}
+__device__ __forceinline__ uint2 buf_ld(Rsrc rs, int off, uint2*) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0));
+}
+__device__ __forceinline__ void buf_st(Rsrc rs, int off, const float4& v) {
+  typedef int i32x4 __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, v), rs, off, 0, 0);
+}
+__device__ __forceinline__ void buf_st(Rsrc rs, int off, const uint2& v) {
+  typedef int i32x2 __attribute__((ext_vector_type(2)));
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(i32x2, v), rs, off, 0, 0);
+}
+// First row of the lane's 16-row strip (wave-uniform): row - r.
+__device__ __forceinline__ int strip_row0(int row) {
+  return __builtin_amdgcn_readfirstlane(row - (threadIdx.x & 15));
+}
+
 // ------------------------------------------------------------------ LDS operand reads
 // Row-major quad: X[row][col .. col+3].
 template <typename T>
@@ -107,13 +144,13 @@ struct RowCopy {
   static constexpr int IT = (MAXROWS * CPR + NTHR - 1) / NTHR;
   uint4 r[IT];
   __device__ __forceinline__ void load(const T* __restrict__ src, int k0, int nrows, int N) {
+    const Rsrc rs = rows_rsrc<T, D>(src, k0, nrows, N);
+    const int b = max(k0, 0);
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int t = threadIdx.x + it * NTHR;
       const int key = k0 + t / CPR;
-      r[it] = make_uint4(0, 0, 0, 0);
-      if (t < nrows * CPR && key >= 0 && key < N)
-        r[it] = *reinterpret_cast<const uint4*>(src + (size_t)key * D + (t % CPR) * Lay<T>::EPC);
+      r[it] = buf_ld(rs, ((key - b) * D + (t % CPR) * Lay<T>::EPC) * (int)sizeof(T), (uint4*)0);
     }
   }
   template <typename F>
@@ -403,13 +440,12 @@ __device__ __forceinline__ void add_far_map(const f32x4* num, float sfw, f32x4* 
 
 template <typename T, int D>
 __device__ __forceinline__ void store_row(T* __restrict__ oh, int row, int N, const f32x4* fo) {
-  using Q = typename QuadOf<T>::type;
-  const int g = (threadIdx.x & 63) >> 4;
-  if (row >= N) return;
+  const int lane = threadIdx.x & 63, g = lane >> 4, r = lane & 15;
+  const Rsrc rs = rows_rsrc<T, D>(oh, strip_row0(row), 16, N);
 #pragma unroll
   for (int nb = 0; nb < D / 16; ++nb) {
     const float o[4] = {fo[nb][0], fo[nb][1], fo[nb][2], fo[nb][3]};
-    *reinterpret_cast<Q*>(oh + (size_t)row * D + 16 * nb + 4 * g) = f32_to_quad<T>(o);
+    buf_st(rs, (r * D + 16 * nb + 4 * g) * (int)sizeof(T), f32_to_quad<T>(o));
   }
 }
 
@@ -418,9 +454,9 @@ template <typename T, int D, int R>
 __device__ __forceinline__ void blend_store(T* __restrict__ oh, int row, int N, float sn,
                                             float sfw, const NearState<D>& st,
                                             const f32x4 (*num)[D / 16 + 1]) {
-  using Q = typename QuadOf<T>::type;
   constexpr int NB = D / 16;
-  const int g = (threadIdx.x & 63) >> 4;
+  const int lane = threadIdx.x & 63, g = lane >> 4, r = lane & 15;
+  const Rsrc rs = rows_rsrc<T, D>(oh, strip_row0(row), 16, N);
   const float a = sn > 0.f ? sn * fast_rcp(st.o[NB][0]) : 0.f;
   float f[R];
 #pragma unroll
@@ -435,8 +471,7 @@ __device__ __forceinline__ void blend_store(T* __restrict__ oh, int row, int N, 
       for (int l = 0; l < R; ++l) x = fmaf(num[l][nb][i], f[l], x);
       o[i] = x;
     }
-    if (row < N)
-      *reinterpret_cast<Q*>(oh + (size_t)row * D + 16 * nb + 4 * g) = f32_to_quad<T>(o);
+    buf_st(rs, (r * D + 16 * nb + 4 * g) * (int)sizeof(T), f32_to_quad<T>(o));
   }
 }
 
@@ -468,10 +503,11 @@ template <typename T, int D>
 __device__ __forceinline__ void load_q(const T* __restrict__ qh, int row, int N,
                                        typename QuadOf<T>::type* qq) {
   using Q = typename QuadOf<T>::type;
-  const int g = (threadIdx.x & 63) >> 4;
+  const int lane = threadIdx.x & 63, g = lane >> 4, r = lane & 15;
+  const Rsrc rs = rows_rsrc<T, D>(qh, strip_row0(row), 16, N);
 #pragma unroll
   for (int cb = 0; cb < D / 16; ++cb)
-    qq[cb] = row < N ? *reinterpret_cast<const Q*>(qh + (size_t)row * D + 16 * cb + 4 * g) : Q{};
+    qq[cb] = buf_ld(rs, (r * D + 16 * cb + 4 * g) * (int)sizeof(T), (Q*)0);
 }
 
 // ------------------------------------------------------------------ causal pieces
@@ -959,14 +995,11 @@ __global__ __launch_bounds__(NT) void k_band_ring(const T* __restrict__ q,
 
   load_state_frags<T, D, R, NT>(fin + (size_t)bh * R * D * (D + 1), sm.sf, sm.sz);
   ring_fill<T, D, R>(sm, kh, vh, map.ua0, U, map, N);
-  Q qq[NB], qn[NB];
+  Q qq[NB];
   load_q<T, D>(qh, s0 + 16 * w + r, N, qq);
   RowCopy<T, D, NT, 64> pk, pv;
-  if (ntile > 1) {
-    pk.load(kh, (map.ua0 + U) * 32, 64, N);
-    pv.load(vh, (map.ua0 + U) * 32, 64, N);
-    load_q<T, D>(qh, s0 + TM + 16 * w + r, N, qn);
-  }
+  pk.load(kh, (map.ua0 + U) * 32, ntile > 1 ? 64 : 0, N);
+  pv.load(vh, (map.ua0 + U) * 32, ntile > 1 ? 64 : 0, N);
   for (int t = 0; t < ntile; ++t) {
     __syncthreads();  // ring holds the window of tile t
     const int t0 = s0 + t * TM, i0 = t0 + 16 * w, row = i0 + r;
@@ -981,24 +1014,25 @@ __global__ __launch_bounds__(NT) void k_band_ring(const T* __restrict__ q,
                                  scale2);
     Q pq[R][NB];
     phi_q<T, D, R>(qq, pq);
+    // the query quads are dead: load the next tile's rows into them (a copy
+    // from separate prefetch registers would make the loop wait for every
+    // outstanding load at its head)
+    load_q<T, D>(qh, t0 + TM + 16 * w + r, t + 1 < ntile ? N : 0, qq);
     f32x4 num[R][NB + 1];
     far_terms<T, D, R, false>(sm.sf, sm.sz, pq, num);
     blend_store<T, D, R>(out + base, row, N, sn, sfw, st, num);
-    if (t + 1 < ntile) {
-      __syncthreads();  // every wave is done with the window of tile t
-      const int ua_new = map.ua0 + 2 * t + U;  // the two units tile t+1 adds
-      const int ra = map(ua_new), rb = map(ua_new + 1);
-      auto rowmap = [=](int i) { return (i < 32 ? ra : rb) + (i & 31); };
-      pk.store(sm.k, ST, 64, rowmap);
-      pv.store(sm.v, ST, 64, rowmap);
-#pragma unroll
-      for (int cb = 0; cb < NB; ++cb) qq[cb] = qn[cb];
-      if (t + 2 < ntile) {
-        pk.load(kh, (ua_new + 2) * 32, 64, N);
-        pv.load(vh, (ua_new + 2) * 32, 64, N);
-        load_q<T, D>(qh, t0 + 2 * TM + 16 * w + r, N, qn);
-      }
-    }
+    // slide the ring (after the last tile this stores zeros nobody reads;
+    // prefetches past the walk are empty row ranges, so there is no branch
+    // around any global load)
+    __syncthreads();  // every wave is done with the window of tile t
+    const int ua_new = map.ua0 + 2 * t + U;  // the two units tile t+1 adds
+    const int ra = map(ua_new), rb = map(ua_new + 1);
+    auto rowmap = [=](int i) { return (i < 32 ? ra : rb) + (i & 31); };
+    pk.store(sm.k, ST, 64, rowmap);
+    pv.store(sm.v, ST, 64, rowmap);
+    const bool pf = t + 2 < ntile;
+    pk.load(kh, (ua_new + 2) * 32, pf ? 64 : 0, N);
+    pv.load(vh, (ua_new + 2) * 32, pf ? 64 : 0, N);
   }
 }
 
@@ -1042,14 +1076,11 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
   if (has_ag) tiles.load(w, prefix + ((size_t)bh * nseg + seg) * R * D * (D + 1));
   ring_fill<T, D, R>(sm, kh, vh, map.ua0, U, map, N);
   if (has_ag) tiles.to_frags(w, sm.sf, sm.sz);
-  Q qq[NB], qn[NB];
+  Q qq[NB];
   load_q<T, D>(qh, s0 + 16 * w + r, N, qq);
   RowCopy<T, D, NT, 64> pk, pv;
-  if (ntile > 1) {
-    pk.load(kh, (map.ua0 + U) * 32, 64, N);
-    pv.load(vh, (map.ua0 + U) * 32, 64, N);
-    load_q<T, D>(qh, s0 + TM + 16 * w + r, N, qn);
-  }
+  pk.load(kh, (map.ua0 + U) * 32, ntile > 1 ? 64 : 0, N);
+  pv.load(vh, (map.ua0 + U) * 32, ntile > 1 ? 64 : 0, N);
   __syncthreads();  // ring filled
   stage_phi_tile<T, D, R>(sm.k, map(s0 >> 5), map((s0 >> 5) + 1), ST, s0, N, sm.pk);
   for (int t = 0; t < ntile; ++t) {
@@ -1069,6 +1100,8 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
     near_out<D>(st, sn, fo);
     Q pq[R][NB];
     phi_q<T, D, R>(qq, pq);
+    // the query quads are dead: load the next tile's rows into them
+    load_q<T, D>(qh, t0 + TM + 16 * w + r, t + 1 < ntile ? N : 0, qq);
 #pragma unroll
     for (int l = 0; l < R; ++l) {
       f32x4 num[NB + 1];
@@ -1079,36 +1112,32 @@ __global__ __launch_bounds__(NT) void k_causal_ring(const T* __restrict__ q,
       add_far_map<D>(num, sfw, fo);
     }
     store_row<T, D>(out + base, row, N, fo);
-    if (t + 1 < ntile) {
-      // everything tile t+1 needs in LDS is prepared in registers first, so
-      // that only plain stores sit between the two barriers (the scheduling
-      // fence keeps this work from being hoisted into the compute above,
-      // where it would raise register pressure)
-      __builtin_amdgcn_sched_barrier(0);
-      if (has_ag) {
-        tiles.add_unit(w, sm.pk, 0, sm.v + rt0 * ST, ST);
-        tiles.add_unit(w, sm.pk, 32, sm.v + rt1 * ST, ST);
-      }
-      typename Tiles::Frags fr;
-      if (has_ag) fr = tiles.pack();
-      PhiRows<T, D, R> ph;
-      ph.compute(pk, t0 + TM, N);  // the prefetched rows are the keys of tile t+1
-      __syncthreads();  // every wave is done with tile t's LDS
-      const int ua_new = map.ua0 + 2 * t + U;
-      const int ra = map(ua_new), rb = map(ua_new + 1);
-      auto rowmap = [=](int i) { return (i < 32 ? ra : rb) + (i & 31); };
-      pk.store(sm.k, ST, 64, rowmap);
-      pv.store(sm.v, ST, 64, rowmap);
-      ph.store(sm.pk, ST);
-      if (has_ag) Tiles::store_frags(w, fr, sm.sf, sm.sz);
-#pragma unroll
-      for (int cb = 0; cb < NB; ++cb) qq[cb] = qn[cb];
-      if (t + 2 < ntile) {
-        pk.load(kh, (ua_new + 2) * 32, 64, N);
-        pv.load(vh, (ua_new + 2) * 32, 64, N);
-        load_q<T, D>(qh, t0 + 2 * TM + 16 * w + r, N, qn);
-      }
+    // everything tile t+1 needs in LDS is prepared in registers first, so
+    // that only plain stores sit between the two barriers (the scheduling
+    // fence keeps this work from being hoisted into the compute above, where
+    // it would raise register pressure).  After the last tile this advances
+    // a state nobody reads; prefetches past the walk are empty row ranges, so
+    // there is no branch around any global load.
+    __builtin_amdgcn_sched_barrier(0);
+    if (has_ag) {
+      tiles.add_unit(w, sm.pk, 0, sm.v + rt0 * ST, ST);
+      tiles.add_unit(w, sm.pk, 32, sm.v + rt1 * ST, ST);
     }
+    typename Tiles::Frags fr;
+    if (has_ag) fr = tiles.pack();
+    PhiRows<T, D, R> ph;
+    ph.compute(pk, t0 + TM, N);  // the prefetched rows are the keys of tile t+1
+    __syncthreads();  // every wave is done with tile t's LDS
+    const int ua_new = map.ua0 + 2 * t + U;
+    const int ra = map(ua_new), rb = map(ua_new + 1);
+    auto rowmap = [=](int i) { return (i < 32 ? ra : rb) + (i & 31); };
+    pk.store(sm.k, ST, 64, rowmap);
+    pv.store(sm.v, ST, 64, rowmap);
+    ph.store(sm.pk, ST);
+    if (has_ag) Tiles::store_frags(w, fr, sm.sf, sm.sz);
+    const bool pf = t + 2 < ntile;
+    pk.load(kh, (ua_new + 2) * 32, pf ? 64 : 0, N);
+    pv.load(vh, (ua_new + 2) * 32, pf ? 64 : 0, N);
   }
 }
 
@@ -1310,7 +1339,7 @@ static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
              dim3(NT), lds, s, q, k, v, o, (const float*)part, a.w_near, a.w_far, a.H, a.N,
              a.band_k, a.L, a.nseg, scale2);
   } else {
-    if (band_pair_applies(a.dtype, a.d, a.band_k, a.causal)) {
+    if (band_pair_applies(a.dtype, a.d, a.band_k, a.causal, a.N)) {
       return launch_band_pair(a, timer, fin);
     } else if (ring) {
       launch_timed(timer, FMM_KERNEL_BAND_APPLY, k_band_ring<T, D, R>, dim3(BH * a.nseg_apply),

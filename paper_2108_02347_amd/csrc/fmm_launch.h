@@ -54,7 +54,7 @@ int tile_rows();
 // Non-causal apply with two 16-row strips per wavefront (fmm_pair.hip): bf16,
 // d = 32 or 64, band half-width <= 64.  Its row segments are multiples of
 // pair_tile_rows().
-bool band_pair_applies(int dtype, int d, int band_k, int causal);
+bool band_pair_applies(int dtype, int d, int band_k, int causal, long long n);
 int pair_tile_rows();
 hipError_t launch_band_pair(const LaunchArgs& a, LaunchTimer* timer, const float* fin);
 

@@ -19,6 +19,8 @@
 // ring row r is stored at chunk c ^ swz(r), which keeps the 16-byte K reads,
 // the transposed 8-byte V reads and the 16-byte row stores free of bank
 // conflicts.  d = 32 rows are padded to 80 bytes instead.
+#include <type_traits>
+
 #include "fmm_device.h"
 #include "fmm_launch.h"
 
@@ -51,6 +53,20 @@ __device__ __forceinline__ void oct_unpack(const Oct& o, float* f) {
   }
 }
 
+// Buffer resource over one head's [N, D] bf16 rows.  Raw buffer loads past
+// its end (or at a negative offset, i.e. a huge unsigned one) return zeros
+// without touching memory and stores there are dropped, so every global access
+// of the walk is branch-free: rows outside [0, N) and skipped prefetches just
+// use out-of-range offsets.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr uint32_t OOB = 0x80000000u;
+__device__ __forceinline__ Rsrc head_rsrc(const bf16_t* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(p), 0, bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 buf_load16(Rsrc rs, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+}
+
 // Byte offset of 16-byte chunk c of ring row r.
 template <int D> struct PairRows;
 template <> struct PairRows<64> {
@@ -79,21 +95,20 @@ struct PairCfg {
   static constexpr int LDS = 2 * RING + FRAG;
 };
 
-// K or V rows [k0, k0 + 128) of a head in registers (zero outside [0, N));
-// thread t holds chunk t % CPR of row t / CPR + (PNT / CPR) * it.
+// K or V rows [k0, k0 + 128) of a head in registers (zero outside [0, N), or
+// everywhere when !on); thread t holds chunk t % CPR of row
+// t / CPR + (PNT / CPR) * it.
 template <int D>
 struct PairCopy {
   static constexpr int CPR = D / 8;
   static constexpr int IT = PTM * CPR / PNT;
   uint4 r[IT];
-  __device__ __forceinline__ void load(const bf16_t* __restrict__ src, int k0, int N) {
+  __device__ __forceinline__ void load(Rsrc rs, int k0, bool on) {
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int x = threadIdx.x + it * PNT;
-      const int key = k0 + x / CPR;
-      r[it] = make_uint4(0, 0, 0, 0);
-      if (key >= 0 && key < N)
-        r[it] = *reinterpret_cast<const uint4*>(src + (size_t)key * D + (x % CPR) * 8);
+      const int e = (k0 + x / CPR) * D + (x % CPR) * 8;
+      r[it] = buf_load16(rs, on ? (uint32_t)(2 * e) : OOB);
     }
   }
   // Unit j (0..3) of the copied rows goes to ring slot slot_of(j) (skipped if < 0).
@@ -110,31 +125,44 @@ struct PairCopy {
   }
 };
 
-// V^T quad of the 16-key block starting at ring row r0, columns 16nb .. 16nb+15:
-// lane (j, g) receives V[r0 + 4g + e][16nb + j], e = 0..3 (see ld_tquad).
+// Per-lane byte offsets of the ring reads within a 16-row block (ring units
+// start at multiples of 32 rows, so the swizzle of a row depends only on its
+// index within the block).  koff[p]: the lane's K oct, row r, chunk 4p + g.
+// voff[nb]: the lane's V^T transposed read for columns 16nb .. 16nb+15: lane
+// t of group g reads row 4g + t/4, columns 16nb + 4(t%4) .. +3, and the
+// hardware hands lane (j, g) the values V[4g + e][16nb + j], e = 0..3.
 template <int D>
-__device__ __forceinline__ uint2 vt_quad(const unsigned char* vr, int r0, int nb) {
-  const int lane = threadIdx.x & 63, g = lane >> 4, t = lane & 15;
-  const int row = r0 + 4 * g + (t >> 2);
-  const unsigned char* p = vr + PairRows<D>::off(row, 2 * nb + ((t & 3) >> 1)) + 8 * (t & 1);
+struct RingOffsets {
+  int koff[D / 32];
+  int voff[D / 16];
+  __device__ __forceinline__ RingOffsets() {
+    const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4, t = lane & 15;
+#pragma unroll
+    for (int p = 0; p < D / 32; ++p) koff[p] = PairRows<D>::off(r, 4 * p + g);
+#pragma unroll
+    for (int nb = 0; nb < D / 16; ++nb)
+      voff[nb] = PairRows<D>::off(4 * g + (t >> 2), 2 * nb + ((t & 3) >> 1)) + 8 * (t & 1);
+  }
+};
+
+__device__ __forceinline__ uint2 ld_tr16(const unsigned char* p) {
   typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
   const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
   return __builtin_bit_cast(uint2, v);
 }
 
-// Query octs of the lane's row of each strip: qo[s][p] = q[i0 + 16s + r][32p + 8g .. +7].
+// Query octs of the lane's row of each strip: qo[s][p] = q[i0 + 16s + r][32p + 8g .. +7]
+// (zero for rows at or beyond N, or everywhere when !on).
 template <int D>
-__device__ __forceinline__ void load_qo(const bf16_t* __restrict__ qh, int i0, int N,
-                                        Oct (*qo)[D / 32]) {
+__device__ __forceinline__ void load_qo(Rsrc rs, int i0, bool on, Oct (*qo)[D / 32]) {
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int row = i0 + 16 * s + r;
+  for (int s = 0; s < 2; ++s)
 #pragma unroll
-    for (int p = 0; p < D / 32; ++p)
-      qo[s][p] = row < N ? *reinterpret_cast<const Oct*>(qh + (size_t)row * D + 32 * p + 8 * g)
-                         : make_uint4(0, 0, 0, 0);
-  }
+    for (int p = 0; p < D / 32; ++p) {
+      const int e = (i0 + 16 * s + r) * D + 32 * p + 8 * g;
+      qo[s][p] = buf_load16(rs, on ? (uint32_t)(2 * e) : OOB);
+    }
 }
 
 // State fragments from the non-causal tile-order record (see k_seg_state):
@@ -168,130 +196,133 @@ __device__ __forceinline__ void pair_frags(const float* __restrict__ rec, Oct* s
     }
 }
 
-// Banded softmax of both strips of the wavefront whose rows start at i0 (a
-// multiple of 32).  Key units u = 0 .. NU-1 (absolute unit i0/32 - KC + u)
-// sit in ring slots (slot0 + u) % U.  Strip A never needs the last 16-key
-// block of the span and strip B never the first.  EXACT: k = 32*KC and the
-// span lies inside [0, N), so only the first and last block of each strip
-// cut the band (triangles); otherwise every block is masked against the
-// row's band clipped to [0, N).  On return o[s][nb] holds the unnormalised
-// P V of strip s and o[s][NB] its row sums.
-template <int D, int R, int KC, bool EXACT>
-__device__ __forceinline__ void pair_near(f32x4 (*o)[D / 16 + 1], Oct (*qo)[D / 32],
+// One 128-row tile of a wavefront: both strips' banded softmax (Eq. (3)),
+// far part (Eq. (8)-(9)), blend (Eq. (11)) and store.  The rows start at i0
+// (a multiple of 32); key units u = 0 .. NU-1 (absolute unit i0/32 - KC + u)
+// sit in ring slots (slot0 + u) % U.  Strip A (s = 0) never needs the last
+// 16-key block of the span and strip B (s = 1) never the first, so strip s
+// scores blocks s .. s + NBK - 2.  Exact tiles (!GENERAL: k = 32*KC and every
+// wavefront's span inside [0, N)) have only the first and last block of each
+// strip cut by the band (triangles); GENERAL tiles mask every block against
+// the row's band clipped to [0, N).
+//
+// The work runs as phases that pair matrix-core products of one strip with
+// vector arithmetic of the other (scheduling fences keep the phases apart):
+//   scores A | scores B + softmax A | P V of A + softmax B |
+//   P V of B + phi(q) | far products + near normalisation | blend, store
+// mid() runs between the near and far phases, once phi(q) is formed.
+template <int D, int R, int KC, bool GENERAL, class Mid>
+__device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
+                                          float scale2, float sn, float sfw, Oct (*qo)[D / 32],
                                           const unsigned char* kr, const unsigned char* vr,
-                                          int slot0, int i0, int N, int band_k, float scale2) {
+                                          int slot0, const RingOffsets<D>& ro, const Oct* sf,
+                                          Oct (*zo)[D / 32], Mid mid) {
   using C = PairCfg<D, R, KC>;
-  constexpr int NB = C::NB, NQ = C::NQ, NU = C::NU, NBK = 2 * NU;
+  constexpr int NB = C::NB, NQ = C::NQ, NU = C::NU, NBK = 2 * NU, NS = NBK - 1;
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
-  int urow[NU];
+  // byte offset of each key unit's first ring row (wave-uniform)
+  int ubase[NU];
 #pragma unroll
-  for (int u = 0; u < NU; ++u) urow[u] = ((slot0 + u) % C::U) * 32;
+  for (int u = 0; u < NU; ++u)
+    ubase[u] = __builtin_amdgcn_readfirstlane(((slot0 + u) % C::U) * 32 * PairRows<D>::RB);
+  const Oct ones = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
 
-  // scores S^T = K Q^T of every (strip, block) the strip needs
-  f32x4 sc[2][NBK];
+  // Exact tiles: the band cuts the first block of each strip below the
+  // diagonal offset (key offset 4g + i < r) and the last block above it; the
+  // score products start from these -inf / 0 biases, so no mask is applied.
+  f32x4 bias_lo, bias_hi;
 #pragma unroll
-  for (int b = 0; b < NBK; ++b) {
-    Oct ko[NQ];
-#pragma unroll
-    for (int p = 0; p < NQ; ++p)
-      ko[p] = *reinterpret_cast<const Oct*>(
-          kr + PairRows<D>::off(urow[b >> 1] + 16 * (b & 1) + r, 4 * p + g));
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      if ((s == 0 && b == NBK - 1) || (s == 1 && b == 0)) continue;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int p = 0; p < NQ; ++p) acc = mma8(ko[p], qo[s][p], acc);
-      sc[s][b] = acc;
-    }
+  for (int i = 0; i < 4; ++i) {
+    bias_lo[i] = (!GENERAL && 4 * g + i < r) ? -INFINITY : 0.f;
+    bias_hi[i] = (!GENERAL && 4 * g + i > r) ? -INFINITY : 0.f;
   }
-
-  // band masks
-  if constexpr (EXACT) {
-    // lower edge (first block of the strip): key offset 4g + i >= r;
-    // upper edge (last block): 4g + i <= r
+  // S^T = K Q^T for blocks s .. s + NS - 1 of strip s
+  auto scores = [&](int s, f32x4* sc) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const bool lo_ok = 4 * g + i >= r, hi_ok = 4 * g + i <= r;
-      if (!lo_ok) { sc[0][0][i] = -INFINITY; sc[1][1][i] = -INFINITY; }
-      if (!hi_ok) { sc[0][NBK - 2][i] = -INFINITY; sc[1][NBK - 1][i] = -INFINITY; }
+    for (int j = 0; j < NS; ++j) {
+      const int b = j + s;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (!GENERAL) acc = j == 0 ? bias_lo : j == NS - 1 ? bias_hi : acc;
+#pragma unroll
+      for (int p = 0; p < NQ; ++p) {
+        const Oct ko = *reinterpret_cast<const Oct*>(kr + ubase[b >> 1] + ro.koff[p] +
+                                                     16 * PairRows<D>::RB * (b & 1));
+        acc = mma8(ko, qo[s][p], acc);
+      }
+      sc[j] = acc;
     }
-  } else {
-    const int kbase = (i0 / 32 - KC) * 32 + 4 * g;  // key of (block 0, element 0) of this lane
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
+  };
+  // band mask of the general tiles
+  auto mask = [&](int s, f32x4* sc) {
+    if constexpr (GENERAL) {
+      const int kbase = (i0 / 32 - KC) * 32 + 4 * g;
       const int row = i0 + 16 * s + r;
       int lo = max(row - band_k, 0) - kbase;
       int span = min(row + band_k, N - 1) - kbase - lo;
       if (span < 0) { lo = 0x40000000; span = 0; }
 #pragma unroll
-      for (int b = 0; b < NBK; ++b) {
-        if ((s == 0 && b == NBK - 1) || (s == 1 && b == 0)) continue;
+      for (int j = 0; j < NS; ++j)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if ((unsigned)(16 * b + i - lo) > (unsigned)span) sc[s][b][i] = -INFINITY;
-      }
+          if ((unsigned)(16 * (j + s) + i - lo) > (unsigned)span) sc[j][i] = -INFINITY;
     }
-  }
-
-  // per-strip row maximum, exponentials, P quads paired per key unit
-  Oct pq[2][NU];
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
+  };
+  // row maximum, exponentials; P quads paired per key unit
+  auto softmax = [&](int s, f32x4* sc, Oct* pq) {
     float mloc = -INFINITY;
 #pragma unroll
-    for (int b = 0; b < NBK; ++b) {
-      if ((s == 0 && b == NBK - 1) || (s == 1 && b == 0)) continue;
+    for (int j = 0; j < NS; ++j)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) mloc = fmaxf(mloc, sc[s][b][i]);
-    }
+      for (int i = 0; i < 4; ++i) mloc = fmaxf(mloc, sc[j][i]);
     const float m = col_max(mloc);
     const float ms = (m == -INFINITY ? 0.f : m) * scale2;
     uint2 qd[NBK];
+    qd[s == 0 ? NBK - 1 : 0] = make_uint2(0, 0);
 #pragma unroll
-    for (int b = 0; b < NBK; ++b) {
-      if ((s == 0 && b == NBK - 1) || (s == 1 && b == 0)) {
-        qd[b] = make_uint2(0, 0);
-        continue;
-      }
+    for (int j = 0; j < NS; ++j) {
       float pv[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pv[i] = __builtin_amdgcn_exp2f(fmaf(sc[s][b][i], scale2, -ms));
-      qd[b] = make_uint2(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]));
+      for (int i = 0; i < 4; ++i) pv[i] = __builtin_amdgcn_exp2f(fmaf(sc[j][i], scale2, -ms));
+      qd[j + s] = make_uint2(pack_bf16x2(pv[0], pv[1]), pack_bf16x2(pv[2], pv[3]));
     }
 #pragma unroll
-    for (int u = 0; u < NU; ++u) pq[s][u] = oct_of(qd[2 * u], qd[2 * u + 1]);
-  }
-
-  // O^T = V^T P^T and the row sums (ones block), V^T shared by both strips
-  const Oct ones = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
+    for (int u = 0; u < NU; ++u) pq[u] = oct_of(qd[2 * u], qd[2 * u + 1]);
+  };
+  // O^T = V^T P^T and the row sums (ones block)
+  auto pv = [&](const Oct* pq, f32x4* o) {
 #pragma unroll
-  for (int s = 0; s < 2; ++s)
+    for (int nb = 0; nb <= NB; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int nb = 0; nb <= NB; ++nb) o[s][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int u = 0; u < NU; ++u) {
 #pragma unroll
-  for (int u = 0; u < NU; ++u) {
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const Oct vt = oct_of(vt_quad<D>(vr, urow[u], nb), vt_quad<D>(vr, urow[u] + 16, nb));
-      o[0][nb] = mma8(vt, pq[0][u], o[0][nb]);
-      o[1][nb] = mma8(vt, pq[1][u], o[1][nb]);
+      for (int nb = 0; nb < NB; ++nb) {
+        const unsigned char* vp = vr + ubase[u] + ro.voff[nb];
+        const Oct vt = oct_of(ld_tr16(vp), ld_tr16(vp + 16 * PairRows<D>::RB));
+        o[nb] = mma8(vt, pq[u], o[nb]);
+      }
+      o[NB] = mma8(ones, pq[u], o[NB]);
     }
-    o[0][NB] = mma8(ones, pq[0][u], o[0][NB]);
-    o[1][NB] = mma8(ones, pq[1][u], o[1][NB]);
-  }
-}
+  };
 
-// Far part and blend of both strips, then the store (Eq. (8)-(9), Eq. (11)).
-template <int D, int R>
-__device__ __forceinline__ void pair_far_store(bf16_t* __restrict__ oh, int i0, int N, float sn,
-                                               float sfw, f32x4 (*o)[D / 16 + 1],
-                                               Oct (*qo)[D / 32], const Oct* sf,
-                                               Oct (*zo)[D / 32]) {
-  constexpr int NB = D / 16, NQ = D / 32;
-  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
-  // phi_1, phi_2 of the query octs (one exp(-|x|) serves both maps)
+  f32x4 scA[NS], scB[NS];
+  Oct pqA[NU], pqB[NU];
+  f32x4 oA[NB + 1], oB[NB + 1];
   Oct ph[R][2][NQ];
+
+  scores(0, scA);
+  __builtin_amdgcn_sched_barrier(0);
+  mask(0, scA);
+  __builtin_amdgcn_sched_barrier(0);
+  scores(1, scB);
+  softmax(0, scA, pqA);
+  __builtin_amdgcn_sched_barrier(0);
+  mask(1, scB);
+  __builtin_amdgcn_sched_barrier(0);
+  pv(pqA, oA);
+  softmax(1, scB, pqB);
+  __builtin_amdgcn_sched_barrier(0);
+  pv(pqB, oB);
+  // phi_1, phi_2 of the query octs (one exp(-|x|) serves both maps)
 #pragma unroll
   for (int s = 0; s < 2; ++s)
 #pragma unroll
@@ -303,57 +334,64 @@ __device__ __forceinline__ void pair_far_store(bf16_t* __restrict__ oh, int i0, 
       ph[0][s][p] = oct_pack(p1);
       if constexpr (R == 2) ph[1][s][p] = oct_pack(p2);
     }
+  __builtin_amdgcn_sched_barrier(0);
+  // the query octs are dead: the caller's step between the phases (it
+  // reloads them with the next tile's rows)
+  mid();
+
+  // far products, with the near normalisation in their shadow
   f32x4 fo[2][NB];
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const float a = sn > 0.f ? sn * fast_rcp(o[s][NB][0]) : 0.f;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) fo[s][nb] = o[s][nb] * a;
-  }
-#pragma unroll
-  for (int l = 0; l < R; ++l) {
-    f32x4 num[2][NB + 1];
+  {
+    const float a0 = sn > 0.f ? sn * fast_rcp(oA[NB][0]) : 0.f;
+    const float a1 = sn > 0.f ? sn * fast_rcp(oB[NB][0]) : 0.f;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
+      fo[0][nb] = oA[nb] * a0;
+      fo[1][nb] = oB[nb] * a1;
+    }
+  }
+  // one strip and one map at a time (each map normalised on its own); the
+  // fragments are read again for each, which keeps them out of registers
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int l = 0; l < R; ++l) {
+      asm volatile("" ::: "memory");
+      f32x4 num[NB + 1];
+#pragma unroll
+      for (int nb = 0; nb <= NB; ++nb) num[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int p = 0; p < NQ; ++p) {
-        const Oct f = sf[((l * NB + nb) * NQ + p) * 64 + lane];
-        a0 = mma8(f, ph[l][0][p], a0);
-        a1 = mma8(f, ph[l][1][p], a1);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+          num[nb] = mma8(sf[((l * NB + nb) * NQ + p) * 64 + lane], ph[l][s][p], num[nb]);
+        num[NB] = mma8(zo[l][p], ph[l][s][p], num[NB]);
       }
-      num[0][nb] = a0;
-      num[1][nb] = a1;
+      const float f = sfw > 0.f ? sfw * fast_rcp(num[NB][0]) : 0.f;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) fo[s][nb] += num[nb] * f;
     }
+  // rows at or beyond N fall outside the output buffer and are dropped
+  typedef int i32x2 __attribute__((ext_vector_type(2)));
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      f32x4 den = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < 2; ++s)
 #pragma unroll
-      for (int p = 0; p < NQ; ++p) den = mma8(zo[l][p], ph[l][s][p], den);
-      const float f = sfw > 0.f ? sfw * fast_rcp(den[0]) : 0.f;
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) fo[s][nb] += num[s][nb] * f;
+    for (int nb = 0; nb < NB; ++nb) {
+      const i32x2 v = {(int)pack_bf16x2(fo[s][nb][0], fo[s][nb][1]),
+                       (int)pack_bf16x2(fo[s][nb][2], fo[s][nb][3])};
+      __builtin_amdgcn_raw_buffer_store_b64(v, oh, 2 * ((i0 + 16 * s + r) * D + 16 * nb + 4 * g),
+                                            0, 0);
     }
-  }
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int row = i0 + 16 * s + r;
-    if (row >= N) continue;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-      *reinterpret_cast<uint2*>(oh + (size_t)row * D + 16 * nb + 4 * g) =
-          make_uint2(pack_bf16x2(fo[s][nb][0], fo[s][nb][1]),
-                     pack_bf16x2(fo[s][nb][2], fo[s][nb][3]));
-  }
 }
 
 // grid.x = BH * nseg (XCD-aware remap); the workgroup walks the 128-row tiles
 // of rows [s*L, min(N, s*L + L)), L a multiple of 128.  The window of the
 // tile at t0 is the U units [t0/32 - KC, t0/32 + 4 + KC); unit ua0 + m lives
 // in ring slot m % U, and the ring slides by four units per tile, the next
-// four units and the next query rows prefetched into registers.
+// four units and the next tile's query rows prefetched into registers a tile
+// ahead.
 template <int D, int R, int KC>
-__global__ __launch_bounds__(PNT) void k_band_pair(const bf16_t* __restrict__ q,
+__global__ __launch_bounds__(PNT, 2) void k_band_pair(const bf16_t* __restrict__ q,
                                                    const bf16_t* __restrict__ k,
                                                    const bf16_t* __restrict__ v,
                                                    bf16_t* __restrict__ out,
@@ -371,9 +409,9 @@ __global__ __launch_bounds__(PNT) void k_band_pair(const bf16_t* __restrict__ q,
   const int bh = lin / nseg, seg = lin % nseg, h = bh % H;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const size_t base = (size_t)bh * N * D;
-  const bf16_t* qh = q + base;
-  const bf16_t* kh = k + base;
-  const bf16_t* vh = v + base;
+  const int hbytes = N * D * 2;
+  const Rsrc qh = head_rsrc(q + base, hbytes), kh = head_rsrc(k + base, hbytes),
+             vh = head_rsrc(v + base, hbytes), oh = head_rsrc(out + base, hbytes);
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const int s0 = seg * L, s1 = min(N, s0 + L);
   const int ntile = (s1 - s0 + PTM - 1) / PTM;
@@ -384,46 +422,51 @@ __global__ __launch_bounds__(PNT) void k_band_pair(const bf16_t* __restrict__ q,
 #pragma unroll
   for (int x = 0; x < U; x += 4) {
     PairCopy<D> ck, cv;
-    ck.load(kh, (ua0 + x) * 32, N);
-    cv.load(vh, (ua0 + x) * 32, N);
+    ck.load(kh, (ua0 + x) * 32, true);
+    cv.load(vh, (ua0 + x) * 32, true);
     auto slot = [=](int j) { return x + j < U ? x + j : -1; };
     ck.store(kr, slot);
     cv.store(vr, slot);
   }
+  const RingOffsets<D> ro;
   Oct qo[2][NQ], qn[2][NQ];
-  load_qo<D>(qh, s0 + 32 * w, N, qo);
+  load_qo<D>(qh, s0 + 32 * w, true, qo);
   PairCopy<D> pk, pv;
-  if (ntile > 1) {
-    pk.load(kh, (ua0 + U) * 32, N);
-    pv.load(vh, (ua0 + U) * 32, N);
-    load_qo<D>(qh, s0 + PTM + 32 * w, N, qn);
-  }
-  for (int t = 0; t < ntile; ++t) {
+  pk.load(kh, (ua0 + U) * 32, ntile > 1);
+  pv.load(vh, (ua0 + U) * 32, ntile > 1);
+  load_qo<D>(qh, s0 + PTM + 32 * w, ntile > 1, qn);
+  // one tile, then the ring slides by the four prefetched units (past the
+  // last tile the loads and stores are harmless no-ops on zeros)
+  auto step = [&](int t, auto general) {
     __syncthreads();  // the ring holds the window of tile t
     const int i0 = s0 + t * PTM + 32 * w;
     const int slot0 = (4 * t + w) % U;
-    f32x4 o[2][NB + 1];
-    if (band_k == 32 * KC && i0 - band_k >= 0 && i0 + 31 + band_k < N)
-      pair_near<D, R, KC, true>(o, qo, kr, vr, slot0, i0, N, band_k, scale2);
-    else
-      pair_near<D, R, KC, false>(o, qo, kr, vr, slot0, i0, N, band_k, scale2);
-    pair_far_store<D, R>(out + base, i0, N, sn, sfw, o, qo, sf, zo);
-    if (t + 1 < ntile) {
-      __syncthreads();  // every wave is done with the window of tile t
-      auto slot = [=](int j) { return (4 * t + j) % U; };
-      pk.store(kr, slot);
-      pv.store(vr, slot);
+    auto mid = [&]() {};
+    pair_tile<D, R, KC, decltype(general)::value>(oh, i0, N, band_k, scale2, sn, sfw, qo, kr, vr,
+                                                  slot0, ro, sf, zo, mid);
+    __syncthreads();  // every wave is done with the window of tile t
+    auto slot = [=](int j) { return (4 * t + j) % U; };
+    pk.store(kr, slot);
+    pv.store(vr, slot);
 #pragma unroll
-      for (int s = 0; s < 2; ++s)
+    for (int s = 0; s < 2; ++s)
 #pragma unroll
-        for (int p = 0; p < NQ; ++p) qo[s][p] = qn[s][p];
-      if (t + 2 < ntile) {
-        pk.load(kh, (ua0 + U + 4 * (t + 1)) * 32, N);
-        pv.load(vh, (ua0 + U + 4 * (t + 1)) * 32, N);
-        load_qo<D>(qh, s0 + (t + 2) * PTM + 32 * w, N, qn);
-      }
-    }
-  }
+      for (int p = 0; p < NQ; ++p) qo[s][p] = qn[s][p];
+    pk.load(kh, (ua0 + U + 4 * (t + 1)) * 32, t + 2 < ntile);
+    pv.load(vh, (ua0 + U + 4 * (t + 1)) * 32, t + 2 < ntile);
+    load_qo<D>(qh, i0 + 2 * PTM, t + 2 < ntile, qn);
+  };
+  // exact tiles: k = 32*KC and every row's band inside [0, N); they form one
+  // contiguous run of the walk, between the leading and trailing general tiles
+  const bool fit = band_k == 32 * KC;
+  auto interior = [&](int t) {
+    const int t0 = s0 + t * PTM;
+    return fit && t0 - band_k >= 0 && t0 + PTM - 1 + band_k < N;
+  };
+  int t = 0;
+  for (; t < ntile && !interior(t); ++t) step(t, std::true_type{});
+  for (; t < ntile && interior(t); ++t) step(t, std::false_type{});
+  for (; t < ntile; ++t) step(t, std::true_type{});
 }
 
 template <int D, int R, int KC>
@@ -453,8 +496,10 @@ hipError_t launch_pair_d(const LaunchArgs& a, LaunchTimer* t, const float* fin, 
 
 }  // namespace
 
-bool band_pair_applies(int dtype, int d, int band_k, int causal) {
-  return dtype == FMM_DTYPE_BF16 && (d == 32 || d == 64) && band_k <= 64 && !causal;
+bool band_pair_applies(int dtype, int d, int band_k, int causal, long long n) {
+  // 32-bit buffer offsets: one head's rows must stay below 2 GiB
+  return dtype == FMM_DTYPE_BF16 && (d == 32 || d == 64) && band_k <= 64 && !causal &&
+         n * d * 2 < (1LL << 31);
 }
 
 int pair_tile_rows() { return PTM; }
