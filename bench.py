@@ -56,15 +56,37 @@ def parse():
 # library kernel id -> gfx950 kernel of the stress64k workload (bf16, d=64, rank 2)
 STRESS_KERNELS = {
     "seg_state": "k_seg_state<unsigned short, 64, 2>",
-    "band_apply": "k_band_ring<unsigned short, 64, 2>",
+    "band_apply": "k_band_pair<64, 2, 2>",
     "causal_apply": "k_causal_ring<unsigned short, 64, 2>",
 }
 
 
+def _short_kernel_name(name):
+    import re
+    name = name.replace("(anonymous namespace)::", "").replace("void ", "")
+    name = re.sub(r"\(.*", "", name)
+    return name if len(name) <= 70 else name[:67] + "..."
+
+
 def trace_summary(stats_csv):
     import csv
-    import re
+    import statistics
     rows = list(csv.DictReader(open(stats_csv)))
+    # per-dispatch durations of the same run: the stress kernels' launches of
+    # the 50 timed steps (after 5 warm-up steps), comparable with the event
+    # means bench.py reports
+    trace_csv = stats_csv.replace("_kernel_stats.csv", "_kernel_trace.csv")
+    timed = {}
+    if os.path.exists(trace_csv):
+        disp = list(csv.DictReader(open(trace_csv)))
+        for key, needle in STRESS_KERNELS.items():
+            hits = sorted((r for r in disp if needle in r["Kernel_Name"]),
+                          key=lambda r: int(r["Start_Timestamp"]))
+            per_step = 2 if key == "seg_state" else 1
+            sel = hits[5 * per_step:55 * per_step]
+            if sel:
+                timed[key] = statistics.mean(
+                    (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in sel)
     path = os.path.join(ROOT, "profiles", "kernel_trace_stress64k.md")
     with open(path, "w") as f:
         f.write("# rocprofv3 kernel trace of bench.py (stress64k + lra4k)\n\n")
@@ -77,11 +99,16 @@ def trace_summary(stats_csv):
                 "rank 2, then 52 calls of each form alone, then 105 calls of the N=4096 "
                 "shape (B=8 H=2 d=32 bf16 k=20 rank 2, non-causal).\n\n")
         f.write(f"kernel source hash: {kernel_source_hash()}\n\n")
+        if timed:
+            f.write("Mean traced duration over the launches of the 50 timed steps (compare "
+                    "with `kernels.*.mean_us` of the bench line, measured with HIP events "
+                    "attached to each dispatch):\n\n")
+            for key, us in timed.items():
+                f.write(f"- {key} (`{STRESS_KERNELS[key]}`): {us:.2f} us\n")
+            f.write("\n")
         f.write("| kernel | calls | avg us | min us | max us | share % |\n|---|---|---|---|---|---|\n")
         for r in rows:
-            name = re.sub(r"\(.*", "", r["Name"]).replace("void ", "")
-            if len(name) > 70:
-                name = name[:67] + "..."
+            name = _short_kernel_name(r["Name"])
             f.write(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
                     f"{float(r['Percentage']):.1f} |\n")
