@@ -1330,6 +1330,8 @@ static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
 
   if (a.causal) {
+    if (causal_strip_applies(a.dtype, a.d, a.band_k, a.causal, a.N))
+      return launch_causal_strip(a, timer, part);
     if (ring)
       launch_timed(timer, FMM_KERNEL_CAUSAL_APPLY, k_causal_ring<T, D, R>, dim3(BH * a.nseg), dim3(NT),
              lds, s, q, k, v, o, (const float*)part, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L,

@@ -58,4 +58,10 @@ bool band_pair_applies(int dtype, int d, int band_k, int causal, long long n);
 int pair_tile_rows();
 hipError_t launch_band_pair(const LaunchArgs& a, LaunchTimer* timer, const float* fin);
 
+// Causal apply with one 16-row strip per wavefront (fmm_causal.hip): bf16,
+// d = 32 or 64, band half-width <= 64; walks the state segments (a.L rows,
+// a multiple of tile_rows()) from their exclusive prefix records.
+bool causal_strip_applies(int dtype, int d, int band_k, int causal, long long n);
+hipError_t launch_causal_strip(const LaunchArgs& a, LaunchTimer* timer, const float* prefix);
+
 }  // namespace fmm

@@ -1,0 +1,163 @@
+// Building blocks of the bf16 strip kernels (fmm_pair.hip, fmm_causal.hip):
+// oct operands, raw buffer accesses and the swizzled LDS rows of K, V and
+// phi(K).
+//
+// Operands contracted over the head width (scores, far terms) are "octs": the
+// contraction index runs over 32-wide blocks and lane group g holds the eight
+// consecutive indices 8g..8g+7 of a block, so a row's slice is one 16-byte LDS
+// read.  Products contracted over keys (P V, the state sums) take their key
+// operands from transposed 8-byte reads, four keys per lane group and block.
+#pragma once
+
+#include "fmm_device.h"
+
+namespace fmm {
+
+typedef uint4 Oct;  // 8 bf16
+
+__device__ __forceinline__ f32x4 mma8(const Oct& a, const Oct& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ Oct oct_of(const uint2& lo, const uint2& hi) {
+  return make_uint4(lo.x, lo.y, hi.x, hi.y);
+}
+__device__ __forceinline__ Oct oct_pack(const float* f) {
+  return make_uint4(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]),
+                    pack_bf16x2(f[6], f[7]));
+}
+__device__ __forceinline__ void oct_unpack(const Oct& o, float* f) {
+  const uint32_t w[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ uint2 quad_pack(const f32x4& x) {
+  return make_uint2(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]));
+}
+// bf16 1.0 in all eight slots
+__device__ __forceinline__ Oct oct_ones() {
+  return make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
+}
+// phi_1 and phi_2 of eight values (one exp(-|x|) serves both maps)
+__device__ __forceinline__ void phi_oct(const Oct& x, Oct& p1, Oct& p2) {
+  float f[8], a[8], b[8];
+  oct_unpack(x, f);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) phi12(f[i], a[i], b[i]);
+  p1 = oct_pack(a);
+  p2 = oct_pack(b);
+}
+
+// Buffer resource over one head's [N, D] bf16 rows.  Raw buffer loads past
+// its end (or at a negative offset, i.e. a huge unsigned one) return zeros
+// without touching memory and stores there are dropped, so every global access
+// of a walk is branch-free: rows outside [0, N) and skipped prefetches just
+// use out-of-range offsets.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr uint32_t OOB = 0x80000000u;
+__device__ __forceinline__ Rsrc head_rsrc(const bf16_t* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(p), 0, bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 buf_load16(Rsrc rs, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+}
+__device__ __forceinline__ void buf_store8(Rsrc rs, uint32_t off, const uint2& v) {
+  typedef int i32x2 __attribute__((ext_vector_type(2)));
+  const i32x2 x = {(int)v.x, (int)v.y};
+  __builtin_amdgcn_raw_buffer_store_b64(x, rs, off, 0, 0);
+}
+
+// Byte offset of 16-byte chunk c of LDS row r.
+template <int D> struct RingRows;
+template <> struct RingRows<64> {
+  static constexpr int RB = 128;
+  // a permutation of 0..7 on every aligned 8-row group; rows r and r + 8 and
+  // the even (odd) rows of a 16-row group get distinct chunk positions, and
+  // four aligned consecutive rows distinct chunk pairs
+  __device__ __forceinline__ static int swz(int r) {
+    const int a = (r >> 2) & 1;
+    return ((((r & 3) ^ a) << 1) | a) ^ ((r >> 3) & 1);
+  }
+  __device__ __forceinline__ static int off(int r, int c) { return r * RB + ((c ^ swz(r)) << 4); }
+};
+template <> struct RingRows<32> {
+  static constexpr int RB = 80;
+  __device__ __forceinline__ static int off(int r, int c) { return r * RB + (c << 4); }
+};
+
+// Per-lane byte offsets of the reads within a 16-row block (blocks start at
+// multiples of 16 rows, so the swizzle of a row depends only on its index
+// within the block).  koff[p]: the lane's oct of row r, chunk 4p + g.
+// voff[nb]: the lane's transposed read for columns 16nb .. 16nb+15: lane t of
+// group g reads row 4g + t/4, columns 16nb + 4(t%4) .. +3, and the hardware
+// hands lane (j, g) the values X[4g + e][16nb + j], e = 0..3.
+template <int D>
+struct RingOffsets {
+  int koff[D / 32];
+  int voff[D / 16];
+  __device__ __forceinline__ RingOffsets() {
+    const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4, t = lane & 15;
+#pragma unroll
+    for (int p = 0; p < D / 32; ++p) koff[p] = RingRows<D>::off(r, 4 * p + g);
+#pragma unroll
+    for (int nb = 0; nb < D / 16; ++nb)
+      voff[nb] = RingRows<D>::off(4 * g + (t >> 2), 2 * nb + ((t & 3) >> 1)) + 8 * (t & 1);
+  }
+};
+
+__device__ __forceinline__ uint2 ld_tr16(const unsigned char* p) {
+  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+
+// ROWS consecutive K or V rows [k0, k0 + ROWS) of a head in registers (zero
+// outside [0, N), or everywhere when !on); thread t of NTHR holds chunk
+// t % CPR of row t / CPR + (NTHR / CPR) * it.
+template <int D, int ROWS, int NTHR>
+struct RowsCopy {
+  static constexpr int CPR = D / 8;
+  static constexpr int IT = ROWS * CPR / NTHR;
+  static_assert(ROWS * CPR % NTHR == 0, "whole rows per pass");
+  uint4 r[IT];
+  __device__ __forceinline__ void load(Rsrc rs, int k0, bool on) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int x = threadIdx.x + it * NTHR;
+      const int e = (k0 + x / CPR) * D + (x % CPR) * 8;
+      r[it] = buf_load16(rs, on ? (uint32_t)(2 * e) : OOB);
+    }
+  }
+  // 32-row unit j of the copied rows goes to ring slot slot_of(j) (skipped if < 0).
+  template <typename F>
+  __device__ __forceinline__ void store(unsigned char* ring, F slot_of) const {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int x = threadIdx.x + it * NTHR;
+      const int i = x / CPR;
+      const int slot = slot_of(i >> 5);
+      if (slot >= 0)
+        *reinterpret_cast<uint4*>(ring + RingRows<D>::off(slot * 32 + (i & 31), x % CPR)) = r[it];
+    }
+  }
+};
+
+// Query octs of the lane's row of NS consecutive 16-row strips:
+// qo[s][p] = q[i0 + 16s + r][32p + 8g .. +7] (zero for rows at or beyond N,
+// or everywhere when !on).
+template <int D, int NS>
+__device__ __forceinline__ void load_qo(Rsrc rs, int i0, bool on, Oct (*qo)[D / 32]) {
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+#pragma unroll
+    for (int p = 0; p < D / 32; ++p) {
+      const int e = (i0 + 16 * s + r) * D + 32 * p + 8 * g;
+      qo[s][p] = buf_load16(rs, on ? (uint32_t)(2 * e) : OOB);
+    }
+}
+
+}  // namespace fmm

@@ -23,6 +23,7 @@
 
 #include "fmm_device.h"
 #include "fmm_launch.h"
+#include "fmm_oct.h"
 
 namespace fmm {
 namespace {
@@ -31,139 +32,15 @@ constexpr int PW = 4;           // wavefronts per workgroup
 constexpr int PNT = PW * 64;    // threads per workgroup
 constexpr int PTM = 32 * PW;    // query rows per tile
 
-typedef uint4 Oct;  // 8 bf16
-
-__device__ __forceinline__ f32x4 mma8(const Oct& a, const Oct& b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
-__device__ __forceinline__ Oct oct_of(const uint2& lo, const uint2& hi) {
-  return make_uint4(lo.x, lo.y, hi.x, hi.y);
-}
-__device__ __forceinline__ Oct oct_pack(const float* f) {
-  return make_uint4(pack_bf16x2(f[0], f[1]), pack_bf16x2(f[2], f[3]), pack_bf16x2(f[4], f[5]),
-                    pack_bf16x2(f[6], f[7]));
-}
-__device__ __forceinline__ void oct_unpack(const Oct& o, float* f) {
-  const uint32_t w[4] = {o.x, o.y, o.z, o.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    f[2 * i] = __uint_as_float(w[i] << 16);
-    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-  }
-}
-
-// Buffer resource over one head's [N, D] bf16 rows.  Raw buffer loads past
-// its end (or at a negative offset, i.e. a huge unsigned one) return zeros
-// without touching memory and stores there are dropped, so every global access
-// of the walk is branch-free: rows outside [0, N) and skipped prefetches just
-// use out-of-range offsets.
-typedef __amdgpu_buffer_rsrc_t Rsrc;
-constexpr uint32_t OOB = 0x80000000u;
-__device__ __forceinline__ Rsrc head_rsrc(const bf16_t* p, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(p), 0, bytes, 0x00020000);
-}
-__device__ __forceinline__ uint4 buf_load16(Rsrc rs, uint32_t off) {
-  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
-}
-
-// Byte offset of 16-byte chunk c of ring row r.
-template <int D> struct PairRows;
-template <> struct PairRows<64> {
-  static constexpr int RB = 128;
-  // a permutation of 0..7 on every aligned 8-row group; rows r and r + 8 and
-  // the even (odd) rows of a 16-row group get distinct chunk positions, and
-  // four aligned consecutive rows distinct chunk pairs
-  __device__ __forceinline__ static int swz(int r) {
-    const int a = (r >> 2) & 1;
-    return ((((r & 3) ^ a) << 1) | a) ^ ((r >> 3) & 1);
-  }
-  __device__ __forceinline__ static int off(int r, int c) { return r * RB + ((c ^ swz(r)) << 4); }
-};
-template <> struct PairRows<32> {
-  static constexpr int RB = 80;
-  __device__ __forceinline__ static int off(int r, int c) { return r * RB + (c << 4); }
-};
-
 template <int D, int R, int KC>
 struct PairCfg {
   static constexpr int NB = D / 16, NQ = D / 32;
   static constexpr int U = 4 + 2 * KC;   // ring units of 32 keys: a tile's window
   static constexpr int NU = 2 * KC + 1;  // key units spanned by one wavefront's rows
-  static constexpr int RING = U * 32 * PairRows<D>::RB;
+  static constexpr int RING = U * 32 * RingRows<D>::RB;
   static constexpr int FRAG = R * NB * NQ * 64 * 16;
   static constexpr int LDS = 2 * RING + FRAG;
 };
-
-// K or V rows [k0, k0 + 128) of a head in registers (zero outside [0, N), or
-// everywhere when !on); thread t holds chunk t % CPR of row
-// t / CPR + (PNT / CPR) * it.
-template <int D>
-struct PairCopy {
-  static constexpr int CPR = D / 8;
-  static constexpr int IT = PTM * CPR / PNT;
-  uint4 r[IT];
-  __device__ __forceinline__ void load(Rsrc rs, int k0, bool on) {
-#pragma unroll
-    for (int it = 0; it < IT; ++it) {
-      const int x = threadIdx.x + it * PNT;
-      const int e = (k0 + x / CPR) * D + (x % CPR) * 8;
-      r[it] = buf_load16(rs, on ? (uint32_t)(2 * e) : OOB);
-    }
-  }
-  // Unit j (0..3) of the copied rows goes to ring slot slot_of(j) (skipped if < 0).
-  template <typename F>
-  __device__ __forceinline__ void store(unsigned char* ring, F slot_of) const {
-#pragma unroll
-    for (int it = 0; it < IT; ++it) {
-      const int x = threadIdx.x + it * PNT;
-      const int i = x / CPR;
-      const int slot = slot_of(i >> 5);
-      if (slot >= 0)
-        *reinterpret_cast<uint4*>(ring + PairRows<D>::off(slot * 32 + (i & 31), x % CPR)) = r[it];
-    }
-  }
-};
-
-// Per-lane byte offsets of the ring reads within a 16-row block (ring units
-// start at multiples of 32 rows, so the swizzle of a row depends only on its
-// index within the block).  koff[p]: the lane's K oct, row r, chunk 4p + g.
-// voff[nb]: the lane's V^T transposed read for columns 16nb .. 16nb+15: lane
-// t of group g reads row 4g + t/4, columns 16nb + 4(t%4) .. +3, and the
-// hardware hands lane (j, g) the values V[4g + e][16nb + j], e = 0..3.
-template <int D>
-struct RingOffsets {
-  int koff[D / 32];
-  int voff[D / 16];
-  __device__ __forceinline__ RingOffsets() {
-    const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4, t = lane & 15;
-#pragma unroll
-    for (int p = 0; p < D / 32; ++p) koff[p] = PairRows<D>::off(r, 4 * p + g);
-#pragma unroll
-    for (int nb = 0; nb < D / 16; ++nb)
-      voff[nb] = PairRows<D>::off(4 * g + (t >> 2), 2 * nb + ((t & 3) >> 1)) + 8 * (t & 1);
-  }
-};
-
-__device__ __forceinline__ uint2 ld_tr16(const unsigned char* p) {
-  typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p));
-  return __builtin_bit_cast(uint2, v);
-}
-
-// Query octs of the lane's row of each strip: qo[s][p] = q[i0 + 16s + r][32p + 8g .. +7]
-// (zero for rows at or beyond N, or everywhere when !on).
-template <int D>
-__device__ __forceinline__ void load_qo(Rsrc rs, int i0, bool on, Oct (*qo)[D / 32]) {
-  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
-#pragma unroll
-  for (int s = 0; s < 2; ++s)
-#pragma unroll
-    for (int p = 0; p < D / 32; ++p) {
-      const int e = (i0 + 16 * s + r) * D + 32 * p + 8 * g;
-      qo[s][p] = buf_load16(rs, on ? (uint32_t)(2 * e) : OOB);
-    }
-}
 
 // State fragments from the non-causal tile-order record (see k_seg_state):
 // sf[((l*NB + nb)*NQ + p)*64 + lane] holds S_l[32p + 8g + i][16nb + r],
@@ -224,7 +101,7 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
   int ubase[NU];
 #pragma unroll
   for (int u = 0; u < NU; ++u)
-    ubase[u] = __builtin_amdgcn_readfirstlane(((slot0 + u) % C::U) * 32 * PairRows<D>::RB);
+    ubase[u] = __builtin_amdgcn_readfirstlane(((slot0 + u) % C::U) * 32 * RingRows<D>::RB);
   const Oct ones = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
 
   // Exact tiles: the band cuts the first block of each strip below the
@@ -246,7 +123,7 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
 #pragma unroll
       for (int p = 0; p < NQ; ++p) {
         const Oct ko = *reinterpret_cast<const Oct*>(kr + ubase[b >> 1] + ro.koff[p] +
-                                                     16 * PairRows<D>::RB * (b & 1));
+                                                     16 * RingRows<D>::RB * (b & 1));
         acc = mma8(ko, qo[s][p], acc);
       }
       sc[j] = acc;
@@ -297,7 +174,7 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         const unsigned char* vp = vr + ubase[u] + ro.voff[nb];
-        const Oct vt = oct_of(ld_tr16(vp), ld_tr16(vp + 16 * PairRows<D>::RB));
+        const Oct vt = oct_of(ld_tr16(vp), ld_tr16(vp + 16 * RingRows<D>::RB));
         o[nb] = mma8(vt, pq[u], o[nb]);
       }
       o[NB] = mma8(ones, pq[u], o[NB]);
@@ -421,7 +298,7 @@ __global__ __launch_bounds__(PNT, 2) void k_band_pair(const bf16_t* __restrict__
   pair_frags<D, R>(fin + (size_t)bh * R * D * (D + 1), sf, zo);
 #pragma unroll
   for (int x = 0; x < U; x += 4) {
-    PairCopy<D> ck, cv;
+    RowsCopy<D, PTM, PNT> ck, cv;
     ck.load(kh, (ua0 + x) * 32, true);
     cv.load(vh, (ua0 + x) * 32, true);
     auto slot = [=](int j) { return x + j < U ? x + j : -1; };
@@ -430,11 +307,11 @@ __global__ __launch_bounds__(PNT, 2) void k_band_pair(const bf16_t* __restrict__
   }
   const RingOffsets<D> ro;
   Oct qo[2][NQ], qn[2][NQ];
-  load_qo<D>(qh, s0 + 32 * w, true, qo);
-  PairCopy<D> pk, pv;
+  load_qo<D, 2>(qh, s0 + 32 * w, true, qo);
+  RowsCopy<D, PTM, PNT> pk, pv;
   pk.load(kh, (ua0 + U) * 32, ntile > 1);
   pv.load(vh, (ua0 + U) * 32, ntile > 1);
-  load_qo<D>(qh, s0 + PTM + 32 * w, ntile > 1, qn);
+  load_qo<D, 2>(qh, s0 + PTM + 32 * w, ntile > 1, qn);
   // one tile, then the ring slides by the four prefetched units (past the
   // last tile the loads and stores are harmless no-ops on zeros)
   auto step = [&](int t, auto general) {
@@ -454,7 +331,7 @@ __global__ __launch_bounds__(PNT, 2) void k_band_pair(const bf16_t* __restrict__
       for (int p = 0; p < NQ; ++p) qo[s][p] = qn[s][p];
     pk.load(kh, (ua0 + U + 4 * (t + 1)) * 32, t + 2 < ntile);
     pv.load(vh, (ua0 + U + 4 * (t + 1)) * 32, t + 2 < ntile);
-    load_qo<D>(qh, i0 + 2 * PTM, t + 2 < ntile, qn);
+    load_qo<D, 2>(qh, i0 + 2 * PTM, t + 2 < ntile, qn);
   };
   // exact tiles: k = 32*KC and every row's band inside [0, N); they form one
   // contiguous run of the walk, between the leading and trailing general tiles
