@@ -48,16 +48,19 @@ struct CausalCfg {
 
 // The running sums of the walk, T_l = phi_l(K)^T [V | 1], as 16x16 fp32 tiles
 // spread over the wavefronts.  Feature tile (l, p, h) covers the features
-// f(i) = 32p + 8(i/4) + 4h + i%4, i = 0..15, so lane (e, g) of its column
-// block eb holds S_l[32p + 8g + 4h + {0..3}][16eb + e]: the h = 0 and h = 1
-// tiles of (l, p) together are lane (e, g)'s oct of the far product's
-// fragment.  Column block NB is the ones column: every lane holds
-// z_l[32p + 8g + 4h + {0..3}].
+// f(4q + i) = 32p + 8q + 4((q & 1) ^ h) + i, q, i = 0..3, so lane (e, g) of its
+// column block eb holds S_l[32p + 8g + 4((g & 1) ^ h) + {0..3}][16eb + e]: the
+// h = 0 and h = 1 tiles of (l, p) are the two halves of lane (e, g)'s oct of
+// the far product's fragment (in swapped order for odd g), and their
+// transposed phi-row reads alternate between the chunk halves, which keeps
+// those reads free of bank conflicts.  Column block NB is the ones column:
+// every lane holds z_l at the same features.
 template <int D, int R>
 struct CausalState {
   static constexpr int NB = D / 16, NQ = D / 32;
   static constexpr int FT = R * NQ * 2;                 // feature tiles
   static constexpr int AG = FT >= CW ? FT / CW : 1;     // tiles per wavefront
+  static_assert(AG <= 2, "a wavefront holds at most the two halves of one oct");
   f32x4 acc[AG][NB + 1];
   int aoff[AG];  // transposed phi-row read of each tile (lane offset, map base)
 
@@ -78,14 +81,15 @@ struct CausalState {
       int l, p, h;
       tile_of(w, a, l, p, h);
       const float* sl = rec + (size_t)l * D * (D + 1);
-      const int cb = 2 * p + (g >> 1), gp = (2 * g + h) & 3;
+      const int hq = (g & 1) ^ h;
+      const int cb = 2 * p + (g >> 1), gp = (2 * g + hq) & 3;
 #pragma unroll
       for (int eb = 0; eb < NB; ++eb)
         acc[a][eb] = *reinterpret_cast<const f32x4*>(sl + ((cb * NB + eb) * 64 + gp * 16 + e) * 4);
-      acc[a][NB] = *reinterpret_cast<const f32x4*>(sl + D * D + 32 * p + 8 * g + 4 * h);
-      // lane t of group g reads key 4g + t/4, features 32p + 8(t%4) + 4h .. +3
+      acc[a][NB] = *reinterpret_cast<const f32x4*>(sl + D * D + 32 * p + 8 * g + 4 * hq);
+      // lane t of group g reads key 4g + t/4, features 32p + 8(t%4) + 4((t%2) ^ h) .. +3
       aoff[a] = l * CTM * RingRows<D>::RB + RingRows<D>::off(4 * g + (t >> 2), 4 * p + (t & 3)) +
-                8 * h;
+                8 * ((t & 1) ^ h);
     }
   }
 
@@ -130,18 +134,28 @@ struct CausalState {
   // z_l[32p + 8g + {0..7}].
   __device__ __forceinline__ static void store(int w, const Frags& f, Oct* sf, Oct* szo) {
     const int lane = threadIdx.x & 63, e = lane & 15, g = lane >> 4;
-#pragma unroll
-    for (int a = 0; a < AG; ++a) {
+    const bool odd = g & 1;
+    if constexpr (AG == 2) {  // both halves of each oct: one 16-byte store
       int l, p, h;
-      tile_of(w, a, l, p, h);
+      tile_of(w, 0, l, p, h);
+#pragma unroll
+      for (int eb = 0; eb <= NB; ++eb) {
+        const uint2 x = f.q[0][eb], y = f.q[1][eb];
+        const Oct o = odd ? oct_of(y, x) : oct_of(x, y);
+        if (eb < NB) sf[((l * NB + eb) * NQ + p) * 64 + lane] = o;
+        else if (e == 0) szo[(l * NQ + p) * 4 + g] = o;
+      }
+    } else {
+      int l, p, h;
+      tile_of(w, 0, l, p, h);
+      const int hb = 8 * ((g & 1) ^ h);
 #pragma unroll
       for (int eb = 0; eb < NB; ++eb)
         *reinterpret_cast<uint2*>(reinterpret_cast<unsigned char*>(
-                                      sf + ((l * NB + eb) * NQ + p) * 64 + lane) +
-                                  8 * h) = f.q[a][eb];
+                                      sf + ((l * NB + eb) * NQ + p) * 64 + lane) + hb) = f.q[0][eb];
       if (e == 0)
         *reinterpret_cast<uint2*>(reinterpret_cast<unsigned char*>(szo + (l * NQ + p) * 4 + g) +
-                                  8 * h) = f.q[a][NB];
+                                  hb) = f.q[0][NB];
     }
   }
 };
@@ -173,20 +187,34 @@ struct PhiRows {
   }
 };
 
-// One strip of one tile: rows i0 .. i0+15 (i0 = t0 + 16w).  The ring holds
-// the window units [t0/32 - KC, t0/32 + 2), window unit m in ring slot
-// (m0 + m) % U; window block j (16 keys) is unit j/2, half j%2.  The strip's
-// band is window blocks w .. w + 2KC.  Exact tiles (!GENERAL: k = 32*KC and
-// the whole window inside [0, N)) cut only the first block (keys below
-// i - k) and the last (keys above i) and start those score products from
+// One tile of a wavefront: the strip rows i0 .. i0+15 (i0 = t0 + 16w), then
+// the state update by the tile's keys and phi of the next tile's keys.  The
+// ring holds the window units [t0/32 - KC, t0/32 + 2), window unit m in ring
+// slot (m0 + m) % U; window block j (16 keys) is unit j/2, half j%2.  The
+// strip's band is window blocks w .. w + 2KC.  Exact tiles (!GENERAL: k =
+// 32*KC and the whole window inside [0, N)) cut only the first block (keys
+// below i - k) and the last (keys above i) and start those score products from
 // -inf biases; GENERAL tiles mask every block against the band clipped to
-// [0, N).  mid() runs once phi(q) is formed (the query octs are dead then).
-template <int D, int R, int KC, bool GENERAL, class Mid>
-__device__ __forceinline__ void strip_tile(Rsrc oh, int t0, int w, int m0, int N, int band_k,
-                                           float scale2, float sn, float sfw, Oct* qo,
-                                           const unsigned char* kr, const unsigned char* vr,
-                                           const unsigned char* phr, const RingOffsets<D>& ro,
-                                           const Oct* sf, const Oct* szo, Mid mid) {
+// [0, N).  The intra-tile product covers tile blocks 0 .. w in NPAIR = w/2 + 1
+// block pairs; the last pair's masks (lower-triangular diagonal block, and
+// the block after it empty for even w) are tmask.
+//
+// The near and far parts are independent until the blend, so the work runs
+// as phases that pair matrix-core products of one part with vector
+// arithmetic of the other (scheduling fences keep the phases apart):
+//   near scores + phi(q) | softmax + far products of map 0 with the sums
+//   before the tile | P V + intra-tile products of map 0 | far products of
+//   map 1 + near normalisation and blend | state update + phi of the next
+//   tile's keys, store
+// mid() runs once phi(q) is formed (the query octs are dead then).
+template <int D, int R, int KC, bool GENERAL, int NPAIR, class Mid>
+__device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N, int band_k,
+                                          float scale2, float sn, float sfw, const Oct* qo,
+                                          const unsigned char* kr, const unsigned char* vr,
+                                          const unsigned char* phr, const RingOffsets<D>& ro,
+                                          const Oct* sf, const Oct* szo, const uint2* tmask,
+                                          CausalState<D, R>& st, const RowsCopy<D, CTM, CNT>& pk,
+                                          PhiRows<D, R>& phn, Mid mid) {
   using C = CausalCfg<D, R, KC>;
   constexpr int NB = C::NB, NQ = C::NQ, NS = C::NS, RB = C::RB, U = C::U;
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
@@ -198,8 +226,11 @@ __device__ __forceinline__ void strip_tile(Rsrc oh, int t0, int w, int m0, int N
   int kb[NS];
 #pragma unroll
   for (int b = 0; b < NS; ++b) kb[b] = wblock(w + b);
+  int tb[4];  // tile blocks 0..3 are window blocks 2KC..2KC+3
+#pragma unroll
+  for (int j = 0; j < 4; ++j) tb[j] = wblock(2 * KC + j);
 
-  // ---- near field: S^T = K Q^T over the strip's NS blocks
+  // ---- phase 1: near scores S^T = K Q^T over the strip's NS blocks | phi(q)
   f32x4 sc[NS];
   {
     f32x4 bias_lo, bias_hi;
@@ -218,6 +249,18 @@ __device__ __forceinline__ void strip_tile(Rsrc oh, int t0, int w, int m0, int N
       sc[b] = acc;
     }
   }
+  Oct ph[R][NQ];
+#pragma unroll
+  for (int p = 0; p < NQ; ++p) {
+    Oct p2;
+    phi_oct(qo[p], ph[0][p], p2);
+    if constexpr (R == 2) ph[1][p] = p2;
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- phase 2: softmax numerators | far products with the sums before the
+  // tile (Eq. (9) numerator and denominator)
+  mid();
   if constexpr (GENERAL) {
     const int kbase = i0 - 32 * KC + 4 * g;
     const int row = i0 + r;
@@ -230,8 +273,7 @@ __device__ __forceinline__ void strip_tile(Rsrc oh, int t0, int w, int m0, int N
       for (int i = 0; i < 4; ++i)
         if ((unsigned)(16 * b + i - lo) > (unsigned)span) sc[b][i] = -INFINITY;
   }
-  // softmax numerators; P quads in pairs of blocks (the last pair padded)
-  f32x4 o[NB + 1];
+  uint2 pq[NS + 1];
   {
     float mloc = -INFINITY;
 #pragma unroll
@@ -240,7 +282,6 @@ __device__ __forceinline__ void strip_tile(Rsrc oh, int t0, int w, int m0, int N
       for (int i = 0; i < 4; ++i) mloc = fmaxf(mloc, sc[b][i]);
     const float m = col_max(mloc);
     const float ms = (m == -INFINITY ? 0.f : m) * scale2;
-    uint2 pq[NS + 1];
 #pragma unroll
     for (int b = 0; b < NS; ++b) {
       f32x4 pv;
@@ -249,53 +290,13 @@ __device__ __forceinline__ void strip_tile(Rsrc oh, int t0, int w, int m0, int N
       pq[b] = quad_pack(pv);
     }
     pq[NS] = make_uint2(0u, 0u);
-#pragma unroll
-    for (int nb = 0; nb <= NB; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int c = 0; c < (NS + 1) / 2; ++c) {
-      const Oct pc = oct_of(pq[2 * c], pq[2 * c + 1]);
-      const bool two = 2 * c + 1 < NS;
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const uint2 v0 = ld_tr16(vr + kb[2 * c] + ro.voff[nb]);
-        const uint2 v1 = two ? ld_tr16(vr + kb[2 * c + 1] + ro.voff[nb]) : make_uint2(0u, 0u);
-        o[nb] = mma8(oct_of(v0, v1), pc, o[nb]);
-      }
-      o[NB] = mma8(ones, pc, o[NB]);
-    }
   }
-
-  // ---- far field
-  Oct ph[R][NQ];
-#pragma unroll
-  for (int p = 0; p < NQ; ++p) {
-    Oct p2;
-    phi_oct(qo[p], ph[0][p], p2);
-    if constexpr (R == 2) ph[1][p] = p2;
-  }
-  mid();
-
-  f32x4 fo[NB];
-  {
-    const float a = sn > 0.f ? sn * fast_rcp(o[NB][0]) : 0.f;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) fo[nb] = o[nb] * a;
-  }
-  // diagonal block of the intra-tile product: keys 4g + i <= r
-  uint2 dmask;
-  dmask.x = (4 * g <= r ? 0xffffu : 0u) | (4 * g + 1 <= r ? 0xffff0000u : 0u);
-  dmask.y = (4 * g + 2 <= r ? 0xffffu : 0u) | (4 * g + 3 <= r ? 0xffff0000u : 0u);
-  // tile blocks 0..3 are window blocks 2KC..2KC+3
-  int tb[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) tb[j] = wblock(2 * KC + j);
-
-#pragma unroll
-  for (int l = 0; l < R; ++l) {
-    f32x4 num[NB + 1];
+  // far products of map l: sums before the tile (Eq. (9) numerator and
+  // denominator), then the tile's keys t0 .. i (tile blocks 0 .. w, block w
+  // lower-triangular)
+  auto far_prefix = [&](int l, f32x4* num) {
 #pragma unroll
     for (int nb = 0; nb <= NB; ++nb) num[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // sums of the keys before the tile (Eq. (9) numerator and denominator)
 #pragma unroll
     for (int p = 0; p < NQ; ++p) {
 #pragma unroll
@@ -303,11 +304,11 @@ __device__ __forceinline__ void strip_tile(Rsrc oh, int t0, int w, int m0, int N
         num[nb] = mma8(sf[((l * NB + nb) * NQ + p) * 64 + lane], ph[l][p], num[nb]);
       num[NB] = mma8(szo[(l * NQ + p) * 4 + g], ph[l][p], num[NB]);
     }
-    // the tile's keys t0 .. i: blocks 0 .. w, block w lower-triangular
+  };
+  auto far_intra = [&](int l, f32x4* num) {
     const unsigned char* pl = phr + l * CTM * RB;
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      if (2 * c > w) break;
+    for (int c = 0; c < NPAIR; ++c) {
       f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int p = 0; p < NQ; ++p) {
@@ -316,11 +317,10 @@ __device__ __forceinline__ void strip_tile(Rsrc oh, int t0, int w, int m0, int N
                   a1);
       }
       uint2 q0 = quad_pack(a0), q1 = quad_pack(a1);
-      const uint2 all = make_uint2(~0u, ~0u), none = make_uint2(0u, 0u);
-      const uint2 m0q = 2 * c < w ? all : dmask;
-      const uint2 m1q = 2 * c + 1 < w ? all : 2 * c + 1 == w ? dmask : none;
-      q0.x &= m0q.x; q0.y &= m0q.y;
-      q1.x &= m1q.x; q1.y &= m1q.y;
+      if (c == NPAIR - 1) {
+        q0.x &= tmask[0].x; q0.y &= tmask[0].y;
+        q1.x &= tmask[1].x; q1.y &= tmask[1].y;
+      }
       const Oct ac = oct_of(q0, q1);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
@@ -329,10 +329,61 @@ __device__ __forceinline__ void strip_tile(Rsrc oh, int t0, int w, int m0, int N
                        ac, num[nb]);
       num[NB] = mma8(ones, ac, num[NB]);
     }
+  };
+  auto far_blend = [&](const f32x4* num, f32x4* fo) {
     const float f = sfw > 0.f ? sfw * fast_rcp(num[NB][0]) : 0.f;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) fo[nb] += num[nb] * f;
+  };
+  f32x4 num0[NB + 1];
+  far_prefix(0, num0);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- phase 3: O^T = V^T P^T and the row sums | intra-tile scores of map 0
+  f32x4 o[NB + 1];
+#pragma unroll
+  for (int nb = 0; nb <= NB; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int c = 0; c < (NS + 1) / 2; ++c) {
+    const Oct pc = oct_of(pq[2 * c], pq[2 * c + 1]);
+    const bool two = 2 * c + 1 < NS;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const uint2 v0 = ld_tr16(vr + kb[2 * c] + ro.voff[nb]);
+      const uint2 v1 = two ? ld_tr16(vr + kb[2 * c + 1] + ro.voff[nb]) : make_uint2(0u, 0u);
+      o[nb] = mma8(oct_of(v0, v1), pc, o[nb]);
+    }
+    o[NB] = mma8(ones, pc, o[NB]);
   }
+  far_intra(0, num0);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- phase 4: far products of the other map | near normalisation, blend
+  // of map 0
+  f32x4 fo[NB];
+  {
+    const float a = sn > 0.f ? sn * fast_rcp(o[NB][0]) : 0.f;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) fo[nb] = o[nb] * a;
+  }
+  far_blend(num0, fo);
+  if constexpr (R == 2) {
+    f32x4 num1[NB + 1];
+    far_prefix(1, num1);
+    far_intra(1, num1);
+    far_blend(num1, fo);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- phase 5: the sums advance by the tile's 64 keys | phi of the next
+  // tile's keys, store
+  if (CausalState<D, R>::FT >= CW || CausalState<D, R>::active(w)) {
+    int vb[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) vb[u] = __builtin_amdgcn_readfirstlane(((m0 + KC + u) % U) * 32 * RB);
+    st.add(phr, vr, vb, ro);
+  }
+  phn.compute(pk);
   // rows at or beyond N fall outside the output buffer and are dropped
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb)
@@ -375,10 +426,11 @@ __global__ __launch_bounds__(CNT, 2) void k_causal_strip(const bf16_t* __restric
   const int s0 = seg * L, s1 = min(N, s0 + L);
   const int ntile = (s1 - s0 + CTM - 1) / CTM;
   const int ua0 = (s0 >> 5) - KC;
+  constexpr bool all_st = St::FT >= CW;  // every wave owns state tiles
   const bool has_st = St::active(w);
 
   St st;
-  if (has_st) st.load(w, prefix + ((size_t)bh * nseg + seg) * R * D * (D + 1));
+  if (all_st || has_st) st.load(w, prefix + ((size_t)bh * nseg + seg) * R * D * (D + 1));
   using RC = RowsCopy<D, CTM, CNT>;
 #pragma unroll
   for (int x = 0; x < U; x += 2) {
@@ -396,7 +448,7 @@ __global__ __launch_bounds__(CNT, 2) void k_causal_strip(const bf16_t* __restric
     ph.compute(ck);
     ph.store(phr);
   }
-  if (has_st) St::store(w, st.pack(), sf, szo);
+  if (all_st || has_st) St::store(w, st.pack(), sf, szo);
   const RingOffsets<D> ro;
   Oct qo[1][NQ];
   load_qo<D, 1>(qh, s0 + 16 * w, true, qo);
@@ -407,31 +459,40 @@ __global__ __launch_bounds__(CNT, 2) void k_causal_strip(const bf16_t* __restric
   // one tile, then the sums advance, the ring slides by the prefetched units
   // and their phi rows replace the tile's (past the last tile the loads and
   // stores are harmless no-ops on zeros, and the sums are not read again)
+  // masks of the last block pair of the intra-tile product
+  uint2 tmask[2];
+  {
+    const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+    uint2 dm;
+    dm.x = (4 * g <= r ? 0xffffu : 0u) | (4 * g + 1 <= r ? 0xffff0000u : 0u);
+    dm.y = (4 * g + 2 <= r ? 0xffffu : 0u) | (4 * g + 3 <= r ? 0xffff0000u : 0u);
+    tmask[0] = (w & 1) ? make_uint2(~0u, ~0u) : dm;
+    tmask[1] = (w & 1) ? dm : make_uint2(0u, 0u);
+  }
+  // one tile, then the ring slides by the prefetched units and their phi rows
+  // replace the tile's (past the last tile the loads and stores are harmless
+  // no-ops on zeros, and the sums are not read again)
   auto step = [&](int t, auto general) {
+    constexpr bool G = decltype(general)::value;
     __syncthreads();  // ring, phi rows and fragments hold tile t's
     const int t0 = s0 + t * CTM;
     const int m0 = 2 * t;
     auto mid = [&]() { load_qo<D, 1>(qh, t0 + CTM + 16 * w, t + 1 < ntile, qo); };
-    strip_tile<D, R, KC, decltype(general)::value>(oh, t0, w, m0, N, band_k, scale2, sn, sfw,
-                                                   qo[0], kr, vr, phr, ro, sf, szo, mid);
-    __builtin_amdgcn_sched_barrier(0);
+    PhiRows<D, R> phn;
+    if (w < 2)
+      tile_work<D, R, KC, G, 1>(oh, t0, w, m0, N, band_k, scale2, sn, sfw, qo[0], kr, vr, phr,
+                                ro, sf, szo, tmask, st, pk, phn, mid);
+    else
+      tile_work<D, R, KC, G, 2>(oh, t0, w, m0, N, band_k, scale2, sn, sfw, qo[0], kr, vr, phr,
+                                ro, sf, szo, tmask, st, pk, phn, mid);
     typename St::Frags fr;
-    if (has_st) {
-      int vb[2];
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-        vb[u] = __builtin_amdgcn_readfirstlane(((m0 + KC + u) % U) * 32 * RB);
-      st.add(phr, vr, vb, ro);
-      fr = st.pack();
-    }
-    PhiRows<D, R> ph;
-    ph.compute(pk);  // the prefetched rows are the keys of tile t+1
+    if (all_st || has_st) fr = st.pack();
     __syncthreads();  // every wave is done with tile t's LDS
     auto slot = [=](int j) { return (m0 + j) % U; };
     pk.store(kr, slot);
     pv.store(vr, slot);
-    ph.store(phr);
-    if (has_st) St::store(w, fr, sf, szo);
+    phn.store(phr);
+    if (all_st || has_st) St::store(w, fr, sf, szo);
     pk.load(kh, (ua0 + U + m0 + 2) * 32, t + 2 < ntile);
     pv.load(vh, (ua0 + U + m0 + 2) * 32, t + 2 < ntile);
   };

@@ -15,10 +15,9 @@
 // row's slice is one 16-byte LDS read.  The P V product keeps the quad
 // convention of the score output (keys 4g..4g+3 of each 16-key block).
 //
-// K and V rows sit unpadded in an LDS ring; for d = 64 the 16-byte chunk c of
-// ring row r is stored at chunk c ^ swz(r), which keeps the 16-byte K reads,
-// the transposed 8-byte V reads and the 16-byte row stores free of bank
-// conflicts.  d = 32 rows are padded to 80 bytes instead.
+// K and V rows sit unpadded in an LDS ring, their 16-byte chunks permuted per
+// row so that the 16-byte K reads, the transposed 8-byte V reads and the row
+// stores are free of bank conflicts.
 #include <type_traits>
 
 #include "fmm_device.h"
