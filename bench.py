@@ -57,7 +57,7 @@ def parse():
 STRESS_KERNELS = {
     "seg_state": "k_seg_state<unsigned short, 64, 2>",
     "band_apply": "k_band_pair<64, 2, 2>",
-    "causal_apply": "k_causal_ring<unsigned short, 64, 2>",
+    "causal_apply": "k_causal_strip<64, 2, 2>",
 }
 
 
@@ -73,8 +73,9 @@ def trace_summary(stats_csv):
     import statistics
     rows = list(csv.DictReader(open(stats_csv)))
     # per-dispatch durations of the same run: the stress kernels' launches of
-    # the 50 timed steps (after 5 warm-up steps), comparable with the event
-    # means bench.py reports
+    # the 50 timed steps (after 5 warm-up steps, no per-kernel events) and of
+    # the 50 steps that follow with events attached to each dispatch (the
+    # event means bench.py reports)
     trace_csv = stats_csv.replace("_kernel_stats.csv", "_kernel_trace.csv")
     timed = {}
     if os.path.exists(trace_csv):
@@ -83,10 +84,10 @@ def trace_summary(stats_csv):
             hits = sorted((r for r in disp if needle in r["Kernel_Name"]),
                           key=lambda r: int(r["Start_Timestamp"]))
             per_step = 2 if key == "seg_state" else 1
-            sel = hits[5 * per_step:55 * per_step]
-            if sel:
-                timed[key] = statistics.mean(
-                    (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in sel)
+            dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in hits]
+            a, b = dur[5 * per_step:55 * per_step], dur[55 * per_step:105 * per_step]
+            if a and b:
+                timed[key] = (statistics.mean(a), statistics.mean(b))
     path = os.path.join(ROOT, "profiles", "kernel_trace_stress64k.md")
     with open(path, "w") as f:
         f.write("# rocprofv3 kernel trace of bench.py (stress64k + lra4k)\n\n")
@@ -96,15 +97,18 @@ def trace_summary(stats_csv):
         f.write("Rows: rocprofv3's own kernel_stats.csv (durations in microseconds), names "
                 "shortened to the kernel template.  The run times 50 steps (+5 warm-up) of "
                 "one non-causal and one causal forward of B=1 H=8 N=65536 d=64 bf16 k=64 "
-                "rank 2, then 52 calls of each form alone, then 105 calls of the N=4096 "
-                "shape (B=8 H=2 d=32 bf16 k=20 rank 2, non-causal).\n\n")
+                "rank 2, then the same 50 steps with HIP events attached to every dispatch "
+                "(the per-kernel means of the bench line), then 52 calls of each form alone, "
+                "then 105 calls of the N=4096 shape (B=8 H=2 d=32 bf16 k=20 rank 2, "
+                "non-causal).\n\n")
         f.write(f"kernel source hash: {kernel_source_hash()}\n\n")
         if timed:
-            f.write("Mean traced duration over the launches of the 50 timed steps (compare "
-                    "with `kernels.*.mean_us` of the bench line, measured with HIP events "
-                    "attached to each dispatch):\n\n")
-            for key, us in timed.items():
-                f.write(f"- {key} (`{STRESS_KERNELS[key]}`): {us:.2f} us\n")
+            f.write("Mean traced duration over the launches of the 50 timed steps, and over "
+                    "the 50 steps with dispatch events (compare with `kernels.*.mean_us` of the "
+                    "bench line, which the events measure):\n\n")
+            for key, (us, us_ev) in timed.items():
+                f.write(f"- {key} (`{STRESS_KERNELS[key]}`): {us:.2f} us timed steps, "
+                        f"{us_ev:.2f} us steps with events\n")
             f.write("\n")
         f.write("| kernel | calls | avg us | min us | max us | share % |\n|---|---|---|---|---|---|\n")
         for r in rows:
@@ -285,13 +289,15 @@ def main():
         timed(step, args.steps, args.warmup, torch)
         return
 
+    # the timed steps: no per-kernel events attached (they add a completion
+    # signal to every dispatch, several microseconds per launch)
+    t_step = timed(step, args.steps, args.warmup, torch)
+    # the same steps again with a start/stop event pair attached to every
+    # kernel dispatch: per-kernel durations for the roofline
     for name in binding.KERNELS:
         binding.kernel_timing_read(name)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
     binding.kernel_timing(True)
-    t_step = timed(step, args.steps, 0, torch)
+    t_step_ev = timed(step, args.steps, 0, torch)
     binding.kernel_timing(False)
     kt = {}
     for name in binding.KERNELS:
@@ -373,6 +379,7 @@ def main():
             "parallelism": "single-gpu",
         },
         "roofline": roofline,
+        "ms_per_step_with_kernel_events": round(t_step_ev * 1e3, 4),
         "forms": {
             "noncausal": {"tokens_per_s": round(w.B * w.N / t_nc, 1),
                           "ms_per_call": round(t_nc * 1e3, 4),
