@@ -305,32 +305,29 @@ __global__ __launch_bounds__(PNT, 2) void k_band_pair(const bf16_t* __restrict__
     cv.store(vr, slot);
   }
   const RingOffsets<D> ro;
-  Oct qo[2][NQ], qn[2][NQ];
+  Oct qo[2][NQ];
   load_qo<D, 2>(qh, s0 + 32 * w, true, qo);
   RowsCopy<D, PTM, PNT> pk, pv;
   pk.load(kh, (ua0 + U) * 32, ntile > 1);
   pv.load(vh, (ua0 + U) * 32, ntile > 1);
-  load_qo<D, 2>(qh, s0 + PTM + 32 * w, ntile > 1, qn);
   // one tile, then the ring slides by the four prefetched units (past the
-  // last tile the loads and stores are harmless no-ops on zeros)
+  // last tile the loads and stores are harmless no-ops on zeros); the next
+  // tile's query rows are loaded into the query registers as soon as phi(q)
+  // has consumed them (separate prefetch registers cost more in register
+  // pressure than the shorter lead costs in latency)
   auto step = [&](int t, auto general) {
     __syncthreads();  // the ring holds the window of tile t
     const int i0 = s0 + t * PTM + 32 * w;
     const int slot0 = (4 * t + w) % U;
-    auto mid = [&]() {};
+    auto mid = [&]() { load_qo<D, 2>(qh, i0 + PTM, t + 1 < ntile, qo); };
     pair_tile<D, R, KC, decltype(general)::value>(oh, i0, N, band_k, scale2, sn, sfw, qo, kr, vr,
                                                   slot0, ro, sf, zo, mid);
     __syncthreads();  // every wave is done with the window of tile t
     auto slot = [=](int j) { return (4 * t + j) % U; };
     pk.store(kr, slot);
     pv.store(vr, slot);
-#pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int p = 0; p < NQ; ++p) qo[s][p] = qn[s][p];
     pk.load(kh, (ua0 + U + 4 * (t + 1)) * 32, t + 2 < ntile);
     pv.load(vh, (ua0 + U + 4 * (t + 1)) * 32, t + 2 < ntile);
-    load_qo<D, 2>(qh, i0 + 2 * PTM, t + 2 < ntile, qn);
   };
   // exact tiles: k = 32*KC and every row's band inside [0, N); they form one
   // contiguous run of the walk, between the leading and trailing general tiles
