@@ -8,11 +8,13 @@ q, k, v ~ N(0, 1/8^2).  One step = one non-causal and one causal forward over
 the same resident inputs (both forms of the operator), so a step processes
 2 * B * N token-forwards.  Inputs are generated once and stay in HBM.
 
-Printed: one JSON line with the whole-job throughput, the roofline of the
-dominant kernel (algorithmic bytes per launch over its mean duration, timed
-with HIP events recorded by the library on the launch stream during the timed
-steps), the same figures at N=4096 (B=8, H=2, d=32, k=20), and the float64
-CPU oracle timed on a bounded sample of the same workload.
+Printed: one JSON line with the whole-job throughput (timed steps without
+per-kernel events), the roofline of the dominant kernel (algorithmic bytes per
+launch over its mean duration, from HIP events the library attaches to each
+dispatch on the launch stream, in a second pass over the same steps), per-form
+rates including cold calls (last-level cache evicted before each), the same
+figures at N=4096 (B=8, H=2, d=32, k=20) and at that shape with B=128, and the
+float64 CPU oracle timed on a bounded sample of the same workload.
 """
 
 from __future__ import annotations
@@ -100,7 +102,8 @@ def trace_summary(stats_csv):
                 "rank 2, then the same 50 steps with HIP events attached to every dispatch "
                 "(the per-kernel means of the bench line), then 52 calls of each form alone, "
                 "then 105 calls of the N=4096 shape (B=8 H=2 d=32 bf16 k=20 rank 2, "
-                "non-causal).\n\n")
+                "non-causal), 105 calls of that shape with B=128 (same d=32 kernels), and 11 "
+                "cold calls of each stress form.\n\n")
         f.write(f"kernel source hash: {kernel_source_hash()}\n\n")
         if timed:
             f.write("Mean traced duration over the launches of the 50 timed steps, and over "
@@ -357,6 +360,66 @@ def main():
                     for name, ms in kt4.items()},
     }
 
+    # N = 4096 with the batch scaled up (B = 128, 64 MiB per tensor): the same
+    # kernels without launch latency dominating; inputs drawn on the device
+    # from a seeded generator (no oracle comparison is made on them)
+    gen = torch.Generator(device="cuda:0")
+    gen.manual_seed(3)
+    Bs = 128
+    shp = (Bs, w4.H, w4.N, w4.d)
+    qb, kb, vb = (torch.randn(shp, generator=gen, device="cuda:0").to(torch.bfloat16)
+                  for _ in range(3))
+    wnb = torch.randn(w4.H, generator=gen, device="cuda:0")
+    wfb = torch.randn(w4.H, generator=gen, device="cuda:0")
+    ob = torch.empty_like(qb)
+    fb = lambda: binding.forward(qb, kb, vb, wnb, wfb, w4.band_k, w4.rank, 0, out=ob)
+    tb = timed(fb, args.steps, args.warmup, torch)
+    for name in binding.KERNELS:
+        binding.kernel_timing_read(name)
+    binding.kernel_timing(True)
+    timed(fb, args.steps, 0, torch)
+    binding.kernel_timing(False)
+    Xb = Bs * w4.H * w4.N * w4.d * 2
+    ktb = {}
+    for name in binding.KERNELS:
+        ms, n = binding.kernel_timing_read(name)
+        if n:
+            ktb[name] = ms / n
+    n4096_b128 = {
+        "workload": "lra4k shape with B=128: B=128 H=2 N=4096 d=32 bf16 k=20 rank=2 "
+                    "non-causal, 64 MiB per tensor",
+        "tokens_per_s": round(Bs * w4.N / tb, 1), "ms_per_call": round(tb * 1e3, 4),
+        "op_hbm_frac_4X": round(4 * Xb / tb / 1e9 / HBM_PEAK_GBS, 4),
+        "kernels": {name: {"mean_us": round(ms * 1e3, 3),
+                           **({"alg_GBps": round(b / (ms * 1e-3) / 1e9, 1),
+                               "hbm_frac": round(b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+                              if (b := {"seg_state": 2 * Xb, "band_apply": 4 * Xb}.get(name))
+                              else {})}
+                    for name, ms in ktb.items()},
+    }
+    del qb, kb, vb, ob
+
+    # cold calls: a 512 MiB write before each call evicts the 256 MB
+    # last-level cache, so every input byte comes from HBM
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda:0")
+
+    def cold(fn, n=11):
+        ts = []
+        for i in range(n):
+            scratch.fill_(i & 0xFF)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return sorted(ts)[n // 2]
+
+    c_nc = cold(lambda: binding.forward(tq, tk, tv, twn, twf, w.band_k, w.rank, 0, out=out_nc))
+    c_c = cold(lambda: binding.forward(tq, tk, tv, twn, twf, w.band_k, w.rank, 1, out=out_c))
+    del scratch
+
     tokens_per_step = 2 * w.B * w.N
     rec = {
         "metric": METRIC,
@@ -383,13 +446,16 @@ def main():
         "forms": {
             "noncausal": {"tokens_per_s": round(w.B * w.N / t_nc, 1),
                           "ms_per_call": round(t_nc * 1e3, 4),
-                          "op_hbm_frac_4X": round(4 * X / t_nc / 1e9 / HBM_PEAK_GBS, 4)},
+                          "op_hbm_frac_4X": round(4 * X / t_nc / 1e9 / HBM_PEAK_GBS, 4),
+                          "cold_ms_per_call": round(c_nc, 4)},
             "causal": {"tokens_per_s": round(w.B * w.N / t_c, 1),
                        "ms_per_call": round(t_c * 1e3, 4),
-                       "op_hbm_frac_4X": round(4 * X / t_c / 1e9 / HBM_PEAK_GBS, 4)},
+                       "op_hbm_frac_4X": round(4 * X / t_c / 1e9 / HBM_PEAK_GBS, 4),
+                       "cold_ms_per_call": round(c_c, 4)},
         },
         "kernels": per_kernel,
         "n4096": n4096,
+        "n4096_b128": n4096_b128,
         "kernel_source_hash": kernel_source_hash(),
     }
     if not args.no_cpu_baseline:
