@@ -187,8 +187,7 @@ struct PhiRows {
   }
 };
 
-// One tile of a wavefront: the strip rows i0 .. i0+15 (i0 = t0 + 16w), then
-// the state update by the tile's keys and phi of the next tile's keys.  The
+// One tile of a wavefront: the strip rows i0 .. i0+15 (i0 = t0 + 16w).  The
 // ring holds the window units [t0/32 - KC, t0/32 + 2), window unit m in ring
 // slot (m0 + m) % U; window block j (16 keys) is unit j/2, half j%2.  The
 // strip's band is window blocks w .. w + 2KC.  Exact tiles (!GENERAL: k =
@@ -204,8 +203,9 @@ struct PhiRows {
 // arithmetic of the other (scheduling fences keep the phases apart):
 //   near scores + phi(q) | softmax + far products of map 0 with the sums
 //   before the tile | P V + intra-tile products of map 0 | far products of
-//   map 1 + near normalisation and blend | state update + phi of the next
-//   tile's keys, store
+//   map 1 + near normalisation and blend, store
+// (the caller follows with the state update paired with phi of the next
+// tile's keys).
 // mid() runs once phi(q) is formed (the query octs are dead then).
 template <int D, int R, int KC, bool GENERAL, int NPAIR, class Mid>
 __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N, int band_k,
@@ -213,8 +213,7 @@ __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N,
                                           const unsigned char* kr, const unsigned char* vr,
                                           const unsigned char* phr, const RingOffsets<D>& ro,
                                           const Oct* sf, const Oct* szo, const uint2* tmask,
-                                          CausalState<D, R>& st, const RowsCopy<D, CTM, CNT>& pk,
-                                          PhiRows<D, R>& phn, Mid mid) {
+                                          Mid mid) {
   using C = CausalCfg<D, R, KC>;
   constexpr int NB = C::NB, NQ = C::NQ, NS = C::NS, RB = C::RB, U = C::U;
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
@@ -375,15 +374,6 @@ __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N,
   }
   __builtin_amdgcn_sched_barrier(0);
 
-  // ---- phase 5: the sums advance by the tile's 64 keys | phi of the next
-  // tile's keys, store
-  if (CausalState<D, R>::FT >= CW || CausalState<D, R>::active(w)) {
-    int vb[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u) vb[u] = __builtin_amdgcn_readfirstlane(((m0 + KC + u) % U) * 32 * RB);
-    st.add(phr, vr, vb, ro);
-  }
-  phn.compute(pk);
   // rows at or beyond N fall outside the output buffer and are dropped
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb)
@@ -481,10 +471,22 @@ __global__ __launch_bounds__(CNT, 2) void k_causal_strip(const bf16_t* __restric
     PhiRows<D, R> phn;
     if (w < 2)
       tile_work<D, R, KC, G, 1>(oh, t0, w, m0, N, band_k, scale2, sn, sfw, qo[0], kr, vr, phr,
-                                ro, sf, szo, tmask, st, pk, phn, mid);
+                                ro, sf, szo, tmask, mid);
     else
       tile_work<D, R, KC, G, 2>(oh, t0, w, m0, N, band_k, scale2, sn, sfw, qo[0], kr, vr, phr,
-                                ro, sf, szo, tmask, st, pk, phn, mid);
+                                ro, sf, szo, tmask, mid);
+    // the sums advance by the tile's 64 keys | phi of the next tile's keys,
+    // common to both wave classes so that the two share one basic block and
+    // the scheduler pairs the update's matrix-core products with the vector
+    // work of phi
+    __builtin_amdgcn_sched_barrier(0);
+    if (all_st || has_st) {
+      int vb[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) vb[u] = __builtin_amdgcn_readfirstlane(((m0 + KC + u) % U) * 32 * RB);
+      st.add(phr, vr, vb, ro);
+    }
+    phn.compute(pk);
     typename St::Frags fr;
     if (all_st || has_st) fr = st.pack();
     __syncthreads();  // every wave is done with tile t's LDS
