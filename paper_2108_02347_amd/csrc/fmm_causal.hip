@@ -375,9 +375,7 @@ __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N,
   __builtin_amdgcn_sched_barrier(0);
 
   // rows at or beyond N fall outside the output buffer and are dropped
-#pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
-    buf_store8(oh, 2 * ((i0 + r) * D + 16 * nb + 4 * g), quad_pack(fo[nb]));
+  store_strip<D>(oh, i0, fo);
 }
 
 // grid.x = BH * nseg (XCD-aware remap); the workgroup walks the 64-row tiles

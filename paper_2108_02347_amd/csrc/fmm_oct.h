@@ -64,11 +64,6 @@ __device__ __forceinline__ Rsrc head_rsrc(const bf16_t* p, int bytes) {
 __device__ __forceinline__ uint4 buf_load16(Rsrc rs, uint32_t off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
 }
-__device__ __forceinline__ void buf_store8(Rsrc rs, uint32_t off, const uint2& v) {
-  typedef int i32x2 __attribute__((ext_vector_type(2)));
-  const i32x2 x = {(int)v.x, (int)v.y};
-  __builtin_amdgcn_raw_buffer_store_b64(x, rs, off, 0, 0);
-}
 
 // Byte offset of 16-byte chunk c of LDS row r.  The LDS serves 64 banks of 4
 // bytes per cycle: an 8-byte read in two passes of 32 consecutive lanes, a
@@ -147,6 +142,30 @@ struct RowsCopy {
     }
   }
 };
+
+// Store a 16-row strip of output rows row0 .. row0+15 held in the MFMA output
+// layout (lane (r, g) has row r, columns 16nb + 4g .. +3 in fo[nb]) as bf16
+// with 16-byte stores: a lane-group swap exchanges the quads of column blocks
+// 2c and 2c+1 between groups g and g^1, after which lane (r, g) holds the
+// eight consecutive columns 32c + 16(g&1) + 8(g>>1) .. +7 and the four lanes
+// of a row write 64 contiguous bytes per instruction.  Rows at or beyond the
+// buffer's end are dropped.
+template <int D>
+__device__ __forceinline__ void store_strip(Rsrc oh, int row0, const f32x4* fo) {
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int c = 0; c < D / 32; ++c) {
+    const uint2 a = quad_pack(fo[2 * c]), b = quad_pack(fo[2 * c + 1]);
+    // odd lane groups of the first operand trade places with the even groups
+    // of the second
+    const auto x = __builtin_amdgcn_permlane16_swap(a.x, b.x, false, false);
+    const auto y = __builtin_amdgcn_permlane16_swap(a.y, b.y, false, false);
+    typedef int i32x4 __attribute__((ext_vector_type(4)));
+    const i32x4 o = {(int)x[0], (int)y[0], (int)x[1], (int)y[1]};
+    const int col = 32 * c + 16 * (g & 1) + 8 * (g >> 1);
+    __builtin_amdgcn_raw_buffer_store_b128(o, oh, 2 * ((row0 + r) * D + col), 0, 0);
+  }
+}
 
 // Query octs of the lane's row of NS consecutive 16-row strips:
 // qo[s][p] = q[i0 + 16s + r][32p + 8g .. +7] (zero for rows at or beyond N,

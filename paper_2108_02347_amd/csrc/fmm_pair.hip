@@ -248,16 +248,8 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
       for (int nb = 0; nb < NB; ++nb) fo[s][nb] += num[nb] * f;
     }
   // rows at or beyond N fall outside the output buffer and are dropped
-  typedef int i32x2 __attribute__((ext_vector_type(2)));
 #pragma unroll
-  for (int s = 0; s < 2; ++s)
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      const i32x2 v = {(int)pack_bf16x2(fo[s][nb][0], fo[s][nb][1]),
-                       (int)pack_bf16x2(fo[s][nb][2], fo[s][nb][3])};
-      __builtin_amdgcn_raw_buffer_store_b64(v, oh, 2 * ((i0 + 16 * s + r) * D + 16 * nb + 4 * g),
-                                            0, 0);
-    }
+  for (int s = 0; s < 2; ++s) store_strip<D>(oh, i0 + 16 * s, fo[s]);
 }
 
 // grid.x = BH * nseg (XCD-aware remap); the workgroup walks the 128-row tiles
