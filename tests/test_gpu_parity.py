@@ -195,3 +195,16 @@ def test_band_widths_across_ring_sizes(d, dtype, causal):
     for kw in (1, 31, 32, 33, 64, 65, 100, 250):
         worst = max(worst, check_full(1, 1, 3000, d, kw, 2, causal, dtype, 700 + kw))
     log(f"ring sweep d={d} {dtype} causal={causal}: worst {worst:.3e}")
+
+
+# ------------------------------------------------------------------ long walks with a ragged tail
+@pytest.mark.parametrize("causal", [0, 1])
+@pytest.mark.parametrize("d,band_k", [(64, 64), (32, 32), (64, 40)])
+def test_long_walk_ragged(d, band_k, causal):
+    # bf16, one head of N = 20037 (no multiple of any tile or segment): the
+    # causal strip kernel walks segments of 9 (d = 64) or 5 (d = 32) tiles with
+    # the running state crossing tiles, exact tiles where k = 32 ceil(k/32)
+    # and general ones at the ends, in the ragged last segment and for k = 40
+    err = check_full(1, 1, 20037, d, band_k, 2, causal, "bf16", 900 + d + band_k + causal,
+                     1.0 / np.sqrt(d))
+    log(f"long ragged walk d={d} k={band_k} causal={causal}: worst {err:.3e}")
