@@ -140,7 +140,9 @@ int fmm_attn_version(void);
 /*
  * Kernel timing (profiling aid).  fmm_attn_kernel_timing(1) makes every later
  * forward call record a pair of HIP events around each kernel it launches, on
- * the launch stream; fmm_attn_kernel_timing(0) stops recording.
+ * the launch stream (attached to the kernel's own dispatch; each such launch
+ * then carries a completion signal, which adds a few microseconds between
+ * kernels); fmm_attn_kernel_timing(0) stops recording.
  * fmm_attn_kernel_timing_read waits for the recorded events, writes the total
  * elapsed milliseconds and the number of launches of kernel `kernel`
  * (FMM_KERNEL_*) since the last read, and clears that kernel's record.

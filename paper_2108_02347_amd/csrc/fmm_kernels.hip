@@ -18,6 +18,11 @@
 //   k_band_rounds,   the same two operators for bands wider than the ring: every
 //   k_causal_rounds  tile stages its key window in rounds
 //
+// bf16 heads of width 32 or 64 with band half-widths up to 64 take the strip
+// kernels of fmm_pair.hip (non-causal, two 16-row strips per wavefront) and
+// fmm_causal.hip (causal); the ring and rounds kernels here serve every other
+// case (fp32 storage, d = 16, wider bands).
+//
 // Every workgroup of the apply kernels has NW = 4 wavefronts; wave w owns query
 // rows [16w, 16w+16) of a TM = 64-row tile.  All sums are accumulated in fp32
 // in a fixed order, so results are bit-reproducible run to run.
