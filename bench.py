@@ -175,12 +175,19 @@ def traffic_summary(kernel, fetch_csv, write_csv, cfetch_csv, cwrite_csv):
 
 
 def kernel_source_hash() -> str:
+    """Hash of the kernel sources with comments and blank space removed, so a
+    comment edit does not void counter summaries taken with the same code."""
+    import re
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2108_02347_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
-        with open(os.path.join(csrc, name), "rb") as f:
-            h.update(name.encode())
-            h.update(f.read())
+        with open(os.path.join(csrc, name), encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        text = " ".join(text.split())
+        h.update(name.encode())
+        h.update(text.encode())
     return h.hexdigest()[:16]
 
 
