@@ -896,6 +896,9 @@ template <bool CAUSAL>
 __global__ __launch_bounds__(256) void k_state_combine(float* __restrict__ part,
                                                        float* __restrict__ fin, int nseg,
                                                        int rec) {
+  // the causal scan keeps the first CACHE values of its range in registers
+  // between the two passes, so each record is read from memory once
+  constexpr int CACHE = CAUSAL ? 32 : 1;
   __shared__ float tot[4][64];
   const int el = threadIdx.x & 63, qr = threadIdx.x >> 6;
   const int e = blockIdx.x * 64 + el, bh = blockIdx.y;
@@ -903,14 +906,24 @@ __global__ __launch_bounds__(256) void k_state_combine(float* __restrict__ part,
   const int s0 = min(nseg, qr * per), s1 = min(nseg, s0 + per);
   float* p = part + (size_t)bh * nseg * rec + e;
   float s = 0.f;
+  float keep[CACHE];
   if (e < rec) {
-    int j = s0;
-    for (; j + 4 <= s1; j += 4) {
-      const float a0 = p[(size_t)j * rec], a1 = p[(size_t)(j + 1) * rec];
-      const float a2 = p[(size_t)(j + 2) * rec], a3 = p[(size_t)(j + 3) * rec];
-      s += a0; s += a1; s += a2; s += a3;
+    if constexpr (CAUSAL) {
+#pragma unroll
+      for (int jj = 0; jj < CACHE; ++jj) {
+        keep[jj] = s0 + jj < s1 ? p[(size_t)(s0 + jj) * rec] : 0.f;
+        if (s0 + jj < s1) s += keep[jj];
+      }
+      for (int j = s0 + CACHE; j < s1; ++j) s += p[(size_t)j * rec];
+    } else {
+      int j = s0;
+      for (; j + 4 <= s1; j += 4) {
+        const float a0 = p[(size_t)j * rec], a1 = p[(size_t)(j + 1) * rec];
+        const float a2 = p[(size_t)(j + 2) * rec], a3 = p[(size_t)(j + 3) * rec];
+        s += a0; s += a1; s += a2; s += a3;
+      }
+      for (; j < s1; ++j) s += p[(size_t)j * rec];
     }
-    for (; j < s1; ++j) s += p[(size_t)j * rec];
   }
   tot[qr][el] = s;
   __syncthreads();
@@ -920,7 +933,14 @@ __global__ __launch_bounds__(256) void k_state_combine(float* __restrict__ part,
   } else {
     float run = 0.f;
     for (int q2 = 0; q2 < qr; ++q2) run += tot[q2][el];
-    for (int j = s0; j < s1; ++j) {
+#pragma unroll
+    for (int jj = 0; jj < CACHE; ++jj) {
+      if (s0 + jj < s1) {
+        p[(size_t)(s0 + jj) * rec] = run;
+        run += keep[jj];
+      }
+    }
+    for (int j = s0 + CACHE; j < s1; ++j) {
       const float t = p[(size_t)j * rec];
       p[(size_t)j * rec] = run;
       run += t;
