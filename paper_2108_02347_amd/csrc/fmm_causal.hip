@@ -194,9 +194,12 @@ struct PhiRows {
 // 32*KC and the whole window inside [0, N)) cut only the first block (keys
 // below i - k) and the last (keys above i) and start those score products from
 // -inf biases; GENERAL tiles mask every block against the band clipped to
-// [0, N).  The intra-tile product covers tile blocks 0 .. w in NPAIR = w/2 + 1
-// block pairs; the last pair's masks (lower-triangular diagonal block, and
-// the block after it empty for even w) are tmask.
+// [0, N).  The intra-tile product runs over the tile's four blocks in two
+// pairs for every strip, tmask[j] masking tile block j: kept below the
+// strip's own block w, lower-triangular on it, empty above it (the strips of
+// the tile's first half thus spend products on an empty pair, which keeps
+// every wavefront on one straight-line path; they would otherwise wait for
+// the others at the next barrier).
 //
 // The near and far parts are independent until the blend, so the work runs
 // as phases that pair matrix-core products of one part with vector
@@ -207,7 +210,7 @@ struct PhiRows {
 // (the caller follows with the state update paired with phi of the next
 // tile's keys).
 // mid() runs once phi(q) is formed (the query octs are dead then).
-template <int D, int R, int KC, bool GENERAL, int NPAIR, class Mid>
+template <int D, int R, int KC, bool GENERAL, class Mid>
 __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N, int band_k,
                                           float scale2, float sn, float sfw, const Oct* qo,
                                           const unsigned char* kr, const unsigned char* vr,
@@ -307,7 +310,7 @@ __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N,
   auto far_intra = [&](int l, f32x4* num) {
     const unsigned char* pl = phr + l * CTM * RB;
 #pragma unroll
-    for (int c = 0; c < NPAIR; ++c) {
+    for (int c = 0; c < 2; ++c) {
       f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int p = 0; p < NQ; ++p) {
@@ -316,10 +319,8 @@ __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N,
                   a1);
       }
       uint2 q0 = quad_pack(a0), q1 = quad_pack(a1);
-      if (c == NPAIR - 1) {
-        q0.x &= tmask[0].x; q0.y &= tmask[0].y;
-        q1.x &= tmask[1].x; q1.y &= tmask[1].y;
-      }
+      q0.x &= tmask[2 * c].x; q0.y &= tmask[2 * c].y;
+      q1.x &= tmask[2 * c + 1].x; q1.y &= tmask[2 * c + 1].y;
       const Oct ac = oct_of(q0, q1);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
@@ -444,18 +445,18 @@ __global__ __launch_bounds__(CNT, 2) void k_causal_strip(const bf16_t* __restric
   pk.load(kh, (ua0 + U) * 32, ntile > 1);
   pv.load(vh, (ua0 + U) * 32, ntile > 1);
 
-  // one tile, then the sums advance, the ring slides by the prefetched units
-  // and their phi rows replace the tile's (past the last tile the loads and
-  // stores are harmless no-ops on zeros, and the sums are not read again)
-  // masks of the last block pair of the intra-tile product
-  uint2 tmask[2];
+  // masks of the four tile blocks in this strip's intra-tile product: keys
+  // below the strip's block kept, its own block lower-triangular (key 4g + i
+  // <= row r), the blocks above empty
+  uint2 tmask[4];
   {
     const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
     uint2 dm;
     dm.x = (4 * g <= r ? 0xffffu : 0u) | (4 * g + 1 <= r ? 0xffff0000u : 0u);
     dm.y = (4 * g + 2 <= r ? 0xffffu : 0u) | (4 * g + 3 <= r ? 0xffff0000u : 0u);
-    tmask[0] = (w & 1) ? make_uint2(~0u, ~0u) : dm;
-    tmask[1] = (w & 1) ? dm : make_uint2(0u, 0u);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      tmask[j] = j < w ? make_uint2(~0u, ~0u) : j == w ? dm : make_uint2(0u, 0u);
   }
   // one tile, then the ring slides by the prefetched units and their phi rows
   // replace the tile's (past the last tile the loads and stores are harmless
@@ -467,16 +468,10 @@ __global__ __launch_bounds__(CNT, 2) void k_causal_strip(const bf16_t* __restric
     const int m0 = 2 * t;
     auto mid = [&]() { load_qo<D, 1>(qh, t0 + CTM + 16 * w, t + 1 < ntile, qo); };
     PhiRows<D, R> phn;
-    if (w < 2)
-      tile_work<D, R, KC, G, 1>(oh, t0, w, m0, N, band_k, scale2, sn, sfw, qo[0], kr, vr, phr,
-                                ro, sf, szo, tmask, mid);
-    else
-      tile_work<D, R, KC, G, 2>(oh, t0, w, m0, N, band_k, scale2, sn, sfw, qo[0], kr, vr, phr,
-                                ro, sf, szo, tmask, mid);
-    // the sums advance by the tile's 64 keys | phi of the next tile's keys,
-    // common to both wave classes so that the two share one basic block and
-    // the scheduler pairs the update's matrix-core products with the vector
-    // work of phi
+    tile_work<D, R, KC, G>(oh, t0, w, m0, N, band_k, scale2, sn, sfw, qo[0], kr, vr, phr, ro,
+                           sf, szo, tmask, mid);
+    // the sums advance by the tile's 64 keys | phi of the next tile's keys:
+    // the update's matrix-core products paired with the vector work of phi
     __builtin_amdgcn_sched_barrier(0);
     if (all_st || has_st) {
       int vb[2];
