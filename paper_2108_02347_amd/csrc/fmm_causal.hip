@@ -134,28 +134,20 @@ struct CausalState {
   // z_l[32p + 8g + {0..7}].
   __device__ __forceinline__ static void store(int w, const Frags& f, Oct* sf, Oct* szo) {
     const int lane = threadIdx.x & 63, e = lane & 15, g = lane >> 4;
-    const bool odd = g & 1;
-    if constexpr (AG == 2) {  // both halves of each oct: one 16-byte store
-      int l, p, h;
-      tile_of(w, 0, l, p, h);
+    // tile h holds the first half of lane (e, g)'s oct when (g & 1) == h: each
+    // half goes to its place with an 8-byte store (no lane-dependent select)
 #pragma unroll
-      for (int eb = 0; eb <= NB; ++eb) {
-        const uint2 x = f.q[0][eb], y = f.q[1][eb];
-        const Oct o = odd ? oct_of(y, x) : oct_of(x, y);
-        if (eb < NB) sf[((l * NB + eb) * NQ + p) * 64 + lane] = o;
-        else if (e == 0) szo[(l * NQ + p) * 4 + g] = o;
-      }
-    } else {
+    for (int a = 0; a < AG; ++a) {
       int l, p, h;
-      tile_of(w, 0, l, p, h);
+      tile_of(w, a, l, p, h);
       const int hb = 8 * ((g & 1) ^ h);
 #pragma unroll
       for (int eb = 0; eb < NB; ++eb)
         *reinterpret_cast<uint2*>(reinterpret_cast<unsigned char*>(
-                                      sf + ((l * NB + eb) * NQ + p) * 64 + lane) + hb) = f.q[0][eb];
+                                      sf + ((l * NB + eb) * NQ + p) * 64 + lane) + hb) = f.q[a][eb];
       if (e == 0)
         *reinterpret_cast<uint2*>(reinterpret_cast<unsigned char*>(szo + (l * NQ + p) * 4 + g) +
-                                  hb) = f.q[0][NB];
+                                  hb) = f.q[a][NB];
     }
   }
 };
