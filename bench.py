@@ -30,6 +30,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+MFMA_PEAK_TFS = 2500.0  # MI355X dense bf16 matrix peak, published
 METRIC = "FMM attention fwd tokens/sec at N=4096 & 65536; % of HBM roofline"
 
 
@@ -49,6 +50,9 @@ def parse():
                    help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE counter CSVs of the "
                         "profile-only run and of the copy calibration into the traffic "
                         "summary under profiles/ (no GPU needed)")
+    p.add_argument("--counter-summary", metavar="COUNTER_CSV",
+                   help="turn a rocprofv3 --pmc run of the profile-only mode with the MFMA and "
+                        "VALU counters into profiles/sq_counters_stress64k.txt (no GPU needed)")
     p.add_argument("--trace-summary", metavar="KERNEL_STATS_CSV",
                    help="turn the kernel_stats.csv of a rocprofv3 --kernel-trace --stats run "
                         "of this benchmark into profiles/kernel_trace_stress64k.md")
@@ -174,6 +178,78 @@ def traffic_summary(kernel, fetch_csv, write_csv, cfetch_csv, cwrite_csv):
     print(path)
 
 
+SQ_COUNTERS = ("SQ_INSTS_MFMA", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES",
+               "SQ_BUSY_CYCLES", "SQ_INSTS_VALU", "SQ_ACTIVE_INST_VALU", "SQ_WAVE_CYCLES",
+               "GRBM_GUI_ACTIVE")
+
+
+def counter_summary(counter_csv):
+    """Per-dispatch medians of the SQ counters for the stress64k kernels, with
+    the MFMA work they imply: flops = SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512 (each
+    v_mfma_f32_16x16x32_bf16 counts 32 units of 512 flops), and the share of
+    SIMD cycles the matrix cores were busy = SQ_VALU_MFMA_BUSY_CYCLES (summed
+    over all SIMDs) / (GRBM_GUI_ACTIVE / 8 XCDs x 1024 SIMDs)."""
+    import csv
+    import statistics
+    vals = {}
+    for row in csv.DictReader(open(counter_csv)):
+        name = _short_kernel_name(row["Kernel_Name"])
+        vals.setdefault(name, {}).setdefault(row["Counter_Name"], []).append(
+            float(row["Counter_Value"]))
+    path = os.path.join(ROOT, "profiles", "sq_counters_stress64k.txt")
+    with open(path, "w") as f:
+        f.write("# SQ counters of the stress64k kernels (B=1 H=8 N=65536 d=64 bf16, k=64, "
+                "rank 2), per dispatch (median)\n")
+        f.write("# command (repo root on one MI355X, cd /tmp && export TMPDIR=/tmp first):\n")
+        f.write("#   rocprofv3 --pmc " + " ".join(SQ_COUNTERS) + " -f csv -d <out> -o p -- "
+                "python3 <repo>/bench.py --profile-only --steps 5 --warmup 1\n")
+        f.write("# mfma_flops = SQ_INSTS_VALU_MFMA_MOPS_BF16 * 512; mfma_busy_frac = "
+                "SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / 8 * 1024)\n")
+        f.write(f"kernel_source_hash: {kernel_source_hash()}\n")
+        for key, needle in STRESS_KERNELS.items():
+            hit = [n for n in vals if needle in n]
+            if not hit:
+                continue
+            c = {k: statistics.median(v) for k, v in vals[hit[0]].items()}
+            f.write(f"\n[{key}] {needle}\n")
+            f.write(f"dispatches: {len(vals[hit[0]].get('SQ_INSTS_MFMA', []))}\n")
+            for k in SQ_COUNTERS:
+                if k in c:
+                    f.write(f"{k}: {c[k]:.0f}\n")
+            if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in c:
+                f.write(f"mfma_flops: {c['SQ_INSTS_VALU_MFMA_MOPS_BF16'] * 512:.0f}\n")
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in c and c.get("GRBM_GUI_ACTIVE"):
+                busy = c["SQ_VALU_MFMA_BUSY_CYCLES"] / (c["GRBM_GUI_ACTIVE"] / 8 * 1024)
+                f.write(f"mfma_busy_frac: {busy:.4f}\n")
+    print(path)
+
+
+def read_counters(kernel: str):
+    """mfma_flops per launch from the committed counter summary, if it was
+    taken with the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "sq_counters_stress64k.txt")
+    if not os.path.exists(path):
+        return None
+    cur, head, out = None, {}, {}
+    for line in open(path):
+        line = line.strip()
+        if line.startswith("#") or not line:
+            continue
+        if line.startswith("["):
+            cur = line[1:line.index("]")]
+            out[cur] = {}
+            continue
+        a, b = (x.strip() for x in line.split(":", 1))
+        (out[cur] if cur else head)[a] = b
+    if head.get("kernel_source_hash") != kernel_source_hash() or kernel not in out:
+        return None
+    try:
+        return {"mfma_flops": float(out[kernel]["mfma_flops"]),
+                "mfma_busy_frac": float(out[kernel].get("mfma_busy_frac", "nan"))}
+    except (KeyError, ValueError):
+        return None
+
+
 def kernel_source_hash() -> str:
     """Hash of the kernel sources with comments and blank space removed, so a
     comment edit does not void counter summaries taken with the same code."""
@@ -267,6 +343,9 @@ def main():
     if args.trace_summary:
         trace_summary(args.trace_summary)
         return
+    if args.counter_summary:
+        counter_summary(args.counter_summary)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); the operator "
               "is single-GPU in this build, see DESIGN.md for how it would shard.",
@@ -322,6 +401,14 @@ def main():
                    "hbm_frac": round(alg_bytes[name] / (kt[name] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
                   if name in alg_bytes else {})}
         for name in kt if kt[name]}
+    # matrix-core work from the committed SQ counter summary (same sources)
+    for name, rec_k in per_kernel.items():
+        cnt = read_counters(name)
+        if cnt and kt.get(name):
+            tf = cnt["mfma_flops"] / (kt[name] * 1e-3) / 1e12
+            rec_k["mfma_tflops"] = round(tf, 1)
+            rec_k["mfma_frac_of_bf16_peak"] = round(tf / MFMA_PEAK_TFS, 4)
+            rec_k["mfma_busy_frac"] = cnt["mfma_busy_frac"]
     # dominant kernel: the largest time share per step (seg_state runs twice)
     share = {"band_apply": kt["band_apply"], "causal_apply": kt["causal_apply"],
              "seg_state": 2 * kt["seg_state"]}
