@@ -208,3 +208,24 @@ def test_long_walk_ragged(d, band_k, causal):
     err = check_full(1, 1, 20037, d, band_k, 2, causal, "bf16", 900 + d + band_k + causal,
                      1.0 / np.sqrt(d))
     log(f"long ragged walk d={d} k={band_k} causal={causal}: worst {err:.3e}")
+
+
+# ------------------------------------------------------------------ seeded random configurations
+def test_random_configurations():
+    # configurations drawn from a fixed seed across every dimension the ABI
+    # accepts (batch, heads, length, width, band, rank, form, storage), so
+    # that combinations the structured sweeps above do not name are checked too
+    rng = np.random.default_rng(2024)
+    worst = {"f32": 0.0, "bf16": 0.0}
+    for _ in range(24):
+        B, H = int(rng.integers(1, 4)), int(rng.integers(1, 5))
+        N = int(rng.integers(1, 2500))
+        d = int(rng.choice([16, 32, 64]))
+        kw = int(rng.integers(0, 160))
+        rank = int(rng.integers(1, 3))
+        causal = int(rng.integers(0, 2))
+        dtype = str(rng.choice(["f32", "bf16"]))
+        seed = int(rng.integers(0, 1 << 30))
+        err = check_full(B, H, N, d, kw, rank, causal, dtype, seed, 1.0 / np.sqrt(d))
+        worst[dtype] = max(worst[dtype], err)
+    log(f"random configurations: worst f32 {worst['f32']:.3e}, bf16 {worst['bf16']:.3e}")
