@@ -61,7 +61,7 @@ def parse():
 
 # library kernel id -> gfx950 kernel of the stress64k workload (bf16, d=64, rank 2)
 STRESS_KERNELS = {
-    "seg_state": "k_seg_state<unsigned short, 64, 2>",
+    "seg_state": "k_seg_state<unsigned short, 64, 2, 64>",
     "band_apply": "k_band_pair<64, 2, 2>",
     "causal_apply": "k_causal_strip<64, 2, 2>",
 }

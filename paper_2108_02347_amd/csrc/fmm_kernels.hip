@@ -757,20 +757,21 @@ struct StateTiles {
 
 // ------------------------------------------------------------------ k_seg_state
 // grid.x = nseg * BH (segment fastest), 8 waves.  Segment s of head bh covers
-// rows [s*L, min(N, s*L + L)), walked in chunks of 64 keys double-buffered in
+// rows [s*L, min(N, s*L + L)), walked in chunks of TK keys double-buffered in
 // LDS, the next chunk's loads in flight during compute.  Waves sharing a
 // feature block split the 32-key units and are summed in a fixed tree at the
-// end.  Output: the segment's tile-order state record.
+// end.  Output: the segment's tile-order state record.  TK is 64 or, for long
+// segments, 32 units per wave sharing a feature block (128 keys at d = 32,
+// 256 at d = 16), which keeps every wave busy and more bytes in flight.
 constexpr int SW = 8;          // waves in k_seg_state
 constexpr int SNT = SW * 64;
-template <typename T, int D, int R>
+template <typename T, int D, int R, int TK>
 __global__ __launch_bounds__(SNT) void k_seg_state(const T* __restrict__ k,
                                                    const T* __restrict__ v,
                                                    float* __restrict__ part, int N, int L,
                                                    int nseg) {
   constexpr int NB = D / 16;
   constexpr int ST = D + Lay<T>::PAD;
-  constexpr int TK = 64;
   // waves are laid out as (rs, cb): cb = w % NB, rs = w / NB splits the units
   constexpr int RS = SW / NB;
   __shared__ __attribute__((aligned(16))) T s_kv[2][2][TK * ST];  // [buffer][K, V]
@@ -1341,8 +1342,14 @@ static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
   }();
   if (lds_attr != hipSuccess) return lds_attr;
 
-  launch_timed(timer, FMM_KERNEL_SEG_STATE, k_seg_state<T, D, R>, dim3(a.nseg * BH), dim3(SNT), 0, s,
-         k, v, part, a.N, a.L, a.nseg);
+  // long chunks once a segment spans at least four of them
+  constexpr int TKL = 32 * (SW / (D / 16));
+  if (TKL > 64 && a.L >= 4 * TKL)
+    launch_timed(timer, FMM_KERNEL_SEG_STATE, k_seg_state<T, D, R, TKL>, dim3(a.nseg * BH),
+                 dim3(SNT), 0, s, k, v, part, a.N, a.L, a.nseg);
+  else
+    launch_timed(timer, FMM_KERNEL_SEG_STATE, k_seg_state<T, D, R, 64>, dim3(a.nseg * BH),
+                 dim3(SNT), 0, s, k, v, part, a.N, a.L, a.nseg);
   if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
 
   const dim3 cgrid((REC + 63) / 64, BH);

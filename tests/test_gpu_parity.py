@@ -85,6 +85,13 @@ def test_many_segments_and_heads():
             check_full(3, 2, 2500, 32, 7, 2, causal, dtype, 500 + causal)
 
 
+@pytest.mark.parametrize("causal", [0, 1])
+def test_hundreds_of_segments(causal):
+    # one narrow slice split into a few hundred 128-row state segments, so a
+    # combine thread's range is longer than the records it holds in registers
+    check_full(1, 1, 40000, 16, 8, 2, causal, "f32", 520 + causal)
+
+
 # ------------------------------------------------------------------ parts isolated by the blend
 @pytest.mark.parametrize("causal", [0, 1])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
