@@ -64,9 +64,13 @@ struct CausalState {
   f32x4 acc[AG][NB + 1];
   int aoff[AG];  // transposed phi-row read of each tile (lane offset, map base)
 
+  // Wavefronts beyond the FT tiles (d = 32, rank 1) repeat the first ones:
+  // they load, update and pack their copies like the owners, so no branch
+  // separates the update's matrix-core products from the vector code that
+  // follows, and only their fragment stores are skipped.
   __device__ __forceinline__ static bool active(int w) { return w * AG < FT; }
   __device__ __forceinline__ static void tile_of(int w, int a, int& l, int& p, int& h) {
-    const int ft = w * AG + a;
+    const int ft = (w * AG + a) % FT;
     h = ft & 1;
     p = (ft >> 1) % NQ;
     l = (ft >> 1) / NQ;
@@ -93,28 +97,18 @@ struct CausalState {
     }
   }
 
-  // acc += phi_l(K)^T [V | 1] over the tile's 64 keys: phi rows at phr, the
-  // tile's two V units at ring byte offsets vb[0], vb[1].
-  __device__ __forceinline__ void add(const unsigned char* phr, const unsigned char* vr,
-                                      const int* vb, const RingOffsets<D>& ro) {
+  // acc += phi_l(K_u)^T [V_u | 1] over key unit u (32 keys) of the tile: phi
+  // rows at phr, vt[eb] the unit's V^T octs (columns 16eb .. 16eb+15).
+  __device__ __forceinline__ void add_unit(const unsigned char* phr, int u, const Oct* vt) {
     constexpr int RB = RingRows<D>::RB;
     const Oct ones = oct_ones();
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      Oct vt[NB];
+    for (int a = 0; a < AG; ++a) {
+      const unsigned char* pp = phr + 32 * u * RB + aoff[a];
+      const Oct ao = oct_of(ld_tr16(pp), ld_tr16(pp + 16 * RB));
 #pragma unroll
-      for (int eb = 0; eb < NB; ++eb) {
-        const unsigned char* vp = vr + vb[u] + ro.voff[eb];
-        vt[eb] = oct_of(ld_tr16(vp), ld_tr16(vp + 16 * RB));
-      }
-#pragma unroll
-      for (int a = 0; a < AG; ++a) {
-        const unsigned char* pp = phr + 32 * u * RB + aoff[a];
-        const Oct ao = oct_of(ld_tr16(pp), ld_tr16(pp + 16 * RB));
-#pragma unroll
-        for (int eb = 0; eb < NB; ++eb) acc[a][eb] = mma8(ao, vt[eb], acc[a][eb]);
-        acc[a][NB] = mma8(ao, ones, acc[a][NB]);
-      }
+      for (int eb = 0; eb < NB; ++eb) acc[a][eb] = mma8(ao, vt[eb], acc[a][eb]);
+      acc[a][NB] = mma8(ao, ones, acc[a][NB]);
     }
   }
 
@@ -202,13 +196,13 @@ struct PhiRows {
 // (the caller follows with the state update paired with phi of the next
 // tile's keys).
 // mid() runs once phi(q) is formed (the query octs are dead then).
-template <int D, int R, int KC, bool GENERAL, class Mid>
+template <int D, int R, int KC, bool GENERAL, class Mid, class Unit, class Late>
 __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N, int band_k,
                                           float scale2, float sn, float sfw, const Oct* qo,
                                           const unsigned char* kr, const unsigned char* vr,
                                           const unsigned char* phr, const RingOffsets<D>& ro,
                                           const Oct* sf, const Oct* szo, const uint2* tmask,
-                                          Mid mid) {
+                                          Mid mid, Unit unit, Late late) {
   using C = CausalCfg<D, R, KC>;
   constexpr int NB = C::NB, NQ = C::NQ, NS = C::NS, RB = C::RB, U = C::U;
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
@@ -285,53 +279,26 @@ __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N,
     }
     pq[NS] = make_uint2(0u, 0u);
   }
-  // far products of map l: sums before the tile (Eq. (9) numerator and
-  // denominator), then the tile's keys t0 .. i (tile blocks 0 .. w, block w
-  // lower-triangular)
-  auto far_prefix = [&](int l, f32x4* num) {
+  // far products of both maps with the sums before the tile (Eq. (9)
+  // numerator and denominator)
+  f32x4 num[R][NB + 1];
 #pragma unroll
-    for (int nb = 0; nb <= NB; ++nb) num[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int l = 0; l < R; ++l) {
+#pragma unroll
+    for (int nb = 0; nb <= NB; ++nb) num[l][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int p = 0; p < NQ; ++p) {
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
-        num[nb] = mma8(sf[((l * NB + nb) * NQ + p) * 64 + lane], ph[l][p], num[nb]);
-      num[NB] = mma8(szo[(l * NQ + p) * 4 + g], ph[l][p], num[NB]);
+        num[l][nb] = mma8(sf[((l * NB + nb) * NQ + p) * 64 + lane], ph[l][p], num[l][nb]);
+      num[l][NB] = mma8(szo[(l * NQ + p) * 4 + g], ph[l][p], num[l][NB]);
     }
-  };
-  auto far_intra = [&](int l, f32x4* num) {
-    const unsigned char* pl = phr + l * CTM * RB;
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int p = 0; p < NQ; ++p) {
-        a0 = mma8(*reinterpret_cast<const Oct*>(pl + 32 * c * RB + ro.koff[p]), ph[l][p], a0);
-        a1 = mma8(*reinterpret_cast<const Oct*>(pl + (32 * c + 16) * RB + ro.koff[p]), ph[l][p],
-                  a1);
-      }
-      uint2 q0 = quad_pack(a0), q1 = quad_pack(a1);
-      q0.x &= tmask[2 * c].x; q0.y &= tmask[2 * c].y;
-      q1.x &= tmask[2 * c + 1].x; q1.y &= tmask[2 * c + 1].y;
-      const Oct ac = oct_of(q0, q1);
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-        num[nb] = mma8(oct_of(ld_tr16(vr + tb[2 * c] + ro.voff[nb]),
-                              ld_tr16(vr + tb[2 * c + 1] + ro.voff[nb])),
-                       ac, num[nb]);
-      num[NB] = mma8(ones, ac, num[NB]);
-    }
-  };
-  auto far_blend = [&](const f32x4* num, f32x4* fo) {
-    const float f = sfw > 0.f ? sfw * fast_rcp(num[NB][0]) : 0.f;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) fo[nb] += num[nb] * f;
-  };
-  f32x4 num0[NB + 1];
-  far_prefix(0, num0);
+  }
   __builtin_amdgcn_sched_barrier(0);
 
-  // ---- phase 3: O^T = V^T P^T and the row sums | intra-tile scores of map 0
+  // ---- phase 3: O^T = V^T P^T and the row sums | intra-tile scores
+  // phi_l(K) phi_l(q)^T of both maps over the tile's blocks in two pairs,
+  // masked to keys t0 .. i (tile blocks 0 .. w, block w lower-triangular)
   f32x4 o[NB + 1];
 #pragma unroll
   for (int nb = 0; nb <= NB; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -347,23 +314,58 @@ __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N,
     }
     o[NB] = mma8(ones, pc, o[NB]);
   }
-  far_intra(0, num0);
+  Oct ac[R][2];
+#pragma unroll
+  for (int l = 0; l < R; ++l) {
+    const unsigned char* pl = phr + l * CTM * RB;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int p = 0; p < NQ; ++p) {
+        a0 = mma8(*reinterpret_cast<const Oct*>(pl + 32 * c * RB + ro.koff[p]), ph[l][p], a0);
+        a1 = mma8(*reinterpret_cast<const Oct*>(pl + (32 * c + 16) * RB + ro.koff[p]), ph[l][p],
+                  a1);
+      }
+      uint2 q0 = quad_pack(a0), q1 = quad_pack(a1);
+      q0.x &= tmask[2 * c].x; q0.y &= tmask[2 * c].y;
+      q1.x &= tmask[2 * c + 1].x; q1.y &= tmask[2 * c + 1].y;
+      ac[l][c] = oct_of(q0, q1);
+    }
+  }
   __builtin_amdgcn_sched_barrier(0);
 
-  // ---- phase 4: far products of the other map | near normalisation, blend
-  // of map 0
+  // ---- phase 4: per key unit c of the tile, its V^T octs are read once and
+  // feed the intra-tile far products of both maps and the running sums'
+  // update (the caller's) | phi of the next tile's keys (the caller's),
+  // near normalisation, blend
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    Oct vt[NB];
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+      vt[nb] = oct_of(ld_tr16(vr + tb[2 * c] + ro.voff[nb]),
+                      ld_tr16(vr + tb[2 * c + 1] + ro.voff[nb]));
+#pragma unroll
+    for (int l = 0; l < R; ++l) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) num[l][nb] = mma8(vt[nb], ac[l][c], num[l][nb]);
+      num[l][NB] = mma8(ones, ac[l][c], num[l][NB]);
+    }
+    unit(c, vt);
+  }
+  late();
   f32x4 fo[NB];
   {
     const float a = sn > 0.f ? sn * fast_rcp(o[NB][0]) : 0.f;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) fo[nb] = o[nb] * a;
   }
-  far_blend(num0, fo);
-  if constexpr (R == 2) {
-    f32x4 num1[NB + 1];
-    far_prefix(1, num1);
-    far_intra(1, num1);
-    far_blend(num1, fo);
+#pragma unroll
+  for (int l = 0; l < R; ++l) {
+    const float f = sfw > 0.f ? sfw * fast_rcp(num[l][NB][0]) : 0.f;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) fo[nb] += num[l][nb] * f;
   }
   __builtin_amdgcn_sched_barrier(0);
 
@@ -411,7 +413,7 @@ __global__ __launch_bounds__(CNT, 2) void k_causal_strip(const bf16_t* __restric
   const bool has_st = St::active(w);
 
   St st;
-  if (all_st || has_st) st.load(w, prefix + ((size_t)bh * nseg + seg) * R * D * (D + 1));
+  st.load(w, prefix + ((size_t)bh * nseg + seg) * R * D * (D + 1));
   using RC = RowsCopy<D, CTM, CNT>;
 #pragma unroll
   for (int x = 0; x < U; x += 2) {
@@ -460,20 +462,14 @@ __global__ __launch_bounds__(CNT, 2) void k_causal_strip(const bf16_t* __restric
     const int m0 = 2 * t;
     auto mid = [&]() { load_qo<D, 1>(qh, t0 + CTM + 16 * w, t + 1 < ntile, qo); };
     PhiRows<D, R> phn;
+    // the sums advance by the tile's 64 keys inside the tile's last phase,
+    // which hands over each key unit's V^T octs; phi of the next tile's keys
+    // is formed there too, beside the matrix-core products
+    auto unit = [&](int c, const Oct* vt) { st.add_unit(phr, c, vt); };
+    auto late = [&]() { phn.compute(pk); };
     tile_work<D, R, KC, G>(oh, t0, w, m0, N, band_k, scale2, sn, sfw, qo[0], kr, vr, phr, ro,
-                           sf, szo, tmask, mid);
-    // the sums advance by the tile's 64 keys | phi of the next tile's keys:
-    // the update's matrix-core products paired with the vector work of phi
-    __builtin_amdgcn_sched_barrier(0);
-    if (all_st || has_st) {
-      int vb[2];
-#pragma unroll
-      for (int u = 0; u < 2; ++u) vb[u] = __builtin_amdgcn_readfirstlane(((m0 + KC + u) % U) * 32 * RB);
-      st.add(phr, vr, vb, ro);
-    }
-    phn.compute(pk);
-    typename St::Frags fr;
-    if (all_st || has_st) fr = st.pack();
+                           sf, szo, tmask, mid, unit, late);
+    const typename St::Frags fr = st.pack();
     __syncthreads();  // every wave is done with tile t's LDS
     auto slot = [=](int j) { return (m0 + j) % U; };
     pk.store(kr, slot);

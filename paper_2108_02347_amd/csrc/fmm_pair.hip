@@ -82,11 +82,12 @@ __device__ __forceinline__ void pair_frags(const float* __restrict__ rec, Oct* s
 // strip cut by the band (triangles); GENERAL tiles mask every block against
 // the row's band clipped to [0, N).
 //
-// The work runs as phases that pair matrix-core products of one strip with
-// vector arithmetic of the other (scheduling fences keep the phases apart):
-//   scores A | scores B + softmax A | P V of A + softmax B |
-//   P V of B + phi(q) | far products + near normalisation | blend, store
-// mid() runs between the near and far phases, once phi(q) is formed.
+// Every LDS operand is read once per wavefront and feeds both strips.  The
+// work runs as phases that pair matrix-core products with independent vector
+// arithmetic (scheduling fences keep the phases apart):
+//   scores of A and B + phi(q) | softmax of A and B + far products |
+//   P V of A and B + near normalisation, blend, store
+// mid() runs after the first phase, once phi(q) is formed.
 template <int D, int R, int KC, bool GENERAL, class Mid>
 __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
                                           float scale2, float sn, float sfw, Oct (*qo)[D / 32],
@@ -112,22 +113,6 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
     bias_lo[i] = (!GENERAL && 4 * g + i < r) ? -INFINITY : 0.f;
     bias_hi[i] = (!GENERAL && 4 * g + i > r) ? -INFINITY : 0.f;
   }
-  // S^T = K Q^T for blocks s .. s + NS - 1 of strip s
-  auto scores = [&](int s, f32x4* sc) {
-#pragma unroll
-    for (int j = 0; j < NS; ++j) {
-      const int b = j + s;
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      if constexpr (!GENERAL) acc = j == 0 ? bias_lo : j == NS - 1 ? bias_hi : acc;
-#pragma unroll
-      for (int p = 0; p < NQ; ++p) {
-        const Oct ko = *reinterpret_cast<const Oct*>(kr + ubase[b >> 1] + ro.koff[p] +
-                                                     16 * RingRows<D>::RB * (b & 1));
-        acc = mma8(ko, qo[s][p], acc);
-      }
-      sc[j] = acc;
-    }
-  };
   // band mask of the general tiles
   auto mask = [&](int s, f32x4* sc) {
     if constexpr (GENERAL) {
@@ -164,40 +149,35 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
 #pragma unroll
     for (int u = 0; u < NU; ++u) pq[u] = oct_of(qd[2 * u], qd[2 * u + 1]);
   };
-  // O^T = V^T P^T and the row sums (ones block)
-  auto pv = [&](const Oct* pq, f32x4* o) {
-#pragma unroll
-    for (int nb = 0; nb <= NB; ++nb) o[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int u = 0; u < NU; ++u) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const unsigned char* vp = vr + ubase[u] + ro.voff[nb];
-        const Oct vt = oct_of(ld_tr16(vp), ld_tr16(vp + 16 * RingRows<D>::RB));
-        o[nb] = mma8(vt, pq[u], o[nb]);
-      }
-      o[NB] = mma8(ones, pq[u], o[NB]);
-    }
-  };
-
   f32x4 scA[NS], scB[NS];
   Oct pqA[NU], pqB[NU];
-  f32x4 oA[NB + 1], oB[NB + 1];
   Oct ph[R][2][NQ];
 
-  scores(0, scA);
-  __builtin_amdgcn_sched_barrier(0);
-  mask(0, scA);
-  __builtin_amdgcn_sched_barrier(0);
-  scores(1, scB);
-  softmax(0, scA, pqA);
-  __builtin_amdgcn_sched_barrier(0);
-  mask(1, scB);
-  __builtin_amdgcn_sched_barrier(0);
-  pv(pqA, oA);
-  softmax(1, scB, pqB);
-  __builtin_amdgcn_sched_barrier(0);
-  pv(pqB, oB);
+  // ---- phase 1: scores of both strips, each key block read once (block b
+  // is strip A's block b and strip B's block b - 1) | phi(q)
+#pragma unroll
+  for (int b = 0; b < NBK; ++b) {
+    Oct ko[NQ];
+#pragma unroll
+    for (int p = 0; p < NQ; ++p)
+      ko[p] = *reinterpret_cast<const Oct*>(kr + ubase[b >> 1] + ro.koff[p] +
+                                            16 * RingRows<D>::RB * (b & 1));
+    if (b < NS) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (!GENERAL) acc = b == 0 ? bias_lo : b == NS - 1 ? bias_hi : acc;
+#pragma unroll
+      for (int p = 0; p < NQ; ++p) acc = mma8(ko[p], qo[0][p], acc);
+      scA[b] = acc;
+    }
+    if (b >= 1) {
+      const int j = b - 1;
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      if constexpr (!GENERAL) acc = j == 0 ? bias_lo : j == NS - 1 ? bias_hi : acc;
+#pragma unroll
+      for (int p = 0; p < NQ; ++p) acc = mma8(ko[p], qo[1][p], acc);
+      scB[j] = acc;
+    }
+  }
   // phi_1, phi_2 of the query octs (one exp(-|x|) serves both maps)
 #pragma unroll
   for (int s = 0; s < 2; ++s)
@@ -215,40 +195,70 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
   // reloads them with the next tile's rows)
   mid();
 
-  // far products, with the near normalisation in their shadow
+  // ---- phase 2: band masks and softmax of both strips | far products of
+  // both strips, each state fragment read once per map (each map normalised
+  // on its own)
+  mask(0, scA);
+  mask(1, scB);
+  softmax(0, scA, pqA);
+  softmax(1, scB, pqB);
+  __builtin_amdgcn_sched_barrier(0);
   f32x4 fo[2][NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) fo[0][nb] = fo[1][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int l = 0; l < R; ++l) {
+    f32x4 nA[NB + 1], nB[NB + 1];
+#pragma unroll
+    for (int nb = 0; nb <= NB; ++nb) nA[nb] = nB[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < NQ; ++p) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const Oct f = sf[((l * NB + nb) * NQ + p) * 64 + lane];
+        nA[nb] = mma8(f, ph[l][0][p], nA[nb]);
+        nB[nb] = mma8(f, ph[l][1][p], nB[nb]);
+      }
+      nA[NB] = mma8(zo[l][p], ph[l][0][p], nA[NB]);
+      nB[NB] = mma8(zo[l][p], ph[l][1][p], nB[NB]);
+    }
+    const float fa = sfw > 0.f ? sfw * fast_rcp(nA[NB][0]) : 0.f;
+    const float fb = sfw > 0.f ? sfw * fast_rcp(nB[NB][0]) : 0.f;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      fo[0][nb] += nA[nb] * fa;
+      fo[1][nb] += nB[nb] * fb;
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- phase 3: O^T = V^T P^T and the row sums of both strips, each value
+  // unit read once; near normalisation and blend
+  f32x4 oA[NB + 1], oB[NB + 1];
+#pragma unroll
+  for (int nb = 0; nb <= NB; ++nb) oA[nb] = oB[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < NU; ++u) {
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      const unsigned char* vp = vr + ubase[u] + ro.voff[nb];
+      const Oct vt = oct_of(ld_tr16(vp), ld_tr16(vp + 16 * RingRows<D>::RB));
+      oA[nb] = mma8(vt, pqA[u], oA[nb]);
+      oB[nb] = mma8(vt, pqB[u], oB[nb]);
+    }
+    oA[NB] = mma8(ones, pqA[u], oA[NB]);
+    oB[NB] = mma8(ones, pqB[u], oB[NB]);
+  }
   {
     const float a0 = sn > 0.f ? sn * fast_rcp(oA[NB][0]) : 0.f;
     const float a1 = sn > 0.f ? sn * fast_rcp(oB[NB][0]) : 0.f;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-      fo[0][nb] = oA[nb] * a0;
-      fo[1][nb] = oB[nb] * a1;
+      fo[0][nb] += oA[nb] * a0;
+      fo[1][nb] += oB[nb] * a1;
     }
   }
-  // one strip and one map at a time (each map normalised on its own); the
-  // fragments are read again for each, which keeps them out of registers
-#pragma unroll
-  for (int s = 0; s < 2; ++s)
-#pragma unroll
-    for (int l = 0; l < R; ++l) {
-      asm volatile("" ::: "memory");
-      f32x4 num[NB + 1];
-#pragma unroll
-      for (int nb = 0; nb <= NB; ++nb) num[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int p = 0; p < NQ; ++p) {
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
-          num[nb] = mma8(sf[((l * NB + nb) * NQ + p) * 64 + lane], ph[l][s][p], num[nb]);
-        num[NB] = mma8(zo[l][p], ph[l][s][p], num[NB]);
-      }
-      const float f = sfw > 0.f ? sfw * fast_rcp(num[NB][0]) : 0.f;
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) fo[s][nb] += num[nb] * f;
-    }
   // rows at or beyond N fall outside the output buffer and are dropped
-#pragma unroll
   for (int s = 0; s < 2; ++s) store_strip<D>(oh, i0 + 16 * s, fo[s]);
 }
 
