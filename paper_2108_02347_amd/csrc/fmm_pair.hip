@@ -203,6 +203,10 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
   softmax(0, scA, pqA);
   softmax(1, scB, pqB);
   __builtin_amdgcn_sched_barrier(0);
+  // the far and P V products run at a raised wave priority, so the other
+  // wavefront on the SIMD fills their shadow with its vector phases
+  // (measured: 59.2 -> 57.2 us on the 2^16-token workload)
+  __builtin_amdgcn_s_setprio(1);
   f32x4 fo[2][NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) fo[0][nb] = fo[1][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -249,6 +253,7 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
     oA[NB] = mma8(ones, pqA[u], oA[NB]);
     oB[NB] = mma8(ones, pqB[u], oB[NB]);
   }
+  __builtin_amdgcn_s_setprio(0);
   {
     const float a0 = sn > 0.f ? sn * fast_rcp(oA[NB][0]) : 0.f;
     const float a1 = sn > 0.f ? sn * fast_rcp(oB[NB][0]) : 0.f;
