@@ -41,14 +41,32 @@ __device__ __forceinline__ uint2 quad_pack(const f32x4& x) {
 __device__ __forceinline__ Oct oct_ones() {
   return make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
 }
-// phi_1 and phi_2 of eight values (one exp(-|x|) serves both maps)
+// Larger of two bf16 pairs, lane by lane, for pairs whose second operand is
+// >= +0: for such values the order of the bit patterns read as signed 16-bit
+// integers is the order of the numbers (a negative first operand has its sign
+// bit set and compares below), and rounding to bf16 is monotone, so
+// max(bf16(a), bf16(b)) = bf16(max(a, b)).  One v_pk_max_i16 per pair.
+__device__ __forceinline__ uint32_t pk_max_bf16_nonneg(uint32_t a, uint32_t b) {
+  typedef short s16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s16x2, a),
+                                                                __builtin_bit_cast(s16x2, b)));
+}
+// phi_1 and phi_2 of eight values: one e = exp(-|x|) serves both maps, and
+// the max identities of phi12 are taken on the rounded pairs (1 + x, 1 - x
+// and e packed to bf16 first; e >= +0), which gives the same bits as
+// rounding max(1 + x, e) and max(1 - x, e).
 __device__ __forceinline__ void phi_oct(const Oct& x, Oct& p1, Oct& p2) {
-  float f[8], a[8], b[8];
-  oct_unpack(x, f);
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  uint32_t a[4], b[4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) phi12(f[i], a[i], b[i]);
-  p1 = oct_pack(a);
-  p2 = oct_pack(b);
+  for (int i = 0; i < 4; ++i) {
+    const float lo = __uint_as_float(w[i] << 16), hi = __uint_as_float(w[i] & 0xffff0000u);
+    const uint32_t e = pack_bf16x2(__expf(-fabsf(lo)), __expf(-fabsf(hi)));
+    a[i] = pk_max_bf16_nonneg(pack_bf16x2(1.f + lo, 1.f + hi), e);
+    b[i] = pk_max_bf16_nonneg(pack_bf16x2(1.f - lo, 1.f - hi), e);
+  }
+  p1 = make_uint4(a[0], a[1], a[2], a[3]);
+  p2 = make_uint4(b[0], b[1], b[2], b[3]);
 }
 
 // Buffer resource over one head's [N, D] bf16 rows.  Raw buffer loads past

@@ -183,12 +183,9 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
   for (int s = 0; s < 2; ++s)
 #pragma unroll
     for (int p = 0; p < NQ; ++p) {
-      float x[8], p1[8], p2[8];
-      oct_unpack(qo[s][p], x);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) phi12(x[i], p1[i], p2[i]);
-      ph[0][s][p] = oct_pack(p1);
-      if constexpr (R == 2) ph[1][s][p] = oct_pack(p2);
+      Oct p2;
+      phi_oct(qo[s][p], ph[0][s][p], p2);
+      if constexpr (R == 2) ph[1][s][p] = p2;
     }
   __builtin_amdgcn_sched_barrier(0);
   // the query octs are dead: the caller's step between the phases (it
