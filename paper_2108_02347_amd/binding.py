@@ -100,31 +100,40 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
 
+# The raw handle of the current stream: torch's own accessor when this build
+# has it (tens of nanoseconds), else the public Stream object (microseconds).
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
 def _stream_of(t: torch.Tensor):
+    if _raw_stream is not None:
+        return ctypes.c_void_p(_raw_stream(t.device.index))
     return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
 
 
-def _shape(q: torch.Tensor):
-    if q.dim() != 4:
-        raise ValueError("q, k, v must be [B, H, N, d]")
-    return tuple(int(x) for x in q.shape)
+_DTYPES = (torch.float32, torch.bfloat16)
 
 
 def _prep(q, k, v, w_near, w_far):
+    """Checks the operands (same dtype, shape and device, contiguous, on the
+    GPU; w of H float32 values) and returns (B, H, N, d).  Kept lean: at
+    short sequences this runs once per call next to a few-microsecond
+    kernel sequence."""
+    dt, dev, shp = q.dtype, q.device, q.shape
+    if len(shp) != 4:
+        raise ValueError("q, k, v must be [B, H, N, d]")
+    if dev.type != "cuda" or dt not in _DTYPES:
+        raise ValueError("q, k, v must be float32 or bfloat16 CUDA/HIP tensors")
     for name, t in (("q", q), ("k", k), ("v", v)):
-        if not t.is_cuda or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous CUDA/HIP tensor")
-        if t.dtype != q.dtype or t.shape != q.shape or t.device != q.device:
+        if t.dtype != dt or t.shape != shp or t.device != dev:
             raise ValueError("q, k, v must share dtype, shape and device")
-    if q.dtype not in (torch.float32, torch.bfloat16):
-        raise ValueError("q, k, v must be float32 or bfloat16")
-    B, H, N, d = _shape(q)
-    ws = []
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous CUDA/HIP tensor")
+    B, H, N, d = shp
     for name, w in (("w_near", w_near), ("w_far", w_far)):
-        if (not w.is_cuda or w.dtype != torch.float32 or w.numel() != H
-                or not w.is_contiguous() or w.device != q.device):
+        if (w.dtype != torch.float32 or w.device != dev or w.numel() != H
+                or not w.is_contiguous()):
             raise ValueError(f"{name} must be a contiguous float32 device tensor of H values")
-        ws.append(w)
     return B, H, N, d
 
 

@@ -81,3 +81,14 @@ def test_timing_read_rejects_bad_kernel_id():
     lib = binding.lib()
     ms, n = ctypes.c_double(), ctypes.c_longlong()
     assert lib.fmm_attn_kernel_timing_read(9, ctypes.byref(ms), ctypes.byref(n)) == -1
+
+
+def test_binding_rejects_host_tensors_and_wrong_rank():
+    # the Python binding checks its operands before any library call
+    import torch
+    q = torch.zeros(1, 2, 8, 16)
+    w = torch.zeros(2)
+    with pytest.raises(ValueError):
+        binding.forward(q, q, q, w, w, 2, 1, 0)
+    with pytest.raises(ValueError):
+        binding.forward(q[0], q[0], q[0], w, w, 2, 1, 0)

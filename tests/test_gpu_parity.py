@@ -146,6 +146,25 @@ def test_side_stream():
     assert torch.equal(ref_out, side)
 
 
+def test_binding_argument_checks():
+    q, k, v, wn, wf = make_inputs(1, 2, 64, 16, "bf16", 1.0, 49)
+    tq, tk, tv, twn, twf = upload(q, k, v, wn, wf, "bf16")
+    bad = [
+        (tq, tk.float(), tv, twn, twf),                       # mixed dtypes
+        (tq, tk[:, :, :32].contiguous(), tv, twn, twf),        # mixed shapes
+        (tq, tk.transpose(2, 3).contiguous().transpose(2, 3), tv, twn, twf),  # strided
+        (tq, tk, tv, twn[:1].contiguous(), twf),              # w of the wrong length
+        (tq, tk, tv, twn, twf.double()),                      # w not float32
+        (tq.half(), tk.half(), tv.half(), twn, twf),          # unsupported dtype
+    ]
+    for args in bad:
+        with pytest.raises(ValueError):
+            binding.forward(*args, 3, 2, 0)
+    out = binding.forward(tq, tk, tv, twn, twf, 3, 2, 0)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out.float()).all()
+
+
 # ------------------------------------------------------------------ ABI contract on the device
 def test_abi_errors_leave_out_untouched():
     q, k, v, wn, wf = make_inputs(1, 2, 64, 32, "f32", 1.0, 53)
