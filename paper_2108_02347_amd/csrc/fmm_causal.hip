@@ -345,6 +345,7 @@ __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N,
   // feed the intra-tile far products of both maps and the running sums'
   // update (the caller's) | phi of the next tile's keys (the caller's),
   // near normalisation, blend
+  late();
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     Oct vt[NB];
@@ -361,7 +362,6 @@ __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N,
     unit(c, vt);
   }
   __builtin_amdgcn_s_setprio(0);
-  late();
   f32x4 fo[NB];
   {
     const float a = sn > 0.f ? sn * fast_rcp(o[NB][0]) : 0.f;
