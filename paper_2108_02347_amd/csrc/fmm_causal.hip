@@ -419,29 +419,38 @@ __global__ __launch_bounds__(CNT, 2) void k_causal_strip(const bf16_t* __restric
   constexpr bool all_st = St::FT >= CW;  // every wave owns state tiles
   const bool has_st = St::active(w);
 
+  // prologue: every load (the segment's prefix sums, the ring's first window
+  // in rounds of two units, the first tile's keys for their phi rows, the
+  // first query rows) is issued before the first LDS store, so the workgroup
+  // waits for one round trip instead of several
+  using RC = RowsCopy<D, CTM, CNT>;
+  constexpr int NR = (U + 1) / 2;
   St st;
   st.load(w, prefix + ((size_t)bh * nseg + seg) * R * D * (D + 1));
-  using RC = RowsCopy<D, CTM, CNT>;
+  RC rk[NR], rv[NR], ck;
 #pragma unroll
-  for (int x = 0; x < U; x += 2) {
-    RC ck, cv;
-    ck.load(kh, (ua0 + x) * 32, true);
-    cv.load(vh, (ua0 + x) * 32, true);
-    auto slot = [=](int j) { return x + j < U ? x + j : -1; };
-    ck.store(kr, slot);
-    cv.store(vr, slot);
+  for (int i = 0; i < NR; ++i) {
+    rk[i].load(kh, (ua0 + 2 * i) * 32, true);
+    rv[i].load(vh, (ua0 + 2 * i) * 32, true);
+  }
+  ck.load(kh, s0, true);
+  Oct qo[1][NQ];
+  load_qo<D, 1>(qh, s0 + 16 * w, true, qo);
+#pragma unroll
+  for (int i = 0; i < NR; ++i) {
+    // full rounds need no range test (one the compiler cannot fold would
+    // sink their loads behind a branch and a wait)
+    auto slot = [=](int j) { return (U % 2 == 0 || i + 1 < NR) ? 2 * i + j : (j == 0 ? 2 * i : -1); };
+    rk[i].store(kr, slot);
+    rv[i].store(vr, slot);
   }
   {
-    RC ck;
-    ck.load(kh, s0, true);
     PhiRows<D, R> ph;
     ph.compute(ck);
     ph.store(phr);
   }
   if (all_st || has_st) St::store(w, st.pack(), sf, szo);
   const RingOffsets<D> ro;
-  Oct qo[1][NQ];
-  load_qo<D, 1>(qh, s0 + 16 * w, true, qo);
   RC pk, pv;
   pk.load(kh, (ua0 + U) * 32, ntile > 1);
   pv.load(vh, (ua0 + U) * 32, ntile > 1);

@@ -43,34 +43,57 @@ struct PairCfg {
 
 // State fragments from the non-causal tile-order record (see k_seg_state):
 // sf[((l*NB + nb)*NQ + p)*64 + lane] holds S_l[32p + 8g + i][16nb + r],
-// i = 0..7, as an oct; zo[l][p] holds z_l[32p + 8g + i].
+// i = 0..7, as an oct; zo[l][p] holds z_l[32p + 8g + i].  load() issues every
+// read of the record, store() packs and writes the fragments, so the
+// workgroup's other prologue loads can be in flight in between.
 template <int D, int R>
-__device__ __forceinline__ void pair_frags(const float* __restrict__ rec, Oct* sf,
-                                           Oct (*zo)[D / 32]) {
-  constexpr int NB = D / 16, NQ = D / 32;
-  for (int x = threadIdx.x; x < R * NB * NQ * 64; x += PNT) {
-    const int ln = x & 63, blk = x >> 6;
-    const int p = blk % NQ, nb = (blk / NQ) % NB, l = blk / (NQ * NB);
-    const int gg = ln >> 4, rr = ln & 15;
-    const int cb = 2 * p + (gg >> 1);
-    const float* t0 = rec + (size_t)l * D * (D + 1) + ((cb * NB + nb) * 64 + 32 * (gg & 1) + rr) * 4;
-    const float4 a = *reinterpret_cast<const float4*>(t0);
-    const float4 b = *reinterpret_cast<const float4*>(t0 + 64);
-    const float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-    sf[x] = oct_pack(f);
-  }
-  const int g = (threadIdx.x & 63) >> 4;
+struct PairFrags {
+  static constexpr int NB = D / 16, NQ = D / 32;
+  static constexpr int TOT = R * NB * NQ * 64, IT = (TOT + PNT - 1) / PNT;
+  float4 s[IT][2];
+  float4 z[R][NQ][2];
+  __device__ __forceinline__ void load(const float* __restrict__ rec) {
 #pragma unroll
-  for (int l = 0; l < R; ++l)
-#pragma unroll
-    for (int p = 0; p < NQ; ++p) {
-      const float* z = rec + (size_t)l * D * (D + 1) + D * D + 32 * p + 8 * g;
-      const float4 a = *reinterpret_cast<const float4*>(z);
-      const float4 b = *reinterpret_cast<const float4*>(z + 4);
-      const float f[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-      zo[l][p] = oct_pack(f);
+    for (int it = 0; it < IT; ++it) {
+      const int x = threadIdx.x + it * PNT;
+      if (TOT % PNT != 0 && x >= TOT) break;
+      const int ln = x & 63, blk = x >> 6;
+      const int p = blk % NQ, nb = (blk / NQ) % NB, l = blk / (NQ * NB);
+      const int gg = ln >> 4, rr = ln & 15;
+      const int cb = 2 * p + (gg >> 1);
+      const float* t0 = rec + (size_t)l * D * (D + 1) + ((cb * NB + nb) * 64 + 32 * (gg & 1) + rr) * 4;
+      s[it][0] = *reinterpret_cast<const float4*>(t0);
+      s[it][1] = *reinterpret_cast<const float4*>(t0 + 64);
     }
-}
+    const int g = (threadIdx.x & 63) >> 4;
+#pragma unroll
+    for (int l = 0; l < R; ++l)
+#pragma unroll
+      for (int p = 0; p < NQ; ++p) {
+        const float* zp = rec + (size_t)l * D * (D + 1) + D * D + 32 * p + 8 * g;
+        z[l][p][0] = *reinterpret_cast<const float4*>(zp);
+        z[l][p][1] = *reinterpret_cast<const float4*>(zp + 4);
+      }
+  }
+  __device__ __forceinline__ void store(Oct* sf, Oct (*zo)[D / 32]) const {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int x = threadIdx.x + it * PNT;
+      if (TOT % PNT != 0 && x >= TOT) break;
+      const float f[8] = {s[it][0].x, s[it][0].y, s[it][0].z, s[it][0].w,
+                          s[it][1].x, s[it][1].y, s[it][1].z, s[it][1].w};
+      sf[x] = oct_pack(f);
+    }
+#pragma unroll
+    for (int l = 0; l < R; ++l)
+#pragma unroll
+      for (int p = 0; p < NQ; ++p) {
+        const float f[8] = {z[l][p][0].x, z[l][p][0].y, z[l][p][0].z, z[l][p][0].w,
+                            z[l][p][1].x, z[l][p][1].y, z[l][p][1].z, z[l][p][1].w};
+        zo[l][p] = oct_pack(f);
+      }
+  }
+};
 
 // One 128-row tile of a wavefront: both strips' banded softmax (Eq. (3)),
 // far part (Eq. (8)-(9)), blend (Eq. (11)) and store.  The rows start at i0
@@ -297,20 +320,42 @@ __global__ __launch_bounds__(PNT, 2) void k_band_pair(const bf16_t* __restrict__
   const int ntile = (s1 - s0 + PTM - 1) / PTM;
   const int ua0 = (s0 >> 5) - KC;
 
-  Oct zo[R][NQ];
-  pair_frags<D, R>(fin + (size_t)bh * R * D * (D + 1), sf, zo);
+  // prologue: every load (the ring's first window in rounds of four units,
+  // the first query rows, the state record) is issued before the first LDS
+  // store, so the workgroup waits for one round trip instead of several
+  constexpr int NR = U / 4, UREM = U % 4;  // rounds of four units, then the rest
+  static_assert(UREM == 0 || UREM == 2, "ring of 4 + 2 KC units");
+  RowsCopy<D, PTM, PNT> rk[NR], rv[NR];
+  RowsCopy<D, 32 * (UREM ? UREM : 2), PNT> tk, tv;
 #pragma unroll
-  for (int x = 0; x < U; x += 4) {
-    RowsCopy<D, PTM, PNT> ck, cv;
-    ck.load(kh, (ua0 + x) * 32, true);
-    cv.load(vh, (ua0 + x) * 32, true);
-    auto slot = [=](int j) { return x + j < U ? x + j : -1; };
-    ck.store(kr, slot);
-    cv.store(vr, slot);
+  for (int i = 0; i < NR; ++i) {
+    rk[i].load(kh, (ua0 + 4 * i) * 32, true);
+    rv[i].load(vh, (ua0 + 4 * i) * 32, true);
   }
-  const RingOffsets<D> ro;
+  if constexpr (UREM != 0) {
+    tk.load(kh, (ua0 + 4 * NR) * 32, true);
+    tv.load(vh, (ua0 + 4 * NR) * 32, true);
+  }
   Oct qo[2][NQ];
   load_qo<D, 2>(qh, s0 + 32 * w, true, qo);
+  Oct zo[R][NQ];
+  {
+    PairFrags<D, R> fr;
+    fr.load(fin + (size_t)bh * R * D * (D + 1));
+    fr.store(sf, zo);
+  }
+#pragma unroll
+  for (int i = 0; i < NR; ++i) {
+    auto slot = [=](int j) { return 4 * i + j; };
+    rk[i].store(kr, slot);
+    rv[i].store(vr, slot);
+  }
+  if constexpr (UREM != 0) {
+    auto slot = [=](int j) { return 4 * NR + j; };
+    tk.store(kr, slot);
+    tv.store(vr, slot);
+  }
+  const RingOffsets<D> ro;
   RowsCopy<D, PTM, PNT> pk, pv;
   pk.load(kh, (ua0 + U) * 32, ntile > 1);
   pv.load(vh, (ua0 + U) * 32, ntile > 1);
