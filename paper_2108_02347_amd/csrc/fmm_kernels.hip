@@ -158,12 +158,16 @@ struct RowCopy {
       r[it] = buf_ld(rs, ((key - b) * D + (t % CPR) * Lay<T>::EPC) * (int)sizeof(T), (uint4*)0);
     }
   }
+  // A full copy (nrows == MAXROWS filling every thread's passes) stores
+  // without a row test: a test the compiler cannot fold would sink the
+  // copy's loads behind it, after a wait for every load in flight.
   template <typename F>
   __device__ __forceinline__ void store(T* dst, int ST, int nrows, F dst_row) const {
+    const bool full = MAXROWS * CPR == IT * NTHR && nrows == MAXROWS;
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int t = threadIdx.x + it * NTHR;
-      if (t < nrows * CPR)
+      if (full || t < nrows * CPR)
         *reinterpret_cast<uint4*>(dst + dst_row(t / CPR) * ST + (t % CPR) * Lay<T>::EPC) = r[it];
     }
   }
@@ -792,16 +796,16 @@ __global__ __launch_bounds__(SNT) void k_seg_state(const T* __restrict__ k,
 #pragma unroll
     for (int eb = 0; eb <= NB; ++eb) acc[l][eb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  RowCopy<T, D, SNT, TK> ck, cv;
+  // the first two chunks' loads are issued together (a second chunk past the
+  // segment's end has no rows: its loads return zeros without memory access)
+  RowCopy<T, D, SNT, TK> ck, cv, ck0, cv0;
   auto ident = [](int i) { return i; };
-  ck.load(kh, r0, min(TK, r1 - r0), r1);
-  cv.load(vh, r0, min(TK, r1 - r0), r1);
-  ck.store(s_kv[0][0], ST, TK, ident);
-  cv.store(s_kv[0][1], ST, TK, ident);
-  if (nchunk > 1) {
-    ck.load(kh, r0 + TK, min(TK, r1 - r0 - TK), r1);
-    cv.load(vh, r0 + TK, min(TK, r1 - r0 - TK), r1);
-  }
+  ck0.load(kh, r0, min(TK, r1 - r0), r1);
+  cv0.load(vh, r0, min(TK, r1 - r0), r1);
+  ck.load(kh, r0 + TK, min(TK, r1 - r0 - TK), r1);
+  cv.load(vh, r0 + TK, min(TK, r1 - r0 - TK), r1);
+  ck0.store(s_kv[0][0], ST, TK, ident);
+  cv0.store(s_kv[0][1], ST, TK, ident);
   const int r = lane & 15, g = lane >> 4;
   using Q = typename QuadOf<T>::type;
   for (int c = 0; c < nchunk; ++c) {
