@@ -181,10 +181,7 @@ __device__ __forceinline__ void store_strip(Rsrc oh, int row0, const f32x4* fo) 
     typedef int i32x4 __attribute__((ext_vector_type(4)));
     const i32x4 o = {(int)x[0], (int)y[0], (int)x[1], (int)y[1]};
     const int col = 32 * c + 16 * (g & 1) + 8 * (g >> 1);
-    // non-temporal (nt): the output is not read again by the operator, and
-    // streaming it keeps more of the inputs in the last-level cache for the
-    // next call (about 1 % per step measured)
-    __builtin_amdgcn_raw_buffer_store_b128(o, oh, 2 * ((row0 + r) * D + col), 0, 2);
+    __builtin_amdgcn_raw_buffer_store_b128(o, oh, 2 * ((row0 + r) * D + col), 0, 0);
   }
 }
 
