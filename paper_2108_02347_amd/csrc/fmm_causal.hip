@@ -190,11 +190,13 @@ struct PhiRows {
 // The near and far parts are independent until the blend, so the work runs
 // as phases that pair matrix-core products of one part with vector
 // arithmetic of the other (scheduling fences keep the phases apart):
-//   near scores + phi(q) | softmax + far products of map 0 with the sums
-//   before the tile | P V + intra-tile products of map 0 | far products of
-//   map 1 + near normalisation and blend, store
-// (the caller follows with the state update paired with phi of the next
-// tile's keys).
+//   1: near scores + phi(q)
+//   2: softmax + far products of both maps with the sums before the tile
+//   3: P V + intra-tile scores of both maps (masked, packed)
+//   4: per tile key unit, its V^T octs read once for the intra-tile far
+//      products of both maps and the running sums' update (unit()), beside
+//      phi of the next tile's keys (late())
+//   then near normalisation, blend, store.
 // mid() runs once phi(q) is formed (the query octs are dead then).
 template <int D, int R, int KC, bool GENERAL, class Mid, class Unit, class Late>
 __device__ __forceinline__ void tile_work(Rsrc oh, int t0, int w, int m0, int N, int band_k,

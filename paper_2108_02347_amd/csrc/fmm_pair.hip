@@ -106,10 +106,10 @@ struct PairFrags {
 // the row's band clipped to [0, N).
 //
 // Every LDS operand is read once per wavefront and feeds both strips.  The
-// work runs as phases that pair matrix-core products with independent vector
-// arithmetic (scheduling fences keep the phases apart):
-//   scores of A and B + phi(q) | softmax of A and B + far products |
-//   P V of A and B + near normalisation, blend, store
+// work runs as phases separated by scheduling fences:
+//   scores of A and B + phi(q) | softmax of A and B |
+//   far products and P V of A and B (at a raised wave priority) |
+//   near normalisation, blend, store
 // mid() runs after the first phase, once phi(q) is formed.
 template <int D, int R, int KC, bool GENERAL, class Mid>
 __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
