@@ -1,0 +1,132 @@
+"""The oracle's pins catch planted mistakes (CPU only).
+
+Each case below plants one plausible mistake into a copy of the oracle's
+source (a flipped sign, a dropped term, a transposed operand, an index off by
+one, a wrong scale, swapped blend weights), loads the copy as a separate
+module, and runs every pin of tests/test_oracle_pins.py against it with all
+of its parametrisations.  The unmodified copy must pass every pin; each
+mutated copy must fail at least one.  Nothing here touches the real oracle
+module or the GPU library.
+"""
+
+import itertools
+import os
+import types
+
+import pytest
+
+import test_oracle_pins as pins
+
+ORACLE_SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                          "oracle", "fmm_ref.py")
+
+# (name, exact text in the oracle, replacement)
+MUTATIONS = [
+    ("phi_2 without the sign flip",
+     "return _elu(-np.asarray(x, dtype=np.float64)) + 1.0",
+     "return _elu(np.asarray(x, dtype=np.float64)) + 1.0"),
+    ("elu without the -1",
+     "np.expm1(np.minimum(x, 0.0))",
+     "np.exp(np.minimum(x, 0.0))"),
+    ("dense near field scaled by 1/d",
+     'np.einsum("bhic,bhjc->bhij", q, k) / math.sqrt(d)',
+     'np.einsum("bhic,bhjc->bhij", q, k) / d'),
+    ("streamed near field without the scale",
+     "    scale = 1.0 / math.sqrt(d)\n    out = np.empty_like(v)",
+     "    scale = 1.0\n    out = np.empty_like(v)"),
+    ("band one narrower",
+     "return np.abs(i - j) <= band_k",
+     "return np.abs(i - j) < band_k"),
+    ("causal band without the diagonal",
+     "return (j <= i) & (j >= i - band_k)",
+     "return (j < i) & (j >= i - band_k)"),
+    ("streamed band missing its last offset",
+     "offs = np.arange(-kk, 1 if causal else kk + 1)",
+     "offs = np.arange(-kk, 1 if causal else kk)"),
+    ("far state transposed",
+     's = np.einsum("bhjc,bhje->bhce", pk, v)',
+     's = np.einsum("bhjc,bhje->bhec", pk, v)'),
+    ("non-causal far part not normalised",
+     "            out += num / den[..., None]\n            continue",
+     "            out += num / den.mean()\n            continue"),
+    ("causal far sum exclusive of j = i",
+     "s_cum = s_run[:, :, None] + np.cumsum(outer, axis=2)",
+     "s_cum = s_run[:, :, None] + np.cumsum(outer, axis=2) - outer"),
+    ("causal far carry from the block's first row",
+     "            s_run = s_cum[:, :, -1]",
+     "            s_run = s_cum[:, :, 0]"),
+    ("dense causal far triangle without the diagonal",
+     "lower = np.tril(np.ones((n, n), dtype=bool))",
+     "lower = np.tril(np.ones((n, n), dtype=bool), -1)"),
+    ("blend weights swapped",
+     "return np.where(a > 0, a * near, 0.0) + np.where(b > 0, b * far, 0.0)",
+     "return np.where(a > 0, a * far, 0.0) + np.where(b > 0, b * near, 0.0)"),
+    ("dense far field with one normaliser for both maps",
+     "        w = a / a.sum(axis=-1, keepdims=True)",
+     "        w = a / (rank * a.sum(axis=-1, keepdims=True).mean())"),
+    ("rows form: causal band stops one short",
+     "hi = i if causal else min(n - 1, i + band_k)",
+     "hi = i - 1 if causal and i > 0 else min(n - 1, i + band_k)"),
+    ("rows form: non-causal far state transposed",
+     "            s = pk.T @ vs",
+     "            s = (pk.T @ vs).T"),
+]
+
+
+def load_oracle(src: str) -> types.ModuleType:
+    mod = types.ModuleType("oracle_copy")
+    exec(compile(src, ORACLE_SRC + " (copy)", "exec"), mod.__dict__)
+    return mod
+
+
+def pin_calls():
+    """Every pin test with every parametrisation, as (name, fn, kwargs)."""
+    out = []
+    for name in sorted(dir(pins)):
+        fn = getattr(pins, name)
+        if not name.startswith("test_") or not callable(fn):
+            continue
+        grids = []
+        for mark in getattr(fn, "pytestmark", []):
+            if mark.name != "parametrize":
+                continue
+            argnames, values = mark.args[0], mark.args[1]
+            names = [a.strip() for a in argnames.split(",")] if isinstance(argnames, str) \
+                else list(argnames)
+            rows = [v if len(names) > 1 else (v,) for v in values]
+            grids.append([dict(zip(names, r)) for r in rows])
+        for combo in itertools.product(*grids) if grids else [()]:
+            kw = {}
+            for part in combo:
+                kw.update(part)
+            out.append((name, fn, kw))
+    return out
+
+
+def failing_pins(mod):
+    saved = pins.ref
+    pins.ref = mod
+    failed = []
+    try:
+        for name, fn, kw in pin_calls():
+            try:
+                fn(**kw)
+            except Exception:  # noqa: BLE001 - any failure counts as caught
+                failed.append(f"{name}{kw or ''}")
+    finally:
+        pins.ref = saved
+    return failed
+
+
+def test_unmodified_copy_passes_every_pin():
+    src = open(ORACLE_SRC).read()
+    assert failing_pins(load_oracle(src)) == []
+
+
+@pytest.mark.filterwarnings("ignore::RuntimeWarning")  # the broken copies divide by zero
+@pytest.mark.parametrize("name,old,new", MUTATIONS, ids=[m[0] for m in MUTATIONS])
+def test_planted_mistake_is_caught(name, old, new):
+    src = open(ORACLE_SRC).read()
+    assert src.count(old) == 1, f"mutation site for '{name}' must occur exactly once"
+    failed = failing_pins(load_oracle(src.replace(old, new)))
+    assert failed, f"no pin caught: {name}"
