@@ -255,3 +255,15 @@ def test_random_configurations():
         err = check_full(B, H, N, d, kw, rank, causal, dtype, seed, 1.0 / np.sqrt(d))
         worst[dtype] = max(worst[dtype], err)
     log(f"random configurations: worst f32 {worst['f32']:.3e}, bf16 {worst['bf16']:.3e}")
+
+
+@pytest.mark.parametrize("causal", [0, 1])
+def test_large_magnitude_inputs(causal):
+    # q, k, v with standard deviation 4: near-field scores of several hundred
+    # (the row maximum must be taken before the exponentials) and far-field
+    # features dominated by phi's linear branch, through the strip kernels
+    # (bf16, d = 64 / 32) and the fp32 kernels
+    worst = 0.0
+    for d, kw, dtype in ((64, 64, "bf16"), (32, 20, "bf16"), (64, 7, "f32"), (16, 40, "f32")):
+        worst = max(worst, check_full(1, 2, 1500, d, kw, 2, causal, dtype, 700 + d + kw, 4.0))
+    log(f"std-4 inputs causal={causal}: worst {worst:.3e}")
