@@ -1327,24 +1327,20 @@ static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
   const int U = a.causal ? 2 + kc : 2 + 2 * kc;
   const bool ring = U <= (a.causal ? RG::U_C : RG::U_NC);
   const size_t lds = RG::bytes(ring ? U : RG::UR, a.causal != 0);
-  static const hipError_t lds_attr = [] {
-    hipError_t e = hipSuccess, x;
-    if ((x = hipFuncSetAttribute((const void*)k_band_ring<T, D, R>,
-                                 hipFuncAttributeMaxDynamicSharedMemorySize,
-                                 (int)RG::bytes(RG::U_NC, false))) != hipSuccess) e = x;
-    if ((x = hipFuncSetAttribute((const void*)k_causal_ring<T, D, R>,
-                                 hipFuncAttributeMaxDynamicSharedMemorySize,
-                                 (int)RG::bytes(RG::U_C, true))) != hipSuccess) e = x;
-    if ((x = hipFuncSetAttribute((const void*)k_band_rounds<T, D, R>,
-                                 hipFuncAttributeMaxDynamicSharedMemorySize,
-                                 (int)RG::bytes(RG::UR, false))) != hipSuccess) e = x;
-    if ((x = hipFuncSetAttribute((const void*)k_causal_rounds<T, D, R>,
-                                 hipFuncAttributeMaxDynamicSharedMemorySize,
-                                 (int)RG::bytes(RG::UR, true))) != hipSuccess) e = x;
-    (void)hipGetLastError();
-    return e;
-  }();
-  if (lds_attr != hipSuccess) return lds_attr;
+  {
+    static std::atomic<unsigned long long> set_band{0}, set_causal{0}, set_brounds{0},
+        set_crounds{0};
+    hipError_t e;
+    if ((e = lds_limit_once((const void*)k_band_ring<T, D, R>, (int)RG::bytes(RG::U_NC, false),
+                            set_band)) != hipSuccess ||
+        (e = lds_limit_once((const void*)k_causal_ring<T, D, R>, (int)RG::bytes(RG::U_C, true),
+                            set_causal)) != hipSuccess ||
+        (e = lds_limit_once((const void*)k_band_rounds<T, D, R>, (int)RG::bytes(RG::UR, false),
+                            set_brounds)) != hipSuccess ||
+        (e = lds_limit_once((const void*)k_causal_rounds<T, D, R>, (int)RG::bytes(RG::UR, true),
+                            set_crounds)) != hipSuccess)
+      return e;
+  }
 
   // long chunks once a segment spans at least four of them
   constexpr int TKL = 32 * (SW / (D / 16));

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 
+#include <atomic>
+
 #include "../../include/fmm_attn.h"
 
 namespace fmm {
@@ -46,6 +48,26 @@ inline void launch_timed(LaunchTimer* t, int id, F kern, dim3 grid, dim3 block, 
   } else {
     hipLaunchKernelGGL(kern, grid, block, shm, s, args...);
   }
+}
+
+// Raises a kernel's dynamic LDS limit to `bytes` on the current device, once
+// per device (HIP keeps the attribute per device); `done` is the caller's
+// per-kernel record of the devices already set (devices 0..63; others are set
+// on every call).
+inline hipError_t lds_limit_once(const void* kern, int bytes,
+                                 std::atomic<unsigned long long>& done) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return hipErrorNoDevice;
+  }
+  const unsigned long long bit = dev >= 0 && dev < 64 ? 1ull << dev : 0ull;
+  if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+  const hipError_t e =
+      hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  (void)hipGetLastError();
+  if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_acq_rel);
+  return e;
 }
 
 hipError_t launch_forward(const LaunchArgs& a, LaunchTimer* timer);

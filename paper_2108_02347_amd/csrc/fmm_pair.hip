@@ -395,13 +395,10 @@ template <int D, int R, int KC>
 hipError_t launch_pair_kc(const LaunchArgs& a, LaunchTimer* timer, const float* fin,
                           float scale2) {
   using C = PairCfg<D, R, KC>;
-  static const hipError_t attr = [] {
-    const hipError_t e = hipFuncSetAttribute((const void*)k_band_pair<D, R, KC>,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS);
-    (void)hipGetLastError();
+  static std::atomic<unsigned long long> lds_set{0};
+  if (const hipError_t e = lds_limit_once((const void*)k_band_pair<D, R, KC>, C::LDS, lds_set);
+      e != hipSuccess)
     return e;
-  }();
-  if (attr != hipSuccess) return attr;
   launch_timed(timer, FMM_KERNEL_BAND_APPLY, k_band_pair<D, R, KC>,
                dim3(a.B * a.H * a.nseg_apply), dim3(PNT), (size_t)C::LDS,
                (hipStream_t)a.stream, (const bf16_t*)a.q, (const bf16_t*)a.k,
