@@ -401,6 +401,12 @@ def main():
                    "hbm_frac": round(alg_bytes[name] / (kt[name] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
                   if name in alg_bytes else {})}
         for name in kt if kt[name]}
+    # HBM bytes counted by rocprofv3 (committed summaries, same sources)
+    for name, rec_k in per_kernel.items():
+        hbm = read_traffic(name, "stress64k")
+        if hbm and kt.get(name):
+            rec_k["traffic_bytes"] = int(hbm)
+            rec_k["counted_GBps"] = round(hbm / (kt[name] * 1e-3) / 1e9, 1)
     # matrix-core work from the committed SQ counter summary (same sources)
     for name, rec_k in per_kernel.items():
         cnt = read_counters(name)
