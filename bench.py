@@ -347,8 +347,9 @@ def main():
         counter_summary(args.counter_summary)
         return
     if args.gpus != 1:
-        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); the operator "
-              "is single-GPU in this build, see DESIGN.md for how it would shard.",
+        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}): the operator "
+              "runs on one GPU; its (batch, head) slices are independent, so it would "
+              "shard over B x H with no communication.",
               file=sys.stderr)
         sys.exit(2)
     import torch

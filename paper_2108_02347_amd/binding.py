@@ -100,8 +100,9 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
 
-# The raw handle of the current stream: torch's own accessor when this build
-# has it (tens of nanoseconds), else the public Stream object (microseconds).
+# The raw handle of the current stream: torch's own accessor when the
+# installed torch provides it (tens of nanoseconds), else the public Stream
+# object (microseconds).
 _raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
 
 
