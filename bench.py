@@ -308,6 +308,21 @@ def timed(fn, steps, warmup, torch):
     return (time.perf_counter() - t0) / steps
 
 
+def hbm_ceiling(torch):
+    """Achievable HBM rates on this GPU for context next to the published
+    peak: torch's device copy (bytes read + written) and fill (bytes written)
+    over 1 GiB buffers, 20 timed launches each."""
+    n = 1 << 30
+    a = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty_like(a)
+    t_copy = timed(lambda: b.copy_(a), 20, 3, torch)
+    t_fill = timed(lambda: b.fill_(0), 20, 3, torch)
+    del a, b
+    return {"copy_GBps": round(2 * n / t_copy / 1e9, 1),
+            "write_GBps": round(n / t_fill / 1e9, 1),
+            "how": "torch copy_ and fill_ over 1 GiB, 20 launches"}
+
+
 def cpu_baseline(host_inputs, w):
     """Oracle (float64 numpy, single BLAS thread) on head 0 of the workload,
     full sequence, both forms."""
@@ -557,6 +572,7 @@ def main():
         "kernels": per_kernel,
         "n4096": n4096,
         "n4096_b128": n4096_b128,
+        "hbm_achievable": hbm_ceiling(torch),
         "kernel_source_hash": kernel_source_hash(),
     }
     if not args.no_cpu_baseline:
