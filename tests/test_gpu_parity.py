@@ -61,6 +61,26 @@ def test_stress64k_sampled_rows(causal):
     assert worst <= TOL["bf16"]
 
 
+def test_n4096_b128_sampled_rows():
+    # the N = 4096 shape at B = 128 (64 MiB per tensor) that the benchmark also
+    # times: sampled rows of every (batch, head) slice against the oracle
+    B, H, N, d, kw, rank = 128, 2, 4096, 32, 20, 2
+    q, k, v, wn, wf = make_inputs(B, H, N, d, "bf16", 1.0, 4096)
+    log(f"n4096 B=128 bf16: B={B} H={H} N={N} d={d} k={kw}")
+    got = run_gpu(q, k, v, wn, wf, kw, rank, 0, "bf16")
+    assert np.isfinite(got).all()
+    rng = np.random.default_rng(4097)
+    worst = 0.0
+    for b in range(B):
+        for h in range(H):
+            rows = np.unique(np.concatenate([[0, kw, N - 1 - kw, N - 1],
+                                             rng.integers(0, N, 4)]))
+            want = ref.fmm_attention_rows(q, k, v, wn, wf, kw, rank, False, b, h, rows)
+            worst = max(worst, np.abs(got[b, h, rows] - want).max() / np.abs(want).max())
+    log(f"n4096 B=128: worst sampled-slice error {worst:.3e}")
+    assert worst <= TOL["bf16"]
+
+
 # ------------------------------------------------------------------ edge-case sweep
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("causal", [0, 1])
