@@ -35,8 +35,14 @@
  * stream) and returns without synchronising.  Faults inside kernels surface
  * at the caller's next synchronisation.
  *
- * Errors: functions return an int status.  On any error nothing is enqueued
- * and `out` is left untouched.  No C++ exception crosses this interface.
+ * Errors: functions return an int status.  Every check (arguments, sizes,
+ * workspace, and the grid of every kernel the call would launch against the
+ * dispatch limits) runs before the first kernel is enqueued, so on
+ * FMM_ERR_INVALID_ARG, FMM_ERR_UNSUPPORTED and FMM_ERR_OOM nothing is
+ * enqueued and `out` is left untouched.  FMM_ERR_HIP reports a failing HIP
+ * runtime call; when a dispatch itself fails, kernels of the same call that
+ * precede it may already be enqueued and `out` is then unspecified.  No C++
+ * exception crosses this interface.
  */
 #ifndef FMM_ATTN_H
 #define FMM_ATTN_H
@@ -54,7 +60,10 @@ extern "C" {
                                     out overlapping q, k or v, or a shape whose
                                     element count does not fit in int64 */
 #define FMM_ERR_UNSUPPORTED (-2) /* d not in {16, 32, 64}, rank not in {1, 2},
-                                    or dtype code unknown */
+                                    dtype code unknown, B*H above 2^31-1, or
+                                    a kernel grid beyond the dispatch limit
+                                    (2^32 work-items per dimension; about
+                                    8.4 million (batch, head) slices) */
 #define FMM_ERR_HIP         (-3) /* a HIP runtime call or kernel launch failed */
 #define FMM_ERR_OOM         (-4) /* workspace allocation failed, or a
                                     caller-provided workspace is too small */

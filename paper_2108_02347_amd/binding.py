@@ -138,11 +138,21 @@ def _prep(q, k, v, w_near, w_far):
     return B, H, N, d
 
 
+def _check_out(out, q):
+    """A caller-supplied output must match q exactly: the library receives only
+    its address and writes B*H*N*d elements of q's dtype there."""
+    if (not isinstance(out, torch.Tensor) or out.dtype != q.dtype or out.shape != q.shape
+            or out.device != q.device or not out.is_contiguous()):
+        raise ValueError("out must be a contiguous tensor with q's dtype, shape and device")
+
+
 def forward(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool, out=None):
     """FMMformer attention forward; returns out (allocated if not given)."""
     B, H, N, d = _prep(q, k, v, w_near, w_far)
     if out is None:
         out = torch.empty_like(q)
+    else:
+        _check_out(out, q)
     fn = lib().fmm_attn_forward_bf16 if q.dtype == torch.bfloat16 else lib().fmm_attn_forward
     _check(fn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, int(band_k), int(rank),
               int(bool(causal)), _ptr(w_near), _ptr(w_far), _stream_of(q)))
@@ -151,10 +161,16 @@ def forward(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool, out=No
 
 def forward_ws(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool, workspace,
                out=None):
-    """Same operator with a caller-owned workspace (a uint8 device tensor)."""
+    """Same operator with a caller-owned workspace (a contiguous device tensor on
+    q's device; its size in bytes is passed to the library, which checks it)."""
     B, H, N, d = _prep(q, k, v, w_near, w_far)
     if out is None:
         out = torch.empty_like(q)
+    else:
+        _check_out(out, q)
+    if (not isinstance(workspace, torch.Tensor) or workspace.device != q.device
+            or not workspace.is_contiguous()):
+        raise ValueError("workspace must be a contiguous tensor on q's device")
     dt = FMM_DTYPE_BF16 if q.dtype == torch.bfloat16 else FMM_DTYPE_F32
     _check(lib().fmm_attn_forward_ws(
         _ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, int(band_k), int(rank),

@@ -54,9 +54,11 @@ Plan make_plan(int B, int H, int N, int d, int rank, int esize, int apply_tm) {
   p.nseg = (int)((N + L - 1) / L);
   p.L_apply = (int)La;
   p.nseg_apply = (int)((N + La - 1) / La);
-  const size_t rec = (size_t)rank * d * (d + 1);
-  p.ws_bytes = ((size_t)bh * p.nseg + (size_t)bh) * rec * sizeof(float);
-  p.ws_bytes = (p.ws_bytes + 255) / 256 * 256;
+  typedef unsigned __int128 u128;
+  const u128 rec = (u128)rank * d * (d + 1);
+  const u128 ws = ((u128)bh * p.nseg + (u128)bh) * rec * sizeof(float);
+  // a workspace beyond half the address space cannot exist: report it as 0
+  p.ws_bytes = ws > (u128)(SIZE_MAX / 2) ? 0 : (size_t)((ws + 255) / 256 * 256);
   return p;
 }
 
@@ -77,14 +79,17 @@ int validate(const void* q, const void* k, const void* v, void* out, int B, int 
   if (causal != 0 && causal != 1) return FMM_ERR_INVALID_ARG;
   if (dtype != FMM_DTYPE_F32 && dtype != FMM_DTYPE_BF16) return FMM_ERR_UNSUPPORTED;
   if (!supported(d, rank)) return FMM_ERR_UNSUPPORTED;
-  const long long elems = (long long)B * H * N * d;
-  if (elems / d / N / H != B) return FMM_ERR_INVALID_ARG;
   const size_t es = dtype == FMM_DTYPE_BF16 ? 2 : 4;
-  if (elems > (long long)(INT64_MAX / (long long)es)) return FMM_ERR_INVALID_ARG;
+  // sizes in 128-bit arithmetic: four positive ints cannot overflow it
+  typedef unsigned __int128 u128;
+  const u128 bytes128 = (u128)(unsigned)B * (unsigned)H * (unsigned)N * (unsigned)d * es;
+  if (bytes128 > (u128)INT64_MAX) return FMM_ERR_INVALID_ARG;
+  // slices are counted in int by the launchers; grids are checked before launch
+  if ((long long)B * H > INT32_MAX) return FMM_ERR_UNSUPPORTED;
   for (const void* p : {q, k, v, (const void*)out})
     if ((uintptr_t)p % 16) return FMM_ERR_INVALID_ARG;
   if ((uintptr_t)w_near % 4 || (uintptr_t)w_far % 4) return FMM_ERR_INVALID_ARG;
-  const size_t bytes = (size_t)elems * es;
+  const size_t bytes = (size_t)bytes128;
   if (overlaps(out, q, bytes) || overlaps(out, k, bytes) || overlaps(out, v, bytes))
     return FMM_ERR_INVALID_ARG;
   return FMM_OK;
@@ -147,18 +152,19 @@ size_t ws_limit() {
   return (size_t)strtoull(s, nullptr, 10);
 }
 
-// Returns a workspace of at least `bytes` for (current device, stream).
-int acquire_ws(void* stream, size_t bytes, void** out) {
+// Returns a workspace of at least `bytes` for (current device, stream).  The
+// caller holds ws_mutex() until its kernels are enqueued, so no other thread
+// can free the buffer between this lookup and the launches that use it.
+int acquire_ws_locked(void* stream, size_t bytes, void** out) {
   if (bytes > ws_limit()) return FMM_ERR_OOM;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return FMM_ERR_HIP;
-  std::lock_guard<std::mutex> g(ws_mutex());
   WsEntry& e = ws_map()[{dev, stream}];
   if (e.bytes < bytes) {
     if (e.ptr) {
       // kernels enqueued earlier on this stream may still read the old buffer
       if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return FMM_ERR_HIP;
-      hipFree(e.ptr);
+      (void)hipFree(e.ptr);
       e.ptr = nullptr;
       e.bytes = 0;
     }
@@ -174,22 +180,32 @@ int acquire_ws(void* stream, size_t bytes, void** out) {
   return FMM_OK;
 }
 
-int run(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d,
-        int band_k, int rank, int causal, const float* w_near, const float* w_far, int dtype,
-        void* ws, size_t ws_bytes, bool own_ws, void* stream) {
-  int st = validate(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype);
-  if (st != FMM_OK) return st;
-  const int kc = band_k < N ? band_k : N;
-  const int apply_tm = fmm::band_pair_applies(dtype, d, kc, causal, N) ? fmm::pair_tile_rows()
-                                                                    : fmm::tile_rows();
-  const Plan p = make_plan(B, H, N, d, rank, dtype == FMM_DTYPE_BF16 ? 2 : 4, apply_tm);
-  if (own_ws) {
-    st = acquire_ws(stream, p.ws_bytes, &ws);
-    if (st != FMM_OK) return st;
-  } else {
-    if (!ws || (uintptr_t)ws % 256) return FMM_ERR_INVALID_ARG;
-    if (ws_bytes < p.ws_bytes) return FMM_ERR_OOM;
-  }
+// The dry pass over the launch sequence: grid limits and LDS limits, nothing
+// enqueued.  Runs before any workspace is acquired.
+int check_launch(const fmm::LaunchArgs& a) {
+  EventTimer& t = timer();
+  std::lock_guard<std::mutex> g(t.mu);
+  fmm::Launcher dry;
+  dry.timer = &t;
+  dry.dry = true;
+  if (fmm::launch_forward(a, dry) != hipSuccess)
+    return dry.err == hipErrorInvalidConfiguration ? FMM_ERR_UNSUPPORTED : FMM_ERR_HIP;
+  return FMM_OK;
+}
+
+// Enqueues the launch sequence (after check_launch passed).
+int launch_now(const fmm::LaunchArgs& a) {
+  EventTimer& t = timer();
+  std::lock_guard<std::mutex> g(t.mu);
+  fmm::Launcher L;
+  L.timer = &t;
+  return fmm::launch_forward(a, L) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
+}
+
+fmm::LaunchArgs make_args(const void* q, const void* k, const void* v, void* out, int B, int H,
+                          int N, int d, int band_k, int rank, int causal, const float* w_near,
+                          const float* w_far, int dtype, void* ws, const Plan& p,
+                          void* stream) {
   fmm::LaunchArgs a;
   a.q = q;
   a.k = k;
@@ -212,12 +228,64 @@ int run(const void* q, const void* k, const void* v, void* out, int B, int H, in
   a.L = p.L;
   a.nseg_apply = p.nseg_apply;
   a.L_apply = p.L_apply;
-  EventTimer& t = timer();
-  std::lock_guard<std::mutex> g(t.mu);
-  return fmm::launch_forward(a, &t) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
+  return a;
+}
+
+Plan plan_for(int B, int H, int N, int d, int band_k, int rank, int causal, int dtype) {
+  const int kc = band_k < N ? band_k : N;
+  const int apply_tm = fmm::band_pair_applies(dtype, d, kc, causal, N) ? fmm::pair_tile_rows()
+                                                                    : fmm::tile_rows();
+  return make_plan(B, H, N, d, rank, dtype == FMM_DTYPE_BF16 ? 2 : 4, apply_tm);
+}
+
+int run(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d,
+        int band_k, int rank, int causal, const float* w_near, const float* w_far, int dtype,
+        void* ws, size_t ws_bytes, bool own_ws, void* stream) {
+  int st = validate(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype);
+  if (st != FMM_OK) return st;
+  const Plan p = plan_for(B, H, N, d, band_k, rank, causal, dtype);
+  if (p.ws_bytes == 0) return FMM_ERR_UNSUPPORTED;
+  fmm::LaunchArgs a = make_args(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far,
+                                dtype, nullptr, p, stream);
+  st = check_launch(a);
+  if (st != FMM_OK) return st;
+  std::unique_lock<std::mutex> ws_lock(ws_mutex(), std::defer_lock);
+  if (own_ws) {
+    ws_lock.lock();
+    st = acquire_ws_locked(stream, p.ws_bytes, &ws);
+    if (st != FMM_OK) return st;
+  } else {
+    if (!ws || (uintptr_t)ws % 256) return FMM_ERR_INVALID_ARG;
+    if (ws_bytes < p.ws_bytes) return FMM_ERR_OOM;
+  }
+  a.ws = (float*)ws;
+  return launch_now(a);
 }
 
 }  // namespace
+
+namespace fmm {
+
+int validate_forward(const void* q, const void* k, const void* v, void* out, int B, int H,
+                     int N, int d, int band_k, int rank, int causal, const float* w_near,
+                     const float* w_far, int dtype) {
+  return validate(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype);
+}
+
+size_t forward_workspace_bytes(int B, int H, int N, int d, int band_k, int rank, int causal,
+                               int dtype) {
+  return plan_for(B, H, N, d, band_k, rank, causal, dtype).ws_bytes;
+}
+
+int forward_with_workspace(const void* q, const void* k, const void* v, void* out, int B, int H,
+                           int N, int d, int band_k, int rank, int causal, const float* w_near,
+                           const float* w_far, int dtype, void* ws, size_t ws_bytes,
+                           void* stream) {
+  return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype, ws, ws_bytes,
+             false, stream);
+}
+
+}  // namespace fmm
 
 extern "C" {
 
@@ -270,12 +338,12 @@ void fmm_attn_release_workspace(void) {
   const bool have_cur = hipGetDevice(&cur) == hipSuccess;
   for (auto& kv : ws_map()) {
     if (!kv.second.ptr) continue;
-    hipSetDevice(kv.first.first);
-    hipDeviceSynchronize();
-    hipFree(kv.second.ptr);
+    (void)hipSetDevice(kv.first.first);
+    (void)hipDeviceSynchronize();
+    (void)hipFree(kv.second.ptr);
   }
   ws_map().clear();
-  if (have_cur) hipSetDevice(cur);
+  if (have_cur) (void)hipSetDevice(cur);
 }
 
 int fmm_attn_version(void) { return kVersion; }

@@ -511,22 +511,22 @@ __global__ __launch_bounds__(CNT, 2) void k_causal_strip(const bf16_t* __restric
 }
 
 template <int D, int R, int KC>
-hipError_t launch_strip_kc(const LaunchArgs& a, LaunchTimer* timer, const float* prefix,
+hipError_t launch_strip_kc(const LaunchArgs& a, Launcher& L, const float* prefix,
                            float scale2) {
   using C = CausalCfg<D, R, KC>;
   static std::atomic<unsigned long long> lds_set{0};
-  if (const hipError_t e = lds_limit_once((const void*)k_causal_strip<D, R, KC>, C::LDS, lds_set);
-      e != hipSuccess)
-    return e;
-  launch_timed(timer, FMM_KERNEL_CAUSAL_APPLY, k_causal_strip<D, R, KC>, dim3(a.B * a.H * a.nseg),
+  if (L.note(lds_limit_once((const void*)k_causal_strip<D, R, KC>, C::LDS, lds_set)) !=
+      hipSuccess)
+    return L.err;
+  L(FMM_KERNEL_CAUSAL_APPLY, k_causal_strip<D, R, KC>, dim3(a.B * a.H * a.nseg),
                dim3(CNT), (size_t)C::LDS, (hipStream_t)a.stream, (const bf16_t*)a.q,
                (const bf16_t*)a.k, (const bf16_t*)a.v, (bf16_t*)a.out, prefix, a.w_near,
                a.w_far, a.H, a.N, a.band_k, a.L, a.nseg, scale2);
-  return hipGetLastError();
+  return L.err;
 }
 
 template <int D, int R>
-hipError_t launch_strip_d(const LaunchArgs& a, LaunchTimer* t, const float* prefix,
+hipError_t launch_strip_d(const LaunchArgs& a, Launcher& t, const float* prefix,
                           float scale2) {
   return a.band_k <= 32 ? launch_strip_kc<D, R, 1>(a, t, prefix, scale2)
                         : launch_strip_kc<D, R, 2>(a, t, prefix, scale2);
@@ -540,7 +540,7 @@ bool causal_strip_applies(int dtype, int d, int band_k, int causal, long long n)
          n * d * 2 < (1LL << 31);
 }
 
-hipError_t launch_causal_strip(const LaunchArgs& a, LaunchTimer* t, const float* prefix) {
+hipError_t launch_causal_strip(const LaunchArgs& a, Launcher& t, const float* prefix) {
   const float scale2 = 1.4426950408889634f / sqrtf((float)a.d);
   switch (a.d * 4 + a.rank) {
     case 32 * 4 + 1: return launch_strip_d<32, 1>(a, t, prefix, scale2);

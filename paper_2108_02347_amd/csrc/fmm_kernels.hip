@@ -900,13 +900,15 @@ __global__ __launch_bounds__(SNT) void k_seg_state(const T* __restrict__ k,
 template <bool CAUSAL>
 __global__ __launch_bounds__(256) void k_state_combine(float* __restrict__ part,
                                                        float* __restrict__ fin, int nseg,
-                                                       int rec) {
+                                                       int rec, int nchunk) {
   // the causal scan keeps the first CACHE values of its range in registers
   // between the two passes, so each record is read from memory once
   constexpr int CACHE = CAUSAL ? 32 : 1;
   __shared__ float tot[4][64];
   const int el = threadIdx.x & 63, qr = threadIdx.x >> 6;
-  const int e = blockIdx.x * 64 + el, bh = blockIdx.y;
+  // one-dimensional grid: (batch, head) slice major, 64-element chunk minor
+  const int bh = blockIdx.x / nchunk;
+  const int e = (blockIdx.x - bh * nchunk) * 64 + el;
   const int per = (nseg + 3) / 4;
   const int s0 = min(nseg, qr * per), s1 = min(nseg, s0 + per);
   float* p = part + (size_t)bh * nseg * rec + e;
@@ -1311,7 +1313,7 @@ __global__ __launch_bounds__(NT) void k_causal_rounds(const T* __restrict__ q,
 
 // ------------------------------------------------------------------ launchers
 template <typename T, int D, int R>
-static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
+static hipError_t launch_all(const LaunchArgs& a, Launcher& L) {
   using RG = Ring<T, D, R>;
   const int BH = a.B * a.H;
   const float scale2 = 1.4426950408889634f / sqrtf((float)D);
@@ -1322,7 +1324,9 @@ static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
   const T* v = (const T*)a.v;
   T* o = (T*)a.out;
   float* part = a.ws;
-  float* fin = a.ws + (size_t)BH * a.nseg * REC;
+  // (integer arithmetic: the dry pass runs with no workspace yet)
+  float* fin = reinterpret_cast<float*>(reinterpret_cast<uintptr_t>(a.ws) +
+                                        (size_t)BH * a.nseg * REC * sizeof(float));
   const int kc = (a.band_k + 31) / 32;
   const int U = a.causal ? 2 + kc : 2 + 2 * kc;
   const bool ring = U <= (a.causal ? RG::U_C : RG::U_NC);
@@ -1330,80 +1334,79 @@ static hipError_t launch_all(const LaunchArgs& a, LaunchTimer* timer) {
   {
     static std::atomic<unsigned long long> set_band{0}, set_causal{0}, set_brounds{0},
         set_crounds{0};
-    hipError_t e;
-    if ((e = lds_limit_once((const void*)k_band_ring<T, D, R>, (int)RG::bytes(RG::U_NC, false),
-                            set_band)) != hipSuccess ||
-        (e = lds_limit_once((const void*)k_causal_ring<T, D, R>, (int)RG::bytes(RG::U_C, true),
-                            set_causal)) != hipSuccess ||
-        (e = lds_limit_once((const void*)k_band_rounds<T, D, R>, (int)RG::bytes(RG::UR, false),
-                            set_brounds)) != hipSuccess ||
-        (e = lds_limit_once((const void*)k_causal_rounds<T, D, R>, (int)RG::bytes(RG::UR, true),
-                            set_crounds)) != hipSuccess)
-      return e;
+    if (L.note(lds_limit_once((const void*)k_band_ring<T, D, R>, (int)RG::bytes(RG::U_NC, false),
+                              set_band)) != hipSuccess ||
+        L.note(lds_limit_once((const void*)k_causal_ring<T, D, R>, (int)RG::bytes(RG::U_C, true),
+                              set_causal)) != hipSuccess ||
+        L.note(lds_limit_once((const void*)k_band_rounds<T, D, R>, (int)RG::bytes(RG::UR, false),
+                              set_brounds)) != hipSuccess ||
+        L.note(lds_limit_once((const void*)k_causal_rounds<T, D, R>,
+                              (int)RG::bytes(RG::UR, true), set_crounds)) != hipSuccess)
+      return L.err;
   }
 
   // long chunks once a segment spans at least four of them
   constexpr int TKL = 32 * (SW / (D / 16));
   if (TKL > 64 && a.L >= 4 * TKL)
-    launch_timed(timer, FMM_KERNEL_SEG_STATE, k_seg_state<T, D, R, TKL>, dim3(a.nseg * BH),
-                 dim3(SNT), 0, s, k, v, part, a.N, a.L, a.nseg);
+    L(FMM_KERNEL_SEG_STATE, k_seg_state<T, D, R, TKL>, dim3(a.nseg * BH), dim3(SNT), 0, s, k, v,
+      part, a.N, a.L, a.nseg);
   else
-    launch_timed(timer, FMM_KERNEL_SEG_STATE, k_seg_state<T, D, R, 64>, dim3(a.nseg * BH),
-                 dim3(SNT), 0, s, k, v, part, a.N, a.L, a.nseg);
-  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    L(FMM_KERNEL_SEG_STATE, k_seg_state<T, D, R, 64>, dim3(a.nseg * BH), dim3(SNT), 0, s, k, v,
+      part, a.N, a.L, a.nseg);
 
-  const dim3 cgrid((REC + 63) / 64, BH);
+  const int nchunk = (REC + 63) / 64;
+  // (clamped: a grid this large fails the dry pass's dispatch-limit check)
+  const dim3 cgrid((unsigned)std::min<long long>((long long)nchunk * BH, 0xFFFFFFFFll));
   if (a.causal)
-    launch_timed(timer, FMM_KERNEL_STATE_COMBINE, k_state_combine<true>, cgrid, dim3(256), 0, s, part,
-           fin, a.nseg, REC);
+    L(FMM_KERNEL_STATE_COMBINE, k_state_combine<true>, cgrid, dim3(256), 0, s, part, fin, a.nseg,
+      REC, nchunk);
   else
-    launch_timed(timer, FMM_KERNEL_STATE_COMBINE, k_state_combine<false>, cgrid, dim3(256), 0, s, part,
-           fin, a.nseg, REC);
-  if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+    L(FMM_KERNEL_STATE_COMBINE, k_state_combine<false>, cgrid, dim3(256), 0, s, part, fin,
+      a.nseg, REC, nchunk);
 
   if (a.causal) {
     if (causal_strip_applies(a.dtype, a.d, a.band_k, a.causal, a.N))
-      return launch_causal_strip(a, timer, part);
+      return launch_causal_strip(a, L, part);
     if (ring)
-      launch_timed(timer, FMM_KERNEL_CAUSAL_APPLY, k_causal_ring<T, D, R>, dim3(BH * a.nseg), dim3(NT),
-             lds, s, q, k, v, o, (const float*)part, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L,
-             a.nseg, scale2);
+      L(FMM_KERNEL_CAUSAL_APPLY, k_causal_ring<T, D, R>, dim3(BH * a.nseg), dim3(NT), lds, s, q,
+        k, v, o, (const float*)part, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L, a.nseg, scale2);
     else
-      launch_timed(timer, FMM_KERNEL_CAUSAL_APPLY, k_causal_rounds<T, D, R>, dim3(BH * a.nseg),
-             dim3(NT), lds, s, q, k, v, o, (const float*)part, a.w_near, a.w_far, a.H, a.N,
-             a.band_k, a.L, a.nseg, scale2);
+      L(FMM_KERNEL_CAUSAL_APPLY, k_causal_rounds<T, D, R>, dim3(BH * a.nseg), dim3(NT), lds, s,
+        q, k, v, o, (const float*)part, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L, a.nseg,
+        scale2);
   } else {
     if (band_pair_applies(a.dtype, a.d, a.band_k, a.causal, a.N)) {
-      return launch_band_pair(a, timer, fin);
+      return launch_band_pair(a, L, fin);
     } else if (ring) {
-      launch_timed(timer, FMM_KERNEL_BAND_APPLY, k_band_ring<T, D, R>, dim3(BH * a.nseg_apply),
-             dim3(NT), lds, s, q, k, v, o, (const float*)fin, a.w_near, a.w_far, a.H, a.N,
-             a.band_k, a.L_apply, a.nseg_apply, scale2);
+      L(FMM_KERNEL_BAND_APPLY, k_band_ring<T, D, R>, dim3(BH * a.nseg_apply), dim3(NT), lds, s,
+        q, k, v, o, (const float*)fin, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L_apply,
+        a.nseg_apply, scale2);
     } else {
-      const int ntile = (a.N + TM - 1) / TM;
-      launch_timed(timer, FMM_KERNEL_BAND_APPLY, k_band_rounds<T, D, R>, dim3(BH * ntile), dim3(NT),
-             lds, s, q, k, v, o, (const float*)fin, a.w_near, a.w_far, a.H, a.N, a.band_k, ntile,
-             scale2);
+      const long long ntile = (a.N + TM - 1) / TM;
+      if ((long long)BH * ntile > 0x7FFFFFFFLL) return L.note(hipErrorInvalidConfiguration);
+      L(FMM_KERNEL_BAND_APPLY, k_band_rounds<T, D, R>, dim3((unsigned)(BH * ntile)), dim3(NT),
+        lds, s, q, k, v, o, (const float*)fin, a.w_near, a.w_far, a.H, a.N, a.band_k,
+        (int)ntile, scale2);
     }
   }
-  return hipGetLastError();
+  return L.err;
 }
 
 template <typename T>
-static hipError_t dispatch_d(const LaunchArgs& a, LaunchTimer* t) {
+static hipError_t dispatch_d(const LaunchArgs& a, Launcher& L) {
   switch (a.d * 4 + a.rank) {
-    case 16 * 4 + 1: return launch_all<T, 16, 1>(a, t);
-    case 16 * 4 + 2: return launch_all<T, 16, 2>(a, t);
-    case 32 * 4 + 1: return launch_all<T, 32, 1>(a, t);
-    case 32 * 4 + 2: return launch_all<T, 32, 2>(a, t);
-    case 64 * 4 + 1: return launch_all<T, 64, 1>(a, t);
-    case 64 * 4 + 2: return launch_all<T, 64, 2>(a, t);
-    default: return hipErrorInvalidValue;
+    case 16 * 4 + 1: return launch_all<T, 16, 1>(a, L);
+    case 16 * 4 + 2: return launch_all<T, 16, 2>(a, L);
+    case 32 * 4 + 1: return launch_all<T, 32, 1>(a, L);
+    case 32 * 4 + 2: return launch_all<T, 32, 2>(a, L);
+    case 64 * 4 + 1: return launch_all<T, 64, 1>(a, L);
+    case 64 * 4 + 2: return launch_all<T, 64, 2>(a, L);
+    default: return L.note(hipErrorInvalidValue);
   }
 }
 
-hipError_t launch_forward(const LaunchArgs& a, LaunchTimer* t) {
-  return a.dtype == FMM_DTYPE_BF16 ? dispatch_d<bf16_t>(a, t) : dispatch_d<float>(a, t);
+hipError_t launch_forward(const LaunchArgs& a, Launcher& L) {
+  return a.dtype == FMM_DTYPE_BF16 ? dispatch_d<bf16_t>(a, L) : dispatch_d<float>(a, L);
 }
 
 int tile_rows() { return TM; }

@@ -5,6 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 
+#include <algorithm>
 #include <atomic>
 
 #include "../../include/fmm_attn.h"
@@ -42,13 +43,46 @@ template <typename F, typename... Args>
 inline void launch_timed(LaunchTimer* t, int id, F kern, dim3 grid, dim3 block, size_t shm,
                          hipStream_t s, Args... args) {
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (t->take(id, &e0, &e1)) {
+  if (t && t->take(id, &e0, &e1)) {
     hipExtLaunchKernelGGL(kern, grid, block, (uint32_t)shm, s, e0, e1, 0, args...);
     t->commit(id, e0, e1);
   } else {
     hipLaunchKernelGGL(kern, grid, block, shm, s, args...);
   }
 }
+
+// Runs the launch sequence of one forward call in two passes over the same
+// code: a dry pass that only checks every grid against the dispatch limits
+// (work-items per dimension below 2^32) and raises the kernels' LDS limits,
+// then the real pass that enqueues.  A call that fails the dry pass therefore
+// enqueues nothing.  The first error stops every later launch.
+struct Launcher {
+  LaunchTimer* timer = nullptr;
+  bool dry = false;
+  hipError_t err = hipSuccess;
+
+  template <typename F, typename... Args>
+  void operator()(int id, F kern, dim3 grid, dim3 block, size_t shm, hipStream_t s,
+                  Args... args) {
+    if (err != hipSuccess) return;
+    if (dry) {
+      const unsigned long long lim = 0xFFFFFFFFull;
+      if (grid.x == 0 || grid.y == 0 || grid.z == 0 ||
+          (unsigned long long)grid.x * block.x > lim ||
+          (unsigned long long)grid.y * block.y > lim ||
+          (unsigned long long)grid.z * block.z > lim)
+        err = hipErrorInvalidConfiguration;
+      return;
+    }
+    launch_timed(timer, id, kern, grid, block, shm, s, args...);
+    err = hipGetLastError();
+  }
+  // records the result of a host-side step (an LDS attribute, a dispatch)
+  hipError_t note(hipError_t e) {
+    if (err == hipSuccess) err = e;
+    return err;
+  }
+};
 
 // Raises a kernel's dynamic LDS limit to `bytes` on the current device, once
 // per device (HIP keeps the attribute per device); `done` is the caller's
@@ -70,7 +104,8 @@ inline hipError_t lds_limit_once(const void* kern, int bytes,
   return e;
 }
 
-hipError_t launch_forward(const LaunchArgs& a, LaunchTimer* timer);
+// Enqueues the forward operator (or, with L.dry, only checks and prepares it).
+hipError_t launch_forward(const LaunchArgs& a, Launcher& L);
 int tile_rows();
 
 // Non-causal apply with two 16-row strips per wavefront (fmm_pair.hip): bf16,
@@ -78,12 +113,25 @@ int tile_rows();
 // pair_tile_rows().
 bool band_pair_applies(int dtype, int d, int band_k, int causal, long long n);
 int pair_tile_rows();
-hipError_t launch_band_pair(const LaunchArgs& a, LaunchTimer* timer, const float* fin);
+hipError_t launch_band_pair(const LaunchArgs& a, Launcher& L, const float* fin);
 
 // Causal apply with one 16-row strip per wavefront (fmm_causal.hip): bf16,
 // d = 32 or 64, band half-width <= 64; walks the state segments (a.L rows,
 // a multiple of tile_rows()) from their exclusive prefix records.
 bool causal_strip_applies(int dtype, int d, int band_k, int causal, long long n);
-hipError_t launch_causal_strip(const LaunchArgs& a, LaunchTimer* timer, const float* prefix);
+hipError_t launch_causal_strip(const LaunchArgs& a, Launcher& L, const float* prefix);
+
+// The C ABI's host logic (fmm_api.cpp), shared with the no-allocation entry
+// point (fmm_noalloc.hip): argument checks, the workspace size of the call's
+// segment plan, and the checked launch with a given workspace.
+int validate_forward(const void* q, const void* k, const void* v, void* out, int B, int H,
+                     int N, int d, int band_k, int rank, int causal, const float* w_near,
+                     const float* w_far, int dtype);
+size_t forward_workspace_bytes(int B, int H, int N, int d, int band_k, int rank, int causal,
+                               int dtype);
+int forward_with_workspace(const void* q, const void* k, const void* v, void* out, int B, int H,
+                           int N, int d, int band_k, int rank, int causal, const float* w_near,
+                           const float* w_far, int dtype, void* ws, size_t ws_bytes,
+                           void* stream);
 
 }  // namespace fmm

@@ -392,23 +392,22 @@ __global__ __launch_bounds__(PNT, 2) void k_band_pair(const bf16_t* __restrict__
 }
 
 template <int D, int R, int KC>
-hipError_t launch_pair_kc(const LaunchArgs& a, LaunchTimer* timer, const float* fin,
+hipError_t launch_pair_kc(const LaunchArgs& a, Launcher& L, const float* fin,
                           float scale2) {
   using C = PairCfg<D, R, KC>;
   static std::atomic<unsigned long long> lds_set{0};
-  if (const hipError_t e = lds_limit_once((const void*)k_band_pair<D, R, KC>, C::LDS, lds_set);
-      e != hipSuccess)
-    return e;
-  launch_timed(timer, FMM_KERNEL_BAND_APPLY, k_band_pair<D, R, KC>,
+  if (L.note(lds_limit_once((const void*)k_band_pair<D, R, KC>, C::LDS, lds_set)) != hipSuccess)
+    return L.err;
+  L(FMM_KERNEL_BAND_APPLY, k_band_pair<D, R, KC>,
                dim3(a.B * a.H * a.nseg_apply), dim3(PNT), (size_t)C::LDS,
                (hipStream_t)a.stream, (const bf16_t*)a.q, (const bf16_t*)a.k,
                (const bf16_t*)a.v, (bf16_t*)a.out, fin, a.w_near, a.w_far, a.H, a.N, a.band_k,
                a.L_apply, a.nseg_apply, scale2);
-  return hipGetLastError();
+  return L.err;
 }
 
 template <int D, int R>
-hipError_t launch_pair_d(const LaunchArgs& a, LaunchTimer* t, const float* fin, float scale2) {
+hipError_t launch_pair_d(const LaunchArgs& a, Launcher& t, const float* fin, float scale2) {
   return a.band_k <= 32 ? launch_pair_kc<D, R, 1>(a, t, fin, scale2)
                         : launch_pair_kc<D, R, 2>(a, t, fin, scale2);
 }
@@ -423,7 +422,7 @@ bool band_pair_applies(int dtype, int d, int band_k, int causal, long long n) {
 
 int pair_tile_rows() { return PTM; }
 
-hipError_t launch_band_pair(const LaunchArgs& a, LaunchTimer* t, const float* fin) {
+hipError_t launch_band_pair(const LaunchArgs& a, Launcher& t, const float* fin) {
   const float scale2 = 1.4426950408889634f / sqrtf((float)a.d);
   switch (a.d * 4 + a.rank) {
     case 32 * 4 + 1: return launch_pair_d<32, 1>(a, t, fin, scale2);

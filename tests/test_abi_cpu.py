@@ -92,3 +92,32 @@ def test_binding_rejects_host_tensors_and_wrong_rank():
         binding.forward(q, q, q, w, w, 2, 1, 0)
     with pytest.raises(ValueError):
         binding.forward(q[0], q[0], q[0], w, w, 2, 1, 0)
+
+
+def test_host_validation_huge_shapes():
+    # element counts beyond int64 are rejected before any arithmetic can wrap
+    big = 2**31 - 1
+    assert call(B=big, H=big, N=big, d=64) == binding.FMM_ERR_INVALID_ARG
+    assert call(B=big, H=big, N=big, d=16, bf16=True) == binding.FMM_ERR_INVALID_ARG
+    # B*H beyond int32 (the launchers count slices in int): unsupported, with
+    # addresses far enough apart that the operands do not overlap
+    T = 1 << 40
+    assert (binding.raw_forward(T, 2 * T, 3 * T, 4 * T, 65536, 65536, 1, 16, 0, 1, 0,
+                                5 * T, 6 * T, 0, False) == binding.FMM_ERR_UNSUPPORTED)
+
+
+def test_binding_rejects_bad_out_and_workspace():
+    # out and workspace are checked by the binding: the library gets only
+    # their addresses (and the workspace's size)
+    import torch
+    q = torch.zeros(1, 2, 8, 16)
+    w = torch.zeros(2)
+    with pytest.raises(ValueError):
+        binding._check_out(torch.zeros(1, 2, 8, 16, dtype=torch.bfloat16), q)
+    with pytest.raises(ValueError):
+        binding._check_out(torch.zeros(1, 2, 8, 15), q)
+    with pytest.raises(ValueError):
+        binding._check_out(torch.zeros(1, 2, 16, 8).transpose(2, 3), q)
+    with pytest.raises(ValueError):
+        binding._check_out(None, q)
+    binding._check_out(torch.zeros(1, 2, 8, 16), q)

@@ -287,3 +287,80 @@ def test_large_magnitude_inputs(causal):
     for d, kw, dtype in ((64, 64, "bf16"), (32, 20, "bf16"), (64, 7, "f32"), (16, 40, "f32")):
         worst = max(worst, check_full(1, 2, 1500, d, kw, 2, causal, dtype, 700 + d + kw, 4.0))
     log(f"std-4 inputs causal={causal}: worst {worst:.3e}")
+
+
+# ------------------------------------------------------------------ contract: streams, limits, grids
+def test_null_stream_matches_current_stream():
+    # stream argument NULL = the default stream
+    q, k, v, wn, wf = make_inputs(2, 2, 700, 32, "bf16", 1.0, 61)
+    tq, tk, tv, twn, twf = upload(q, k, v, wn, wf, "bf16")
+    for causal in (0, 1):
+        ref_out = binding.forward(tq, tk, tv, twn, twf, 9, 2, causal)
+        torch.cuda.synchronize()
+        out = torch.empty_like(tq)
+        st = binding.raw_forward(tq.data_ptr(), tk.data_ptr(), tv.data_ptr(), out.data_ptr(),
+                                 2, 2, 700, 32, 9, 2, causal, twn.data_ptr(), twf.data_ptr(),
+                                 0, True)
+        assert st == binding.FMM_OK
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), ref_out.view(torch.int16))
+
+
+def test_workspace_limit_reports_oom(monkeypatch):
+    # FMM_ATTN_WS_LIMIT caps the library-owned workspace; a call that would
+    # need more returns FMM_ERR_OOM with nothing enqueued
+    q, k, v, wn, wf = make_inputs(1, 2, 2000, 32, "f32", 1.0, 67)
+    tq, tk, tv, twn, twf = upload(q, k, v, wn, wf, "f32")
+    out = torch.full_like(tq, 5.0)
+    need = binding.workspace_bytes(1, 2, 2000, 32, 2, 0)
+    monkeypatch.setenv("FMM_ATTN_WS_LIMIT", str(need - 1))
+    with pytest.raises(binding.FmmError) as ei:
+        binding.forward(tq, tk, tv, twn, twf, 5, 2, 0, out=out)
+    assert ei.value.status == binding.FMM_ERR_OOM
+    torch.cuda.synchronize()
+    assert bool((out == 5.0).all())
+    monkeypatch.setenv("FMM_ATTN_WS_LIMIT", str(need))
+    binding.forward(tq, tk, tv, twn, twf, 5, 2, 0, out=out)
+    torch.cuda.synchronize()
+    want = ref.fmm_attention_stream(q, k, v, wn, wf, 5, 2, False)
+    assert slice_errors(out.double().cpu().numpy(), want).max() <= TOL["f32"]
+
+
+@pytest.mark.parametrize("causal", [0, 1])
+def test_more_slices_than_a_grid_dimension(causal):
+    # B*H = 70000 > 65535 slices: every kernel takes the slices on grid x
+    q, k, v, wn, wf = make_inputs(35000, 2, 3, 16, "f32", 1.0, 71 + causal)
+    got = run_gpu(q, k, v, wn, wf, 1, 2, causal, "f32")
+    want = ref.fmm_attention_stream(q, k, v, wn, wf, 1, 2, bool(causal))
+    err = slice_errors(got, want).max()
+    log(f"70000 slices causal={causal}: max slice error {err:.3e}")
+    assert err <= TOL["f32"]
+
+
+def test_grid_beyond_dispatch_limit_is_rejected():
+    # 2^23 + 1 slices of one row: the state kernel's grid (512 work-items per
+    # workgroup) would exceed 2^32 work-items; rejected before any launch
+    B = (1 << 23) + 1
+    t = [torch.zeros(B, 1, 1, 16, device="cuda:0") for _ in range(3)]
+    out = torch.full_like(t[0], 3.0)
+    w = torch.zeros(1, device="cuda:0")
+    st = binding.raw_forward(t[0].data_ptr(), t[1].data_ptr(), t[2].data_ptr(), out.data_ptr(),
+                             B, 1, 1, 16, 0, 1, 0, w.data_ptr(), w.data_ptr(),
+                             torch.cuda.current_stream().cuda_stream, False)
+    assert st == binding.FMM_ERR_UNSUPPORTED
+    torch.cuda.synchronize()
+    assert bool((out == 3.0).all())
+
+
+def test_binding_rejects_bad_out_on_device():
+    q, k, v, wn, wf = make_inputs(1, 2, 64, 16, "bf16", 1.0, 73)
+    tq, tk, tv, twn, twf = upload(q, k, v, wn, wf, "bf16")
+    for bad in (torch.empty_like(tq, dtype=torch.float32),      # fp32 out for bf16 inputs
+                torch.empty(1, 2, 63, 16, dtype=torch.bfloat16, device="cuda:0"),
+                torch.empty(1, 2, 16, 64, dtype=torch.bfloat16, device="cuda:0").transpose(2, 3),
+                torch.empty(1, 2, 64, 16, dtype=torch.bfloat16)):   # host tensor
+        with pytest.raises(ValueError):
+            binding.forward(tq, tk, tv, twn, twf, 3, 2, 0, out=bad)
+    ws = torch.empty(binding.workspace_bytes(1, 2, 64, 16, 2, 0), dtype=torch.uint8)
+    with pytest.raises(ValueError):
+        binding.forward_ws(tq, tk, tv, twn, twf, 3, 2, 0, ws)       # host workspace
