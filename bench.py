@@ -128,13 +128,6 @@ def trace_summary(stats_csv):
         _, d4 = _durations(window, needle)
         n4["instep"][key] = statistics.mean(d4[warm:warm + steps])
         n4["events"][key] = statistics.mean(d4[warm + steps:warm + 2 * steps])
-    span = sorted(window, key=lambda r: int(r["Start_Timestamp"]))
-    # in-step time per call: from the first timed call's first dispatch to
-    # the last timed call's last dispatch
-    calls = [r for r in span if N4096_KERNELS["band_apply"] in r["Kernel_Name"]]
-    firsts = [r for r in span if N4096_KERNELS["seg_state"] in r["Kernel_Name"]]
-    n4["instep_call_us"] = (int(calls[warm + steps - 1]["End_Timestamp"])
-                            - int(firsts[warm]["Start_Timestamp"])) / 1e3 / steps
     rec = {"kernel_source_hash": kernel_source_hash(), "stress64k_instep_us": instep,
            "stress64k_events_us": events, "n4096": n4}
     with open(TRACE_JSON, "w") as f:
@@ -158,8 +151,7 @@ def trace_summary(stats_csv):
                     f"{instep[key]:.2f} | {events[key]:.2f} |\n")
         for key in n4["instep"]:
             f.write(f"| N=4096 | {key} | {n4['instep'][key]:.2f} | {n4['events'][key]:.2f} |\n")
-        f.write(f"\nN=4096: {n4['instep_call_us']:.2f} us per call in the timed loop "
-                "(first dispatch of the first timed call to the end of the last).\n\n")
+        f.write("\n")
         f.write("rocprofv3's own kernel_stats.csv over the whole run (every leg, both "
                 "modes; names shortened to the kernel template):\n\n")
         f.write("| kernel | calls | avg us | min us | max us | share % |\n|---|---|---|---|---|---|\n")
@@ -304,13 +296,19 @@ def read_counters(kernel: str):
         return None
 
 
+# the sources of the kernels the profiles describe (host-side code excluded,
+# so a change to argument checks or bindings does not void them)
+KERNEL_SOURCES = ("fmm_device.h", "fmm_oct.h", "fmm_kernels.hip", "fmm_pair.hip",
+                  "fmm_causal.hip")
+
+
 def kernel_source_hash() -> str:
     """Hash of the kernel sources with comments and blank space removed, so a
     comment edit does not void counter summaries taken with the same code."""
     import re
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2108_02347_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    for name in KERNEL_SOURCES:
         with open(os.path.join(csrc, name), encoding="utf-8") as f:
             text = f.read()
         text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
