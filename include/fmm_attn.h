@@ -67,6 +67,8 @@ extern "C" {
 #define FMM_ERR_HIP         (-3) /* a HIP runtime call or kernel launch failed */
 #define FMM_ERR_OOM         (-4) /* workspace allocation failed, or a
                                     caller-provided workspace is too small */
+#define FMM_ERR_SCRATCH     (-5) /* fmm_attn_forward_noalloc: the shape needs
+                                    more scratch than its fixed array holds */
 
 /* dtype codes for fmm_attn_forward_ws */
 #define FMM_DTYPE_F32  0
@@ -132,6 +134,29 @@ int fmm_attn_forward_ws(const void* q, const void* k, const void* v, void* out,
                         int B, int H, int N, int d, int band_k, int rank,
                         int causal, const float* w_near, const float* w_far,
                         int dtype, void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * fmm_attn_forward_noalloc - the same operator for callers that cannot
+ * allocate device memory (code under stream capture, serving loops, harnesses
+ * that forbid allocation).  It allocates nothing: the far-field segment
+ * records go to a fixed device array of fmm_attn_noalloc_max_bytes() bytes
+ * (32 MiB) that the library holds on every GPU it runs on until the process
+ * ends.  Arguments as fmm_attn_forward_ws without the workspace; dtype is
+ * FMM_DTYPE_F32 or FMM_DTYPE_BF16.  Returns FMM_ERR_SCRATCH, with nothing
+ * enqueued, when fmm_attn_workspace_bytes(...) of the shape exceeds that size.
+ * All calls on one GPU share its array: calls that can overlap in time on one
+ * GPU (different streams without ordering between them) race and must not be
+ * made; calls on one stream are ordered by it.  Every value the kernels read
+ * from the array is written earlier in the same call, so nothing needs
+ * clearing between calls.
+ */
+int fmm_attn_forward_noalloc(const void* q, const void* k, const void* v, void* out,
+                             int B, int H, int N, int d, int band_k, int rank,
+                             int causal, const float* w_near, const float* w_far,
+                             int dtype, void* stream);
+
+/* Size in bytes of fmm_attn_forward_noalloc's fixed per-GPU array. */
+size_t fmm_attn_noalloc_max_bytes(void);
 
 /* Human-readable text for a status code; never NULL, static storage. */
 const char* fmm_attn_status_string(int status);

@@ -19,6 +19,7 @@ FMM_ERR_INVALID_ARG = -1
 FMM_ERR_UNSUPPORTED = -2
 FMM_ERR_HIP = -3
 FMM_ERR_OOM = -4
+FMM_ERR_SCRATCH = -5
 
 FMM_DTYPE_F32 = 0
 FMM_DTYPE_BF16 = 1
@@ -29,6 +30,7 @@ EXPORTS = (
     "fmm_attn_forward", "fmm_attn_forward_bf16", "fmm_attn_workspace_bytes",
     "fmm_attn_forward_ws", "fmm_attn_status_string", "fmm_attn_release_workspace",
     "fmm_attn_version", "fmm_attn_kernel_timing", "fmm_attn_kernel_timing_read",
+    "fmm_attn_forward_noalloc", "fmm_attn_noalloc_max_bytes",
 )
 
 _lib = None
@@ -58,6 +60,10 @@ def lib() -> ctypes.CDLL:
         fn.restype = ci
     h.fmm_attn_forward_ws.argtypes = fwd_args[:-1] + [ci, vp, ctypes.c_size_t, vp]
     h.fmm_attn_forward_ws.restype = ci
+    h.fmm_attn_forward_noalloc.argtypes = fwd_args[:-1] + [ci, vp]
+    h.fmm_attn_forward_noalloc.restype = ci
+    h.fmm_attn_noalloc_max_bytes.argtypes = []
+    h.fmm_attn_noalloc_max_bytes.restype = ctypes.c_size_t
     h.fmm_attn_workspace_bytes.argtypes = [ci] * 6
     h.fmm_attn_workspace_bytes.restype = ctypes.c_size_t
     h.fmm_attn_status_string.argtypes = [ci]
@@ -177,6 +183,26 @@ def forward_ws(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool, wor
         int(bool(causal)), _ptr(w_near), _ptr(w_far), dt, _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream_of(q)))
     return out
+
+
+def forward_noalloc(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool, out=None):
+    """Same operator through the entry point that allocates nothing in the
+    library (its scratch is a fixed per-GPU array); `out` may be given so that
+    the call allocates nothing at all."""
+    B, H, N, d = _prep(q, k, v, w_near, w_far)
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _check_out(out, q)
+    dt = FMM_DTYPE_BF16 if q.dtype == torch.bfloat16 else FMM_DTYPE_F32
+    _check(lib().fmm_attn_forward_noalloc(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, int(band_k), int(rank),
+        int(bool(causal)), _ptr(w_near), _ptr(w_far), dt, _stream_of(q)))
+    return out
+
+
+def noalloc_max_bytes() -> int:
+    return int(lib().fmm_attn_noalloc_max_bytes())
 
 
 def raw_forward(q_ptr, k_ptr, v_ptr, out_ptr, B, H, N, d, band_k, rank, causal, wn_ptr,

@@ -328,6 +328,8 @@ const char* fmm_attn_status_string(int status) {
     case FMM_ERR_UNSUPPORTED: return "FMM_ERR_UNSUPPORTED: d must be 16, 32 or 64 and rank 1 or 2";
     case FMM_ERR_HIP: return "FMM_ERR_HIP: a HIP runtime call or kernel launch failed";
     case FMM_ERR_OOM: return "FMM_ERR_OOM: workspace allocation failed or workspace too small";
+    case FMM_ERR_SCRATCH:
+      return "FMM_ERR_SCRATCH: the shape needs more scratch than the fixed no-allocation array";
     default: return "unknown fmm_attn status";
   }
 }

@@ -31,10 +31,10 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     assert binding.version() == 10000
-    for st in (0, -1, -2, -3, -4):
+    for st in (0, -1, -2, -3, -4, -5):
         assert binding.status_string(st).startswith(
             {0: "FMM_OK", -1: "FMM_ERR_INVALID_ARG", -2: "FMM_ERR_UNSUPPORTED",
-             -3: "FMM_ERR_HIP", -4: "FMM_ERR_OOM"}[st])
+             -3: "FMM_ERR_HIP", -4: "FMM_ERR_OOM", -5: "FMM_ERR_SCRATCH"}[st])
     assert "unknown" in binding.status_string(17)
 
 
@@ -121,3 +121,17 @@ def test_binding_rejects_bad_out_and_workspace():
     with pytest.raises(ValueError):
         binding._check_out(None, q)
     binding._check_out(torch.zeros(1, 2, 8, 16), q)
+
+
+def test_noalloc_host_checks():
+    # argument errors come first; a shape needing more than the fixed array is
+    # refused on the host (no GPU is touched on either path)
+    lib = binding.lib()
+    assert binding.noalloc_max_bytes() == 32 << 20
+    T = 1 << 40
+    vp = ctypes.c_void_p
+    args = lambda q, H, N: (vp(q), vp(2 * T), vp(3 * T), vp(4 * T), 1, H, N, 64, 64, 2, 1,
+                            vp(5 * T), vp(6 * T), 1, vp(0))
+    assert lib.fmm_attn_forward_noalloc(*args(0, 1024, 64)) == binding.FMM_ERR_INVALID_ARG
+    assert binding.workspace_bytes(1, 1024, 64, 64, 2, 1) > binding.noalloc_max_bytes()
+    assert lib.fmm_attn_forward_noalloc(*args(T, 1024, 64)) == binding.FMM_ERR_SCRATCH
