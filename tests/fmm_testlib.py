@@ -43,6 +43,14 @@ def slice_errors(got: np.ndarray, want: np.ndarray) -> np.ndarray:
     return num / np.maximum(den, 1e-30)
 
 
+def floored_mean_rel_error(got: np.ndarray, want: np.ndarray) -> float:
+    """Mean over all elements of |g - o| / max(|o|, 1e-3 max|o|), the floor
+    taken per (b, h) slice: an elementwise measure that the max-normalised
+    slice error can hide on small outputs."""
+    floor = 1e-3 * np.abs(want).max(axis=(-2, -1), keepdims=True)
+    return float((np.abs(got - want) / np.maximum(np.abs(want), np.maximum(floor, 1e-30))).mean())
+
+
 def check_full(B, H, N, d, band_k, rank, causal, dtype, seed, std=1.0, wn=None, wf=None):
     q, k, v, wn0, wf0 = make_inputs(B, H, N, d, dtype, std, seed)
     wn = wn0 if wn is None else wn
@@ -53,5 +61,7 @@ def check_full(B, H, N, d, band_k, rank, causal, dtype, seed, std=1.0, wn=None, 
     want = ref.fmm_attention_stream(q, k, v, wn, wf, band_k, rank, bool(causal))
     assert np.isfinite(got).all(), "non-finite GPU output"
     err = slice_errors(got, want).max()
+    log(f"  max slice error {err:.3e}, floored mean relative error "
+        f"{floored_mean_rel_error(got, want):.3e}")
     assert err <= TOL[dtype], f"max slice error {err:.3e} > {TOL[dtype]}"
     return err

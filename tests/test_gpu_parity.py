@@ -81,6 +81,44 @@ def test_n4096_b128_sampled_rows():
     assert worst <= TOL["bf16"]
 
 
+@pytest.mark.parametrize("causal", [0, 1])
+def test_multi_tile_walks_full_output(causal):
+    # B*H = 128 slices of 2048 rows at d = 64, k = 64 (bf16): the non-causal
+    # pair kernel walks four 128-row tiles per workgroup (ring slide and
+    # prefetch across tiles), the causal strip kernel several 64-row tiles per
+    # state segment.  Eight slices spread over the batch are compared in full
+    # (every row, so every workgroup position of the walk in those slices).
+    from fmm_testlib import floored_mean_rel_error
+    B, H, N, d, kw = 64, 2, 2048, 64, 64
+    q, k, v, wn, wf = make_inputs(B, H, N, d, "bf16", 1.0 / 8.0, 810 + causal)
+    log(f"multi-tile walks B={B} H={H} N={N} d={d} k={kw} causal={causal}")
+    got = run_gpu(q, k, v, wn, wf, kw, 2, causal, "bf16")
+    bs = [0, 21, 42, 63]
+    want = ref.fmm_attention_stream(q[bs], k[bs], v[bs], wn, wf, kw, 2, bool(causal))
+    err = slice_errors(got[bs], want).max()
+    log(f"multi-tile walks causal={causal}: max slice error {err:.3e}, floored mean "
+        f"relative {floored_mean_rel_error(got[bs], want):.3e}")
+    assert err <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("causal", [0, 1])
+def test_stress64k_head0_all_rows(causal):
+    # every one of the 65536 rows of head 0 at the benchmark shape and launch
+    # configuration (the whole problem runs; head 0 is compared in full)
+    from fmm_testlib import floored_mean_rel_error
+    w = WORKLOADS["stress64k"]
+    q, k, v, wn, wf = workload_inputs("stress64k")
+    log(f"stress64k head 0 all rows, causal={causal}")
+    got = run_gpu(q, k, v, wn, wf, w.band_k, w.rank, causal, "bf16")
+    sl = (slice(0, 1), slice(0, 1))
+    want = ref.fmm_attention_stream(q[sl], k[sl], v[sl], wn[:1], wf[:1], w.band_k, w.rank,
+                                    bool(causal))
+    err = slice_errors(got[sl], want).max()
+    log(f"stress64k head 0 causal={causal}: max error {err:.3e}, floored mean relative "
+        f"{floored_mean_rel_error(got[sl], want):.3e}")
+    assert err <= TOL["bf16"]
+
+
 # ------------------------------------------------------------------ edge-case sweep
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("causal", [0, 1])
