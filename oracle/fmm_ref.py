@@ -18,6 +18,7 @@ What it computes (FMMformer, arXiv 2108.02347):
       F(i) = [0, N-1]; causal: [0, i] (the sum truncated at i, Sec. 3.2.1).
   feature maps, Sec. 3.2.1 "Feature map selection":
       phi_1(x) = elu(x) + 1,  phi_2(x) = elu(-x) + 1  (elementwise, elu with alpha 1)
+      phi_3(x) = tanh(x)      (the third map of the rank-3 far field, Sec. 4.1)
   blend, Sec. 3.3, Eq. (11):
       out = sigmoid(w_near[h]) * near + sigmoid(w_far[h]) * far
 
@@ -28,6 +29,22 @@ feature map is normalised on its own as Eq. (9) writes it; the far sum runs over
 all of F(i) (the band is not excluded); there is no epsilon in the far
 denominator; the 1/sqrt(d) scale applies to the near field only; the blend
 weights are raw per-head logits passed through a sigmoid.
+
+Far-field normalisation.  norm="map" (the default) divides each map by its
+own denominator, as Eq. (9) writes the sum of fractions.  norm="joint" divides
+the sum of the maps' numerators by the sum of their denominators, i.e. it
+normalises the rows of L = sum_l phi_l(Q) phi_l(K)^T as one matrix, the reading
+of the introduction's remark that rows are normalised to sum to one (Sec. 1.2).
+For rank 1 the two agree.  There is no epsilon: phi_3 = tanh can make a
+denominator zero or negative, and the division is then carried out as IEEE
+arithmetic gives it (no clamping).
+
+Backward (gradients of a scalar loss L through dL/dout), written out from the
+definitions above: the banded softmax of Eq. (3) (softmax derivative
+p (dp - sum p dp)), the fractions of Eq. (9) (quotient rule, with the causal
+sums of Eq. (7) truncated at i, so the key-side gradients become suffix sums
+over the rows i >= j), the feature-map derivatives and the sigmoid of
+Eq. (11) (sigma' = sigma (1 - sigma)).
 
 Three forms, all float64:
   * dense:     builds the N x N matrices of the definitions (tiny N only);
@@ -49,6 +66,7 @@ import numpy as np
 
 __all__ = [
     "phi",
+    "phi_grad",
     "sigmoid",
     "band_mask",
     "near_dense",
@@ -58,6 +76,8 @@ __all__ = [
     "far_stream",
     "fmm_attention_stream",
     "fmm_attention_rows",
+    "far_terms_stream",
+    "fmm_attention_backward_stream",
 ]
 
 
@@ -70,12 +90,28 @@ def _elu(x: np.ndarray) -> np.ndarray:
 
 
 def phi(x: np.ndarray, l: int) -> np.ndarray:
-    """Feature map phi_l (Sec. 3.2.1): l = 1 -> elu(x)+1, l = 2 -> elu(-x)+1."""
+    """Feature map phi_l (Sec. 3.2.1): l = 1 -> elu(x)+1, l = 2 -> elu(-x)+1,
+    l = 3 -> tanh(x)."""
     if l == 1:
         return _elu(x) + 1.0
     if l == 2:
         return _elu(-np.asarray(x, dtype=np.float64)) + 1.0
-    raise ValueError(f"feature map {l} is not defined for this operator (rank 1 or 2)")
+    if l == 3:
+        return np.tanh(np.asarray(x, dtype=np.float64))
+    raise ValueError(f"feature map {l} is not defined for this operator (rank 1 to 3)")
+
+
+def phi_grad(x: np.ndarray, l: int) -> np.ndarray:
+    """d phi_l / dx elementwise: elu'(x) = 1 for x > 0 and exp(x) otherwise, so
+    phi_1' = elu'(x), phi_2' = -elu'(-x), phi_3' = 1 - tanh(x)^2."""
+    x = np.asarray(x, dtype=np.float64)
+    if l == 1:
+        return np.where(x > 0.0, 1.0, np.exp(np.minimum(x, 0.0)))
+    if l == 2:
+        return -np.where(-x > 0.0, 1.0, np.exp(np.minimum(-x, 0.0)))
+    if l == 3:
+        return 1.0 - np.tanh(x) ** 2
+    raise ValueError(f"feature map {l} is not defined for this operator (rank 1 to 3)")
 
 
 def sigmoid(w: np.ndarray) -> np.ndarray:
@@ -118,21 +154,35 @@ def near_dense(q, k, v, band_k: int, causal: bool) -> np.ndarray:
     return np.einsum("bhij,bhjc->bhic", p, v)
 
 
-def far_dense(q, k, v, rank: int, causal: bool) -> np.ndarray:
+def far_dense(q, k, v, rank: int, causal: bool, norm: str = "map") -> np.ndarray:
     """Far field, Eq. (8)-(9): for each map the explicit N x N matrix
     phi_l(Q) phi_l(K)^T (lower triangle only when causal), each row divided by
-    its own sum, applied to V; the r results are added."""
+    its own sum, applied to V; the r results are added.  norm="joint": the r
+    matrices are added first and the rows of the sum are divided by their
+    sums."""
     q, k, v = _check(q, k, v)
+    _check_norm(norm)
     n = q.shape[2]
     out = np.zeros_like(v)
     lower = np.tril(np.ones((n, n), dtype=bool))
+    total = np.zeros(q.shape[:2] + (n, n))
     for l in range(1, rank + 1):
         a = np.einsum("bhic,bhjc->bhij", phi(q, l), phi(k, l))
         if causal:
             a = np.where(lower, a, 0.0)
+        if norm == "joint":
+            total += a
+            continue
         w = a / a.sum(axis=-1, keepdims=True)
         out += np.einsum("bhij,bhjc->bhic", w, v)
+    if norm == "joint":
+        out = np.einsum("bhij,bhjc->bhic", total / total.sum(axis=-1, keepdims=True), v)
     return out
+
+
+def _check_norm(norm: str) -> None:
+    if norm not in ("map", "joint"):
+        raise ValueError(f"unknown far-field normalisation {norm!r}")
 
 
 def _blend(near, far, w_near, w_far):
@@ -144,10 +194,10 @@ def _blend(near, far, w_near, w_far):
 
 
 def fmm_attention_dense(q, k, v, w_near, w_far, band_k: int, rank: int,
-                        causal: bool) -> np.ndarray:
+                        causal: bool, norm: str = "map") -> np.ndarray:
     """out = sigmoid(w_near) D V + sigmoid(w_far) L V (Eq. (9), Eq. (11))."""
     return _blend(near_dense(q, k, v, band_k, causal),
-                  far_dense(q, k, v, rank, causal), w_near, w_far)
+                  far_dense(q, k, v, rank, causal, norm), w_near, w_far)
 
 
 # ---------------------------------------------------------------- stream form
@@ -188,17 +238,19 @@ def near_stream(q, k, v, band_k: int, causal: bool, row_chunk: int = 16384) -> n
     return out
 
 
-def far_stream(q, k, v, rank: int, causal: bool, row_chunk: int = 512) -> np.ndarray:
-    """Far field through associativity (Eq. (5), Eq. (7)).
+def far_terms_stream(q, k, v, rank: int, causal: bool, row_chunk: int = 512):
+    """Numerator and denominator of every map of the far field (Eq. (7)-(9)),
+    through associativity (Eq. (5)): a list over l = 1..rank of
+    (num_l [B,H,N,d], den_l [B,H,N]) with num_l,i = phi_l(q_i)^T S_l(i) and
+    den_l,i = phi_l(q_i)^T z_l(i).
 
-    Non-causal: S_l = phi_l(K)^T V and z_l = phi_l(K)^T 1 once per slice, then
-    far_i = sum_l phi_l(q_i)^T S_l / phi_l(q_i)^T z_l.
+    Non-causal: S_l = phi_l(K)^T V and z_l = phi_l(K)^T 1 once per slice.
     Causal: the sums are truncated at i (Sec. 3.2.1); the running sums
     S_l(i), z_l(i) are formed as explicit cumulative sums of the outer products
     phi_l(k_j) v_j^T, carried from one row block to the next."""
     q, k, v = _check(q, k, v)
     b_, h_, n, d = q.shape
-    out = np.zeros_like(v)
+    terms = []
     for l in range(1, rank + 1):
         pq = phi(q, l)
         pk = phi(k, l)
@@ -207,8 +259,10 @@ def far_stream(q, k, v, rank: int, causal: bool, row_chunk: int = 512) -> np.nda
             z = pk.sum(axis=2)
             num = np.einsum("bhic,bhce->bhie", pq, s)
             den = np.einsum("bhic,bhc->bhi", pq, z)
-            out += num / den[..., None]
+            terms.append((num, den))
             continue
+        num = np.empty_like(v)
+        den = np.empty((b_, h_, n))
         s_run = np.zeros((b_, h_, d, d))
         z_run = np.zeros((b_, h_, d))
         for i0 in range(0, n, row_chunk):
@@ -216,25 +270,41 @@ def far_stream(q, k, v, rank: int, causal: bool, row_chunk: int = 512) -> np.nda
             outer = pk[:, :, i0:i1, :, None] * v[:, :, i0:i1, None, :]
             s_cum = s_run[:, :, None] + np.cumsum(outer, axis=2)
             z_cum = z_run[:, :, None] + np.cumsum(pk[:, :, i0:i1], axis=2)
-            num = np.einsum("bhic,bhice->bhie", pq[:, :, i0:i1], s_cum)
-            den = np.einsum("bhic,bhic->bhi", pq[:, :, i0:i1], z_cum)
-            out[:, :, i0:i1] += num / den[..., None]
+            num[:, :, i0:i1] = np.einsum("bhic,bhice->bhie", pq[:, :, i0:i1], s_cum)
+            den[:, :, i0:i1] = np.einsum("bhic,bhic->bhi", pq[:, :, i0:i1], z_cum)
             s_run = s_cum[:, :, -1]
             z_run = z_cum[:, :, -1]
+        terms.append((num, den))
+    return terms
+
+
+def far_stream(q, k, v, rank: int, causal: bool, row_chunk: int = 512,
+               norm: str = "map") -> np.ndarray:
+    """Far field from the per-map terms: sum_l num_l / den_l (Eq. (9)), or
+    (sum_l num_l) / (sum_l den_l) with norm="joint"."""
+    _check_norm(norm)
+    terms = far_terms_stream(q, k, v, rank, causal, row_chunk)
+    if norm == "joint":
+        num = sum(t[0] for t in terms)
+        den = sum(t[1] for t in terms)
+        return num / den[..., None]
+    out = np.zeros_like(terms[0][0])
+    for num, den in terms:
+        out += num / den[..., None]
     return out
 
 
 def fmm_attention_stream(q, k, v, w_near, w_far, band_k: int, rank: int,
-                         causal: bool) -> np.ndarray:
+                         causal: bool, norm: str = "map") -> np.ndarray:
     """Same operator as fmm_attention_dense, any N."""
     return _blend(near_stream(q, k, v, band_k, causal),
-                  far_stream(q, k, v, rank, causal), w_near, w_far)
+                  far_stream(q, k, v, rank, causal, norm=norm), w_near, w_far)
 
 
 # ---------------------------------------------------------------- sampled rows
 
 def fmm_attention_rows(q, k, v, w_near, w_far, band_k: int, rank: int,
-                       causal: bool, b: int, h: int, rows) -> np.ndarray:
+                       causal: bool, b: int, h: int, rows, norm: str = "map") -> np.ndarray:
     """The operator's output at the given rows of slice (b, h) only.
 
     q, k, v: [B, H, N, d]; returns [len(rows), d] in the order of `rows`.
@@ -255,15 +325,19 @@ def fmm_attention_rows(q, k, v, w_near, w_far, band_k: int, rank: int,
         sc = ks[lo:hi + 1] @ qs[i] * scale
         p = np.exp(sc - sc.max())
         near[t] = (p / p.sum()) @ vs[lo:hi + 1]
-    far = np.zeros((rows.size, d))
+    _check_norm(norm)
+    nums, dens = [], []
     for l in range(1, rank + 1):
         pq = phi(qs[rows], l)
         pk = phi(ks, l)
         if not causal:
             s = pk.T @ vs
             z = pk.sum(axis=0)
-            far += (pq @ s) / (pq @ z)[:, None]
+            nums.append(pq @ s)
+            dens.append(pq @ z)
             continue
+        num = np.zeros((rows.size, d))
+        den = np.zeros(rows.size)
         order = np.argsort(rows, kind="stable")
         s_run = np.zeros((d, d))
         z_run = np.zeros(d)
@@ -274,7 +348,16 @@ def fmm_attention_rows(q, k, v, w_near, w_far, band_k: int, rank: int,
                 s_run = s_run + pk[done:i + 1].T @ vs[done:i + 1]
                 z_run = z_run + pk[done:i + 1].sum(axis=0)
                 done = i + 1
-            far[t] += (pq[t] @ s_run) / (pq[t] @ z_run)
+            num[t] = pq[t] @ s_run
+            den[t] = pq[t] @ z_run
+        nums.append(num)
+        dens.append(den)
+    if norm == "joint":
+        far = sum(nums) / sum(dens)[:, None]
+    else:
+        far = np.zeros((rows.size, d))
+        for num, den in zip(nums, dens):
+            far += num / den[:, None]
     a = float(sigmoid(w_near[h]))
     c = float(sigmoid(w_far[h]))
     out = np.zeros((rows.size, d))
@@ -283,3 +366,145 @@ def fmm_attention_rows(q, k, v, w_near, w_far, band_k: int, rank: int,
     if c > 0:
         out += c * far
     return out
+
+
+# ---------------------------------------------------------------- backward
+
+def _near_backward(q, k, v, g, band_k: int, causal: bool):
+    """Gradients of the near field (Eq. (3)) for the upstream gradient g of
+    near.  With p_i the softmax over the band of s_ij = tau q_i.k_j:
+        dv_j += sum_i p_ij g_i
+        ds_ij = p_ij (g_i.v_j - g_i.near_i)          (softmax derivative)
+        dq_i  = tau sum_j ds_ij k_j,  dk_j += tau sum_i ds_ij q_i
+    computed per band offset o = j - i, like near_stream."""
+    b_, h_, n, d = q.shape
+    kk = min(band_k, n - 1)
+    offs = np.arange(-kk, (0 if causal else kk) + 1)
+    tau = 1.0 / math.sqrt(d)
+    rows = np.arange(n)
+    valid = [(rows + o >= 0) & (rows + o < n) for o in offs]
+    score = np.full((b_, h_, n, len(offs)), -np.inf)
+    for t, o in enumerate(offs):
+        ok = valid[t]
+        score[:, :, ok, t] = np.einsum("bhic,bhic->bhi", q[:, :, rows[ok]],
+                                       k[:, :, rows[ok] + o]) * tau
+    score = score - score.max(axis=-1, keepdims=True)
+    p = np.exp(score)
+    p = p / p.sum(axis=-1, keepdims=True)
+    near = np.zeros_like(v)
+    dp = np.zeros_like(p)
+    for t, o in enumerate(offs):
+        ok = valid[t]
+        near[:, :, ok] += p[:, :, ok, t, None] * v[:, :, rows[ok] + o]
+        dp[:, :, ok, t] = np.einsum("bhic,bhic->bhi", g[:, :, ok], v[:, :, rows[ok] + o])
+    gn = np.einsum("bhic,bhic->bhi", g, near)
+    ds = p * (dp - gn[..., None])
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    for t, o in enumerate(offs):
+        ok = valid[t]
+        j = rows[ok] + o
+        dq[:, :, ok] += tau * ds[:, :, ok, t, None] * k[:, :, j]
+        dk[:, :, j] += tau * ds[:, :, ok, t, None] * q[:, :, rows[ok]]
+        dv[:, :, j] += p[:, :, ok, t, None] * g[:, :, ok]
+    return near, dq, dk, dv
+
+
+def _far_backward(q, k, v, f, rank: int, causal: bool, norm: str, row_chunk: int = 512):
+    """Gradients of the far field (Eq. (7)-(9)) for the upstream gradient f of
+    far.  Per map, num_i = phi(q_i)^T S(i), den_i = phi(q_i)^T z(i):
+      norm="map":   dnum_i = f_i / den_i,   dden_i = -(f_i.num_i) / den_i^2
+      norm="joint": dnum_i = f_i / Den_i,   dden_i = -(f_i.far_i) / Den_i
+                    (Den_i = sum_l den_l,i; the same for every map)
+      dphi(q_i) = S(i) dnum_i + z(i) dden_i
+      dS(j) = sum_{i in G(j)} phi(q_i) dnum_i^T,  dz(j) = sum_{i in G(j)} phi(q_i) dden_i
+              G(j) = all rows (non-causal), rows i >= j (causal: suffix sums)
+      dphi(k_j) = dS(j) v_j + dz(j),  dv_j += dS(j)^T phi(k_j)
+    and dq, dk through phi_l'."""
+    b_, h_, n, d = q.shape
+    terms = far_terms_stream(q, k, v, rank, causal, row_chunk)
+    if norm == "joint":
+        den_all = sum(t[1] for t in terms)
+        far = sum(t[0] for t in terms) / den_all[..., None]
+    else:
+        far = np.zeros_like(v)
+        for num, den in terms:
+            far += num / den[..., None]
+    dq = np.zeros_like(q)
+    dk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    for l in range(1, rank + 1):
+        num, den = terms[l - 1]
+        if norm == "joint":
+            dnum = f / den_all[..., None]
+            dden = -np.einsum("bhic,bhic->bhi", f, far) / den_all
+        else:
+            dnum = f / den[..., None]
+            dden = -np.einsum("bhic,bhic->bhi", f, num) / den ** 2
+        pq = phi(q, l)
+        pk = phi(k, l)
+        if not causal:
+            state = np.einsum("bhjc,bhje->bhce", pk, v)
+            zsum = pk.sum(axis=2)
+            dpq = (np.einsum("bhce,bhie->bhic", state, dnum)
+                   + zsum[:, :, None, :] * dden[..., None])
+            ds = np.einsum("bhic,bhie->bhce", pq, dnum)
+            dz = np.einsum("bhic,bhi->bhc", pq, dden)
+            dpk = np.einsum("bhce,bhje->bhjc", ds, v) + dz[:, :, None, :]
+            dv += np.einsum("bhjc,bhce->bhje", pk, ds)
+        else:
+            # prefix sums S(i), z(i) over keys j <= i, as in the forward
+            dpq = np.empty_like(q)
+            s_pre = np.zeros((b_, h_, d, d))
+            z_pre = np.zeros((b_, h_, d))
+            for i0 in range(0, n, row_chunk):
+                i1 = min(n, i0 + row_chunk)
+                kv = pk[:, :, i0:i1, :, None] * v[:, :, i0:i1, None, :]
+                s_i = s_pre[:, :, None] + np.cumsum(kv, axis=2)
+                z_i = z_pre[:, :, None] + np.cumsum(pk[:, :, i0:i1], axis=2)
+                dpq[:, :, i0:i1] = (np.einsum("bhice,bhie->bhic", s_i, dnum[:, :, i0:i1])
+                                    + z_i * dden[:, :, i0:i1, None])
+                s_pre = s_i[:, :, -1]
+                z_pre = z_i[:, :, -1]
+            # suffix sums over rows i >= j, walked from the end
+            dpk = np.empty_like(k)
+            ds_run = np.zeros((b_, h_, d, d))
+            dz_run = np.zeros((b_, h_, d))
+            for i1 in range(n, 0, -row_chunk):
+                i0 = max(0, i1 - row_chunk)
+                outer = pq[:, :, i0:i1, :, None] * dnum[:, :, i0:i1, None, :]
+                ds_suf = ds_run[:, :, None] + np.cumsum(outer[:, :, ::-1], axis=2)[:, :, ::-1]
+                dz_suf = dz_run[:, :, None] + np.cumsum(
+                    (pq[:, :, i0:i1] * dden[:, :, i0:i1, None])[:, :, ::-1], axis=2)[:, :, ::-1]
+                dpk[:, :, i0:i1] = (np.einsum("bhjce,bhje->bhjc", ds_suf, v[:, :, i0:i1])
+                                    + dz_suf)
+                dv[:, :, i0:i1] += np.einsum("bhjc,bhjce->bhje", pk[:, :, i0:i1], ds_suf)
+                ds_run = ds_suf[:, :, 0]
+                dz_run = dz_suf[:, :, 0]
+        dq += phi_grad(q, l) * dpq
+        dk += phi_grad(k, l) * dpk
+    return far, dq, dk, dv
+
+
+def fmm_attention_backward_stream(q, k, v, w_near, w_far, dout, band_k: int, rank: int,
+                                  causal: bool, norm: str = "map", row_chunk: int = 512):
+    """Gradients of sum(dout * out) with out = fmm_attention_stream(...):
+    returns (dq, dk, dv, dw_near, dw_far).  Eq. (11): out = a near + c far with
+    a = sigmoid(w_near[h]), c = sigmoid(w_far[h]); so near and far receive
+    a dout and c dout, and dw = sigmoid'(w) sum over (b, i, channel) of
+    dout * part, with sigmoid' = sigmoid (1 - sigmoid)."""
+    q, k, v = _check(q, k, v)
+    _check_norm(norm)
+    dout = np.asarray(dout, dtype=np.float64)
+    a = sigmoid(w_near)[None, :, None, None]
+    c = sigmoid(w_far)[None, :, None, None]
+    near, dq, dk, dv = _near_backward(q, k, v, a * dout, band_k, causal)
+    far, dqf, dkf, dvf = _far_backward(q, k, v, c * dout, rank, causal, norm, row_chunk)
+    dq += dqf
+    dk += dkf
+    dv += dvf
+    sa, sc = sigmoid(w_near), sigmoid(w_far)
+    dw_near = sa * (1.0 - sa) * np.einsum("bhic,bhic->h", dout, near)
+    dw_far = sc * (1.0 - sc) * np.einsum("bhic,bhic->h", dout, far)
+    return dq, dk, dv, dw_near, dw_far

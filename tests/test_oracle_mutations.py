@@ -47,8 +47,8 @@ MUTATIONS = [
      's = np.einsum("bhjc,bhje->bhce", pk, v)',
      's = np.einsum("bhjc,bhje->bhec", pk, v)'),
     ("non-causal far part not normalised",
-     "            out += num / den[..., None]\n            continue",
-     "            out += num / den.mean()\n            continue"),
+     "    for num, den in terms:\n        out += num / den[..., None]",
+     "    for num, den in terms:\n        out += num / den.mean()"),
     ("causal far sum exclusive of j = i",
      "s_cum = s_run[:, :, None] + np.cumsum(outer, axis=2)",
      "s_cum = s_run[:, :, None] + np.cumsum(outer, axis=2) - outer"),
@@ -70,6 +70,39 @@ MUTATIONS = [
     ("rows form: non-causal far state transposed",
      "            s = pk.T @ vs",
      "            s = (pk.T @ vs).T"),
+    ("phi_3 not tanh",
+     "return np.tanh(np.asarray(x, dtype=np.float64))",
+     "return np.sin(np.asarray(x, dtype=np.float64))"),
+    ("streamed joint far field with the denominators averaged",
+     "        return num / den[..., None]",
+     "        return num / (den[..., None] / len(terms))"),
+    ("dense joint far field not row-normalised",
+     "total / total.sum(axis=-1, keepdims=True), v)",
+     "total, v)"),
+    ("rows form: joint far field summed per map",
+     "        far = sum(nums) / sum(dens)[:, None]",
+     "        far = sum(nm / dn[:, None] for nm, dn in zip(nums, dens))"),
+    ("backward: softmax derivative without the row term",
+     "ds = p * (dp - gn[..., None])",
+     "ds = p * dp"),
+    ("backward: quotient rule with the wrong sign",
+     "dden = -np.einsum(\"bhic,bhic->bhi\", f, num) / den ** 2",
+     "dden = np.einsum(\"bhic,bhic->bhi\", f, num) / den ** 2"),
+    ("backward: joint denominator squared",
+     "dden = -np.einsum(\"bhic,bhic->bhi\", f, far) / den_all",
+     "dden = -np.einsum(\"bhic,bhic->bhi\", f, far) / den_all ** 2"),
+    ("backward: causal key gradients carried from the wrong end",
+     "                ds_run = ds_suf[:, :, 0]",
+     "                ds_run = ds_suf[:, :, -1]"),
+    ("backward: phi_2 derivative without its sign",
+     "return -np.where(-x > 0.0, 1.0, np.exp(np.minimum(-x, 0.0)))",
+     "return np.where(-x > 0.0, 1.0, np.exp(np.minimum(-x, 0.0)))"),
+    ("backward: sigmoid derivative missing its (1 - sigma)",
+     "dw_near = sa * (1.0 - sa) * np.einsum",
+     "dw_near = sa * np.einsum"),
+    ("backward: key-side near gradient unscaled",
+     "dk[:, :, j] += tau * ds[:, :, ok, t, None] * q[:, :, rows[ok]]",
+     "dk[:, :, j] += ds[:, :, ok, t, None] * q[:, :, rows[ok]]"),
 ]
 
 

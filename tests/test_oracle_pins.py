@@ -38,6 +38,8 @@ def bf_elu(x):
 
 
 def bf_phi(x, l):
+    if l == 3:
+        return math.tanh(x)
     return bf_elu(x) + 1.0 if l == 1 else bf_elu(-x) + 1.0
 
 
@@ -54,16 +56,21 @@ def bf_near(qs, ks, vs, kw, causal):
     return np.array(out)
 
 
-def bf_far(qs, ks, vs, rank, causal):
+def bf_far(qs, ks, vs, rank, causal, joint=False):
     n, d = len(qs), len(qs[0])
     out = np.zeros((n, d))
-    for l in range(1, rank + 1):
-        for i in range(n):
-            js = range(i + 1) if causal else range(n)
+    for i in range(n):
+        js = range(i + 1) if causal else range(n)
+        nums, dens = [], []
+        for l in range(1, rank + 1):
             a = {j: sum(bf_phi(qs[i][c], l) * bf_phi(ks[j][c], l) for c in range(d)) for j in js}
-            tot = sum(a.values())
-            for c in range(d):
-                out[i, c] += sum(a[j] * vs[j][c] for j in js) / tot
+            nums.append([sum(a[j] * vs[j][c] for j in js) for c in range(d)])
+            dens.append(sum(a.values()))
+        for c in range(d):
+            if joint:
+                out[i, c] = sum(nm[c] for nm in nums) / sum(dens)
+            else:
+                out[i, c] = sum(nm[c] / dn for nm, dn in zip(nums, dens))
     return out
 
 
@@ -81,8 +88,25 @@ def test_phi_closed_forms():
     x = rnd(1000, 0) * 5
     assert np.array_equal(ref.phi(x, 2), ref.phi(-x, 1))
     assert (ref.phi(x, 1) > 0).all() and (ref.phi(x, 2) > 0).all()
+    # phi_3 = tanh: odd, tanh(ln 3) = (9 - 1) / (9 + 1)
+    assert ref.phi(np.array(0.0), 3) == 0.0
+    assert ref.phi(np.array(math.log(3.0)), 3) == pytest.approx(0.8, rel=1e-15)
+    assert np.array_equal(ref.phi(-x, 3), -ref.phi(x, 3))
     with pytest.raises(ValueError):
-        ref.phi(x, 3)
+        ref.phi(x, 4)
+
+
+def test_phi_grad_closed_forms_and_differences():
+    e = math.exp
+    g = lambda x, l: float(ref.phi_grad(np.array(x), l))
+    assert g(1.0, 1) == 1.0 and g(-1.0, 1) == pytest.approx(e(-1.0))
+    assert g(1.0, 2) == pytest.approx(-e(-1.0)) and g(-2.0, 2) == -1.0
+    assert g(math.log(3.0), 3) == pytest.approx(1.0 - 0.64, rel=1e-14)
+    x = rnd(200, 1) * 3
+    x = x[np.abs(x) > 1e-3]  # away from the kink-free but piecewise point 0
+    for l in (1, 2, 3):
+        fd = (ref.phi(x + 1e-6, l) - ref.phi(x - 1e-6, l)) / 2e-6
+        np.testing.assert_allclose(ref.phi_grad(x, l), fd, rtol=1e-7, atol=1e-9)
 
 
 def test_sigmoid_closed_forms():
@@ -174,14 +198,56 @@ def test_near_translation_equivariance_interior():
 # ------------------------------------------------------------------ far field
 
 @pytest.mark.parametrize("causal", [False, True])
-@pytest.mark.parametrize("rank", [1, 2])
-def test_far_brute_force(causal, rank):
+@pytest.mark.parametrize("rank", [1, 2, 3])
+@pytest.mark.parametrize("norm", ["map", "joint"])
+def test_far_brute_force(causal, rank, norm):
     n, d = 9, 3
     q, k, v = (rnd((1, 1, n, d), s) for s in (20, 21, 22))
-    want = bf_far(q[0, 0].tolist(), k[0, 0].tolist(), v[0, 0].tolist(), rank, causal)
+    if rank == 3:  # keep tanh's denominator away from zero
+        q, k = q + 1.5, k + 1.5
+    want = bf_far(q[0, 0].tolist(), k[0, 0].tolist(), v[0, 0].tolist(), rank, causal,
+                  joint=norm == "joint")
     for fn in (ref.far_dense, ref.far_stream):
-        np.testing.assert_allclose(fn(q, k, v, rank, causal)[0, 0], want, rtol=1e-12,
-                                   atol=1e-12)
+        np.testing.assert_allclose(fn(q, k, v, rank, causal, norm=norm)[0, 0], want,
+                                   rtol=1e-11, atol=1e-12)
+
+
+def test_far_joint_rows_sum_to_one():
+    # joint normalisation: the rows of the whole far matrix sum to one (per map
+    # they sum to one each, so the per-map far matrix rows sum to the rank);
+    # rank 1 is the same under both readings
+    n, d = 13, 3
+    q, k = rnd((1, 1, n, d), 70) + 1.0, rnd((1, 1, n, d), 71) + 1.0
+    c = rnd(d, 72)
+    v = np.broadcast_to(c, (1, 1, n, d)).copy()
+    for causal in (False, True):
+        for rank in (1, 2, 3):
+            np.testing.assert_allclose(ref.far_stream(q, k, v, rank, causal, norm="joint"),
+                                       np.broadcast_to(c, v.shape), rtol=1e-12)
+            np.testing.assert_allclose(ref.far_stream(q, k, v, rank, causal, norm="map"),
+                                       rank * np.broadcast_to(c, v.shape), rtol=1e-12)
+        v2 = rnd((1, 1, n, d), 73)
+        np.testing.assert_array_equal(ref.far_stream(q, k, v2, 1, causal, norm="joint"),
+                                      ref.far_stream(q, k, v2, 1, causal, norm="map"))
+
+
+def test_far_rank3_closed_form():
+    # d = 1, one key k = ln 3 (phi_1 = 1 + ln 3, phi_2 = 1/3, phi_3 = 0.8), value 2,
+    # query ln 3 too: every map's weight matrix is the 1 x 1 matrix [1], so per
+    # map far = 3 * 2, joint far = 2.  A second key 0 (phi = 1, 1, 0) with value
+    # 0 and the same query: map 3's weight on key 0 is 0, so its term is 2 again.
+    x = math.log(3.0)
+    q = np.array([x, x]).reshape(1, 1, 2, 1)
+    k = np.array([x, 0.0]).reshape(1, 1, 2, 1)
+    v = np.array([2.0, 0.0]).reshape(1, 1, 2, 1)
+    p1, p2 = (1.0 + x), 1.0 / 3.0
+    want = 2.0 * (p1 * p1 / (p1 * p1 + p1) + p2 * p2 / (p2 * p2 + p2) + 1.0)
+    got = ref.far_stream(q, k, v, 3, False)[0, 0, :, 0]
+    np.testing.assert_allclose(got, [want, want], rtol=1e-14)
+    den = p1 * p1 + p1 + p2 * p2 + p2 + 0.64
+    num = 2.0 * (p1 * p1 + p2 * p2 + 0.64)
+    np.testing.assert_allclose(ref.far_stream(q, k, v, 3, False, norm="joint")[0, 0, :, 0],
+                               [num / den] * 2, rtol=1e-14)
 
 
 def test_far_rank2_closed_form():
@@ -340,6 +406,21 @@ def test_dense_equals_stream(shape, causal, rank):
         np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-12)
 
 
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("rank,norm", [(3, "map"), (2, "joint"), (3, "joint")])
+def test_dense_equals_stream_extended_maps(causal, rank, norm):
+    q, k, v = (rnd((2, 2, 33, 8), s) + 0.7 for s in (74, 75, 76))
+    wn, wf = rnd(2, 77), rnd(2, 78)
+    a = ref.fmm_attention_dense(q, k, v, wn, wf, 4, rank, causal, norm)
+    b = ref.fmm_attention_stream(q, k, v, wn, wf, 4, rank, causal, norm)
+    np.testing.assert_allclose(a, b, rtol=1e-11, atol=1e-12)
+    rows = [32, 0, 5, 17]
+    for bb in range(2):
+        for hh in range(2):
+            got = ref.fmm_attention_rows(q, k, v, wn, wf, 4, rank, causal, bb, hh, rows, norm)
+            np.testing.assert_allclose(got, b[bb, hh, rows], rtol=1e-11, atol=1e-12)
+
+
 def test_stream_chunking_is_invisible():
     q, k, v = (rnd((1, 2, 300, 4), s) for s in (56, 57, 58))
     for causal in (False, True):
@@ -362,3 +443,111 @@ def test_rows_form_equals_stream(causal):
         for hh in range(h):
             got = ref.fmm_attention_rows(q, k, v, wn, wf, 6, 2, causal, bb, hh, rows)
             np.testing.assert_allclose(got, full[bb, hh, rows], rtol=1e-12, atol=1e-13)
+
+
+# ------------------------------------------------------------------ backward
+# The gradients of sum(dout * out) are pinned by central finite differences
+# of the forward oracle and by torch float64 autograd of a dense forward
+# written with torch's own softmax, masking and sigmoid.
+
+def _fd_grads(q, k, v, wn, wf, dout, kw, rank, causal, norm, eps=1e-6):
+    f = lambda *a: float((ref.fmm_attention_stream(*a, kw, rank, causal, norm) * dout).sum())
+    args = [q, k, v, wn, wf]
+    out = []
+    for ai, x in enumerate(args):
+        g = np.zeros_like(x)
+        for idx in np.ndindex(x.shape):
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += eps
+            xm[idx] -= eps
+            a1, a2 = list(args), list(args)
+            a1[ai], a2[ai] = xp, xm
+            g[idx] = (f(*a1) - f(*a2)) / (2 * eps)
+        out.append(g)
+    return out
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("rank,norm", [(1, "map"), (2, "map"), (3, "map"), (2, "joint"),
+                                       (3, "joint")])
+def test_backward_finite_differences(causal, rank, norm):
+    b, h, n, d, kw = 1, 2, 8, 3, 2
+    q, k, v, dout = (rnd((b, h, n, d), s) for s in (80, 81, 82, 83))
+    if rank == 3:
+        q, k = q + 1.0, k + 1.0
+    wn, wf = rnd(h, 84), rnd(h, 85)
+    got = ref.fmm_attention_backward_stream(q, k, v, wn, wf, dout, kw, rank, causal, norm)
+    want = _fd_grads(q, k, v, wn, wf, dout, kw, rank, causal, norm)
+    for g, w in zip(got, want):
+        np.testing.assert_allclose(g, w, rtol=1e-6, atol=1e-7 * np.abs(w).max())
+
+
+def _torch_dense_forward(q, k, v, wn, wf, kw, rank, causal, norm):
+    n, d = q.shape[-2], q.shape[-1]
+    i = torch.arange(n)[:, None]
+    j = torch.arange(n)[None, :]
+    band = ((j <= i) & (j >= i - kw)) if causal else ((i - j).abs() <= kw)
+    s = (q @ k.transpose(-1, -2)) / math.sqrt(d)
+    p = torch.softmax(s.masked_fill(~band, float("-inf")), dim=-1)
+    near = p @ v
+    maps = [lambda x: torch.nn.functional.elu(x) + 1, lambda x: torch.nn.functional.elu(-x) + 1,
+            torch.tanh]
+    lower = torch.ones(n, n, dtype=torch.bool).tril()
+    mats = []
+    for l in range(rank):
+        a = maps[l](q) @ maps[l](k).transpose(-1, -2)
+        mats.append(a.masked_fill(~lower, 0.0) if causal else a)
+    if norm == "joint":
+        tot = sum(mats)
+        far = (tot / tot.sum(-1, keepdim=True)) @ v
+    else:
+        far = sum((a / a.sum(-1, keepdim=True)) @ v for a in mats)
+    return (torch.sigmoid(wn)[None, :, None, None] * near
+            + torch.sigmoid(wf)[None, :, None, None] * far)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("rank,norm", [(1, "map"), (2, "map"), (3, "map"), (2, "joint"),
+                                       (3, "joint")])
+def test_backward_matches_torch_autograd(causal, rank, norm):
+    b, h, n, d, kw = 2, 2, 21, 5, 3
+    q, k, v, dout = (rnd((b, h, n, d), s) for s in (86, 87, 88, 89))
+    if rank == 3:
+        q, k = q + 1.0, k + 1.0
+    wn, wf = rnd(h, 90), rnd(h, 91)
+    ts = [torch.tensor(x, requires_grad=True) for x in (q, k, v, wn, wf)]
+    out = _torch_dense_forward(*ts, kw, rank, causal, norm)
+    (out * torch.tensor(dout)).sum().backward()
+    got = ref.fmm_attention_backward_stream(q, k, v, wn, wf, dout, kw, rank, causal, norm)
+    for g, t in zip(got, ts):
+        np.testing.assert_allclose(g, t.grad.numpy(), rtol=1e-10, atol=1e-12)
+
+
+def test_backward_zero_band_without_far_part():
+    # k = 0 makes near = v and w_far = -inf removes the far part: out =
+    # sigmoid(w_near) v, so dq = dk = 0, dv = sigmoid(w_near) dout,
+    # dw_near = sigmoid' sum(dout * v), dw_far = 0
+    q, k, v, dout = (rnd((2, 2, 10, 4), s) for s in (92, 93, 94, 95))
+    wn = rnd(2, 96)
+    wf = np.array([-np.inf, -np.inf])
+    for causal in (False, True):
+        dq, dk, dv, dwn, dwf = ref.fmm_attention_backward_stream(q, k, v, wn, wf, dout, 0, 2,
+                                                                 causal)
+        np.testing.assert_array_equal(dq, 0.0)
+        np.testing.assert_array_equal(dk, 0.0)
+        sn = 1.0 / (1.0 + np.exp(-wn))
+        np.testing.assert_allclose(dv, sn[None, :, None, None] * dout, rtol=1e-14)
+        np.testing.assert_allclose(dwn, sn * (1 - sn) * np.einsum("bhic,bhic->h", dout, v),
+                                   rtol=1e-13)
+        np.testing.assert_array_equal(dwf, 0.0)
+
+
+def test_backward_chunking_is_invisible():
+    # the causal prefix and suffix sums are carried across row blocks
+    q, k, v, dout = (rnd((1, 2, 70, 4), s) for s in (97, 98, 99, 100))
+    wn, wf = rnd(2, 101), rnd(2, 102)
+    for causal in (False, True):
+        a = ref.fmm_attention_backward_stream(q, k, v, wn, wf, dout, 3, 2, causal, row_chunk=9)
+        b = ref.fmm_attention_backward_stream(q, k, v, wn, wf, dout, 3, 2, causal)
+        for x, y in zip(a, b):
+            np.testing.assert_allclose(x, y, rtol=1e-12, atol=1e-13)
