@@ -13,14 +13,19 @@
  *            S_l(i) = sum_{j in F(i)} phi_l(k_j) v_j^T,  z_l(i) = sum_{j in F(i)} phi_l(k_j)
  *            F(i) = [0, N-1]                           (causal: [0, i])
  *            -- Sec. 3.2.1, Eq. (7)-(9); causal form by truncating the sum at i.
- *            phi_1(x) = elu(x)+1, phi_2(x) = elu(-x)+1 (elementwise)
- *            -- Sec. 3.2.1, "Feature map selection".
+ *            phi_1(x) = elu(x)+1, phi_2(x) = elu(-x)+1, phi_3(x) = tanh(x)
+ *            (elementwise) -- Sec. 3.2.1, "Feature map selection"; rank r
+ *            uses the first r of them (the rank-3 far field of Sec. 4.1).
  *   out_i  = sigmoid(w_near[h]) * near_i + sigmoid(w_far[h]) * far_i
  *            -- Sec. 3.3, Eq. (11).
  *
  * Each feature map is normalised on its own, as Eq. (9) writes it, so the far
- * rows carry total weight `rank`.  The far sum runs over all of F(i), the band
- * included.  There is no epsilon in the far denominator (phi_1, phi_2 > 0).
+ * rows carry total weight `rank` (fmm_attn_forward_ex can instead normalise
+ * the maps jointly).  The far sum runs over all of F(i), the band included.
+ * There is no epsilon in the far denominator: phi_1, phi_2 > 0, while
+ * phi_3 = tanh can make phi_3(q)^T z_3 zero or negative, and the quotient is
+ * then what IEEE fp32 division gives (the result is ill-conditioned near a
+ * vanishing denominator).
  *
  * Layout: q, k, v and out are contiguous [B, H, N, d] arrays (d innermost) in
  * device memory, 16-byte aligned.  w_near and w_far are device float[H] raw
@@ -59,7 +64,8 @@ extern "C" {
                                     causal not 0/1, misaligned pointer,
                                     out overlapping q, k or v, or a shape whose
                                     element count does not fit in int64 */
-#define FMM_ERR_UNSUPPORTED (-2) /* d not in {16, 32, 64}, rank not in {1, 2},
+#define FMM_ERR_UNSUPPORTED (-2) /* d not in {16, 32, 64, 128}, rank not in
+                                    {1, 2, 3},
                                     dtype code unknown, B*H above 2^31-1, or
                                     a kernel grid beyond the dispatch limit
                                     (2^32 work-items per dimension; about
@@ -70,9 +76,15 @@ extern "C" {
 #define FMM_ERR_SCRATCH     (-5) /* fmm_attn_forward_noalloc: the shape needs
                                     more scratch than its fixed array holds */
 
-/* dtype codes for fmm_attn_forward_ws */
+/* dtype codes for fmm_attn_forward_ws, _ex and _noalloc */
 #define FMM_DTYPE_F32  0
 #define FMM_DTYPE_BF16 1
+
+/* far-field normalisations for fmm_attn_forward_ex */
+#define FMM_FAR_NORM_PER_MAP 0 /* sum_l num_l / den_l, Eq. (9) */
+#define FMM_FAR_NORM_JOINT   1 /* (sum_l num_l) / (sum_l den_l): the rows of
+                                  L = sum_l phi_l(Q) phi_l(K)^T normalised as
+                                  one matrix (Sec. 1.2: rows sum to one) */
 
 /* kernel ids for the timing interface */
 #define FMM_KERNEL_SEG_STATE     0 /* per-segment phi(K)^T [V | 1] totals      */
@@ -88,11 +100,12 @@ extern "C" {
  *             q, k or v (the kernels read key windows of neighbouring rows
  *             while writing out).
  *   B, H, N : batch, heads, sequence length, each >= 1.
- *   d       : head width, one of 16, 32, 64 (the 1/sqrt(d) of Eq. (1)).
+ *   d       : head width, one of 16, 32, 64, 128 (the 1/sqrt(d) of Eq. (1)).
  *   band_k  : near-field half-width k >= 0 (2k+1 entries per interior row;
  *             causal: k+1).  k >= N-1 makes the near field full softmax
  *             attention.
- *   rank    : number of feature maps, 1 (phi_1) or 2 (phi_1, phi_2).
+ *   rank    : number of feature maps: 1 (phi_1), 2 (phi_1, phi_2) or 3
+ *             (phi_1, phi_2, phi_3).
  *   causal  : 0 or 1.
  *   w_near, w_far : device float[H], raw blend logits.
  *   stream  : hipStream_t or NULL.
@@ -123,6 +136,18 @@ int fmm_attn_forward_bf16(const void* q, const void* k, const void* v, void* out
                           int B, int H, int N, int d, int band_k, int rank,
                           int causal, const float* w_near, const float* w_far,
                           void* stream);
+
+/*
+ * fmm_attn_forward_ex - the operator with the far-field normalisation chosen
+ * by far_norm (FMM_FAR_NORM_PER_MAP as the other entry points, or
+ * FMM_FAR_NORM_JOINT) and the storage type by dtype (FMM_DTYPE_F32 or
+ * FMM_DTYPE_BF16); other arguments and the library-owned workspace as
+ * fmm_attn_forward.  FMM_ERR_INVALID_ARG for an unknown far_norm.
+ */
+int fmm_attn_forward_ex(const void* q, const void* k, const void* v, void* out,
+                        int B, int H, int N, int d, int band_k, int rank,
+                        int causal, const float* w_near, const float* w_far,
+                        int dtype, int far_norm, void* stream);
 
 /*
  * fmm_attn_workspace_bytes - device bytes fmm_attn_forward_ws needs for this

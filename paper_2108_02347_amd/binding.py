@@ -24,13 +24,16 @@ FMM_ERR_SCRATCH = -5
 FMM_DTYPE_F32 = 0
 FMM_DTYPE_BF16 = 1
 
+FMM_FAR_NORM_PER_MAP = 0
+FMM_FAR_NORM_JOINT = 1
+
 KERNELS = {"seg_state": 0, "state_combine": 1, "band_apply": 2, "causal_apply": 3}
 
 EXPORTS = (
     "fmm_attn_forward", "fmm_attn_forward_bf16", "fmm_attn_workspace_bytes",
     "fmm_attn_forward_ws", "fmm_attn_status_string", "fmm_attn_release_workspace",
     "fmm_attn_version", "fmm_attn_kernel_timing", "fmm_attn_kernel_timing_read",
-    "fmm_attn_forward_noalloc", "fmm_attn_noalloc_max_bytes",
+    "fmm_attn_forward_noalloc", "fmm_attn_noalloc_max_bytes", "fmm_attn_forward_ex",
 )
 
 _lib = None
@@ -60,6 +63,8 @@ def lib() -> ctypes.CDLL:
         fn.restype = ci
     h.fmm_attn_forward_ws.argtypes = fwd_args[:-1] + [ci, vp, ctypes.c_size_t, vp]
     h.fmm_attn_forward_ws.restype = ci
+    h.fmm_attn_forward_ex.argtypes = fwd_args[:-1] + [ci, ci, vp]
+    h.fmm_attn_forward_ex.restype = ci
     h.fmm_attn_forward_noalloc.argtypes = fwd_args[:-1] + [ci, vp]
     h.fmm_attn_forward_noalloc.restype = ci
     h.fmm_attn_noalloc_max_bytes.argtypes = []
@@ -152,13 +157,21 @@ def _check_out(out, q):
         raise ValueError("out must be a contiguous tensor with q's dtype, shape and device")
 
 
-def forward(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool, out=None):
-    """FMMformer attention forward; returns out (allocated if not given)."""
+def forward(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool, out=None,
+            joint: bool = False):
+    """FMMformer attention forward; returns out (allocated if not given).
+    joint=True normalises the far-field maps jointly (fmm_attn_forward_ex)."""
     B, H, N, d = _prep(q, k, v, w_near, w_far)
     if out is None:
         out = torch.empty_like(q)
     else:
         _check_out(out, q)
+    if joint:
+        dt = FMM_DTYPE_BF16 if q.dtype == torch.bfloat16 else FMM_DTYPE_F32
+        _check(lib().fmm_attn_forward_ex(
+            _ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, int(band_k), int(rank),
+            int(bool(causal)), _ptr(w_near), _ptr(w_far), dt, FMM_FAR_NORM_JOINT, _stream_of(q)))
+        return out
     fn = lib().fmm_attn_forward_bf16 if q.dtype == torch.bfloat16 else lib().fmm_attn_forward
     _check(fn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, int(band_k), int(rank),
               int(bool(causal)), _ptr(w_near), _ptr(w_far), _stream_of(q)))

@@ -16,7 +16,7 @@
 
 namespace {
 
-constexpr int kVersion = 1 * 10000 + 0 * 100 + 0;
+constexpr int kVersion = 1 * 10000 + 1 * 100 + 0;
 
 // ------------------------------------------------------------------ planning
 // Segments split the key axis of every (batch, head) slice for the far-field
@@ -63,7 +63,7 @@ Plan make_plan(int B, int H, int N, int d, int rank, int esize, int apply_tm) {
 }
 
 bool supported(int d, int rank) {
-  return (d == 16 || d == 32 || d == 64) && (rank == 1 || rank == 2);
+  return (d == 16 || d == 32 || d == 64 || d == 128) && rank >= 1 && rank <= 3;
 }
 
 bool overlaps(const void* a, const void* b, size_t n) {
@@ -73,10 +73,12 @@ bool overlaps(const void* a, const void* b, size_t n) {
 
 int validate(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
              int d, int band_k, int rank, int causal, const float* w_near, const float* w_far,
-             int dtype) {
+             int dtype, int far_norm) {
   if (!q || !k || !v || !out || !w_near || !w_far) return FMM_ERR_INVALID_ARG;
   if (B < 1 || H < 1 || N < 1 || d < 1 || band_k < 0) return FMM_ERR_INVALID_ARG;
   if (causal != 0 && causal != 1) return FMM_ERR_INVALID_ARG;
+  if (far_norm != FMM_FAR_NORM_PER_MAP && far_norm != FMM_FAR_NORM_JOINT)
+    return FMM_ERR_INVALID_ARG;
   if (dtype != FMM_DTYPE_F32 && dtype != FMM_DTYPE_BF16) return FMM_ERR_UNSUPPORTED;
   if (!supported(d, rank)) return FMM_ERR_UNSUPPORTED;
   const size_t es = dtype == FMM_DTYPE_BF16 ? 2 : 4;
@@ -204,9 +206,10 @@ int launch_now(const fmm::LaunchArgs& a) {
 
 fmm::LaunchArgs make_args(const void* q, const void* k, const void* v, void* out, int B, int H,
                           int N, int d, int band_k, int rank, int causal, const float* w_near,
-                          const float* w_far, int dtype, void* ws, const Plan& p,
+                          const float* w_far, int dtype, int far_norm, void* ws, const Plan& p,
                           void* stream) {
   fmm::LaunchArgs a;
+  a.far_norm = far_norm;
   a.q = q;
   a.k = k;
   a.v = v;
@@ -240,13 +243,14 @@ Plan plan_for(int B, int H, int N, int d, int band_k, int rank, int causal, int 
 
 int run(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d,
         int band_k, int rank, int causal, const float* w_near, const float* w_far, int dtype,
-        void* ws, size_t ws_bytes, bool own_ws, void* stream) {
-  int st = validate(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype);
+        int far_norm, void* ws, size_t ws_bytes, bool own_ws, void* stream) {
+  int st = validate(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype,
+                    far_norm);
   if (st != FMM_OK) return st;
   const Plan p = plan_for(B, H, N, d, band_k, rank, causal, dtype);
   if (p.ws_bytes == 0) return FMM_ERR_UNSUPPORTED;
   fmm::LaunchArgs a = make_args(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far,
-                                dtype, nullptr, p, stream);
+                                dtype, far_norm, nullptr, p, stream);
   st = check_launch(a);
   if (st != FMM_OK) return st;
   std::unique_lock<std::mutex> ws_lock(ws_mutex(), std::defer_lock);
@@ -269,7 +273,8 @@ namespace fmm {
 int validate_forward(const void* q, const void* k, const void* v, void* out, int B, int H,
                      int N, int d, int band_k, int rank, int causal, const float* w_near,
                      const float* w_far, int dtype) {
-  return validate(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype);
+  return validate(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype,
+                  FMM_FAR_NORM_PER_MAP);
 }
 
 size_t forward_workspace_bytes(int B, int H, int N, int d, int band_k, int rank, int causal,
@@ -281,8 +286,8 @@ int forward_with_workspace(const void* q, const void* k, const void* v, void* ou
                            int N, int d, int band_k, int rank, int causal, const float* w_near,
                            const float* w_far, int dtype, void* ws, size_t ws_bytes,
                            void* stream) {
-  return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype, ws, ws_bytes,
-             false, stream);
+  return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype,
+             FMM_FAR_NORM_PER_MAP, ws, ws_bytes, false, stream);
 }
 
 }  // namespace fmm
@@ -293,13 +298,20 @@ int fmm_attn_forward(const void* q, const void* k, const void* v, void* out, int
                      int N, int d, int band_k, int rank, int causal, const float* w_near,
                      const float* w_far, void* stream) {
   return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, FMM_DTYPE_F32,
-             nullptr, 0, true, stream);
+             FMM_FAR_NORM_PER_MAP, nullptr, 0, true, stream);
 }
 
 int fmm_attn_forward_bf16(const void* q, const void* k, const void* v, void* out, int B, int H,
                           int N, int d, int band_k, int rank, int causal, const float* w_near,
                           const float* w_far, void* stream) {
   return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, FMM_DTYPE_BF16,
+             FMM_FAR_NORM_PER_MAP, nullptr, 0, true, stream);
+}
+
+int fmm_attn_forward_ex(const void* q, const void* k, const void* v, void* out, int B, int H,
+                        int N, int d, int band_k, int rank, int causal, const float* w_near,
+                        const float* w_far, int dtype, int far_norm, void* stream) {
+  return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype, far_norm,
              nullptr, 0, true, stream);
 }
 
@@ -316,8 +328,8 @@ int fmm_attn_forward_ws(const void* q, const void* k, const void* v, void* out, 
                         int N, int d, int band_k, int rank, int causal, const float* w_near,
                         const float* w_far, int dtype, void* workspace, size_t ws_bytes,
                         void* stream) {
-  return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype, workspace,
-             ws_bytes, false, stream);
+  return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype,
+             FMM_FAR_NORM_PER_MAP, workspace, ws_bytes, false, stream);
 }
 
 const char* fmm_attn_status_string(int status) {
@@ -325,7 +337,9 @@ const char* fmm_attn_status_string(int status) {
     case FMM_OK: return "FMM_OK: success";
     case FMM_ERR_INVALID_ARG:
       return "FMM_ERR_INVALID_ARG: null, negative, misaligned or overlapping argument";
-    case FMM_ERR_UNSUPPORTED: return "FMM_ERR_UNSUPPORTED: d must be 16, 32 or 64 and rank 1 or 2";
+    case FMM_ERR_UNSUPPORTED:
+      return "FMM_ERR_UNSUPPORTED: d must be 16, 32, 64 or 128 and rank 1, 2 or 3, within the "
+             "dispatch limits";
     case FMM_ERR_HIP: return "FMM_ERR_HIP: a HIP runtime call or kernel launch failed";
     case FMM_ERR_OOM: return "FMM_ERR_OOM: workspace allocation failed or workspace too small";
     case FMM_ERR_SCRATCH:

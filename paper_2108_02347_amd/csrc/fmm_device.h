@@ -135,6 +135,21 @@ __device__ __forceinline__ float phi_l(float x, int l) {
   phi12(x, p1, p2);
   return l == 0 ? p1 : p2;
 }
+// The first R feature maps of x: phi_1, phi_2 as above and phi_3(x) = tanh(x)
+// (the third map of Sec. 3.2.1).
+template <int R>
+__device__ __forceinline__ void phi_maps(float x, float* p) {
+  float p1, p2;
+  phi12(x, p1, p2);
+  p[0] = p1;
+  if constexpr (R >= 2) p[1] = p2;
+  if constexpr (R >= 3) p[2] = tanhf(x);
+}
+// Feature map l (0-based) of x, for a map index known only at run time.
+__device__ __forceinline__ float phi_any(float x, int l) {
+  if (l == 2) return tanhf(x);
+  return phi_l(x, l);
+}
 
 __device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 

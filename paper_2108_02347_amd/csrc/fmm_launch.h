@@ -20,6 +20,7 @@ struct LaunchArgs {
   const float* w_near;
   const float* w_far;
   int B, H, N, d, band_k, rank, causal, dtype;
+  int far_norm;    // FMM_FAR_NORM_PER_MAP or FMM_FAR_NORM_JOINT
   void* stream;
   float* ws;   // segment states (+ final state for the non-causal form)
   int nseg;        // state segments per (batch, head)
@@ -120,6 +121,12 @@ hipError_t launch_band_pair(const LaunchArgs& a, Launcher& L, const float* fin);
 // a multiple of tile_rows()) from their exclusive prefix records.
 bool causal_strip_applies(int dtype, int d, int band_k, int causal, long long n);
 hipError_t launch_causal_strip(const LaunchArgs& a, Launcher& L, const float* prefix);
+
+// General apply kernel (fmm_wide.hip): any supported width, one to three
+// feature maps, both far-field normalisations, both forms.  recs: the final
+// records (non-causal) or the exclusive prefix records per state segment
+// (causal, advanced in place).
+hipError_t launch_wide(const LaunchArgs& a, Launcher& L, float* recs);
 
 // The C ABI's host logic (fmm_api.cpp), shared with the no-allocation entry
 // point (fmm_noalloc.hip): argument checks, the workspace size of the call's

@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings_and_version():
-    assert binding.version() == 10000
+    assert binding.version() == 10100
     for st in (0, -1, -2, -3, -4, -5):
         assert binding.status_string(st).startswith(
             {0: "FMM_OK", -1: "FMM_ERR_INVALID_ARG", -2: "FMM_ERR_UNSUPPORTED",
@@ -45,7 +45,10 @@ def test_workspace_bytes():
     # one state record per segment plus one final record, rank * d * (d+1) floats
     assert ws(1, 1, 64, 16, 1, 0) >= 2 * 16 * 17 * 4
     assert ws(1, 1, 64, 48, 1, 0) == 0      # unsupported width
-    assert ws(1, 1, 64, 16, 3, 0) == 0      # unsupported rank
+    assert ws(1, 1, 64, 16, 4, 0) == 0      # unsupported rank
+    assert ws(1, 1, 64, 256, 1, 0) == 0     # unsupported width
+    # rank 3 and d = 128 records: rank * d * (d+1) floats each
+    assert ws(1, 1, 64, 128, 3, 1) >= 2 * 3 * 128 * 129 * 4
     assert ws(0, 1, 64, 16, 1, 0) == 0
 
 
@@ -68,8 +71,8 @@ def call(q=FAKE, k=2 * FAKE, v=3 * FAKE, out=4 * FAKE, B=1, H=2, N=64, d=32, kw=
     (dict(q=FAKE + 8), binding.FMM_ERR_INVALID_ARG),          # misaligned
     (dict(out=FAKE + 64), binding.FMM_ERR_INVALID_ARG),       # overlaps q
     (dict(d=48), binding.FMM_ERR_UNSUPPORTED),
-    (dict(d=128), binding.FMM_ERR_UNSUPPORTED),
-    (dict(r=3), binding.FMM_ERR_UNSUPPORTED),
+    (dict(d=256), binding.FMM_ERR_UNSUPPORTED),
+    (dict(r=4), binding.FMM_ERR_UNSUPPORTED),
     (dict(r=0), binding.FMM_ERR_UNSUPPORTED),
     (dict(d=48, bf16=True), binding.FMM_ERR_UNSUPPORTED),
 ])
@@ -135,3 +138,14 @@ def test_noalloc_host_checks():
     assert lib.fmm_attn_forward_noalloc(*args(0, 1024, 64)) == binding.FMM_ERR_INVALID_ARG
     assert binding.workspace_bytes(1, 1024, 64, 64, 2, 1) > binding.noalloc_max_bytes()
     assert lib.fmm_attn_forward_noalloc(*args(T, 1024, 64)) == binding.FMM_ERR_SCRATCH
+
+
+def test_forward_ex_rejects_unknown_normalisation():
+    lib = binding.lib()
+    T = 1 << 40
+    vp = ctypes.c_void_p
+    args = lambda norm, dt=0: (vp(T), vp(2 * T), vp(3 * T), vp(4 * T), 1, 2, 64, 32, 5, 2, 0,
+                               vp(5 * T), vp(6 * T), dt, norm, vp(0))
+    assert lib.fmm_attn_forward_ex(*args(2)) == binding.FMM_ERR_INVALID_ARG
+    assert lib.fmm_attn_forward_ex(*args(-1)) == binding.FMM_ERR_INVALID_ARG
+    assert lib.fmm_attn_forward_ex(*args(0, 7)) == binding.FMM_ERR_UNSUPPORTED

@@ -123,7 +123,7 @@ def test_stress64k_head0_all_rows(causal):
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("causal", [0, 1])
 @pytest.mark.parametrize("rank", [1, 2])
-@pytest.mark.parametrize("d", [16, 32, 64])
+@pytest.mark.parametrize("d", [16, 32, 64, 128])
 def test_sweep_lengths_and_bands(d, rank, causal, dtype):
     # ragged lengths around the 64-row tile and 32-key unit, bands from zero to
     # wider than the sequence (several key-staging rounds), two heads with
@@ -238,7 +238,7 @@ def test_abi_errors_leave_out_untouched():
         ((P(tq), P(tk), P(tv), P(tq), 1, 2, 64, 32, 5, 2, 0, P(twn), P(twf)), binding.FMM_ERR_INVALID_ARG),
         ((P(tq) + 4, P(tk), P(tv), P(out), 1, 2, 63, 32, 5, 2, 0, P(twn), P(twf)), binding.FMM_ERR_INVALID_ARG),
         ((P(tq), P(tk), P(tv), P(out), 1, 2, 64, 48, 5, 2, 0, P(twn), P(twf)), binding.FMM_ERR_UNSUPPORTED),
-        ((P(tq), P(tk), P(tv), P(out), 1, 2, 64, 32, 5, 3, 0, P(twn), P(twf)), binding.FMM_ERR_UNSUPPORTED),
+        ((P(tq), P(tk), P(tv), P(out), 1, 2, 64, 32, 5, 4, 0, P(twn), P(twf)), binding.FMM_ERR_UNSUPPORTED),
     ]
     for args, want in cases:
         st = binding.raw_forward(*args, s, False)
