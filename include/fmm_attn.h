@@ -91,7 +91,10 @@ extern "C" {
 #define FMM_KERNEL_STATE_COMBINE 1 /* sum (non-causal) or exclusive scan       */
 #define FMM_KERNEL_BAND_APPLY    2 /* non-causal near field + far apply + blend */
 #define FMM_KERNEL_CAUSAL_APPLY  3 /* causal near field + prefix far + blend    */
-#define FMM_KERNEL_COUNT         4
+#define FMM_KERNEL_BWD_ROWS      4 /* backward row pass: dq, dS partials        */
+#define FMM_KERNEL_BWD_KEYS      5 /* backward key pass: dk, dv                 */
+#define FMM_KERNEL_BWD_DW        6 /* backward blend-logit reduction            */
+#define FMM_KERNEL_COUNT         7
 
 /*
  * fmm_attn_forward - the operator of Eq. (9) blended as in Eq. (11), fp32.
@@ -189,6 +192,29 @@ int fmm_attn_forward_noalloc(const void* q, const void* k, const void* v, void* 
 
 /* Size in bytes of fmm_attn_forward_noalloc's fixed per-GPU array. */
 size_t fmm_attn_noalloc_max_bytes(void);
+
+/*
+ * fmm_attn_backward - gradients of a scalar loss through dout = dL/d(out) of
+ * the operator computed by fmm_attn_forward / _bf16 (per-map normalisation,
+ * Eq. (9)) with the same arguments:
+ *   dq, dk, dv : [B, H, N, d] of the storage type (dtype), written completely;
+ *   dw_near, dw_far : device float[H], the gradients with respect to the raw
+ *                blend logits (through the sigmoid of Eq. (11)), overwritten.
+ * The gradient formulas are those of the definitions: the banded softmax of
+ * Eq. (3), the quotient of each map in Eq. (9) with the causal sums of Eq. (7)
+ * truncated at i (so the key-side far gradients are suffix sums over the rows
+ * i >= j), the feature-map derivatives and the sigmoid's.  q, k, v, dout are
+ * read only; dq, dk, dv overlap none of them nor each other.  dtype is
+ * FMM_DTYPE_F32 or FMM_DTYPE_BF16 (all gradients accumulated in fp32); fp32
+ * storage at d = 128 returns FMM_ERR_UNSUPPORTED (bf16 is supported).  Uses
+ * the library-owned workspace of (device, stream): the forward state records,
+ * the same amount for the far-field gradient state, and 12 + 8 rank bytes per
+ * row.  Errors as the forward.
+ */
+int fmm_attn_backward(const void* q, const void* k, const void* v, const void* dout,
+                      void* dq, void* dk, void* dv, float* dw_near, float* dw_far,
+                      int B, int H, int N, int d, int band_k, int rank, int causal,
+                      const float* w_near, const float* w_far, int dtype, void* stream);
 
 /* Human-readable text for a status code; never NULL, static storage. */
 const char* fmm_attn_status_string(int status);

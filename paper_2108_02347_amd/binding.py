@@ -27,13 +27,15 @@ FMM_DTYPE_BF16 = 1
 FMM_FAR_NORM_PER_MAP = 0
 FMM_FAR_NORM_JOINT = 1
 
-KERNELS = {"seg_state": 0, "state_combine": 1, "band_apply": 2, "causal_apply": 3}
+KERNELS = {"seg_state": 0, "state_combine": 1, "band_apply": 2, "causal_apply": 3,
+           "bwd_rows": 4, "bwd_keys": 5, "bwd_dw": 6}
 
 EXPORTS = (
     "fmm_attn_forward", "fmm_attn_forward_bf16", "fmm_attn_workspace_bytes",
     "fmm_attn_forward_ws", "fmm_attn_status_string", "fmm_attn_release_workspace",
     "fmm_attn_version", "fmm_attn_kernel_timing", "fmm_attn_kernel_timing_read",
     "fmm_attn_forward_noalloc", "fmm_attn_noalloc_max_bytes", "fmm_attn_forward_ex",
+    "fmm_attn_backward",
 )
 
 _lib = None
@@ -63,6 +65,8 @@ def lib() -> ctypes.CDLL:
         fn.restype = ci
     h.fmm_attn_forward_ws.argtypes = fwd_args[:-1] + [ci, vp, ctypes.c_size_t, vp]
     h.fmm_attn_forward_ws.restype = ci
+    h.fmm_attn_backward.argtypes = [vp] * 9 + [ci] * 7 + [cf, cf, ci, vp]
+    h.fmm_attn_backward.restype = ci
     h.fmm_attn_forward_ex.argtypes = fwd_args[:-1] + [ci, ci, vp]
     h.fmm_attn_forward_ex.restype = ci
     h.fmm_attn_forward_noalloc.argtypes = fwd_args[:-1] + [ci, vp]
@@ -216,6 +220,22 @@ def forward_noalloc(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool
 
 def noalloc_max_bytes() -> int:
     return int(lib().fmm_attn_noalloc_max_bytes())
+
+
+def backward(q, k, v, dout, w_near, w_far, band_k: int, rank: int, causal: bool):
+    """Gradients of the forward (per-map normalisation) for dout = dL/d(out):
+    returns (dq, dk, dv, dw_near, dw_far)."""
+    B, H, N, d = _prep(q, k, v, w_near, w_far)
+    _check_out(dout, q)
+    dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+    dwn = torch.empty_like(w_near)
+    dwf = torch.empty_like(w_far)
+    dt = FMM_DTYPE_BF16 if q.dtype == torch.bfloat16 else FMM_DTYPE_F32
+    _check(lib().fmm_attn_backward(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwn),
+        _ptr(dwf), B, H, N, d, int(band_k), int(rank), int(bool(causal)), _ptr(w_near),
+        _ptr(w_far), dt, _stream_of(q)))
+    return dq, dk, dv, dwn, dwf
 
 
 def raw_forward(q_ptr, k_ptr, v_ptr, out_ptr, B, H, N, d, band_k, rank, causal, wn_ptr,

@@ -6,6 +6,7 @@
 #include <stdint.h>
 #include <stdlib.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <utility>
@@ -266,6 +267,125 @@ int run(const void* q, const void* k, const void* v, void* out, int B, int H, in
   return launch_now(a);
 }
 
+// ------------------------------------------------------------------ backward
+struct BwdPlan {
+  Plan p;
+  size_t off_dpart, off_rowstat, off_rowfar, off_dwpart, total;
+};
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+// Workspace of the backward pass: the forward state records (as the forward
+// plan), the dS records of the same shape, per-row softmax statistics and far
+// quotients, and per-segment blend sums.  0 when it cannot exist.
+BwdPlan bwd_plan(int B, int H, int N, int d, int rank, int dtype) {
+  BwdPlan b;
+  b.p = make_plan(B, H, N, d, rank, dtype == FMM_DTYPE_BF16 ? 2 : 4, fmm::tile_rows());
+  b.total = 0;
+  if (b.p.ws_bytes == 0) return b;
+  typedef unsigned __int128 u128;
+  const u128 bhn = (u128)B * H * N;
+  const u128 rowstat = (u128)align256((size_t)std::min<u128>(bhn * 12, SIZE_MAX / 8));
+  const u128 rowfar = (u128)align256((size_t)std::min<u128>(bhn * rank * 8, SIZE_MAX / 8));
+  const u128 dwp = align256((size_t)B * H * b.p.nseg * 8);
+  const u128 tot = 2 * (u128)b.p.ws_bytes + rowstat + rowfar + dwp;
+  if (tot > (u128)(SIZE_MAX / 4)) return b;
+  b.off_dpart = b.p.ws_bytes;
+  b.off_rowstat = 2 * b.p.ws_bytes;
+  b.off_rowfar = b.off_rowstat + (size_t)rowstat;
+  b.off_dwpart = b.off_rowfar + (size_t)rowfar;
+  b.total = (size_t)tot;
+  return b;
+}
+
+void fill_bwd_args(fmm::BwdArgs& a, const BwdPlan& bp, void* ws, int B, int H) {
+  const uintptr_t w = reinterpret_cast<uintptr_t>(ws);
+  const size_t rec = (size_t)a.rank * a.d * (a.d + 1);
+  const size_t fin_off = (size_t)B * H * bp.p.nseg * rec * sizeof(float);
+  a.part = reinterpret_cast<float*>(w);
+  a.fin = reinterpret_cast<float*>(w + fin_off);
+  a.dpart = reinterpret_cast<float*>(w + bp.off_dpart);
+  a.dfin = reinterpret_cast<float*>(w + bp.off_dpart + fin_off);
+  a.rowstat = reinterpret_cast<float*>(w + bp.off_rowstat);
+  a.rowfar = reinterpret_cast<float*>(w + bp.off_rowfar);
+  a.dwpart = reinterpret_cast<float*>(w + bp.off_dwpart);
+}
+
+int run_backward(const void* q, const void* k, const void* v, const void* dout, void* dq,
+                 void* dk, void* dv, float* dw_near, float* dw_far, int B, int H, int N, int d,
+                 int band_k, int rank, int causal, const float* w_near, const float* w_far,
+                 int dtype, void* stream) {
+  // the inputs as in the forward (dout takes the place of out for the checks)
+  int st = validate(q, k, v, dq, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype,
+                    FMM_FAR_NORM_PER_MAP);
+  if (st != FMM_OK) return st;
+  if (!dout || !dk || !dv || !dw_near || !dw_far) return FMM_ERR_INVALID_ARG;
+  if (d == 128 && dtype == FMM_DTYPE_F32) return FMM_ERR_UNSUPPORTED;
+  const size_t es = dtype == FMM_DTYPE_BF16 ? 2 : 4;
+  const size_t bytes = (size_t)B * H * N * d * es;  // fits: validate checked it
+  for (const void* p : {dout, (const void*)dk, (const void*)dv})
+    if ((uintptr_t)p % 16) return FMM_ERR_INVALID_ARG;
+  if ((uintptr_t)dw_near % 4 || (uintptr_t)dw_far % 4) return FMM_ERR_INVALID_ARG;
+  // gradients overlap neither the inputs nor one another
+  const void* ins[4] = {q, k, v, dout};
+  void* outs[3] = {dq, dk, dv};
+  for (void* o : outs)
+    for (const void* i : ins)
+      if (overlaps(o, i, bytes)) return FMM_ERR_INVALID_ARG;
+  if (overlaps(dq, dk, bytes) || overlaps(dq, dv, bytes) || overlaps(dk, dv, bytes))
+    return FMM_ERR_INVALID_ARG;
+  if (overlaps(dw_near, dw_far, (size_t)H * 4)) return FMM_ERR_INVALID_ARG;
+  const BwdPlan bp = bwd_plan(B, H, N, d, rank, dtype);
+  if (bp.total == 0) return FMM_ERR_UNSUPPORTED;
+  fmm::LaunchArgs fa = make_args(q, k, v, dq, B, H, N, d, band_k, rank, causal, w_near, w_far,
+                                 dtype, FMM_FAR_NORM_PER_MAP, nullptr, bp.p, stream);
+  fmm::BwdArgs ba;
+  ba.q = q;
+  ba.k = k;
+  ba.v = v;
+  ba.dout = dout;
+  ba.dq = dq;
+  ba.dk = dk;
+  ba.dv = dv;
+  ba.dw_near = dw_near;
+  ba.dw_far = dw_far;
+  ba.w_near = w_near;
+  ba.w_far = w_far;
+  ba.B = B;
+  ba.H = H;
+  ba.N = N;
+  ba.d = d;
+  ba.band_k = fa.band_k;
+  ba.rank = rank;
+  ba.causal = causal;
+  ba.dtype = dtype;
+  ba.stream = stream;
+  ba.nseg = bp.p.nseg;
+  ba.L = bp.p.L;
+  fill_bwd_args(ba, bp, nullptr, B, H);
+  EventTimer& t = timer();
+  {
+    std::lock_guard<std::mutex> g(t.mu);
+    fmm::Launcher dry;
+    dry.timer = &t;
+    dry.dry = true;
+    if (fmm::launch_state_only(fa, dry) != hipSuccess ||
+        fmm::launch_backward_tail(ba, dry) != hipSuccess)
+      return dry.err == hipErrorInvalidConfiguration ? FMM_ERR_UNSUPPORTED : FMM_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> wl(ws_mutex());
+  void* ws = nullptr;
+  st = acquire_ws_locked(stream, bp.total, &ws);
+  if (st != FMM_OK) return st;
+  fa.ws = (float*)ws;
+  fill_bwd_args(ba, bp, ws, B, H);
+  std::lock_guard<std::mutex> g(t.mu);
+  fmm::Launcher L;
+  L.timer = &t;
+  if (fmm::launch_state_only(fa, L) != hipSuccess) return FMM_ERR_HIP;
+  return fmm::launch_backward_tail(ba, L) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
+}
+
 }  // namespace
 
 namespace fmm {
@@ -313,6 +433,14 @@ int fmm_attn_forward_ex(const void* q, const void* k, const void* v, void* out, 
                         const float* w_far, int dtype, int far_norm, void* stream) {
   return run(q, k, v, out, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype, far_norm,
              nullptr, 0, true, stream);
+}
+
+int fmm_attn_backward(const void* q, const void* k, const void* v, const void* dout, void* dq,
+                      void* dk, void* dv, float* dw_near, float* dw_far, int B, int H, int N,
+                      int d, int band_k, int rank, int causal, const float* w_near,
+                      const float* w_far, int dtype, void* stream) {
+  return run_backward(q, k, v, dout, dq, dk, dv, dw_near, dw_far, B, H, N, d, band_k, rank,
+                      causal, w_near, w_far, dtype, stream);
 }
 
 size_t fmm_attn_workspace_bytes(int B, int H, int N, int d, int rank, int causal) {

@@ -1,0 +1,862 @@
+// Backward pass of the FMMformer attention operator: the gradients of a loss
+// L through g = dL/dout with respect to q, k, v and the two blend logits.
+// For one (batch, head) slice, with a = sigmoid(w_near), c = sigmoid(w_far):
+//
+//   near field (Eq. (3)), p_ij the banded softmax of tau q_i.k_j:
+//     D_i = a g_i . near_i
+//     ds_ij = p_ij (a g_i . v_j - D_i)
+//     dq_i += tau sum_j ds_ij k_j,  dk_j += tau sum_i ds_ij q_i,
+//     dv_j += a sum_i p_ij g_i
+//   far field (Eq. (7)-(9)), per map l with num_i = phi(q_i)^T S(i),
+//   den_i = phi(q_i)^T z(i):
+//     dnum_i = c g_i / den_i,  dden_i = -c g_i . num_i / den_i^2
+//     dphi(q_i) = S(i) dnum_i + z(i) dden_i
+//     dS(j) = sum_{i in G(j)} phi(q_i) dnum_i^T,  dz(j) = sum_{i in G(j)} phi(q_i) dden_i
+//             (G(j): every row; causal: the rows i >= j, a suffix sum)
+//     dphi(k_j) = dS(j) v_j + dz(j),  dv_j += dS(j)^T phi(k_j)
+//     dq += phi'(q) * dphi(q),  dk += phi'(k) * dphi(k)
+//   blend (Eq. (11)): dw_near = a (1 - a) sum g . near, dw_far = c (1 - c) sum g . far
+//
+// Launch sequence (after the forward state k_seg_state + k_state_combine):
+//   k_bwd_rows   per state segment, walking 64-row tiles: recomputes the near
+//                softmax statistics (row maximum, sum) and D_i, then dq of the
+//                near field in a second sweep over the staged keys; per map
+//                the far numerator and denominator (state record, plus the
+//                intra-tile part and the running prefix in the causal form),
+//                dq of the far field, and the segment's partial
+//                dS = sum phi(q_i) [dnum_i | dden_i]^T; writes dq, the per-row
+//                softmax statistics and (1/den, dden) per map, and the
+//                segment's sums of g . near and g . far
+//   k_state_combine / k_suffix_scan
+//                the dS partials summed per slice (non-causal) or turned into
+//                exclusive suffix sums over segments (causal)
+//   k_bwd_keys   per state segment, walking 64-key tiles (last tile first in
+//                the causal form): near-field dk and dv over the rows whose
+//                band holds the key, the far-field dk and dv from dS (causal:
+//                the segment's suffix record advanced tile by tile plus the
+//                intra-tile rows i >= j); writes dk, dv
+//   k_dw_reduce  the blend-logit gradients, summed in a fixed order
+//
+// Fragment conventions are those of fmm_device.h: a 16-row strip per wave,
+// row-quad accumulators (lane 16g + r holds row r, columns 16cb + 4g + {0..3}),
+// products over 32 buffer rows through the transposed LDS reads.
+#include "fmm_apply.h"
+#include "fmm_device.h"
+#include "fmm_launch.h"
+
+namespace fmm {
+namespace {
+
+template <typename T, int D>
+struct BwdCfg {
+  static constexpr int ST = D + Lay<T>::PAD;
+  static constexpr int ROW = ST * (int)sizeof(T);
+  static constexpr int TILE = TM * ROW;         // 64 staged rows
+  static constexpr int UNIT2 = 2 * 32 * ROW;    // two buffers of one 32-row unit
+  static constexpr int STAT_UNIT = 32 * 3 * 4;  // key pass: m, 1/l, D per row
+  static constexpr int BUDGET = 150 * 1024;
+  static constexpr int UR_FIT = (BUDGET - 2 * TILE - 256 - 2 * NT * 4) / (UNIT2 + STAT_UNIT);
+  static constexpr int UR = UR_FIT > 8 ? 8 : UR_FIT;
+  static_assert(UR >= 2, "a round must hold one tile");
+  static constexpr int WK = 32 * UR;  // rows per staging round
+  // per staged row of the key pass: scaled maximum, 1/l, D; the row pass
+  // reuses the area for its block reduction (2 x NT floats)
+  static constexpr int STAT_BYTES = WK * 12 > 2 * NT * 4 ? WK * 12 : 2 * NT * 4;
+  // [buffer A: WK rows][buffer B: WK rows][tile buffer 1][tile buffer 2][64 floats][stats]
+  static constexpr int LDS = 2 * WK * ROW + 2 * TILE + 256 + STAT_BYTES;
+};
+
+__device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"); }
+
+// Rows [r0, r0 + n) of two [N, D] tensors (rows at or beyond kend read as
+// zero) into row-major LDS buffers of stride ST.
+template <typename T, int D>
+__device__ __forceinline__ void stage_pair(T* sa, T* sb, const T* ha, const T* hb, int r0, int n,
+                                           int kend) {
+  constexpr int ST = D + Lay<T>::PAD;
+  auto ident = [](int i) { return i; };
+  for (int x = 0; x < n; x += 64) {
+    const int m = min(64, n - x);
+    RowCopy<T, D, NT, 64> ca, cb;
+    ca.load(ha, r0 + x, m, kend);
+    cb.load(hb, r0 + x, m, kend);
+    ca.store(sa + x * ST, ST, m, ident);
+    cb.store(sb + x * ST, ST, m, ident);
+  }
+}
+
+// phi_l of 64 rows staged at src (stride ST) into dst; rows at or beyond
+// N - r0 give 0.
+template <typename T, int D>
+__device__ __forceinline__ void stage_phi_rows(const T* src, int r0, int N, int l, T* dst) {
+  using LY = Lay<T>;
+  constexpr int ST = D + LY::PAD, CPR = D / LY::EPC;
+  for (int t = threadIdx.x; t < TM * CPR; t += NT) {
+    const int row = t / CPR, c = t % CPR;
+    const uint4 raw = *reinterpret_cast<const uint4*>(src + row * ST + c * LY::EPC);
+    float x[LY::EPC];
+    if constexpr (sizeof(T) == 2) {
+      const uint16_t* e = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+      for (int i = 0; i < LY::EPC; ++i) x[i] = bf16_to_f32(e[i]);
+    } else {
+      const float* e = reinterpret_cast<const float*>(&raw);
+#pragma unroll
+      for (int i = 0; i < LY::EPC; ++i) x[i] = e[i];
+    }
+    const bool ok = r0 + row < N;
+    float p[LY::EPC];
+#pragma unroll
+    for (int i = 0; i < LY::EPC; ++i) p[i] = ok ? phi_any(x[i], l) : 0.f;
+    uint4 outw;
+    if constexpr (sizeof(T) == 2) {
+      outw = make_uint4(pack_bf16x2(p[0], p[1]), pack_bf16x2(p[2], p[3]),
+                        pack_bf16x2(p[4], p[5]), pack_bf16x2(p[6], p[7]));
+    } else {
+      outw = make_uint4(__float_as_uint(p[0]), __float_as_uint(p[1]), __float_as_uint(p[2]),
+                        __float_as_uint(p[3]));
+    }
+    *reinterpret_cast<uint4*>(dst + row * ST + c * LY::EPC) = outw;
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ typename QuadOf<T>::type rec_quad(const float* p) {
+  const float4 v = *reinterpret_cast<const float4*>(p);
+  const float f[4] = {v.x, v.y, v.z, v.w};
+  return f32_to_quad<T>(f);
+}
+
+// Transposed operand from a tile-order record: lane (r, g) gets
+// X[16cb + r][16eb + 4g + {0..3}] where the record tile (cb, eb) stores
+// X[16cb + 4g' + i][16eb + r'] at lane 16g' + r'.
+template <typename T>
+__device__ __forceinline__ typename QuadOf<T>::type rec_quad_t(const float* rl, int NB, int cb,
+                                                               int eb) {
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const float* p = rl + ((cb * NB + eb) * 64 + 16 * (r >> 2) + 4 * g) * 4 + (r & 3);
+  const float f[4] = {p[0], p[4], p[8], p[12]};
+  return f32_to_quad<T>(f);
+}
+
+template <typename T>
+__device__ __forceinline__ typename QuadOf<T>::type to_quad(const f32x4& x) {
+  const float f[4] = {x[0], x[1], x[2], x[3]};
+  return f32_to_quad<T>(f);
+}
+
+// rec_l += phi(X)^T [Y | y] over the 64 staged rows: px holds phi of the rows
+// (stride ST), py the second factor's rows, ycol (64 floats) the extra column
+// that lands in z; wave w updates feature blocks w, w + 4, ...
+template <typename T, int D>
+__device__ __forceinline__ void record_add(float* rl, const T* px, const T* py,
+                                           const float* ycol, int ST, int w) {
+  using Q = typename QuadOf<T>::type;
+  constexpr int NB = D / 16;
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  for (int cb = w; cb < NB; cb += NW) {
+    f32x4 acc[NB + 1];
+#pragma unroll
+    for (int eb = 0; eb < NB; ++eb)
+      acc[eb] = *reinterpret_cast<const f32x4*>(rl + ((cb * NB + eb) * 64 + lane) * 4);
+    acc[NB] = r == 0 ? *reinterpret_cast<const f32x4*>(rl + D * D + 16 * cb + 4 * g) : zero;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const Q a0 = ld_tquad(px, 32 * u, 16 * cb, ST);
+      const Q a1 = ld_tquad(px, 32 * u + 16, 16 * cb, ST);
+#pragma unroll
+      for (int eb = 0; eb < NB; ++eb)
+        acc[eb] = mma_step2(a0, a1, ld_tquad(py, 32 * u, 16 * eb, ST),
+                            ld_tquad(py, 32 * u + 16, 16 * eb, ST), acc[eb]);
+      float c0[4], c1[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        c0[i] = r == 0 ? ycol[32 * u + 4 * g + i] : 0.f;
+        c1[i] = r == 0 ? ycol[32 * u + 16 + 4 * g + i] : 0.f;
+      }
+      acc[NB] = mma_step2(a0, a1, f32_to_quad<T>(c0), f32_to_quad<T>(c1), acc[NB]);
+    }
+#pragma unroll
+    for (int eb = 0; eb < NB; ++eb)
+      *reinterpret_cast<f32x4*>(rl + ((cb * NB + eb) * 64 + lane) * 4) = acc[eb];
+    if (r == 0) *reinterpret_cast<f32x4*>(rl + D * D + 16 * cb + 4 * g) = acc[NB];
+  }
+}
+
+// Band validity of key j (unit-local offset 16b + 4g + i from j0) for query
+// row `row`: the interval logic of near_units.
+template <bool CAUSAL>
+__device__ __forceinline__ void band_interval(int row, int j0, int g, int N, int band_k, int& lo,
+                                              int& span) {
+  lo = max(row - band_k, 0) - j0 - 4 * g;
+  span = min(CAUSAL ? row : row + band_k, N - 1) - j0 - 4 * g - lo;
+  if (span < 0) {
+    lo = 64;
+    span = 0;
+  }
+}
+
+// ------------------------------------------------------------------ row pass
+// Near-field dq of the strip over key units [ua_lo, ua_hi] staged through map:
+// dq += tau sum_j p_ij (a g_i . v_j - D_i) k_j with p from the final row
+// statistics (maximum m of the raw scores, 1/l).
+template <typename T, int D, bool CAUSAL, class Map>
+__device__ __forceinline__ void near_dq_units(f32x4* dq, const typename QuadOf<T>::type* qq,
+                                              const typename QuadOf<T>::type* gq, const T* kr,
+                                              const T* vr, int ST, Map map, int ua_lo, int ua_hi,
+                                              int i0, int N, int band_k, float scale2, float ms,
+                                              float inv_l, float Di, float a_tau, float a) {
+  using Q = typename QuadOf<T>::type;
+  constexpr int NB = D / 16;
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const int row = i0 + r;
+  for (int ua = ua_lo; ua <= ua_hi; ++ua) {
+    const T* kx = kr + map(ua) * ST;
+    const T* vx = vr + map(ua) * ST;
+    int lo, span;
+    band_interval<CAUSAL>(row, ua * 32, g, N, band_k, lo, span);
+    float ds[2][4];
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      Q ka[NB], va[NB];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        ka[cb] = ld_quad(kx, 16 * b + r, 16 * cb + 4 * g, ST);
+        va[cb] = ld_quad(vx, 16 * b + r, 16 * cb + 4 * g, ST);
+      }
+      const f32x4 s = contract<NB>(ka, qq, f32x4{0.f, 0.f, 0.f, 0.f});
+      const f32x4 dp = contract<NB>(va, gq, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = (unsigned)(16 * b + i - lo) <= (unsigned)span;
+        const float p = ok ? __builtin_amdgcn_exp2f(fmaf(s[i], scale2, -ms)) * inv_l : 0.f;
+        ds[b][i] = p * fmaf(a, dp[i], -Di) * a_tau;
+      }
+    }
+    const Q d0 = f32_to_quad<T>(ds[0]), d1 = f32_to_quad<T>(ds[1]);
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb)
+      dq[cb] = mma_step2(ld_tquad(kx, 0, 16 * cb, ST), ld_tquad(kx, 16, 16 * cb, ST), d0, d1,
+                         dq[cb]);
+  }
+  mfma_drain();
+}
+
+template <typename T, int D, bool CAUSAL>
+__global__ __launch_bounds__(NT) void k_bwd_rows(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const T* __restrict__ dout, T* __restrict__ dq, float* __restrict__ recs,
+    float* __restrict__ dpart, float* __restrict__ rowstat, float* __restrict__ rowfar,
+    float* __restrict__ dwpart, const float* __restrict__ w_near, const float* __restrict__ w_far,
+    int H, int N, int band_k, int L, int nseg, int rank, float scale2) {
+  using Q = typename QuadOf<T>::type;
+  using C = BwdCfg<T, D>;
+  constexpr int NB = D / 16, ST = C::ST;
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
+  T* sk = reinterpret_cast<T*>(dyn_smem);
+  T* sv = sk + C::WK * ST;
+  T* tb1 = sv + C::WK * ST;  // phi_l of the tile's keys, then of its queries
+  T* tb2 = tb1 + TM * ST;    // dnum rows of the tile
+  float* dden_s = reinterpret_cast<float*>(tb2 + TM * ST);
+  float* red = dden_s + 64;  // block reduction of the blend-logit sums
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int bh = lin / nseg, seg = lin % nseg, h = bh % H;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const size_t base = (size_t)bh * N * D;
+  const size_t REC = (size_t)rank * D * (D + 1);
+  float* rec = CAUSAL ? recs + ((size_t)bh * nseg + seg) * REC : recs + (size_t)bh * REC;
+  float* drec = dpart + ((size_t)bh * nseg + seg) * REC;
+  const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
+  const float tau = scale2 * 0.69314718055994531f;  // 1/sqrt(d)
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  for (size_t t = threadIdx.x; t < REC; t += NT) drec[t] = 0.f;
+  float acc_near = 0.f, acc_far = 0.f;  // this lane's share of g . near and g . far
+  const int s0 = seg * L, s1 = min(N, s0 + L);
+  for (int t0 = s0; t0 < s1; t0 += TM) {
+    const int i0 = t0 + 16 * w, row = i0 + r;
+    const bool row_ok = row < N;
+    Q qq[NB], gq[NB];
+    load_q<T, D>(q + base, row, N, qq);
+    load_q<T, D>(dout + base, row, N, gq);
+    float gf[NB][4];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) quad_to_f32(gq[cb], gf[cb]);
+    // ---- near field: statistics, then dq in a second sweep
+    NearState<D> st;
+    st.init();
+    const int ka = (max(0, t0 - band_k) >> 5) << 5;
+    const int hi = CAUSAL ? t0 + TM : ((min(N, t0 + TM + band_k) + 31) & ~31);
+    const int nr = (hi - ka + C::WK - 1) / C::WK;
+    int ks = ka;
+    for (int rr = nr - 1; rr >= 0; --rr) {
+      const int ke = hi - rr * C::WK;
+      ks = max(ka, ke - C::WK);
+      __syncthreads();
+      stage_pair<T, D>(sk, sv, k + base, v + base, ks, ke - ks, N);
+      __syncthreads();
+      const int lo = max(max(0, i0 - band_k), ks);
+      const int hj = min(min(N - 1, CAUSAL ? i0 + 15 : i0 + 15 + band_k), ke - 1);
+      if (lo <= hj)
+        near_units<T, D, CAUSAL, 2>(st, qq, sk, sv, ST, RoundMap{ks}, lo >> 5, hj >> 5, i0, N,
+                                    band_k, scale2);
+    }
+    mfma_drain();
+    const float inv_l = row_ok ? 1.f / st.o[NB][0] : 0.f;
+    float gn = 0.f;  // g . (unnormalised near) over this lane's columns
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) gn = fmaf(gf[nb][i], st.o[nb][i], gn);
+    const float gnear = col_sum(gn) * inv_l;  // g_i . near_i
+    acc_near += gn * inv_l;
+    const float Di = sn * gnear;
+    const float ms = (st.m == -INFINITY ? 0.f : st.m) * scale2;
+    if (row_ok && g == 0) {
+      float* sp = rowstat + ((size_t)bh * N + row) * 3;
+      sp[0] = ms;
+      sp[1] = inv_l;
+      sp[2] = Di;
+    }
+    f32x4 dqa[NB];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) dqa[cb] = zero;
+    for (int rr = nr - 1; rr >= 0; --rr) {
+      const int ke = hi - rr * C::WK;
+      const int ks2 = max(ka, ke - C::WK);
+      if (nr > 1) {
+        __syncthreads();
+        stage_pair<T, D>(sk, sv, k + base, v + base, ks2, ke - ks2, N);
+        __syncthreads();
+      }
+      const int lo = max(max(0, i0 - band_k), ks2);
+      const int hj = min(min(N - 1, CAUSAL ? i0 + 15 : i0 + 15 + band_k), ke - 1);
+      if (lo <= hj)
+        near_dq_units<T, D, CAUSAL>(dqa, qq, gq, sk, sv, ST, RoundMap{ks2}, lo >> 5, hj >> 5, i0,
+                                    N, band_k, scale2, ms, inv_l, Di, tau, sn);
+    }
+    // ks: first key of the last staged round, which holds the tile's keys
+    // (causal form)
+    // ---- far field, one map at a time
+    for (int l = 0; l < rank; ++l) {
+      Q pq[NB];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        float x[4], p[4];
+        quad_to_f32(qq[cb], x);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[i] = phi_any(x[i], l);
+        pq[cb] = f32_to_quad<T>(p);
+      }
+      float* rl = rec + (size_t)l * D * (D + 1);
+      float* drl = drec + (size_t)l * D * (D + 1);
+      const T* vt = sv + (t0 - ks) * ST;
+      f32x4 num[NB + 1];
+#pragma unroll
+      for (int nb = 0; nb <= NB; ++nb) num[nb] = zero;
+      if constexpr (CAUSAL) {
+        // the tile's keys: phi_l(K_t) into tb1; intra-tile part of num, den
+        __syncthreads();
+        stage_phi_rows<T, D>(sk + (t0 - ks) * ST, t0, N, l, tb1);
+        __syncthreads();
+        const Q ones = quad_fill<T>(1.f);
+        for (int u = 0; u <= (w >> 1); ++u) {
+          const bool diag = u == (w >> 1);
+          float a2[2][4];
+#pragma unroll
+          for (int b = 0; b < 2; ++b) {
+            Q ka2[NB];
+#pragma unroll
+            for (int cb = 0; cb < NB; ++cb)
+              ka2[cb] = ld_quad(tb1, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
+            const f32x4 at = contract<NB>(ka2, pq, zero);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int j = t0 + 32 * u + 16 * b + 4 * g + i;
+              a2[b][i] = (!diag || j <= row) ? at[i] : 0.f;
+            }
+          }
+          const Q p0 = f32_to_quad<T>(a2[0]), p1 = f32_to_quad<T>(a2[1]);
+          const T* vx = vt + 32 * u * ST;
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            num[nb] = mma_step2(ld_tquad(vx, 0, 16 * nb, ST), ld_tquad(vx, 16, 16 * nb, ST), p0,
+                                p1, num[nb]);
+          num[NB] = mma_step2(ones, ones, p0, p1, num[NB]);
+        }
+        mfma_drain();
+      }
+      // the product with the record (non-causal: the slice's total; causal:
+      // the prefix before the tile)
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        Q a[NB];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) a[cb] = rec_quad<T>(rl + ((cb * NB + nb) * 64 + lane) * 4);
+        num[nb] = contract<NB>(a, pq, num[nb]);
+      }
+      {
+        Q zq[NB];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) zq[cb] = rec_quad<T>(rl + D * D + 16 * cb + 4 * g);
+        num[NB] = contract<NB>(zq, pq, num[NB]);
+      }
+      // quotient rule
+      const float inv_den = row_ok ? fast_rcp(num[NB][0]) : 0.f;
+      float gnum = 0.f;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) gnum = fmaf(gf[nb][i], num[nb][i], gnum);
+      acc_far += gnum * inv_den;
+      const float dden = -sfw * col_sum(gnum) * inv_den * inv_den;
+      const float cid = sfw * inv_den;
+      Q dnq[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        float f[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) f[i] = gf[nb][i] * cid;
+        dnq[nb] = f32_to_quad<T>(f);
+      }
+      if (row_ok && g == 0) {
+        float* fp = rowfar + (((size_t)bh * N + row) * rank + l) * 2;
+        fp[0] = inv_den;
+        fp[1] = dden;
+      }
+      // dphi(q) = S dnum + z dden (+ intra-tile keys in the causal form)
+      f32x4 dph[NB];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) dph[cb] = zero;
+      if constexpr (CAUSAL) {
+        for (int u = 0; u <= (w >> 1); ++u) {
+          const bool diag = u == (w >> 1);
+          float a2[2][4];
+#pragma unroll
+          for (int b = 0; b < 2; ++b) {
+            Q va[NB];
+#pragma unroll
+            for (int eb = 0; eb < NB; ++eb)
+              va[eb] = ld_quad(vt, 32 * u + 16 * b + r, 16 * eb + 4 * g, ST);
+            const f32x4 at = contract<NB>(va, dnq, zero);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int j = t0 + 32 * u + 16 * b + 4 * g + i;
+              a2[b][i] = (!diag || j <= row) ? at[i] + dden : 0.f;
+            }
+          }
+          const Q p0 = f32_to_quad<T>(a2[0]), p1 = f32_to_quad<T>(a2[1]);
+#pragma unroll
+          for (int cb = 0; cb < NB; ++cb)
+            dph[cb] = mma_step2(ld_tquad(tb1, 32 * u, 16 * cb, ST),
+                                ld_tquad(tb1, 32 * u + 16, 16 * cb, ST), p0, p1, dph[cb]);
+        }
+        mfma_drain();
+      }
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        Q a[NB];
+#pragma unroll
+        for (int eb = 0; eb < NB; ++eb) a[eb] = rec_quad_t<T>(rl, NB, cb, eb);
+        dph[cb] = contract<NB>(a, dnq, dph[cb]);
+      }
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float4 z = *reinterpret_cast<const float4*>(rl + D * D + 16 * cb + 4 * g);
+        const float zf[4] = {z.x, z.y, z.z, z.w};
+        float x[4];
+        quad_to_f32(qq[cb], x);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float dg = 0.f;
+          if (l == 0) dg = x[i] > 0.f ? 1.f : __expf(x[i]);
+          else if (l == 1) dg = x[i] < 0.f ? -1.f : -__expf(-x[i]);
+          else {
+            const float t = tanhf(x[i]);
+            dg = 1.f - t * t;
+          }
+          dqa[cb][i] = fmaf(dg, dph[cb][i] + zf[i] * dden, dqa[cb][i]);
+        }
+      }
+      if constexpr (CAUSAL) {
+        // advance the forward prefix record by the tile's keys (tb1 still
+        // holds phi_l(K_t)), unless this is the segment's last tile
+        if (t0 + TM < s1) {
+          __syncthreads();  // every wave has read record l for this tile
+          float* ones_col = dden_s;
+          if (threadIdx.x < 64) ones_col[threadIdx.x] = 1.f;
+          __syncthreads();
+          record_add<T, D>(rl, tb1, vt, ones_col, ST, w);
+        }
+      }
+      // the segment's dS partial: rows' phi_l(q) into tb1, dnum into tb2,
+      // dden into dden_s
+      __syncthreads();
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        *reinterpret_cast<Q*>(tb1 + (16 * w + r) * ST + 16 * cb + 4 * g) = pq[cb];
+        *reinterpret_cast<Q*>(tb2 + (16 * w + r) * ST + 16 * cb + 4 * g) =
+            row_ok ? dnq[cb] : to_quad<T>(zero);
+      }
+      if (g == 0) dden_s[16 * w + r] = row_ok ? dden : 0.f;
+      __syncthreads();
+      record_add<T, D>(drl, tb1, tb2, dden_s, ST, w);
+    }
+    store_row<T, D>(dq + base, row, N, dqa);
+  }
+  // the segment's sums of g . near and g . far, in a fixed order
+  __syncthreads();
+  red[threadIdx.x] = acc_near;
+  red[NT + threadIdx.x] = acc_far;
+  __syncthreads();
+  if (threadIdx.x < 2) {
+    float s = 0.f;
+    for (int t = 0; t < NT; ++t) s += red[threadIdx.x * NT + t];
+    dwpart[((size_t)bh * nseg + seg) * 2 + threadIdx.x] = s;
+  }
+}
+
+// ------------------------------------------------------------------ suffix scan
+// Causal dS: each segment's record becomes the sum of the records of the
+// segments after it (exclusive suffix), in place, in a fixed order.
+__global__ __launch_bounds__(256) void k_suffix_scan(float* __restrict__ part, int nseg, int rec,
+                                                     int nchunk) {
+  const int bh = blockIdx.x / nchunk;
+  const int e = (blockIdx.x - bh * nchunk) * 256 + threadIdx.x;
+  if (e >= rec) return;
+  float* p = part + (size_t)bh * nseg * rec + e;
+  float run = 0.f;
+  for (int s = nseg - 1; s >= 0; --s) {
+    const float t = p[(size_t)s * rec];
+    p[(size_t)s * rec] = run;
+    run += t;
+  }
+}
+
+// ------------------------------------------------------------------ key pass
+template <typename T, int D, bool CAUSAL>
+__global__ __launch_bounds__(NT) void k_bwd_keys(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const T* __restrict__ dout, T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ drecs,
+    const float* __restrict__ rowstat, const float* __restrict__ rowfar,
+    const float* __restrict__ w_near, const float* __restrict__ w_far, int H, int N, int band_k,
+    int L, int nseg, int rank, float scale2) {
+  using Q = typename QuadOf<T>::type;
+  using C = BwdCfg<T, D>;
+  constexpr int NB = D / 16, ST = C::ST;
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
+  T* sq = reinterpret_cast<T*>(dyn_smem);
+  T* sg = sq + C::WK * ST;
+  T* tb1 = sg + C::WK * ST;  // phi_l of the tile's query rows
+  T* tb2 = tb1 + TM * ST;    // dnum rows of the tile
+  float* dden_s = reinterpret_cast<float*>(tb2 + TM * ST);
+  float* stat = dden_s + 64;  // per staged row: scaled maximum, 1/l, D
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int bh = lin / nseg, seg = lin % nseg, h = bh % H;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const size_t base = (size_t)bh * N * D;
+  const size_t REC = (size_t)rank * D * (D + 1);
+  float* drec = CAUSAL ? drecs + ((size_t)bh * nseg + seg) * REC : drecs + (size_t)bh * REC;
+  const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
+  const float tau = scale2 * 0.69314718055994531f;
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  const int s0 = seg * L, s1 = min(N, s0 + L);
+  const int ntile = (s1 - s0 + TM - 1) / TM;
+  for (int tt = 0; tt < ntile; ++tt) {
+    // causal: last tile first, so that the suffix record covers the rows
+    // after the tile
+    const int t0 = CAUSAL ? s0 + (ntile - 1 - tt) * TM : s0 + tt * TM;
+    const int j0 = t0 + 16 * w, key = j0 + r;
+    Q kq[NB], vq[NB];
+    load_q<T, D>(k + base, key, N, kq);
+    load_q<T, D>(v + base, key, N, vq);
+    f32x4 dka[NB], dva[NB];
+#pragma unroll
+    for (int cb = 0; cb < NB; ++cb) {
+      dka[cb] = zero;
+      dva[cb] = zero;
+    }
+    // ---- near field over the rows whose band holds the strip's keys
+    const int ra = CAUSAL ? t0 : (max(0, t0 - band_k) >> 5) << 5;
+    const int rb = (min(N, t0 + TM + band_k) + 31) & ~31;
+    for (int rs = ra; rs < rb; rs += C::WK) {
+      const int nrow = min(C::WK, rb - rs);
+      __syncthreads();
+      stage_pair<T, D>(sq, sg, q + base, dout + base, rs, nrow, N);
+      for (int t = threadIdx.x; t < nrow; t += NT) {
+        const int i = rs + t;
+        const bool ok = i < N;
+        const float* sp = rowstat + ((size_t)bh * N + (ok ? i : 0)) * 3;
+        stat[3 * t] = ok ? sp[0] : 0.f;
+        stat[3 * t + 1] = ok ? sp[1] : 0.f;
+        stat[3 * t + 2] = ok ? sp[2] : 0.f;
+      }
+      __syncthreads();
+      // rows of this round that can hold the strip's keys in their band
+      const int lo = max(max(0, j0 - (CAUSAL ? 0 : band_k)), rs);
+      const int hj = min(min(N - 1, j0 + 15 + band_k), rs + nrow - 1);
+      for (int ua = lo >> 5; ua <= (hj >> 5) && lo <= hj; ++ua) {
+        const int ur = ua * 32 - rs;  // LDS row of the unit
+        const T* qx = sq + ur * ST;
+        const T* gx = sg + ur * ST;
+        float pp[2][4], ds[2][4];
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          Q qa[NB], ga[NB];
+#pragma unroll
+          for (int cb = 0; cb < NB; ++cb) {
+            qa[cb] = ld_quad(qx, 16 * b + r, 16 * cb + 4 * g, ST);
+            ga[cb] = ld_quad(gx, 16 * b + r, 16 * cb + 4 * g, ST);
+          }
+          const f32x4 s = contract<NB>(qa, kq, zero);
+          const f32x4 dp = contract<NB>(ga, vq, zero);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int lr = ur + 16 * b + 4 * g + i;  // staged row
+            const int irow = rs + lr;
+            const bool ok = irow < N && key < N &&
+                            (CAUSAL ? (irow >= key && irow - key <= band_k)
+                                    : (irow - key <= band_k && key - irow <= band_k));
+            const float p = ok ? __builtin_amdgcn_exp2f(fmaf(s[i], scale2, -stat[3 * lr])) *
+                                     stat[3 * lr + 1]
+                               : 0.f;
+            pp[b][i] = p * sn;
+            ds[b][i] = p * fmaf(sn, dp[i], -stat[3 * lr + 2]) * tau;
+          }
+        }
+        const Q p0 = f32_to_quad<T>(pp[0]), p1 = f32_to_quad<T>(pp[1]);
+        const Q d0 = f32_to_quad<T>(ds[0]), d1 = f32_to_quad<T>(ds[1]);
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+          dva[cb] = mma_step2(ld_tquad(gx, 0, 16 * cb, ST), ld_tquad(gx, 16, 16 * cb, ST), p0, p1,
+                              dva[cb]);
+          dka[cb] = mma_step2(ld_tquad(qx, 0, 16 * cb, ST), ld_tquad(qx, 16, 16 * cb, ST), d0, d1,
+                              dka[cb]);
+        }
+      }
+      mfma_drain();
+    }
+    // ---- far field, one map at a time
+    for (int l = 0; l < rank; ++l) {
+      Q pk[NB];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        float x[4], p[4];
+        quad_to_f32(kq[cb], x);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[i] = phi_any(x[i], l);
+        pk[cb] = f32_to_quad<T>(p);
+      }
+      float* drl = drec + (size_t)l * D * (D + 1);
+      f32x4 dph[NB];
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) dph[cb] = zero;
+      if constexpr (CAUSAL) {
+        // the tile's rows: phi_l(q) into tb1, dnum = c g / den into tb2,
+        // dden into dden_s
+        __syncthreads();
+        {
+          RowCopy<T, D, NT, 64> cq, cg;
+          cq.load(q + base, t0, TM, N);
+          cg.load(dout + base, t0, TM, N);
+          auto ident = [](int i) { return i; };
+          cq.store(sq, ST, TM, ident);
+          cg.store(sg, ST, TM, ident);
+        }
+        if (threadIdx.x < 64) {
+          const int i = t0 + threadIdx.x;
+          const bool ok = i < N;
+          const float* fp = rowfar + (((size_t)bh * N + (ok ? i : 0)) * rank + l) * 2;
+          dden_s[threadIdx.x] = ok ? fp[1] : 0.f;
+          stat[threadIdx.x] = ok ? sfw * fp[0] : 0.f;  // c / den
+        }
+        __syncthreads();
+        stage_phi_rows<T, D>(sq, t0, N, l, tb1);
+        {
+          using LY = Lay<T>;
+          constexpr int CPR = D / LY::EPC;
+          for (int t = threadIdx.x; t < TM * CPR; t += NT) {
+            const int rr = t / CPR, c = t % CPR;
+            const uint4 raw = *reinterpret_cast<const uint4*>(sg + rr * ST + c * LY::EPC);
+            const float f = stat[rr];
+            uint4 outw;
+            if constexpr (sizeof(T) == 2) {
+              const uint16_t* e = reinterpret_cast<const uint16_t*>(&raw);
+              float x[8];
+#pragma unroll
+              for (int i = 0; i < 8; ++i) x[i] = bf16_to_f32(e[i]) * f;
+              outw = make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]),
+                                pack_bf16x2(x[4], x[5]), pack_bf16x2(x[6], x[7]));
+            } else {
+              const float* e = reinterpret_cast<const float*>(&raw);
+              outw = make_uint4(__float_as_uint(e[0] * f), __float_as_uint(e[1] * f),
+                                __float_as_uint(e[2] * f), __float_as_uint(e[3] * f));
+            }
+            *reinterpret_cast<uint4*>(tb2 + rr * ST + c * LY::EPC) = outw;
+          }
+        }
+        __syncthreads();
+        // rows i >= j of the tile: units (w >> 1) .. 1, the first one masked
+        for (int u = (w >> 1); u < 2; ++u) {
+          const bool diag = u == (w >> 1);
+          float cc[2][4], ee[2][4];
+#pragma unroll
+          for (int b = 0; b < 2; ++b) {
+            Q na[NB], fa[NB];
+#pragma unroll
+            for (int cb = 0; cb < NB; ++cb) {
+              na[cb] = ld_quad(tb2, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
+              fa[cb] = ld_quad(tb1, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
+            }
+            const f32x4 c1 = contract<NB>(na, vq, zero);
+            const f32x4 e1 = contract<NB>(fa, pk, zero);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int lr = 32 * u + 16 * b + 4 * g + i;
+              const bool ok = !diag || t0 + lr >= key;
+              cc[b][i] = ok ? c1[i] + dden_s[lr] : 0.f;
+              ee[b][i] = ok ? e1[i] : 0.f;
+            }
+          }
+          const Q c0q = f32_to_quad<T>(cc[0]), c1q = f32_to_quad<T>(cc[1]);
+          const Q e0q = f32_to_quad<T>(ee[0]), e1q = f32_to_quad<T>(ee[1]);
+#pragma unroll
+          for (int cb = 0; cb < NB; ++cb) {
+            dph[cb] = mma_step2(ld_tquad(tb1, 32 * u, 16 * cb, ST),
+                                ld_tquad(tb1, 32 * u + 16, 16 * cb, ST), c0q, c1q, dph[cb]);
+            dva[cb] = mma_step2(ld_tquad(tb2, 32 * u, 16 * cb, ST),
+                                ld_tquad(tb2, 32 * u + 16, 16 * cb, ST), e0q, e1q, dva[cb]);
+          }
+        }
+        mfma_drain();
+      }
+      // dS (j) from the record: dphi(k) += dS v + dz, dv += dS^T phi(k)
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        Q a[NB];
+#pragma unroll
+        for (int eb = 0; eb < NB; ++eb) a[eb] = rec_quad_t<T>(drl, NB, cb, eb);
+        dph[cb] = contract<NB>(a, vq, dph[cb]);
+      }
+#pragma unroll
+      for (int eb = 0; eb < NB; ++eb) {
+        Q a[NB];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb)
+          a[cb] = rec_quad<T>(drl + ((cb * NB + eb) * 64 + lane) * 4);
+        dva[eb] = contract<NB>(a, pk, dva[eb]);
+      }
+#pragma unroll
+      for (int cb = 0; cb < NB; ++cb) {
+        const float4 z = *reinterpret_cast<const float4*>(drl + D * D + 16 * cb + 4 * g);
+        const float zf[4] = {z.x, z.y, z.z, z.w};
+        float x[4];
+        quad_to_f32(kq[cb], x);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float dg = 0.f;
+          if (l == 0) dg = x[i] > 0.f ? 1.f : __expf(x[i]);
+          else if (l == 1) dg = x[i] < 0.f ? -1.f : -__expf(-x[i]);
+          else {
+            const float t = tanhf(x[i]);
+            dg = 1.f - t * t;
+          }
+          dka[cb][i] = fmaf(dg, dph[cb][i] + zf[i], dka[cb][i]);
+        }
+      }
+      if constexpr (CAUSAL) {
+        // advance the suffix record by the tile's rows, unless this is the
+        // segment's first tile (the last one walked)
+        if (tt + 1 < ntile) {
+          __syncthreads();  // every wave has read record l for this tile
+          record_add<T, D>(drl, tb1, tb2, dden_s, ST, w);
+        }
+      }
+    }
+    store_row<T, D>(dk + base, key, N, dka);
+    store_row<T, D>(dv + base, key, N, dva);
+  }
+}
+
+// ------------------------------------------------------------------ dw
+__global__ void k_dw_reduce(const float* __restrict__ dwpart, const float* __restrict__ w_near,
+                            const float* __restrict__ w_far, float* __restrict__ dw_near,
+                            float* __restrict__ dw_far, int B, int H, int nseg) {
+  const int h = blockIdx.x * blockDim.x + threadIdx.x;
+  if (h >= H) return;
+  float sn = 0.f, sf = 0.f;
+  for (int b = 0; b < B; ++b)
+    for (int s = 0; s < nseg; ++s) {
+      const float* p = dwpart + (((size_t)b * H + h) * nseg + s) * 2;
+      sn += p[0];
+      sf += p[1];
+    }
+  const float a = sigmoidf_exact(w_near[h]), c = sigmoidf_exact(w_far[h]);
+  dw_near[h] = a * (1.f - a) * sn;
+  dw_far[h] = c * (1.f - c) * sf;
+}
+
+template <typename T, int D, bool CAUSAL>
+hipError_t launch_bwd_dc(const BwdArgs& a, Launcher& L) {
+  using C = BwdCfg<T, D>;
+  static std::atomic<unsigned long long> set_rows{0}, set_keys{0};
+  if (L.note(lds_limit_once((const void*)k_bwd_rows<T, D, CAUSAL>, C::LDS, set_rows)) !=
+          hipSuccess ||
+      L.note(lds_limit_once((const void*)k_bwd_keys<T, D, CAUSAL>, C::LDS, set_keys)) !=
+          hipSuccess)
+    return L.err;
+  const float scale2 = 1.4426950408889634f / sqrtf((float)D);
+  const int BH = a.B * a.H;
+  const size_t REC = (size_t)a.rank * D * (D + 1);
+  hipStream_t s = (hipStream_t)a.stream;
+  const dim3 grid(BH * a.nseg);
+  L(FMM_KERNEL_BWD_ROWS, k_bwd_rows<T, D, CAUSAL>, grid, dim3(NT), (size_t)C::LDS, s,
+    (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, (T*)a.dq,
+    CAUSAL ? a.part : a.fin, a.dpart, a.rowstat, a.rowfar, a.dwpart, a.w_near, a.w_far, a.H, a.N,
+    a.band_k, a.L, a.nseg, a.rank, scale2);
+  const int nchunk = (int)((REC + 255) / 256);
+  const dim3 sgrid((unsigned)std::min<long long>((long long)nchunk * BH, 0xFFFFFFFFll));
+  if constexpr (CAUSAL) {
+    L(FMM_KERNEL_STATE_COMBINE, k_suffix_scan, sgrid, dim3(256), 0, s, a.dpart, a.nseg, (int)REC,
+      nchunk);
+  } else {
+    (void)launch_state_sum(L, a.dpart, a.dfin, a.nseg, (int)REC, BH, s);
+  }
+  L(FMM_KERNEL_BWD_KEYS, k_bwd_keys<T, D, CAUSAL>, grid, dim3(NT), (size_t)C::LDS, s,
+    (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, (T*)a.dk, (T*)a.dv,
+    CAUSAL ? a.dpart : a.dfin, (const float*)a.rowstat, (const float*)a.rowfar, a.w_near, a.w_far,
+    a.H, a.N, a.band_k, a.L, a.nseg, a.rank, scale2);
+  L(FMM_KERNEL_BWD_DW, k_dw_reduce, dim3((a.H + 63) / 64), dim3(64), 0, s,
+    (const float*)a.dwpart, a.w_near, a.w_far, a.dw_near, a.dw_far, a.B, a.H, a.nseg);
+  return L.err;
+}
+
+template <typename T, int D>
+hipError_t launch_bwd_d(const BwdArgs& a, Launcher& L) {
+  return a.causal ? launch_bwd_dc<T, D, true>(a, L) : launch_bwd_dc<T, D, false>(a, L);
+}
+
+template <typename T>
+hipError_t launch_bwd_t(const BwdArgs& a, Launcher& L) {
+  switch (a.d) {
+    case 16: return launch_bwd_d<T, 16>(a, L);
+    case 32: return launch_bwd_d<T, 32>(a, L);
+    case 64: return launch_bwd_d<T, 64>(a, L);
+    case 128:
+      // fp32 at d = 128 holds twice the operand registers of bf16 and is not
+      // built (the host rejects it as unsupported)
+      if constexpr (sizeof(T) == 2) return launch_bwd_d<T, 128>(a, L);
+      return L.note(hipErrorInvalidConfiguration);
+    default: return L.note(hipErrorInvalidValue);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_backward_tail(const BwdArgs& a, Launcher& L) {
+  return a.dtype == FMM_DTYPE_BF16 ? launch_bwd_t<bf16_t>(a, L) : launch_bwd_t<float>(a, L);
+}
+
+}  // namespace fmm

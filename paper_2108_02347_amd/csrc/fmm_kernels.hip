@@ -897,10 +897,11 @@ static hipError_t launch_tuned(const LaunchArgs& a, Launcher& L, float* part, fl
   return L.err;
 }
 
+// The far-field state: per-segment records T_l = phi_l(K)^T [V | 1], then the
+// fixed-order sum (non-causal, into the final records) or the exclusive scan
+// over segments (causal, in place).
 template <typename T, int D, int R>
-static hipError_t launch_all(const LaunchArgs& a, Launcher& L) {
-  // widths above 64 and three feature maps take the general apply kernel
-  constexpr bool tuned = D <= 64 && R <= 2;
+static hipError_t launch_state(const LaunchArgs& a, Launcher& L) {
   const int BH = a.B * a.H;
   const int REC = R * D * (D + 1);
   hipStream_t s = (hipStream_t)a.stream;
@@ -935,35 +936,56 @@ static hipError_t launch_all(const LaunchArgs& a, Launcher& L) {
   else
     L(FMM_KERNEL_STATE_COMBINE, k_state_combine<false>, cgrid, dim3(256), 0, s, part, fin,
       a.nseg, REC, nchunk);
-  if (L.err != hipSuccess) return L.err;
+  return L.err;
+}
 
+template <typename T, int D, int R>
+static hipError_t launch_all(const LaunchArgs& a, Launcher& L) {
+  // widths above 64 and three feature maps take the general apply kernel
+  constexpr bool tuned = D <= 64 && R <= 2;
+  if (launch_state<T, D, R>(a, L) != hipSuccess) return L.err;
+  float* part = a.ws;
+  float* fin = reinterpret_cast<float*>(reinterpret_cast<uintptr_t>(a.ws) +
+                                        (size_t)a.B * a.H * a.nseg * R * D * (D + 1) *
+                                            sizeof(float));
   if constexpr (tuned) {
     if (a.far_norm == FMM_FAR_NORM_PER_MAP) return launch_tuned<T, D, R>(a, L, part, fin);
   }
   return launch_wide(a, L, a.causal ? part : fin);
 }
 
-template <typename T>
+template <typename T, bool STATE_ONLY>
 static hipError_t dispatch_d(const LaunchArgs& a, Launcher& L) {
+#define FMM_CASE(DD, RR)                                                          \
+  case DD * 4 + RR:                                                              \
+    return STATE_ONLY ? launch_state<T, DD, RR>(a, L) : launch_all<T, DD, RR>(a, L);
   switch (a.d * 4 + a.rank) {
-    case 16 * 4 + 1: return launch_all<T, 16, 1>(a, L);
-    case 16 * 4 + 2: return launch_all<T, 16, 2>(a, L);
-    case 16 * 4 + 3: return launch_all<T, 16, 3>(a, L);
-    case 32 * 4 + 1: return launch_all<T, 32, 1>(a, L);
-    case 32 * 4 + 2: return launch_all<T, 32, 2>(a, L);
-    case 32 * 4 + 3: return launch_all<T, 32, 3>(a, L);
-    case 64 * 4 + 1: return launch_all<T, 64, 1>(a, L);
-    case 64 * 4 + 2: return launch_all<T, 64, 2>(a, L);
-    case 64 * 4 + 3: return launch_all<T, 64, 3>(a, L);
-    case 128 * 4 + 1: return launch_all<T, 128, 1>(a, L);
-    case 128 * 4 + 2: return launch_all<T, 128, 2>(a, L);
-    case 128 * 4 + 3: return launch_all<T, 128, 3>(a, L);
+    FMM_CASE(16, 1) FMM_CASE(16, 2) FMM_CASE(16, 3)
+    FMM_CASE(32, 1) FMM_CASE(32, 2) FMM_CASE(32, 3)
+    FMM_CASE(64, 1) FMM_CASE(64, 2) FMM_CASE(64, 3)
+    FMM_CASE(128, 1) FMM_CASE(128, 2) FMM_CASE(128, 3)
     default: return L.note(hipErrorInvalidValue);
   }
+#undef FMM_CASE
 }
 
 hipError_t launch_forward(const LaunchArgs& a, Launcher& L) {
-  return a.dtype == FMM_DTYPE_BF16 ? dispatch_d<bf16_t>(a, L) : dispatch_d<float>(a, L);
+  return a.dtype == FMM_DTYPE_BF16 ? dispatch_d<bf16_t, false>(a, L)
+                                   : dispatch_d<float, false>(a, L);
+}
+
+hipError_t launch_state_only(const LaunchArgs& a, Launcher& L) {
+  return a.dtype == FMM_DTYPE_BF16 ? dispatch_d<bf16_t, true>(a, L)
+                                   : dispatch_d<float, true>(a, L);
+}
+
+hipError_t launch_state_sum(Launcher& L, float* part, float* fin, int nseg, int rec, int BH,
+                            hipStream_t s) {
+  const int nchunk = (rec + 63) / 64;
+  const dim3 cgrid((unsigned)std::min<long long>((long long)nchunk * BH, 0xFFFFFFFFll));
+  L(FMM_KERNEL_STATE_COMBINE, k_state_combine<false>, cgrid, dim3(256), 0, s, part, fin, nseg,
+    rec, nchunk);
+  return L.err;
 }
 
 int tile_rows() { return TM; }

@@ -128,6 +128,38 @@ hipError_t launch_causal_strip(const LaunchArgs& a, Launcher& L, const float* pr
 // (causal, advanced in place).
 hipError_t launch_wide(const LaunchArgs& a, Launcher& L, float* recs);
 
+// Backward pass (fmm_bwd.hip).  The forward state (k_seg_state +
+// k_state_combine into part / fin) is launched first by launch_state_only;
+// launch_backward_tail then runs the row pass, the dS combine, the key pass
+// and the blend-logit reduction.
+struct BwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const void* dout;
+  void* dq;
+  void* dk;
+  void* dv;
+  float* dw_near;
+  float* dw_far;
+  const float* w_near;
+  const float* w_far;
+  int B, H, N, d, band_k, rank, causal, dtype;
+  void* stream;
+  int nseg, L;      // state segments (as the forward plan)
+  float* part;      // forward segment records (causal: exclusive prefix)
+  float* fin;       // forward final records (non-causal)
+  float* dpart;     // dS partial records per segment (causal: exclusive suffix)
+  float* dfin;      // dS totals per slice (non-causal)
+  float* rowstat;   // [B*H*N][3]: scaled row maximum, 1/l, D
+  float* rowfar;    // [B*H*N][rank][2]: 1/den, dden
+  float* dwpart;    // [B*H*nseg][2]: sums of g . near, g . far
+};
+hipError_t launch_state_only(const LaunchArgs& a, Launcher& L);
+hipError_t launch_state_sum(Launcher& L, float* part, float* fin, int nseg, int rec, int BH,
+                            hipStream_t s);
+hipError_t launch_backward_tail(const BwdArgs& a, Launcher& L);
+
 // The C ABI's host logic (fmm_api.cpp), shared with the no-allocation entry
 // point (fmm_noalloc.hip): argument checks, the workspace size of the call's
 // segment plan, and the checked launch with a given workspace.
