@@ -619,6 +619,65 @@ def main():
     }
     del qb, kb, vb, ob
 
+    # forward + backward (the paper's efficiency measurement times both): the
+    # stress64k shape in both forms and the N = 4096 shape; per-kernel event
+    # means of the backward's row and key passes
+    gq = torch.randn(tq.shape, generator=torch.Generator(device="cuda:0").manual_seed(7),
+                     device="cuda:0").to(tq.dtype)
+    fb_rec = {}
+    for form, causal in (("noncausal", 0), ("causal", 1)):
+        def fwd_bwd():
+            binding.forward(tq, tk, tv, twn, twf, w.band_k, w.rank, causal, out=out_c)
+            binding.backward(tq, tk, tv, gq, twn, twf, w.band_k, w.rank, causal)
+        t_fb = timed(fwd_bwd, max(5, args.steps // 4), 2, torch)
+        t_b = timed(lambda: binding.backward(tq, tk, tv, gq, twn, twf, w.band_k, w.rank, causal),
+                    max(5, args.steps // 4), 1, torch)
+        for name in binding.KERNELS:
+            binding.kernel_timing_read(name)
+        binding.kernel_timing(True)
+        timed(lambda: binding.backward(tq, tk, tv, gq, twn, twf, w.band_k, w.rank, causal),
+              max(5, args.steps // 4), 0, torch)
+        binding.kernel_timing(False)
+        kb = {}
+        for name in ("bwd_rows", "bwd_keys"):
+            ms, n = binding.kernel_timing_read(name)
+            if n:
+                us = ms * 1e3 / n
+                byt = (5 if name == "bwd_rows" else 6) * X
+                kb[name] = {"events_us": round(us, 3), "alg_bytes": byt,
+                            "events_hbm_frac": round(byt / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+        fb_rec[form] = {"fwd_bwd_ms": round(t_fb * 1e3, 4),
+                        "fwd_bwd_tokens_per_s": round(w.B * w.N / t_fb, 1),
+                        "bwd_ms": round(t_b * 1e3, 4), "kernels": kb}
+    t4fb = timed(lambda: (binding.forward(q4, k4, v4, wn4, wf4, w4.band_k, w4.rank, 0, out=o4),
+                          binding.backward(q4, k4, v4, o4, wn4, wf4, w4.band_k, w4.rank, 0)),
+                 max(5, args.steps // 2), 2, torch)
+    fb_rec["n4096_noncausal"] = {"fwd_bwd_ms": round(t4fb * 1e3, 4),
+                                 "fwd_bwd_tokens_per_s": round(w4.B * w4.N / t4fb, 1)}
+    del gq
+
+    # the general path at the 2^16-token shape: head width 128, three feature
+    # maps, joint normalisation (whole-call rates)
+    ext = {}
+    for label, dd, rank, joint in (("d128_rank2", 128, 2, False), ("d64_rank3", 64, 3, False),
+                                   ("d64_rank2_joint", 64, 2, True)):
+        gen2 = torch.Generator(device="cuda:0").manual_seed(11)
+        shp2 = (w.B, w.H, w.N, dd)
+        qe, ke, ve = (torch.randn(shp2, generator=gen2, device="cuda:0").mul_(dd ** -0.5)
+                      .to(torch.bfloat16) for _ in range(3))
+        oe = torch.empty_like(qe)
+        rr = {}
+        for causal in (0, 1):
+            te = timed(lambda: binding.forward(qe, ke, ve, twn, twf, w.band_k, rank, causal,
+                                               out=oe, joint=joint),
+                       max(5, args.steps // 4), 2, torch)
+            Xe = w.B * w.H * w.N * dd * 2
+            rr["causal" if causal else "noncausal"] = {
+                "ms_per_call": round(te * 1e3, 4), "tokens_per_s": round(w.B * w.N / te, 1),
+                "op_hbm_frac_4X": round(4 * Xe / te / 1e9 / HBM_PEAK_GBS, 4)}
+        ext[label] = rr
+        del qe, ke, ve, oe
+
     # the other workloads: whole-call throughput, no per-kernel figures
     others = {}
     for name, dtype in (("tiny", "f32"), ("lra1k", "f32"), ("lra1k", "bf16"), ("lm256", "f32")):
@@ -694,6 +753,8 @@ def main():
         "n4096": n4096,
         "n4096_b128": n4096_b128,
         "other_workloads": others,
+        "forward_backward": fb_rec,
+        "general_path": ext,
         "hbm_achievable": hbm_ceiling(torch),
         "kernel_source_hash": kernel_source_hash(),
     }
