@@ -78,6 +78,7 @@ __all__ = [
     "fmm_attention_rows",
     "far_terms_stream",
     "fmm_attention_backward_stream",
+    "fmm_layer_forward",
 ]
 
 
@@ -508,3 +509,27 @@ def fmm_attention_backward_stream(q, k, v, w_near, w_far, dout, band_k: int, ran
     dw_near = sa * (1.0 - sa) * np.einsum("bhic,bhic->h", dout, near)
     dw_far = sc * (1.0 - sc) * np.einsum("bhic,bhic->h", dout, far)
     return dq, dk, dv, dw_near, dw_far
+
+
+# ---------------------------------------------------------------- attention layer
+
+def fmm_layer_forward(x, w_qkv, w_out, heads: int, w_near, w_far, band_k: int, rank: int,
+                      causal: bool, norm: str = "map") -> np.ndarray:
+    """The attention layer around the operator (Sec. 1.1, Step 1, and the
+    output projection): per token t, [q_t | k_t | v_t] = x_t W_qkv (W_qkv of
+    shape [E, 3E]; within each of q, k, v the E = heads * d columns are the
+    heads in order, d columns each); the operator runs per head on
+    [B, heads, N, d]; the heads' outputs are concatenated per token (head
+    order) and multiplied by W_out [E, E].  x: [B, N, E]; returns [B, N, E]."""
+    x = np.asarray(x, dtype=np.float64)
+    w_qkv = np.asarray(w_qkv, dtype=np.float64)
+    w_out = np.asarray(w_out, dtype=np.float64)
+    b_, n, e = x.shape
+    if e % heads or w_qkv.shape != (e, 3 * e) or w_out.shape != (e, e):
+        raise ValueError("x [B, N, E], w_qkv [E, 3E], w_out [E, E], E divisible by heads")
+    d = e // heads
+    qkv = (x @ w_qkv).reshape(b_, n, 3, heads, d)
+    q, k, v = (np.ascontiguousarray(qkv[:, :, p].transpose(0, 2, 1, 3)) for p in range(3))
+    o = fmm_attention_stream(q, k, v, w_near, w_far, band_k, rank, causal, norm)
+    merged = o.transpose(0, 2, 1, 3).reshape(b_, n, e)
+    return merged @ w_out

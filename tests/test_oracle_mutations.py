@@ -100,6 +100,12 @@ MUTATIONS = [
     ("backward: sigmoid derivative missing its (1 - sigma)",
      "dw_near = sa * (1.0 - sa) * np.einsum",
      "dw_near = sa * np.einsum"),
+    ("layer: heads taken d-major",
+     "qkv = (x @ w_qkv).reshape(b_, n, 3, heads, d)",
+     "qkv = (x @ w_qkv).reshape(b_, n, 3, d, heads).transpose(0, 1, 2, 4, 3)"),
+    ("layer: heads merged in the wrong order",
+     "merged = o.transpose(0, 2, 1, 3).reshape(b_, n, e)",
+     "merged = o.transpose(0, 2, 3, 1).reshape(b_, n, e)"),
     ("backward: key-side near gradient unscaled",
      "dk[:, :, j] += tau * ds[:, :, ok, t, None] * q[:, :, rows[ok]]",
      "dk[:, :, j] += ds[:, :, ok, t, None] * q[:, :, rows[ok]]"),

@@ -551,3 +551,48 @@ def test_backward_chunking_is_invisible():
         b = ref.fmm_attention_backward_stream(q, k, v, wn, wf, dout, 3, 2, causal)
         for x, y in zip(a, b):
             np.testing.assert_allclose(x, y, rtol=1e-12, atol=1e-13)
+
+
+# ------------------------------------------------------------------ attention layer
+
+def test_layer_with_identity_projections_is_the_operator():
+    # W_qkv = [I | I | I], W_out = I: the layer is the operator applied to the
+    # token vectors split into heads (head h = columns h*d .. h*d + d - 1)
+    b, n, h, d = 2, 37, 3, 4
+    e = h * d
+    x = rnd((b, n, e), 110)
+    eye = np.eye(e)
+    wn, wf = rnd(h, 111), rnd(h, 112)
+    for causal in (False, True):
+        got = ref.fmm_layer_forward(x, np.concatenate([eye, eye, eye], axis=1), eye, h, wn, wf,
+                                    3, 2, causal)
+        heads = np.ascontiguousarray(x.reshape(b, n, h, d).transpose(0, 2, 1, 3))
+        op = ref.fmm_attention_stream(heads, heads, heads, wn, wf, 3, 2, causal)
+        np.testing.assert_allclose(got, op.transpose(0, 2, 1, 3).reshape(b, n, e), rtol=1e-13,
+                                   atol=1e-14)
+
+
+def test_layer_projections_by_brute_force():
+    # distinct q, k, v projections and an output projection, checked against
+    # per-token loops over the weight matrices and the per-head operator
+    b, n, h, d = 1, 9, 2, 3
+    e = h * d
+    x = rnd((b, n, e), 113)
+    wqkv, wo = rnd((e, 3 * e), 114), rnd((e, e), 115)
+    wn, wf = rnd(h, 116), rnd(h, 117)
+    got = ref.fmm_layer_forward(x, wqkv, wo, h, wn, wf, 2, 1, False)
+    q = np.zeros((b, h, n, d)); k = np.zeros_like(q); v = np.zeros_like(q)
+    for t in range(n):
+        for hh in range(h):
+            for c in range(d):
+                col = hh * d + c
+                q[0, hh, t, c] = sum(x[0, t, i] * wqkv[i, col] for i in range(e))
+                k[0, hh, t, c] = sum(x[0, t, i] * wqkv[i, e + col] for i in range(e))
+                v[0, hh, t, c] = sum(x[0, t, i] * wqkv[i, 2 * e + col] for i in range(e))
+    o = ref.fmm_attention_stream(q, k, v, wn, wf, 2, 1, False)
+    want = np.zeros((b, n, e))
+    for t in range(n):
+        for j in range(e):
+            want[0, t, j] = sum(o[0, hh, t, c] * wo[hh * d + c, j]
+                                for hh in range(h) for c in range(d))
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-13)
