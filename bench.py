@@ -678,6 +678,24 @@ def main():
         ext[label] = rr
         del qe, ke, ve, oe
 
+    # the attention layer at the long-range model shape (2 heads, 64-dim
+    # embedding) and 4K tokens: QKV projection + operator + output projection
+    gen3 = torch.Generator(device="cuda:0").manual_seed(13)
+    E4, H4 = 64, 2
+    xl = torch.randn((w4.B, w4.N, E4), generator=gen3, device="cuda:0").to(torch.bfloat16)
+    wl = torch.randn((E4, 3 * E4), generator=gen3, device="cuda:0").div_(E4 ** 0.5).to(
+        torch.bfloat16)
+    wo = torch.randn((E4, E4), generator=gen3, device="cuda:0").div_(E4 ** 0.5).to(
+        torch.bfloat16)
+    yl = torch.empty_like(xl)
+    tl = timed(lambda: binding.layer_forward(xl, wl, wo, H4, wn4, wf4, w4.band_k, w4.rank, 0,
+                                             out=yl), args.steps, args.warmup, torch)
+    layer_rec = {"shape": "B=8 N=4096 E=64 H=2 (d=32) bf16 k=20 rank=2 non-causal",
+                 "ms_per_call": round(tl * 1e3, 4),
+                 "tokens_per_s": round(w4.B * w4.N / tl, 1),
+                 "operator_ms_per_call": round(t4 * 1e3, 4)}
+    del xl, wl, wo, yl
+
     # the other workloads: whole-call throughput, no per-kernel figures
     others = {}
     for name, dtype in (("tiny", "f32"), ("lra1k", "f32"), ("lra1k", "bf16"), ("lm256", "f32")):
@@ -754,6 +772,7 @@ def main():
         "n4096_b128": n4096_b128,
         "other_workloads": others,
         "forward_backward": fb_rec,
+        "attention_layer": layer_rec,
         "general_path": ext,
         "hbm_achievable": hbm_ceiling(torch),
         "kernel_source_hash": kernel_source_hash(),

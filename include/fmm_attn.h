@@ -94,7 +94,8 @@ extern "C" {
 #define FMM_KERNEL_BWD_ROWS      4 /* backward row pass: dq, dS partials        */
 #define FMM_KERNEL_BWD_KEYS      5 /* backward key pass: dk, dv                 */
 #define FMM_KERNEL_BWD_DW        6 /* backward blend-logit reduction            */
-#define FMM_KERNEL_COUNT         7
+#define FMM_KERNEL_LAYER_COPY    7 /* attention layer: head split and merge     */
+#define FMM_KERNEL_COUNT         8
 
 /*
  * fmm_attn_forward - the operator of Eq. (9) blended as in Eq. (11), fp32.
@@ -215,6 +216,30 @@ int fmm_attn_backward(const void* q, const void* k, const void* v, const void* d
                       void* dq, void* dk, void* dv, float* dw_near, float* dw_far,
                       int B, int H, int N, int d, int band_k, int rank, int causal,
                       const float* w_near, const float* w_far, int dtype, void* stream);
+
+/*
+ * fmm_attn_layer_forward - the attention layer around the operator: the
+ * Step-1 projections of Sec. 1.1 and an output projection, per token t
+ *   [q_t | k_t | v_t] = x_t W_qkv,  out_t = concat_h(o_{h,t}) W_out
+ * with the operator (per-map normalisation, as fmm_attn_forward) between.
+ *   x       : [B, N, E] tokens, E = H * d with d in {16, 32, 64, 128}.
+ *   w_qkv   : [E, 3E] row-major; columns [0, E) give q, [E, 2E) k, [2E, 3E)
+ *             v, each with the H heads in order (d columns per head).
+ *   w_out   : [E, E] row-major; rows h*d .. h*d + d-1 multiply head h.
+ *   y       : [B, N, E], written completely; must overlap none of x, w_qkv,
+ *             w_out.
+ *   B, N, E, H, band_k, rank, causal, w_near, w_far: as fmm_attn_forward
+ *             (w_near, w_far hold H logits).
+ *   dtype   : FMM_DTYPE_F32 or FMM_DTYPE_BF16 for x, the weights, y and the
+ *             intermediate q, k, v and head outputs (fp32 accumulation).
+ * The projections are rocBLAS GEMMs on `stream`; the intermediates live in the
+ * library-owned workspace of (device, stream).  B * N must stay below 2^31.
+ * Argument errors enqueue nothing; FMM_ERR_HIP also covers a failing rocBLAS
+ * call (earlier steps of the call may then be enqueued).
+ */
+int fmm_attn_layer_forward(const void* x, const void* w_qkv, const void* w_out, void* y,
+                           int B, int N, int E, int H, int band_k, int rank, int causal,
+                           const float* w_near, const float* w_far, int dtype, void* stream);
 
 /* Human-readable text for a status code; never NULL, static storage. */
 const char* fmm_attn_status_string(int status);

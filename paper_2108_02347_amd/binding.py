@@ -28,14 +28,14 @@ FMM_FAR_NORM_PER_MAP = 0
 FMM_FAR_NORM_JOINT = 1
 
 KERNELS = {"seg_state": 0, "state_combine": 1, "band_apply": 2, "causal_apply": 3,
-           "bwd_rows": 4, "bwd_keys": 5, "bwd_dw": 6}
+           "bwd_rows": 4, "bwd_keys": 5, "bwd_dw": 6, "layer_copy": 7}
 
 EXPORTS = (
     "fmm_attn_forward", "fmm_attn_forward_bf16", "fmm_attn_workspace_bytes",
     "fmm_attn_forward_ws", "fmm_attn_status_string", "fmm_attn_release_workspace",
     "fmm_attn_version", "fmm_attn_kernel_timing", "fmm_attn_kernel_timing_read",
     "fmm_attn_forward_noalloc", "fmm_attn_noalloc_max_bytes", "fmm_attn_forward_ex",
-    "fmm_attn_backward",
+    "fmm_attn_backward", "fmm_attn_layer_forward",
 )
 
 _lib = None
@@ -65,6 +65,8 @@ def lib() -> ctypes.CDLL:
         fn.restype = ci
     h.fmm_attn_forward_ws.argtypes = fwd_args[:-1] + [ci, vp, ctypes.c_size_t, vp]
     h.fmm_attn_forward_ws.restype = ci
+    h.fmm_attn_layer_forward.argtypes = [vp] * 4 + [ci] * 7 + [cf, cf, ci, vp]
+    h.fmm_attn_layer_forward.restype = ci
     h.fmm_attn_backward.argtypes = [vp] * 9 + [ci] * 7 + [cf, cf, ci, vp]
     h.fmm_attn_backward.restype = ci
     h.fmm_attn_forward_ex.argtypes = fwd_args[:-1] + [ci, ci, vp]
@@ -236,6 +238,34 @@ def backward(q, k, v, dout, w_near, w_far, band_k: int, rank: int, causal: bool)
         _ptr(dwf), B, H, N, d, int(band_k), int(rank), int(bool(causal)), _ptr(w_near),
         _ptr(w_far), dt, _stream_of(q)))
     return dq, dk, dv, dwn, dwf
+
+
+def layer_forward(x, w_qkv, w_out, heads: int, w_near, w_far, band_k: int, rank: int,
+                  causal: bool, out=None):
+    """The attention layer: [q | k | v] = x W_qkv, the operator per head, the
+    heads concatenated per token times W_out.  x [B, N, E]; returns [B, N, E]."""
+    if x.dim() != 3 or x.device.type != "cuda" or x.dtype not in _DTYPES:
+        raise ValueError("x must be a [B, N, E] float32 or bfloat16 CUDA/HIP tensor")
+    B, N, E = x.shape
+    for name, t, shp in (("w_qkv", w_qkv, (E, 3 * E)), ("w_out", w_out, (E, E))):
+        if t.dtype != x.dtype or t.device != x.device or tuple(t.shape) != shp:
+            raise ValueError(f"{name} must be a {shp} tensor of x's dtype on x's device")
+    for t in (x, w_qkv, w_out):
+        if not t.is_contiguous():
+            raise ValueError("x, w_qkv and w_out must be contiguous")
+    for name, w in (("w_near", w_near), ("w_far", w_far)):
+        if (w.dtype != torch.float32 or w.device != x.device or w.numel() != heads
+                or not w.is_contiguous()):
+            raise ValueError(f"{name} must be a contiguous float32 device tensor of H values")
+    if out is None:
+        out = torch.empty_like(x)
+    else:
+        _check_out(out, x)
+    dt = FMM_DTYPE_BF16 if x.dtype == torch.bfloat16 else FMM_DTYPE_F32
+    _check(lib().fmm_attn_layer_forward(
+        _ptr(x), _ptr(w_qkv), _ptr(w_out), _ptr(out), B, N, E, int(heads), int(band_k),
+        int(rank), int(bool(causal)), _ptr(w_near), _ptr(w_far), dt, _stream_of(x)))
+    return out
 
 
 def raw_forward(q_ptr, k_ptr, v_ptr, out_ptr, B, H, N, d, band_k, rank, causal, wn_ptr,

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libfmm_attn.so")
 SOURCES = ["fmm_kernels.hip", "fmm_wide.hip", "fmm_bwd.hip", "fmm_pair.hip", "fmm_causal.hip",
-           "fmm_noalloc.hip", "fmm_api.cpp"]
+           "fmm_noalloc.hip", "fmm_layer.hip", "fmm_api.cpp"]
 HEADERS = ["fmm_device.h", "fmm_launch.h", "fmm_oct.h", "fmm_apply.h"]
 
 
@@ -66,7 +66,9 @@ def build(verbose: bool = False) -> str:
                 sys.stderr.write(out)
         if failed:
             raise RuntimeError(f"hipcc failed on {', '.join(failed)}")
-        cmd = [cc, "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + ["-o", LIB + ".tmp"]
+        # rocBLAS serves the attention layer's projections
+        cmd = ([cc, "--offload-arch=gfx950", "-shared", "-fPIC"] + objs +
+               ["-L/opt/rocm/lib", "-lrocblas", "-Wl,-rpath,/opt/rocm/lib", "-o", LIB + ".tmp"])
         if verbose:
             print(" ".join(cmd), flush=True)
         res = subprocess.run(cmd, capture_output=True, text=True)

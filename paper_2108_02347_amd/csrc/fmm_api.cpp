@@ -386,6 +386,102 @@ int run_backward(const void* q, const void* k, const void* v, const void* dout, 
   return fmm::launch_backward_tail(ba, L) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
 }
 
+// ------------------------------------------------------------------ layer
+std::mutex& blas_mutex() {
+  static std::mutex* m = new std::mutex();
+  return *m;
+}
+
+// rocBLAS handle of the current device (created once per device).
+void* blas_handle() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  static std::map<int, void*>* handles = new std::map<int, void*>();
+  void*& h = (*handles)[dev];
+  if (!h) h = fmm::layer_blas_handle_create();
+  return h;
+}
+
+int run_layer(const void* x, const void* w_qkv, const void* w_out, void* y, int B, int N, int E,
+              int H, int band_k, int rank, int causal, const float* w_near, const float* w_far,
+              int dtype, void* stream) {
+  if (!x || !w_qkv || !w_out || !y || !w_near || !w_far) return FMM_ERR_INVALID_ARG;
+  if (B < 1 || N < 1 || E < 1 || H < 1 || band_k < 0 || E % H) return FMM_ERR_INVALID_ARG;
+  if (causal != 0 && causal != 1) return FMM_ERR_INVALID_ARG;
+  if (dtype != FMM_DTYPE_F32 && dtype != FMM_DTYPE_BF16) return FMM_ERR_UNSUPPORTED;
+  const int d = E / H;
+  if (!supported(d, rank)) return FMM_ERR_UNSUPPORTED;
+  const size_t es = dtype == FMM_DTYPE_BF16 ? 2 : 4;
+  typedef unsigned __int128 u128;
+  const u128 tokens = (u128)B * N;
+  if (tokens > (u128)INT32_MAX || (u128)3 * E > (u128)INT32_MAX) return FMM_ERR_UNSUPPORTED;
+  const u128 xbytes = tokens * E * es;
+  if (xbytes * 8 > (u128)INT64_MAX) return FMM_ERR_INVALID_ARG;
+  for (const void* p : {x, w_qkv, w_out, (const void*)y})
+    if ((uintptr_t)p % 16) return FMM_ERR_INVALID_ARG;
+  if ((uintptr_t)w_near % 4 || (uintptr_t)w_far % 4) return FMM_ERR_INVALID_ARG;
+  const size_t xb = (size_t)xbytes, wq = (size_t)E * 3 * E * es, wo = (size_t)E * E * es;
+  if (overlaps(y, x, xb) || overlaps(y, w_qkv, std::max(xb, wq)) ||
+      overlaps(y, w_out, std::max(xb, wo)))
+    return FMM_ERR_INVALID_ARG;
+  // workspace: qkv, q, k, v, o, merged heads, then the operator's records
+  const Plan p = plan_for(B, H, N, d, band_k, rank, causal, dtype);
+  if (p.ws_bytes == 0) return FMM_ERR_UNSUPPORTED;
+  const size_t seg = align256(xb);
+  const size_t off_qkv = 0, off_q = 3 * seg, off_k = 4 * seg, off_v = 5 * seg, off_o = 6 * seg,
+               off_m = 7 * seg, off_ws = 8 * seg;
+  const size_t total = off_ws + p.ws_bytes;
+  auto at = [](void* base, size_t off) {
+    return reinterpret_cast<void*>(reinterpret_cast<uintptr_t>(base) + off);
+  };
+  fmm::LaunchArgs a = make_args(at(nullptr, off_q), at(nullptr, off_k), at(nullptr, off_v),
+                                at(nullptr, off_o), B, H, N, d, band_k, rank, causal, w_near,
+                                w_far, dtype, FMM_FAR_NORM_PER_MAP, nullptr, p, stream);
+  int st = check_launch(a);
+  if (st != FMM_OK) return st;
+  {
+    EventTimer& t = timer();
+    std::lock_guard<std::mutex> g(t.mu);
+    fmm::Launcher dry;
+    dry.timer = &t;
+    dry.dry = true;
+    fmm::launch_layer_copy(dry, true, dtype, nullptr, nullptr, nullptr, nullptr, B, N, H, d,
+                           (hipStream_t)stream);
+    fmm::launch_layer_copy(dry, false, dtype, nullptr, nullptr, nullptr, nullptr, B, N, H, d,
+                           (hipStream_t)stream);
+    if (dry.err != hipSuccess)
+      return dry.err == hipErrorInvalidConfiguration ? FMM_ERR_UNSUPPORTED : FMM_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> bl(blas_mutex());
+  void* hdl = blas_handle();
+  if (!hdl) return FMM_ERR_HIP;
+  std::lock_guard<std::mutex> wl(ws_mutex());
+  void* ws = nullptr;
+  st = acquire_ws_locked(stream, total, &ws);
+  if (st != FMM_OK) return st;
+  a.q = at(ws, off_q);
+  a.k = at(ws, off_k);
+  a.v = at(ws, off_v);
+  a.out = at(ws, off_o);
+  a.ws = (float*)at(ws, off_ws);
+  const int M = B * N;
+  if (fmm::layer_gemm(hdl, stream, dtype, x, w_qkv, at(ws, off_qkv), M, E, 3 * E) != hipSuccess)
+    return FMM_ERR_HIP;
+  EventTimer& t = timer();
+  std::lock_guard<std::mutex> g(t.mu);
+  fmm::Launcher L;
+  L.timer = &t;
+  if (fmm::launch_layer_copy(L, true, dtype, at(ws, off_qkv), at(ws, off_q), at(ws, off_k),
+                             at(ws, off_v), B, N, H, d, (hipStream_t)stream) != hipSuccess ||
+      fmm::launch_forward(a, L) != hipSuccess ||
+      fmm::launch_layer_copy(L, false, dtype, at(ws, off_o), at(ws, off_m), nullptr, nullptr, B,
+                             N, H, d, (hipStream_t)stream) != hipSuccess)
+    return FMM_ERR_HIP;
+  if (fmm::layer_gemm(hdl, stream, dtype, at(ws, off_m), w_out, y, M, E, E) != hipSuccess)
+    return FMM_ERR_HIP;
+  return FMM_OK;
+}
+
 }  // namespace
 
 namespace fmm {
@@ -441,6 +537,13 @@ int fmm_attn_backward(const void* q, const void* k, const void* v, const void* d
                       const float* w_far, int dtype, void* stream) {
   return run_backward(q, k, v, dout, dq, dk, dv, dw_near, dw_far, B, H, N, d, band_k, rank,
                       causal, w_near, w_far, dtype, stream);
+}
+
+int fmm_attn_layer_forward(const void* x, const void* w_qkv, const void* w_out, void* y, int B,
+                           int N, int E, int H, int band_k, int rank, int causal,
+                           const float* w_near, const float* w_far, int dtype, void* stream) {
+  return run_layer(x, w_qkv, w_out, y, B, N, E, H, band_k, rank, causal, w_near, w_far, dtype,
+                   stream);
 }
 
 size_t fmm_attn_workspace_bytes(int B, int H, int N, int d, int rank, int causal) {

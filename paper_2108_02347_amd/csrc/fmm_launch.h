@@ -160,6 +160,15 @@ hipError_t launch_state_sum(Launcher& L, float* part, float* fin, int nseg, int 
                             hipStream_t s);
 hipError_t launch_backward_tail(const BwdArgs& a, Launcher& L);
 
+// Attention layer pieces (fmm_layer.hip): the head split / merge copies, the
+// projections through rocBLAS (row-major C [M, Nc] = A [M, K] B [K, Nc] on
+// `stream`), and a rocBLAS handle (nullptr on failure).
+hipError_t launch_layer_copy(Launcher& L, bool split, int dtype, const void* src, void* d0,
+                             void* d1, void* d2, int B, int N, int H, int d, hipStream_t s);
+hipError_t layer_gemm(void* handle, void* stream, int dtype, const void* A, const void* Bm,
+                      void* C, int M, int K, int Nc);
+void* layer_blas_handle_create();
+
 // The C ABI's host logic (fmm_api.cpp), shared with the no-allocation entry
 // point (fmm_noalloc.hip): argument checks, the workspace size of the call's
 // segment plan, and the checked launch with a given workspace.

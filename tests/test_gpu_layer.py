@@ -1,0 +1,68 @@
+"""Parity of the attention layer (fmm_attn_layer_forward: QKV projection, the
+operator per head, output projection) with the float64 oracle layer, at the
+long-range-classification model shape (2 heads, 64-dim embedding) and a wider
+one.  The GPU keeps q, k, v and the heads' outputs in the storage type between
+the steps; the oracle works on the rounded inputs and weights in float64
+throughout, so the bf16 bound also covers those intermediate roundings."""
+
+import numpy as np
+import pytest
+import torch
+
+from fmm_testlib import TOL, log
+from oracle import fmm_ref as ref
+from paper_2108_02347_amd import binding
+from paper_2108_02347_amd.inputs import to_dtype
+
+pytestmark = pytest.mark.gpu
+
+TD = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def check_layer(B, N, E, H, kw, rank, causal, dtype, seed):
+    rng = np.random.default_rng(seed)
+    x = to_dtype(rng.standard_normal((B, N, E)), dtype)
+    wqkv = to_dtype(rng.standard_normal((E, 3 * E)) / np.sqrt(E), dtype)
+    wo = to_dtype(rng.standard_normal((E, E)) / np.sqrt(E), dtype)
+    wn, wf = rng.standard_normal(H), rng.standard_normal(H)
+    log(f"layer B={B} N={N} E={E} H={H} k={kw} r={rank} causal={causal} {dtype}")
+    dev = "cuda:0"
+    tx, tw, to = (torch.from_numpy(np.asarray(a, dtype=np.float32)).to(dev).to(TD[dtype])
+                  .contiguous() for a in (x, wqkv, wo))
+    twn, twf = (torch.from_numpy(np.asarray(a, dtype=np.float32)).to(dev) for a in (wn, wf))
+    got = binding.layer_forward(tx, tw, to, H, twn, twf, kw, rank, causal)
+    torch.cuda.synchronize()
+    got = got.float().cpu().numpy().astype(np.float64)
+    want = ref.fmm_layer_forward(x, wqkv, wo, H, wn, wf, kw, rank, bool(causal))
+    assert np.isfinite(got).all()
+    err = (np.abs(got - want).max(axis=(1, 2)) / np.abs(want).max(axis=(1, 2))).max()
+    log(f"  worst batch-element error {err:.3e}")
+    assert err <= TOL[dtype]
+    return err
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("causal", [0, 1])
+def test_layer_lra_shape(causal, dtype):
+    check_layer(4, 1024, 64, 2, 20, 2, causal, dtype, 3000 + causal)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_layer_wider(dtype):
+    check_layer(2, 777, 256, 4, 33, 2, 0, dtype, 3010)
+    check_layer(1, 300, 256, 2, 9, 3, 1, dtype, 3011)
+
+
+def test_layer_argument_checks():
+    x = torch.zeros(1, 8, 64, device="cuda:0")
+    w = torch.zeros(64, 192, device="cuda:0")
+    wo = torch.zeros(64, 64, device="cuda:0")
+    h = torch.zeros(2, device="cuda:0")
+    with pytest.raises(ValueError):
+        binding.layer_forward(x, w[:, :128].contiguous(), wo, 2, h, h, 3, 2, 0)
+    with pytest.raises(ValueError):
+        binding.layer_forward(x.bfloat16(), w, wo, 2, h, h, 3, 2, 0)
+    with pytest.raises(binding.FmmError) as ei:   # E not divisible into heads of width 16..128
+        binding.layer_forward(x, w, wo, 3, torch.zeros(3, device="cuda:0"),
+                              torch.zeros(3, device="cuda:0"), 3, 2, 0)
+    assert ei.value.status in (binding.FMM_ERR_INVALID_ARG, binding.FMM_ERR_UNSUPPORTED)
