@@ -71,6 +71,11 @@ bool overlaps(const void* a, const void* b, size_t n) {
   const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
   return x < y + n && y < x + n;
 }
+// [a, a + na) and [b, b + nb) share a byte
+bool overlaps2(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
+}
 
 int validate(const void* q, const void* k, const void* v, void* out, int B, int H, int N,
              int d, int band_k, int rank, int causal, const float* w_near, const float* w_far,
@@ -421,8 +426,7 @@ int run_layer(const void* x, const void* w_qkv, const void* w_out, void* y, int 
     if ((uintptr_t)p % 16) return FMM_ERR_INVALID_ARG;
   if ((uintptr_t)w_near % 4 || (uintptr_t)w_far % 4) return FMM_ERR_INVALID_ARG;
   const size_t xb = (size_t)xbytes, wq = (size_t)E * 3 * E * es, wo = (size_t)E * E * es;
-  if (overlaps(y, x, xb) || overlaps(y, w_qkv, std::max(xb, wq)) ||
-      overlaps(y, w_out, std::max(xb, wo)))
+  if (overlaps2(y, xb, x, xb) || overlaps2(y, xb, w_qkv, wq) || overlaps2(y, xb, w_out, wo))
     return FMM_ERR_INVALID_ARG;
   // workspace: qkv, q, k, v, o, merged heads, then the operator's records
   const Plan p = plan_for(B, H, N, d, band_k, rank, causal, dtype);
