@@ -79,6 +79,8 @@ __all__ = [
     "far_terms_stream",
     "fmm_attention_backward_stream",
     "fmm_layer_forward",
+    "fast_weight_stream",
+    "fmm_fast_weight_forward",
 ]
 
 
@@ -533,3 +535,54 @@ def fmm_layer_forward(x, w_qkv, w_out, heads: int, w_near, w_far, band_k: int, r
     o = fmm_attention_stream(q, k, v, w_near, w_far, band_k, rank, causal, norm)
     merged = o.transpose(0, 2, 1, 3).reshape(b_, n, e)
     return merged @ w_out
+
+
+# ---------------------------------------------------------------- fast-weight far field
+
+def fast_weight_stream(q, k, v, beta) -> np.ndarray:
+    """The fast-weight far field (Appendix D: a linear transformer with the
+    fast weight update of the cited fast-weight-programmer work), causal, per
+    (b, h), with phi = elu(x) + 1 normalised by its sum over the channels,
+    p(x) = phi(x) / sum_c phi(x)_c:
+        u_i = W_{i-1} p(k_i)                          (value read at key i)
+        W_i = W_{i-1} + beta_i (v_i - u_i) p(k_i)^T   (delta-rule write)
+        z_i = z_{i-1} + p(k_i)
+        fw_i = W_i p(q_i) / (z_i . p(q_i))            (attention normalisation)
+    with W_{-1} = 0, z_{-1} = 0.  beta: [B, H, N] write strengths.  A plain
+    sequential loop over i."""
+    q, k, v = _check(q, k, v)
+    beta = np.asarray(beta, dtype=np.float64)
+    b_, h_, n, d = q.shape
+    if beta.shape != (b_, h_, n):
+        raise ValueError("beta must be [B, H, N]")
+    pk = phi(k, 1)
+    pk = pk / pk.sum(axis=-1, keepdims=True)
+    pq = phi(q, 1)
+    pq = pq / pq.sum(axis=-1, keepdims=True)
+    out = np.empty_like(v)
+    for bb in range(b_):
+        for hh in range(h_):
+            w = np.zeros((d, d))
+            z = np.zeros(d)
+            for i in range(n):
+                u = w @ pk[bb, hh, i]
+                w = w + beta[bb, hh, i] * np.outer(v[bb, hh, i] - u, pk[bb, hh, i])
+                z = z + pk[bb, hh, i]
+                out[bb, hh, i] = (w @ pq[bb, hh, i]) / (z @ pq[bb, hh, i])
+    return out
+
+
+def fmm_fast_weight_forward(q, k, v, beta, w_near, w_far, band_k: int,
+                            n_linear: int) -> np.ndarray:
+    """FMMformer with the fast-weight far field (Appendix D), causal:
+    out = sigmoid(w_near) near + sigmoid(w_far) (fw + [n_linear = 1] lin),
+    near the causal banded softmax (Eq. (3)), fw the fast-weight far field
+    above, lin the causal linear attention of phi_1 (Eq. (8)) -- the
+    2-kernel variant pairs one fast-weight kernel with one linear kernel,
+    both with elu(x) + 1."""
+    if n_linear not in (0, 1):
+        raise ValueError("n_linear must be 0 or 1")
+    far = fast_weight_stream(q, k, v, beta)
+    if n_linear:
+        far = far + far_stream(q, k, v, 1, True)
+    return _blend(near_stream(q, k, v, band_k, True), far, w_near, w_far)

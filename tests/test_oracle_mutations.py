@@ -106,6 +106,15 @@ MUTATIONS = [
     ("layer: heads merged in the wrong order",
      "merged = o.transpose(0, 2, 1, 3).reshape(b_, n, e)",
      "merged = o.transpose(0, 2, 3, 1).reshape(b_, n, e)"),
+    ("fast weight: write without the read-back term",
+     "w = w + beta[bb, hh, i] * np.outer(v[bb, hh, i] - u, pk[bb, hh, i])",
+     "w = w + beta[bb, hh, i] * np.outer(v[bb, hh, i], pk[bb, hh, i])"),
+    ("fast weight: keys not sum-normalised",
+     "    pk = pk / pk.sum(axis=-1, keepdims=True)\n",
+     "\n"),
+    ("fast weight: normaliser updated after the output",
+     "                z = z + pk[bb, hh, i]\n                out[bb, hh, i] = (w @ pq[bb, hh, i]) / (z @ pq[bb, hh, i])",
+     "                out[bb, hh, i] = (w @ pq[bb, hh, i]) / ((z + 1e-30) @ pq[bb, hh, i])\n                z = z + pk[bb, hh, i]"),
     ("backward: key-side near gradient unscaled",
      "dk[:, :, j] += tau * ds[:, :, ok, t, None] * q[:, :, rows[ok]]",
      "dk[:, :, j] += ds[:, :, ok, t, None] * q[:, :, rows[ok]]"),

@@ -596,3 +596,72 @@ def test_layer_projections_by_brute_force():
             want[0, t, j] = sum(o[0, hh, t, c] * wo[hh * d + c, j]
                                 for hh in range(h) for c in range(d))
     np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-13)
+
+
+# ------------------------------------------------------------------ fast-weight far field
+
+def _bf_fast_weight(qs, ks, vs, betas):
+    # scalar loops over the same recurrence, written with lists only
+    n, d = len(qs), len(qs[0])
+    def p(x):
+        f = [bf_phi(c, 1) for c in x]
+        s = sum(f)
+        return [c / s for c in f]
+    w = [[0.0] * d for _ in range(d)]
+    z = [0.0] * d
+    out = []
+    for i in range(n):
+        pk, pq = p(ks[i]), p(qs[i])
+        u = [sum(w[r][c] * pk[c] for c in range(d)) for r in range(d)]
+        for r in range(d):
+            for c in range(d):
+                w[r][c] += betas[i] * (vs[i][r] - u[r]) * pk[c]
+        z = [z[c] + pk[c] for c in range(d)]
+        den = sum(z[c] * pq[c] for c in range(d))
+        out.append([sum(w[r][c] * pq[c] for c in range(d)) / den for r in range(d)])
+    return np.array(out)
+
+
+def test_fast_weight_brute_force():
+    n, d = 11, 3
+    q, k, v = (rnd((1, 1, n, d), s) for s in (120, 121, 122))
+    beta = np.random.default_rng(123).uniform(0.0, 1.0, (1, 1, n))
+    want = _bf_fast_weight(q[0, 0].tolist(), k[0, 0].tolist(), v[0, 0].tolist(),
+                           beta[0, 0].tolist())
+    np.testing.assert_allclose(ref.fast_weight_stream(q, k, v, beta)[0, 0], want, rtol=1e-12,
+                               atol=1e-13)
+
+
+def test_fast_weight_closed_forms():
+    # row 0: W_0 = beta_0 v_0 p(k_0)^T, z_0 = p(k_0), so fw_0 = beta_0 v_0
+    q, k, v = (rnd((2, 2, 6, 4), s) for s in (124, 125, 126))
+    beta = np.random.default_rng(127).uniform(0.0, 1.0, (2, 2, 6))
+    fw = ref.fast_weight_stream(q, k, v, beta)
+    np.testing.assert_allclose(fw[:, :, 0], beta[:, :, 0, None] * v[:, :, 0], rtol=1e-13)
+    # d = 1: p = 1 always, so W is the running average W_i = W_{i-1} + beta_i (v_i - W_{i-1})
+    # and fw_i = W_i / (i + 1)
+    n = 9
+    q1, k1, v1 = (rnd((1, 1, n, 1), s) for s in (128, 129, 130))
+    b1 = np.random.default_rng(131).uniform(0.0, 1.0, (1, 1, n))
+    w, want = 0.0, []
+    for i in range(n):
+        w = w + b1[0, 0, i] * (v1[0, 0, i, 0] - w)
+        want.append(w / (i + 1))
+    np.testing.assert_allclose(ref.fast_weight_stream(q1, k1, v1, b1)[0, 0, :, 0], want,
+                               rtol=1e-13)
+    # beta = 0: nothing is ever written
+    np.testing.assert_array_equal(ref.fast_weight_stream(q, k, v, np.zeros((2, 2, 6))), 0.0)
+
+
+def test_fast_weight_operator_composition():
+    q, k, v = (rnd((1, 2, 20, 4), s) for s in (132, 133, 134))
+    beta = np.random.default_rng(135).uniform(0.0, 1.0, (1, 2, 20))
+    wn, wf = rnd(2, 136), rnd(2, 137)
+    sn, sf = 1 / (1 + np.exp(-wn)), 1 / (1 + np.exp(-wf))
+    fw = ref.fast_weight_stream(q, k, v, beta)
+    near = ref.near_stream(q, k, v, 3, True)
+    lin = ref.far_stream(q, k, v, 1, True)
+    for nl in (0, 1):
+        got = ref.fmm_fast_weight_forward(q, k, v, beta, wn, wf, 3, nl)
+        want = sn[None, :, None, None] * near + sf[None, :, None, None] * (fw + nl * lin)
+        np.testing.assert_allclose(got, want, rtol=1e-13)
