@@ -95,7 +95,8 @@ extern "C" {
 #define FMM_KERNEL_BWD_KEYS      5 /* backward key pass: dk, dv                 */
 #define FMM_KERNEL_BWD_DW        6 /* backward blend-logit reduction            */
 #define FMM_KERNEL_LAYER_COPY    7 /* attention layer: head split and merge     */
-#define FMM_KERNEL_COUNT         8
+#define FMM_KERNEL_FAST_WEIGHT   8 /* fast-weight far field scan               */
+#define FMM_KERNEL_COUNT         9
 
 /*
  * fmm_attn_forward - the operator of Eq. (9) blended as in Eq. (11), fp32.
@@ -240,6 +241,29 @@ int fmm_attn_backward(const void* q, const void* k, const void* v, const void* d
 int fmm_attn_layer_forward(const void* x, const void* w_qkv, const void* w_out, void* y,
                            int B, int N, int E, int H, int band_k, int rank, int causal,
                            const float* w_near, const float* w_far, int dtype, void* stream);
+
+/*
+ * fmm_attn_forward_fastweight - FMMformer with the fast-weight far field of
+ * Appendix D (causal only): the linear transformer with the delta-rule fast
+ * weight update of the work the appendix cites.  Per (b, h) and row i, with
+ * p(x) = phi_1(x) / sum_c phi_1(x)_c:
+ *   u_i = W_{i-1} p(k_i),  W_i = W_{i-1} + beta_i (v_i - u_i) p(k_i)^T,
+ *   z_i = z_{i-1} + p(k_i),  fw_i = W_i p(q_i) / (z_i . p(q_i))   (W, z start at 0)
+ *   out_i = sigmoid(w_near[h]) near_i + sigmoid(w_far[h]) (fw_i + n_linear lin_i)
+ * near_i is the causal banded softmax (Eq. (3)), lin_i the causal linear
+ * attention of phi_1 (Eq. (8)); n_linear = 1 gives the two-kernel variant
+ * (one fast-weight and one linear kernel, both with elu + 1).
+ *   beta    : device float[B, H, N], the write strengths (the model's
+ *             sigmoid of a projection; used as given).
+ *   n_linear: 0 or 1.
+ * Other arguments as fmm_attn_forward_ex (dtype FMM_DTYPE_F32 or _BF16).  The
+ * recurrence is sequential in i: its cost grows with N at one step latency
+ * per row, not with bandwidth.  Uses the library-owned workspace.
+ */
+int fmm_attn_forward_fastweight(const void* q, const void* k, const void* v,
+                                const float* beta, void* out, int B, int H, int N, int d,
+                                int band_k, int n_linear, const float* w_near,
+                                const float* w_far, int dtype, void* stream);
 
 /* Human-readable text for a status code; never NULL, static storage. */
 const char* fmm_attn_status_string(int status);

@@ -28,14 +28,14 @@ FMM_FAR_NORM_PER_MAP = 0
 FMM_FAR_NORM_JOINT = 1
 
 KERNELS = {"seg_state": 0, "state_combine": 1, "band_apply": 2, "causal_apply": 3,
-           "bwd_rows": 4, "bwd_keys": 5, "bwd_dw": 6, "layer_copy": 7}
+           "bwd_rows": 4, "bwd_keys": 5, "bwd_dw": 6, "layer_copy": 7, "fast_weight": 8}
 
 EXPORTS = (
     "fmm_attn_forward", "fmm_attn_forward_bf16", "fmm_attn_workspace_bytes",
     "fmm_attn_forward_ws", "fmm_attn_status_string", "fmm_attn_release_workspace",
     "fmm_attn_version", "fmm_attn_kernel_timing", "fmm_attn_kernel_timing_read",
     "fmm_attn_forward_noalloc", "fmm_attn_noalloc_max_bytes", "fmm_attn_forward_ex",
-    "fmm_attn_backward", "fmm_attn_layer_forward",
+    "fmm_attn_backward", "fmm_attn_layer_forward", "fmm_attn_forward_fastweight",
 )
 
 _lib = None
@@ -65,6 +65,8 @@ def lib() -> ctypes.CDLL:
         fn.restype = ci
     h.fmm_attn_forward_ws.argtypes = fwd_args[:-1] + [ci, vp, ctypes.c_size_t, vp]
     h.fmm_attn_forward_ws.restype = ci
+    h.fmm_attn_forward_fastweight.argtypes = [vp] * 5 + [ci] * 6 + [cf, cf, ci, vp]
+    h.fmm_attn_forward_fastweight.restype = ci
     h.fmm_attn_layer_forward.argtypes = [vp] * 4 + [ci] * 7 + [cf, cf, ci, vp]
     h.fmm_attn_layer_forward.restype = ci
     h.fmm_attn_backward.argtypes = [vp] * 9 + [ci] * 7 + [cf, cf, ci, vp]
@@ -265,6 +267,24 @@ def layer_forward(x, w_qkv, w_out, heads: int, w_near, w_far, band_k: int, rank:
     _check(lib().fmm_attn_layer_forward(
         _ptr(x), _ptr(w_qkv), _ptr(w_out), _ptr(out), B, N, E, int(heads), int(band_k),
         int(rank), int(bool(causal)), _ptr(w_near), _ptr(w_far), dt, _stream_of(x)))
+    return out
+
+
+def forward_fastweight(q, k, v, beta, w_near, w_far, band_k: int, n_linear: int, out=None):
+    """FMMformer with the fast-weight far field (causal); beta: [B, H, N]
+    float32 write strengths."""
+    B, H, N, d = _prep(q, k, v, w_near, w_far)
+    if (beta.dtype != torch.float32 or beta.device != q.device
+            or tuple(beta.shape) != (B, H, N) or not beta.is_contiguous()):
+        raise ValueError("beta must be a contiguous float32 [B, H, N] tensor on q's device")
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _check_out(out, q)
+    dt = FMM_DTYPE_BF16 if q.dtype == torch.bfloat16 else FMM_DTYPE_F32
+    _check(lib().fmm_attn_forward_fastweight(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(out), B, H, N, d, int(band_k),
+        int(n_linear), _ptr(w_near), _ptr(w_far), dt, _stream_of(q)))
     return out
 
 

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libfmm_attn.so")
 SOURCES = ["fmm_kernels.hip", "fmm_wide.hip", "fmm_bwd.hip", "fmm_pair.hip", "fmm_causal.hip",
-           "fmm_noalloc.hip", "fmm_layer.hip", "fmm_api.cpp"]
+           "fmm_noalloc.hip", "fmm_layer.hip", "fmm_fastweight.hip", "fmm_api.cpp"]
 HEADERS = ["fmm_device.h", "fmm_launch.h", "fmm_oct.h", "fmm_apply.h"]
 
 

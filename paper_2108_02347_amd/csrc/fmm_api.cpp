@@ -3,6 +3,7 @@
 // kernel timer.  Every kernel is launched asynchronously on the caller's stream.
 #include <hip/hip_runtime.h>
 
+#include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 
@@ -486,6 +487,62 @@ int run_layer(const void* x, const void* w_qkv, const void* w_out, void* y, int 
   return FMM_OK;
 }
 
+// ------------------------------------------------------------------ fast weight
+int run_fastweight(const void* q, const void* k, const void* v, const float* beta, void* out,
+                   int B, int H, int N, int d, int band_k, int n_linear, const float* w_near,
+                   const float* w_far, int dtype, void* stream) {
+  int st = validate(q, k, v, out, B, H, N, d, band_k, 1, 1, w_near, w_far, dtype,
+                    FMM_FAR_NORM_PER_MAP);
+  if (st != FMM_OK) return st;
+  if (!beta || (uintptr_t)beta % 4 || (n_linear != 0 && n_linear != 1))
+    return FMM_ERR_INVALID_ARG;
+  const Plan p = plan_for(B, H, N, d, band_k, 1, 1, dtype);
+  if (p.ws_bytes == 0) return FMM_ERR_UNSUPPORTED;
+  // the operator's records, then H floats of -inf that remove its linear
+  // far part when n_linear = 0
+  const size_t total = p.ws_bytes + align256((size_t)H * 4);
+  fmm::LaunchArgs a = make_args(q, k, v, out, B, H, N, d, band_k, 1, 1, w_near, w_far, dtype,
+                                FMM_FAR_NORM_PER_MAP, nullptr, p, stream);
+  fmm::FwArgs f;
+  f.q = q;
+  f.k = k;
+  f.v = v;
+  f.beta = beta;
+  f.out = out;
+  f.w_far = w_far;
+  f.B = B;
+  f.H = H;
+  f.N = N;
+  f.d = d;
+  f.dtype = dtype;
+  f.stream = stream;
+  EventTimer& t = timer();
+  {
+    std::lock_guard<std::mutex> g(t.mu);
+    fmm::Launcher dry;
+    dry.timer = &t;
+    dry.dry = true;
+    if (fmm::launch_forward(a, dry) != hipSuccess || fmm::launch_fast_weight(dry, f) != hipSuccess)
+      return dry.err == hipErrorInvalidConfiguration ? FMM_ERR_UNSUPPORTED : FMM_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> wl(ws_mutex());
+  void* ws = nullptr;
+  st = acquire_ws_locked(stream, total, &ws);
+  if (st != FMM_OK) return st;
+  a.ws = (float*)ws;
+  float* minus_inf =
+      reinterpret_cast<float*>(reinterpret_cast<uintptr_t>(ws) + p.ws_bytes);
+  std::lock_guard<std::mutex> g(t.mu);
+  fmm::Launcher L;
+  L.timer = &t;
+  if (!n_linear) {
+    if (fmm::launch_fill(L, minus_inf, H, -INFINITY, stream) != hipSuccess) return FMM_ERR_HIP;
+    a.w_far = minus_inf;
+  }
+  if (fmm::launch_forward(a, L) != hipSuccess) return FMM_ERR_HIP;
+  return fmm::launch_fast_weight(L, f) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
+}
+
 }  // namespace
 
 namespace fmm {
@@ -548,6 +605,14 @@ int fmm_attn_layer_forward(const void* x, const void* w_qkv, const void* w_out, 
                            const float* w_near, const float* w_far, int dtype, void* stream) {
   return run_layer(x, w_qkv, w_out, y, B, N, E, H, band_k, rank, causal, w_near, w_far, dtype,
                    stream);
+}
+
+int fmm_attn_forward_fastweight(const void* q, const void* k, const void* v, const float* beta,
+                                void* out, int B, int H, int N, int d, int band_k, int n_linear,
+                                const float* w_near, const float* w_far, int dtype,
+                                void* stream) {
+  return run_fastweight(q, k, v, beta, out, B, H, N, d, band_k, n_linear, w_near, w_far, dtype,
+                        stream);
 }
 
 size_t fmm_attn_workspace_bytes(int B, int H, int N, int d, int rank, int causal) {

@@ -169,6 +169,21 @@ hipError_t layer_gemm(void* handle, void* stream, int dtype, const void* A, cons
                       void* C, int M, int K, int Nc);
 void* layer_blas_handle_create();
 
+// Fast-weight far field (fmm_fastweight.hip): adds sigmoid(w_far) fw to out.
+struct FwArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const float* beta;
+  void* out;
+  const float* w_far;
+  int B, H, N, d, dtype;
+  void* stream;
+};
+hipError_t launch_fast_weight(Launcher& L, const FwArgs& a);
+// n floats at p set to x (on `stream`)
+hipError_t launch_fill(Launcher& L, float* p, int n, float x, void* stream);
+
 // The C ABI's host logic (fmm_api.cpp), shared with the no-allocation entry
 // point (fmm_noalloc.hip): argument checks, the workspace size of the call's
 // segment plan, and the checked launch with a given workspace.
