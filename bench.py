@@ -696,6 +696,28 @@ def main():
                  "operator_ms_per_call": round(t4 * 1e3, 4)}
     del xl, wl, wo, yl
 
+    # the fast-weight far field (Appendix D) at the language-model shape,
+    # causal, two kernels (fast weight + linear), fp32
+    wl4 = WORKLOADS["lm256"]
+    _, (qf, kf, vf, wnf, wff) = make_device_inputs("lm256", "f32", torch)
+    bf = torch.rand((wl4.B, wl4.H, wl4.N), generator=torch.Generator(device="cuda:0")
+                    .manual_seed(17), device="cuda:0")
+    of = torch.empty_like(qf)
+    tfw = timed(lambda: binding.forward_fastweight(qf, kf, vf, bf, wnf, wff, wl4.band_k, 1,
+                                                   out=of), args.steps, args.warmup, torch)
+    for name in binding.KERNELS:
+        binding.kernel_timing_read(name)
+    binding.kernel_timing(True)
+    timed(lambda: binding.forward_fastweight(qf, kf, vf, bf, wnf, wff, wl4.band_k, 1, out=of),
+          args.steps, 0, torch)
+    binding.kernel_timing(False)
+    ms_fw, n_fw = binding.kernel_timing_read("fast_weight")
+    fw_rec = {"shape": "B=16 H=8 N=256 d=16 f32 k=20, fast weight + linear far field, causal",
+              "ms_per_call": round(tfw * 1e3, 4),
+              "tokens_per_s": round(wl4.B * wl4.N / tfw, 1),
+              "scan_kernel_us": round(ms_fw * 1e3 / n_fw, 3) if n_fw else None}
+    del qf, kf, vf, of, bf
+
     # the other workloads: whole-call throughput, no per-kernel figures
     others = {}
     for name, dtype in (("tiny", "f32"), ("lra1k", "f32"), ("lra1k", "bf16"), ("lm256", "f32")):
@@ -773,6 +795,7 @@ def main():
         "other_workloads": others,
         "forward_backward": fb_rec,
         "attention_layer": layer_rec,
+        "fast_weight": fw_rec,
         "general_path": ext,
         "hbm_achievable": hbm_ceiling(torch),
         "kernel_source_hash": kernel_source_hash(),
