@@ -68,6 +68,9 @@ struct BwdCfg {
 
 __device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"); }
 
+constexpr int SWB = 8;          // waves of k_seg_grad
+constexpr int SNTB = SWB * 64;
+
 // Rows [r0, r0 + n) of two [N, D] tensors (rows at or beyond kend read as
 // zero) into row-major LDS buffers of stride ST.
 template <typename T, int D>
@@ -247,7 +250,7 @@ template <typename T, int D, bool CAUSAL>
 __global__ __launch_bounds__(NT) void k_bwd_rows(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, T* __restrict__ dq, float* __restrict__ recs,
-    float* __restrict__ dpart, float* __restrict__ rowstat, float* __restrict__ rowfar,
+    float* __restrict__ rowstat, float* __restrict__ rowfar,
     float* __restrict__ dwpart, const float* __restrict__ w_near, const float* __restrict__ w_far,
     int H, int N, int band_k, int L, int nseg, int rank, float scale2) {
   using Q = typename QuadOf<T>::type;
@@ -267,11 +270,9 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
   const size_t base = (size_t)bh * N * D;
   const size_t REC = (size_t)rank * D * (D + 1);
   float* rec = CAUSAL ? recs + ((size_t)bh * nseg + seg) * REC : recs + (size_t)bh * REC;
-  float* drec = dpart + ((size_t)bh * nseg + seg) * REC;
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const float tau = scale2 * 0.69314718055994531f;  // 1/sqrt(d)
   const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
-  for (size_t t = threadIdx.x; t < REC; t += NT) drec[t] = 0.f;
   float acc_near = 0.f, acc_far = 0.f;  // this lane's share of g . near and g . far
   const int s0 = seg * L, s1 = min(N, s0 + L);
   for (int t0 = s0; t0 < s1; t0 += TM) {
@@ -350,7 +351,6 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
         pq[cb] = f32_to_quad<T>(p);
       }
       float* rl = rec + (size_t)l * D * (D + 1);
-      float* drl = drec + (size_t)l * D * (D + 1);
       const T* vt = sv + (t0 - ks) * ST;
       f32x4 num[NB + 1];
 #pragma unroll
@@ -490,18 +490,6 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
           record_add<T, D>(rl, tb1, vt, ones_col, ST, w);
         }
       }
-      // the segment's dS partial: rows' phi_l(q) into tb1, dnum into tb2,
-      // dden into dden_s
-      __syncthreads();
-#pragma unroll
-      for (int cb = 0; cb < NB; ++cb) {
-        *reinterpret_cast<Q*>(tb1 + (16 * w + r) * ST + 16 * cb + 4 * g) = pq[cb];
-        *reinterpret_cast<Q*>(tb2 + (16 * w + r) * ST + 16 * cb + 4 * g) =
-            row_ok ? dnq[cb] : to_quad<T>(zero);
-      }
-      if (g == 0) dden_s[16 * w + r] = row_ok ? dden : 0.f;
-      __syncthreads();
-      record_add<T, D>(drl, tb1, tb2, dden_s, ST, w);
     }
     store_row<T, D>(dq + base, row, N, dqa);
   }
@@ -531,6 +519,156 @@ __global__ __launch_bounds__(256) void k_suffix_scan(float* __restrict__ part, i
     const float t = p[(size_t)s * rec];
     p[(size_t)s * rec] = run;
     run += t;
+  }
+}
+
+// ------------------------------------------------------------------ dS partials
+// Per state segment, the far-field gradient state of map l:
+//   dS_l = sum_i phi_l(q_i) dnum_i^T,  dz_l = sum_i phi_l(q_i) dden_i,
+//   dnum_i = c g_i / den_l,i  (c = sigmoid(w_far[h]))
+// from q, dout and the row pass's (1/den, dden), in the record's tile order.
+// Same structure as k_seg_state: 8 waves, (rs, cb) = wave split of the
+// 32-row units and feature block, 64-row chunks staged in LDS, a fixed-order
+// tree over the waves sharing a feature block.
+template <typename T, int D, int R>
+__global__ __launch_bounds__(SNTB) void k_seg_grad(const T* __restrict__ q,
+                                                   const T* __restrict__ dout,
+                                                   const float* __restrict__ rowfar,
+                                                   const float* __restrict__ w_far,
+                                                   float* __restrict__ dpart, int H, int N, int L,
+                                                   int nseg) {
+  using Q = typename QuadOf<T>::type;
+  constexpr int NB = D / 16;
+  constexpr int ST = D + Lay<T>::PAD;
+  constexpr int RS = SWB / NB > 0 ? SWB / NB : 1;
+  constexpr int TK = 64;
+  // the two 64-row staging buffers, reused for the reduction tree at the end
+  constexpr int STAGE = 2 * TK * ST * (int)sizeof(T);
+  constexpr int REDB = SWB / 2 * (NB + 1) * 64 * 16;
+  __shared__ __attribute__((aligned(16))) unsigned char s_buf[STAGE > REDB ? STAGE : REDB];
+  __shared__ float s_sc[R][TK], s_dd[R][TK];
+  T* s_q = reinterpret_cast<T*>(s_buf);
+  T* s_g = s_q + TK * ST;
+  const int seg = blockIdx.x % nseg, bh = blockIdx.x / nseg, h = bh % H;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const int cbw = w % NB, rs = w / NB;
+  const bool owner = w < NB * RS;
+  const int r0 = seg * L, r1 = min(N, r0 + L);
+  const size_t base = (size_t)bh * N * D;
+  const float sfw = sigmoidf_exact(w_far[h]);
+  f32x4 acc[R][NB + 1];
+#pragma unroll
+  for (int l = 0; l < R; ++l)
+#pragma unroll
+    for (int eb = 0; eb <= NB; ++eb) acc[l][eb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto ident = [](int i) { return i; };
+  for (int c0 = r0; c0 < r1; c0 += TK) {
+    const int nrow = min(TK, r1 - c0);
+    RowCopy<T, D, SNTB, TK> cq, cg;
+    cq.load(q + base, c0, nrow, r1);
+    cg.load(dout + base, c0, nrow, r1);
+    __syncthreads();  // the previous chunk is consumed
+    cq.store(s_q, ST, TK, ident);
+    cg.store(s_g, ST, TK, ident);
+    for (int t = threadIdx.x; t < R * TK; t += SNTB) {
+      const int l = t / TK, i = t % TK;
+      const bool ok = c0 + i < r1;
+      const float* fp = rowfar + (((size_t)bh * N + (ok ? c0 + i : 0)) * R + l) * 2;
+      s_sc[l][i] = ok ? sfw * fp[0] : 0.f;
+      s_dd[l][i] = ok ? fp[1] : 0.f;
+    }
+    __syncthreads();
+    if (owner) {
+#pragma unroll
+      for (int u = 0; u < TK / 32; ++u) {
+        if ((u % RS) != rs) continue;
+        float qf[2][4];
+#pragma unroll
+        for (int b = 0; b < 2; ++b) quad_to_f32(ld_tquad(s_q, 32 * u + 16 * b, 16 * cbw, ST), qf[b]);
+#pragma unroll
+        for (int l = 0; l < R; ++l) {
+          float pa[2][4];
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int row = 32 * u + 16 * b + 4 * g + i;
+              pa[b][i] = c0 + row < r1 ? phi_any(qf[b][i], l) : 0.f;
+            }
+          const Q a0 = f32_to_quad<T>(pa[0]), a1 = f32_to_quad<T>(pa[1]);
+#pragma unroll
+          for (int eb = 0; eb < NB; ++eb) {
+            float gb[2][4];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+              quad_to_f32(ld_tquad(s_g, 32 * u + 16 * b, 16 * eb, ST), gb[b]);
+#pragma unroll
+              for (int i = 0; i < 4; ++i) gb[b][i] *= s_sc[l][32 * u + 16 * b + 4 * g + i];
+            }
+            acc[l][eb] = mma_step2(a0, a1, f32_to_quad<T>(gb[0]), f32_to_quad<T>(gb[1]),
+                                   acc[l][eb]);
+          }
+          float zb[2][4];
+#pragma unroll
+          for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              zb[b][i] = r == 0 ? s_dd[l][32 * u + 16 * b + 4 * g + i] : 0.f;
+          acc[l][NB] = mma_step2(a0, a1, f32_to_quad<T>(zb[0]), f32_to_quad<T>(zb[1]),
+                                 acc[l][NB]);
+        }
+      }
+    }
+  }
+  mfma_drain();
+  // fixed-order tree over the RS waves of a feature block, through s_q
+  f32x4* red = reinterpret_cast<f32x4*>(s_buf);
+#pragma unroll
+  for (int l = 0; l < R; ++l) {
+#pragma unroll
+    for (int st = RS / 2; st >= 1; st >>= 1) {
+      __syncthreads();
+      if (owner && rs >= st && rs < 2 * st)
+#pragma unroll
+        for (int eb = 0; eb <= NB; ++eb)
+          red[(((rs - st) * NB + cbw) * (NB + 1) + eb) * 64 + lane] = acc[l][eb];
+      __syncthreads();
+      if (owner && rs < st)
+#pragma unroll
+        for (int eb = 0; eb <= NB; ++eb)
+          acc[l][eb] += red[((rs * NB + cbw) * (NB + 1) + eb) * 64 + lane];
+    }
+  }
+  if (!owner || rs != 0) return;
+  float* outp = dpart + ((size_t)bh * nseg + seg) * (R * D * (D + 1));
+#pragma unroll
+  for (int l = 0; l < R; ++l) {
+    float* sl = outp + (size_t)l * D * (D + 1);
+#pragma unroll
+    for (int eb = 0; eb < NB; ++eb)
+      *reinterpret_cast<f32x4*>(sl + ((cbw * NB + eb) * 64 + lane) * 4) = acc[l][eb];
+    if (r == 0) *reinterpret_cast<f32x4*>(sl + D * D + 16 * cbw + 4 * g) = acc[l][NB];
+  }
+}
+
+template <typename T, int D>
+void launch_seg_grad(const BwdArgs& a, Launcher& L) {
+  const dim3 grid(a.B * a.H * a.nseg);
+  hipStream_t s = (hipStream_t)a.stream;
+  switch (a.rank) {
+    case 1:
+      L(FMM_KERNEL_BWD_ROWS, k_seg_grad<T, D, 1>, grid, dim3(SNTB), 0, s, (const T*)a.q,
+        (const T*)a.dout, (const float*)a.rowfar, a.w_far, a.dpart, a.H, a.N, a.L, a.nseg);
+      break;
+    case 2:
+      L(FMM_KERNEL_BWD_ROWS, k_seg_grad<T, D, 2>, grid, dim3(SNTB), 0, s, (const T*)a.q,
+        (const T*)a.dout, (const float*)a.rowfar, a.w_far, a.dpart, a.H, a.N, a.L, a.nseg);
+      break;
+    default:
+      L(FMM_KERNEL_BWD_ROWS, k_seg_grad<T, D, 3>, grid, dim3(SNTB), 0, s, (const T*)a.q,
+        (const T*)a.dout, (const float*)a.rowfar, a.w_far, a.dpart, a.H, a.N, a.L, a.nseg);
+      break;
   }
 }
 
@@ -814,8 +952,9 @@ hipError_t launch_bwd_dc(const BwdArgs& a, Launcher& L) {
   const dim3 grid(BH * a.nseg);
   L(FMM_KERNEL_BWD_ROWS, k_bwd_rows<T, D, CAUSAL>, grid, dim3(NT), (size_t)C::LDS, s,
     (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, (T*)a.dq,
-    CAUSAL ? a.part : a.fin, a.dpart, a.rowstat, a.rowfar, a.dwpart, a.w_near, a.w_far, a.H, a.N,
+    CAUSAL ? a.part : a.fin, a.rowstat, a.rowfar, a.dwpart, a.w_near, a.w_far, a.H, a.N,
     a.band_k, a.L, a.nseg, a.rank, scale2);
+  launch_seg_grad<T, D>(a, L);
   const int nchunk = (int)((REC + 255) / 256);
   const dim3 sgrid((unsigned)std::min<long long>((long long)nchunk * BH, 0xFFFFFFFFll));
   if constexpr (CAUSAL) {
