@@ -55,7 +55,11 @@ struct BwdCfg {
   static constexpr int UNIT2 = 2 * 32 * ROW;    // two buffers of one 32-row unit
   static constexpr int STAT_UNIT = 32 * 3 * 4;  // key pass: m, 1/l, D per row
   static constexpr int BUDGET = 150 * 1024;
-  static constexpr int UR_FIT = (BUDGET - 2 * TILE - 256 - 2 * NT * 4) / (UNIT2 + STAT_UNIT);
+  // the far-field records of up to three maps, kept in LDS for widths up to
+  // 64 (read every tile; the causal ones are also advanced there)
+  static constexpr int REC_BYTES = D <= 64 ? 3 * D * (D + 1) * 4 : 0;
+  static constexpr int UR_FIT =
+      (BUDGET - 2 * TILE - 256 - 2 * NT * 4 - REC_BYTES) / (UNIT2 + STAT_UNIT);
   static constexpr int UR = UR_FIT > 8 ? 8 : UR_FIT;
   static_assert(UR >= 2, "a round must hold one tile");
   static constexpr int WK = 32 * UR;  // rows per staging round
@@ -63,7 +67,9 @@ struct BwdCfg {
   // reuses the area for its block reduction (2 x NT floats)
   static constexpr int STAT_BYTES = WK * 12 > 2 * NT * 4 ? WK * 12 : 2 * NT * 4;
   // [buffer A: WK rows][buffer B: WK rows][tile buffer 1][tile buffer 2][64 floats][stats]
-  static constexpr int LDS = 2 * WK * ROW + 2 * TILE + 256 + STAT_BYTES;
+  // [records]
+  static constexpr int REC_OFF = 2 * WK * ROW + 2 * TILE + 256 + STAT_BYTES;
+  static constexpr int LDS = REC_OFF + REC_BYTES;
 };
 
 __device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"); }
@@ -121,6 +127,13 @@ __device__ __forceinline__ void stage_phi_rows(const T* src, int r0, int N, int 
     }
     *reinterpret_cast<uint4*>(dst + row * ST + c * LY::EPC) = outw;
   }
+}
+
+// The slice's or segment's records (n floats) into LDS, 16 bytes per thread
+// and pass; the caller synchronises before reading them.
+__device__ __forceinline__ void stage_records(float* dst, const float* src, int n) {
+  for (int t = threadIdx.x; 4 * t < n; t += NT)
+    *reinterpret_cast<float4*>(dst + 4 * t) = *reinterpret_cast<const float4*>(src + 4 * t);
 }
 
 template <typename T>
@@ -269,7 +282,10 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
   const size_t base = (size_t)bh * N * D;
   const size_t REC = (size_t)rank * D * (D + 1);
-  float* rec = CAUSAL ? recs + ((size_t)bh * nseg + seg) * REC : recs + (size_t)bh * REC;
+  float* grec = CAUSAL ? recs + ((size_t)bh * nseg + seg) * REC : recs + (size_t)bh * REC;
+  float* srec = reinterpret_cast<float*>(dyn_smem + C::REC_OFF);
+  if constexpr (C::REC_BYTES > 0) stage_records(srec, grec, (int)REC);
+  float* rec = C::REC_BYTES > 0 ? srec : grec;  // (the first tile's barriers order the copy)
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const float tau = scale2 * 0.69314718055994531f;  // 1/sqrt(d)
   const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
@@ -696,7 +712,10 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
   const size_t base = (size_t)bh * N * D;
   const size_t REC = (size_t)rank * D * (D + 1);
-  float* drec = CAUSAL ? drecs + ((size_t)bh * nseg + seg) * REC : drecs + (size_t)bh * REC;
+  float* gdrec = CAUSAL ? drecs + ((size_t)bh * nseg + seg) * REC : drecs + (size_t)bh * REC;
+  float* sdrec = reinterpret_cast<float*>(dyn_smem + C::REC_OFF);
+  if constexpr (C::REC_BYTES > 0) stage_records(sdrec, gdrec, (int)REC);
+  float* drec = C::REC_BYTES > 0 ? sdrec : gdrec;  // (the first tile's barriers order the copy)
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const float tau = scale2 * 0.69314718055994531f;
   const f32x4 zero = {0.f, 0.f, 0.f, 0.f};

@@ -7,12 +7,14 @@
 // the rest.
 //
 // Differences from the tuned kernels, chosen so that any width fits:
-//   * the far state stays in the workspace record (global memory, read through
-//     the caches) instead of being copied into LDS as operand fragments: at
-//     d = 128 the fp32 fragments alone would fill the CU's LDS;
-//   * the causal running state is also kept in the segment's record, updated
-//     in place after each tile (one map and one 16-feature block at a time,
-//     36 accumulator registers), instead of in registers;
+//   * the far state is read as the record itself (fp32, tile order) rather
+//     than as operand fragments: for widths up to 64 the records of up to
+//     three maps are copied into LDS once per workgroup; at d = 128 they stay
+//     in the workspace (global memory, read through the caches), since the
+//     fp32 records alone would fill the CU's LDS;
+//   * the causal running state is that record, advanced after each tile (one
+//     map and one 16-feature block at a time, 36 accumulator registers),
+//     instead of in registers;
 //   * the maps are processed one after another, so only one map's numerator
 //     tiles are live at a time.
 // Per 64-row tile (4 waves, one 16-row strip each): the key window is staged
@@ -35,11 +37,15 @@ struct WideCfg {
   static constexpr int PK_BYTES = TM * ROW;     // phi_l of the tile's keys (causal)
   static constexpr int UNIT2 = 2 * 32 * ROW;    // K and V rows of one 32-key unit
   static constexpr int BUDGET = 150 * 1024;
-  static constexpr int UR_FIT = (BUDGET - PK_BYTES) / UNIT2;
+  // the state records of up to three maps, kept in LDS for widths up to 64
+  // (read every tile; the causal ones are also advanced there)
+  static constexpr int REC_BYTES = D <= 64 ? 3 * D * (D + 1) * 4 : 0;
+  static constexpr int UR_FIT = (BUDGET - PK_BYTES - REC_BYTES) / UNIT2;
   static constexpr int UR = UR_FIT > 8 ? 8 : UR_FIT;
   static_assert(UR >= 2, "a round must hold one tile of keys");
   static constexpr int WK = 32 * UR;            // keys per round
-  static constexpr int LDS = 2 * WK * ROW + PK_BYTES;
+  static constexpr int REC_OFF = 2 * WK * ROW + PK_BYTES;
+  static constexpr int LDS = REC_OFF + REC_BYTES;
 };
 
 // Wait states after a loop whose last matrix-core results are read by vector
@@ -170,7 +176,14 @@ __global__ __launch_bounds__(NT) void k_wide(const T* __restrict__ q, const T* _
   const size_t REC = (size_t)rank * D * (D + 1);
   // non-causal: the slice's final record; causal: the segment's exclusive
   // prefix record, advanced tile by tile
-  float* rec = CAUSAL ? recs + ((size_t)bh * nseg + seg) * REC : recs + (size_t)bh * REC;
+  float* grec = CAUSAL ? recs + ((size_t)bh * nseg + seg) * REC : recs + (size_t)bh * REC;
+  float* srec = reinterpret_cast<float*>(dyn_smem + C::REC_OFF);
+  if constexpr (C::REC_BYTES > 0) {
+    // (the first tile's staging barriers order the copy before any read)
+    for (int t = threadIdx.x; 4 * t < (int)REC; t += NT)
+      *reinterpret_cast<float4*>(srec + 4 * t) = *reinterpret_cast<const float4*>(grec + 4 * t);
+  }
+  float* rec = C::REC_BYTES > 0 ? srec : grec;
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
   const int s0 = seg * L, s1 = min(N, s0 + L);
