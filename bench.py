@@ -76,10 +76,10 @@ def _short_kernel_name(name):
     return name if len(name) <= 70 else name[:67] + "..."
 
 
-# kernels of the N = 4096 workload (bf16, d = 32, rank 2, k = 20)
+# kernel of the N = 4096 workload (bf16, d = 32, rank 2, k = 20): one launch
+# (state exchange, near field, far field and blend in one kernel)
 N4096_KERNELS = {
-    "seg_state": "k_seg_state<unsigned short, 32, 2, 64>",
-    "band_apply": "k_band_pair<32, 2, 1>",
+    "band_apply": "k_band_fused<32, 2, 1>",
 }
 TRACE_JSON = os.path.join(ROOT, "profiles", "kernel_trace_stress64k.json")
 
@@ -114,18 +114,11 @@ def trace_summary(stats_csv):
         _, dur = _durations(disp, needle)
         instep[key] = statistics.mean(dur[warm:warm + steps])
         events[key] = statistics.mean(dur[warm + steps:warm + 2 * steps])
-    # the N = 4096 leg: its first 105 apply launches, and every dispatch
-    # between the first of its state launches and the last of those
-    hits, dur = _durations(disp, N4096_KERNELS["band_apply"])
-    t_end = int(hits[warm + 2 * steps - 1]["End_Timestamp"])
-    s_hits, _ = _durations(disp, N4096_KERNELS["seg_state"])
-    t_beg = int(s_hits[0]["Start_Timestamp"])
-    window = [r for r in disp if t_beg <= int(r["Start_Timestamp"]) <= t_end]
+    # the N = 4096 leg: the first 105 launches of its kernel (the lra1k and
+    # layer legs, which launch the same kernel, run later)
     n4 = {"instep": {}, "events": {}}
-    for key, needle in (("seg_state", N4096_KERNELS["seg_state"]),
-                        ("combine", "k_state_combine<false>"),
-                        ("band_apply", N4096_KERNELS["band_apply"])):
-        _, d4 = _durations(window, needle)
+    for key, needle in N4096_KERNELS.items():
+        _, d4 = _durations(disp, needle)
         n4["instep"][key] = statistics.mean(d4[warm:warm + steps])
         n4["events"][key] = statistics.mean(d4[warm + steps:warm + 2 * steps])
     rec = {"kernel_source_hash": kernel_source_hash(), "stress64k_instep_us": instep,
@@ -298,8 +291,8 @@ def read_counters(kernel: str):
 
 # the sources of the kernels the profiles describe (host-side code excluded,
 # so a change to argument checks or bindings does not void them)
-KERNEL_SOURCES = ("fmm_device.h", "fmm_oct.h", "fmm_kernels.hip", "fmm_pair.hip",
-                  "fmm_causal.hip")
+KERNEL_SOURCES = ("fmm_device.h", "fmm_oct.h", "fmm_apply.h", "fmm_launch.h",
+                  "fmm_kernels.hip", "fmm_pair.hip", "fmm_causal.hip")
 
 
 def kernel_source_hash() -> str:
@@ -558,6 +551,8 @@ def main():
     timed(f4, args.steps, 0, torch)
     binding.kernel_timing(False)
     X4 = w4.B * w4.H * w4.N * w4.d * 2
+    # one launch: Q, K, V read once and the output written (4X); the state
+    # exchange goes through the L2
     b4 = {"seg_state": 2 * X4, "band_apply": 4 * X4}
     kt4 = {}
     for name in binding.KERNELS:
@@ -639,11 +634,11 @@ def main():
               max(5, args.steps // 4), 0, torch)
         binding.kernel_timing(False)
         kb = {}
-        for name in ("bwd_rows", "bwd_keys"):
+        for name, nx in (("bwd_rows", 5), ("bwd_seg_grad", 2), ("bwd_keys", 6)):
             ms, n = binding.kernel_timing_read(name)
             if n:
                 us = ms * 1e3 / n
-                byt = (5 if name == "bwd_rows" else 6) * X
+                byt = nx * X
                 kb[name] = {"events_us": round(us, 3), "alg_bytes": byt,
                             "events_hbm_frac": round(byt / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
         fb_rec[form] = {"fwd_bwd_ms": round(t_fb * 1e3, 4),

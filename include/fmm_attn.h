@@ -91,12 +91,13 @@ extern "C" {
 #define FMM_KERNEL_STATE_COMBINE 1 /* sum (non-causal) or exclusive scan       */
 #define FMM_KERNEL_BAND_APPLY    2 /* non-causal near field + far apply + blend */
 #define FMM_KERNEL_CAUSAL_APPLY  3 /* causal near field + prefix far + blend    */
-#define FMM_KERNEL_BWD_ROWS      4 /* backward row pass: dq, dS partials        */
+#define FMM_KERNEL_BWD_ROWS      4 /* backward row pass: dq, row statistics     */
 #define FMM_KERNEL_BWD_KEYS      5 /* backward key pass: dk, dv                 */
 #define FMM_KERNEL_BWD_DW        6 /* backward blend-logit reduction            */
 #define FMM_KERNEL_LAYER_COPY    7 /* attention layer: head split and merge     */
 #define FMM_KERNEL_FAST_WEIGHT   8 /* fast-weight far field scan               */
-#define FMM_KERNEL_COUNT         9
+#define FMM_KERNEL_BWD_SEG_GRAD  9 /* backward per-segment far-state gradients */
+#define FMM_KERNEL_COUNT        10
 
 /*
  * fmm_attn_forward - the operator of Eq. (9) blended as in Eq. (11), fp32.
@@ -277,6 +278,22 @@ void fmm_attn_release_workspace(void);
 
 /* Library version as major*10000 + minor*100 + patch. */
 int fmm_attn_version(void);
+
+/*
+ * One-launch path for short sequences (non-causal, bf16, d = 32 or 64, band
+ * half-width <= 64, one or two maps, per-map normalisation, B*H a multiple
+ * of 8, at most 64 tiles of 128 rows per slice and at most two workgroups per
+ * compute unit in total).  There the state, its sum and the apply run as one
+ * kernel whose workgroups exchange partial far-field states through memory;
+ * its results are deterministic and identical in every mode below, and
+ * within the forward's tolerance of the three-launch path's (the state is
+ * summed in another order).  Mode 0: never; 1: wherever it applies (the
+ * default); 2: wherever it applies, but every workgroup forms its slice's
+ * state itself instead of exchanging (slower; a check of the exchange).
+ * Process-wide; returns the previous mode, or -1 for a mode outside 0..2.
+ * The workspace sizes above include what this path needs.
+ */
+int fmm_attn_set_one_launch(int mode);
 
 /*
  * Kernel timing (profiling aid).  fmm_attn_kernel_timing(1) makes every later

@@ -28,7 +28,8 @@ FMM_FAR_NORM_PER_MAP = 0
 FMM_FAR_NORM_JOINT = 1
 
 KERNELS = {"seg_state": 0, "state_combine": 1, "band_apply": 2, "causal_apply": 3,
-           "bwd_rows": 4, "bwd_keys": 5, "bwd_dw": 6, "layer_copy": 7, "fast_weight": 8}
+           "bwd_rows": 4, "bwd_keys": 5, "bwd_dw": 6, "layer_copy": 7, "fast_weight": 8,
+           "bwd_seg_grad": 9}
 
 EXPORTS = (
     "fmm_attn_forward", "fmm_attn_forward_bf16", "fmm_attn_workspace_bytes",
@@ -36,6 +37,7 @@ EXPORTS = (
     "fmm_attn_version", "fmm_attn_kernel_timing", "fmm_attn_kernel_timing_read",
     "fmm_attn_forward_noalloc", "fmm_attn_noalloc_max_bytes", "fmm_attn_forward_ex",
     "fmm_attn_backward", "fmm_attn_layer_forward", "fmm_attn_forward_fastweight",
+    "fmm_attn_set_one_launch",
 )
 
 _lib = None
@@ -87,6 +89,8 @@ def lib() -> ctypes.CDLL:
     h.fmm_attn_version.restype = ci
     h.fmm_attn_kernel_timing.argtypes = [ci]
     h.fmm_attn_kernel_timing.restype = ci
+    h.fmm_attn_set_one_launch.argtypes = [ci]
+    h.fmm_attn_set_one_launch.restype = ci
     h.fmm_attn_kernel_timing_read.argtypes = [ci, ctypes.POINTER(ctypes.c_double),
                                               ctypes.POINTER(ctypes.c_longlong)]
     h.fmm_attn_kernel_timing_read.restype = ci
@@ -295,6 +299,16 @@ def raw_forward(q_ptr, k_ptr, v_ptr, out_ptr, B, H, N, d, band_k, rank, causal, 
     v = ctypes.c_void_p
     return fn(v(q_ptr), v(k_ptr), v(v_ptr), v(out_ptr), B, H, N, d, band_k, rank, causal,
               v(wn_ptr), v(wf_ptr), v(stream_ptr))
+
+
+def set_one_launch(mode: int) -> int:
+    """Mode of the one-launch path for short non-causal slices (0 never, 1 where
+    it applies, 2 where it applies without the workgroups' exchange); returns
+    the previous mode."""
+    prev = lib().fmm_attn_set_one_launch(int(mode))
+    if prev < 0:
+        raise ValueError("one-launch mode must be 0, 1 or 2")
+    return prev
 
 
 def kernel_timing(enable: bool) -> None:

@@ -8,8 +8,10 @@
 #include <stdlib.h>
 
 #include <algorithm>
+#include <atomic>
 #include <map>
 #include <mutex>
+#include <random>
 #include <utility>
 #include <vector>
 
@@ -18,7 +20,7 @@
 
 namespace {
 
-constexpr int kVersion = 1 * 10000 + 1 * 100 + 0;
+constexpr int kVersion = 1 * 10000 + 2 * 100 + 0;
 
 // ------------------------------------------------------------------ planning
 // Segments split the key axis of every (batch, head) slice for the far-field
@@ -31,7 +33,13 @@ struct Plan {
   int nseg_apply;
   int L_apply;
   size_t ws_bytes;
+  int fused_g = 0;  // workgroups per slice of the one-launch path (0: not available)
 };
+
+// The one-launch path for short non-causal slices is planned for MI355X's 256
+// compute units at two workgroups each; a device with fewer CUs (checked per
+// call) takes the three-launch path with the same workspace.
+constexpr int kFusedPlanWorkgroups = 512;
 
 // Rows per segment so that B*H*segments is about `target_wg` workgroups.
 long long seg_rows(long long bh, int N, long long target_wg, int tm) {
@@ -211,6 +219,48 @@ int launch_now(const fmm::LaunchArgs& a) {
   return fmm::launch_forward(a, L) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
 }
 
+// ------------------------------------------------------------------ one-launch path
+// Mode: 0 never, 1 wherever it applies (default), 2 wherever it applies but
+// with every workgroup forming its slice's state itself (no exchange).
+std::atomic<int>& one_launch_mode() {
+  static std::atomic<int> m{1};
+  return m;
+}
+
+// Epochs of the one-launch path's stamps: unique per call within the process,
+// starting from a random 48-bit value so that stale stamps left in memory by
+// another process (or garbage) match a call's epoch with negligible
+// probability.  56 bits (the stamp's low 8 bits hold the XCC id).
+unsigned long long next_epoch() {
+  static std::atomic<unsigned long long> e{[] {
+    std::random_device rd;
+    const unsigned long long s = ((unsigned long long)rd() << 20) ^ (unsigned long long)rd();
+    return (s & ((1ull << 47) - 1)) | (1ull << 47);
+  }()};
+  return e.fetch_add(1, std::memory_order_relaxed) & ((1ull << 56) - 1);
+}
+
+// Workgroups of k_band_fused that fit on the current device at once (two per CU).
+int resident_fused_workgroups() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  if (dev >= 0 && dev < 64) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  if (dev >= 0 && dev < 64) cache[dev].store(2 * cus, std::memory_order_relaxed);
+  return 2 * cus;
+}
+
 fmm::LaunchArgs make_args(const void* q, const void* k, const void* v, void* out, int B, int H,
                           int N, int d, int band_k, int rank, int causal, const float* w_near,
                           const float* w_far, int dtype, int far_norm, void* ws, const Plan& p,
@@ -238,15 +288,35 @@ fmm::LaunchArgs make_args(const void* q, const void* k, const void* v, void* out
   a.L = p.L;
   a.nseg_apply = p.nseg_apply;
   a.L_apply = p.L_apply;
+  const int mode = one_launch_mode().load(std::memory_order_relaxed);
+  if (p.fused_g > 0 && mode != 0 && far_norm == FMM_FAR_NORM_PER_MAP &&
+      (long long)B * H * p.fused_g <= resident_fused_workgroups()) {
+    a.fused_g = p.fused_g;
+    a.exchange = mode == 2 ? 0 : 1;
+    a.epoch = next_epoch();
+  }
   return a;
+}
+
+// Adds the one-launch path's workspace to a plan (the larger of the two).
+void add_fused(Plan& p, long long bh, int G, int d, int rank) {
+  p.fused_g = G;
+  if (G <= 0 || p.ws_bytes == 0) return;
+  const size_t f = fmm::fused_layout(bh, G, (long long)rank * d * (d + 1)).total;
+  if (f > p.ws_bytes) p.ws_bytes = f;
 }
 
 Plan plan_for(int B, int H, int N, int d, int band_k, int rank, int causal, int dtype) {
   const int kc = band_k < N ? band_k : N;
   const int apply_tm = fmm::band_pair_applies(dtype, d, kc, causal, N) ? fmm::pair_tile_rows()
                                                                     : fmm::tile_rows();
-  return make_plan(B, H, N, d, rank, dtype == FMM_DTYPE_BF16 ? 2 : 4, apply_tm);
+  Plan p = make_plan(B, H, N, d, rank, dtype == FMM_DTYPE_BF16 ? 2 : 4, apply_tm);
+  const long long bh = (long long)B * H;
+  add_fused(p, bh, fmm::fused_groups(dtype, d, kc, rank, causal, bh, N, kFusedPlanWorkgroups), d,
+            rank);
+  return p;
 }
+
 
 int run(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d,
         int band_k, int rank, int causal, const float* w_near, const float* w_far, int dtype,
@@ -620,8 +690,18 @@ size_t fmm_attn_workspace_bytes(int B, int H, int N, int d, int rank, int causal
   // the plan depends on the element size only through the segment length
   // floor; report the larger of the two dtypes' needs
   const int tm = fmm::tile_rows();
-  const Plan a = make_plan(B, H, N, d, rank, 2, tm), b = make_plan(B, H, N, d, rank, 4, tm);
+  Plan a = make_plan(B, H, N, d, rank, 2, tm), b = make_plan(B, H, N, d, rank, 4, tm);
+  // the one-launch path (bf16, any band it takes)
+  const long long bh = (long long)B * H;
+  add_fused(a, bh,
+            fmm::fused_groups(FMM_DTYPE_BF16, d, 0, rank, causal, bh, N, kFusedPlanWorkgroups),
+            d, rank);
   return a.ws_bytes > b.ws_bytes ? a.ws_bytes : b.ws_bytes;
+}
+
+int fmm_attn_set_one_launch(int mode) {
+  if (mode < 0 || mode > 2) return -1;
+  return one_launch_mode().exchange(mode);
 }
 
 int fmm_attn_forward_ws(const void* q, const void* k, const void* v, void* out, int B, int H,

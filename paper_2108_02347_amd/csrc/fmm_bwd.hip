@@ -674,15 +674,15 @@ void launch_seg_grad(const BwdArgs& a, Launcher& L) {
   hipStream_t s = (hipStream_t)a.stream;
   switch (a.rank) {
     case 1:
-      L(FMM_KERNEL_BWD_ROWS, k_seg_grad<T, D, 1>, grid, dim3(SNTB), 0, s, (const T*)a.q,
+      L(FMM_KERNEL_BWD_SEG_GRAD, k_seg_grad<T, D, 1>, grid, dim3(SNTB), 0, s, (const T*)a.q,
         (const T*)a.dout, (const float*)a.rowfar, a.w_far, a.dpart, a.H, a.N, a.L, a.nseg);
       break;
     case 2:
-      L(FMM_KERNEL_BWD_ROWS, k_seg_grad<T, D, 2>, grid, dim3(SNTB), 0, s, (const T*)a.q,
+      L(FMM_KERNEL_BWD_SEG_GRAD, k_seg_grad<T, D, 2>, grid, dim3(SNTB), 0, s, (const T*)a.q,
         (const T*)a.dout, (const float*)a.rowfar, a.w_far, a.dpart, a.H, a.N, a.L, a.nseg);
       break;
     default:
-      L(FMM_KERNEL_BWD_ROWS, k_seg_grad<T, D, 3>, grid, dim3(SNTB), 0, s, (const T*)a.q,
+      L(FMM_KERNEL_BWD_SEG_GRAD, k_seg_grad<T, D, 3>, grid, dim3(SNTB), 0, s, (const T*)a.q,
         (const T*)a.dout, (const float*)a.rowfar, a.w_far, a.dpart, a.H, a.N, a.L, a.nseg);
       break;
   }

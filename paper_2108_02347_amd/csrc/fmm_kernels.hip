@@ -943,6 +943,10 @@ template <typename T, int D, int R>
 static hipError_t launch_all(const LaunchArgs& a, Launcher& L) {
   // widths above 64 and three feature maps take the general apply kernel
   constexpr bool tuned = D <= 64 && R <= 2;
+  if constexpr (tuned && sizeof(T) == 2) {
+    if (a.fused_g > 0 && !a.causal && a.far_norm == FMM_FAR_NORM_PER_MAP)
+      return launch_band_fused(a, L);
+  }
   if (launch_state<T, D, R>(a, L) != hipSuccess) return L.err;
   float* part = a.ws;
   float* fin = reinterpret_cast<float*>(reinterpret_cast<uintptr_t>(a.ws) +

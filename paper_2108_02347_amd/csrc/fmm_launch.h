@@ -27,6 +27,13 @@ struct LaunchArgs {
   int L;           // rows per state segment (multiple of the tile height)
   int nseg_apply;  // row segments walked by one non-causal apply workgroup
   int L_apply;     // rows per apply segment (multiple of the tile height)
+  // one-launch path for short non-causal slices (k_band_fused): workgroups
+  // per slice (0: the three-launch path), the call's epoch for its stamps,
+  // and whether the workgroups exchange partial states (0: each computes its
+  // slice's state itself)
+  int fused_g = 0;
+  unsigned long long epoch = 0;
+  int exchange = 1;
 };
 
 // Supplies a start/stop HIP event pair per kernel launch when timing is
@@ -115,6 +122,29 @@ int tile_rows();
 bool band_pair_applies(int dtype, int d, int band_k, int causal, long long n);
 int pair_tile_rows();
 hipError_t launch_band_pair(const LaunchArgs& a, Launcher& L, const float* fin);
+
+// One launch for short non-causal slices (fmm_pair.hip, k_band_fused): the
+// workgroups per slice G (one per 128-row tile) when the shape qualifies and
+// B*H*G <= max_workgroups, else 0.
+int fused_groups(int dtype, int d, int band_k, int rank, int causal, long long bh, long long n,
+                 int max_workgroups);
+hipError_t launch_band_fused(const LaunchArgs& a, Launcher& L);
+// Its workspace: G partial records per slice, one total record per slice,
+// two 8-byte stamps per workgroup.
+struct FusedLayout {
+  size_t off_part, off_tot, off_stamp, total;
+};
+inline FusedLayout fused_layout(long long bh, int G, long long rec) {
+  auto al = [](size_t x) { return (x + 255) / 256 * 256; };
+  FusedLayout f;
+  f.off_part = 0;
+  f.off_tot = al((size_t)bh * G * rec * sizeof(float));
+  f.off_stamp = f.off_tot + al((size_t)bh * rec * sizeof(float));
+  f.total = f.off_stamp + al((size_t)bh * G * 2 * sizeof(unsigned long long));
+  return f;
+}
+// polls of a stamp wait before a workgroup computes its slice's state itself
+constexpr int kFusedSpinLimit = 20000;
 
 // Causal apply with one 16-row strip per wavefront (fmm_causal.hip): bf16,
 // d = 32 or 64, band half-width <= 64; walks the state segments (a.L rows,

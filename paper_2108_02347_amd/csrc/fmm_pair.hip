@@ -110,13 +110,55 @@ struct PairFrags {
 //   scores of A and B + phi(q) | softmax of A and B |
 //   far products and P V of A and B (at a raised wave priority) |
 //   near normalisation, blend, store
-// mid() runs after the first phase, once phi(q) is formed.
-template <int D, int R, int KC, bool GENERAL, class Mid>
+// mid() runs after the first phase, once phi(q) is formed.  With FAR_LAST
+// the far products move behind the near field's P V product and
+// normalisation, and pre_far() runs just before them: the state fragments
+// (sf, zo) need to be in place only from then on.
+struct NoStep {
+  __device__ __forceinline__ void operator()() const {}
+};
+
+// Far part of both strips (Eq. (8)-(9), each map normalised on its own),
+// each state fragment read once per map, added to fo with weight sfw.
+template <int D, int R>
+__device__ __forceinline__ void pair_far(const Oct* sf, Oct (*zo)[D / 32],
+                                         Oct (*ph)[2][D / 32], float sfw,
+                                         f32x4 (*fo)[D / 16]) {
+  constexpr int NB = D / 16, NQ = D / 32;
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int l = 0; l < R; ++l) {
+    f32x4 nA[NB + 1], nB[NB + 1];
+#pragma unroll
+    for (int nb = 0; nb <= NB; ++nb) nA[nb] = nB[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < NQ; ++p) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const Oct f = sf[((l * NB + nb) * NQ + p) * 64 + lane];
+        nA[nb] = mma8(f, ph[l][0][p], nA[nb]);
+        nB[nb] = mma8(f, ph[l][1][p], nB[nb]);
+      }
+      nA[NB] = mma8(zo[l][p], ph[l][0][p], nA[NB]);
+      nB[NB] = mma8(zo[l][p], ph[l][1][p], nB[NB]);
+    }
+    const float fa = sfw > 0.f ? sfw * fast_rcp(nA[NB][0]) : 0.f;
+    const float fb = sfw > 0.f ? sfw * fast_rcp(nB[NB][0]) : 0.f;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      fo[0][nb] += nA[nb] * fa;
+      fo[1][nb] += nB[nb] * fb;
+    }
+  }
+}
+
+template <int D, int R, int KC, bool GENERAL, bool FAR_LAST = false, class Mid,
+          class PreFar = NoStep>
 __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
                                           float scale2, float sn, float sfw, Oct (*qo)[D / 32],
                                           const unsigned char* kr, const unsigned char* vr,
                                           int slot0, const RingOffsets<D>& ro, const Oct* sf,
-                                          Oct (*zo)[D / 32], Mid mid) {
+                                          Oct (*zo)[D / 32], Mid mid, PreFar pre_far = {}) {
   using C = PairCfg<D, R, KC>;
   constexpr int NB = C::NB, NQ = C::NQ, NU = C::NU, NBK = 2 * NU, NS = NBK - 1;
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
@@ -230,30 +272,7 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
   f32x4 fo[2][NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) fo[0][nb] = fo[1][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int l = 0; l < R; ++l) {
-    f32x4 nA[NB + 1], nB[NB + 1];
-#pragma unroll
-    for (int nb = 0; nb <= NB; ++nb) nA[nb] = nB[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int p = 0; p < NQ; ++p) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const Oct f = sf[((l * NB + nb) * NQ + p) * 64 + lane];
-        nA[nb] = mma8(f, ph[l][0][p], nA[nb]);
-        nB[nb] = mma8(f, ph[l][1][p], nB[nb]);
-      }
-      nA[NB] = mma8(zo[l][p], ph[l][0][p], nA[NB]);
-      nB[NB] = mma8(zo[l][p], ph[l][1][p], nB[NB]);
-    }
-    const float fa = sfw > 0.f ? sfw * fast_rcp(nA[NB][0]) : 0.f;
-    const float fb = sfw > 0.f ? sfw * fast_rcp(nB[NB][0]) : 0.f;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) {
-      fo[0][nb] += nA[nb] * fa;
-      fo[1][nb] += nB[nb] * fb;
-    }
-  }
+  if constexpr (!FAR_LAST) pair_far<D, R>(sf, zo, ph, sfw, fo);
   __builtin_amdgcn_sched_barrier(0);
 
   // ---- phase 3: O^T = V^T P^T and the row sums of both strips, each value
@@ -282,6 +301,10 @@ __device__ __forceinline__ void pair_tile(Rsrc oh, int i0, int N, int band_k,
       fo[0][nb] += oA[nb] * a0;
       fo[1][nb] += oB[nb] * a1;
     }
+  }
+  if constexpr (FAR_LAST) {
+    pre_far();
+    pair_far<D, R>(sf, zo, ph, sfw, fo);
   }
   // rows at or beyond N fall outside the output buffer and are dropped
   for (int s = 0; s < 2; ++s) store_strip<D>(oh, i0 + 16 * s, fo[s]);
@@ -391,6 +414,350 @@ __global__ __launch_bounds__(PNT, 2) void k_band_pair(const bf16_t* __restrict__
   for (; t < ntile; ++t) step(t, std::true_type{});
 }
 
+// ------------------------------------------------------------------ one launch for short slices
+// For short sequences the three dependent launches of the state, its sum and
+// the apply cost more than their bytes.  k_band_fused does all three in one
+// launch: workgroup j of a (batch, head) slice owns rows [128 j, 128 j + 128)
+// and, besides its tile of the operator, the partial far-field state of those
+// rows.  The slice's G workgroups exchange their partial states through
+// memory: each writes its record and then a stamp; once every stamp of the
+// slice is there, workgroup j sums elements [j C, (j + 1) C) of the G records
+// (C = ceil(rec / G)) in slice order and stamps again; once all of those are
+// there, each reads the slice's total.  The tile's near field covers the
+// waits: the first stamp goes out after the score phase (by when the
+// record's stores have long reached L2), the first wait comes after the P V
+// product.
+//
+// The exchange relies on the slice's workgroups sharing one L2: the grid is
+// ordered so that each slice's workgroups are consecutive after xcd_remap,
+// which places them on one XCD when B*H is a multiple of 8.  A record is
+// written with ordinary stores and s_waitcnt vmcnt(0) (the stores have
+// reached L2) precedes its stamp; stamps are written and polled with
+// device-scope atomics (which bypass the vector L1; plain loads of a stamp
+// can keep hitting a stale L1 line), and a workgroup reads the records only
+// after it has seen their stamps, so no line of them is in its L1 before.  A stamp holds the call's
+// epoch and the XCC id of its writer.  Any stamp from another XCC (or one
+// marking a workgroup that gave up), or a wait beyond spin_limit polls, makes
+// the workgroup compute its slice's total itself from K and V in memory: the
+// same partial states (same products, same order) summed in the same order,
+// so every path gives the same bits.  Waits are bounded, so the kernel always
+// drains, and no workgroup's result depends on where its peers ran.
+
+// stamps: (epoch << 8) | XCC id of the writer; this XCC id marks a workgroup
+// that gave up on the exchange
+constexpr unsigned kGaveUp = 0xffu;
+
+__device__ __forceinline__ unsigned xcc_id() {
+  unsigned x;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+  return x & 0xfu;
+}
+
+// Partial far-field state of the 128 keys r0 .. r0+127 held in ring slots
+// slot0 .. slot0+3 (keys at or beyond N excluded): T_l = phi_l(K)^T [V | 1]
+// for the feature block cb, in record order: acc[l][eb], lane (r, g) holds
+// T_l[16cb + 4g + i][16eb + r]; acc[l][NB] (lanes r = 0) holds z_l[16cb + 4g
+// + i].  The key operands are the transposed ring reads of the P V product,
+// so phi_l(K)^T and [V | 1] share one key order.
+template <int D, int R>
+__device__ __forceinline__ void tile_state(const unsigned char* kr, const unsigned char* vr,
+                                           int slot0, int r0, int N, const RingOffsets<D>& ro,
+                                           int cb, f32x4 (*acc)[D / 16 + 1]) {
+  constexpr int NB = D / 16, RB = RingRows<D>::RB;
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const Oct onecol = r == 0 ? oct_ones() : make_uint4(0u, 0u, 0u, 0u);
+  // the transposed read of columns 16cb .. 16cb+15 (RingOffsets::voff[cb],
+  // formed here since cb is not a compile-time index)
+  const int kcol = RingRows<D>::off(4 * g + (r >> 2), 2 * cb + ((r & 3) >> 1)) + 8 * (r & 1);
+#pragma unroll
+  for (int l = 0; l < R; ++l)
+#pragma unroll
+    for (int eb = 0; eb <= NB; ++eb) acc[l][eb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int ub = (slot0 + u) * 32 * RB;
+    const unsigned char* kp = kr + ub + kcol;
+    Oct pk[2];
+    phi_oct(oct_of(ld_tr16(kp), ld_tr16(kp + 16 * RB)), pk[0], pk[1]);
+    // slot 2i (low half of word i) and 2i + 1 hold keys 4g + 2i, 4g + 2i + 1
+    // (i < 2) or 16 + 4g + 2(i - 2), ... of the unit
+    const int kvalid = N - (r0 + 32 * u);
+    if (kvalid < 32) {
+#pragma unroll
+      for (int l = 0; l < R; ++l) {
+        uint32_t wv[4] = {pk[l].x, pk[l].y, pk[l].z, pk[l].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int k0 = i < 2 ? 4 * g + 2 * i : 16 + 4 * g + 2 * (i - 2);
+          wv[i] &= (k0 < kvalid ? 0x0000ffffu : 0u) | (k0 + 1 < kvalid ? 0xffff0000u : 0u);
+        }
+        pk[l] = make_uint4(wv[0], wv[1], wv[2], wv[3]);
+      }
+    }
+#pragma unroll
+    for (int eb = 0; eb < NB; ++eb) {
+      const unsigned char* vp = vr + ub + ro.voff[eb];
+      const Oct vt = oct_of(ld_tr16(vp), ld_tr16(vp + 16 * RB));
+#pragma unroll
+      for (int l = 0; l < R; ++l) acc[l][eb] = mma8(pk[l], vt, acc[l][eb]);
+    }
+#pragma unroll
+    for (int l = 0; l < R; ++l) acc[l][NB] = mma8(pk[l], onecol, acc[l][NB]);
+  }
+}
+
+// The tiles of feature block cb in a state record (the layout k_seg_state writes).
+template <int D, int R>
+__device__ __forceinline__ void store_record_block(float* rec, int cb,
+                                                   const f32x4 (*acc)[D / 16 + 1]) {
+  constexpr int NB = D / 16;
+  const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+#pragma unroll
+  for (int l = 0; l < R; ++l) {
+    float* sl = rec + (size_t)l * D * (D + 1);
+#pragma unroll
+    for (int eb = 0; eb < NB; ++eb)
+      *reinterpret_cast<f32x4*>(sl + ((cb * NB + eb) * 64 + lane) * 4) = acc[l][eb];
+    if (r == 0) *reinterpret_cast<f32x4*>(sl + D * D + 16 * cb + 4 * g) = acc[l][NB];
+  }
+}
+
+// Wave 0 polls stamp[2 i + level] of the slice's G workgroups (G <= 64) until
+// all carry this call's epoch; true when every one is `mine` (same epoch,
+// same XCC), false as soon as a stamp of this epoch is anything else or after
+// spin_limit polls.  Uniform over the workgroup.
+__device__ __forceinline__ bool wait_stamps(const unsigned long long* stamp, int level, int G,
+                                            unsigned long long epoch, unsigned long long mine,
+                                            int spin_limit, int* s_flag) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    int res = 2;
+    for (int it = 0; it <= spin_limit; ++it) {
+      const unsigned long long x =
+          lane < G ? __hip_atomic_load(stamp + 2 * lane + level, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT)
+                   : mine;
+      const bool fresh = (x >> 8) == epoch;
+      if (__any(fresh && x != mine)) break;
+      if (__all(fresh)) {
+        res = 1;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if (lane == 0) *s_flag = res;
+  }
+  __syncthreads();
+  const bool ok = *s_flag == 1;
+  __syncthreads();  // the flag is reused by the next wait
+  return ok;
+}
+
+__device__ __forceinline__ void put_stamp(unsigned long long* p, unsigned long long x) {
+  __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// grid.x = BH * G, G = ceil(N / 128) <= 64.  part: G records per slice; tot:
+// one record per slice; stamp: 2 G per slice.  exchange = 0 skips the exchange
+// (every workgroup computes its slice's total itself).
+template <int D, int R, int KC>
+__global__ __launch_bounds__(PNT, 2) void k_band_fused(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
+    bf16_t* __restrict__ out, float* __restrict__ part, float* __restrict__ tot,
+    unsigned long long* __restrict__ stamp, const float* __restrict__ w_near,
+    const float* __restrict__ w_far, int H, int N, int band_k, int G, float scale2,
+    unsigned long long epoch, int spin_limit, int exchange) {
+  using C = PairCfg<D, R, KC>;
+  constexpr int NB = C::NB, NQ = C::NQ, U = C::U;
+  constexpr int REC = R * D * (D + 1);
+  static_assert(REC * 4 <= 2 * C::RING, "the ring holds a record in the fallback");
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
+  unsigned char* kr = dyn_smem;
+  unsigned char* vr = dyn_smem + C::RING;
+  Oct* sf = reinterpret_cast<Oct*>(dyn_smem + 2 * C::RING);
+  // the waits' flag lives in the ring once the near field is done with it
+  // (a static LDS word would take d = 64 past two workgroups per CU)
+  int* s_flag = reinterpret_cast<int*>(dyn_smem);
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int bh = lin / G, j = lin % G, h = bh % H;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const size_t base = (size_t)bh * N * D;
+  const int hbytes = N * D * 2;
+  const Rsrc qh = head_rsrc(q + base, hbytes), kh = head_rsrc(k + base, hbytes),
+             vh = head_rsrc(v + base, hbytes), oh = head_rsrc(out + base, hbytes);
+  const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
+  const int t0 = j * PTM;
+  const int ua0 = (t0 >> 5) - KC;
+
+  // the tile's window: units ua0 + m in ring slot m; the wavefront's query
+  // rows (every load issued before the first LDS store)
+  constexpr int NR = U / 4, UREM = U % 4;
+  static_assert(UREM == 0 || UREM == 2, "ring of 4 + 2 KC units");
+  Oct qo[2][NQ];
+  {
+    RowsCopy<D, PTM, PNT> rk[NR], rv[NR];
+    RowsCopy<D, 32 * (UREM ? UREM : 2), PNT> tk, tv;
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      rk[i].load(kh, (ua0 + 4 * i) * 32, true);
+      rv[i].load(vh, (ua0 + 4 * i) * 32, true);
+    }
+    if constexpr (UREM != 0) {
+      tk.load(kh, (ua0 + 4 * NR) * 32, true);
+      tv.load(vh, (ua0 + 4 * NR) * 32, true);
+    }
+    load_qo<D, 2>(qh, t0 + 32 * w, true, qo);
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      auto slot = [=](int jj) { return 4 * i + jj; };
+      rk[i].store(kr, slot);
+      rv[i].store(vr, slot);
+    }
+    if constexpr (UREM != 0) {
+      auto slot = [=](int jj) { return 4 * NR + jj; };
+      tk.store(kr, slot);
+      tv.store(vr, slot);
+    }
+  }
+  __syncthreads();
+  const RingOffsets<D> ro;
+  const unsigned long long mine = (epoch << 8) | xcc_id();
+  unsigned long long* st = stamp + (size_t)bh * G * 2;
+  float* prec = part + (size_t)bh * G * REC;
+  float* trec = tot + (size_t)bh * REC;
+
+  // the partial state of the tile's own 128 keys (ring slots KC .. KC+3);
+  // its stamp follows the near field's first phase, by when the stores have
+  // long reached L2, so no wave stalls on them
+  if (exchange && w < NB) {
+    f32x4 acc[R][NB + 1];
+    tile_state<D, R>(kr, vr, KC, t0, N, ro, w, acc);
+    store_record_block<D, R>(prec + (size_t)j * REC, w, acc);
+  }
+  auto publish = [&]() {
+    if (exchange) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the record is in L2
+      __syncthreads();
+      if (threadIdx.x == 0) put_stamp(st + 2 * j, mine);
+    }
+  };
+
+  Oct zo[R][NQ];
+  auto pre_far = [&]() {
+    __syncthreads();  // every wave is done with the ring
+    bool ok = exchange != 0 && wait_stamps(st, 0, G, epoch, mine, spin_limit, s_flag);
+    if (ok) {
+      // elements [e0, e0 + cnt) of the G records: every value loaded at
+      // once (flat index f = i CH + el, record i, element e0 + el), staged
+      // in LDS, then each element summed over the records in slice order
+      const int CH = (REC + G - 1) / G;
+      const int e0 = j * CH, cnt = min(CH, REC - e0), nflat = G * CH;
+      // i = f / CH as umulhi(f, M), exact for f, CH < 2^16
+      const unsigned M = 0xffffffffu / (unsigned)CH + 1u;
+      const Rsrc ph = __builtin_amdgcn_make_buffer_rsrc(prec, 0, G * REC * 4, 0x00020000);
+      constexpr int IT = (REC + 63 + PNT - 1) / PNT;  // G CH < REC + G <= REC + 64
+      float* stage = reinterpret_cast<float*>(dyn_smem + 256);  // past the flag
+      static_assert(256 + 4 * (REC + 64) <= 2 * C::RING, "staging fits the ring");
+      float x[IT];
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const unsigned f = threadIdx.x + PNT * it;
+        const unsigned i = __umulhi(f, M), el = f - i * CH;
+        const bool on = (int)f < nflat && (int)el < cnt;
+        x[it] = __builtin_bit_cast(
+            float, __builtin_amdgcn_raw_buffer_load_b32(ph, on ? 4 * (i * REC + e0 + el) : OOB,
+                                                        0, 0));
+      }
+#pragma unroll
+      for (int it = 0; it < IT; ++it) {
+        const int f = threadIdx.x + PNT * it;
+        if (f < nflat) stage[f] = x[it];
+      }
+      __syncthreads();
+      for (int el = threadIdx.x; el < cnt; el += PNT) {
+        float sum = 0.f;
+#pragma unroll 8
+        for (int i = 0; i < G; ++i) sum += stage[i * CH + el];
+        trec[e0 + el] = sum;
+      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (threadIdx.x == 0) put_stamp(st + 2 * j + 1, mine);
+      ok = wait_stamps(st, 1, G, epoch, mine, spin_limit, s_flag);
+    } else if (exchange && threadIdx.x == 0) {
+      // peers waiting for this workgroup's sum stop waiting
+      put_stamp(st + 2 * j + 1, (epoch << 8) | kGaveUp);
+    }
+    if (ok) {
+      PairFrags<D, R> fr;
+      fr.load(trec);
+      fr.store(sf, zo);
+    } else {
+      // the slice's total from K and V in memory: each tile's partial state
+      // as its own workgroup forms it, added in slice order
+      f32x4 tacc[R][NB + 1];
+#pragma unroll
+      for (int l = 0; l < R; ++l)
+#pragma unroll
+        for (int eb = 0; eb <= NB; ++eb) tacc[l][eb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int i = 0; i < G; ++i) {
+        RowsCopy<D, PTM, PNT> fk, fv;
+        fk.load(kh, i * PTM, true);
+        fv.load(vh, i * PTM, true);
+        __syncthreads();  // the ring is free (the previous tile's products are done)
+        auto slot = [](int jj) { return jj; };
+        fk.store(kr, slot);
+        fv.store(vr, slot);
+        __syncthreads();
+        if (w < NB) {
+          f32x4 pacc[R][NB + 1];
+          tile_state<D, R>(kr, vr, 0, i * PTM, N, ro, w, pacc);
+#pragma unroll
+          for (int l = 0; l < R; ++l)
+#pragma unroll
+            for (int eb = 0; eb <= NB; ++eb) tacc[l][eb] += pacc[l][eb];
+        }
+      }
+      __syncthreads();
+      float* lrec = reinterpret_cast<float*>(dyn_smem);
+      if (w < NB) store_record_block<D, R>(lrec, w, tacc);
+      __syncthreads();
+      PairFrags<D, R> fr;
+      fr.load(lrec);
+      fr.store(sf, zo);
+    }
+    __syncthreads();  // the fragments are in place
+  };
+  const int i0 = t0 + 32 * w;
+  const bool exact = band_k == 32 * KC && t0 - band_k >= 0 && t0 + PTM - 1 + band_k < N;
+  if (exact)
+    pair_tile<D, R, KC, false, true>(oh, i0, N, band_k, scale2, sn, sfw, qo, kr, vr, w, ro, sf,
+                                     zo, publish, pre_far);
+  else
+    pair_tile<D, R, KC, true, true>(oh, i0, N, band_k, scale2, sn, sfw, qo, kr, vr, w, ro, sf,
+                                    zo, publish, pre_far);
+}
+
+template <int D, int R, int KC>
+hipError_t launch_fused_kc(const LaunchArgs& a, Launcher& L, float scale2) {
+  using C = PairCfg<D, R, KC>;
+  static std::atomic<unsigned long long> lds_set{0};
+  if (L.note(lds_limit_once((const void*)k_band_fused<D, R, KC>, C::LDS, lds_set)) !=
+      hipSuccess)
+    return L.err;
+  const int BH = a.B * a.H, G = a.fused_g;
+  const FusedLayout f = fused_layout(BH, G, R * D * (D + 1));
+  // (integer arithmetic: the dry pass runs with no workspace yet)
+  const uintptr_t ws = reinterpret_cast<uintptr_t>(a.ws);
+  L(FMM_KERNEL_BAND_APPLY, k_band_fused<D, R, KC>, dim3(BH * G), dim3(PNT), (size_t)C::LDS,
+    (hipStream_t)a.stream, (const bf16_t*)a.q, (const bf16_t*)a.k, (const bf16_t*)a.v,
+    (bf16_t*)a.out, reinterpret_cast<float*>(ws + f.off_part),
+    reinterpret_cast<float*>(ws + f.off_tot),
+    reinterpret_cast<unsigned long long*>(ws + f.off_stamp), a.w_near, a.w_far, a.H, a.N,
+    a.band_k, G, scale2, a.epoch, kFusedSpinLimit, a.exchange);
+  return L.err;
+}
+
 template <int D, int R, int KC>
 hipError_t launch_pair_kc(const LaunchArgs& a, Launcher& L, const float* fin,
                           float scale2) {
@@ -420,7 +787,35 @@ bool band_pair_applies(int dtype, int d, int band_k, int causal, long long n) {
          n * d * 2 < (1LL << 31);
 }
 
+int fused_groups(int dtype, int d, int band_k, int rank, int causal, long long bh, long long n,
+                 int max_workgroups) {
+  // one or two maps (the pair kernel's tile); B*H a multiple of 8, so that
+  // each slice's workgroups share an XCD; at most 64 tiles per slice (one
+  // wave polls the stamps); every workgroup resident at once (two per CU)
+  if (!band_pair_applies(dtype, d, band_k, causal, n) || rank > 2 || bh % 8 != 0 || n < 1)
+    return 0;
+  const long long G = (n + PTM - 1) / PTM;
+  if (G > 64 || bh * G > max_workgroups) return 0;
+  return (int)G;
+}
+
 int pair_tile_rows() { return PTM; }
+
+hipError_t launch_band_fused(const LaunchArgs& a, Launcher& t) {
+  const float scale2 = 1.4426950408889634f / sqrtf((float)a.d);
+  const bool kc1 = a.band_k <= 32;
+  switch (a.d * 4 + a.rank) {
+    case 32 * 4 + 1:
+      return kc1 ? launch_fused_kc<32, 1, 1>(a, t, scale2) : launch_fused_kc<32, 1, 2>(a, t, scale2);
+    case 32 * 4 + 2:
+      return kc1 ? launch_fused_kc<32, 2, 1>(a, t, scale2) : launch_fused_kc<32, 2, 2>(a, t, scale2);
+    case 64 * 4 + 1:
+      return kc1 ? launch_fused_kc<64, 1, 1>(a, t, scale2) : launch_fused_kc<64, 1, 2>(a, t, scale2);
+    case 64 * 4 + 2:
+      return kc1 ? launch_fused_kc<64, 2, 1>(a, t, scale2) : launch_fused_kc<64, 2, 2>(a, t, scale2);
+    default: return t.note(hipErrorInvalidValue);
+  }
+}
 
 hipError_t launch_band_pair(const LaunchArgs& a, Launcher& t, const float* fin) {
   const float scale2 = 1.4426950408889634f / sqrtf((float)a.d);

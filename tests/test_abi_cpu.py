@@ -30,7 +30,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings_and_version():
-    assert binding.version() == 10100
+    assert binding.version() == 10200
     for st in (0, -1, -2, -3, -4, -5):
         assert binding.status_string(st).startswith(
             {0: "FMM_OK", -1: "FMM_ERR_INVALID_ARG", -2: "FMM_ERR_UNSUPPORTED",
@@ -83,7 +83,9 @@ def test_host_validation(kwargs, status):
 def test_timing_read_rejects_bad_kernel_id():
     lib = binding.lib()
     ms, n = ctypes.c_double(), ctypes.c_longlong()
-    assert lib.fmm_attn_kernel_timing_read(9, ctypes.byref(ms), ctypes.byref(n)) == -1
+    # ids run from 0 to FMM_KERNEL_COUNT - 1 (10 kernels)
+    assert lib.fmm_attn_kernel_timing_read(10, ctypes.byref(ms), ctypes.byref(n)) == -1
+    assert lib.fmm_attn_kernel_timing_read(-1, ctypes.byref(ms), ctypes.byref(n)) == -1
 
 
 def test_binding_rejects_host_tensors_and_wrong_rank():
@@ -149,3 +151,24 @@ def test_forward_ex_rejects_unknown_normalisation():
     assert lib.fmm_attn_forward_ex(*args(2)) == binding.FMM_ERR_INVALID_ARG
     assert lib.fmm_attn_forward_ex(*args(-1)) == binding.FMM_ERR_INVALID_ARG
     assert lib.fmm_attn_forward_ex(*args(0, 7)) == binding.FMM_ERR_UNSUPPORTED
+
+
+def test_one_launch_knob_and_workspace():
+    # the mode is process-wide: 0 never, 1 where it applies (default), 2
+    # without the exchange; anything else is refused and changes nothing
+    prev = binding.set_one_launch(1)
+    try:
+        assert prev == 1
+        with pytest.raises(ValueError):
+            binding.set_one_launch(3)
+        assert binding.set_one_launch(2) == 1
+        assert binding.set_one_launch(0) == 2
+    finally:
+        binding.set_one_launch(prev)
+    # the workspace covers the one-launch path: per slice G = ceil(N / 128)
+    # partial records, one total and 2 G stamps of 8 bytes (each part
+    # 256-byte aligned); the N = 4096, B*H = 16, d = 32 shape qualifies
+    rec = 2 * 32 * 33 * 4
+    al = lambda x: (x + 255) // 256 * 256
+    need = al(16 * 32 * rec) + al(16 * rec) + al(16 * 32 * 2 * 8)
+    assert binding.workspace_bytes(8, 2, 4096, 32, 2, 0) >= need
