@@ -51,10 +51,13 @@ __device__ __forceinline__ uint32_t pk_max_bf16_nonneg(uint32_t a, uint32_t b) {
   return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s16x2, a),
                                                                 __builtin_bit_cast(s16x2, b)));
 }
-// phi_1 and phi_2 of eight values: one e = exp(-|x|) serves both maps, and
-// the max identities of phi12 are taken on the rounded pairs (1 + x, 1 - x
-// and e packed to bf16 first; e >= +0), which gives the same bits as
-// rounding max(1 + x, e) and max(1 - x, e).
+// phi_1 and phi_2 of eight values.  Of the two numbers 1 + |x| and
+// e = exp(-|x|), phi_1(x) = elu(x) + 1 takes 1 + |x| for x >= 0 and e for
+// x < 0, phi_2(x) = elu(-x) + 1 the other one (both are 1 at x = 0).  Both are
+// packed to bf16 (the same bits as rounding phi_1, phi_2 themselves), and each
+// 16-bit half is picked by the sign bit of its input: a byte permute whose
+// selectors 8 and 9 replicate bits 15 and 31 turns the two signs into
+// half-word masks, a bit-select per map does the rest.
 __device__ __forceinline__ void phi_oct(const Oct& x, Oct& p1, Oct& p2) {
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
   uint32_t a[4], b[4];
@@ -62,8 +65,11 @@ __device__ __forceinline__ void phi_oct(const Oct& x, Oct& p1, Oct& p2) {
   for (int i = 0; i < 4; ++i) {
     const float lo = __uint_as_float(w[i] << 16), hi = __uint_as_float(w[i] & 0xffff0000u);
     const uint32_t e = pack_bf16x2(__expf(-fabsf(lo)), __expf(-fabsf(hi)));
-    a[i] = pk_max_bf16_nonneg(pack_bf16x2(1.f + lo, 1.f + hi), e);
-    b[i] = pk_max_bf16_nonneg(pack_bf16x2(1.f - lo, 1.f - hi), e);
+    const uint32_t o = pack_bf16x2(1.f + fabsf(lo), 1.f + fabsf(hi));
+    // 0xffff in each half whose input has its sign bit set
+    const uint32_t m = __builtin_amdgcn_perm(0u, w[i], 0x09090808u);
+    a[i] = (e & m) | (o & ~m);
+    b[i] = (o & m) | (e & ~m);
   }
   p1 = make_uint4(a[0], a[1], a[2], a[3]);
   p2 = make_uint4(b[0], b[1], b[2], b[3]);
