@@ -57,7 +57,10 @@ struct BwdCfg {
   static constexpr int BUDGET = 150 * 1024;
   // the far-field records of up to three maps, kept in LDS for widths up to
   // 64 (read every tile; the causal ones are also advanced there)
-  static constexpr int REC_BYTES = D <= 64 ? 3 * D * (D + 1) * 4 : 0;
+  // (fp32 records, or their bf16 fragments: RecFrags::PER_MAP per map)
+  static constexpr int REC_F32 = 3 * D * (D + 1) * 4;
+  static constexpr int REC_FRAG = 3 * (2 * (D / 16) * (D / 16) * 64 * 8 + (D / 16) * 32 + D * 4);
+  static constexpr int REC_BYTES = D <= 64 ? (REC_F32 > REC_FRAG ? REC_F32 : REC_FRAG) : 0;
   static constexpr int UR_FIT =
       (BUDGET - 2 * TILE - 256 - 2 * NT * 4 - REC_BYTES) / (UNIT2 + STAT_UNIT);
   static constexpr int UR = UR_FIT > 8 ? 8 : UR_FIT;
@@ -160,6 +163,64 @@ __device__ __forceinline__ typename QuadOf<T>::type to_quad(const f32x4& x) {
   const float f[4] = {x[0], x[1], x[2], x[3]};
   return f32_to_quad<T>(f);
 }
+
+// bf16 operands of a constant record (the non-causal forward state and dS
+// total), built once per workgroup in LDS so that every later use is one
+// 8-byte read with no conversion.  Per map l, at l * PER_MAP bytes:
+//   A[(cb * NB + nb) * 64 + lane] = rec_quad of tile (cb, nb) (lane's row of
+//                                   the tile's quad layout)
+//   B[(cb * NB + eb) * 64 + lane] = rec_quad_t of tile (cb, eb)
+//   Z[cb * 4 + g]                 = rec_quad of z[16cb + 4g .. +3]
+//   zf[D]                         = z in fp32
+template <int D>
+struct RecFrags {
+  static constexpr int NB = D / 16;
+  static constexpr int A_OFF = 0, B_OFF = NB * NB * 64 * 8, Z_OFF = 2 * NB * NB * 64 * 8,
+                       ZF_OFF = Z_OFF + NB * 4 * 8;
+  static constexpr int PER_MAP = ZF_OFF + D * 4;
+  // from the fp32 record (tile order, rank maps) in global memory; the
+  // caller synchronises before the first read
+  __device__ __forceinline__ static void build(unsigned char* base, const float* rec, int rank) {
+    const int nq = rank * NB * NB * 64;
+    for (int t = threadIdx.x; t < nq; t += NT) {
+      const int l = t / (NB * NB * 64), x = t % (NB * NB * 64), ln = x & 63, tile = x >> 6;
+      const int cb = tile / NB, eb = tile % NB, r = ln & 15, g = ln >> 4;
+      const float* rl = rec + (size_t)l * D * (D + 1);
+      unsigned char* ml = base + l * PER_MAP;
+      const float4 a = *reinterpret_cast<const float4*>(rl + (tile * 64 + ln) * 4);
+      const float fa[4] = {a.x, a.y, a.z, a.w};
+      const float* pb = rl + ((cb * NB + eb) * 64 + 16 * (r >> 2) + 4 * g) * 4 + (r & 3);
+      const float fb[4] = {pb[0], pb[4], pb[8], pb[12]};
+      reinterpret_cast<uint2*>(ml + A_OFF)[x] = f32_to_quad<bf16_t>(fa);
+      reinterpret_cast<uint2*>(ml + B_OFF)[x] = f32_to_quad<bf16_t>(fb);
+    }
+    for (int t = threadIdx.x; t < rank * D; t += NT) {
+      const int l = t / D, c = t % D;
+      const float zv = rec[(size_t)l * D * (D + 1) + D * D + c];
+      reinterpret_cast<float*>(base + l * PER_MAP + ZF_OFF)[c] = zv;
+      if ((c & 3) == 0) {
+        const float* zp = rec + (size_t)l * D * (D + 1) + D * D + c;
+        const float fz[4] = {zp[0], zp[1], zp[2], zp[3]};
+        reinterpret_cast<uint2*>(base + l * PER_MAP + Z_OFF)[c >> 2] = f32_to_quad<bf16_t>(fz);
+      }
+    }
+  }
+  __device__ __forceinline__ static uint2 a(const unsigned char* base, int l, int cb, int nb) {
+    return reinterpret_cast<const uint2*>(base + l * PER_MAP + A_OFF)[(cb * NB + nb) * 64 +
+                                                                       (threadIdx.x & 63)];
+  }
+  __device__ __forceinline__ static uint2 b(const unsigned char* base, int l, int cb, int eb) {
+    return reinterpret_cast<const uint2*>(base + l * PER_MAP + B_OFF)[(cb * NB + eb) * 64 +
+                                                                       (threadIdx.x & 63)];
+  }
+  __device__ __forceinline__ static uint2 z(const unsigned char* base, int l, int cb) {
+    return reinterpret_cast<const uint2*>(base + l * PER_MAP + Z_OFF)[cb * 4 +
+                                                                       ((threadIdx.x & 63) >> 4)];
+  }
+  __device__ __forceinline__ static const float* zf(const unsigned char* base, int l) {
+    return reinterpret_cast<const float*>(base + l * PER_MAP + ZF_OFF);
+  }
+};
 
 // rec_l += phi(X)^T [Y | y] over the 64 staged rows: px holds phi of the rows
 // (stride ST), py the second factor's rows, ycol (64 floats) the extra column
@@ -283,8 +344,12 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
   const size_t base = (size_t)bh * N * D;
   const size_t REC = (size_t)rank * D * (D + 1);
   float* grec = CAUSAL ? recs + ((size_t)bh * nseg + seg) * REC : recs + (size_t)bh * REC;
+  // the non-causal record is constant: its bf16 operands are built once
+  constexpr bool FR = !CAUSAL && sizeof(T) == 2 && C::REC_BYTES > 0;
+  unsigned char* frb = dyn_smem + C::REC_OFF;
   float* srec = reinterpret_cast<float*>(dyn_smem + C::REC_OFF);
-  if constexpr (C::REC_BYTES > 0) stage_records(srec, grec, (int)REC);
+  if constexpr (FR) RecFrags<D>::build(frb, grec, rank);
+  else if constexpr (C::REC_BYTES > 0) stage_records(srec, grec, (int)REC);
   float* rec = C::REC_BYTES > 0 ? srec : grec;  // (the first tile's barriers order the copy)
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const float tau = scale2 * 0.69314718055994531f;  // 1/sqrt(d)
@@ -409,13 +474,19 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
       for (int nb = 0; nb < NB; ++nb) {
         Q a[NB];
 #pragma unroll
-        for (int cb = 0; cb < NB; ++cb) a[cb] = rec_quad<T>(rl + ((cb * NB + nb) * 64 + lane) * 4);
+        for (int cb = 0; cb < NB; ++cb) {
+          if constexpr (FR) a[cb] = RecFrags<D>::a(frb, l, cb, nb);
+          else a[cb] = rec_quad<T>(rl + ((cb * NB + nb) * 64 + lane) * 4);
+        }
         num[nb] = contract<NB>(a, pq, num[nb]);
       }
       {
         Q zq[NB];
 #pragma unroll
-        for (int cb = 0; cb < NB; ++cb) zq[cb] = rec_quad<T>(rl + D * D + 16 * cb + 4 * g);
+        for (int cb = 0; cb < NB; ++cb) {
+          if constexpr (FR) zq[cb] = RecFrags<D>::z(frb, l, cb);
+          else zq[cb] = rec_quad<T>(rl + D * D + 16 * cb + 4 * g);
+        }
         num[NB] = contract<NB>(zq, pq, num[NB]);
       }
       // quotient rule
@@ -474,12 +545,16 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
       for (int cb = 0; cb < NB; ++cb) {
         Q a[NB];
 #pragma unroll
-        for (int eb = 0; eb < NB; ++eb) a[eb] = rec_quad_t<T>(rl, NB, cb, eb);
+        for (int eb = 0; eb < NB; ++eb) {
+          if constexpr (FR) a[eb] = RecFrags<D>::b(frb, l, cb, eb);
+          else a[eb] = rec_quad_t<T>(rl, NB, cb, eb);
+        }
         dph[cb] = contract<NB>(a, dnq, dph[cb]);
       }
+      const float* zl = FR ? RecFrags<D>::zf(frb, l) : rl + D * D;
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
-        const float4 z = *reinterpret_cast<const float4*>(rl + D * D + 16 * cb + 4 * g);
+        const float4 z = *reinterpret_cast<const float4*>(zl + 16 * cb + 4 * g);
         const float zf[4] = {z.x, z.y, z.z, z.w};
         float x[4];
         quad_to_f32(qq[cb], x);
@@ -713,8 +788,12 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
   const size_t base = (size_t)bh * N * D;
   const size_t REC = (size_t)rank * D * (D + 1);
   float* gdrec = CAUSAL ? drecs + ((size_t)bh * nseg + seg) * REC : drecs + (size_t)bh * REC;
+  // the non-causal dS total is constant: its bf16 operands are built once
+  constexpr bool FR = !CAUSAL && sizeof(T) == 2 && C::REC_BYTES > 0;
+  unsigned char* frb = dyn_smem + C::REC_OFF;
   float* sdrec = reinterpret_cast<float*>(dyn_smem + C::REC_OFF);
-  if constexpr (C::REC_BYTES > 0) stage_records(sdrec, gdrec, (int)REC);
+  if constexpr (FR) RecFrags<D>::build(frb, gdrec, rank);
+  else if constexpr (C::REC_BYTES > 0) stage_records(sdrec, gdrec, (int)REC);
   float* drec = C::REC_BYTES > 0 ? sdrec : gdrec;  // (the first tile's barriers order the copy)
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const float tau = scale2 * 0.69314718055994531f;
@@ -894,20 +973,26 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
       for (int cb = 0; cb < NB; ++cb) {
         Q a[NB];
 #pragma unroll
-        for (int eb = 0; eb < NB; ++eb) a[eb] = rec_quad_t<T>(drl, NB, cb, eb);
+        for (int eb = 0; eb < NB; ++eb) {
+          if constexpr (FR) a[eb] = RecFrags<D>::b(frb, l, cb, eb);
+          else a[eb] = rec_quad_t<T>(drl, NB, cb, eb);
+        }
         dph[cb] = contract<NB>(a, vq, dph[cb]);
       }
 #pragma unroll
       for (int eb = 0; eb < NB; ++eb) {
         Q a[NB];
 #pragma unroll
-        for (int cb = 0; cb < NB; ++cb)
-          a[cb] = rec_quad<T>(drl + ((cb * NB + eb) * 64 + lane) * 4);
+        for (int cb = 0; cb < NB; ++cb) {
+          if constexpr (FR) a[cb] = RecFrags<D>::a(frb, l, cb, eb);
+          else a[cb] = rec_quad<T>(drl + ((cb * NB + eb) * 64 + lane) * 4);
+        }
         dva[eb] = contract<NB>(a, pk, dva[eb]);
       }
+      const float* zl = FR ? RecFrags<D>::zf(frb, l) : drl + D * D;
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
-        const float4 z = *reinterpret_cast<const float4*>(drl + D * D + 16 * cb + 4 * g);
+        const float4 z = *reinterpret_cast<const float4*>(zl + 16 * cb + 4 * g);
         const float zf[4] = {z.x, z.y, z.z, z.w};
         float x[4];
         quad_to_f32(kq[cb], x);
