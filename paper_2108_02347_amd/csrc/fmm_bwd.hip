@@ -47,7 +47,10 @@
 namespace fmm {
 namespace {
 
-template <typename T, int D>
+// FC: causal with at most two maps, whose records are kept twice: in fp32
+// (advanced every tile) and as bf16 operands (RecFrags, rebuilt by the
+// owning wave after each advance).
+template <typename T, int D, bool FC = false>
 struct BwdCfg {
   static constexpr int ST = D + Lay<T>::PAD;
   static constexpr int ROW = ST * (int)sizeof(T);
@@ -57,10 +60,15 @@ struct BwdCfg {
   static constexpr int BUDGET = 150 * 1024;
   // the far-field records of up to three maps, kept in LDS for widths up to
   // 64 (read every tile; the causal ones are also advanced there)
-  // (fp32 records, or their bf16 fragments: RecFrags::PER_MAP per map)
+  // (fp32 records, or their bf16 fragments: RecFrags::PER_MAP per map; both
+  // for two maps with FC)
+  static constexpr int FRAG_MAP = 2 * (D / 16) * (D / 16) * 64 * 8 + (D / 16) * 32 + D * 4;
   static constexpr int REC_F32 = 3 * D * (D + 1) * 4;
-  static constexpr int REC_FRAG = 3 * (2 * (D / 16) * (D / 16) * 64 * 8 + (D / 16) * 32 + D * 4);
-  static constexpr int REC_BYTES = D <= 64 ? (REC_F32 > REC_FRAG ? REC_F32 : REC_FRAG) : 0;
+  static constexpr int REC_FRAG = 3 * FRAG_MAP;
+  static constexpr int REC_BYTES =
+      D > 64 ? 0 : FC ? 2 * D * (D + 1) * 4 + 2 * FRAG_MAP : (REC_F32 > REC_FRAG ? REC_F32 : REC_FRAG);
+  // offset of the fragments within the record area
+  static constexpr int FRAG_OFF = FC ? 2 * D * (D + 1) * 4 : 0;
   static constexpr int UR_FIT =
       (BUDGET - 2 * TILE - 256 - 2 * NT * 4 - REC_BYTES) / (UNIT2 + STAT_UNIT);
   static constexpr int UR = UR_FIT > 8 ? 8 : UR_FIT;
@@ -225,9 +233,14 @@ struct RecFrags {
 // rec_l += phi(X)^T [Y | y] over the 64 staged rows: px holds phi of the rows
 // (stride ST), py the second factor's rows, ycol (64 floats) the extra column
 // that lands in z; wave w updates feature blocks w, w + 4, ...
+//
+// With frl (bf16 only), the wave also rebuilds the RecFrags operands of its
+// blocks from the updated tiles (A and Z from its registers, B read back
+// transposed from the tiles it has just stored).
 template <typename T, int D>
 __device__ __forceinline__ void record_add(float* rl, const T* px, const T* py,
-                                           const float* ycol, int ST, int w) {
+                                           const float* ycol, int ST, int w,
+                                           unsigned char* frl = nullptr) {
   using Q = typename QuadOf<T>::type;
   constexpr int NB = D / 16;
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
@@ -258,6 +271,19 @@ __device__ __forceinline__ void record_add(float* rl, const T* px, const T* py,
     for (int eb = 0; eb < NB; ++eb)
       *reinterpret_cast<f32x4*>(rl + ((cb * NB + eb) * 64 + lane) * 4) = acc[eb];
     if (r == 0) *reinterpret_cast<f32x4*>(rl + D * D + 16 * cb + 4 * g) = acc[NB];
+    if constexpr (sizeof(T) == 2) {
+      if (frl) {
+        using RF = RecFrags<D>;
+#pragma unroll
+        for (int eb = 0; eb < NB; ++eb) {
+          reinterpret_cast<uint2*>(frl + RF::A_OFF)[(cb * NB + eb) * 64 + lane] =
+              to_quad<bf16_t>(acc[eb]);
+          reinterpret_cast<uint2*>(frl + RF::B_OFF)[(cb * NB + eb) * 64 + lane] =
+              rec_quad_t<bf16_t>(rl, NB, cb, eb);
+        }
+        if (r == 0) reinterpret_cast<uint2*>(frl + RF::Z_OFF)[cb * 4 + g] = to_quad<bf16_t>(acc[NB]);
+      }
+    }
   }
 }
 
@@ -320,7 +346,7 @@ __device__ __forceinline__ void near_dq_units(f32x4* dq, const typename QuadOf<T
   mfma_drain();
 }
 
-template <typename T, int D, bool CAUSAL>
+template <typename T, int D, bool CAUSAL, bool FC>
 __global__ __launch_bounds__(NT) void k_bwd_rows(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, T* __restrict__ dq, float* __restrict__ recs,
@@ -328,7 +354,7 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
     float* __restrict__ dwpart, const float* __restrict__ w_near, const float* __restrict__ w_far,
     int H, int N, int band_k, int L, int nseg, int rank, float scale2) {
   using Q = typename QuadOf<T>::type;
-  using C = BwdCfg<T, D>;
+  using C = BwdCfg<T, D, FC>;
   constexpr int NB = D / 16, ST = C::ST;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
   T* sk = reinterpret_cast<T*>(dyn_smem);
@@ -344,12 +370,14 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
   const size_t base = (size_t)bh * N * D;
   const size_t REC = (size_t)rank * D * (D + 1);
   float* grec = CAUSAL ? recs + ((size_t)bh * nseg + seg) * REC : recs + (size_t)bh * REC;
-  // the non-causal record is constant: its bf16 operands are built once
-  constexpr bool FR = !CAUSAL && sizeof(T) == 2 && C::REC_BYTES > 0;
-  unsigned char* frb = dyn_smem + C::REC_OFF;
+  // bf16 operands of the record: the non-causal record is constant and they
+  // are built once; the causal one (FC) keeps its fp32 copy too and the
+  // operands follow each advance
+  constexpr bool FR = (!CAUSAL || FC) && sizeof(T) == 2 && C::REC_BYTES > 0;
+  unsigned char* frb = dyn_smem + C::REC_OFF + C::FRAG_OFF;
   float* srec = reinterpret_cast<float*>(dyn_smem + C::REC_OFF);
   if constexpr (FR) RecFrags<D>::build(frb, grec, rank);
-  else if constexpr (C::REC_BYTES > 0) stage_records(srec, grec, (int)REC);
+  if constexpr (C::REC_BYTES > 0 && (!FR || CAUSAL)) stage_records(srec, grec, (int)REC);
   float* rec = C::REC_BYTES > 0 ? srec : grec;  // (the first tile's barriers order the copy)
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const float tau = scale2 * 0.69314718055994531f;  // 1/sqrt(d)
@@ -551,7 +579,7 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
         }
         dph[cb] = contract<NB>(a, dnq, dph[cb]);
       }
-      const float* zl = FR ? RecFrags<D>::zf(frb, l) : rl + D * D;
+      const float* zl = FR && !CAUSAL ? RecFrags<D>::zf(frb, l) : rl + D * D;
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
         const float4 z = *reinterpret_cast<const float4*>(zl + 16 * cb + 4 * g);
@@ -578,7 +606,8 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
           float* ones_col = dden_s;
           if (threadIdx.x < 64) ones_col[threadIdx.x] = 1.f;
           __syncthreads();
-          record_add<T, D>(rl, tb1, vt, ones_col, ST, w);
+          record_add<T, D>(rl, tb1, vt, ones_col, ST, w,
+                           FR ? frb + l * RecFrags<D>::PER_MAP : nullptr);
         }
       }
     }
@@ -764,7 +793,7 @@ void launch_seg_grad(const BwdArgs& a, Launcher& L) {
 }
 
 // ------------------------------------------------------------------ key pass
-template <typename T, int D, bool CAUSAL>
+template <typename T, int D, bool CAUSAL, bool FC>
 __global__ __launch_bounds__(NT) void k_bwd_keys(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ drecs,
@@ -772,7 +801,7 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
     const float* __restrict__ w_near, const float* __restrict__ w_far, int H, int N, int band_k,
     int L, int nseg, int rank, float scale2) {
   using Q = typename QuadOf<T>::type;
-  using C = BwdCfg<T, D>;
+  using C = BwdCfg<T, D, FC>;
   constexpr int NB = D / 16, ST = C::ST;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
   T* sq = reinterpret_cast<T*>(dyn_smem);
@@ -788,12 +817,12 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
   const size_t base = (size_t)bh * N * D;
   const size_t REC = (size_t)rank * D * (D + 1);
   float* gdrec = CAUSAL ? drecs + ((size_t)bh * nseg + seg) * REC : drecs + (size_t)bh * REC;
-  // the non-causal dS total is constant: its bf16 operands are built once
-  constexpr bool FR = !CAUSAL && sizeof(T) == 2 && C::REC_BYTES > 0;
-  unsigned char* frb = dyn_smem + C::REC_OFF;
+  // bf16 operands of the dS record, as in the row pass
+  constexpr bool FR = (!CAUSAL || FC) && sizeof(T) == 2 && C::REC_BYTES > 0;
+  unsigned char* frb = dyn_smem + C::REC_OFF + C::FRAG_OFF;
   float* sdrec = reinterpret_cast<float*>(dyn_smem + C::REC_OFF);
   if constexpr (FR) RecFrags<D>::build(frb, gdrec, rank);
-  else if constexpr (C::REC_BYTES > 0) stage_records(sdrec, gdrec, (int)REC);
+  if constexpr (C::REC_BYTES > 0 && (!FR || CAUSAL)) stage_records(sdrec, gdrec, (int)REC);
   float* drec = C::REC_BYTES > 0 ? sdrec : gdrec;  // (the first tile's barriers order the copy)
   const float sn = sigmoidf_exact(w_near[h]), sfw = sigmoidf_exact(w_far[h]);
   const float tau = scale2 * 0.69314718055994531f;
@@ -989,7 +1018,7 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
         }
         dva[eb] = contract<NB>(a, pk, dva[eb]);
       }
-      const float* zl = FR ? RecFrags<D>::zf(frb, l) : drl + D * D;
+      const float* zl = FR && !CAUSAL ? RecFrags<D>::zf(frb, l) : drl + D * D;
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
         const float4 z = *reinterpret_cast<const float4*>(zl + 16 * cb + 4 * g);
@@ -1013,7 +1042,8 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
         // segment's first tile (the last one walked)
         if (tt + 1 < ntile) {
           __syncthreads();  // every wave has read record l for this tile
-          record_add<T, D>(drl, tb1, tb2, dden_s, ST, w);
+          record_add<T, D>(drl, tb1, tb2, dden_s, ST, w,
+                           FR ? frb + l * RecFrags<D>::PER_MAP : nullptr);
         }
       }
     }
@@ -1040,13 +1070,13 @@ __global__ void k_dw_reduce(const float* __restrict__ dwpart, const float* __res
   dw_far[h] = c * (1.f - c) * sf;
 }
 
-template <typename T, int D, bool CAUSAL>
-hipError_t launch_bwd_dc(const BwdArgs& a, Launcher& L) {
-  using C = BwdCfg<T, D>;
+template <typename T, int D, bool CAUSAL, bool FC>
+hipError_t launch_bwd_dcf(const BwdArgs& a, Launcher& L) {
+  using C = BwdCfg<T, D, FC>;
   static std::atomic<unsigned long long> set_rows{0}, set_keys{0};
-  if (L.note(lds_limit_once((const void*)k_bwd_rows<T, D, CAUSAL>, C::LDS, set_rows)) !=
+  if (L.note(lds_limit_once((const void*)k_bwd_rows<T, D, CAUSAL, FC>, C::LDS, set_rows)) !=
           hipSuccess ||
-      L.note(lds_limit_once((const void*)k_bwd_keys<T, D, CAUSAL>, C::LDS, set_keys)) !=
+      L.note(lds_limit_once((const void*)k_bwd_keys<T, D, CAUSAL, FC>, C::LDS, set_keys)) !=
           hipSuccess)
     return L.err;
   const float scale2 = 1.4426950408889634f / sqrtf((float)D);
@@ -1054,7 +1084,7 @@ hipError_t launch_bwd_dc(const BwdArgs& a, Launcher& L) {
   const size_t REC = (size_t)a.rank * D * (D + 1);
   hipStream_t s = (hipStream_t)a.stream;
   const dim3 grid(BH * a.nseg);
-  L(FMM_KERNEL_BWD_ROWS, k_bwd_rows<T, D, CAUSAL>, grid, dim3(NT), (size_t)C::LDS, s,
+  L(FMM_KERNEL_BWD_ROWS, k_bwd_rows<T, D, CAUSAL, FC>, grid, dim3(NT), (size_t)C::LDS, s,
     (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, (T*)a.dq,
     CAUSAL ? a.part : a.fin, a.rowstat, a.rowfar, a.dwpart, a.w_near, a.w_far, a.H, a.N,
     a.band_k, a.L, a.nseg, a.rank, scale2);
@@ -1067,7 +1097,7 @@ hipError_t launch_bwd_dc(const BwdArgs& a, Launcher& L) {
   } else {
     (void)launch_state_sum(L, a.dpart, a.dfin, a.nseg, (int)REC, BH, s);
   }
-  L(FMM_KERNEL_BWD_KEYS, k_bwd_keys<T, D, CAUSAL>, grid, dim3(NT), (size_t)C::LDS, s,
+  L(FMM_KERNEL_BWD_KEYS, k_bwd_keys<T, D, CAUSAL, FC>, grid, dim3(NT), (size_t)C::LDS, s,
     (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, (T*)a.dk, (T*)a.dv,
     CAUSAL ? a.dpart : a.dfin, (const float*)a.rowstat, (const float*)a.rowfar, a.w_near, a.w_far,
     a.H, a.N, a.band_k, a.L, a.nseg, a.rank, scale2);
@@ -1078,7 +1108,12 @@ hipError_t launch_bwd_dc(const BwdArgs& a, Launcher& L) {
 
 template <typename T, int D>
 hipError_t launch_bwd_d(const BwdArgs& a, Launcher& L) {
-  return a.causal ? launch_bwd_dc<T, D, true>(a, L) : launch_bwd_dc<T, D, false>(a, L);
+  if (!a.causal) return launch_bwd_dcf<T, D, false, false>(a, L);
+  // causal bf16 with at most two maps keeps bf16 operands of its records
+  if constexpr (sizeof(T) == 2 && D <= 64) {
+    if (a.rank <= 2) return launch_bwd_dcf<T, D, true, true>(a, L);
+  }
+  return launch_bwd_dcf<T, D, true, false>(a, L);
 }
 
 template <typename T>
