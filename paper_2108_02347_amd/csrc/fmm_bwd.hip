@@ -846,6 +846,10 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
     // ---- near field over the rows whose band holds the strip's keys
     const int ra = CAUSAL ? t0 : (max(0, t0 - band_k) >> 5) << 5;
     const int rb = (min(N, t0 + TM + band_k) + 31) & ~31;
+    // causal, one staging round of at least the tile's 64 rows: the staged
+    // rows start with the tile's own rows t0 .. t0+63 (zero at or beyond N),
+    // which the far part reads again
+    const bool staged_tile = CAUSAL && rb - ra <= C::WK && rb - ra >= TM;
     for (int rs = ra; rs < rb; rs += C::WK) {
       const int nrow = min(C::WK, rb - rs);
       __syncthreads();
@@ -922,7 +926,7 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
         // the tile's rows: phi_l(q) into tb1, dnum = c g / den into tb2,
         // dden into dden_s
         __syncthreads();
-        {
+        if (!staged_tile) {
           RowCopy<T, D, NT, 64> cq, cg;
           cq.load(q + base, t0, TM, N);
           cg.load(dout + base, t0, TM, N);
