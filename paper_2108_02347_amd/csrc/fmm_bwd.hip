@@ -69,18 +69,21 @@ struct BwdCfg {
       D > 64 ? 0 : FC ? 2 * D * (D + 1) * 4 + 2 * FRAG_MAP : (REC_F32 > REC_FRAG ? REC_F32 : REC_FRAG);
   // offset of the fragments within the record area
   static constexpr int FRAG_OFF = FC ? 2 * D * (D + 1) * 4 : 0;
+  // tile buffers: phi and dnum rows of the tile (FC: of both maps at once)
+  static constexpr int NTB = FC ? 4 : 2;
   static constexpr int UR_FIT =
-      (BUDGET - 2 * TILE - 256 - 2 * NT * 4 - REC_BYTES) / (UNIT2 + STAT_UNIT);
+      (BUDGET - NTB * TILE - 256 - 2 * NT * 4 - REC_BYTES) / (UNIT2 + STAT_UNIT);
   static constexpr int UR = UR_FIT > 8 ? 8 : UR_FIT;
   static_assert(UR >= 2, "a round must hold one tile");
   static constexpr int WK = 32 * UR;  // rows per staging round
   // per staged row of the key pass: scaled maximum, 1/l, D; the row pass
   // reuses the area for its block reduction (2 x NT floats)
   static constexpr int STAT_BYTES = WK * 12 > 2 * NT * 4 ? WK * 12 : 2 * NT * 4;
-  // [buffer A: WK rows][buffer B: WK rows][tile buffer 1][tile buffer 2][64 floats][stats]
-  // [records]
+  // [buffer A: WK rows][buffer B: WK rows][tile buffers 1, 2][64 floats][stats]
+  // [records][tile buffers 3, 4 (FC)]
   static constexpr int REC_OFF = 2 * WK * ROW + 2 * TILE + 256 + STAT_BYTES;
-  static constexpr int LDS = REC_OFF + REC_BYTES;
+  static constexpr int TB34_OFF = REC_OFF + REC_BYTES;
+  static constexpr int LDS = TB34_OFF + (NTB - 2) * TILE;
 };
 
 __device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"); }
@@ -383,6 +386,9 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
   const float tau = scale2 * 0.69314718055994531f;  // 1/sqrt(d)
   const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
   float acc_near = 0.f, acc_far = 0.f;  // this lane's share of g . near and g . far
+  // the ones column of the forward record's update (z), for every tile
+  float* ones_col = dden_s;
+  if (threadIdx.x < 64) ones_col[threadIdx.x] = 1.f;
   const int s0 = seg * L, s1 = min(N, s0 + L);
   for (int t0 = s0; t0 < s1; t0 += TM) {
     const int i0 = t0 + 16 * w, row = i0 + r;
@@ -448,8 +454,18 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
     }
     // ks: first key of the last staged round, which holds the tile's keys
     // (causal form)
-    // ---- far field, one map at a time
+    // ---- far field, one map at a time (FC: phi of the tile's keys for both
+    // maps staged at once, into tb1 and tb2, and both records advanced after
+    // both maps' products)
+    const T* vt = sv + (t0 - ks) * ST;
+    if constexpr (CAUSAL && FC) {
+      __syncthreads();
+      stage_phi_rows<T, D>(sk + (t0 - ks) * ST, t0, N, 0, tb1);
+      if (rank > 1) stage_phi_rows<T, D>(sk + (t0 - ks) * ST, t0, N, 1, tb2);
+      __syncthreads();
+    }
     for (int l = 0; l < rank; ++l) {
+      const T* tbl = CAUSAL && FC && l == 1 ? tb2 : tb1;
       Q pq[NB];
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
@@ -460,15 +476,17 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
         pq[cb] = f32_to_quad<T>(p);
       }
       float* rl = rec + (size_t)l * D * (D + 1);
-      const T* vt = sv + (t0 - ks) * ST;
       f32x4 num[NB + 1];
 #pragma unroll
       for (int nb = 0; nb <= NB; ++nb) num[nb] = zero;
       if constexpr (CAUSAL) {
-        // the tile's keys: phi_l(K_t) into tb1; intra-tile part of num, den
-        __syncthreads();
-        stage_phi_rows<T, D>(sk + (t0 - ks) * ST, t0, N, l, tb1);
-        __syncthreads();
+        // the tile's keys: phi_l(K_t) into tb1 (FC: staged above); intra-tile
+        // part of num, den
+        if constexpr (!FC) {
+          __syncthreads();
+          stage_phi_rows<T, D>(sk + (t0 - ks) * ST, t0, N, l, tb1);
+          __syncthreads();
+        }
         const Q ones = quad_fill<T>(1.f);
         for (int u = 0; u <= (w >> 1); ++u) {
           const bool diag = u == (w >> 1);
@@ -478,7 +496,7 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
             Q ka2[NB];
 #pragma unroll
             for (int cb = 0; cb < NB; ++cb)
-              ka2[cb] = ld_quad(tb1, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
+              ka2[cb] = ld_quad(tbl, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
             const f32x4 at = contract<NB>(ka2, pq, zero);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -564,8 +582,8 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
           const Q p0 = f32_to_quad<T>(a2[0]), p1 = f32_to_quad<T>(a2[1]);
 #pragma unroll
           for (int cb = 0; cb < NB; ++cb)
-            dph[cb] = mma_step2(ld_tquad(tb1, 32 * u, 16 * cb, ST),
-                                ld_tquad(tb1, 32 * u + 16, 16 * cb, ST), p0, p1, dph[cb]);
+            dph[cb] = mma_step2(ld_tquad(tbl, 32 * u, 16 * cb, ST),
+                                ld_tquad(tbl, 32 * u + 16, 16 * cb, ST), p0, p1, dph[cb]);
         }
         mfma_drain();
       }
@@ -598,17 +616,24 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
           dqa[cb][i] = fmaf(dg, dph[cb][i] + zf[i] * dden, dqa[cb][i]);
         }
       }
-      if constexpr (CAUSAL) {
+      if constexpr (CAUSAL && !FC) {
         // advance the forward prefix record by the tile's keys (tb1 still
         // holds phi_l(K_t)), unless this is the segment's last tile
         if (t0 + TM < s1) {
           __syncthreads();  // every wave has read record l for this tile
-          float* ones_col = dden_s;
-          if (threadIdx.x < 64) ones_col[threadIdx.x] = 1.f;
-          __syncthreads();
           record_add<T, D>(rl, tb1, vt, ones_col, ST, w,
                            FR ? frb + l * RecFrags<D>::PER_MAP : nullptr);
         }
+      }
+    }
+    if constexpr (CAUSAL && FC) {
+      // both records advance by the tile's keys (tb1, tb2 hold phi_0, phi_1
+      // of them), unless this is the segment's last tile
+      if (t0 + TM < s1) {
+        __syncthreads();  // every wave has read both records for this tile
+        for (int l = 0; l < rank; ++l)
+          record_add<T, D>(rec + (size_t)l * D * (D + 1), l == 1 ? tb2 : tb1, vt, ones_col, ST,
+                           w, FR ? frb + l * RecFrags<D>::PER_MAP : nullptr);
       }
     }
     store_row<T, D>(dq + base, row, N, dqa);
@@ -907,8 +932,73 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
       }
       mfma_drain();
     }
-    // ---- far field, one map at a time
+    // ---- far field, one map at a time.  Causal: per map the tile's rows as
+    // phi_l(q) rows, dnum = c g / den rows, and dden (FC: both maps staged at
+    // once, map 1 into tb3, tb4 and the statistics area, and both records
+    // advanced after both maps' products)
+    T* tb3 = reinterpret_cast<T*>(dyn_smem + C::TB34_OFF);
+    T* tb4 = tb3 + TM * ST;
+    auto phq_of = [&](int l) { return CAUSAL && FC && l == 1 ? tb3 : tb1; };
+    auto dnr_of = [&](int l) { return CAUSAL && FC && l == 1 ? tb4 : tb2; };
+    auto dd_of = [&](int l) { return CAUSAL && FC && l == 1 ? stat + 64 : dden_s; };
+    auto cd_of = [&](int l) { return CAUSAL && FC ? stat + 128 + 64 * l : stat; };
+    auto reload_tile = [&]() {
+      if (!staged_tile) {
+        RowCopy<T, D, NT, 64> cq, cg;
+        cq.load(q + base, t0, TM, N);
+        cg.load(dout + base, t0, TM, N);
+        auto ident = [](int i) { return i; };
+        cq.store(sq, ST, TM, ident);
+        cg.store(sg, ST, TM, ident);
+      }
+    };
+    auto far_row_terms = [&](int l) {  // dden and c / den of the tile's rows
+      if (threadIdx.x < 64) {
+        const int i = t0 + threadIdx.x;
+        const bool ok = i < N;
+        const float* fp = rowfar + (((size_t)bh * N + (ok ? i : 0)) * rank + l) * 2;
+        dd_of(l)[threadIdx.x] = ok ? fp[1] : 0.f;
+        cd_of(l)[threadIdx.x] = ok ? sfw * fp[0] : 0.f;
+      }
+    };
+    auto dnum_rows = [&](T* dst, const float* cd) {
+      using LY = Lay<T>;
+      constexpr int CPR = D / LY::EPC;
+      for (int t = threadIdx.x; t < TM * CPR; t += NT) {
+        const int rr = t / CPR, c = t % CPR;
+        const uint4 raw = *reinterpret_cast<const uint4*>(sg + rr * ST + c * LY::EPC);
+        const float f = cd[rr];
+        uint4 outw;
+        if constexpr (sizeof(T) == 2) {
+          const uint16_t* e = reinterpret_cast<const uint16_t*>(&raw);
+          float x[8];
+#pragma unroll
+          for (int ii = 0; ii < 8; ++ii) x[ii] = bf16_to_f32(e[ii]) * f;
+          outw = make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]),
+                            pack_bf16x2(x[4], x[5]), pack_bf16x2(x[6], x[7]));
+        } else {
+          const float* e = reinterpret_cast<const float*>(&raw);
+          outw = make_uint4(__float_as_uint(e[0] * f), __float_as_uint(e[1] * f),
+                            __float_as_uint(e[2] * f), __float_as_uint(e[3] * f));
+        }
+        *reinterpret_cast<uint4*>(dst + rr * ST + c * LY::EPC) = outw;
+      }
+    };
+    if constexpr (CAUSAL && FC) {
+      __syncthreads();
+      reload_tile();
+      for (int l = 0; l < rank; ++l) far_row_terms(l);
+      __syncthreads();
+      for (int l = 0; l < rank; ++l) {
+        stage_phi_rows<T, D>(sq, t0, N, l, phq_of(l));
+        dnum_rows(dnr_of(l), cd_of(l));
+      }
+      __syncthreads();
+    }
     for (int l = 0; l < rank; ++l) {
+      const T* phq = phq_of(l);
+      const T* dnr = dnr_of(l);
+      const float* ddl = dd_of(l);
       Q pk[NB];
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
@@ -923,50 +1013,15 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) dph[cb] = zero;
       if constexpr (CAUSAL) {
-        // the tile's rows: phi_l(q) into tb1, dnum = c g / den into tb2,
-        // dden into dden_s
-        __syncthreads();
-        if (!staged_tile) {
-          RowCopy<T, D, NT, 64> cq, cg;
-          cq.load(q + base, t0, TM, N);
-          cg.load(dout + base, t0, TM, N);
-          auto ident = [](int i) { return i; };
-          cq.store(sq, ST, TM, ident);
-          cg.store(sg, ST, TM, ident);
+        if constexpr (!FC) {
+          __syncthreads();
+          reload_tile();
+          far_row_terms(l);
+          __syncthreads();
+          stage_phi_rows<T, D>(sq, t0, N, l, tb1);
+          dnum_rows(tb2, stat);
+          __syncthreads();
         }
-        if (threadIdx.x < 64) {
-          const int i = t0 + threadIdx.x;
-          const bool ok = i < N;
-          const float* fp = rowfar + (((size_t)bh * N + (ok ? i : 0)) * rank + l) * 2;
-          dden_s[threadIdx.x] = ok ? fp[1] : 0.f;
-          stat[threadIdx.x] = ok ? sfw * fp[0] : 0.f;  // c / den
-        }
-        __syncthreads();
-        stage_phi_rows<T, D>(sq, t0, N, l, tb1);
-        {
-          using LY = Lay<T>;
-          constexpr int CPR = D / LY::EPC;
-          for (int t = threadIdx.x; t < TM * CPR; t += NT) {
-            const int rr = t / CPR, c = t % CPR;
-            const uint4 raw = *reinterpret_cast<const uint4*>(sg + rr * ST + c * LY::EPC);
-            const float f = stat[rr];
-            uint4 outw;
-            if constexpr (sizeof(T) == 2) {
-              const uint16_t* e = reinterpret_cast<const uint16_t*>(&raw);
-              float x[8];
-#pragma unroll
-              for (int i = 0; i < 8; ++i) x[i] = bf16_to_f32(e[i]) * f;
-              outw = make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]),
-                                pack_bf16x2(x[4], x[5]), pack_bf16x2(x[6], x[7]));
-            } else {
-              const float* e = reinterpret_cast<const float*>(&raw);
-              outw = make_uint4(__float_as_uint(e[0] * f), __float_as_uint(e[1] * f),
-                                __float_as_uint(e[2] * f), __float_as_uint(e[3] * f));
-            }
-            *reinterpret_cast<uint4*>(tb2 + rr * ST + c * LY::EPC) = outw;
-          }
-        }
-        __syncthreads();
         // rows i >= j of the tile: units (w >> 1) .. 1, the first one masked
         for (int u = (w >> 1); u < 2; ++u) {
           const bool diag = u == (w >> 1);
@@ -976,8 +1031,8 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
             Q na[NB], fa[NB];
 #pragma unroll
             for (int cb = 0; cb < NB; ++cb) {
-              na[cb] = ld_quad(tb2, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
-              fa[cb] = ld_quad(tb1, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
+              na[cb] = ld_quad(dnr, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
+              fa[cb] = ld_quad(phq, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
             }
             const f32x4 c1 = contract<NB>(na, vq, zero);
             const f32x4 e1 = contract<NB>(fa, pk, zero);
@@ -985,7 +1040,7 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
             for (int i = 0; i < 4; ++i) {
               const int lr = 32 * u + 16 * b + 4 * g + i;
               const bool ok = !diag || t0 + lr >= key;
-              cc[b][i] = ok ? c1[i] + dden_s[lr] : 0.f;
+              cc[b][i] = ok ? c1[i] + ddl[lr] : 0.f;
               ee[b][i] = ok ? e1[i] : 0.f;
             }
           }
@@ -993,10 +1048,10 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
           const Q e0q = f32_to_quad<T>(ee[0]), e1q = f32_to_quad<T>(ee[1]);
 #pragma unroll
           for (int cb = 0; cb < NB; ++cb) {
-            dph[cb] = mma_step2(ld_tquad(tb1, 32 * u, 16 * cb, ST),
-                                ld_tquad(tb1, 32 * u + 16, 16 * cb, ST), c0q, c1q, dph[cb]);
-            dva[cb] = mma_step2(ld_tquad(tb2, 32 * u, 16 * cb, ST),
-                                ld_tquad(tb2, 32 * u + 16, 16 * cb, ST), e0q, e1q, dva[cb]);
+            dph[cb] = mma_step2(ld_tquad(phq, 32 * u, 16 * cb, ST),
+                                ld_tquad(phq, 32 * u + 16, 16 * cb, ST), c0q, c1q, dph[cb]);
+            dva[cb] = mma_step2(ld_tquad(dnr, 32 * u, 16 * cb, ST),
+                                ld_tquad(dnr, 32 * u + 16, 16 * cb, ST), e0q, e1q, dva[cb]);
           }
         }
         mfma_drain();
@@ -1041,7 +1096,7 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
           dka[cb][i] = fmaf(dg, dph[cb][i] + zf[i], dka[cb][i]);
         }
       }
-      if constexpr (CAUSAL) {
+      if constexpr (CAUSAL && !FC) {
         // advance the suffix record by the tile's rows, unless this is the
         // segment's first tile (the last one walked)
         if (tt + 1 < ntile) {
@@ -1049,6 +1104,14 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
           record_add<T, D>(drl, tb1, tb2, dden_s, ST, w,
                            FR ? frb + l * RecFrags<D>::PER_MAP : nullptr);
         }
+      }
+    }
+    if constexpr (CAUSAL && FC) {
+      if (tt + 1 < ntile) {
+        __syncthreads();  // every wave has read both records for this tile
+        for (int l = 0; l < rank; ++l)
+          record_add<T, D>(drec + (size_t)l * D * (D + 1), phq_of(l), dnr_of(l), dd_of(l), ST, w,
+                           FR ? frb + l * RecFrags<D>::PER_MAP : nullptr);
       }
     }
     store_row<T, D>(dk + base, key, N, dka);
