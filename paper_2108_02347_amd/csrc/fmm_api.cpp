@@ -500,8 +500,10 @@ int run_layer(const void* x, const void* w_qkv, const void* w_out, void* y, int 
   if (overlaps2(y, xb, x, xb) || overlaps2(y, xb, w_qkv, wq) || overlaps2(y, xb, w_out, wo))
     return FMM_ERR_INVALID_ARG;
   // workspace: qkv, q, k, v, o, merged heads, then the operator's records
+  // (with the library's own projection kernels only q, k, v and o are used)
   const Plan p = plan_for(B, H, N, d, band_k, rank, causal, dtype);
   if (p.ws_bytes == 0) return FMM_ERR_UNSUPPORTED;
+  const bool own_proj = fmm::layer_proj_applies(dtype, E);
   const size_t seg = align256(xb);
   const size_t off_qkv = 0, off_q = 3 * seg, off_k = 4 * seg, off_v = 5 * seg, off_o = 6 * seg,
                off_m = 7 * seg, off_ws = 8 * seg;
@@ -520,10 +522,17 @@ int run_layer(const void* x, const void* w_qkv, const void* w_out, void* y, int 
     fmm::Launcher dry;
     dry.timer = &t;
     dry.dry = true;
-    fmm::launch_layer_copy(dry, true, dtype, nullptr, nullptr, nullptr, nullptr, B, N, H, d,
-                           (hipStream_t)stream);
-    fmm::launch_layer_copy(dry, false, dtype, nullptr, nullptr, nullptr, nullptr, B, N, H, d,
-                           (hipStream_t)stream);
+    if (own_proj) {
+      fmm::launch_layer_proj(dry, true, nullptr, nullptr, nullptr, nullptr, nullptr, B, N, H, d,
+                             (hipStream_t)stream);
+      fmm::launch_layer_proj(dry, false, nullptr, nullptr, nullptr, nullptr, nullptr, B, N, H,
+                             d, (hipStream_t)stream);
+    } else {
+      fmm::launch_layer_copy(dry, true, dtype, nullptr, nullptr, nullptr, nullptr, B, N, H, d,
+                             (hipStream_t)stream);
+      fmm::launch_layer_copy(dry, false, dtype, nullptr, nullptr, nullptr, nullptr, B, N, H, d,
+                             (hipStream_t)stream);
+    }
     if (dry.err != hipSuccess)
       return dry.err == hipErrorInvalidConfiguration ? FMM_ERR_UNSUPPORTED : FMM_ERR_HIP;
   }
@@ -540,6 +549,19 @@ int run_layer(const void* x, const void* w_qkv, const void* w_out, void* y, int 
   a.out = at(ws, off_o);
   a.ws = (float*)at(ws, off_ws);
   const int M = B * N;
+  if (own_proj) {
+    EventTimer& t = timer();
+    std::lock_guard<std::mutex> g(t.mu);
+    fmm::Launcher L;
+    L.timer = &t;
+    if (fmm::launch_layer_proj(L, true, x, w_qkv, at(ws, off_q), at(ws, off_k), at(ws, off_v), B,
+                               N, H, d, (hipStream_t)stream) != hipSuccess ||
+        fmm::launch_forward(a, L) != hipSuccess ||
+        fmm::launch_layer_proj(L, false, at(ws, off_o), w_out, y, nullptr, nullptr, B, N, H, d,
+                               (hipStream_t)stream) != hipSuccess)
+      return FMM_ERR_HIP;
+    return FMM_OK;
+  }
   if (fmm::layer_gemm(hdl, stream, dtype, x, w_qkv, at(ws, off_qkv), M, E, 3 * E) != hipSuccess)
     return FMM_ERR_HIP;
   EventTimer& t = timer();

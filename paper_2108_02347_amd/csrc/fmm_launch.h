@@ -195,6 +195,12 @@ hipError_t launch_backward_tail(const BwdArgs& a, Launcher& L);
 // `stream`), and a rocBLAS handle (nullptr on failure).
 hipError_t launch_layer_copy(Launcher& L, bool split, int dtype, const void* src, void* d0,
                              void* d1, void* d2, int B, int N, int H, int d, hipStream_t s);
+// The layer's projections as kernels of this library (fmm_layer.hip, k_proj):
+// bf16 with E = 32, 64, 96 or 128.  qkv: x [B N, E] -> q, k, v [B, H, N, d]
+// (o0, o1, o2); otherwise the heads [B, H, N, d] -> y [B N, E] (o0).
+bool layer_proj_applies(int dtype, int E);
+hipError_t launch_layer_proj(Launcher& L, bool qkv, const void* in, const void* w, void* o0,
+                             void* o1, void* o2, int B, int N, int H, int d, hipStream_t s);
 hipError_t layer_gemm(void* handle, void* stream, int dtype, const void* A, const void* Bm,
                       void* C, int M, int K, int Nc);
 void* layer_blas_handle_create();

@@ -5,14 +5,20 @@
 //   x [B, N, E] --GEMM--> qkv [B*N, 3E] --k_split_heads--> q, k, v [B, H, N, d]
 //     --operator--> o [B, H, N, d] --k_merge_heads--> m [B*N, E] --GEMM--> y [B, N, E]
 //
-// The two projections are plain GEMMs and go to rocBLAS (gemm_ex, fp32
-// accumulation, the storage type in and out); the head split and merge are
-// coalesced 16-byte copies; the operator is this library's.
+// bf16 with E a multiple of 32 up to 128 (the long-range models' 64-wide
+// embedding among them): each projection is one kernel of this file that
+// reads its input rows once and writes its output in the layout the next
+// step reads (k_proj: x -> q, k, v per head; heads -> y), matrix-core
+// products with fp32 accumulation.  Otherwise the projections go to rocBLAS
+// (gemm_ex, fp32 accumulation, the storage type in and out) with the head
+// split and merge as coalesced 16-byte copies.  The operator is this
+// library's either way.
 #include <hip/hip_runtime.h>
 #include <rocblas/rocblas.h>
 
 #include "fmm_device.h"
 #include "fmm_launch.h"
+#include "fmm_oct.h"
 
 namespace fmm {
 namespace {
@@ -75,6 +81,93 @@ void launch_merge(Launcher& L, const void* o, void* m, int B, int N, int H, int 
     dim3(256), 0, s, (const T*)o, (T*)m, nchunk, N, H, d);
 }
 
+// ------------------------------------------------------------------ k_proj
+// One projection of the layer for bf16, E = K = 32 KB (KB = 1 .. 4):
+// out[t][c] = sum_e in[t][e] W[e][c], c < OUTC (3E for QKV, E for the
+// output).  MODE 0 (QKV): in = x rows [T, E]; column c goes to q, k or v
+// (c / E), head (c % E) / d, feature c % d of [B, H, N, d].  MODE 1 (output):
+// in row t = the heads' outputs of token t side by side (gathered from
+// [B, H, N, d]); out = y rows [T, E].
+//
+// A workgroup (4 waves) takes 64 tokens, a wave 16.  W is staged in LDS
+// (rows padded by 8 elements); the product is formed transposed, D[c][t] =
+// sum_e W[e][c] in[t][e]: the W operand comes from transposed LDS reads
+// (keys 4g.. and 16 + 4g.. of each 32-wide block, as the P V product reads V),
+// the token operand straight from memory in the same order, and each lane
+// ends with four consecutive columns of one token, stored as 8 bytes.
+template <int E, int MODE>
+__global__ __launch_bounds__(256) void k_proj(const bf16_t* __restrict__ in,
+                                              const bf16_t* __restrict__ w,
+                                              bf16_t* __restrict__ o0, bf16_t* __restrict__ o1,
+                                              bf16_t* __restrict__ o2, int T, int N, int H,
+                                              int d) {
+  constexpr int OUTC = MODE == 0 ? 3 * E : E;
+  constexpr int KB = E / 32, NCB = OUTC / 16;
+  constexpr int WS = OUTC + 8;  // padded LDS row (elements)
+  static_assert(E % 32 == 0 && E <= 128, "E = 32, 64, 96 or 128");
+  __shared__ __attribute__((aligned(16))) bf16_t wl[E * WS];
+  for (int i = threadIdx.x; i < E * (OUTC / 8); i += 256) {
+    const int row = i / (OUTC / 8), c8 = i % (OUTC / 8);
+    *reinterpret_cast<uint4*>(wl + row * WS + 8 * c8) =
+        *reinterpret_cast<const uint4*>(w + (size_t)row * OUTC + 8 * c8);
+  }
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
+  const long long tok = (long long)blockIdx.x * 64 + 16 * wv + r;  // this lane's token
+  const bool ok = tok < T;
+  const long long b = ok ? tok / N : 0, n = ok ? tok - b * N : 0;
+  // in[tok][k .. k+3] as 8 bytes (zero past T)
+  auto piece = [&](int kk) -> uint2 {
+    if (!ok) return make_uint2(0u, 0u);
+    if constexpr (MODE == 0) {
+      return *reinterpret_cast<const uint2*>(in + tok * E + kk);
+    } else {
+      const int hh = kk / d, f = kk - hh * d;
+      return *reinterpret_cast<const uint2*>(in + (((b * H + hh) * N + n) * d + f));
+    }
+  };
+  Oct xo[KB];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) xo[kb] = oct_of(piece(32 * kb + 4 * g), piece(32 * kb + 16 + 4 * g));
+  __syncthreads();
+  // lane (t, g) of a transposed read: W row 4g + t/4, columns 16cb + 4(t%4) .. +3
+  const int tr_off = (4 * g + (r >> 2)) * WS + 4 * (r & 3);
+#pragma unroll 4
+  for (int cb = 0; cb < NCB; ++cb) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const unsigned char* p =
+          reinterpret_cast<const unsigned char*>(wl + (32 * kb) * WS + 16 * cb + tr_off);
+      const Oct wo = oct_of(ld_tr16(p), ld_tr16(p + 16 * WS * 2));
+      acc = mma8(wo, xo[kb], acc);
+    }
+    if (!ok) continue;
+    // lane (r, g): columns 16cb + 4g .. +3 of token tok
+    const int c = 16 * cb + 4 * g;
+    const uint2 val = quad_pack(acc);
+    if constexpr (MODE == 0) {
+      const int part = c / E, hc = c - part * E, hh = hc / d, f = hc - hh * d;
+      bf16_t* dst = part == 0 ? o0 : (part == 1 ? o1 : o2);
+      *reinterpret_cast<uint2*>(dst + (((b * H + hh) * N + n) * d + f)) = val;
+    } else {
+      *reinterpret_cast<uint2*>(o0 + tok * E + c) = val;
+    }
+  }
+}
+
+template <int E>
+void launch_proj_e(Launcher& L, bool qkv, const void* in, const void* w, void* o0, void* o1,
+                   void* o2, int B, int N, int H, int d, hipStream_t s) {
+  const long long T = (long long)B * N;
+  const dim3 grid((unsigned)std::min<long long>((T + 63) / 64, 0xFFFFFFFFll));
+  if (qkv)
+    L(FMM_KERNEL_LAYER_COPY, k_proj<E, 0>, grid, dim3(256), 0, s, (const bf16_t*)in,
+      (const bf16_t*)w, (bf16_t*)o0, (bf16_t*)o1, (bf16_t*)o2, (int)T, N, H, d);
+  else
+    L(FMM_KERNEL_LAYER_COPY, k_proj<E, 1>, grid, dim3(256), 0, s, (const bf16_t*)in,
+      (const bf16_t*)w, (bf16_t*)o0, (bf16_t*)nullptr, (bf16_t*)nullptr, (int)T, N, H, d);
+}
+
 // Row-major C [M, Nc] = A [M, K] B [K, Nc] as the column-major product
 // C^T = B^T A^T.
 hipError_t gemm_rm(rocblas_handle hdl, int dtype, const void* A, const void* Bm, void* C, int M,
@@ -98,6 +191,22 @@ hipError_t launch_layer_copy(Launcher& L, bool split, int dtype, const void* src
   } else {
     if (split) launch_split<float>(L, src, d0, d1, d2, B, N, H, d, s);
     else launch_merge<float>(L, src, d0, B, N, H, d, s);
+  }
+  return L.err;
+}
+
+bool layer_proj_applies(int dtype, int E) {
+  return dtype == FMM_DTYPE_BF16 && E % 32 == 0 && E >= 32 && E <= 128;
+}
+
+hipError_t launch_layer_proj(Launcher& L, bool qkv, const void* in, const void* w, void* o0,
+                             void* o1, void* o2, int B, int N, int H, int d, hipStream_t s) {
+  switch (H * d) {
+    case 32: launch_proj_e<32>(L, qkv, in, w, o0, o1, o2, B, N, H, d, s); break;
+    case 64: launch_proj_e<64>(L, qkv, in, w, o0, o1, o2, B, N, H, d, s); break;
+    case 96: launch_proj_e<96>(L, qkv, in, w, o0, o1, o2, B, N, H, d, s); break;
+    case 128: launch_proj_e<128>(L, qkv, in, w, o0, o1, o2, B, N, H, d, s); break;
+    default: return L.note(hipErrorInvalidValue);
   }
   return L.err;
 }

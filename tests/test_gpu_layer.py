@@ -68,3 +68,12 @@ def test_layer_argument_checks():
         binding.layer_forward(x, w, wo, 3, torch.zeros(3, device="cuda:0"),
                               torch.zeros(3, device="cuda:0"), 3, 2, 0)
     assert ei.value.status in (binding.FMM_ERR_INVALID_ARG, binding.FMM_ERR_UNSUPPORTED)
+
+
+@pytest.mark.parametrize("E,H", [(32, 2), (96, 3), (128, 1), (128, 4)])
+def test_layer_projection_widths(E, H):
+    # bf16 widths that the library's own projection kernels take (E = 32 with
+    # heads of 16, whose 32-wide contraction blocks span two heads; E = 96;
+    # E = 128 as one head of 128 and as four of 32); 600 tokens leave a
+    # partial last block of 64
+    check_layer(2, 300, E, H, 9, 2, int(E == 96), "bf16", 3100 + E + H)
