@@ -879,22 +879,34 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
       const int nrow = min(C::WK, rb - rs);
       __syncthreads();
       stage_pair<T, D>(sq, sg, q + base, dout + base, rs, nrow, N);
+      // per staged row (three arrays, read four rows at a time): the scaled
+      // maximum, 1/l and D
+      float* sm = stat;
+      float* sli = stat + C::WK;
+      float* sD = stat + 2 * C::WK;
       for (int t = threadIdx.x; t < nrow; t += NT) {
         const int i = rs + t;
         const bool ok = i < N;
         const float* sp = rowstat + ((size_t)bh * N + (ok ? i : 0)) * 3;
-        stat[3 * t] = ok ? sp[0] : 0.f;
-        stat[3 * t + 1] = ok ? sp[1] : 0.f;
-        stat[3 * t + 2] = ok ? sp[2] : 0.f;
+        sm[t] = ok ? sp[0] : 0.f;
+        sli[t] = ok ? sp[1] : 0.f;
+        sD[t] = ok ? sp[2] : 0.f;
       }
       __syncthreads();
       // rows of this round that can hold the strip's keys in their band
       const int lo = max(max(0, j0 - (CAUSAL ? 0 : band_k)), rs);
       const int hj = min(min(N - 1, j0 + 15 + band_k), rs + nrow - 1);
+      // rows whose band holds this lane's key: [rlo, rhi] (empty past N)
+      const int rlo = max(key - (CAUSAL ? 0 : band_k), 0);
+      const int rhi = key < N ? min(key + band_k, N - 1) : -1;
       for (int ua = lo >> 5; ua <= (hj >> 5) && lo <= hj; ++ua) {
-        const int ur = ua * 32 - rs;  // LDS row of the unit
+        const int ur = ua * 32 - rs;  // LDS row of the unit (a multiple of 32)
         const T* qx = sq + ur * ST;
         const T* gx = sg + ur * ST;
+        // unit-local row offsets c = 16b + i of this lane group (rows
+        // ua*32 + 4g + c) inside the interval
+        int ilo = rlo - ua * 32 - 4 * g, ispan = rhi - rlo;
+        if (ispan < 0) { ilo = 64; ispan = 0; }
         float pp[2][4], ds[2][4];
 #pragma unroll
         for (int b = 0; b < 2; ++b) {
@@ -906,18 +918,18 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
           }
           const f32x4 s = contract<NB>(qa, kq, zero);
           const f32x4 dp = contract<NB>(ga, vq, zero);
+          const int lr0 = ur + 16 * b + 4 * g;  // staged rows lr0 .. lr0+3
+          const float4 m4 = *reinterpret_cast<const float4*>(sm + lr0);
+          const float4 l4 = *reinterpret_cast<const float4*>(sli + lr0);
+          const float4 d4 = *reinterpret_cast<const float4*>(sD + lr0);
+          const float mv[4] = {m4.x, m4.y, m4.z, m4.w}, lv[4] = {l4.x, l4.y, l4.z, l4.w},
+                      dv4[4] = {d4.x, d4.y, d4.z, d4.w};
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int lr = ur + 16 * b + 4 * g + i;  // staged row
-            const int irow = rs + lr;
-            const bool ok = irow < N && key < N &&
-                            (CAUSAL ? (irow >= key && irow - key <= band_k)
-                                    : (irow - key <= band_k && key - irow <= band_k));
-            const float p = ok ? __builtin_amdgcn_exp2f(fmaf(s[i], scale2, -stat[3 * lr])) *
-                                     stat[3 * lr + 1]
-                               : 0.f;
+            const bool ok = (unsigned)(16 * b + i - ilo) <= (unsigned)ispan;
+            const float p = ok ? __builtin_amdgcn_exp2f(fmaf(s[i], scale2, -mv[i])) * lv[i] : 0.f;
             pp[b][i] = p * sn;
-            ds[b][i] = p * fmaf(sn, dp[i], -stat[3 * lr + 2]) * tau;
+            ds[b][i] = p * fmaf(sn, dp[i], -dv4[i]) * tau;
           }
         }
         const Q p0 = f32_to_quad<T>(pp[0]), p1 = f32_to_quad<T>(pp[1]);
