@@ -184,9 +184,11 @@ int fmm_attn_forward_ws(const void* q, const void* k, const void* v, void* out,
  * enqueued, when fmm_attn_workspace_bytes(...) of the shape exceeds that size.
  * All calls on one GPU share its array: calls that can overlap in time on one
  * GPU (different streams without ordering between them) race and must not be
- * made; calls on one stream are ordered by it.  Every value the kernels read
- * from the array is written earlier in the same call, so nothing needs
- * clearing between calls.
+ * made; calls on one stream are ordered by it.  Every value the kernels use
+ * from the array is written earlier in the same call (the one-launch path's
+ * stamps left by earlier calls carry another epoch and are ignored), so
+ * nothing needs clearing between calls, and a call captured into a graph may
+ * be replayed any number of times.
  */
 int fmm_attn_forward_noalloc(const void* q, const void* k, const void* v, void* out,
                              int B, int H, int N, int d, int band_k, int rank,
@@ -291,7 +293,10 @@ int fmm_attn_version(void);
  * default); 2: wherever it applies, but every workgroup forms its slice's
  * state itself instead of exchanging (slower; a check of the exchange).
  * Process-wide; returns the previous mode, or -1 for a mode outside 0..2.
- * The workspace sizes above include what this path needs.
+ * The workspace sizes above include what this path needs.  The path may be
+ * captured into a graph: each launch's stamps carry an epoch formed from the
+ * call and the dispatch's own id, so a replay never takes the stamps of an
+ * earlier replay for its own.
  */
 int fmm_attn_set_one_launch(int mode);
 

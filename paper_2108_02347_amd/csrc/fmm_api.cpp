@@ -227,17 +227,23 @@ std::atomic<int>& one_launch_mode() {
   return m;
 }
 
-// Epochs of the one-launch path's stamps: unique per call within the process,
-// starting from a random 48-bit value so that stale stamps left in memory by
-// another process (or garbage) match a call's epoch with negligible
-// probability.  56 bits (the stamp's low 8 bits hold the XCC id).
+// Epochs of the one-launch path's stamps (56 bits, formed on the device): this
+// call's number in bits 32-55, from a random start, and in bits 0-31 a random
+// per-process offset to which each launch adds its dispatch id.  Eager calls
+// differ in the call number, replays of a captured graph (frozen arguments)
+// in the dispatch id; the random parts make a match with stale stamps left in
+// memory by another process unlikely.
 unsigned long long next_epoch() {
-  static std::atomic<unsigned long long> e{[] {
+  static const unsigned long long offset = [] {
     std::random_device rd;
-    const unsigned long long s = ((unsigned long long)rd() << 20) ^ (unsigned long long)rd();
-    return (s & ((1ull << 47) - 1)) | (1ull << 47);
+    return (unsigned long long)rd();
+  }();
+  static std::atomic<unsigned long long> n{[] {
+    std::random_device rd;
+    return (unsigned long long)rd();
   }()};
-  return e.fetch_add(1, std::memory_order_relaxed) & ((1ull << 56) - 1);
+  const unsigned long long c = n.fetch_add(1, std::memory_order_relaxed) & 0xffffffull;
+  return (c << 32) | (offset & 0xffffffffull);
 }
 
 // Workgroups of k_band_fused that fit on the current device at once (two per CU).

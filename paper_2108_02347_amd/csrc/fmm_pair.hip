@@ -435,8 +435,11 @@ __global__ __launch_bounds__(PNT, 2) void k_band_pair(const bf16_t* __restrict__
 // reached L2) precedes its stamp; stamps are written and polled with
 // device-scope atomics (which bypass the vector L1; plain loads of a stamp
 // can keep hitting a stale L1 line), and a workgroup reads the records only
-// after it has seen their stamps, so no line of them is in its L1 before.  A stamp holds the call's
-// epoch and the XCC id of its writer.  Any stamp from another XCC (or one
+// after it has seen their stamps, so no line of them is in its L1 before.  A
+// stamp holds the launch's epoch and the XCC id of its writer.  The epoch
+// differs from launch to launch, also between replays of a captured graph
+// (it includes the dispatch id), so stamps left by an earlier launch in the
+// same workspace never count as this launch's.  Any stamp from another XCC (or one
 // marking a workgroup that gave up), or a wait beyond spin_limit polls, makes
 // the workgroup compute its slice's total itself from K and V in memory: the
 // same partial states (same products, same order) summed in the same order,
@@ -446,6 +449,18 @@ __global__ __launch_bounds__(PNT, 2) void k_band_pair(const bf16_t* __restrict__
 // stamps: (epoch << 8) | XCC id of the writer; this XCC id marks a workgroup
 // that gave up on the exchange
 constexpr unsigned kGaveUp = 0xffu;
+
+// The dispatch's packet index on its queue (the hardware's 64-bit dispatch
+// id, the same for every workgroup of one launch and new for every launch,
+// also for each replay of a captured graph, whose kernel arguments are frozen).
+extern "C" __device__ unsigned long long fmm_dispatch_id() __asm("llvm.amdgcn.dispatch.id");
+
+// A launch's epoch (56 bits): the host's call number in bits 32-55 and, in
+// bits 0-31, the host's per-process offset plus the dispatch id.
+__device__ __forceinline__ unsigned long long launch_epoch(unsigned long long host) {
+  return (host & 0x00ffffff00000000ull) |
+         (unsigned)((unsigned)host + (unsigned)fmm_dispatch_id());
+}
 
 __device__ __forceinline__ unsigned xcc_id() {
   unsigned x;
@@ -566,7 +581,7 @@ __global__ __launch_bounds__(PNT, 2) void k_band_fused(
     bf16_t* __restrict__ out, float* __restrict__ part, float* __restrict__ tot,
     unsigned long long* __restrict__ stamp, const float* __restrict__ w_near,
     const float* __restrict__ w_far, int H, int N, int band_k, int G, float scale2,
-    unsigned long long epoch, int spin_limit, int exchange) {
+    unsigned long long host_epoch, int spin_limit, int exchange) {
   using C = PairCfg<D, R, KC>;
   constexpr int NB = C::NB, NQ = C::NQ, U = C::U;
   constexpr int REC = R * D * (D + 1);
@@ -621,6 +636,7 @@ __global__ __launch_bounds__(PNT, 2) void k_band_fused(
   }
   __syncthreads();
   const RingOffsets<D> ro;
+  const unsigned long long epoch = launch_epoch(host_epoch);
   const unsigned long long mine = (epoch << 8) | xcc_id();
   unsigned long long* st = stamp + (size_t)bh * G * 2;
   float* prec = part + (size_t)bh * G * REC;
