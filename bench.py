@@ -291,7 +291,7 @@ def read_counters(kernel: str):
 
 # the sources of the kernels the profiles describe (host-side code excluded,
 # so a change to argument checks or bindings does not void them)
-KERNEL_SOURCES = ("fmm_device.h", "fmm_oct.h", "fmm_apply.h", "fmm_launch.h",
+KERNEL_SOURCES = ("fmm_device.h", "fmm_oct.h", "fmm_apply.h", "fmm_launch.h", "fmm_xchg.h",
                   "fmm_kernels.hip", "fmm_pair.hip", "fmm_causal.hip")
 
 

@@ -528,16 +528,17 @@ int run_layer(const void* x, const void* w_qkv, const void* w_out, void* y, int 
     fmm::Launcher dry;
     dry.timer = &t;
     dry.dry = true;
+    // (the dry passes record their result in dry.err)
     if (own_proj) {
-      fmm::launch_layer_proj(dry, true, nullptr, nullptr, nullptr, nullptr, nullptr, B, N, H, d,
-                             (hipStream_t)stream);
-      fmm::launch_layer_proj(dry, false, nullptr, nullptr, nullptr, nullptr, nullptr, B, N, H,
-                             d, (hipStream_t)stream);
+      (void)fmm::launch_layer_proj(dry, true, nullptr, nullptr, nullptr, nullptr, nullptr, B, N,
+                                   H, d, (hipStream_t)stream);
+      (void)fmm::launch_layer_proj(dry, false, nullptr, nullptr, nullptr, nullptr, nullptr, B, N,
+                                   H, d, (hipStream_t)stream);
     } else {
-      fmm::launch_layer_copy(dry, true, dtype, nullptr, nullptr, nullptr, nullptr, B, N, H, d,
-                             (hipStream_t)stream);
-      fmm::launch_layer_copy(dry, false, dtype, nullptr, nullptr, nullptr, nullptr, B, N, H, d,
-                             (hipStream_t)stream);
+      (void)fmm::launch_layer_copy(dry, true, dtype, nullptr, nullptr, nullptr, nullptr, B, N, H,
+                                   d, (hipStream_t)stream);
+      (void)fmm::launch_layer_copy(dry, false, dtype, nullptr, nullptr, nullptr, nullptr, B, N,
+                                   H, d, (hipStream_t)stream);
     }
     if (dry.err != hipSuccess)
       return dry.err == hipErrorInvalidConfiguration ? FMM_ERR_UNSUPPORTED : FMM_ERR_HIP;

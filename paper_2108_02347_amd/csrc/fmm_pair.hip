@@ -23,6 +23,7 @@
 #include "fmm_device.h"
 #include "fmm_launch.h"
 #include "fmm_oct.h"
+#include "fmm_xchg.h"
 
 namespace fmm {
 namespace {
@@ -446,27 +447,6 @@ __global__ __launch_bounds__(PNT, 2) void k_band_pair(const bf16_t* __restrict__
 // so every path gives the same bits.  Waits are bounded, so the kernel always
 // drains, and no workgroup's result depends on where its peers ran.
 
-// stamps: (epoch << 8) | XCC id of the writer; this XCC id marks a workgroup
-// that gave up on the exchange
-constexpr unsigned kGaveUp = 0xffu;
-
-// The dispatch's packet index on its queue (the hardware's 64-bit dispatch
-// id, the same for every workgroup of one launch and new for every launch,
-// also for each replay of a captured graph, whose kernel arguments are frozen).
-extern "C" __device__ unsigned long long fmm_dispatch_id() __asm("llvm.amdgcn.dispatch.id");
-
-// A launch's epoch (56 bits): the host's call number in bits 32-55 and, in
-// bits 0-31, the host's per-process offset plus the dispatch id.
-__device__ __forceinline__ unsigned long long launch_epoch(unsigned long long host) {
-  return (host & 0x00ffffff00000000ull) |
-         (unsigned)((unsigned)host + (unsigned)fmm_dispatch_id());
-}
-
-__device__ __forceinline__ unsigned xcc_id() {
-  unsigned x;
-  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
-  return x & 0xfu;
-}
 
 // Partial far-field state of the 128 keys r0 .. r0+127 held in ring slots
 // slot0 .. slot0+3 (keys at or beyond N excluded): T_l = phi_l(K)^T [V | 1]
@@ -537,40 +517,6 @@ __device__ __forceinline__ void store_record_block(float* rec, int cb,
   }
 }
 
-// Wave 0 polls stamp[2 i + level] of the slice's G workgroups (G <= 64) until
-// all carry this call's epoch; true when every one is `mine` (same epoch,
-// same XCC), false as soon as a stamp of this epoch is anything else or after
-// spin_limit polls.  Uniform over the workgroup.
-__device__ __forceinline__ bool wait_stamps(const unsigned long long* stamp, int level, int G,
-                                            unsigned long long epoch, unsigned long long mine,
-                                            int spin_limit, int* s_flag) {
-  if (threadIdx.x < 64) {
-    const int lane = threadIdx.x;
-    int res = 2;
-    for (int it = 0; it <= spin_limit; ++it) {
-      const unsigned long long x =
-          lane < G ? __hip_atomic_load(stamp + 2 * lane + level, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT)
-                   : mine;
-      const bool fresh = (x >> 8) == epoch;
-      if (__any(fresh && x != mine)) break;
-      if (__all(fresh)) {
-        res = 1;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-    if (lane == 0) *s_flag = res;
-  }
-  __syncthreads();
-  const bool ok = *s_flag == 1;
-  __syncthreads();  // the flag is reused by the next wait
-  return ok;
-}
-
-__device__ __forceinline__ void put_stamp(unsigned long long* p, unsigned long long x) {
-  __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 // grid.x = BH * G, G = ceil(N / 128) <= 64.  part: G records per slice; tot:
 // one record per slice; stamp: 2 G per slice.  exchange = 0 skips the exchange
@@ -661,7 +607,7 @@ __global__ __launch_bounds__(PNT, 2) void k_band_fused(
   Oct zo[R][NQ];
   auto pre_far = [&]() {
     __syncthreads();  // every wave is done with the ring
-    bool ok = exchange != 0 && wait_stamps(st, 0, G, epoch, mine, spin_limit, s_flag);
+    bool ok = exchange != 0 && wait_stamps(st, 2, 0, G, epoch, mine, spin_limit, s_flag);
     if (ok) {
       // elements [e0, e0 + cnt) of the G records: every value loaded at
       // once (flat index f = i CH + el, record i, element e0 + el), staged
@@ -699,7 +645,7 @@ __global__ __launch_bounds__(PNT, 2) void k_band_fused(
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
       if (threadIdx.x == 0) put_stamp(st + 2 * j + 1, mine);
-      ok = wait_stamps(st, 1, G, epoch, mine, spin_limit, s_flag);
+      ok = wait_stamps(st, 2, 1, G, epoch, mine, spin_limit, s_flag);
     } else if (exchange && threadIdx.x == 0) {
       // peers waiting for this workgroup's sum stop waiting
       put_stamp(st + 2 * j + 1, (epoch << 8) | kGaveUp);
