@@ -378,16 +378,39 @@ def graph_timed(fn, calls, replays, torch):
 def hbm_ceiling(torch):
     """Achievable HBM rates on this GPU for context next to the published
     peak: torch's device copy (bytes read + written) and fill (bytes written)
-    over 1 GiB buffers, 20 timed launches each."""
+    over 1 GiB buffers, 20 timed launches each; and the read/write mix of the
+    band kernel (three 64 MiB bf16 tensors read, one written, as torch's
+    elementwise addcmul), 50 launches back to back like the timed steps."""
     n = 1 << 30
     a = torch.ones(n, dtype=torch.uint8, device="cuda:0")
     b = torch.empty_like(a)
     t_copy = timed(lambda: b.copy_(a), 20, 3, torch)
     t_fill = timed(lambda: b.fill_(0), 20, 3, torch)
     del a, b
+    m = 32 << 20  # 64 MiB of bf16
+    # two sets of four tensors used in turn (512 MiB, twice the last-level
+    # cache: mostly HBM), and one set alone (256 MiB: largely cache-resident)
+    sets = [[torch.ones(m, dtype=torch.bfloat16, device="cuda:0") for _ in range(4)]
+            for _ in range(2)]
+    it = [0]
+
+    def mix():
+        x, y, z, o = sets[it[0] & 1]
+        it[0] += 1
+        torch.addcmul(x, y, z, out=o)
+
+    t_mix = timed(mix, 50, 6, torch)
+    x, y, z, o = sets[0]
+    t_mix1 = timed(lambda: torch.addcmul(x, y, z, out=o), 50, 5, torch)
+    del sets, x, y, z, o
     return {"copy_GBps": round(2 * n / t_copy / 1e9, 1),
             "write_GBps": round(n / t_fill / 1e9, 1),
-            "how": "torch copy_ and fill_ over 1 GiB, 20 launches"}
+            "read3_write1_GBps": round(4 * 2 * m / t_mix / 1e9, 1),
+            "read3_write1_cache_resident_GBps": round(4 * 2 * m / t_mix1 / 1e9, 1),
+            "how": "torch copy_ and fill_ over 1 GiB, 20 launches; addcmul of three 64 MiB "
+                   "bf16 tensors into a fourth (3 reads : 1 write, the band kernel's mix), "
+                   "50 launches alternating between two such sets (512 MiB, twice the "
+                   "last-level cache) and, cache_resident, on one set (256 MiB)"}
 
 
 def _blas_threads():
