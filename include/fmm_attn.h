@@ -40,6 +40,14 @@
  * stream) and returns without synchronising.  Faults inside kernels surface
  * at the caller's next synchronisation.
  *
+ * Graph capture: the calls enqueue kernels only (no copies, fills or host
+ * synchronisation), so they may be captured into a HIP graph.  The entry
+ * points with a library-owned workspace allocate it on first use per
+ * (device, stream) and grow it when a larger call comes; a stream under
+ * capture can do neither, and such a call returns FMM_ERR_UNSUPPORTED with
+ * nothing enqueued.  Make one call of the largest shape on that stream
+ * before capturing, or use fmm_attn_forward_ws or fmm_attn_forward_noalloc.
+ *
  * Errors: functions return an int status.  Every check (arguments, sizes,
  * workspace, and the grid of every kernel the call would launch against the
  * dispatch limits) runs before the first kernel is enqueued, so on
@@ -69,7 +77,10 @@ extern "C" {
                                     dtype code unknown, B*H above 2^31-1, or
                                     a kernel grid beyond the dispatch limit
                                     (2^32 work-items per dimension; about
-                                    8.4 million (batch, head) slices) */
+                                    8.4 million (batch, head) slices), or a
+                                    library-owned workspace that would have
+                                    to be allocated on a stream under graph
+                                    capture */
 #define FMM_ERR_HIP         (-3) /* a HIP runtime call or kernel launch failed */
 #define FMM_ERR_OOM         (-4) /* workspace allocation failed, or a
                                     caller-provided workspace is too small */

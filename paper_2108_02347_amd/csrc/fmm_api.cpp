@@ -178,6 +178,14 @@ int acquire_ws_locked(void* stream, size_t bytes, void** out) {
   if (hipGetDevice(&dev) != hipSuccess) return FMM_ERR_HIP;
   WsEntry& e = ws_map()[{dev, stream}];
   if (e.bytes < bytes) {
+    // a stream under graph capture can neither allocate nor synchronise: its
+    // workspace has to come from an earlier call outside the capture
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing((hipStream_t)stream, &cs) != hipSuccess) {
+      (void)hipGetLastError();
+      return FMM_ERR_HIP;
+    }
+    if (cs != hipStreamCaptureStatusNone) return FMM_ERR_UNSUPPORTED;
     if (e.ptr) {
       // kernels enqueued earlier on this stream may still read the old buffer
       if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return FMM_ERR_HIP;

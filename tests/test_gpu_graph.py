@@ -88,3 +88,38 @@ def test_graph_replays_match_eager(case):
         del g
     finally:
         binding.set_one_launch(prev)
+
+
+def test_capture_needing_a_new_workspace_is_rejected():
+    # a fresh stream has no library-owned workspace yet, and a stream under
+    # capture cannot allocate one: the call must fail with nothing enqueued
+    B, H, N, d, kw, rank = 2, 2, 700, 32, 9, 2
+    q, k, v, wn, wf = make_inputs(B, H, N, d, "bf16", 1.0 / np.sqrt(d), 1300)
+    tq, tk, tv, twn, twf = upload(q, k, v, wn, wf, "bf16")
+    # one call on the current stream first (one-time kernel set-up), which
+    # leaves the new stream below without a workspace
+    binding.forward(tq, tk, tv, twn, twf, kw, rank, 1)
+    torch.cuda.synchronize()
+    out = torch.full_like(tq, 3.0)
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    status = None
+    with torch.cuda.graph(g, stream=s):
+        try:
+            binding.forward(tq, tk, tv, twn, twf, kw, rank, 1, out=out)
+        except binding.FmmError as e:
+            status = e.status
+    torch.cuda.synchronize()
+    assert status == binding.FMM_ERR_UNSUPPORTED
+    assert bool((out == 3.0).all())
+    del g
+    # after one call on that stream outside the capture, capturing works
+    with torch.cuda.stream(s):
+        want = binding.forward(tq, tk, tv, twn, twf, kw, rank, 1)
+    torch.cuda.synchronize()
+    g2 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g2, stream=s):
+        binding.forward(tq, tk, tv, twn, twf, kw, rank, 1, out=out)
+    g2.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), want.view(torch.int16))
