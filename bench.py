@@ -423,12 +423,16 @@ def _blas_threads():
     return max(n) if n else None
 
 
-def cpu_baseline(host_inputs, w):
+def cpu_baseline(host_inputs, w, gpu_head0=None):
     """The float64 oracle on head 0 of the workload (all rows, both forms),
     timed twice: with every host core this process may use (BLAS pools at
     their default size) and with the BLAS pools limited to one thread.  The
     near-field part is numpy elementwise work and runs on one core either way;
-    the far-field products use the BLAS threads."""
+    the far-field products use the BLAS threads.  When the GPU's outputs for
+    head 0 of the timed steps are given ({"noncausal": [N, d], "causal": [N,
+    d]}), the first run's oracle outputs also give their error: the largest
+    |gpu - oracle| over the largest |oracle| of the head, and the mean of
+    |gpu - oracle| / max(|oracle|, 1e-3 max|oracle|) over all elements."""
     import contextlib
     import numpy as np
     from oracle import fmm_ref as ref
@@ -442,13 +446,29 @@ def cpu_baseline(host_inputs, w):
     tokens = 2.0 * w.B * w.N / w.H  # one head of H, both forms
     affinity = len(os.sched_getaffinity(0))
 
+    outs = {}
+
     def one_run():
         t0 = time.perf_counter()
         for causal in (False, True):
-            ref.fmm_attention_stream(qs, ks, vs, wn[:1], wf[:1], w.band_k, w.rank, causal)
+            outs[causal] = ref.fmm_attention_stream(qs, ks, vs, wn[:1], wf[:1], w.band_k,
+                                                    w.rank, causal)
         return time.perf_counter() - t0
 
     dt_all = one_run()
+    accuracy = None
+    if gpu_head0 is not None:
+        accuracy = {"rows": f"head 0 of {w.H}, all {w.N} rows, the timed steps' outputs",
+                    "tolerance_max_rel": 2e-2}
+        for causal, key in ((False, "noncausal"), (True, "causal")):
+            want = np.asarray(outs[causal], dtype=np.float64)[0, 0]
+            got = np.asarray(gpu_head0[key], dtype=np.float64)
+            top = np.abs(want).max()
+            diff = np.abs(got - want)
+            accuracy[key] = {
+                "max_rel_err": float(f"{diff.max() / top:.3e}"),
+                "floored_mean_rel_err": float(
+                    f"{(diff / np.maximum(np.abs(want), 1e-3 * top)).mean():.3e}")}
     blas_all = _blas_threads()
     single = None
     if threadpool_limits is not None:
@@ -459,7 +479,7 @@ def cpu_baseline(host_inputs, w):
             single = {"value": round(tokens / dt_one, 1), "unit": "tokens/s", "cores": 1,
                       "blas_threads": 1, "seconds": round(dt_one, 2)}
     return {"value": round(tokens / dt_all, 1), "unit": "tokens/s", "cores": affinity,
-            "blas_threads": blas_all, "kind": "oracle",
+            "blas_threads": blas_all, "kind": "oracle", "gpu_accuracy": accuracy,
             "sample": f"head 0 of {w.H}, batch 0, all {w.N} rows, non-causal + causal "
                       f"forward (float64 numpy oracle); {dt_all:.1f} s for {tokens:.0f} "
                       f"token-forwards with the {affinity} cores of this process's affinity "
@@ -514,6 +534,10 @@ def main():
 
     # the timed steps: no per-kernel events attached
     t_step = timed(step, args.steps, args.warmup, torch)
+    # head 0 of the timed steps' outputs, for the comparison with the oracle
+    # in the CPU baseline leg
+    head0 = {"noncausal": out_nc[0, 0].float().cpu().numpy(),
+             "causal": out_c[0, 0].float().cpu().numpy()}
     # the same steps again with a start/stop event pair attached to every
     # kernel dispatch (each then carries a completion signal, which shortens
     # the kernels' own spans and adds gaps between them)
@@ -849,7 +873,7 @@ def main():
         "kernel_source_hash": kernel_source_hash(),
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(host, w)
+        rec["cpu_baseline"] = cpu_baseline(host, w, head0)
     print(json.dumps(rec), flush=True)
 
 
