@@ -49,30 +49,34 @@ namespace {
 
 // FC: causal with at most two maps, whose records are kept twice: in fp32
 // (advanced every tile) and as bf16 operands (RecFrags, rebuilt by the
-// owning wave after each advance).
-template <typename T, int D, bool FC = false>
+// owning wave after each advance).  NM: maps the record area holds (2 or 3).
+// TWO: an LDS budget of half a CU's LDS, so that two workgroups (two waves
+// per SIMD) share a CU, where the rounds still hold a tile (FITS); else the
+// budget of one workgroup per CU.
+template <typename T, int D, bool FC = false, int NM = 3, bool TWO = false>
 struct BwdCfg {
   static constexpr int ST = D + Lay<T>::PAD;
   static constexpr int ROW = ST * (int)sizeof(T);
   static constexpr int TILE = TM * ROW;         // 64 staged rows
   static constexpr int UNIT2 = 2 * 32 * ROW;    // two buffers of one 32-row unit
   static constexpr int STAT_UNIT = 32 * 3 * 4;  // key pass: m, 1/l, D per row
-  static constexpr int BUDGET = 150 * 1024;
-  // the far-field records of up to three maps, kept in LDS for widths up to
+  // the far-field records of up to NM maps, kept in LDS for widths up to
   // 64 (read every tile; the causal ones are also advanced there)
   // (fp32 records, or their bf16 fragments: RecFrags::PER_MAP per map; both
   // for two maps with FC)
   static constexpr int FRAG_MAP = 2 * (D / 16) * (D / 16) * 64 * 8 + (D / 16) * 32 + D * 4;
-  static constexpr int REC_F32 = 3 * D * (D + 1) * 4;
-  static constexpr int REC_FRAG = 3 * FRAG_MAP;
+  static constexpr int REC_F32 = NM * D * (D + 1) * 4;
+  static constexpr int REC_FRAG = NM * FRAG_MAP;
   static constexpr int REC_BYTES =
       D > 64 ? 0 : FC ? 2 * D * (D + 1) * 4 + 2 * FRAG_MAP : (REC_F32 > REC_FRAG ? REC_F32 : REC_FRAG);
   // offset of the fragments within the record area
   static constexpr int FRAG_OFF = FC ? 2 * D * (D + 1) * 4 : 0;
   // tile buffers: phi and dnum rows of the tile (FC: of both maps at once)
   static constexpr int NTB = FC ? 4 : 2;
-  static constexpr int UR_FIT =
-      (BUDGET - NTB * TILE - 256 - 2 * NT * 4 - REC_BYTES) / (UNIT2 + STAT_UNIT);
+  static constexpr int FIXED = NTB * TILE + 256 + 2 * NT * 4 + REC_BYTES;
+  static constexpr bool FITS = (80 * 1024 - FIXED) / (UNIT2 + STAT_UNIT) >= 2;
+  static constexpr int BUDGET = TWO && FITS ? 80 * 1024 : 150 * 1024;
+  static constexpr int UR_FIT = (BUDGET - FIXED) / (UNIT2 + STAT_UNIT);
   static constexpr int UR = UR_FIT > 8 ? 8 : UR_FIT;
   static_assert(UR >= 2, "a round must hold one tile");
   static constexpr int WK = 32 * UR;  // rows per staging round
@@ -349,7 +353,7 @@ __device__ __forceinline__ void near_dq_units(f32x4* dq, const typename QuadOf<T
   mfma_drain();
 }
 
-template <typename T, int D, bool CAUSAL, bool FC>
+template <typename T, int D, bool CAUSAL, bool FC, int NM, bool TWO>
 __global__ __launch_bounds__(NT) void k_bwd_rows(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, T* __restrict__ dq, float* __restrict__ recs,
@@ -357,7 +361,7 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
     float* __restrict__ dwpart, const float* __restrict__ w_near, const float* __restrict__ w_far,
     int H, int N, int band_k, int L, int nseg, int rank, float scale2) {
   using Q = typename QuadOf<T>::type;
-  using C = BwdCfg<T, D, FC>;
+  using C = BwdCfg<T, D, FC, NM, TWO>;
   constexpr int NB = D / 16, ST = C::ST;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
   T* sk = reinterpret_cast<T*>(dyn_smem);
@@ -818,7 +822,7 @@ void launch_seg_grad(const BwdArgs& a, Launcher& L) {
 }
 
 // ------------------------------------------------------------------ key pass
-template <typename T, int D, bool CAUSAL, bool FC>
+template <typename T, int D, bool CAUSAL, bool FC, int NM, bool TWO>
 __global__ __launch_bounds__(NT) void k_bwd_keys(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ drecs,
@@ -826,7 +830,7 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
     const float* __restrict__ w_near, const float* __restrict__ w_far, int H, int N, int band_k,
     int L, int nseg, int rank, float scale2) {
   using Q = typename QuadOf<T>::type;
-  using C = BwdCfg<T, D, FC>;
+  using C = BwdCfg<T, D, FC, NM, TWO>;
   constexpr int NB = D / 16, ST = C::ST;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
   T* sq = reinterpret_cast<T*>(dyn_smem);
@@ -1149,21 +1153,21 @@ __global__ void k_dw_reduce(const float* __restrict__ dwpart, const float* __res
   dw_far[h] = c * (1.f - c) * sf;
 }
 
-template <typename T, int D, bool CAUSAL, bool FC>
+template <typename T, int D, bool CAUSAL, bool FC, int NM = 3, bool TWO = false>
 hipError_t launch_bwd_dcf(const BwdArgs& a, Launcher& L) {
-  using C = BwdCfg<T, D, FC>;
+  using C = BwdCfg<T, D, FC, NM, TWO>;
   static std::atomic<unsigned long long> set_rows{0}, set_keys{0};
-  if (L.note(lds_limit_once((const void*)k_bwd_rows<T, D, CAUSAL, FC>, C::LDS, set_rows)) !=
-          hipSuccess ||
-      L.note(lds_limit_once((const void*)k_bwd_keys<T, D, CAUSAL, FC>, C::LDS, set_keys)) !=
-          hipSuccess)
+  if (L.note(lds_limit_once((const void*)k_bwd_rows<T, D, CAUSAL, FC, NM, TWO>, C::LDS,
+                            set_rows)) != hipSuccess ||
+      L.note(lds_limit_once((const void*)k_bwd_keys<T, D, CAUSAL, FC, NM, TWO>, C::LDS,
+                            set_keys)) != hipSuccess)
     return L.err;
   const float scale2 = 1.4426950408889634f / sqrtf((float)D);
   const int BH = a.B * a.H;
   const size_t REC = (size_t)a.rank * D * (D + 1);
   hipStream_t s = (hipStream_t)a.stream;
   const dim3 grid(BH * a.nseg);
-  L(FMM_KERNEL_BWD_ROWS, k_bwd_rows<T, D, CAUSAL, FC>, grid, dim3(NT), (size_t)C::LDS, s,
+  L(FMM_KERNEL_BWD_ROWS, k_bwd_rows<T, D, CAUSAL, FC, NM, TWO>, grid, dim3(NT), (size_t)C::LDS, s,
     (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, (T*)a.dq,
     CAUSAL ? a.part : a.fin, a.rowstat, a.rowfar, a.dwpart, a.w_near, a.w_far, a.H, a.N,
     a.band_k, a.L, a.nseg, a.rank, scale2);
@@ -1176,7 +1180,7 @@ hipError_t launch_bwd_dcf(const BwdArgs& a, Launcher& L) {
   } else {
     (void)launch_state_sum(L, a.dpart, a.dfin, a.nseg, (int)REC, BH, s);
   }
-  L(FMM_KERNEL_BWD_KEYS, k_bwd_keys<T, D, CAUSAL, FC>, grid, dim3(NT), (size_t)C::LDS, s,
+  L(FMM_KERNEL_BWD_KEYS, k_bwd_keys<T, D, CAUSAL, FC, NM, TWO>, grid, dim3(NT), (size_t)C::LDS, s,
     (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, (T*)a.dk, (T*)a.dv,
     CAUSAL ? a.dpart : a.dfin, (const float*)a.rowstat, (const float*)a.rowfar, a.w_near, a.w_far,
     a.H, a.N, a.band_k, a.L, a.nseg, a.rank, scale2);
@@ -1187,7 +1191,17 @@ hipError_t launch_bwd_dcf(const BwdArgs& a, Launcher& L) {
 
 template <typename T, int D>
 hipError_t launch_bwd_d(const BwdArgs& a, Launcher& L) {
-  if (!a.causal) return launch_bwd_dcf<T, D, false, false>(a, L);
+  if (!a.causal) {
+    // the non-causal passes stay within 256 registers at d <= 64: with the
+    // records of at most two maps their LDS fits two workgroups per CU
+    if constexpr (D <= 64) {
+      if (a.rank <= 2) {
+        constexpr bool two = BwdCfg<T, D, false, 2, true>::FITS;
+        return launch_bwd_dcf<T, D, false, false, 2, two>(a, L);
+      }
+    }
+    return launch_bwd_dcf<T, D, false, false>(a, L);
+  }
   // causal bf16 with at most two maps keeps bf16 operands of its records
   if constexpr (sizeof(T) == 2 && D <= 64) {
     if (a.rank <= 2) return launch_bwd_dcf<T, D, true, true>(a, L);
