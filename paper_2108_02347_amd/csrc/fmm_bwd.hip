@@ -47,13 +47,10 @@
 namespace fmm {
 namespace {
 
-// FC: causal with at most two maps, whose records are kept twice: in fp32
-// (advanced every tile) and as bf16 operands (RecFrags, rebuilt by the
-// owning wave after each advance).  NM: maps the record area holds (2 or 3).
-// TWO: an LDS budget of half a CU's LDS, so that two workgroups (two waves
-// per SIMD) share a CU, where the rounds still hold a tile (FITS); else the
-// budget of one workgroup per CU.
-template <typename T, int D, bool FC = false, int NM = 3, bool TWO = false>
+// NM: maps the record area holds (2 or 3).  TWO: an LDS budget of half a
+// CU's LDS, so that two workgroups (two waves per SIMD) share a CU, where the
+// rounds still hold a tile (FITS); else the budget of one workgroup per CU.
+template <typename T, int D, int NM = 3, bool TWO = false>
 struct BwdCfg {
   static constexpr int ST = D + Lay<T>::PAD;
   static constexpr int ROW = ST * (int)sizeof(T);
@@ -61,18 +58,15 @@ struct BwdCfg {
   static constexpr int UNIT2 = 2 * 32 * ROW;    // two buffers of one 32-row unit
   static constexpr int STAT_UNIT = 32 * 3 * 4;  // key pass: m, 1/l, D per row
   // the far-field records of up to NM maps, kept in LDS for widths up to
-  // 64 (read every tile; the causal ones are also advanced there)
-  // (fp32 records, or their bf16 fragments: RecFrags::PER_MAP per map; both
-  // for two maps with FC)
+  // 64 (read every tile; the causal ones are also advanced there): fp32
+  // records (causal), or their bf16 fragments (non-causal bf16:
+  // RecFrags::PER_MAP per map)
   static constexpr int FRAG_MAP = 2 * (D / 16) * (D / 16) * 64 * 8 + (D / 16) * 32 + D * 4;
   static constexpr int REC_F32 = NM * D * (D + 1) * 4;
   static constexpr int REC_FRAG = NM * FRAG_MAP;
-  static constexpr int REC_BYTES =
-      D > 64 ? 0 : FC ? 2 * D * (D + 1) * 4 + 2 * FRAG_MAP : (REC_F32 > REC_FRAG ? REC_F32 : REC_FRAG);
-  // offset of the fragments within the record area
-  static constexpr int FRAG_OFF = FC ? 2 * D * (D + 1) * 4 : 0;
-  // tile buffers: phi and dnum rows of the tile (FC: of both maps at once)
-  static constexpr int NTB = FC ? 4 : 2;
+  static constexpr int REC_BYTES = D > 64 ? 0 : (REC_F32 > REC_FRAG ? REC_F32 : REC_FRAG);
+  // tile buffers: phi and dnum rows of the tile
+  static constexpr int NTB = 2;
   static constexpr int FIXED = NTB * TILE + 256 + 2 * NT * 4 + REC_BYTES;
   static constexpr bool FITS = (80 * 1024 - FIXED) / (UNIT2 + STAT_UNIT) >= 2;
   static constexpr int BUDGET = TWO && FITS ? 80 * 1024 : 150 * 1024;
@@ -84,10 +78,9 @@ struct BwdCfg {
   // reuses the area for its block reduction (2 x NT floats)
   static constexpr int STAT_BYTES = WK * 12 > 2 * NT * 4 ? WK * 12 : 2 * NT * 4;
   // [buffer A: WK rows][buffer B: WK rows][tile buffers 1, 2][64 floats][stats]
-  // [records][tile buffers 3, 4 (FC)]
+  // [records]
   static constexpr int REC_OFF = 2 * WK * ROW + 2 * TILE + 256 + STAT_BYTES;
-  static constexpr int TB34_OFF = REC_OFF + REC_BYTES;
-  static constexpr int LDS = TB34_OFF + (NTB - 2) * TILE;
+  static constexpr int LDS = REC_OFF + REC_BYTES;
 };
 
 __device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7"); }
@@ -353,15 +346,15 @@ __device__ __forceinline__ void near_dq_units(f32x4* dq, const typename QuadOf<T
   mfma_drain();
 }
 
-template <typename T, int D, bool CAUSAL, bool FC, int NM, bool TWO>
-__global__ __launch_bounds__(NT) void k_bwd_rows(
+template <typename T, int D, bool CAUSAL, int NM, bool TWO>
+__global__ __launch_bounds__(NT, TWO && CAUSAL ? 2 : 1) void k_bwd_rows(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, T* __restrict__ dq, float* __restrict__ recs,
     float* __restrict__ rowstat, float* __restrict__ rowfar,
     float* __restrict__ dwpart, const float* __restrict__ w_near, const float* __restrict__ w_far,
     int H, int N, int band_k, int L, int nseg, int rank, float scale2) {
   using Q = typename QuadOf<T>::type;
-  using C = BwdCfg<T, D, FC, NM, TWO>;
+  using C = BwdCfg<T, D, NM, TWO>;
   constexpr int NB = D / 16, ST = C::ST;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
   T* sk = reinterpret_cast<T*>(dyn_smem);
@@ -378,10 +371,9 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
   const size_t REC = (size_t)rank * D * (D + 1);
   float* grec = CAUSAL ? recs + ((size_t)bh * nseg + seg) * REC : recs + (size_t)bh * REC;
   // bf16 operands of the record: the non-causal record is constant and they
-  // are built once; the causal one (FC) keeps its fp32 copy too and the
-  // operands follow each advance
-  constexpr bool FR = (!CAUSAL || FC) && sizeof(T) == 2 && C::REC_BYTES > 0;
-  unsigned char* frb = dyn_smem + C::REC_OFF + C::FRAG_OFF;
+  // are built once
+  constexpr bool FR = !CAUSAL && sizeof(T) == 2 && C::REC_BYTES > 0;
+  unsigned char* frb = dyn_smem + C::REC_OFF;
   float* srec = reinterpret_cast<float*>(dyn_smem + C::REC_OFF);
   if constexpr (FR) RecFrags<D>::build(frb, grec, rank);
   if constexpr (C::REC_BYTES > 0 && (!FR || CAUSAL)) stage_records(srec, grec, (int)REC);
@@ -458,18 +450,10 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
     }
     // ks: first key of the last staged round, which holds the tile's keys
     // (causal form)
-    // ---- far field, one map at a time (FC: phi of the tile's keys for both
-    // maps staged at once, into tb1 and tb2, and both records advanced after
-    // both maps' products)
+    // ---- far field, one map at a time
     const T* vt = sv + (t0 - ks) * ST;
-    if constexpr (CAUSAL && FC) {
-      __syncthreads();
-      stage_phi_rows<T, D>(sk + (t0 - ks) * ST, t0, N, 0, tb1);
-      if (rank > 1) stage_phi_rows<T, D>(sk + (t0 - ks) * ST, t0, N, 1, tb2);
-      __syncthreads();
-    }
     for (int l = 0; l < rank; ++l) {
-      const T* tbl = CAUSAL && FC && l == 1 ? tb2 : tb1;
+      const T* tbl = tb1;
       Q pq[NB];
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
@@ -484,13 +468,10 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
 #pragma unroll
       for (int nb = 0; nb <= NB; ++nb) num[nb] = zero;
       if constexpr (CAUSAL) {
-        // the tile's keys: phi_l(K_t) into tb1 (FC: staged above); intra-tile
-        // part of num, den
-        if constexpr (!FC) {
-          __syncthreads();
-          stage_phi_rows<T, D>(sk + (t0 - ks) * ST, t0, N, l, tb1);
-          __syncthreads();
-        }
+        // the tile's keys: phi_l(K_t) into tb1; intra-tile part of num, den
+        __syncthreads();
+        stage_phi_rows<T, D>(sk + (t0 - ks) * ST, t0, N, l, tb1);
+        __syncthreads();
         const Q ones = quad_fill<T>(1.f);
         for (int u = 0; u <= (w >> 1); ++u) {
           const bool diag = u == (w >> 1);
@@ -620,24 +601,13 @@ __global__ __launch_bounds__(NT) void k_bwd_rows(
           dqa[cb][i] = fmaf(dg, dph[cb][i] + zf[i] * dden, dqa[cb][i]);
         }
       }
-      if constexpr (CAUSAL && !FC) {
+      if constexpr (CAUSAL) {
         // advance the forward prefix record by the tile's keys (tb1 still
         // holds phi_l(K_t)), unless this is the segment's last tile
         if (t0 + TM < s1) {
           __syncthreads();  // every wave has read record l for this tile
-          record_add<T, D>(rl, tb1, vt, ones_col, ST, w,
-                           FR ? frb + l * RecFrags<D>::PER_MAP : nullptr);
+          record_add<T, D>(rl, tb1, vt, ones_col, ST, w, nullptr);
         }
-      }
-    }
-    if constexpr (CAUSAL && FC) {
-      // both records advance by the tile's keys (tb1, tb2 hold phi_0, phi_1
-      // of them), unless this is the segment's last tile
-      if (t0 + TM < s1) {
-        __syncthreads();  // every wave has read both records for this tile
-        for (int l = 0; l < rank; ++l)
-          record_add<T, D>(rec + (size_t)l * D * (D + 1), l == 1 ? tb2 : tb1, vt, ones_col, ST,
-                           w, FR ? frb + l * RecFrags<D>::PER_MAP : nullptr);
       }
     }
     store_row<T, D>(dq + base, row, N, dqa);
@@ -822,15 +792,15 @@ void launch_seg_grad(const BwdArgs& a, Launcher& L) {
 }
 
 // ------------------------------------------------------------------ key pass
-template <typename T, int D, bool CAUSAL, bool FC, int NM, bool TWO>
-__global__ __launch_bounds__(NT) void k_bwd_keys(
+template <typename T, int D, bool CAUSAL, int NM, bool TWO>
+__global__ __launch_bounds__(NT, TWO && CAUSAL ? 2 : 1) void k_bwd_keys(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ drecs,
     const float* __restrict__ rowstat, const float* __restrict__ rowfar,
     const float* __restrict__ w_near, const float* __restrict__ w_far, int H, int N, int band_k,
     int L, int nseg, int rank, float scale2) {
   using Q = typename QuadOf<T>::type;
-  using C = BwdCfg<T, D, FC, NM, TWO>;
+  using C = BwdCfg<T, D, NM, TWO>;
   constexpr int NB = D / 16, ST = C::ST;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
   T* sq = reinterpret_cast<T*>(dyn_smem);
@@ -847,8 +817,8 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
   const size_t REC = (size_t)rank * D * (D + 1);
   float* gdrec = CAUSAL ? drecs + ((size_t)bh * nseg + seg) * REC : drecs + (size_t)bh * REC;
   // bf16 operands of the dS record, as in the row pass
-  constexpr bool FR = (!CAUSAL || FC) && sizeof(T) == 2 && C::REC_BYTES > 0;
-  unsigned char* frb = dyn_smem + C::REC_OFF + C::FRAG_OFF;
+  constexpr bool FR = !CAUSAL && sizeof(T) == 2 && C::REC_BYTES > 0;
+  unsigned char* frb = dyn_smem + C::REC_OFF;
   float* sdrec = reinterpret_cast<float*>(dyn_smem + C::REC_OFF);
   if constexpr (FR) RecFrags<D>::build(frb, gdrec, rank);
   if constexpr (C::REC_BYTES > 0 && (!FR || CAUSAL)) stage_records(sdrec, gdrec, (int)REC);
@@ -949,15 +919,7 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
       mfma_drain();
     }
     // ---- far field, one map at a time.  Causal: per map the tile's rows as
-    // phi_l(q) rows, dnum = c g / den rows, and dden (FC: both maps staged at
-    // once, map 1 into tb3, tb4 and the statistics area, and both records
-    // advanced after both maps' products)
-    T* tb3 = reinterpret_cast<T*>(dyn_smem + C::TB34_OFF);
-    T* tb4 = tb3 + TM * ST;
-    auto phq_of = [&](int l) { return CAUSAL && FC && l == 1 ? tb3 : tb1; };
-    auto dnr_of = [&](int l) { return CAUSAL && FC && l == 1 ? tb4 : tb2; };
-    auto dd_of = [&](int l) { return CAUSAL && FC && l == 1 ? stat + 64 : dden_s; };
-    auto cd_of = [&](int l) { return CAUSAL && FC ? stat + 128 + 64 * l : stat; };
+    // phi_l(q) rows, dnum = c g / den rows, and dden
     auto reload_tile = [&]() {
       if (!staged_tile) {
         RowCopy<T, D, NT, 64> cq, cg;
@@ -973,8 +935,8 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
         const int i = t0 + threadIdx.x;
         const bool ok = i < N;
         const float* fp = rowfar + (((size_t)bh * N + (ok ? i : 0)) * rank + l) * 2;
-        dd_of(l)[threadIdx.x] = ok ? fp[1] : 0.f;
-        cd_of(l)[threadIdx.x] = ok ? sfw * fp[0] : 0.f;
+        dden_s[threadIdx.x] = ok ? fp[1] : 0.f;
+        stat[threadIdx.x] = ok ? sfw * fp[0] : 0.f;
       }
     };
     auto dnum_rows = [&](T* dst, const float* cd) {
@@ -1000,21 +962,10 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
         *reinterpret_cast<uint4*>(dst + rr * ST + c * LY::EPC) = outw;
       }
     };
-    if constexpr (CAUSAL && FC) {
-      __syncthreads();
-      reload_tile();
-      for (int l = 0; l < rank; ++l) far_row_terms(l);
-      __syncthreads();
-      for (int l = 0; l < rank; ++l) {
-        stage_phi_rows<T, D>(sq, t0, N, l, phq_of(l));
-        dnum_rows(dnr_of(l), cd_of(l));
-      }
-      __syncthreads();
-    }
     for (int l = 0; l < rank; ++l) {
-      const T* phq = phq_of(l);
-      const T* dnr = dnr_of(l);
-      const float* ddl = dd_of(l);
+      const T* phq = tb1;
+      const T* dnr = tb2;
+      const float* ddl = dden_s;
       Q pk[NB];
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) {
@@ -1029,15 +980,13 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
 #pragma unroll
       for (int cb = 0; cb < NB; ++cb) dph[cb] = zero;
       if constexpr (CAUSAL) {
-        if constexpr (!FC) {
-          __syncthreads();
-          reload_tile();
-          far_row_terms(l);
-          __syncthreads();
-          stage_phi_rows<T, D>(sq, t0, N, l, tb1);
-          dnum_rows(tb2, stat);
-          __syncthreads();
-        }
+        __syncthreads();
+        reload_tile();
+        far_row_terms(l);
+        __syncthreads();
+        stage_phi_rows<T, D>(sq, t0, N, l, tb1);
+        dnum_rows(tb2, stat);
+        __syncthreads();
         // rows i >= j of the tile: units (w >> 1) .. 1, the first one masked
         for (int u = (w >> 1); u < 2; ++u) {
           const bool diag = u == (w >> 1);
@@ -1112,22 +1061,13 @@ __global__ __launch_bounds__(NT) void k_bwd_keys(
           dka[cb][i] = fmaf(dg, dph[cb][i] + zf[i], dka[cb][i]);
         }
       }
-      if constexpr (CAUSAL && !FC) {
+      if constexpr (CAUSAL) {
         // advance the suffix record by the tile's rows, unless this is the
         // segment's first tile (the last one walked)
         if (tt + 1 < ntile) {
           __syncthreads();  // every wave has read record l for this tile
-          record_add<T, D>(drl, tb1, tb2, dden_s, ST, w,
-                           FR ? frb + l * RecFrags<D>::PER_MAP : nullptr);
+          record_add<T, D>(drl, tb1, tb2, dden_s, ST, w, nullptr);
         }
-      }
-    }
-    if constexpr (CAUSAL && FC) {
-      if (tt + 1 < ntile) {
-        __syncthreads();  // every wave has read both records for this tile
-        for (int l = 0; l < rank; ++l)
-          record_add<T, D>(drec + (size_t)l * D * (D + 1), phq_of(l), dnr_of(l), dd_of(l), ST, w,
-                           FR ? frb + l * RecFrags<D>::PER_MAP : nullptr);
       }
     }
     store_row<T, D>(dk + base, key, N, dka);
@@ -1153,13 +1093,13 @@ __global__ void k_dw_reduce(const float* __restrict__ dwpart, const float* __res
   dw_far[h] = c * (1.f - c) * sf;
 }
 
-template <typename T, int D, bool CAUSAL, bool FC, int NM = 3, bool TWO = false>
+template <typename T, int D, bool CAUSAL, int NM = 3, bool TWO = false>
 hipError_t launch_bwd_dcf(const BwdArgs& a, Launcher& L) {
-  using C = BwdCfg<T, D, FC, NM, TWO>;
+  using C = BwdCfg<T, D, NM, TWO>;
   static std::atomic<unsigned long long> set_rows{0}, set_keys{0};
-  if (L.note(lds_limit_once((const void*)k_bwd_rows<T, D, CAUSAL, FC, NM, TWO>, C::LDS,
+  if (L.note(lds_limit_once((const void*)k_bwd_rows<T, D, CAUSAL, NM, TWO>, C::LDS,
                             set_rows)) != hipSuccess ||
-      L.note(lds_limit_once((const void*)k_bwd_keys<T, D, CAUSAL, FC, NM, TWO>, C::LDS,
+      L.note(lds_limit_once((const void*)k_bwd_keys<T, D, CAUSAL, NM, TWO>, C::LDS,
                             set_keys)) != hipSuccess)
     return L.err;
   const float scale2 = 1.4426950408889634f / sqrtf((float)D);
@@ -1167,7 +1107,7 @@ hipError_t launch_bwd_dcf(const BwdArgs& a, Launcher& L) {
   const size_t REC = (size_t)a.rank * D * (D + 1);
   hipStream_t s = (hipStream_t)a.stream;
   const dim3 grid(BH * a.nseg);
-  L(FMM_KERNEL_BWD_ROWS, k_bwd_rows<T, D, CAUSAL, FC, NM, TWO>, grid, dim3(NT), (size_t)C::LDS, s,
+  L(FMM_KERNEL_BWD_ROWS, k_bwd_rows<T, D, CAUSAL, NM, TWO>, grid, dim3(NT), (size_t)C::LDS, s,
     (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, (T*)a.dq,
     CAUSAL ? a.part : a.fin, a.rowstat, a.rowfar, a.dwpart, a.w_near, a.w_far, a.H, a.N,
     a.band_k, a.L, a.nseg, a.rank, scale2);
@@ -1180,7 +1120,7 @@ hipError_t launch_bwd_dcf(const BwdArgs& a, Launcher& L) {
   } else {
     (void)launch_state_sum(L, a.dpart, a.dfin, a.nseg, (int)REC, BH, s);
   }
-  L(FMM_KERNEL_BWD_KEYS, k_bwd_keys<T, D, CAUSAL, FC, NM, TWO>, grid, dim3(NT), (size_t)C::LDS, s,
+  L(FMM_KERNEL_BWD_KEYS, k_bwd_keys<T, D, CAUSAL, NM, TWO>, grid, dim3(NT), (size_t)C::LDS, s,
     (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, (T*)a.dk, (T*)a.dv,
     CAUSAL ? a.dpart : a.dfin, (const float*)a.rowstat, (const float*)a.rowfar, a.w_near, a.w_far,
     a.H, a.N, a.band_k, a.L, a.nseg, a.rank, scale2);
@@ -1191,22 +1131,17 @@ hipError_t launch_bwd_dcf(const BwdArgs& a, Launcher& L) {
 
 template <typename T, int D>
 hipError_t launch_bwd_d(const BwdArgs& a, Launcher& L) {
-  if (!a.causal) {
-    // the non-causal passes stay within 256 registers at d <= 64: with the
-    // records of at most two maps their LDS fits two workgroups per CU
-    if constexpr (D <= 64) {
-      if (a.rank <= 2) {
-        constexpr bool two = BwdCfg<T, D, false, 2, true>::FITS;
-        return launch_bwd_dcf<T, D, false, false, 2, two>(a, L);
-      }
+  // at d <= 64 with one or two maps the records of two maps leave room for
+  // two workgroups per CU (two waves per SIMD; the causal passes are held
+  // to 256 registers for it)
+  if constexpr (D <= 64) {
+    if (a.rank <= 2) {
+      constexpr bool two = BwdCfg<T, D, 2, true>::FITS;
+      return a.causal ? launch_bwd_dcf<T, D, true, 2, two>(a, L)
+                      : launch_bwd_dcf<T, D, false, 2, two>(a, L);
     }
-    return launch_bwd_dcf<T, D, false, false>(a, L);
   }
-  // causal bf16 with at most two maps keeps bf16 operands of its records
-  if constexpr (sizeof(T) == 2 && D <= 64) {
-    if (a.rank <= 2) return launch_bwd_dcf<T, D, true, true>(a, L);
-  }
-  return launch_bwd_dcf<T, D, true, false>(a, L);
+  return a.causal ? launch_bwd_dcf<T, D, true>(a, L) : launch_bwd_dcf<T, D, false>(a, L);
 }
 
 template <typename T>
