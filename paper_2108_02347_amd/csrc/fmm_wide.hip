@@ -30,16 +30,20 @@
 namespace fmm {
 namespace {
 
-template <typename T, int D>
+// TWO: an LDS budget of half a CU's LDS, so that two workgroups (two waves
+// per SIMD) share a CU, where a round still holds a tile of keys (FITS);
+// else the budget of one workgroup per CU.
+template <typename T, int D, bool TWO = false>
 struct WideCfg {
   static constexpr int ST = D + Lay<T>::PAD;
   static constexpr int ROW = ST * (int)sizeof(T);
   static constexpr int PK_BYTES = TM * ROW;     // phi_l of the tile's keys (causal)
   static constexpr int UNIT2 = 2 * 32 * ROW;    // K and V rows of one 32-key unit
-  static constexpr int BUDGET = 150 * 1024;
   // the state records of up to three maps, kept in LDS for widths up to 64
   // (read every tile; the causal ones are also advanced there)
   static constexpr int REC_BYTES = D <= 64 ? 3 * D * (D + 1) * 4 : 0;
+  static constexpr bool FITS = (80 * 1024 - PK_BYTES - REC_BYTES) / UNIT2 >= 2;
+  static constexpr int BUDGET = TWO && FITS ? 80 * 1024 : 150 * 1024;
   static constexpr int UR_FIT = (BUDGET - PK_BYTES - REC_BYTES) / UNIT2;
   static constexpr int UR = UR_FIT > 8 ? 8 : UR_FIT;
   static_assert(UR >= 2, "a round must hold one tile of keys");
@@ -153,7 +157,7 @@ __device__ __forceinline__ void intra_map(const T* pk, const T* vt, int ST, int 
   mfma_drain();
 }
 
-template <typename T, int D, bool CAUSAL, bool JOINT>
+template <typename T, int D, bool CAUSAL, bool JOINT, bool TWO>
 __global__ __launch_bounds__(NT) void k_wide(const T* __restrict__ q, const T* __restrict__ k,
                                              const T* __restrict__ v, T* __restrict__ out,
                                              float* __restrict__ recs,
@@ -162,7 +166,7 @@ __global__ __launch_bounds__(NT) void k_wide(const T* __restrict__ q, const T* _
                                              int band_k, int L, int nseg, int rank,
                                              float scale2) {
   using Q = typename QuadOf<T>::type;
-  using C = WideCfg<T, D>;
+  using C = WideCfg<T, D, TWO>;
   constexpr int NB = D / 16, ST = C::ST;
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
   T* sk = reinterpret_cast<T*>(dyn_smem);
@@ -305,13 +309,16 @@ __global__ __launch_bounds__(NT) void k_wide(const T* __restrict__ q, const T* _
 
 template <typename T, int D, bool CAUSAL, bool JOINT>
 hipError_t launch_wide_k(const LaunchArgs& a, Launcher& L, float* recs) {
-  using C = WideCfg<T, D>;
+  // two workgroups per CU where the LDS allows it at d <= 64 (the kernels
+  // stay within 256 registers there)
+  constexpr bool TWO = D <= 64 && WideCfg<T, D, true>::FITS;
+  using C = WideCfg<T, D, TWO>;
   static std::atomic<unsigned long long> lds_set{0};
-  if (L.note(lds_limit_once((const void*)k_wide<T, D, CAUSAL, JOINT>, C::LDS, lds_set)) !=
+  if (L.note(lds_limit_once((const void*)k_wide<T, D, CAUSAL, JOINT, TWO>, C::LDS, lds_set)) !=
       hipSuccess)
     return L.err;
   const float scale2 = 1.4426950408889634f / sqrtf((float)D);
-  L(a.causal ? FMM_KERNEL_CAUSAL_APPLY : FMM_KERNEL_BAND_APPLY, k_wide<T, D, CAUSAL, JOINT>,
+  L(a.causal ? FMM_KERNEL_CAUSAL_APPLY : FMM_KERNEL_BAND_APPLY, k_wide<T, D, CAUSAL, JOINT, TWO>,
     dim3(a.B * a.H * a.nseg), dim3(NT), (size_t)C::LDS, (hipStream_t)a.stream, (const T*)a.q,
     (const T*)a.k, (const T*)a.v, (T*)a.out, recs, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L,
     a.nseg, a.rank, scale2);
