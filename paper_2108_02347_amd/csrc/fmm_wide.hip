@@ -158,7 +158,7 @@ __device__ __forceinline__ void intra_map(const T* pk, const T* vt, int ST, int 
 }
 
 template <typename T, int D, bool CAUSAL, bool JOINT, bool TWO>
-__global__ __launch_bounds__(NT) void k_wide(const T* __restrict__ q, const T* __restrict__ k,
+__global__ __launch_bounds__(NT, TWO && D > 64 && (CAUSAL || JOINT) ? 2 : 1) void k_wide(const T* __restrict__ q, const T* __restrict__ k,
                                              const T* __restrict__ v, T* __restrict__ out,
                                              float* __restrict__ recs,
                                              const float* __restrict__ w_near,
@@ -309,9 +309,10 @@ __global__ __launch_bounds__(NT) void k_wide(const T* __restrict__ q, const T* _
 
 template <typename T, int D, bool CAUSAL, bool JOINT>
 hipError_t launch_wide_k(const LaunchArgs& a, Launcher& L, float* recs) {
-  // two workgroups per CU where the LDS allows it at d <= 64 (the kernels
-  // stay within 256 registers there)
-  constexpr bool TWO = D <= 64 && WideCfg<T, D, true>::FITS;
+  // two workgroups per CU where the LDS allows it (bf16 at any width, fp32
+  // up to 32); the kernels then stay within 256 registers (held there at
+  // d = 128 causal or joint, a few of them spilled, which still pays)
+  constexpr bool TWO = (D <= 64 || sizeof(T) == 2) && WideCfg<T, D, true>::FITS;
   using C = WideCfg<T, D, TWO>;
   static std::atomic<unsigned long long> lds_set{0};
   if (L.note(lds_limit_once((const void*)k_wide<T, D, CAUSAL, JOINT, TWO>, C::LDS, lds_set)) !=
