@@ -661,13 +661,13 @@ __global__ __launch_bounds__(SNTB) void k_seg_grad(const T* __restrict__ q,
   constexpr int ST = D + Lay<T>::PAD;
   constexpr int RS = SWB / NB > 0 ? SWB / NB : 1;
   constexpr int TK = 64;
-  // the two 64-row staging buffers, reused for the reduction tree at the end
-  constexpr int STAGE = 2 * TK * ST * (int)sizeof(T);
+  // two 64-row chunks of q and dout double-buffered (the next chunk's loads
+  // in flight during the current one's products), reused for the reduction
+  // tree at the end
+  constexpr int STAGE = 2 * 2 * TK * ST * (int)sizeof(T);
   constexpr int REDB = SWB / 2 * (NB + 1) * 64 * 16;
   __shared__ __attribute__((aligned(16))) unsigned char s_buf[STAGE > REDB ? STAGE : REDB];
-  __shared__ float s_sc[R][TK], s_dd[R][TK];
-  T* s_q = reinterpret_cast<T*>(s_buf);
-  T* s_g = s_q + TK * ST;
+  __shared__ float s_sc[2][R][TK], s_dd[2][R][TK];
   const int seg = blockIdx.x % nseg, bh = blockIdx.x / nseg, h = bh % H;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, r = lane & 15, g = lane >> 4;
@@ -676,28 +676,64 @@ __global__ __launch_bounds__(SNTB) void k_seg_grad(const T* __restrict__ q,
   const int r0 = seg * L, r1 = min(N, r0 + L);
   const size_t base = (size_t)bh * N * D;
   const float sfw = sigmoidf_exact(w_far[h]);
+  const int nchunk = (r1 - r0 + TK - 1) / TK;
   f32x4 acc[R][NB + 1];
 #pragma unroll
   for (int l = 0; l < R; ++l)
 #pragma unroll
     for (int eb = 0; eb <= NB; ++eb) acc[l][eb] = f32x4{0.f, 0.f, 0.f, 0.f};
   auto ident = [](int i) { return i; };
-  for (int c0 = r0; c0 < r1; c0 += TK) {
-    const int nrow = min(TK, r1 - c0);
-    RowCopy<T, D, SNTB, TK> cq, cg;
-    cq.load(q + base, c0, nrow, r1);
-    cg.load(dout + base, c0, nrow, r1);
-    __syncthreads();  // the previous chunk is consumed
-    cq.store(s_q, ST, TK, ident);
-    cg.store(s_g, ST, TK, ident);
-    for (int t = threadIdx.x; t < R * TK; t += SNTB) {
-      const int l = t / TK, i = t % TK;
-      const bool ok = c0 + i < r1;
-      const float* fp = rowfar + (((size_t)bh * N + (ok ? c0 + i : 0)) * R + l) * 2;
-      s_sc[l][i] = ok ? sfw * fp[0] : 0.f;
-      s_dd[l][i] = ok ? fp[1] : 0.f;
+  // a chunk's per-row (c / den, dden) pairs: thread t < R TK holds map t / TK,
+  // row t % TK (zeros past the segment)
+  // (a buffer over the segment's rows: pairs past it read as zeros, so the
+  // loads need no branch)
+  static_assert(R * TK <= SNTB, "one pair per thread");
+  const __amdgpu_buffer_rsrc_t far_rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(rowfar + ((size_t)bh * N + r0) * R * 2), 0, (r1 - r0) * R * 8,
+      0x00020000);
+  auto load_far = [&](int c0) {
+    const int t = threadIdx.x, l = t / TK, i = t % TK;
+    const bool on = t < R * TK && c0 + i < r1;
+    const uint32_t off = on ? (uint32_t)(((c0 - r0 + i) * R + l) * 8) : 0x80000000u;
+    return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(far_rs, off, 0, 0));
+  };
+  auto store_far = [&](int buf, float2 f) {
+    const int t = threadIdx.x;
+    if (t < R * TK) {
+      s_sc[buf][t / TK][t % TK] = sfw * f.x;
+      s_dd[buf][t / TK][t % TK] = f.y;
     }
-    __syncthreads();
+  };
+  auto sq_of = [&](int buf) { return reinterpret_cast<T*>(s_buf) + buf * 2 * TK * ST; };
+  // the first two chunks' loads together, the first stored
+  RowCopy<T, D, SNTB, TK> cq, cg, cq0, cg0;
+  cq0.load(q + base, r0, min(TK, r1 - r0), r1);
+  cg0.load(dout + base, r0, min(TK, r1 - r0), r1);
+  float2 f0 = load_far(r0);
+  cq.load(q + base, r0 + TK, min(TK, r1 - r0 - TK), r1);
+  cg.load(dout + base, r0 + TK, min(TK, r1 - r0 - TK), r1);
+  float2 f1 = load_far(r0 + TK);
+  cq0.store(sq_of(0), ST, TK, ident);
+  cg0.store(sq_of(0) + TK * ST, ST, TK, ident);
+  store_far(0, f0);
+  for (int c = 0; c < nchunk; ++c) {
+    const int c0 = r0 + c * TK;
+    __syncthreads();  // chunk c is in its buffer; chunk c - 1's buffer is free
+    if (c + 1 < nchunk) {
+      cq.store(sq_of((c + 1) & 1), ST, TK, ident);
+      cg.store(sq_of((c + 1) & 1) + TK * ST, ST, TK, ident);
+      store_far((c + 1) & 1, f1);
+    }
+    if (c + 2 < nchunk) {
+      const int cn = c0 + 2 * TK;
+      cq.load(q + base, cn, min(TK, r1 - cn), r1);
+      cg.load(dout + base, cn, min(TK, r1 - cn), r1);
+      f1 = load_far(cn);
+    }
+    const T* s_q = sq_of(c & 1);
+    const T* s_g = s_q + TK * ST;
+    const float(*sc)[TK] = s_sc[c & 1];
+    const float(*dd)[TK] = s_dd[c & 1];
     if (owner) {
 #pragma unroll
       for (int u = 0; u < TK / 32; ++u) {
@@ -723,7 +759,7 @@ __global__ __launch_bounds__(SNTB) void k_seg_grad(const T* __restrict__ q,
             for (int b = 0; b < 2; ++b) {
               quad_to_f32(ld_tquad(s_g, 32 * u + 16 * b, 16 * eb, ST), gb[b]);
 #pragma unroll
-              for (int i = 0; i < 4; ++i) gb[b][i] *= s_sc[l][32 * u + 16 * b + 4 * g + i];
+              for (int i = 0; i < 4; ++i) gb[b][i] *= sc[l][32 * u + 16 * b + 4 * g + i];
             }
             acc[l][eb] = mma_step2(a0, a1, f32_to_quad<T>(gb[0]), f32_to_quad<T>(gb[1]),
                                    acc[l][eb]);
@@ -733,7 +769,7 @@ __global__ __launch_bounds__(SNTB) void k_seg_grad(const T* __restrict__ q,
           for (int b = 0; b < 2; ++b)
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-              zb[b][i] = r == 0 ? s_dd[l][32 * u + 16 * b + 4 * g + i] : 0.f;
+              zb[b][i] = r == 0 ? dd[l][32 * u + 16 * b + 4 * g + i] : 0.f;
           acc[l][NB] = mma_step2(a0, a1, f32_to_quad<T>(zb[0]), f32_to_quad<T>(zb[1]),
                                  acc[l][NB]);
         }
