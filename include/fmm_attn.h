@@ -1,6 +1,7 @@
 /*
- * fmm_attn.h - C ABI of the FMMformer attention forward operator on AMD
- * MI355X (gfx950).
+ * fmm_attn.h - C ABI of the FMMformer attention operator on AMD MI355X
+ * (gfx950): the forward in its forms, its backward, the attention layer
+ * around it and the fast-weight far field.
  *
  * The operator (FMMformer, arXiv 2108.02347) blends a banded softmax "near
  * field" with a kernelized low-rank "far field", per batch b, head h and
