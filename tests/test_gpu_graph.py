@@ -91,15 +91,16 @@ def test_graph_replays_match_eager(case):
 
 
 def test_capture_needing_a_new_workspace_is_rejected():
-    # a fresh stream has no library-owned workspace yet, and a stream under
-    # capture cannot allocate one: the call must fail with nothing enqueued
+    # a stream without a library-owned workspace cannot get one while it is
+    # under capture: the call must fail with nothing enqueued
     B, H, N, d, kw, rank = 2, 2, 700, 32, 9, 2
     q, k, v, wn, wf = make_inputs(B, H, N, d, "bf16", 1.0 / np.sqrt(d), 1300)
     tq, tk, tv, twn, twf = upload(q, k, v, wn, wf, "bf16")
-    # one call on the current stream first (one-time kernel set-up), which
-    # leaves the new stream below without a workspace
+    # one call first (one-time kernel set-up), then every workspace freed, so
+    # that the stream below has none whichever stream of torch's pool it is
     binding.forward(tq, tk, tv, twn, twf, kw, rank, 1)
     torch.cuda.synchronize()
+    binding.release_workspace()
     out = torch.full_like(tq, 3.0)
     s = torch.cuda.Stream()
     g = torch.cuda.CUDAGraph()
