@@ -246,6 +246,30 @@ def backward(q, k, v, dout, w_near, w_far, band_k: int, rank: int, causal: bool)
     return dq, dk, dv, dwn, dwf
 
 
+class _FmmAttention(torch.autograd.Function):
+    """The operator (per-map normalisation) as a torch.autograd function: its
+    forward and backward are the library's entry points."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, w_near, w_far, band_k, rank, causal):
+        ctx.save_for_backward(q, k, v, w_near, w_far)
+        ctx.args = (int(band_k), int(rank), bool(causal))
+        return forward(q, k, v, w_near, w_far, band_k, rank, causal)
+
+    @staticmethod
+    def backward(ctx, g):
+        q, k, v, w_near, w_far = ctx.saved_tensors
+        dq, dk, dv, dwn, dwf = backward(q, k, v, g.contiguous(), w_near, w_far, *ctx.args)
+        return dq, dk, dv, dwn, dwf, None, None, None
+
+
+def fmm_attention(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool):
+    """The operator as a differentiable function of q, k, v and the two blend
+    logits (torch.autograd), for training through it: out = forward(...), and
+    out's gradient reaches q, k, v, w_near and w_far through backward(...)."""
+    return _FmmAttention.apply(q, k, v, w_near, w_far, band_k, rank, causal)
+
+
 def layer_forward(x, w_qkv, w_out, heads: int, w_near, w_far, band_k: int, rank: int,
                   causal: bool, out=None):
     """The attention layer: [q | k | v] = x W_qkv, the operator per head, the

@@ -1,0 +1,55 @@
+"""The operator as a torch.autograd function (binding.fmm_attention): its
+output is the forward entry point's and the gradients that autograd hands to
+q, k, v and the two blend logits are the backward entry point's, bit for bit
+(the entry points themselves are checked against the float64 oracle in the
+forward and backward tests)."""
+
+import numpy as np
+import pytest
+import torch
+
+from fmm_testlib import log, upload
+from paper_2108_02347_amd import binding
+from paper_2108_02347_amd.inputs import make_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("dtype,d,causal", [("bf16", 64, 0), ("bf16", 64, 1), ("f32", 32, 1),
+                                            ("bf16", 32, 0)])
+def test_autograd_matches_entry_points(dtype, d, causal):
+    B, H, N, kw, rank = 2, 2, 1000, 32, 2
+    log(f"autograd B={B} H={H} N={N} d={d} k={kw} r={rank} causal={causal} {dtype}")
+    q, k, v, wn, wf = make_inputs(B, H, N, d, dtype, 1.0 / np.sqrt(d), 1600 + d + causal)
+    t = upload(q, k, v, wn, wf, dtype)
+    gen = torch.Generator(device="cuda:0")
+    gen.manual_seed(1601)
+    g = torch.randn(t[0].shape, generator=gen, device="cuda:0").to(t[0].dtype)
+    leaves = [x.clone().requires_grad_(True) for x in t]
+    out = binding.fmm_attention(*leaves, kw, rank, causal)
+    # the loss sum(out * g): its gradient with respect to out is g
+    (out.float() * g.float()).sum().backward()
+    want_out = binding.forward(*t, kw, rank, causal)
+    want = binding.backward(t[0], t[1], t[2], g, t[3], t[4], kw, rank, causal)
+    torch.cuda.synchronize()
+    assert torch.equal(out.detach(), want_out)
+    for name, leaf, w in zip(("q", "k", "v", "w_near", "w_far"), leaves, want):
+        assert leaf.grad is not None and leaf.grad.shape == leaf.shape, name
+        assert torch.equal(leaf.grad, w), name
+
+
+def test_autograd_only_where_asked():
+    # inputs without requires_grad get no gradient; the others still do
+    B, H, N, d, kw, rank = 1, 2, 700, 32, 16, 2
+    q, k, v, wn, wf = make_inputs(B, H, N, d, "bf16", 1.0 / np.sqrt(d), 1650)
+    tq, tk, tv, twn, twf = upload(q, k, v, wn, wf, "bf16")
+    tq.requires_grad_(True)
+    twf.requires_grad_(True)
+    out = binding.fmm_attention(tq, tk, tv, twn, twf, kw, rank, 0)
+    out.float().sum().backward()
+    torch.cuda.synchronize()
+    assert tq.grad is not None and twf.grad is not None
+    assert tk.grad is None and tv.grad is None and twn.grad is None
+    want = binding.backward(tq.detach(), tk, tv, torch.ones_like(out), twn, twf.detach(), kw,
+                            rank, 0)
+    assert torch.equal(tq.grad, want[0]) and torch.equal(twf.grad, want[4])
