@@ -222,8 +222,7 @@ size_t fmm_attn_noalloc_max_bytes(void);
  * truncated at i (so the key-side far gradients are suffix sums over the rows
  * i >= j), the feature-map derivatives and the sigmoid's.  q, k, v, dout are
  * read only; dq, dk, dv overlap none of them nor each other.  dtype is
- * FMM_DTYPE_F32 or FMM_DTYPE_BF16 (all gradients accumulated in fp32); fp32
- * storage at d = 128 returns FMM_ERR_UNSUPPORTED (bf16 is supported).  Uses
+ * FMM_DTYPE_F32 or FMM_DTYPE_BF16 (all gradients accumulated in fp32).  Uses
  * the library-owned workspace of (device, stream): the forward state records,
  * the same amount for the far-field gradient state, and 12 + 8 rank bytes per
  * row.  Errors as the forward.

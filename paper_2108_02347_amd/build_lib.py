@@ -17,6 +17,13 @@ CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libfmm_attn.so")
 SOURCES = ["fmm_kernels.hip", "fmm_wide.hip", "fmm_bwd.hip", "fmm_pair.hip", "fmm_causal.hip",
            "fmm_noalloc.hip", "fmm_layer.hip", "fmm_fastweight.hip", "fmm_api.cpp"]
+# translation units compiled a second time with other options: (source, object
+# name, extra flags, whether MFMA results are forced into vector registers)
+VARIANTS = [
+    # the backward's fp32 d = 128 passes: one workgroup per CU, with the
+    # accumulation registers beside the vector registers
+    ("fmm_bwd.hip", "fmm_bwd_f32_d128", ["-DFMM_BWD_F32_D128"], False),
+]
 HEADERS = ["fmm_device.h", "fmm_launch.h", "fmm_oct.h", "fmm_apply.h"]
 
 
@@ -27,18 +34,18 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found; the HIP library cannot be built")
 
 
-def _flags():
-    return [
+def _flags(vgpr_form: bool = True):
+    f = [
         "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
         # keep the compiler from forming packed fp32 instructions
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    ]
+    if vgpr_form:
         # keep MFMA accumulators in ordinary VGPRs: the kernels scale and
         # blend them with VALU code, which would otherwise copy them out of
         # and back into AGPRs
-        "-mllvm", "-amdgpu-mfma-vgpr-form=1",
-        "-Wno-unused-result",
-        "-I", os.path.join(ROOT, "include"),
-    ]
+        f += ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
+    return f + ["-Wno-unused-result", "-I", os.path.join(ROOT, "include")]
 
 
 def build(verbose: bool = False) -> str:
@@ -48,13 +55,14 @@ def build(verbose: bool = False) -> str:
     tmpdir = tempfile.mkdtemp(prefix="fmm_build_")
     try:
         objs, procs = [], []
-        for src in SOURCES:
-            obj = os.path.join(tmpdir, src + ".o")
-            cmd = [cc] + _flags() + ["-c", os.path.join(CSRC, src), "-o", obj]
+        units = [(src, src, [], True) for src in SOURCES] + VARIANTS
+        for src, name, extra, vgpr_form in units:
+            obj = os.path.join(tmpdir, name + ".o")
+            cmd = [cc] + _flags(vgpr_form) + extra + ["-c", os.path.join(CSRC, src), "-o", obj]
             if verbose:
                 print(" ".join(cmd), flush=True)
-            procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE,
-                                                stderr=subprocess.STDOUT, text=True)))
+            procs.append((name, subprocess.Popen(cmd, stdout=subprocess.PIPE,
+                                                 stderr=subprocess.STDOUT, text=True)))
             objs.append(obj)
         failed = []
         for src, pr in procs:

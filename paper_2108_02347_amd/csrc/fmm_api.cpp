@@ -410,7 +410,6 @@ int run_backward(const void* q, const void* k, const void* v, const void* dout, 
                     FMM_FAR_NORM_PER_MAP);
   if (st != FMM_OK) return st;
   if (!dout || !dk || !dv || !dw_near || !dw_far) return FMM_ERR_INVALID_ARG;
-  if (d == 128 && dtype == FMM_DTYPE_F32) return FMM_ERR_UNSUPPORTED;
   const size_t es = dtype == FMM_DTYPE_BF16 ? 2 : 4;
   const size_t bytes = (size_t)B * H * N * d * es;  // fits: validate checked it
   for (const void* p : {dout, (const void*)dk, (const void*)dv})

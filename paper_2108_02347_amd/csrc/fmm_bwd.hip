@@ -45,6 +45,11 @@
 #include "fmm_launch.h"
 
 namespace fmm {
+
+// The fp32 d = 128 passes, defined in the second compilation of this file
+// (with FMM_BWD_F32_D128, see the end of the file).
+hipError_t launch_backward_f32_d128(const BwdArgs& a, Launcher& L);
+
 namespace {
 
 // NM: maps the record area holds (2 or 3).  TWO: an LDS budget of half a
@@ -1180,6 +1185,7 @@ hipError_t launch_bwd_d(const BwdArgs& a, Launcher& L) {
   return a.causal ? launch_bwd_dcf<T, D, true>(a, L) : launch_bwd_dcf<T, D, false>(a, L);
 }
 
+#ifndef FMM_BWD_F32_D128
 template <typename T>
 hipError_t launch_bwd_t(const BwdArgs& a, Launcher& L) {
   switch (a.d) {
@@ -1187,18 +1193,29 @@ hipError_t launch_bwd_t(const BwdArgs& a, Launcher& L) {
     case 32: return launch_bwd_d<T, 32>(a, L);
     case 64: return launch_bwd_d<T, 64>(a, L);
     case 128:
-      // fp32 at d = 128 holds twice the operand registers of bf16 and is not
-      // built (the host rejects it as unsupported)
+      // fp32 at d = 128 is built in a translation unit of its own (below)
       if constexpr (sizeof(T) == 2) return launch_bwd_d<T, 128>(a, L);
-      return L.note(hipErrorInvalidConfiguration);
+      return launch_backward_f32_d128(a, L);
     default: return L.note(hipErrorInvalidValue);
   }
 }
+#endif
 
 }  // namespace
 
+#ifdef FMM_BWD_F32_D128
+// fp32 storage at d = 128 holds twice the operand registers of bf16: its
+// passes run at one workgroup per CU and need the accumulation registers
+// beside the 256 vector registers, so this file is compiled a second time,
+// with this macro and without forcing MFMA results into vector registers
+// (with that option the compiler fails on the causal key pass).
+hipError_t launch_backward_f32_d128(const BwdArgs& a, Launcher& L) {
+  return launch_bwd_d<float, 128>(a, L);
+}
+#else
 hipError_t launch_backward_tail(const BwdArgs& a, Launcher& L) {
   return a.dtype == FMM_DTYPE_BF16 ? launch_bwd_t<bf16_t>(a, L) : launch_bwd_t<float>(a, L);
 }
+#endif
 
 }  // namespace fmm

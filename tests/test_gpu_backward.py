@@ -55,8 +55,6 @@ def check_backward(B, H, N, d, kw, rank, causal, dtype, seed, std=1.0, shift=0.0
 @pytest.mark.parametrize("causal", [0, 1])
 @pytest.mark.parametrize("d", [16, 32, 64, 128])
 def test_backward_widths(d, causal, dtype):
-    if d == 128 and dtype == "f32":
-        pytest.skip("fp32 storage at d = 128 is not built for the backward")
     worst = 0.0
     for B, H, N, kw, rank in ((1, 2, 300, 5, 2), (2, 1, 777, 20, 1), (1, 1, 1500, 64, 2),
                               (1, 2, 64, 0, 2), (1, 1, 33, 40, 2)):
@@ -72,6 +70,7 @@ def test_backward_wide_band_and_rank3(causal, dtype):
     # shifted inputs (tanh's denominator away from zero)
     check_backward(1, 2, 1200, 32, 300, 2, causal, dtype, 2100 + causal)
     check_backward(2, 1, 900, 64, 30, 3, causal, dtype, 2200 + causal, shift=1.0)
+    check_backward(1, 1, 700, 128, 40, 3, causal, dtype, 2250 + causal, shift=1.0)
 
 
 @pytest.mark.parametrize("causal", [0, 1])
@@ -80,9 +79,8 @@ def test_backward_benchmark_shape_slices(causal):
     check_backward(2, 2, 4096, 32, 20, 2, causal, "bf16", 2300 + causal)
 
 
-def test_backward_fp32_d128_is_unsupported():
-    q, k, v, wn, wf = make_inputs(1, 1, 64, 128, "f32", 1.0, 2400)
-    tq, tk, tv, twn, twf = upload(q, k, v, wn, wf, "f32")
-    with pytest.raises(binding.FmmError) as ei:
-        binding.backward(tq, tk, tv, tq.clone(), twn, twf, 5, 2, 0)
-    assert ei.value.status == binding.FMM_ERR_UNSUPPORTED
+@pytest.mark.parametrize("causal", [0, 1])
+def test_backward_fp32_d128_several_segments(causal):
+    # fp32 at d = 128 (its own translation unit): several state segments and
+    # staging rounds per slice, a ragged tail
+    check_backward(1, 2, 2500, 128, 64, 2, causal, "f32", 2400 + causal, std=0.18)
