@@ -233,6 +233,21 @@ int fmm_attn_backward(const void* q, const void* k, const void* v, const void* d
                       const float* w_near, const float* w_far, int dtype, void* stream);
 
 /*
+ * fmm_attn_backward_ex - fmm_attn_backward for the forward of a given
+ * far-field normalisation (far_norm as in fmm_attn_forward_ex): with
+ * FMM_FAR_NORM_JOINT, far = sum_l num_l / Den with Den = sum_l den_l, so
+ * dnum_l = c g / Den and dden_l = -c g . far / Den for every map l (Sec. 1.2,
+ * the rows of sum_l phi_l(Q) phi_l(K)^T normalised as one matrix);
+ * FMM_FAR_NORM_PER_MAP is fmm_attn_backward.  An unknown far_norm returns
+ * FMM_ERR_INVALID_ARG.  Otherwise as fmm_attn_backward.
+ */
+int fmm_attn_backward_ex(const void* q, const void* k, const void* v, const void* dout,
+                         void* dq, void* dk, void* dv, float* dw_near, float* dw_far,
+                         int B, int H, int N, int d, int band_k, int rank, int causal,
+                         const float* w_near, const float* w_far, int dtype, int far_norm,
+                         void* stream);
+
+/*
  * fmm_attn_layer_forward - the attention layer around the operator: the
  * Step-1 projections of Sec. 1.1 and an output projection, per token t
  *   [q_t | k_t | v_t] = x_t W_qkv,  out_t = concat_h(o_{h,t}) W_out

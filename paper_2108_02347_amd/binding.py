@@ -36,7 +36,8 @@ EXPORTS = (
     "fmm_attn_forward_ws", "fmm_attn_status_string", "fmm_attn_release_workspace",
     "fmm_attn_version", "fmm_attn_kernel_timing", "fmm_attn_kernel_timing_read",
     "fmm_attn_forward_noalloc", "fmm_attn_noalloc_max_bytes", "fmm_attn_forward_ex",
-    "fmm_attn_backward", "fmm_attn_layer_forward", "fmm_attn_forward_fastweight",
+    "fmm_attn_backward", "fmm_attn_backward_ex", "fmm_attn_layer_forward",
+    "fmm_attn_forward_fastweight",
     "fmm_attn_set_one_launch",
 )
 
@@ -73,6 +74,8 @@ def lib() -> ctypes.CDLL:
     h.fmm_attn_layer_forward.restype = ci
     h.fmm_attn_backward.argtypes = [vp] * 9 + [ci] * 7 + [cf, cf, ci, vp]
     h.fmm_attn_backward.restype = ci
+    h.fmm_attn_backward_ex.argtypes = [vp] * 9 + [ci] * 7 + [cf, cf, ci, ci, vp]
+    h.fmm_attn_backward_ex.restype = ci
     h.fmm_attn_forward_ex.argtypes = fwd_args[:-1] + [ci, ci, vp]
     h.fmm_attn_forward_ex.restype = ci
     h.fmm_attn_forward_noalloc.argtypes = fwd_args[:-1] + [ci, vp]
@@ -230,44 +233,52 @@ def noalloc_max_bytes() -> int:
     return int(lib().fmm_attn_noalloc_max_bytes())
 
 
-def backward(q, k, v, dout, w_near, w_far, band_k: int, rank: int, causal: bool):
-    """Gradients of the forward (per-map normalisation) for dout = dL/d(out):
-    returns (dq, dk, dv, dw_near, dw_far)."""
+def backward(q, k, v, dout, w_near, w_far, band_k: int, rank: int, causal: bool,
+             joint: bool = False):
+    """Gradients of the forward for dout = dL/d(out): returns (dq, dk, dv,
+    dw_near, dw_far).  joint=True: of the forward with jointly normalised
+    far-field maps (fmm_attn_backward_ex)."""
     B, H, N, d = _prep(q, k, v, w_near, w_far)
     _check_out(dout, q)
     dq, dk, dv = (torch.empty_like(q) for _ in range(3))
     dwn = torch.empty_like(w_near)
     dwf = torch.empty_like(w_far)
     dt = FMM_DTYPE_BF16 if q.dtype == torch.bfloat16 else FMM_DTYPE_F32
-    _check(lib().fmm_attn_backward(
-        _ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwn),
-        _ptr(dwf), B, H, N, d, int(band_k), int(rank), int(bool(causal)), _ptr(w_near),
-        _ptr(w_far), dt, _stream_of(q)))
+    args = (_ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dwn),
+            _ptr(dwf), B, H, N, d, int(band_k), int(rank), int(bool(causal)), _ptr(w_near),
+            _ptr(w_far), dt)
+    if joint:
+        _check(lib().fmm_attn_backward_ex(*args, FMM_FAR_NORM_JOINT, _stream_of(q)))
+    else:
+        _check(lib().fmm_attn_backward(*args, _stream_of(q)))
     return dq, dk, dv, dwn, dwf
 
 
 class _FmmAttention(torch.autograd.Function):
-    """The operator (per-map normalisation) as a torch.autograd function: its
-    forward and backward are the library's entry points."""
+    """The operator as a torch.autograd function: its forward and backward
+    are the library's entry points."""
 
     @staticmethod
-    def forward(ctx, q, k, v, w_near, w_far, band_k, rank, causal):
+    def forward(ctx, q, k, v, w_near, w_far, band_k, rank, causal, joint):
         ctx.save_for_backward(q, k, v, w_near, w_far)
-        ctx.args = (int(band_k), int(rank), bool(causal))
-        return forward(q, k, v, w_near, w_far, band_k, rank, causal)
+        ctx.args = (int(band_k), int(rank), bool(causal), bool(joint))
+        return forward(q, k, v, w_near, w_far, band_k, rank, causal, joint=bool(joint))
 
     @staticmethod
     def backward(ctx, g):
         q, k, v, w_near, w_far = ctx.saved_tensors
-        dq, dk, dv, dwn, dwf = backward(q, k, v, g.contiguous(), w_near, w_far, *ctx.args)
-        return dq, dk, dv, dwn, dwf, None, None, None
+        band_k, rank, causal, joint = ctx.args
+        dq, dk, dv, dwn, dwf = backward(q, k, v, g.contiguous(), w_near, w_far, band_k, rank,
+                                        causal, joint=joint)
+        return dq, dk, dv, dwn, dwf, None, None, None, None
 
 
-def fmm_attention(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool):
+def fmm_attention(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool,
+                  joint: bool = False):
     """The operator as a differentiable function of q, k, v and the two blend
     logits (torch.autograd), for training through it: out = forward(...), and
     out's gradient reaches q, k, v, w_near and w_far through backward(...)."""
-    return _FmmAttention.apply(q, k, v, w_near, w_far, band_k, rank, causal)
+    return _FmmAttention.apply(q, k, v, w_near, w_far, band_k, rank, causal, joint)
 
 
 def layer_forward(x, w_qkv, w_out, heads: int, w_near, w_far, band_k: int, rank: int,

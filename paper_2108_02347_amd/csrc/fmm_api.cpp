@@ -404,10 +404,10 @@ void fill_bwd_args(fmm::BwdArgs& a, const BwdPlan& bp, void* ws, int B, int H) {
 int run_backward(const void* q, const void* k, const void* v, const void* dout, void* dq,
                  void* dk, void* dv, float* dw_near, float* dw_far, int B, int H, int N, int d,
                  int band_k, int rank, int causal, const float* w_near, const float* w_far,
-                 int dtype, void* stream) {
+                 int dtype, int far_norm, void* stream) {
   // the inputs as in the forward (dout takes the place of out for the checks)
   int st = validate(q, k, v, dq, B, H, N, d, band_k, rank, causal, w_near, w_far, dtype,
-                    FMM_FAR_NORM_PER_MAP);
+                    far_norm);
   if (st != FMM_OK) return st;
   if (!dout || !dk || !dv || !dw_near || !dw_far) return FMM_ERR_INVALID_ARG;
   const size_t es = dtype == FMM_DTYPE_BF16 ? 2 : 4;
@@ -448,6 +448,7 @@ int run_backward(const void* q, const void* k, const void* v, const void* dout, 
   ba.rank = rank;
   ba.causal = causal;
   ba.dtype = dtype;
+  ba.far_norm = far_norm;
   ba.stream = stream;
   ba.nseg = bp.p.nseg;
   ba.L = bp.p.L;
@@ -703,7 +704,16 @@ int fmm_attn_backward(const void* q, const void* k, const void* v, const void* d
                       int d, int band_k, int rank, int causal, const float* w_near,
                       const float* w_far, int dtype, void* stream) {
   return run_backward(q, k, v, dout, dq, dk, dv, dw_near, dw_far, B, H, N, d, band_k, rank,
-                      causal, w_near, w_far, dtype, stream);
+                      causal, w_near, w_far, dtype, FMM_FAR_NORM_PER_MAP, stream);
+}
+
+int fmm_attn_backward_ex(const void* q, const void* k, const void* v, const void* dout,
+                         void* dq, void* dk, void* dv, float* dw_near, float* dw_far, int B,
+                         int H, int N, int d, int band_k, int rank, int causal,
+                         const float* w_near, const float* w_far, int dtype, int far_norm,
+                         void* stream) {
+  return run_backward(q, k, v, dout, dq, dk, dv, dw_near, dw_far, B, H, N, d, band_k, rank,
+                      causal, w_near, w_far, dtype, far_norm, stream);
 }
 
 int fmm_attn_layer_forward(const void* x, const void* w_qkv, const void* w_out, void* y, int B,

@@ -16,6 +16,9 @@
 //     dphi(k_j) = dS(j) v_j + dz(j),  dv_j += dS(j)^T phi(k_j)
 //     dq += phi'(q) * dphi(q),  dk += phi'(k) * dphi(k)
 //   blend (Eq. (11)): dw_near = a (1 - a) sum g . near, dw_far = c (1 - c) sum g . far
+//   joint normalisation (far = sum_l num_l / Den, Den = sum_l den_l): the
+//   same with dnum_i = c g_i / Den_i and dden_i = -c g_i . far_i / Den_i for
+//   every map, which the row pass forms in a first sweep over the maps
 //
 // Launch sequence (after the forward state k_seg_state + k_state_combine):
 //   k_bwd_rows   per state segment, walking 64-row tiles: recomputes the near
@@ -351,7 +354,7 @@ __device__ __forceinline__ void near_dq_units(f32x4* dq, const typename QuadOf<T
   mfma_drain();
 }
 
-template <typename T, int D, bool CAUSAL, int NM, bool TWO>
+template <typename T, int D, bool CAUSAL, int NM, bool TWO, bool JOINT>
 __global__ __launch_bounds__(NT, TWO && CAUSAL ? 2 : 1) void k_bwd_rows(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, T* __restrict__ dq, float* __restrict__ recs,
@@ -455,163 +458,347 @@ __global__ __launch_bounds__(NT, TWO && CAUSAL ? 2 : 1) void k_bwd_rows(
     }
     // ks: first key of the last staged round, which holds the tile's keys
     // (causal form)
-    // ---- far field, one map at a time
-    const T* vt = sv + (t0 - ks) * ST;
-    for (int l = 0; l < rank; ++l) {
-      const T* tbl = tb1;
-      Q pq[NB];
-#pragma unroll
-      for (int cb = 0; cb < NB; ++cb) {
-        float x[4], p[4];
-        quad_to_f32(qq[cb], x);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) p[i] = phi_any(x[i], l);
-        pq[cb] = f32_to_quad<T>(p);
+    // ---- far field, one map at a time (joint normalisation: below)
+    if constexpr (!JOINT) {
+      const T* vt = sv + (t0 - ks) * ST;
+      for (int l = 0; l < rank; ++l) {
+        const T* tbl = tb1;
+        Q pq[NB];
+  #pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+          float x[4], p[4];
+          quad_to_f32(qq[cb], x);
+  #pragma unroll
+          for (int i = 0; i < 4; ++i) p[i] = phi_any(x[i], l);
+          pq[cb] = f32_to_quad<T>(p);
+        }
+        float* rl = rec + (size_t)l * D * (D + 1);
+        f32x4 num[NB + 1];
+  #pragma unroll
+        for (int nb = 0; nb <= NB; ++nb) num[nb] = zero;
+        if constexpr (CAUSAL) {
+          // the tile's keys: phi_l(K_t) into tb1; intra-tile part of num, den
+          __syncthreads();
+          stage_phi_rows<T, D>(sk + (t0 - ks) * ST, t0, N, l, tb1);
+          __syncthreads();
+          const Q ones = quad_fill<T>(1.f);
+          for (int u = 0; u <= (w >> 1); ++u) {
+            const bool diag = u == (w >> 1);
+            float a2[2][4];
+  #pragma unroll
+            for (int b = 0; b < 2; ++b) {
+              Q ka2[NB];
+  #pragma unroll
+              for (int cb = 0; cb < NB; ++cb)
+                ka2[cb] = ld_quad(tbl, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
+              const f32x4 at = contract<NB>(ka2, pq, zero);
+  #pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const int j = t0 + 32 * u + 16 * b + 4 * g + i;
+                a2[b][i] = (!diag || j <= row) ? at[i] : 0.f;
+              }
+            }
+            const Q p0 = f32_to_quad<T>(a2[0]), p1 = f32_to_quad<T>(a2[1]);
+            const T* vx = vt + 32 * u * ST;
+  #pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+              num[nb] = mma_step2(ld_tquad(vx, 0, 16 * nb, ST), ld_tquad(vx, 16, 16 * nb, ST), p0,
+                                  p1, num[nb]);
+            num[NB] = mma_step2(ones, ones, p0, p1, num[NB]);
+          }
+          mfma_drain();
+        }
+        // the product with the record (non-causal: the slice's total; causal:
+        // the prefix before the tile)
+  #pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          Q a[NB];
+  #pragma unroll
+          for (int cb = 0; cb < NB; ++cb) {
+            if constexpr (FR) a[cb] = RecFrags<D>::a(frb, l, cb, nb);
+            else a[cb] = rec_quad<T>(rl + ((cb * NB + nb) * 64 + lane) * 4);
+          }
+          num[nb] = contract<NB>(a, pq, num[nb]);
+        }
+        {
+          Q zq[NB];
+  #pragma unroll
+          for (int cb = 0; cb < NB; ++cb) {
+            if constexpr (FR) zq[cb] = RecFrags<D>::z(frb, l, cb);
+            else zq[cb] = rec_quad<T>(rl + D * D + 16 * cb + 4 * g);
+          }
+          num[NB] = contract<NB>(zq, pq, num[NB]);
+        }
+        // quotient rule
+        const float inv_den = row_ok ? fast_rcp(num[NB][0]) : 0.f;
+        float gnum = 0.f;
+  #pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+  #pragma unroll
+          for (int i = 0; i < 4; ++i) gnum = fmaf(gf[nb][i], num[nb][i], gnum);
+        acc_far += gnum * inv_den;
+        const float dden = -sfw * col_sum(gnum) * inv_den * inv_den;
+        const float cid = sfw * inv_den;
+        Q dnq[NB];
+  #pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          float f[4];
+  #pragma unroll
+          for (int i = 0; i < 4; ++i) f[i] = gf[nb][i] * cid;
+          dnq[nb] = f32_to_quad<T>(f);
+        }
+        if (row_ok && g == 0) {
+          float* fp = rowfar + (((size_t)bh * N + row) * rank + l) * 2;
+          fp[0] = inv_den;
+          fp[1] = dden;
+        }
+        // dphi(q) = S dnum + z dden (+ intra-tile keys in the causal form)
+        f32x4 dph[NB];
+  #pragma unroll
+        for (int cb = 0; cb < NB; ++cb) dph[cb] = zero;
+        if constexpr (CAUSAL) {
+          for (int u = 0; u <= (w >> 1); ++u) {
+            const bool diag = u == (w >> 1);
+            float a2[2][4];
+  #pragma unroll
+            for (int b = 0; b < 2; ++b) {
+              Q va[NB];
+  #pragma unroll
+              for (int eb = 0; eb < NB; ++eb)
+                va[eb] = ld_quad(vt, 32 * u + 16 * b + r, 16 * eb + 4 * g, ST);
+              const f32x4 at = contract<NB>(va, dnq, zero);
+  #pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const int j = t0 + 32 * u + 16 * b + 4 * g + i;
+                a2[b][i] = (!diag || j <= row) ? at[i] + dden : 0.f;
+              }
+            }
+            const Q p0 = f32_to_quad<T>(a2[0]), p1 = f32_to_quad<T>(a2[1]);
+  #pragma unroll
+            for (int cb = 0; cb < NB; ++cb)
+              dph[cb] = mma_step2(ld_tquad(tbl, 32 * u, 16 * cb, ST),
+                                  ld_tquad(tbl, 32 * u + 16, 16 * cb, ST), p0, p1, dph[cb]);
+          }
+          mfma_drain();
+        }
+  #pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+          Q a[NB];
+  #pragma unroll
+          for (int eb = 0; eb < NB; ++eb) {
+            if constexpr (FR) a[eb] = RecFrags<D>::b(frb, l, cb, eb);
+            else a[eb] = rec_quad_t<T>(rl, NB, cb, eb);
+          }
+          dph[cb] = contract<NB>(a, dnq, dph[cb]);
+        }
+        const float* zl = FR && !CAUSAL ? RecFrags<D>::zf(frb, l) : rl + D * D;
+  #pragma unroll
+        for (int cb = 0; cb < NB; ++cb) {
+          const float4 z = *reinterpret_cast<const float4*>(zl + 16 * cb + 4 * g);
+          const float zf[4] = {z.x, z.y, z.z, z.w};
+          float x[4];
+          quad_to_f32(qq[cb], x);
+  #pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            float dg = 0.f;
+            if (l == 0) dg = x[i] > 0.f ? 1.f : __expf(x[i]);
+            else if (l == 1) dg = x[i] < 0.f ? -1.f : -__expf(-x[i]);
+            else {
+              const float t = tanhf(x[i]);
+              dg = 1.f - t * t;
+            }
+            dqa[cb][i] = fmaf(dg, dph[cb][i] + zf[i] * dden, dqa[cb][i]);
+          }
+        }
+        if constexpr (CAUSAL) {
+          // advance the forward prefix record by the tile's keys (tb1 still
+          // holds phi_l(K_t)), unless this is the segment's last tile
+          if (t0 + TM < s1) {
+            __syncthreads();  // every wave has read record l for this tile
+            record_add<T, D>(rl, tb1, vt, ones_col, ST, w, nullptr);
+          }
+        }
       }
-      float* rl = rec + (size_t)l * D * (D + 1);
-      f32x4 num[NB + 1];
+    } else {
+      const T* vt = sv + (t0 - ks) * ST;
+      const T* tbl = tb1;
+      auto phi_q = [&](int l, Q* pq) {
 #pragma unroll
-      for (int nb = 0; nb <= NB; ++nb) num[nb] = zero;
-      if constexpr (CAUSAL) {
-        // the tile's keys: phi_l(K_t) into tb1; intra-tile part of num, den
+        for (int cb = 0; cb < NB; ++cb) {
+          float x[4], p[4];
+          quad_to_f32(qq[cb], x);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) p[i] = phi_any(x[i], l);
+          pq[cb] = f32_to_quad<T>(p);
+        }
+      };
+      // the causal form's phi_l(K_t) rows into tb1 (for the intra-tile parts
+      // and the record's advance)
+      auto stage_keys = [&](int l) {
         __syncthreads();
         stage_phi_rows<T, D>(sk + (t0 - ks) * ST, t0, N, l, tb1);
         __syncthreads();
-        const Q ones = quad_fill<T>(1.f);
-        for (int u = 0; u <= (w >> 1); ++u) {
-          const bool diag = u == (w >> 1);
-          float a2[2][4];
+      };
+      // num and den (column NB) of map l for the strip's rows
+      auto far_num = [&](int l, const Q* pq, f32x4* num) {
+        const float* rl = rec + (size_t)l * D * (D + 1);
 #pragma unroll
-          for (int b = 0; b < 2; ++b) {
-            Q ka2[NB];
+        for (int nb = 0; nb <= NB; ++nb) num[nb] = zero;
+        if constexpr (CAUSAL) {
+          // the tile's keys: intra-tile part of num, den
+          stage_keys(l);
+          const Q ones = quad_fill<T>(1.f);
+          for (int u = 0; u <= (w >> 1); ++u) {
+            const bool diag = u == (w >> 1);
+            float a2[2][4];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+              Q ka2[NB];
+#pragma unroll
+              for (int cb = 0; cb < NB; ++cb)
+                ka2[cb] = ld_quad(tbl, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
+              const f32x4 at = contract<NB>(ka2, pq, zero);
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const int j = t0 + 32 * u + 16 * b + 4 * g + i;
+                a2[b][i] = (!diag || j <= row) ? at[i] : 0.f;
+              }
+            }
+            const Q p0 = f32_to_quad<T>(a2[0]), p1 = f32_to_quad<T>(a2[1]);
+            const T* vx = vt + 32 * u * ST;
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+              num[nb] = mma_step2(ld_tquad(vx, 0, 16 * nb, ST), ld_tquad(vx, 16, 16 * nb, ST), p0,
+                                  p1, num[nb]);
+            num[NB] = mma_step2(ones, ones, p0, p1, num[NB]);
+          }
+          mfma_drain();
+        }
+        // the product with the record (non-causal: the slice's total; causal:
+        // the prefix before the tile)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          Q a[NB];
+#pragma unroll
+          for (int cb = 0; cb < NB; ++cb) {
+            if constexpr (FR) a[cb] = RecFrags<D>::a(frb, l, cb, nb);
+            else a[cb] = rec_quad<T>(rl + ((cb * NB + nb) * 64 + lane) * 4);
+          }
+          num[nb] = contract<NB>(a, pq, num[nb]);
+        }
+        {
+          Q zq[NB];
+#pragma unroll
+          for (int cb = 0; cb < NB; ++cb) {
+            if constexpr (FR) zq[cb] = RecFrags<D>::z(frb, l, cb);
+            else zq[cb] = rec_quad<T>(rl + D * D + 16 * cb + 4 * g);
+          }
+          num[NB] = contract<NB>(zq, pq, num[NB]);
+        }
+      };
+      // one quotient for all maps: far = sum_l num_l / Den, Den = sum_l
+      // den_l, so dnum_l = c g / Den and dden_l = -c g . (sum_l num_l) / Den^2
+      // for every l; a first sweep over the maps forms Den and g . sum_l num_l
+      float den = 0.f, gsum = 0.f;
+      for (int l = 0; l < rank; ++l) {
+        Q pq[NB];
+        phi_q(l, pq);
+        f32x4 num[NB + 1];
+        far_num(l, pq, num);
+        den += num[NB][0];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) gsum = fmaf(gf[nb][i], num[nb][i], gsum);
+      }
+      const float inv_den = row_ok ? fast_rcp(den) : 0.f;
+      acc_far += gsum * inv_den;
+      const float dden = -sfw * col_sum(gsum) * inv_den * inv_den;
+      const float cid = sfw * inv_den;
+      // then, per map, dq through phi_l'(q) and (causal) the record's advance
+      for (int l = 0; l < rank; ++l) {
+        float* rl = rec + (size_t)l * D * (D + 1);
+        Q pq[NB];
+        phi_q(l, pq);
+        if constexpr (CAUSAL) stage_keys(l);
+        Q dnq[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          float f[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) f[i] = gf[nb][i] * cid;
+          dnq[nb] = f32_to_quad<T>(f);
+        }
+        if (row_ok && g == 0) {
+          float* fp = rowfar + (((size_t)bh * N + row) * rank + l) * 2;
+          fp[0] = inv_den;
+          fp[1] = dden;
+        }
+        // dphi(q) = S dnum + z dden (+ intra-tile keys in the causal form)
+        f32x4 dph[NB];
+#pragma unroll
+        for (int cb = 0; cb < NB; ++cb) dph[cb] = zero;
+        if constexpr (CAUSAL) {
+          for (int u = 0; u <= (w >> 1); ++u) {
+            const bool diag = u == (w >> 1);
+            float a2[2][4];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+              Q va[NB];
+#pragma unroll
+              for (int eb = 0; eb < NB; ++eb)
+                va[eb] = ld_quad(vt, 32 * u + 16 * b + r, 16 * eb + 4 * g, ST);
+              const f32x4 at = contract<NB>(va, dnq, zero);
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const int j = t0 + 32 * u + 16 * b + 4 * g + i;
+                a2[b][i] = (!diag || j <= row) ? at[i] + dden : 0.f;
+              }
+            }
+            const Q p0 = f32_to_quad<T>(a2[0]), p1 = f32_to_quad<T>(a2[1]);
 #pragma unroll
             for (int cb = 0; cb < NB; ++cb)
-              ka2[cb] = ld_quad(tbl, 32 * u + 16 * b + r, 16 * cb + 4 * g, ST);
-            const f32x4 at = contract<NB>(ka2, pq, zero);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int j = t0 + 32 * u + 16 * b + 4 * g + i;
-              a2[b][i] = (!diag || j <= row) ? at[i] : 0.f;
-            }
+              dph[cb] = mma_step2(ld_tquad(tbl, 32 * u, 16 * cb, ST),
+                                  ld_tquad(tbl, 32 * u + 16, 16 * cb, ST), p0, p1, dph[cb]);
           }
-          const Q p0 = f32_to_quad<T>(a2[0]), p1 = f32_to_quad<T>(a2[1]);
-          const T* vx = vt + 32 * u * ST;
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            num[nb] = mma_step2(ld_tquad(vx, 0, 16 * nb, ST), ld_tquad(vx, 16, 16 * nb, ST), p0,
-                                p1, num[nb]);
-          num[NB] = mma_step2(ones, ones, p0, p1, num[NB]);
+          mfma_drain();
         }
-        mfma_drain();
-      }
-      // the product with the record (non-causal: the slice's total; causal:
-      // the prefix before the tile)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        Q a[NB];
 #pragma unroll
         for (int cb = 0; cb < NB; ++cb) {
-          if constexpr (FR) a[cb] = RecFrags<D>::a(frb, l, cb, nb);
-          else a[cb] = rec_quad<T>(rl + ((cb * NB + nb) * 64 + lane) * 4);
+          Q a[NB];
+#pragma unroll
+          for (int eb = 0; eb < NB; ++eb) {
+            if constexpr (FR) a[eb] = RecFrags<D>::b(frb, l, cb, eb);
+            else a[eb] = rec_quad_t<T>(rl, NB, cb, eb);
+          }
+          dph[cb] = contract<NB>(a, dnq, dph[cb]);
         }
-        num[nb] = contract<NB>(a, pq, num[nb]);
-      }
-      {
-        Q zq[NB];
+        const float* zl = FR && !CAUSAL ? RecFrags<D>::zf(frb, l) : rl + D * D;
 #pragma unroll
         for (int cb = 0; cb < NB; ++cb) {
-          if constexpr (FR) zq[cb] = RecFrags<D>::z(frb, l, cb);
-          else zq[cb] = rec_quad<T>(rl + D * D + 16 * cb + 4 * g);
-        }
-        num[NB] = contract<NB>(zq, pq, num[NB]);
-      }
-      // quotient rule
-      const float inv_den = row_ok ? fast_rcp(num[NB][0]) : 0.f;
-      float gnum = 0.f;
+          const float4 z = *reinterpret_cast<const float4*>(zl + 16 * cb + 4 * g);
+          const float zf[4] = {z.x, z.y, z.z, z.w};
+          float x[4];
+          quad_to_f32(qq[cb], x);
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) gnum = fmaf(gf[nb][i], num[nb][i], gnum);
-      acc_far += gnum * inv_den;
-      const float dden = -sfw * col_sum(gnum) * inv_den * inv_den;
-      const float cid = sfw * inv_den;
-      Q dnq[NB];
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        float f[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) f[i] = gf[nb][i] * cid;
-        dnq[nb] = f32_to_quad<T>(f);
-      }
-      if (row_ok && g == 0) {
-        float* fp = rowfar + (((size_t)bh * N + row) * rank + l) * 2;
-        fp[0] = inv_den;
-        fp[1] = dden;
-      }
-      // dphi(q) = S dnum + z dden (+ intra-tile keys in the causal form)
-      f32x4 dph[NB];
-#pragma unroll
-      for (int cb = 0; cb < NB; ++cb) dph[cb] = zero;
-      if constexpr (CAUSAL) {
-        for (int u = 0; u <= (w >> 1); ++u) {
-          const bool diag = u == (w >> 1);
-          float a2[2][4];
-#pragma unroll
-          for (int b = 0; b < 2; ++b) {
-            Q va[NB];
-#pragma unroll
-            for (int eb = 0; eb < NB; ++eb)
-              va[eb] = ld_quad(vt, 32 * u + 16 * b + r, 16 * eb + 4 * g, ST);
-            const f32x4 at = contract<NB>(va, dnq, zero);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int j = t0 + 32 * u + 16 * b + 4 * g + i;
-              a2[b][i] = (!diag || j <= row) ? at[i] + dden : 0.f;
+          for (int i = 0; i < 4; ++i) {
+            float dg = 0.f;
+            if (l == 0) dg = x[i] > 0.f ? 1.f : __expf(x[i]);
+            else if (l == 1) dg = x[i] < 0.f ? -1.f : -__expf(-x[i]);
+            else {
+              const float t = tanhf(x[i]);
+              dg = 1.f - t * t;
             }
+            dqa[cb][i] = fmaf(dg, dph[cb][i] + zf[i] * dden, dqa[cb][i]);
           }
-          const Q p0 = f32_to_quad<T>(a2[0]), p1 = f32_to_quad<T>(a2[1]);
-#pragma unroll
-          for (int cb = 0; cb < NB; ++cb)
-            dph[cb] = mma_step2(ld_tquad(tbl, 32 * u, 16 * cb, ST),
-                                ld_tquad(tbl, 32 * u + 16, 16 * cb, ST), p0, p1, dph[cb]);
         }
-        mfma_drain();
-      }
-#pragma unroll
-      for (int cb = 0; cb < NB; ++cb) {
-        Q a[NB];
-#pragma unroll
-        for (int eb = 0; eb < NB; ++eb) {
-          if constexpr (FR) a[eb] = RecFrags<D>::b(frb, l, cb, eb);
-          else a[eb] = rec_quad_t<T>(rl, NB, cb, eb);
-        }
-        dph[cb] = contract<NB>(a, dnq, dph[cb]);
-      }
-      const float* zl = FR && !CAUSAL ? RecFrags<D>::zf(frb, l) : rl + D * D;
-#pragma unroll
-      for (int cb = 0; cb < NB; ++cb) {
-        const float4 z = *reinterpret_cast<const float4*>(zl + 16 * cb + 4 * g);
-        const float zf[4] = {z.x, z.y, z.z, z.w};
-        float x[4];
-        quad_to_f32(qq[cb], x);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float dg = 0.f;
-          if (l == 0) dg = x[i] > 0.f ? 1.f : __expf(x[i]);
-          else if (l == 1) dg = x[i] < 0.f ? -1.f : -__expf(-x[i]);
-          else {
-            const float t = tanhf(x[i]);
-            dg = 1.f - t * t;
+        if constexpr (CAUSAL) {
+          // advance the forward prefix record by the tile's keys (tb1 still
+          // holds phi_l(K_t)), unless this is the segment's last tile
+          if (t0 + TM < s1) {
+            __syncthreads();  // every wave has read record l for this tile
+            record_add<T, D>(rl, tb1, vt, ones_col, ST, w, nullptr);
           }
-          dqa[cb][i] = fmaf(dg, dph[cb][i] + zf[i] * dden, dqa[cb][i]);
-        }
-      }
-      if constexpr (CAUSAL) {
-        // advance the forward prefix record by the tile's keys (tb1 still
-        // holds phi_l(K_t)), unless this is the segment's last tile
-        if (t0 + TM < s1) {
-          __syncthreads();  // every wave has read record l for this tile
-          record_add<T, D>(rl, tb1, vt, ones_col, ST, w, nullptr);
         }
       }
     }
@@ -1137,9 +1324,12 @@ __global__ void k_dw_reduce(const float* __restrict__ dwpart, const float* __res
 template <typename T, int D, bool CAUSAL, int NM = 3, bool TWO = false>
 hipError_t launch_bwd_dcf(const BwdArgs& a, Launcher& L) {
   using C = BwdCfg<T, D, NM, TWO>;
-  static std::atomic<unsigned long long> set_rows{0}, set_keys{0};
-  if (L.note(lds_limit_once((const void*)k_bwd_rows<T, D, CAUSAL, NM, TWO>, C::LDS,
-                            set_rows)) != hipSuccess ||
+  const bool joint = a.far_norm == FMM_FAR_NORM_JOINT;
+  static std::atomic<unsigned long long> set_rows{0}, set_rows_j{0}, set_keys{0};
+  if (L.note(joint ? lds_limit_once((const void*)k_bwd_rows<T, D, CAUSAL, NM, TWO, true>,
+                                    C::LDS, set_rows_j)
+                   : lds_limit_once((const void*)k_bwd_rows<T, D, CAUSAL, NM, TWO, false>,
+                                    C::LDS, set_rows)) != hipSuccess ||
       L.note(lds_limit_once((const void*)k_bwd_keys<T, D, CAUSAL, NM, TWO>, C::LDS,
                             set_keys)) != hipSuccess)
     return L.err;
@@ -1148,10 +1338,14 @@ hipError_t launch_bwd_dcf(const BwdArgs& a, Launcher& L) {
   const size_t REC = (size_t)a.rank * D * (D + 1);
   hipStream_t s = (hipStream_t)a.stream;
   const dim3 grid(BH * a.nseg);
-  L(FMM_KERNEL_BWD_ROWS, k_bwd_rows<T, D, CAUSAL, NM, TWO>, grid, dim3(NT), (size_t)C::LDS, s,
-    (const T*)a.q, (const T*)a.k, (const T*)a.v, (const T*)a.dout, (T*)a.dq,
-    CAUSAL ? a.part : a.fin, a.rowstat, a.rowfar, a.dwpart, a.w_near, a.w_far, a.H, a.N,
-    a.band_k, a.L, a.nseg, a.rank, scale2);
+  auto rows = [&](auto kern) {
+    L(FMM_KERNEL_BWD_ROWS, kern, grid, dim3(NT), (size_t)C::LDS, s, (const T*)a.q,
+      (const T*)a.k, (const T*)a.v, (const T*)a.dout, (T*)a.dq, CAUSAL ? a.part : a.fin,
+      a.rowstat, a.rowfar, a.dwpart, a.w_near, a.w_far, a.H, a.N, a.band_k, a.L, a.nseg,
+      a.rank, scale2);
+  };
+  if (joint) rows(k_bwd_rows<T, D, CAUSAL, NM, TWO, true>);
+  else rows(k_bwd_rows<T, D, CAUSAL, NM, TWO, false>);
   launch_seg_grad<T, D>(a, L);
   const int nchunk = (int)((REC + 255) / 256);
   const dim3 sgrid((unsigned)std::min<long long>((long long)nchunk * BH, 0xFFFFFFFFll));

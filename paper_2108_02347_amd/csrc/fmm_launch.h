@@ -184,6 +184,7 @@ struct BwdArgs {
   float* rowstat;   // [B*H*N][3]: scaled row maximum, 1/l, D
   float* rowfar;    // [B*H*N][rank][2]: 1/den, dden
   float* dwpart;    // [B*H*nseg][2]: sums of g . near, g . far
+  int far_norm = FMM_FAR_NORM_PER_MAP;  // of the forward whose gradients these are
 };
 hipError_t launch_state_only(const LaunchArgs& a, Launcher& L);
 hipError_t launch_state_sum(Launcher& L, float* part, float* fin, int nseg, int rec, int BH,

@@ -153,6 +153,18 @@ def test_forward_ex_rejects_unknown_normalisation():
     assert lib.fmm_attn_forward_ex(*args(0, 7)) == binding.FMM_ERR_UNSUPPORTED
 
 
+def test_backward_ex_rejects_unknown_normalisation():
+    lib = binding.lib()
+    T = 1 << 40
+    vp = ctypes.c_void_p
+    args = lambda norm, dt=0: (vp(T), vp(2 * T), vp(3 * T), vp(4 * T), vp(5 * T), vp(6 * T),
+                               vp(7 * T), vp(8 * T), vp(9 * T), 1, 2, 64, 32, 5, 2, 0,
+                               vp(10 * T), vp(11 * T), dt, norm, vp(0))
+    assert lib.fmm_attn_backward_ex(*args(2)) == binding.FMM_ERR_INVALID_ARG
+    assert lib.fmm_attn_backward_ex(*args(-1)) == binding.FMM_ERR_INVALID_ARG
+    assert lib.fmm_attn_backward_ex(*args(0, 7)) == binding.FMM_ERR_UNSUPPORTED
+
+
 def test_one_launch_knob_and_workspace():
     # the mode is process-wide: 0 never, 1 where it applies (default), 2
     # without the exchange; anything else is refused and changes nothing

@@ -38,6 +38,25 @@ def test_autograd_matches_entry_points(dtype, d, causal):
         assert torch.equal(leaf.grad, w), name
 
 
+@pytest.mark.parametrize("causal", [0, 1])
+def test_autograd_joint_normalisation(causal):
+    B, H, N, d, kw, rank = 1, 2, 800, 64, 24, 3
+    q, k, v, wn, wf = make_inputs(B, H, N, d, "bf16", 1.0 / np.sqrt(d), 1620 + causal)
+    t = upload(q, k, v, wn, wf, "bf16")
+    gen = torch.Generator(device="cuda:0")
+    gen.manual_seed(1621)
+    g = torch.randn(t[0].shape, generator=gen, device="cuda:0").to(t[0].dtype)
+    leaves = [x.clone().requires_grad_(True) for x in t]
+    out = binding.fmm_attention(*leaves, kw, rank, causal, joint=True)
+    (out.float() * g.float()).sum().backward()
+    want_out = binding.forward(*t, kw, rank, causal, joint=True)
+    want = binding.backward(t[0], t[1], t[2], g, t[3], t[4], kw, rank, causal, joint=True)
+    torch.cuda.synchronize()
+    assert torch.equal(out.detach(), want_out)
+    for name, leaf, w in zip(("q", "k", "v", "w_near", "w_far"), leaves, want):
+        assert torch.equal(leaf.grad, w), name
+
+
 def test_autograd_only_where_asked():
     # inputs without requires_grad get no gradient; the others still do
     B, H, N, d, kw, rank = 1, 2, 700, 32, 16, 2

@@ -18,26 +18,28 @@ from paper_2108_02347_amd.inputs import make_inputs, to_dtype
 pytestmark = pytest.mark.gpu
 
 
-def check_backward(B, H, N, d, kw, rank, causal, dtype, seed, std=1.0, shift=0.0):
+def check_backward(B, H, N, d, kw, rank, causal, dtype, seed, std=1.0, shift=0.0, joint=False):
     q, k, v, wn, wf = make_inputs(B, H, N, d, dtype, std, seed)
     if shift:
         q, k = to_dtype(q + shift, dtype), to_dtype(k + shift, dtype)
     g = to_dtype(np.random.default_rng(seed + 1).standard_normal(q.shape), dtype)
     log(f"backward B={B} H={H} N={N} d={d} k={kw} r={rank} causal={causal} {dtype} "
-        f"seed={seed}")
+        f"joint={joint} seed={seed}")
     tq, tk, tv, twn, twf = upload(q, k, v, wn, wf, dtype)
     tg = torch.from_numpy(np.asarray(g, dtype=np.float32)).to("cuda:0").to(tq.dtype)
-    got = binding.backward(tq, tk, tv, tg, twn, twf, kw, rank, causal)
+    norm = "joint" if joint else "map"
+    got = binding.backward(tq, tk, tv, tg, twn, twf, kw, rank, causal, joint=joint)
     torch.cuda.synchronize()
     got = [x.float().cpu().numpy().astype(np.float64) for x in got]
-    want = ref.fmm_attention_backward_stream(q, k, v, wn, wf, g, kw, rank, bool(causal))
+    want = ref.fmm_attention_backward_stream(q, k, v, wn, wf, g, kw, rank, bool(causal),
+                                             norm=norm)
     errs = []
     for name, a, b in zip(("dq", "dk", "dv"), got[:3], want[:3]):
         assert np.isfinite(a).all(), f"non-finite {name}"
         errs.append(slice_errors(a, b).max())
     # dw: scale by the absolute sums of the terms
     near = ref.near_stream(q, k, v, kw, bool(causal))
-    far = ref.far_stream(q, k, v, rank, bool(causal))
+    far = ref.far_stream(q, k, v, rank, bool(causal), norm=norm)
     sa, sc = ref.sigmoid(wn), ref.sigmoid(wf)
     scale_n = sa * (1 - sa) * np.einsum("bhic,bhic->h", np.abs(g), np.abs(near))
     scale_f = sc * (1 - sc) * np.einsum("bhic,bhic->h", np.abs(g), np.abs(far))
@@ -71,6 +73,21 @@ def test_backward_wide_band_and_rank3(causal, dtype):
     check_backward(1, 2, 1200, 32, 300, 2, causal, dtype, 2100 + causal)
     check_backward(2, 1, 900, 64, 30, 3, causal, dtype, 2200 + causal, shift=1.0)
     check_backward(1, 1, 700, 128, 40, 3, causal, dtype, 2250 + causal, shift=1.0)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("causal", [0, 1])
+def test_backward_joint_normalisation(causal, dtype):
+    # the far maps normalised as one matrix (Sec. 1.2): every width, one to
+    # three maps, several segments and staging rounds
+    worst = 0.0
+    for B, H, N, d, kw, rank in ((1, 2, 700, 32, 20, 2), (2, 1, 900, 64, 40, 3),
+                                 (1, 1, 500, 128, 16, 2), (1, 2, 300, 16, 5, 1),
+                                 (1, 1, 1500, 64, 64, 2)):
+        worst = max(worst, check_backward(B, H, N, d, kw, rank, causal, dtype,
+                                          2500 + d + N + causal, std=1.0 / np.sqrt(d) * 2,
+                                          joint=True))
+    log(f"joint backward causal={causal} {dtype}: worst {worst:.2e}")
 
 
 @pytest.mark.parametrize("causal", [0, 1])
