@@ -572,6 +572,101 @@ def fast_weight_stream(q, k, v, beta) -> np.ndarray:
     return out
 
 
+def _normalised_phi(x):
+    """p = phi_1(x) / sum_c phi_1(x)_c over the last axis, and that sum."""
+    f = phi(x, 1)
+    s = f.sum(axis=-1, keepdims=True)
+    return f / s, s
+
+
+def fast_weight_backward_stream(q, k, v, beta, f):
+    """Gradients of sum(f * fw) with fw = fast_weight_stream(q, k, v, beta):
+    returns (fw, dq, dk, dv, dbeta).  The recurrence differentiated and run
+    backwards, per (b, h), with G_i the gradient with respect to W_i and Zs_i
+    the one with respect to z_i (both including every later use):
+        n_i = W_i pq_i,  s_i = z_i . pq_i,  fw_i = n_i / s_i
+        dn_i = f_i / s_i,  ds_i = -(f_i . fw_i) / s_i
+        G_i = dn_i pq_i^T + G_{i+1} (I - beta_{i+1} pk_{i+1} pk_{i+1}^T),  G_N = 0
+        Zs_i = ds_i pq_i + Zs_{i+1},  Zs_N = 0
+        dpq_i = W_i^T dn_i + ds_i z_i
+        e_i = v_i - u_i,  gp_i = G_i pk_i
+        dv_i = beta_i gp_i,  dbeta_i = e_i . gp_i
+        dpk_i = beta_i (G_i^T e_i - W_{i-1}^T gp_i) + Zs_i
+    and through p = phi / sum(phi): dphi = (dp - dp . p) / sum(phi), then
+    dx = phi_1'(x) dphi.  The forward states W_i are kept from a forward
+    sweep (plain loops)."""
+    q, k, v = _check(q, k, v)
+    beta = np.asarray(beta, dtype=np.float64)
+    f = np.asarray(f, dtype=np.float64)
+    b_, h_, n, d = q.shape
+    pk, sk = _normalised_phi(k)
+    pq, sq = _normalised_phi(q)
+    fw = np.empty_like(v)
+    dpq = np.zeros_like(q)
+    dpk = np.zeros_like(k)
+    dv = np.zeros_like(v)
+    dbeta = np.zeros_like(beta)
+    for bb in range(b_):
+        for hh in range(h_):
+            ws = [np.zeros((d, d))]          # ws[i + 1] = W_i, ws[0] = W_{-1}
+            zs = [np.zeros(d)]
+            us = []
+            for i in range(n):
+                p = pk[bb, hh, i]
+                u = ws[-1] @ p
+                us.append(u)
+                ws.append(ws[-1] + beta[bb, hh, i] * np.outer(v[bb, hh, i] - u, p))
+                zs.append(zs[-1] + p)
+                fw[bb, hh, i] = (ws[-1] @ pq[bb, hh, i]) / (zs[-1] @ pq[bb, hh, i])
+            g_w = np.zeros((d, d))
+            z_s = np.zeros(d)
+            for i in range(n - 1, -1, -1):
+                if i + 1 < n:  # carry G_{i+1} back through W_{i+1}'s update
+                    p1 = pk[bb, hh, i + 1]
+                    g_w = g_w - beta[bb, hh, i + 1] * np.outer(g_w @ p1, p1)
+                wi, wprev, zi = ws[i + 1], ws[i], zs[i + 1]
+                pqi, p = pq[bb, hh, i], pk[bb, hh, i]
+                s_i = zi @ pqi
+                dn = f[bb, hh, i] / s_i
+                ds = -(f[bb, hh, i] @ fw[bb, hh, i]) / s_i
+                g_w = g_w + np.outer(dn, pqi)
+                z_s = z_s + ds * pqi
+                dpq[bb, hh, i] = wi.T @ dn + ds * zi
+                e = v[bb, hh, i] - us[i]
+                gp = g_w @ p
+                dv[bb, hh, i] = beta[bb, hh, i] * gp
+                dbeta[bb, hh, i] = e @ gp
+                dpk[bb, hh, i] = beta[bb, hh, i] * (g_w.T @ e - wprev.T @ gp) + z_s
+    dq = phi_grad(q, 1) * (dpq - (dpq * pq).sum(axis=-1, keepdims=True)) / sq
+    dk = phi_grad(k, 1) * (dpk - (dpk * pk).sum(axis=-1, keepdims=True)) / sk
+    return fw, dq, dk, dv, dbeta
+
+
+def fmm_fast_weight_backward(q, k, v, beta, w_near, w_far, dout, band_k: int, n_linear: int):
+    """Gradients of sum(dout * out) with out = fmm_fast_weight_forward(...):
+    returns (dq, dk, dv, dbeta, dw_near, dw_far).  With a = sigmoid(w_near),
+    c = sigmoid(w_far): the near field receives a dout, the fast-weight far
+    field and (n_linear = 1) the linear far part c dout, and
+    dw_near = a (1 - a) sum dout . near, dw_far = c (1 - c) sum dout . far."""
+    if n_linear not in (0, 1):
+        raise ValueError("n_linear must be 0 or 1")
+    q, k, v = _check(q, k, v)
+    dout = np.asarray(dout, dtype=np.float64)
+    a = sigmoid(w_near)[None, :, None, None]
+    c = sigmoid(w_far)[None, :, None, None]
+    near, dq, dk, dv = _near_backward(q, k, v, a * dout, band_k, True)
+    far, dqf, dkf, dvf, dbeta = fast_weight_backward_stream(q, k, v, beta, c * dout)
+    dq, dk, dv = dq + dqf, dk + dkf, dv + dvf
+    if n_linear:
+        lin, dql, dkl, dvl = _far_backward(q, k, v, c * dout, 1, True, "map")
+        far = far + lin
+        dq, dk, dv = dq + dql, dk + dkl, dv + dvl
+    sa, sc = sigmoid(w_near), sigmoid(w_far)
+    dw_near = sa * (1.0 - sa) * np.einsum("bhic,bhic->h", dout, near)
+    dw_far = sc * (1.0 - sc) * np.einsum("bhic,bhic->h", dout, far)
+    return dq, dk, dv, dbeta, dw_near, dw_far
+
+
 def fmm_fast_weight_forward(q, k, v, beta, w_near, w_far, band_k: int,
                             n_linear: int) -> np.ndarray:
     """FMMformer with the fast-weight far field (Appendix D), causal:

@@ -118,6 +118,18 @@ MUTATIONS = [
     ("backward: key-side near gradient unscaled",
      "dk[:, :, j] += tau * ds[:, :, ok, t, None] * q[:, :, rows[ok]]",
      "dk[:, :, j] += ds[:, :, ok, t, None] * q[:, :, rows[ok]]"),
+    ("fast-weight backward: W gradient not carried through the next write",
+     "g_w = g_w - beta[bb, hh, i + 1] * np.outer(g_w @ p1, p1)",
+     "g_w = g_w + 0.0 * beta[bb, hh, i + 1]"),
+    ("fast-weight backward: key gradient reads W_i instead of W_{i-1}",
+     "dpk[bb, hh, i] = beta[bb, hh, i] * (g_w.T @ e - wprev.T @ gp) + z_s",
+     "dpk[bb, hh, i] = beta[bb, hh, i] * (g_w.T @ e - wi.T @ gp) + z_s"),
+    ("fast-weight backward: normalisation derivative without the projection",
+     "dk = phi_grad(k, 1) * (dpk - (dpk * pk).sum(axis=-1, keepdims=True)) / sk",
+     "dk = phi_grad(k, 1) * dpk / sk"),
+    ("fast-weight operator backward: linear part's gradients dropped",
+     "        dq, dk, dv = dq + dql, dk + dkl, dv + dvl",
+     "        dq, dk, dv = dq, dk, dv"),
 ]
 
 

@@ -665,3 +665,79 @@ def test_fast_weight_operator_composition():
         got = ref.fmm_fast_weight_forward(q, k, v, beta, wn, wf, 3, nl)
         want = sn[None, :, None, None] * near + sf[None, :, None, None] * (fw + nl * lin)
         np.testing.assert_allclose(got, want, rtol=1e-13)
+
+
+# ------------------------------------------------------------------ fast-weight backward
+# The gradients of the fast-weight far field and of the whole fast-weight
+# operator are pinned by central finite differences of the forward oracle and
+# by torch float64 autograd of the recurrence written in torch.
+
+def _fd(fn, args, eps=1e-6):
+    out = []
+    for ai, x in enumerate(args):
+        g = np.zeros_like(x)
+        for idx in np.ndindex(x.shape):
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += eps
+            xm[idx] -= eps
+            a1, a2 = list(args), list(args)
+            a1[ai], a2[ai] = xp, xm
+            g[idx] = (fn(*a1) - fn(*a2)) / (2 * eps)
+        out.append(g)
+    return out
+
+
+def test_fast_weight_backward_finite_differences():
+    b, h, n, d = 1, 2, 7, 3
+    q, k, v, f = (rnd((b, h, n, d), s) for s in (700, 701, 702, 703))
+    beta = np.random.default_rng(704).uniform(0.0, 1.0, (b, h, n))
+    fw, dq, dk, dv, dbeta = ref.fast_weight_backward_stream(q, k, v, beta, f)
+    np.testing.assert_array_equal(fw, ref.fast_weight_stream(q, k, v, beta))
+    loss = lambda q_, k_, v_, b_: float((ref.fast_weight_stream(q_, k_, v_, b_) * f).sum())
+    want = _fd(loss, [q, k, v, beta])
+    for g, w in zip((dq, dk, dv, dbeta), want):
+        np.testing.assert_allclose(g, w, rtol=1e-6, atol=1e-8 * max(1.0, np.abs(w).max()))
+
+
+def _torch_fast_weight(q, k, v, beta):
+    def p(x):
+        f = torch.nn.functional.elu(x) + 1
+        return f / f.sum(-1, keepdim=True)
+    pk, pq = p(k), p(q)
+    b, h, n, d = q.shape
+    w = torch.zeros(b, h, d, d, dtype=q.dtype)
+    z = torch.zeros(b, h, d, dtype=q.dtype)
+    outs = []
+    for i in range(n):
+        ki, qi = pk[:, :, i], pq[:, :, i]
+        u = (w @ ki[..., None])[..., 0]
+        w = w + beta[:, :, i, None, None] * (v[:, :, i] - u)[..., None] * ki[..., None, :]
+        z = z + ki
+        outs.append((w @ qi[..., None])[..., 0] / (z * qi).sum(-1, keepdim=True))
+    return torch.stack(outs, dim=2)
+
+
+def test_fast_weight_backward_matches_torch_autograd():
+    b, h, n, d = 2, 2, 13, 4
+    q, k, v, f = (rnd((b, h, n, d), s) for s in (710, 711, 712, 713))
+    beta = np.random.default_rng(714).uniform(0.0, 1.0, (b, h, n))
+    ts = [torch.tensor(x, requires_grad=True) for x in (q, k, v, beta)]
+    (_torch_fast_weight(*ts) * torch.tensor(f)).sum().backward()
+    got = ref.fast_weight_backward_stream(q, k, v, beta, f)[1:]
+    for g, t in zip(got, ts):
+        np.testing.assert_allclose(g, t.grad.numpy(), rtol=1e-9, atol=1e-12)
+
+
+@pytest.mark.parametrize("n_linear", [0, 1])
+def test_fast_weight_operator_backward_finite_differences(n_linear):
+    b, h, n, d, kw = 1, 2, 6, 3, 2
+    q, k, v, g = (rnd((b, h, n, d), s) for s in (720, 721, 722, 723))
+    beta = np.random.default_rng(724).uniform(0.0, 1.0, (b, h, n))
+    wn, wf = rnd(h, 725), rnd(h, 726)
+    got = ref.fmm_fast_weight_backward(q, k, v, beta, wn, wf, g, kw, n_linear)
+    loss = lambda q_, k_, v_, b_, wn_, wf_: float(
+        (ref.fmm_fast_weight_forward(q_, k_, v_, b_, wn_, wf_, kw, n_linear) * g).sum())
+    want = _fd(loss, [q, k, v, beta, wn, wf])
+    # got: dq, dk, dv, dbeta, dw_near, dw_far (the inputs' order)
+    for gg, w in zip(got, want):
+        np.testing.assert_allclose(gg, w, rtol=1e-6, atol=1e-8 * max(1.0, np.abs(w).max()))
