@@ -661,9 +661,9 @@ def fmm_fast_weight_backward(q, k, v, beta, w_near, w_far, dout, band_k: int, n_
         lin, dql, dkl, dvl = _far_backward(q, k, v, c * dout, 1, True, "map")
         far = far + lin
         dq, dk, dv = dq + dql, dk + dkl, dv + dvl
-    sa, sc = sigmoid(w_near), sigmoid(w_far)
-    dw_near = sa * (1.0 - sa) * np.einsum("bhic,bhic->h", dout, near)
-    dw_far = sc * (1.0 - sc) * np.einsum("bhic,bhic->h", dout, far)
+    s_near, s_far = sigmoid(w_near), sigmoid(w_far)
+    dw_near = s_near * (1.0 - s_near) * np.einsum("bhic,bhic->h", dout, near)
+    dw_far = s_far * (1.0 - s_far) * np.einsum("bhic,bhic->h", dout, far)
     return dq, dk, dv, dbeta, dw_near, dw_far
 
 
