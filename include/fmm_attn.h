@@ -294,6 +294,28 @@ int fmm_attn_forward_fastweight(const void* q, const void* k, const void* v,
                                 int band_k, int n_linear, const float* w_near,
                                 const float* w_far, int dtype, void* stream);
 
+/*
+ * fmm_attn_backward_fastweight - gradients of sum(dout * out) for the output
+ * of fmm_attn_forward_fastweight with the same arguments (Appendix D):
+ *   dq, dk, dv : [B, H, N, d] of dtype, written completely;
+ *   dbeta      : device float[B, H, N], the gradient with respect to beta;
+ *   dw_near, dw_far : device float[H], with respect to the blend logits.
+ * The fast-weight part is differentiated through its recurrence: with G_i
+ * the gradient with respect to W_i, G_i = dn_i p(q_i)^T + G_{i+1} (I -
+ * beta_{i+1} p(k_{i+1}) p(k_{i+1})^T), from which dv_i = beta_i G_i p(k_i),
+ * dbeta_i = (v_i - u_i) . G_i p(k_i) and the key and query gradients follow;
+ * the near field and the linear part are those of fmm_attn_backward (rank 1,
+ * causal).  The states W_i of every step are kept in the library-owned
+ * workspace: B*H*N*d*(d+1) floats beside the backward's own.  No output may
+ * overlap an input or another output.  Errors as fmm_attn_backward.
+ */
+int fmm_attn_backward_fastweight(const void* q, const void* k, const void* v,
+                                 const float* beta, const void* dout, void* dq, void* dk,
+                                 void* dv, float* dbeta, float* dw_near, float* dw_far,
+                                 int B, int H, int N, int d, int band_k, int n_linear,
+                                 const float* w_near, const float* w_far, int dtype,
+                                 void* stream);
+
 /* Human-readable text for a status code; never NULL, static storage. */
 const char* fmm_attn_status_string(int status);
 

@@ -37,7 +37,7 @@ EXPORTS = (
     "fmm_attn_version", "fmm_attn_kernel_timing", "fmm_attn_kernel_timing_read",
     "fmm_attn_forward_noalloc", "fmm_attn_noalloc_max_bytes", "fmm_attn_forward_ex",
     "fmm_attn_backward", "fmm_attn_backward_ex", "fmm_attn_layer_forward",
-    "fmm_attn_forward_fastweight",
+    "fmm_attn_forward_fastweight", "fmm_attn_backward_fastweight",
     "fmm_attn_set_one_launch",
 )
 
@@ -70,6 +70,8 @@ def lib() -> ctypes.CDLL:
     h.fmm_attn_forward_ws.restype = ci
     h.fmm_attn_forward_fastweight.argtypes = [vp] * 5 + [ci] * 6 + [cf, cf, ci, vp]
     h.fmm_attn_forward_fastweight.restype = ci
+    h.fmm_attn_backward_fastweight.argtypes = [vp] * 11 + [ci] * 6 + [cf, cf, ci, vp]
+    h.fmm_attn_backward_fastweight.restype = ci
     h.fmm_attn_layer_forward.argtypes = [vp] * 4 + [ci] * 7 + [cf, cf, ci, vp]
     h.fmm_attn_layer_forward.restype = ci
     h.fmm_attn_backward.argtypes = [vp] * 9 + [ci] * 7 + [cf, cf, ci, vp]
@@ -281,6 +283,30 @@ def fmm_attention(q, k, v, w_near, w_far, band_k: int, rank: int, causal: bool,
     return _FmmAttention.apply(q, k, v, w_near, w_far, band_k, rank, causal, joint)
 
 
+class _FmmFastWeight(torch.autograd.Function):
+    """The fast-weight operator (Appendix D) as a torch.autograd function over
+    forward_fastweight and backward_fastweight."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, beta, w_near, w_far, band_k, n_linear):
+        ctx.save_for_backward(q, k, v, beta, w_near, w_far)
+        ctx.args = (int(band_k), int(n_linear))
+        return forward_fastweight(q, k, v, beta, w_near, w_far, band_k, n_linear)
+
+    @staticmethod
+    def backward(ctx, g):
+        q, k, v, beta, w_near, w_far = ctx.saved_tensors
+        dq, dk, dv, dbeta, dwn, dwf = backward_fastweight(q, k, v, beta, g.contiguous(), w_near,
+                                                          w_far, *ctx.args)
+        return dq, dk, dv, dbeta, dwn, dwf, None, None
+
+
+def fmm_fast_weight_attention(q, k, v, beta, w_near, w_far, band_k: int, n_linear: int):
+    """The fast-weight operator as a differentiable function of q, k, v, beta
+    and the two blend logits (torch.autograd)."""
+    return _FmmFastWeight.apply(q, k, v, beta, w_near, w_far, band_k, n_linear)
+
+
 def layer_forward(x, w_qkv, w_out, heads: int, w_near, w_far, band_k: int, rank: int,
                   causal: bool, out=None):
     """The attention layer: [q | k | v] = x W_qkv, the operator per head, the
@@ -325,6 +351,27 @@ def forward_fastweight(q, k, v, beta, w_near, w_far, band_k: int, n_linear: int,
         _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(out), B, H, N, d, int(band_k),
         int(n_linear), _ptr(w_near), _ptr(w_far), dt, _stream_of(q)))
     return out
+
+
+def backward_fastweight(q, k, v, beta, dout, w_near, w_far, band_k: int, n_linear: int):
+    """Gradients of the fast-weight operator (forward_fastweight) for dout =
+    dL/d(out): returns (dq, dk, dv, dbeta, dw_near, dw_far)."""
+    B, H, N, d = _prep(q, k, v, w_near, w_far)
+    _check_out(dout, q)
+    if (not isinstance(beta, torch.Tensor) or beta.dtype != torch.float32
+            or beta.device != q.device or tuple(beta.shape) != (B, H, N)
+            or not beta.is_contiguous()):
+        raise ValueError("beta must be a contiguous float32 [B, H, N] tensor on q's device")
+    dq, dk, dv = (torch.empty_like(q) for _ in range(3))
+    dbeta = torch.empty_like(beta)
+    dwn = torch.empty_like(w_near)
+    dwf = torch.empty_like(w_far)
+    dt = FMM_DTYPE_BF16 if q.dtype == torch.bfloat16 else FMM_DTYPE_F32
+    _check(lib().fmm_attn_backward_fastweight(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv),
+        _ptr(dbeta), _ptr(dwn), _ptr(dwf), B, H, N, d, int(band_k), int(n_linear),
+        _ptr(w_near), _ptr(w_far), dt, _stream_of(q)))
+    return dq, dk, dv, dbeta, dwn, dwf
 
 
 def raw_forward(q_ptr, k_ptr, v_ptr, out_ptr, B, H, N, d, band_k, rank, causal, wn_ptr,

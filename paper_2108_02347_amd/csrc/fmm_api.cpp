@@ -650,6 +650,132 @@ int run_fastweight(const void* q, const void* k, const void* v, const float* bet
   return fmm::launch_fast_weight(L, f) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
 }
 
+// Backward of the fast-weight operator: the operator's backward at rank 1,
+// causal (the near field, and the linear far part when n_linear = 1; with
+// n_linear = 0 its far part is removed by -inf logits), then the fast-weight
+// kernel, which adds its gradients to dq, dk, dv, writes dbeta and adds its
+// share to dw_far.
+int run_backward_fastweight(const void* q, const void* k, const void* v, const float* beta,
+                            const void* dout, void* dq, void* dk, void* dv, float* dbeta,
+                            float* dw_near, float* dw_far, int B, int H, int N, int d,
+                            int band_k, int n_linear, const float* w_near, const float* w_far,
+                            int dtype, void* stream) {
+  int st = validate(q, k, v, dq, B, H, N, d, band_k, 1, 1, w_near, w_far, dtype,
+                    FMM_FAR_NORM_PER_MAP);
+  if (st != FMM_OK) return st;
+  if (!dout || !dk || !dv || !dw_near || !dw_far || !beta || !dbeta) return FMM_ERR_INVALID_ARG;
+  if (n_linear != 0 && n_linear != 1) return FMM_ERR_INVALID_ARG;
+  const size_t es = dtype == FMM_DTYPE_BF16 ? 2 : 4;
+  const size_t bytes = (size_t)B * H * N * d * es;  // fits: validate checked it
+  for (const void* p : {dout, (const void*)dk, (const void*)dv})
+    if ((uintptr_t)p % 16) return FMM_ERR_INVALID_ARG;
+  if ((uintptr_t)dw_near % 4 || (uintptr_t)dw_far % 4 || (uintptr_t)beta % 4 ||
+      (uintptr_t)dbeta % 4)
+    return FMM_ERR_INVALID_ARG;
+  const void* ins[4] = {q, k, v, dout};
+  void* outs[3] = {dq, dk, dv};
+  for (void* o : outs)
+    for (const void* i : ins)
+      if (overlaps(o, i, bytes)) return FMM_ERR_INVALID_ARG;
+  if (overlaps(dq, dk, bytes) || overlaps(dq, dv, bytes) || overlaps(dk, dv, bytes))
+    return FMM_ERR_INVALID_ARG;
+  const size_t nb = (size_t)B * H * N * 4;
+  for (const void* o : {(const void*)dq, (const void*)dk, (const void*)dv})
+    if (overlaps2(dbeta, nb, o, bytes)) return FMM_ERR_INVALID_ARG;
+  if (overlaps2(dbeta, nb, beta, nb) || overlaps(dw_near, dw_far, (size_t)H * 4))
+    return FMM_ERR_INVALID_ARG;
+  const BwdPlan bp = bwd_plan(B, H, N, d, 1, dtype);
+  if (bp.total == 0) return FMM_ERR_UNSUPPORTED;
+  // after the backward's workspace: W_i and z_i of every step, the per-slice
+  // sums, H floats of -inf
+  typedef unsigned __int128 u128;
+  const u128 wst = (u128)B * H * N * d * d * 4, zst = (u128)B * H * N * d * 4;
+  const u128 tot = (u128)bp.total + align256((size_t)std::min<u128>(wst, SIZE_MAX / 8)) +
+                   align256((size_t)std::min<u128>(zst, SIZE_MAX / 8)) +
+                   align256((size_t)B * H * 4) + align256((size_t)H * 4);
+  if (tot > (u128)(SIZE_MAX / 4)) return FMM_ERR_UNSUPPORTED;
+  const size_t off_w = bp.total, off_z = off_w + align256((size_t)wst);
+  const size_t off_g = off_z + align256((size_t)zst), off_m = off_g + align256((size_t)B * H * 4);
+  fmm::LaunchArgs fa = make_args(q, k, v, dq, B, H, N, d, band_k, 1, 1, w_near, w_far, dtype,
+                                 FMM_FAR_NORM_PER_MAP, nullptr, bp.p, stream);
+  fmm::BwdArgs ba;
+  ba.q = q;
+  ba.k = k;
+  ba.v = v;
+  ba.dout = dout;
+  ba.dq = dq;
+  ba.dk = dk;
+  ba.dv = dv;
+  ba.dw_near = dw_near;
+  ba.dw_far = dw_far;
+  ba.w_near = w_near;
+  ba.w_far = w_far;
+  ba.B = B;
+  ba.H = H;
+  ba.N = N;
+  ba.d = d;
+  ba.band_k = fa.band_k;
+  ba.rank = 1;
+  ba.causal = 1;
+  ba.dtype = dtype;
+  ba.stream = stream;
+  ba.nseg = bp.p.nseg;
+  ba.L = bp.p.L;
+  fill_bwd_args(ba, bp, nullptr, B, H);
+  fmm::FwBwdArgs fb;
+  fb.q = q;
+  fb.k = k;
+  fb.v = v;
+  fb.beta = beta;
+  fb.dout = dout;
+  fb.dq = dq;
+  fb.dk = dk;
+  fb.dv = dv;
+  fb.dbeta = dbeta;
+  fb.dw_far = dw_far;
+  fb.w_far = w_far;
+  fb.wst = fb.zst = fb.gfw = nullptr;
+  fb.B = B;
+  fb.H = H;
+  fb.N = N;
+  fb.d = d;
+  fb.dtype = dtype;
+  fb.stream = stream;
+  EventTimer& t = timer();
+  {
+    std::lock_guard<std::mutex> g(t.mu);
+    fmm::Launcher dry;
+    dry.timer = &t;
+    dry.dry = true;
+    if (fmm::launch_state_only(fa, dry) != hipSuccess ||
+        fmm::launch_backward_tail(ba, dry) != hipSuccess ||
+        fmm::launch_fast_weight_backward(dry, fb) != hipSuccess)
+      return dry.err == hipErrorInvalidConfiguration ? FMM_ERR_UNSUPPORTED : FMM_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> wl(ws_mutex());
+  void* ws = nullptr;
+  st = acquire_ws_locked(stream, (size_t)tot, &ws);
+  if (st != FMM_OK) return st;
+  const uintptr_t w = reinterpret_cast<uintptr_t>(ws);
+  fa.ws = (float*)ws;
+  fill_bwd_args(ba, bp, ws, B, H);
+  fb.wst = reinterpret_cast<float*>(w + off_w);
+  fb.zst = reinterpret_cast<float*>(w + off_z);
+  fb.gfw = reinterpret_cast<float*>(w + off_g);
+  float* minus_inf = reinterpret_cast<float*>(w + off_m);
+  std::lock_guard<std::mutex> g(t.mu);
+  fmm::Launcher L;
+  L.timer = &t;
+  if (!n_linear) {
+    if (fmm::launch_fill(L, minus_inf, H, -INFINITY, stream) != hipSuccess) return FMM_ERR_HIP;
+    fa.w_far = minus_inf;
+    ba.w_far = minus_inf;
+  }
+  if (fmm::launch_state_only(fa, L) != hipSuccess) return FMM_ERR_HIP;
+  if (fmm::launch_backward_tail(ba, L) != hipSuccess) return FMM_ERR_HIP;
+  return fmm::launch_fast_weight_backward(L, fb) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
+}
+
 }  // namespace
 
 namespace fmm {
@@ -714,6 +840,15 @@ int fmm_attn_backward_ex(const void* q, const void* k, const void* v, const void
                          void* stream) {
   return run_backward(q, k, v, dout, dq, dk, dv, dw_near, dw_far, B, H, N, d, band_k, rank,
                       causal, w_near, w_far, dtype, far_norm, stream);
+}
+
+int fmm_attn_backward_fastweight(const void* q, const void* k, const void* v, const float* beta,
+                                 const void* dout, void* dq, void* dk, void* dv, float* dbeta,
+                                 float* dw_near, float* dw_far, int B, int H, int N, int d,
+                                 int band_k, int n_linear, const float* w_near,
+                                 const float* w_far, int dtype, void* stream) {
+  return run_backward_fastweight(q, k, v, beta, dout, dq, dk, dv, dbeta, dw_near, dw_far, B, H,
+                                 N, d, band_k, n_linear, w_near, w_far, dtype, stream);
 }
 
 int fmm_attn_layer_forward(const void* x, const void* w_qkv, const void* w_out, void* y, int B,

@@ -15,6 +15,8 @@
 // operator (near field and, for the two-kernel variant, the linear far part).
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include "fmm_device.h"
 #include "fmm_launch.h"
 
@@ -151,6 +153,243 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight(
   }
 }
 
+// ------------------------------------------------------------------ backward
+// Gradients of sum(f . fw) for f_i = sigmoid(w_far[h]) g_i, per (b, h), by the
+// recurrence differentiated and run backwards (G_i: the gradient with respect
+// to W_i including every later use, Zs_i: with respect to z_i):
+//   n_i = W_i p(q_i),  s_i = z_i . p(q_i),  fw_i = n_i / s_i
+//   dn_i = f_i / s_i,  ds_i = -(f_i . fw_i) / s_i
+//   G_i = dn_i p(q_i)^T + G_{i+1} (I - beta_{i+1} p(k_{i+1}) p(k_{i+1})^T)
+//   Zs_i = ds_i p(q_i) + Zs_{i+1}
+//   dp(q_i) = W_i^T dn_i + ds_i z_i
+//   e_i = v_i - W_{i-1} p(k_i),  gp_i = G_i p(k_i)
+//   dv_i = beta_i gp_i,  dbeta_i = e_i . gp_i
+//   dp(k_i) = beta_i (G_i^T e_i - W_{i-1}^T gp_i) + Zs_i
+// then through p = phi_1 / sum(phi_1): dx = phi_1'(x) (dp - dp . p) / sum(phi_1).
+// A forward sweep first stores W_i and z_i (thread r: row r of W_i, z_i[r]) in
+// the workspace; the backward sweep keeps row r of G and Zs[r] in registers,
+// forms the two column sums (W_i^T dn and G^T e - W_{i-1}^T gp) through LDS and
+// adds its dq, dk, dv to the gradients already in place (the near field and
+// the linear part, from the operator's backward); it writes dbeta and, per
+// slice, sum_i g_i . fw_i for dw_far.
+template <typename T, int D>
+__global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const float* __restrict__ beta, const T* __restrict__ dout, T* __restrict__ dq,
+    T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ dbeta,
+    float* __restrict__ wst, float* __restrict__ zst, float* __restrict__ gfw,
+    const float* __restrict__ w_far, int H, int N) {
+  constexpr int NWV = D > 64 ? D / 64 : 1;
+  constexpr int ROWS = D >= 64 ? 4 : D / 16;
+  constexpr int LD = D + 1;  // padded rows of the column-sum buffers
+  __shared__ float pk_s[2][D], pq_s[2][D];
+  __shared__ float red[2 * 3 * NWV];
+  extern __shared__ float colbuf[];  // two D x LD buffers
+  float* cb1 = colbuf;
+  float* cb2 = colbuf + D * LD;
+  const int bh = blockIdx.x, h = bh % H;
+  const int r = threadIdx.x;
+  const bool act = r < D;
+  const size_t base = (size_t)bh * N * D;
+  float* ws = wst + (size_t)bh * N * D * D;
+  float* zs = zst + (size_t)bh * N * D;
+  const float sf = sigmoidf_exact(w_far[h]);
+  int slot = 0;  // parity of the block sums' scratch
+  auto bsum = [&](float x, int which) {
+    const float t = block_sum<NWV, ROWS>(x, red + 2 * which * NWV, slot);
+    return t;
+  };
+  auto norm_phi = [&](float x, float* p_s, float& p, float& sum) {
+    const float f = act ? phi_l(x, 0) : 0.f;
+    sum = bsum(f, 0);
+    p = f / sum;
+    if (act) p_s[r] = p;
+  };
+
+  // ---- forward sweep: W_i and z_i of every step into the workspace
+  {
+    float wrow[D];
+#pragma unroll
+    for (int c = 0; c < D; ++c) wrow[c] = 0.f;
+    float zr = 0.f;
+    for (int i = 0; i < N; ++i) {
+      const int par = i & 1;
+      slot = par;
+      const size_t o = base + (size_t)i * D + r;
+      const float xk = act ? ld_elem<T>(k + o) : 0.f;
+      const float xv = act ? ld_elem<T>(v + o) : 0.f;
+      const float bt = beta[(size_t)bh * N + i];
+      float pk, sk;
+      norm_phi(xk, pk_s[par], pk, sk);
+      if constexpr (NWV > 1) __syncthreads();
+      float u = 0.f;
+#pragma unroll
+      for (int c = 0; c < D; ++c) u = fmaf(wrow[c], pk_s[par][c], u);
+      const float coef = bt * (xv - u);
+#pragma unroll
+      for (int c = 0; c < D; ++c) wrow[c] = fmaf(coef, pk_s[par][c], wrow[c]);
+      zr += pk;
+      if (act) {
+        float* dst = ws + ((size_t)i * D + r) * D;
+#pragma unroll
+        for (int c = 0; c < D; c += 4)
+          *reinterpret_cast<float4*>(dst + c) =
+              make_float4(wrow[c], wrow[c + 1], wrow[c + 2], wrow[c + 3]);
+        zs[(size_t)i * D + r] = zr;
+      }
+    }
+  }
+  // the stores above are read back below by other threads of the workgroup
+  __threadfence_block();
+  __syncthreads();
+
+  // ---- backward sweep
+  float grow[D];
+#pragma unroll
+  for (int c = 0; c < D; ++c) grow[c] = 0.f;
+  float zsr = 0.f;       // Zs[r]
+  float bt_next = 0.f;   // beta_{i+1}
+  float acc_gfw = 0.f;   // this thread's share of sum_i g_i . fw_i
+  for (int i = N - 1; i >= 0; --i) {
+    const int par = i & 1;
+    slot = par;
+    const size_t o = base + (size_t)i * D + r;
+    const float xk = act ? ld_elem<T>(k + o) : 0.f;
+    const float xq = act ? ld_elem<T>(q + o) : 0.f;
+    const float xv = act ? ld_elem<T>(v + o) : 0.f;
+    const float xg = act ? ld_elem<T>(dout + o) : 0.f;
+    const float bt = beta[(size_t)bh * N + i];
+    float wi[D], wp[D];
+    const float* wsrc = ws + ((size_t)i * D + (act ? r : 0)) * D;
+#pragma unroll
+    for (int c = 0; c < D; c += 4) {
+      const float4 a = *reinterpret_cast<const float4*>(wsrc + c);
+      wi[c] = a.x; wi[c + 1] = a.y; wi[c + 2] = a.z; wi[c + 3] = a.w;
+      if (i > 0) {
+        const float4 b = *reinterpret_cast<const float4*>(wsrc - D * D + c);
+        wp[c] = b.x; wp[c + 1] = b.y; wp[c + 2] = b.z; wp[c + 3] = b.w;
+      } else {
+        wp[c] = wp[c + 1] = wp[c + 2] = wp[c + 3] = 0.f;
+      }
+    }
+    const float zi = act ? zs[(size_t)i * D + r] : 0.f;
+    // G_{i+1} carried back through step i + 1's write (p(k_{i+1}) still in
+    // pk_s[par ^ 1], written last iteration)
+    if (i + 1 < N) {
+      float gp1 = 0.f;
+#pragma unroll
+      for (int c = 0; c < D; ++c) gp1 = fmaf(grow[c], pk_s[par ^ 1][c], gp1);
+      const float m = bt_next * gp1;
+#pragma unroll
+      for (int c = 0; c < D; ++c) grow[c] = fmaf(-m, pk_s[par ^ 1][c], grow[c]);
+    }
+    if constexpr (NWV > 1) __syncthreads();  // pk_s[par ^ 1] read before rewrite below
+    float pk, sk, pq, sq;
+    norm_phi(xk, pk_s[par], pk, sk);
+    slot ^= 1;
+    norm_phi(xq, pq_s[par], pq, sq);
+    slot ^= 1;
+    if constexpr (NWV > 1) __syncthreads();
+    // n_r, s, fw_r; dn_r, ds
+    float nr = 0.f;
+#pragma unroll
+    for (int c = 0; c < D; ++c) nr = fmaf(wi[c], pq_s[par][c], nr);
+    const float s_i = bsum(act ? zi * pq : 0.f, 1);
+    const float fw = nr / s_i;
+    const float gdot = bsum(act ? xg * fw : 0.f, 2);  // g_i . fw_i
+    acc_gfw += r == 0 ? gdot : 0.f;
+    const float dn = act ? sf * xg / s_i : 0.f;
+    const float ds = -sf * gdot / s_i;
+    // G_i, Zs_i
+#pragma unroll
+    for (int c = 0; c < D; ++c) grow[c] = fmaf(dn, pq_s[par][c], grow[c]);
+    zsr = fmaf(ds, pq, zsr);
+    // e_r, gp_r, dv, dbeta
+    float u = 0.f, gp = 0.f;
+#pragma unroll
+    for (int c = 0; c < D; ++c) {
+      u = fmaf(wp[c], pk_s[par][c], u);
+      gp = fmaf(grow[c], pk_s[par][c], gp);
+    }
+    const float e = act ? xv - u : 0.f;
+    slot ^= 1;
+    const float db = bsum(e * gp, 1);
+    slot ^= 1;
+    // the two column sums through LDS: W_i^T dn and G_i^T e - W_{i-1}^T gp
+    if (act) {
+#pragma unroll
+      for (int c = 0; c < D; ++c) {
+        cb1[r * LD + c] = wi[c] * dn;
+        cb2[r * LD + c] = fmaf(grow[c], e, -wp[c] * gp);
+      }
+    }
+    __syncthreads();
+    float c1 = 0.f, c2 = 0.f;
+    if (act) {
+      for (int rr = 0; rr < D; ++rr) {
+        c1 += cb1[rr * LD + r];
+        c2 += cb2[rr * LD + r];
+      }
+    }
+    __syncthreads();  // the buffers are rewritten next step
+    const float dpq = c1 + ds * zi;
+    const float dpk = bt * c2 + zsr;
+    const float tq = bsum(act ? dpq * pq : 0.f, 2);
+    slot ^= 1;
+    const float tk = bsum(act ? dpk * pk : 0.f, 2);
+    slot ^= 1;
+    if (act) {
+      const float gq = (xq > 0.f ? 1.f : __expf(xq)) * (dpq - tq) / sq;
+      const float gk = (xk > 0.f ? 1.f : __expf(xk)) * (dpk - tk) / sk;
+      st_elem<T>(dq + o, ld_elem<T>(dq + o) + gq);
+      st_elem<T>(dk + o, ld_elem<T>(dk + o) + gk);
+      st_elem<T>(dv + o, ld_elem<T>(dv + o) + bt * gp);
+    }
+    if (r == 0) dbeta[(size_t)bh * N + i] = db;
+    bt_next = bt;
+  }
+  if (r == 0) gfw[bh] = acc_gfw;
+}
+
+// dw_far[h] += c (1 - c) sum_b sum_i g . fw over the slices of head h, in
+// batch order
+__global__ void k_fw_dw(const float* __restrict__ gfw, const float* __restrict__ w_far,
+                        float* __restrict__ dw_far, int B, int H) {
+  const int h = blockIdx.x * blockDim.x + threadIdx.x;
+  if (h >= H) return;
+  float s = 0.f;
+  for (int b = 0; b < B; ++b) s += gfw[(size_t)b * H + h];
+  const float c = sigmoidf_exact(w_far[h]);
+  dw_far[h] += c * (1.f - c) * s;
+}
+
+template <typename T, int D>
+void launch_fw_bwd_d(Launcher& L, const FwBwdArgs& a) {
+  const size_t lds = (size_t)2 * D * (D + 1) * sizeof(float);
+  static std::atomic<unsigned long long> lds_set{0};
+  if (L.note(lds_limit_once((const void*)k_fast_weight_bwd<T, D>, (int)lds, lds_set)) !=
+      hipSuccess)
+    return;
+  L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight_bwd<T, D>, dim3(a.B * a.H), dim3(D > 64 ? D : 64), lds,
+    (hipStream_t)a.stream, (const T*)a.q, (const T*)a.k, (const T*)a.v, a.beta,
+    (const T*)a.dout, (T*)a.dq, (T*)a.dk, (T*)a.dv, a.dbeta, a.wst, a.zst, a.gfw, a.w_far, a.H,
+    a.N);
+  L(FMM_KERNEL_FAST_WEIGHT, k_fw_dw, dim3((a.H + 63) / 64), dim3(64), 0, (hipStream_t)a.stream,
+    (const float*)a.gfw, a.w_far, a.dw_far, a.B, a.H);
+}
+
+template <typename T>
+hipError_t launch_fw_bwd_t(Launcher& L, const FwBwdArgs& a) {
+  switch (a.d) {
+    case 16: launch_fw_bwd_d<T, 16>(L, a); break;
+    case 32: launch_fw_bwd_d<T, 32>(L, a); break;
+    case 64: launch_fw_bwd_d<T, 64>(L, a); break;
+    case 128: launch_fw_bwd_d<T, 128>(L, a); break;
+    default: return L.note(hipErrorInvalidValue);
+  }
+  return L.err;
+}
+
 template <typename T, int D>
 void launch_fw_d(Launcher& L, const FwArgs& a) {
   L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight<T, D>, dim3(a.B * a.H), dim3(D > 64 ? D : 64), 0,
@@ -179,6 +418,10 @@ __global__ void k_fill(float* __restrict__ p, int n, float x) {
 
 hipError_t launch_fast_weight(Launcher& L, const FwArgs& a) {
   return a.dtype == FMM_DTYPE_BF16 ? launch_fw_t<bf16_t>(L, a) : launch_fw_t<float>(L, a);
+}
+
+hipError_t launch_fast_weight_backward(Launcher& L, const FwBwdArgs& a) {
+  return a.dtype == FMM_DTYPE_BF16 ? launch_fw_bwd_t<bf16_t>(L, a) : launch_fw_bwd_t<float>(L, a);
 }
 
 hipError_t launch_fill(Launcher& L, float* p, int n, float x, void* stream) {

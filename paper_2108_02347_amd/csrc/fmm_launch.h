@@ -218,6 +218,29 @@ struct FwArgs {
   void* stream;
 };
 hipError_t launch_fast_weight(Launcher& L, const FwArgs& a);
+// Its backward (fmm_fastweight.hip): adds the fast-weight part's dq, dk, dv to
+// the gradients in place, writes dbeta, and adds its share to dw_far; wst and
+// zst hold W_i and z_i of every step (B*H*N*d*d and B*H*N*d floats), gfw one
+// float per (batch, head).
+struct FwBwdArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const float* beta;
+  const void* dout;
+  void* dq;
+  void* dk;
+  void* dv;
+  float* dbeta;
+  float* dw_far;
+  const float* w_far;
+  float* wst;
+  float* zst;
+  float* gfw;
+  int B, H, N, d, dtype;
+  void* stream;
+};
+hipError_t launch_fast_weight_backward(Launcher& L, const FwBwdArgs& a);
 // n floats at p set to x (on `stream`)
 hipError_t launch_fill(Launcher& L, float* p, int n, float x, void* stream);
 

@@ -72,3 +72,25 @@ def test_autograd_only_where_asked():
     want = binding.backward(tq.detach(), tk, tv, torch.ones_like(out), twn, twf.detach(), kw,
                             rank, 0)
     assert torch.equal(tq.grad, want[0]) and torch.equal(twf.grad, want[4])
+
+
+@pytest.mark.parametrize("n_linear", [0, 1])
+def test_fast_weight_autograd_matches_entry_points(n_linear):
+    B, H, N, d, kw = 2, 2, 200, 16, 20
+    q, k, v, wn, wf = make_inputs(B, H, N, d, "bf16", 1.0, 1660 + n_linear)
+    t = list(upload(q, k, v, wn, wf, "bf16"))
+    beta = torch.from_numpy(np.random.default_rng(1661).uniform(0, 1, (B, H, N))
+                            .astype(np.float32)).to("cuda:0")
+    gen = torch.Generator(device="cuda:0")
+    gen.manual_seed(1662)
+    g = torch.randn(t[0].shape, generator=gen, device="cuda:0").to(t[0].dtype)
+    ins = [t[0], t[1], t[2], beta, t[3], t[4]]
+    leaves = [x.clone().requires_grad_(True) for x in ins]
+    out = binding.fmm_fast_weight_attention(*leaves, kw, n_linear)
+    (out.float() * g.float()).sum().backward()
+    want_out = binding.forward_fastweight(t[0], t[1], t[2], beta, t[3], t[4], kw, n_linear)
+    want = binding.backward_fastweight(t[0], t[1], t[2], beta, g, t[3], t[4], kw, n_linear)
+    torch.cuda.synchronize()
+    assert torch.equal(out.detach(), want_out)
+    for name, leaf, w in zip(("q", "k", "v", "beta", "w_near", "w_far"), leaves, want):
+        assert torch.equal(leaf.grad, w), name
