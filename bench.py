@@ -784,10 +784,15 @@ def main():
           args.steps, 0, torch)
     binding.kernel_timing(False)
     ms_fw, n_fw = binding.kernel_timing_read("fast_weight")
+    # its backward (the operator's backward at rank 1 plus the fast-weight
+    # sweeps), with the forward's output as the upstream gradient
+    tfwb = timed(lambda: binding.backward_fastweight(qf, kf, vf, bf, of, wnf, wff, wl4.band_k,
+                                                     1), args.steps, args.warmup, torch)
     fw_rec = {"shape": "B=16 H=8 N=256 d=16 f32 k=20, fast weight + linear far field, causal",
               "ms_per_call": round(tfw * 1e3, 4),
               "tokens_per_s": round(wl4.B * wl4.N / tfw, 1),
-              "scan_kernel_us": round(ms_fw * 1e3 / n_fw, 3) if n_fw else None}
+              "scan_kernel_us": round(ms_fw * 1e3 / n_fw, 3) if n_fw else None,
+              "backward_ms_per_call": round(tfwb * 1e3, 4)}
     del qf, kf, vf, of, bf
 
     # the other workloads: whole-call throughput, no per-kernel figures
