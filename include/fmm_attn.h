@@ -41,8 +41,9 @@
  * stream) and returns without synchronising.  Faults inside kernels surface
  * at the caller's next synchronisation.
  *
- * Graph capture: the calls enqueue kernels only (no copies, fills or host
- * synchronisation), so they may be captured into a HIP graph.  The entry
+ * Graph capture: the calls (forward and backward) enqueue kernels only (no
+ * copies, fills or host synchronisation), so they may be captured into a HIP
+ * graph.  The entry
  * points with a library-owned workspace allocate it on first use per
  * (device, stream) and grow it when a larger call comes; a stream under
  * capture can do neither, and such a call returns FMM_ERR_UNSUPPORTED with

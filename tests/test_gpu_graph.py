@@ -124,3 +124,39 @@ def test_capture_needing_a_new_workspace_is_rejected():
     g2.replay()
     torch.cuda.synchronize()
     assert torch.equal(out.view(torch.int16), want.view(torch.int16))
+
+
+def test_backward_graph_replays_match_eager():
+    # the backward enqueues kernels only: captured once (after an eager call
+    # that sets up its workspace) and replayed with new inputs, it must give
+    # the eager call's bits
+    B, H, N, d, kw, rank, causal = 2, 2, 1500, 64, 32, 2, 1
+    sets = []
+    for i in range(3):
+        q, k, v, wn, wf = make_inputs(B, H, N, d, "bf16", 1.0 / np.sqrt(d), 1700 + i)
+        t = upload(q, k, v, wn, wf, "bf16")
+        g = upload(make_inputs(B, H, N, d, "bf16", 1.0, 1710 + i)[0], q, q, wn, wf, "bf16")[0]
+        sets.append((t, g))
+    (tq, tk, tv, twn, twf), tg = sets[0]
+    sq, sk, sv, sg = tq.clone(), tk.clone(), tv.clone(), tg.clone()
+    # the library's workspace is per stream: one eager call on the stream that
+    # will capture sets it up
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        binding.backward(sq, sk, sv, sg, twn, twf, kw, rank, causal)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=s):
+        outs = binding.backward(sq, sk, sv, sg, twn, twf, kw, rank, causal)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        (q_, k_, v_, _, _), g_ = sets[rep]
+        sq.copy_(q_), sk.copy_(k_), sv.copy_(v_), sg.copy_(g_)
+        graph.replay()
+        got = [o.clone() for o in outs]
+        want = binding.backward(q_, k_, v_, g_, twn, twf, kw, rank, causal)
+        torch.cuda.synchronize()
+        for name, a, b in zip(("dq", "dk", "dv", "dw_near", "dw_far"), got, want):
+            assert torch.equal(a, b), (rep, name)
+    del graph
