@@ -94,3 +94,44 @@ def test_fast_weight_autograd_matches_entry_points(n_linear):
     assert torch.equal(out.detach(), want_out)
     for name, leaf, w in zip(("q", "k", "v", "beta", "w_near", "w_far"), leaves, want):
         assert torch.equal(leaf.grad, w), name
+
+
+def test_training_steps_through_the_operator():
+    # a small attention layer trained through the operator: projections in
+    # torch, the operator through fmm_attention (bf16, causal, rank 2), SGD
+    # on a fixed synthetic regression target; the loss must fall, and every
+    # gradient that reaches the layer's parameters must be finite
+    torch.manual_seed(1700)
+    B, N, E, H, kw, rank = 2, 512, 64, 2, 32, 2
+    d = E // H
+    dev = "cuda:0"
+    w_qkv = (torch.randn(E, 3 * E, device=dev) / np.sqrt(E)).requires_grad_(True)
+    w_out = (torch.randn(E, E, device=dev) / np.sqrt(E)).requires_grad_(True)
+    w_near = torch.zeros(H, device=dev, requires_grad=True)
+    w_far = torch.zeros(H, device=dev, requires_grad=True)
+    x = torch.randn(B, N, E, device=dev)
+    target = torch.roll(x, 1, dims=1) * 0.5  # a causal target: the previous token
+
+    def layer(x):
+        qkv = (x @ w_qkv).to(torch.bfloat16)
+        q, k, v = (t.reshape(B, N, H, d).permute(0, 2, 1, 3).contiguous()
+                   for t in qkv.split(E, dim=-1))
+        o = binding.fmm_attention(q, k, v, w_near, w_far, kw, rank, True)
+        return o.permute(0, 2, 1, 3).reshape(B, N, E).float() @ w_out
+
+    losses = []
+    params = [w_qkv, w_out, w_near, w_far]
+    for step in range(30):
+        loss = ((layer(x) - target) ** 2).mean()
+        for p in params:
+            p.grad = None
+        loss.backward()
+        for p in params:
+            assert p.grad is not None and torch.isfinite(p.grad).all()
+        with torch.no_grad():
+            for p in params:
+                p -= 0.5 * p.grad
+        losses.append(float(loss.detach()))
+    log(f"training loss {losses[0]:.4f} -> {losses[10]:.4f} -> {losses[-1]:.4f}")
+    assert losses[-1] < losses[10] < losses[0]
+    assert losses[-1] < 0.95 * losses[0]
