@@ -515,6 +515,19 @@ def fmm_attention_backward_stream(q, k, v, w_near, w_far, dout, band_k: int, ran
 
 # ---------------------------------------------------------------- attention layer
 
+def _layer_heads(x, w_qkv, w_out, heads: int):
+    """q, k, v [B, heads, N, d] of the layer's input projection qkv = x W_qkv
+    (within each of q, k, v the heads in order, d columns each)."""
+    x = np.asarray(x, dtype=np.float64)
+    w_qkv = np.asarray(w_qkv, dtype=np.float64)
+    b_, n, e = x.shape
+    if e % heads or w_qkv.shape != (e, 3 * e) or np.shape(w_out) != (e, e):
+        raise ValueError("x [B, N, E], w_qkv [E, 3E], w_out [E, E], E divisible by heads")
+    d = e // heads
+    qkv = (x @ w_qkv).reshape(b_, n, 3, heads, d)
+    return tuple(np.ascontiguousarray(qkv[:, :, p].transpose(0, 2, 1, 3)) for p in range(3))
+
+
 def fmm_layer_forward(x, w_qkv, w_out, heads: int, w_near, w_far, band_k: int, rank: int,
                       causal: bool, norm: str = "map") -> np.ndarray:
     """The attention layer around the operator (Sec. 1.1, Step 1, and the
@@ -524,18 +537,42 @@ def fmm_layer_forward(x, w_qkv, w_out, heads: int, w_near, w_far, band_k: int, r
     [B, heads, N, d]; the heads' outputs are concatenated per token (head
     order) and multiplied by W_out [E, E].  x: [B, N, E]; returns [B, N, E]."""
     x = np.asarray(x, dtype=np.float64)
-    w_qkv = np.asarray(w_qkv, dtype=np.float64)
     w_out = np.asarray(w_out, dtype=np.float64)
     b_, n, e = x.shape
-    if e % heads or w_qkv.shape != (e, 3 * e) or w_out.shape != (e, e):
-        raise ValueError("x [B, N, E], w_qkv [E, 3E], w_out [E, E], E divisible by heads")
-    d = e // heads
-    qkv = (x @ w_qkv).reshape(b_, n, 3, heads, d)
-    q, k, v = (np.ascontiguousarray(qkv[:, :, p].transpose(0, 2, 1, 3)) for p in range(3))
+    q, k, v = _layer_heads(x, w_qkv, w_out, heads)
     o = fmm_attention_stream(q, k, v, w_near, w_far, band_k, rank, causal, norm)
     merged = o.transpose(0, 2, 1, 3).reshape(b_, n, e)
     return merged @ w_out
 
+
+
+def fmm_layer_backward(x, w_qkv, w_out, heads: int, w_near, w_far, dy, band_k: int, rank: int,
+                       causal: bool, norm: str = "map"):
+    """Gradients of sum(dy * y) with y = fmm_layer_forward(...): returns
+    (dx, dw_qkv, dw_out, dw_near, dw_far).  With m the concatenated heads'
+    outputs and qkv = x W_qkv:
+        dm = dy W_out^T,  dW_out = m^T dy   (summed over every token)
+        the operator's backward for the heads' share of dm gives dq, dk, dv
+        dqkv = [dq | dk | dv] per token,  dx = dqkv W_qkv^T,  dW_qkv = x^T dqkv."""
+    x = np.asarray(x, dtype=np.float64)
+    w_qkv = np.asarray(w_qkv, dtype=np.float64)
+    w_out = np.asarray(w_out, dtype=np.float64)
+    dy = np.asarray(dy, dtype=np.float64)
+    b_, n, e = x.shape
+    d = e // heads
+    q, k, v = _layer_heads(x, w_qkv, w_out, heads)
+    o = fmm_attention_stream(q, k, v, w_near, w_far, band_k, rank, causal, norm)
+    m = o.transpose(0, 2, 1, 3).reshape(b_ * n, e)
+    dyf = dy.reshape(b_ * n, e)
+    dw_out = m.T @ dyf
+    do = (dyf @ w_out.T).reshape(b_, n, heads, d).transpose(0, 2, 1, 3)
+    dq, dk, dv, dw_near, dw_far = fmm_attention_backward_stream(q, k, v, w_near, w_far, do,
+                                                                band_k, rank, causal, norm)
+    dqkv = np.stack([g.transpose(0, 2, 1, 3).reshape(b_ * n, e) for g in (dq, dk, dv)], axis=1)
+    dqkv = dqkv.reshape(b_ * n, 3 * e)
+    dx = (dqkv @ w_qkv.T).reshape(b_, n, e)
+    dw_qkv = x.reshape(b_ * n, e).T @ dqkv
+    return dx, dw_qkv, dw_out, dw_near, dw_far
 
 # ---------------------------------------------------------------- fast-weight far field
 

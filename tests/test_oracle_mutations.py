@@ -127,6 +127,12 @@ MUTATIONS = [
     ("fast-weight backward: normalisation derivative without the projection",
      "dk = phi_grad(k, 1) * (dpk - (dpk * pk).sum(axis=-1, keepdims=True)) / sk",
      "dk = phi_grad(k, 1) * dpk / sk"),
+    ("layer backward: W_out gradient transposed",
+     "    dw_out = m.T @ dyf\n",
+     "    dw_out = (m.T @ dyf).T\n"),
+    ("layer backward: x gradient through W_qkv untransposed",
+     "    dx = (dqkv @ w_qkv.T).reshape(b_, n, e)",
+     "    dx = (dqkv[:, :e] @ w_qkv[:, :e]).reshape(b_, n, e)"),
     ("fast-weight operator backward: linear part's gradients dropped",
      "        dq, dk, dv = dq + dql, dk + dkl, dv + dvl",
      "        dq, dk, dv = dq, dk, dv"),

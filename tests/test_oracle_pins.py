@@ -741,3 +741,39 @@ def test_fast_weight_operator_backward_finite_differences(n_linear):
     # got: dq, dk, dv, dbeta, dw_near, dw_far (the inputs' order)
     for gg, w in zip(got, want):
         np.testing.assert_allclose(gg, w, rtol=1e-6, atol=1e-8 * max(1.0, np.abs(w).max()))
+
+
+# ------------------------------------------------------------------ layer backward
+# Pinned by central finite differences of the layer's forward oracle and by
+# torch float64 autograd of the layer written with the dense torch forward.
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_layer_backward_finite_differences(causal):
+    b, n, e, heads, kw, rank = 1, 5, 4, 2, 2, 2
+    x = rnd((b, n, e), 730)
+    wq, wo = rnd((e, 3 * e), 731, 0.5), rnd((e, e), 732, 0.5)
+    wn, wf, dy = rnd(heads, 733), rnd(heads, 734), rnd((b, n, e), 735)
+    got = ref.fmm_layer_backward(x, wq, wo, heads, wn, wf, dy, kw, rank, causal)
+    loss = lambda x_, wq_, wo_, wn_, wf_: float(
+        (ref.fmm_layer_forward(x_, wq_, wo_, heads, wn_, wf_, kw, rank, causal) * dy).sum())
+    want = _fd(loss, [x, wq, wo, wn, wf])
+    for g, w in zip(got, want):
+        np.testing.assert_allclose(g, w, rtol=1e-6, atol=1e-8 * max(1.0, np.abs(w).max()))
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_layer_backward_matches_torch_autograd(causal):
+    b, n, e, heads, kw, rank = 2, 9, 6, 2, 2, 2
+    d = e // heads
+    x = rnd((b, n, e), 740)
+    wq, wo = rnd((e, 3 * e), 741, 0.5), rnd((e, e), 742, 0.5)
+    wn, wf, dy = rnd(heads, 743), rnd(heads, 744), rnd((b, n, e), 745)
+    ts = [torch.tensor(a, requires_grad=True) for a in (x, wq, wo, wn, wf)]
+    qkv = (ts[0] @ ts[1]).reshape(b, n, 3, heads, d)
+    q, k, v = (qkv[:, :, p].permute(0, 2, 1, 3) for p in range(3))
+    o = _torch_dense_forward(q, k, v, ts[3], ts[4], kw, rank, causal, "map")
+    y = o.permute(0, 2, 1, 3).reshape(b, n, e) @ ts[2]
+    (y * torch.tensor(dy)).sum().backward()
+    got = ref.fmm_layer_backward(x, wq, wo, heads, wn, wf, dy, kw, rank, causal)
+    for g, t in zip(got, ts):
+        np.testing.assert_allclose(g, t.grad.numpy(), rtol=1e-9, atol=1e-12)
