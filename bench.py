@@ -762,10 +762,15 @@ def main():
     yl = torch.empty_like(xl)
     tl = timed(lambda: binding.layer_forward(xl, wl, wo, H4, wn4, wf4, w4.band_k, w4.rank, 0,
                                              out=yl), args.steps, args.warmup, torch)
+    # its backward (the forward recomputed, rocBLAS projections, the
+    # operator's backward), with the forward's output as dy
+    tlb = timed(lambda: binding.layer_backward(xl, wl, wo, yl, H4, wn4, wf4, w4.band_k, w4.rank,
+                                               0), args.steps, args.warmup, torch)
     layer_rec = {"shape": "B=8 N=4096 E=64 H=2 (d=32) bf16 k=20 rank=2 non-causal",
                  "ms_per_call": round(tl * 1e3, 4),
                  "tokens_per_s": round(w4.B * w4.N / tl, 1),
-                 "operator_ms_per_call": round(t4 * 1e3, 4)}
+                 "operator_ms_per_call": round(t4 * 1e3, 4),
+                 "backward_ms_per_call": round(tlb * 1e3, 4)}
     del xl, wl, wo, yl
 
     # the fast-weight far field (Appendix D) at the language-model shape,

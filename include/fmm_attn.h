@@ -273,6 +273,26 @@ int fmm_attn_layer_forward(const void* x, const void* w_qkv, const void* w_out, 
                            const float* w_near, const float* w_far, int dtype, void* stream);
 
 /*
+ * fmm_attn_layer_backward - gradients of sum(dy * y) for the output y of
+ * fmm_attn_layer_forward with the same arguments:
+ *   dm = dy W_out^T,  dW_out = m^T dy  (m: the heads' outputs side by side)
+ *   the operator's backward (fmm_attn_backward) for the heads' share of dm
+ *   dqkv = [dq | dk | dv] per token,  dx = dqkv W_qkv^T,  dW_qkv = x^T dqkv
+ *   dy      : [B, N, E] of dtype, read only.
+ *   dx      : [B, N, E]; dw_qkv [E, 3E]; dw_out [E, E] (of dtype, written
+ *             completely; the weight gradients summed over every token);
+ *             dw_near, dw_far: device float[H].  No output may overlap an
+ *             input or another output.
+ * The forward is recomputed (rocBLAS projections, the operator); the
+ * intermediates live in the library-owned workspace (13 token-by-E arrays
+ * beside the operator's records).  Errors as fmm_attn_layer_forward.
+ */
+int fmm_attn_layer_backward(const void* x, const void* w_qkv, const void* w_out, const void* dy,
+                            void* dx, void* dw_qkv, void* dw_out, float* dw_near, float* dw_far,
+                            int B, int N, int E, int H, int band_k, int rank, int causal,
+                            const float* w_near, const float* w_far, int dtype, void* stream);
+
+/*
  * fmm_attn_forward_fastweight - FMMformer with the fast-weight far field of
  * Appendix D (causal only): the linear transformer with the delta-rule fast
  * weight update of the work the appendix cites.  Per (b, h) and row i, with

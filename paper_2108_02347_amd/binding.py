@@ -37,6 +37,7 @@ EXPORTS = (
     "fmm_attn_version", "fmm_attn_kernel_timing", "fmm_attn_kernel_timing_read",
     "fmm_attn_forward_noalloc", "fmm_attn_noalloc_max_bytes", "fmm_attn_forward_ex",
     "fmm_attn_backward", "fmm_attn_backward_ex", "fmm_attn_layer_forward",
+    "fmm_attn_layer_backward",
     "fmm_attn_forward_fastweight", "fmm_attn_backward_fastweight",
     "fmm_attn_set_one_launch",
 )
@@ -74,6 +75,8 @@ def lib() -> ctypes.CDLL:
     h.fmm_attn_backward_fastweight.restype = ci
     h.fmm_attn_layer_forward.argtypes = [vp] * 4 + [ci] * 7 + [cf, cf, ci, vp]
     h.fmm_attn_layer_forward.restype = ci
+    h.fmm_attn_layer_backward.argtypes = [vp] * 9 + [ci] * 7 + [cf, cf, ci, vp]
+    h.fmm_attn_layer_backward.restype = ci
     h.fmm_attn_backward.argtypes = [vp] * 9 + [ci] * 7 + [cf, cf, ci, vp]
     h.fmm_attn_backward.restype = ci
     h.fmm_attn_backward_ex.argtypes = [vp] * 9 + [ci] * 7 + [cf, cf, ci, ci, vp]
@@ -333,6 +336,34 @@ def layer_forward(x, w_qkv, w_out, heads: int, w_near, w_far, band_k: int, rank:
         _ptr(x), _ptr(w_qkv), _ptr(w_out), _ptr(out), B, N, E, int(heads), int(band_k),
         int(rank), int(bool(causal)), _ptr(w_near), _ptr(w_far), dt, _stream_of(x)))
     return out
+
+
+def layer_backward(x, w_qkv, w_out, dy, heads: int, w_near, w_far, band_k: int, rank: int,
+                   causal: bool):
+    """Gradients of the layer (layer_forward) for dy = dL/dy: returns (dx,
+    dw_qkv, dw_out, dw_near, dw_far)."""
+    if x.dim() != 3 or x.device.type != "cuda" or x.dtype not in _DTYPES:
+        raise ValueError("x must be a [B, N, E] float32 or bfloat16 CUDA/HIP tensor")
+    B, N, E = x.shape
+    for name, t, shp in (("w_qkv", w_qkv, (E, 3 * E)), ("w_out", w_out, (E, E)),
+                         ("dy", dy, (B, N, E))):
+        if (not isinstance(t, torch.Tensor) or t.dtype != x.dtype or t.device != x.device
+                or tuple(t.shape) != shp or not t.is_contiguous()):
+            raise ValueError(f"{name} must be a contiguous {shp} tensor of x's dtype on x's device")
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous")
+    for name, w in (("w_near", w_near), ("w_far", w_far)):
+        if (w.dtype != torch.float32 or w.device != x.device or w.numel() != heads
+                or not w.is_contiguous()):
+            raise ValueError(f"{name} must be a contiguous float32 device tensor of H values")
+    dx, dwq, dwo = torch.empty_like(x), torch.empty_like(w_qkv), torch.empty_like(w_out)
+    dwn, dwf = torch.empty_like(w_near), torch.empty_like(w_far)
+    dt = FMM_DTYPE_BF16 if x.dtype == torch.bfloat16 else FMM_DTYPE_F32
+    _check(lib().fmm_attn_layer_backward(
+        _ptr(x), _ptr(w_qkv), _ptr(w_out), _ptr(dy), _ptr(dx), _ptr(dwq), _ptr(dwo), _ptr(dwn),
+        _ptr(dwf), B, N, E, int(heads), int(band_k), int(rank), int(bool(causal)),
+        _ptr(w_near), _ptr(w_far), dt, _stream_of(x)))
+    return dx, dwq, dwo, dwn, dwf
 
 
 def forward_fastweight(q, k, v, beta, w_near, w_far, band_k: int, n_linear: int, out=None):

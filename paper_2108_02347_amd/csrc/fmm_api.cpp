@@ -594,6 +594,182 @@ int run_layer(const void* x, const void* w_qkv, const void* w_out, void* y, int 
   return FMM_OK;
 }
 
+// Backward of the layer: the forward recomputed through rocBLAS and the
+// operator (qkv, the heads q, k, v, their outputs o and the merged rows m),
+// then dm = dy W_out^T, dW_out = m^T dy, the operator's backward for the
+// heads' share of dm, dqkv = [dq | dk | dv] per token, dx = dqkv W_qkv^T and
+// dW_qkv = x^T dqkv.
+int run_layer_backward(const void* x, const void* w_qkv, const void* w_out, const void* dy,
+                       void* dx, void* dw_qkv, void* dw_out, float* dw_near, float* dw_far,
+                       int B, int N, int E, int H, int band_k, int rank, int causal,
+                       const float* w_near, const float* w_far, int dtype, void* stream) {
+  if (!x || !w_qkv || !w_out || !dy || !dx || !dw_qkv || !dw_out || !dw_near || !dw_far ||
+      !w_near || !w_far)
+    return FMM_ERR_INVALID_ARG;
+  if (B < 1 || N < 1 || E < 1 || H < 1 || band_k < 0 || E % H) return FMM_ERR_INVALID_ARG;
+  if (causal != 0 && causal != 1) return FMM_ERR_INVALID_ARG;
+  if (dtype != FMM_DTYPE_F32 && dtype != FMM_DTYPE_BF16) return FMM_ERR_UNSUPPORTED;
+  const int d = E / H;
+  if (!supported(d, rank)) return FMM_ERR_UNSUPPORTED;
+  const size_t es = dtype == FMM_DTYPE_BF16 ? 2 : 4;
+  typedef unsigned __int128 u128;
+  const u128 tokens = (u128)B * N;
+  if (tokens > (u128)INT32_MAX || (u128)3 * E > (u128)INT32_MAX) return FMM_ERR_UNSUPPORTED;
+  const u128 xbytes = tokens * E * es;
+  if (xbytes * 16 > (u128)INT64_MAX) return FMM_ERR_INVALID_ARG;
+  for (const void* p : {x, w_qkv, w_out, dy, (const void*)dx, (const void*)dw_qkv,
+                        (const void*)dw_out})
+    if ((uintptr_t)p % 16) return FMM_ERR_INVALID_ARG;
+  if ((uintptr_t)w_near % 4 || (uintptr_t)w_far % 4 || (uintptr_t)dw_near % 4 ||
+      (uintptr_t)dw_far % 4)
+    return FMM_ERR_INVALID_ARG;
+  const size_t xb = (size_t)xbytes, wq = (size_t)E * 3 * E * es, wo = (size_t)E * E * es;
+  // outputs overlap neither the inputs nor one another
+  const void* ins[4] = {x, w_qkv, w_out, dy};
+  const size_t in_b[4] = {xb, wq, wo, xb};
+  void* outs[3] = {dx, dw_qkv, dw_out};
+  const size_t out_b[3] = {xb, wq, wo};
+  for (int o = 0; o < 3; ++o) {
+    for (int i = 0; i < 4; ++i)
+      if (overlaps2(outs[o], out_b[o], ins[i], in_b[i])) return FMM_ERR_INVALID_ARG;
+    for (int o2 = o + 1; o2 < 3; ++o2)
+      if (overlaps2(outs[o], out_b[o], outs[o2], out_b[o2])) return FMM_ERR_INVALID_ARG;
+  }
+  if (overlaps(dw_near, dw_far, (size_t)H * 4)) return FMM_ERR_INVALID_ARG;
+  // workspace: qkv (later dqkv), q, k, v, o, m, dm, do, dq, dk, dv, then the
+  // forward operator's and the backward's records
+  const Plan p = plan_for(B, H, N, d, band_k, rank, causal, dtype);
+  const BwdPlan bp = bwd_plan(B, H, N, d, rank, dtype);
+  if (p.ws_bytes == 0 || bp.total == 0) return FMM_ERR_UNSUPPORTED;
+  const size_t seg = align256(xb);
+  const size_t off_qkv = 0, off_q = 3 * seg, off_k = 4 * seg, off_v = 5 * seg, off_o = 6 * seg,
+               off_m = 7 * seg, off_dm = 8 * seg, off_do = 9 * seg, off_dq = 10 * seg,
+               off_dk = 11 * seg, off_dv = 12 * seg, off_fws = 13 * seg,
+               off_bws = off_fws + align256(p.ws_bytes);
+  const size_t total = off_bws + bp.total;
+  auto at = [](void* base, size_t off) {
+    return reinterpret_cast<void*>(reinterpret_cast<uintptr_t>(base) + off);
+  };
+  fmm::LaunchArgs a = make_args(at(nullptr, off_q), at(nullptr, off_k), at(nullptr, off_v),
+                                at(nullptr, off_o), B, H, N, d, band_k, rank, causal, w_near,
+                                w_far, dtype, FMM_FAR_NORM_PER_MAP, nullptr, p, stream);
+  int st = check_launch(a);
+  if (st != FMM_OK) return st;
+  fmm::LaunchArgs fa = make_args(at(nullptr, off_q), at(nullptr, off_k), at(nullptr, off_v),
+                                 at(nullptr, off_dq), B, H, N, d, band_k, rank, causal, w_near,
+                                 w_far, dtype, FMM_FAR_NORM_PER_MAP, nullptr, bp.p, stream);
+  fmm::BwdArgs ba;
+  ba.q = at(nullptr, off_q);
+  ba.k = at(nullptr, off_k);
+  ba.v = at(nullptr, off_v);
+  ba.dout = at(nullptr, off_do);
+  ba.dq = at(nullptr, off_dq);
+  ba.dk = at(nullptr, off_dk);
+  ba.dv = at(nullptr, off_dv);
+  ba.dw_near = dw_near;
+  ba.dw_far = dw_far;
+  ba.w_near = w_near;
+  ba.w_far = w_far;
+  ba.B = B;
+  ba.H = H;
+  ba.N = N;
+  ba.d = d;
+  ba.band_k = fa.band_k;
+  ba.rank = rank;
+  ba.causal = causal;
+  ba.dtype = dtype;
+  ba.stream = stream;
+  ba.nseg = bp.p.nseg;
+  ba.L = bp.p.L;
+  fill_bwd_args(ba, bp, nullptr, B, H);
+  hipStream_t s = (hipStream_t)stream;
+  {
+    EventTimer& t = timer();
+    std::lock_guard<std::mutex> g(t.mu);
+    fmm::Launcher dry;
+    dry.timer = &t;
+    dry.dry = true;
+    (void)fmm::launch_layer_copy(dry, true, dtype, nullptr, nullptr, nullptr, nullptr, B, N, H, d,
+                                 s);
+    (void)fmm::launch_layer_copy(dry, false, dtype, nullptr, nullptr, nullptr, nullptr, B, N, H,
+                                 d, s);
+    (void)fmm::launch_layer_split1(dry, dtype, nullptr, nullptr, B, N, H, d, s);
+    (void)fmm::launch_layer_merge_part(dry, dtype, nullptr, nullptr, 0, B, N, H, d, s);
+    if (dry.err == hipSuccess) (void)fmm::launch_state_only(fa, dry);
+    if (dry.err == hipSuccess) (void)fmm::launch_backward_tail(ba, dry);
+    if (dry.err != hipSuccess)
+      return dry.err == hipErrorInvalidConfiguration ? FMM_ERR_UNSUPPORTED : FMM_ERR_HIP;
+  }
+  std::lock_guard<std::mutex> bl(blas_mutex());
+  void* hdl = blas_handle();
+  if (!hdl) return FMM_ERR_HIP;
+  std::lock_guard<std::mutex> wl(ws_mutex());
+  void* ws = nullptr;
+  st = acquire_ws_locked(stream, total, &ws);
+  if (st != FMM_OK) return st;
+  a.q = ba.q = at(ws, off_q);
+  a.k = ba.k = at(ws, off_k);
+  a.v = ba.v = at(ws, off_v);
+  a.out = at(ws, off_o);
+  a.ws = (float*)at(ws, off_fws);
+  fa.q = a.q;
+  fa.k = a.k;
+  fa.v = a.v;
+  fa.ws = (float*)at(ws, off_bws);
+  ba.dout = at(ws, off_do);
+  ba.dq = at(ws, off_dq);
+  ba.dk = at(ws, off_dk);
+  ba.dv = at(ws, off_dv);
+  fill_bwd_args(ba, bp, at(ws, off_bws), B, H);
+  const int M = B * N;
+  EventTimer& t = timer();
+  // the forward: qkv, the heads, the operator, the merged rows
+  if (fmm::layer_gemm(hdl, stream, dtype, x, w_qkv, at(ws, off_qkv), M, E, 3 * E) != hipSuccess)
+    return FMM_ERR_HIP;
+  {
+    std::lock_guard<std::mutex> g(t.mu);
+    fmm::Launcher L;
+    L.timer = &t;
+    if (fmm::launch_layer_copy(L, true, dtype, at(ws, off_qkv), at(ws, off_q), at(ws, off_k),
+                               at(ws, off_v), B, N, H, d, s) !=
+            hipSuccess ||
+        fmm::launch_forward(a, L) != hipSuccess ||
+        fmm::launch_layer_copy(L, false, dtype, a.out, at(ws, off_m), nullptr, nullptr, B, N, H,
+                               d, s) != hipSuccess)
+      return FMM_ERR_HIP;
+  }
+  // dm = dy W_out^T, dW_out = m^T dy
+  if (fmm::layer_gemm(hdl, stream, dtype, dy, w_out, at(ws, off_dm), M, E, E, false, true) !=
+          hipSuccess ||
+      fmm::layer_gemm(hdl, stream, dtype, at(ws, off_m), dy, dw_out, E, M, E, true, false) !=
+          hipSuccess)
+    return FMM_ERR_HIP;
+  // the operator's backward on the heads' share of dm, then dqkv per token
+  {
+    std::lock_guard<std::mutex> g(t.mu);
+    fmm::Launcher L;
+    L.timer = &t;
+    if (fmm::launch_layer_split1(L, dtype, at(ws, off_dm), at(ws, off_do), B, N, H, d, s) !=
+            hipSuccess ||
+        fmm::launch_state_only(fa, L) != hipSuccess ||
+        fmm::launch_backward_tail(ba, L) != hipSuccess ||
+        fmm::launch_layer_merge_part(L, dtype, ba.dq, at(ws, off_qkv), 0, B, N, H, d, s) !=
+            hipSuccess ||
+        fmm::launch_layer_merge_part(L, dtype, ba.dk, at(ws, off_qkv), 1, B, N, H, d, s) !=
+            hipSuccess ||
+        fmm::launch_layer_merge_part(L, dtype, ba.dv, at(ws, off_qkv), 2, B, N, H, d, s) !=
+            hipSuccess)
+      return FMM_ERR_HIP;
+  }
+  // dx = dqkv W_qkv^T, dW_qkv = x^T dqkv
+  if (fmm::layer_gemm(hdl, stream, dtype, at(ws, off_qkv), w_qkv, dx, M, 3 * E, E, false,
+                      true) != hipSuccess ||
+      fmm::layer_gemm(hdl, stream, dtype, x, at(ws, off_qkv), dw_qkv, E, M, 3 * E, true,
+                      false) != hipSuccess)
+    return FMM_ERR_HIP;
+  return FMM_OK;
+}
+
 // ------------------------------------------------------------------ fast weight
 int run_fastweight(const void* q, const void* k, const void* v, const float* beta, void* out,
                    int B, int H, int N, int d, int band_k, int n_linear, const float* w_near,
@@ -840,6 +1016,14 @@ int fmm_attn_backward_ex(const void* q, const void* k, const void* v, const void
                          void* stream) {
   return run_backward(q, k, v, dout, dq, dk, dv, dw_near, dw_far, B, H, N, d, band_k, rank,
                       causal, w_near, w_far, dtype, far_norm, stream);
+}
+
+int fmm_attn_layer_backward(const void* x, const void* w_qkv, const void* w_out, const void* dy,
+                            void* dx, void* dw_qkv, void* dw_out, float* dw_near, float* dw_far,
+                            int B, int N, int E, int H, int band_k, int rank, int causal,
+                            const float* w_near, const float* w_far, int dtype, void* stream) {
+  return run_layer_backward(x, w_qkv, w_out, dy, dx, dw_qkv, dw_out, dw_near, dw_far, B, N, E, H,
+                            band_k, rank, causal, w_near, w_far, dtype, stream);
 }
 
 int fmm_attn_backward_fastweight(const void* q, const void* k, const void* v, const float* beta,

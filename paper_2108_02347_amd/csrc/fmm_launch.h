@@ -202,9 +202,16 @@ hipError_t launch_layer_copy(Launcher& L, bool split, int dtype, const void* src
 bool layer_proj_applies(int dtype, int E);
 hipError_t launch_layer_proj(Launcher& L, bool qkv, const void* in, const void* w, void* o0,
                              void* o1, void* o2, int B, int N, int H, int d, hipStream_t s);
+// ta (tb): A (B) stored transposed ([K, M] and [Nc, K] row-major).
 hipError_t layer_gemm(void* handle, void* stream, int dtype, const void* A, const void* Bm,
-                      void* C, int M, int K, int Nc);
+                      void* C, int M, int K, int Nc, bool ta = false, bool tb = false);
 void* layer_blas_handle_create();
+// The layer's backward copies: [B N, E] rows -> [B, H, N, d] (split1), and
+// [B, H, N, d] -> part `part` (E columns from part * E) of [B N, 3E] rows.
+hipError_t launch_layer_split1(Launcher& L, int dtype, const void* src, void* dst, int B, int N,
+                               int H, int d, hipStream_t s);
+hipError_t launch_layer_merge_part(Launcher& L, int dtype, const void* src, void* dst, int part,
+                                   int B, int N, int H, int d, hipStream_t s);
 
 // Fast-weight far field (fmm_fastweight.hip): adds sigmoid(w_far) fw to out.
 struct FwArgs {

@@ -27,28 +27,31 @@ namespace {
 // part E = H*d wide with the heads in order; chunk c of the row covers
 // columns 8c .. 8c+7 (bf16) or 4c .. 4c+3 (fp32), which never straddle a head
 // since d is a multiple of 16.
+// (parts = 1: rows of one E-wide part, into q only)
 template <typename T>
 __global__ __launch_bounds__(256) void k_split_heads(const T* __restrict__ qkv,
                                                      T* __restrict__ q, T* __restrict__ k,
                                                      T* __restrict__ v, long long nchunk, int N,
-                                                     int H, int d) {
+                                                     int H, int d, int parts) {
   constexpr int EPC = 16 / (int)sizeof(T);
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i >= nchunk) return;
-  const int E = H * d, cpr = 3 * E / EPC;
+  const int E = H * d, cpr = parts * E / EPC;
   const long long t = i / cpr;
   const int col = (int)(i - t * cpr) * EPC;
   const int part = col / E, h = (col % E) / d, c = col % d;
   const long long b = t / N, n = t - b * N;
   T* dst = part == 0 ? q : (part == 1 ? k : v);
-  const uint4 val = *reinterpret_cast<const uint4*>(qkv + t * 3 * E + col);
+  const uint4 val = *reinterpret_cast<const uint4*>(qkv + t * parts * E + col);
   *reinterpret_cast<uint4*>(dst + (((b * H + h) * N + n) * d + c)) = val;
 }
 
-// o [B, H, N, d] -> m [B*N, E] (the heads of a token side by side).
+// o [B, H, N, d] -> m [B*N, E] (the heads of a token side by side), in rows
+// of row_len elements from column col0 (E and 0 for the layer's forward).
 template <typename T>
 __global__ __launch_bounds__(256) void k_merge_heads(const T* __restrict__ o, T* __restrict__ m,
-                                                     long long nchunk, int N, int H, int d) {
+                                                     long long nchunk, int N, int H, int d,
+                                                     int row_len, int col0) {
   constexpr int EPC = 16 / (int)sizeof(T);
   const long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i >= nchunk) return;
@@ -58,27 +61,27 @@ __global__ __launch_bounds__(256) void k_merge_heads(const T* __restrict__ o, T*
   const int h = col / d, c = col % d;
   const long long b = t / N, n = t - b * N;
   const uint4 val = *reinterpret_cast<const uint4*>(o + (((b * H + h) * N + n) * d + c));
-  *reinterpret_cast<uint4*>(m + t * E + col) = val;
+  *reinterpret_cast<uint4*>(m + t * row_len + col0 + col) = val;
 }
 
 template <typename T>
 void launch_split(Launcher& L, const void* qkv, void* q, void* k, void* v, int B, int N, int H,
-                  int d, hipStream_t s) {
+                  int d, hipStream_t s, int parts = 3) {
   constexpr int EPC = 16 / (int)sizeof(T);
-  const long long nchunk = (long long)B * N * 3 * H * d / EPC;
+  const long long nchunk = (long long)B * N * parts * H * d / EPC;
   const long long nb = (nchunk + 255) / 256;
   L(FMM_KERNEL_LAYER_COPY, k_split_heads<T>, dim3((unsigned)std::min<long long>(nb, 0xFFFFFFFFll)),
-    dim3(256), 0, s, (const T*)qkv, (T*)q, (T*)k, (T*)v, nchunk, N, H, d);
+    dim3(256), 0, s, (const T*)qkv, (T*)q, (T*)k, (T*)v, nchunk, N, H, d, parts);
 }
 
 template <typename T>
 void launch_merge(Launcher& L, const void* o, void* m, int B, int N, int H, int d,
-                  hipStream_t s) {
+                  hipStream_t s, int row_len = 0, int col0 = 0) {
   constexpr int EPC = 16 / (int)sizeof(T);
   const long long nchunk = (long long)B * N * H * d / EPC;
   const long long nb = (nchunk + 255) / 256;
   L(FMM_KERNEL_LAYER_COPY, k_merge_heads<T>, dim3((unsigned)std::min<long long>(nb, 0xFFFFFFFFll)),
-    dim3(256), 0, s, (const T*)o, (T*)m, nchunk, N, H, d);
+    dim3(256), 0, s, (const T*)o, (T*)m, nchunk, N, H, d, row_len > 0 ? row_len : H * d, col0);
 }
 
 // ------------------------------------------------------------------ k_proj
@@ -170,14 +173,18 @@ void launch_proj_e(Launcher& L, bool qkv, const void* in, const void* w, void* o
 
 // Row-major C [M, Nc] = A [M, K] B [K, Nc] as the column-major product
 // C^T = B^T A^T.
+// With ta (tb): A (B) is stored transposed, i.e. A is [K, M] (B is [Nc, K])
+// row-major and the product uses its transpose.
 hipError_t gemm_rm(rocblas_handle hdl, int dtype, const void* A, const void* Bm, void* C, int M,
-                   int K, int Nc) {
+                   int K, int Nc, bool ta = false, bool tb = false) {
   const rocblas_datatype t =
       dtype == FMM_DTYPE_BF16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
   const float one = 1.f, zero = 0.f;
   const rocblas_status st = rocblas_gemm_ex(
-      hdl, rocblas_operation_none, rocblas_operation_none, Nc, M, K, &one, Bm, t, Nc, A, t, K,
-      &zero, C, t, Nc, C, t, Nc, rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+      hdl, tb ? rocblas_operation_transpose : rocblas_operation_none,
+      ta ? rocblas_operation_transpose : rocblas_operation_none, Nc, M, K, &one, Bm, t,
+      tb ? K : Nc, A, t, ta ? M : K, &zero, C, t, Nc, C, t, Nc, rocblas_datatype_f32_r,
+      rocblas_gemm_algo_standard, 0, 0);
   return st == rocblas_status_success ? hipSuccess : hipErrorLaunchFailure;
 }
 
@@ -212,11 +219,29 @@ hipError_t launch_layer_proj(Launcher& L, bool qkv, const void* in, const void* 
 }
 
 hipError_t layer_gemm(void* handle, void* stream, int dtype, const void* A, const void* Bm,
-                      void* C, int M, int K, int Nc) {
+                      void* C, int M, int K, int Nc, bool ta, bool tb) {
   rocblas_handle hdl = (rocblas_handle)handle;
   if (rocblas_set_stream(hdl, (hipStream_t)stream) != rocblas_status_success)
     return hipErrorLaunchFailure;
-  return gemm_rm(hdl, dtype, A, Bm, C, M, K, Nc);
+  return gemm_rm(hdl, dtype, A, Bm, C, M, K, Nc, ta, tb);
+}
+
+hipError_t launch_layer_split1(Launcher& L, int dtype, const void* src, void* dst, int B, int N,
+                               int H, int d, hipStream_t s) {
+  if (dtype == FMM_DTYPE_BF16)
+    launch_split<bf16_t>(L, src, dst, nullptr, nullptr, B, N, H, d, s, 1);
+  else
+    launch_split<float>(L, src, dst, nullptr, nullptr, B, N, H, d, s, 1);
+  return L.err;
+}
+
+hipError_t launch_layer_merge_part(Launcher& L, int dtype, const void* src, void* dst, int part,
+                                   int B, int N, int H, int d, hipStream_t s) {
+  if (dtype == FMM_DTYPE_BF16)
+    launch_merge<bf16_t>(L, src, dst, B, N, H, d, s, 3 * H * d, part * H * d);
+  else
+    launch_merge<float>(L, src, dst, B, N, H, d, s, 3 * H * d, part * H * d);
+  return L.err;
 }
 
 void* layer_blas_handle_create() {

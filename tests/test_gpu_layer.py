@@ -77,3 +77,56 @@ def test_layer_projection_widths(E, H):
     # E = 128 as one head of 128 and as four of 32); 600 tokens leave a
     # partial last block of 64
     check_layer(2, 300, E, H, 9, 2, int(E == 96), "bf16", 3100 + E + H)
+
+
+# ------------------------------------------------------------------ backward
+
+def check_layer_backward(B, N, E, H, kw, rank, causal, dtype, seed):
+    rng = np.random.default_rng(seed)
+    x = to_dtype(rng.standard_normal((B, N, E)), dtype)
+    wqkv = to_dtype(rng.standard_normal((E, 3 * E)) / np.sqrt(E), dtype)
+    wo = to_dtype(rng.standard_normal((E, E)) / np.sqrt(E), dtype)
+    dy = to_dtype(rng.standard_normal((B, N, E)), dtype)
+    wn, wf = rng.standard_normal(H), rng.standard_normal(H)
+    log(f"layer backward B={B} N={N} E={E} H={H} k={kw} r={rank} causal={causal} {dtype}")
+    dev = "cuda:0"
+    tx, tw, to, tdy = (torch.from_numpy(np.asarray(a, dtype=np.float32)).to(dev).to(TD[dtype])
+                       .contiguous() for a in (x, wqkv, wo, dy))
+    twn, twf = (torch.from_numpy(np.asarray(a, dtype=np.float32)).to(dev) for a in (wn, wf))
+    got = binding.layer_backward(tx, tw, to, tdy, H, twn, twf, kw, rank, causal)
+    torch.cuda.synchronize()
+    got = [g.float().cpu().numpy().astype(np.float64) for g in got]
+    want = ref.fmm_layer_backward(x, wqkv, wo, H, wn, wf, dy, kw, rank, bool(causal))
+    errs = {}
+    for name, a, b in zip(("dx", "dw_qkv", "dw_out"), got[:3], want[:3]):
+        assert np.isfinite(a).all(), name
+        errs[name] = np.abs(a - b).max() / np.abs(b).max()
+    # the logits' gradients against the sums of absolute terms that form them
+    # (rounding of the intermediates in the storage type enters them directly)
+    qkv = (np.asarray(x) @ wqkv).reshape(B, N, 3, H, E // H)
+    q, k, v = (np.ascontiguousarray(qkv[:, :, p].transpose(0, 2, 1, 3)) for p in range(3))
+    do = (dy.reshape(B * N, E) @ wo.T).reshape(B, N, H, E // H).transpose(0, 2, 1, 3)
+    near = ref.near_stream(q, k, v, kw, bool(causal))
+    far = ref.far_stream(q, k, v, rank, bool(causal))
+    a_, c_ = ref.sigmoid(wn), ref.sigmoid(wf)
+    sn = a_ * (1 - a_) * np.einsum("bhic,bhic->h", np.abs(do), np.abs(near))
+    sf = c_ * (1 - c_) * np.einsum("bhic,bhic->h", np.abs(do), np.abs(far))
+    errs["dw_near"] = (np.abs(got[3] - want[3]) / np.maximum(sn, 1e-30)).max()
+    errs["dw_far"] = (np.abs(got[4] - want[4]) / np.maximum(sf, 1e-30)).max()
+    log("  " + " ".join(f"{kk} {vv:.2e}" for kk, vv in errs.items()))
+    for kk, vv in errs.items():
+        assert vv <= TOL[dtype], (kk, vv)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("causal", [0, 1])
+def test_layer_backward_lra_shape(causal, dtype):
+    # the long-range model's layer (2 heads, 64-wide embedding), fewer tokens
+    check_layer_backward(2, 1024, 64, 2, 20, 2, causal, dtype, 5100 + causal)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_layer_backward_widths(dtype):
+    check_layer_backward(1, 300, 96, 3, 7, 1, 1, dtype, 5200)
+    check_layer_backward(2, 200, 128, 1, 30, 2, 0, dtype, 5300)
+    check_layer_backward(1, 257, 256, 2, 16, 2, 1, dtype, 5400)
