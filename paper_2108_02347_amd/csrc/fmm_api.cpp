@@ -645,8 +645,10 @@ int run_layer_backward(const void* x, const void* w_qkv, const void* w_out, cons
   const size_t off_qkv = 0, off_q = 3 * seg, off_k = 4 * seg, off_v = 5 * seg, off_o = 6 * seg,
                off_m = 7 * seg, off_dm = 8 * seg, off_do = 9 * seg, off_dq = 10 * seg,
                off_dk = 11 * seg, off_dv = 12 * seg, off_fws = 13 * seg,
-               off_bws = off_fws + align256(p.ws_bytes);
-  const size_t total = off_bws + bp.total;
+               off_bws = off_fws + align256(p.ws_bytes),
+               off_wg = off_bws + align256(bp.total);
+  const int Mtok = B * N;  // fits: checked above
+  const size_t total = off_wg + align256(fmm::layer_wgrad_scratch_bytes(Mtok, E, 3 * E));
   auto at = [](void* base, size_t off) {
     return reinterpret_cast<void*>(reinterpret_cast<uintptr_t>(base) + off);
   };
@@ -697,6 +699,9 @@ int run_layer_backward(const void* x, const void* w_qkv, const void* w_out, cons
     (void)fmm::launch_layer_merge_part(dry, dtype, nullptr, nullptr, 0, B, N, H, d, s);
     if (dry.err == hipSuccess) (void)fmm::launch_state_only(fa, dry);
     if (dry.err == hipSuccess) (void)fmm::launch_backward_tail(ba, dry);
+    if (dry.err == hipSuccess)
+      (void)fmm::layer_wgrad(nullptr, dry, stream, dtype, nullptr, nullptr, nullptr, Mtok, E,
+                             3 * E, nullptr);
     if (dry.err != hipSuccess)
       return dry.err == hipErrorInvalidConfiguration ? FMM_ERR_UNSUPPORTED : FMM_ERR_HIP;
   }
@@ -739,11 +744,18 @@ int run_layer_backward(const void* x, const void* w_qkv, const void* w_out, cons
       return FMM_ERR_HIP;
   }
   // dm = dy W_out^T, dW_out = m^T dy
+  float* wg = reinterpret_cast<float*>(at(ws, off_wg));
   if (fmm::layer_gemm(hdl, stream, dtype, dy, w_out, at(ws, off_dm), M, E, E, false, true) !=
-          hipSuccess ||
-      fmm::layer_gemm(hdl, stream, dtype, at(ws, off_m), dy, dw_out, E, M, E, true, false) !=
-          hipSuccess)
+      hipSuccess)
     return FMM_ERR_HIP;
+  {
+    std::lock_guard<std::mutex> g(t.mu);
+    fmm::Launcher L;
+    L.timer = &t;
+    if (fmm::layer_wgrad(hdl, L, stream, dtype, at(ws, off_m), dy, dw_out, M, E, E, wg) !=
+        hipSuccess)
+      return FMM_ERR_HIP;
+  }
   // the operator's backward on the heads' share of dm, then dqkv per token
   {
     std::lock_guard<std::mutex> g(t.mu);
@@ -763,11 +775,15 @@ int run_layer_backward(const void* x, const void* w_qkv, const void* w_out, cons
   }
   // dx = dqkv W_qkv^T, dW_qkv = x^T dqkv
   if (fmm::layer_gemm(hdl, stream, dtype, at(ws, off_qkv), w_qkv, dx, M, 3 * E, E, false,
-                      true) != hipSuccess ||
-      fmm::layer_gemm(hdl, stream, dtype, x, at(ws, off_qkv), dw_qkv, E, M, 3 * E, true,
-                      false) != hipSuccess)
+                      true) != hipSuccess)
     return FMM_ERR_HIP;
-  return FMM_OK;
+  std::lock_guard<std::mutex> g(t.mu);
+  fmm::Launcher L;
+  L.timer = &t;
+  return fmm::layer_wgrad(hdl, L, stream, dtype, x, at(ws, off_qkv), dw_qkv, M, E, 3 * E, wg) ==
+                 hipSuccess
+             ? FMM_OK
+             : FMM_ERR_HIP;
 }
 
 // ------------------------------------------------------------------ fast weight

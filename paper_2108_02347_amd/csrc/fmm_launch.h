@@ -206,6 +206,13 @@ hipError_t launch_layer_proj(Launcher& L, bool qkv, const void* in, const void* 
 hipError_t layer_gemm(void* handle, void* stream, int dtype, const void* A, const void* Bm,
                       void* C, int M, int K, int Nc, bool ta = false, bool tb = false);
 void* layer_blas_handle_create();
+// The layer's weight gradients C [E, Nc] = A^T B (A [M, E], B [M, Nc] of the
+// storage type, C too): per chunk of kWgradChunk tokens into `scratch`
+// (layer_wgrad_scratch_bytes), then summed in chunk order.
+constexpr int kWgradChunk = 1024;
+size_t layer_wgrad_scratch_bytes(int M, int E, int Nc);
+hipError_t layer_wgrad(void* handle, Launcher& L, void* stream, int dtype, const void* A,
+                       const void* Bm, void* C, int M, int E, int Nc, float* scratch);
 // The layer's backward copies: [B N, E] rows -> [B, H, N, d] (split1), and
 // [B, H, N, d] -> part `part` (E columns from part * E) of [B N, 3E] rows.
 hipError_t launch_layer_split1(Launcher& L, int dtype, const void* src, void* dst, int B, int N,

@@ -226,6 +226,72 @@ hipError_t layer_gemm(void* handle, void* stream, int dtype, const void* A, cons
   return gemm_rm(hdl, dtype, A, Bm, C, M, K, Nc, ta, tb);
 }
 
+// Weight gradients C [E, Nc] = A^T B with A [M, E] and B [M, Nc] row-major and
+// M (the tokens) far larger than E and Nc: one product per chunk of KC tokens
+// (a strided batch, fp32 results), then the chunks summed in order into C (the
+// storage type).  A single product would leave most of the GPU idle (a few
+// output tiles, each walking all M tokens).
+namespace {
+template <typename T>
+__global__ __launch_bounds__(256) void k_sum_chunks(const float* __restrict__ part,
+                                                    T* __restrict__ c, int n, int nchunk) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int j = 0; j < nchunk; ++j) s += part[(size_t)j * n + i];
+  if constexpr (sizeof(T) == 2) c[i] = (T)f32_to_bf16_bits(s);
+  else c[i] = s;
+}
+}  // namespace
+
+size_t layer_wgrad_scratch_bytes(int M, int E, int Nc) {
+  const int nchunk = (M + kWgradChunk - 1) / kWgradChunk;
+  return (size_t)nchunk * E * Nc * sizeof(float);
+}
+
+hipError_t layer_wgrad(void* handle, Launcher& L, void* stream, int dtype, const void* A,
+                       const void* Bm, void* C, int M, int E, int Nc, float* scratch) {
+  const int nchunk = (M + kWgradChunk - 1) / kWgradChunk;
+  const int n = E * Nc;
+  hipStream_t s = (hipStream_t)stream;
+  if (!L.dry) {
+    rocblas_handle hdl = (rocblas_handle)handle;
+    if (rocblas_set_stream(hdl, s) != rocblas_status_success) return L.note(hipErrorLaunchFailure);
+    const rocblas_datatype t =
+        dtype == FMM_DTYPE_BF16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
+    const size_t es = dtype == FMM_DTYPE_BF16 ? 2 : 4;
+    const float one = 1.f, zero = 0.f;
+    // column-major: C^T [Nc, E] = B^T [Nc, K] A [K, E] per chunk of K tokens;
+    // the full chunks as one strided batch, a shorter last chunk as one more
+    // product
+    const int full = M / kWgradChunk, rem = M - full * kWgradChunk;
+    auto batch = [&](int k, int count, const void* a0, const void* b0, float* c0) {
+      return rocblas_gemm_strided_batched_ex(
+          hdl, rocblas_operation_none, rocblas_operation_transpose, Nc, E, k, &one, b0, t, Nc,
+          (rocblas_stride)k * Nc, a0, t, E, (rocblas_stride)k * E, &zero, c0,
+          rocblas_datatype_f32_r, Nc, (rocblas_stride)n, c0, rocblas_datatype_f32_r, Nc,
+          (rocblas_stride)n, count, rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+    };
+    if (full > 0 && batch(kWgradChunk, full, A, Bm, scratch) != rocblas_status_success)
+      return L.note(hipErrorLaunchFailure);
+    if (rem > 0) {
+      const size_t off = (size_t)full * kWgradChunk;
+      const void* a1 = static_cast<const unsigned char*>(A) + off * E * es;
+      const void* b1 = static_cast<const unsigned char*>(Bm) + off * Nc * es;
+      if (batch(rem, 1, a1, b1, scratch + (size_t)full * n) != rocblas_status_success)
+        return L.note(hipErrorLaunchFailure);
+    }
+  }
+  const dim3 grid((n + 255) / 256);
+  if (dtype == FMM_DTYPE_BF16)
+    L(FMM_KERNEL_LAYER_COPY, k_sum_chunks<bf16_t>, grid, dim3(256), 0, s,
+      (const float*)scratch, (bf16_t*)C, n, nchunk);
+  else
+    L(FMM_KERNEL_LAYER_COPY, k_sum_chunks<float>, grid, dim3(256), 0, s,
+      (const float*)scratch, (float*)C, n, nchunk);
+  return L.err;
+}
+
 hipError_t launch_layer_split1(Launcher& L, int dtype, const void* src, void* dst, int B, int N,
                                int H, int d, hipStream_t s) {
   if (dtype == FMM_DTYPE_BF16)
