@@ -77,12 +77,40 @@ __device__ __forceinline__ float block_sum(float x, float* red, int slot) {
   }
 }
 
+// a . b over D features with four interleaved partial sums: a dependent chain
+// of D / 4 + 2 operations instead of D, which is what each sequential step
+// waits on
+template <int D>
+__device__ __forceinline__ float dot_split(const float* a, const float* b) {
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+#pragma unroll
+  for (int c = 0; c < D; c += 4) {
+    s0 = fmaf(a[c], b[c], s0);
+    s1 = fmaf(a[c + 1], b[c + 1], s1);
+    s2 = fmaf(a[c + 2], b[c + 2], s2);
+    s3 = fmaf(a[c + 3], b[c + 3], s3);
+  }
+  return (s0 + s1) + (s2 + s3);
+}
+
+// Takes x out of its ring slot here: the register allocator then reuses the
+// slot for the load issued next instead of copying the slot at the loop's
+// back edge (a copy of a register whose load is in flight waits for it).
+__device__ __forceinline__ void take(float& x) { asm volatile("" : "+v"(x)); }
+
+// steps between loading a step's inputs and running it (even: the LDS
+// buffers alternate by step parity; two for the widest heads, whose rows
+// already fill the registers)
+template <int D>
+constexpr int ahead_steps() { return D >= 128 ? 2 : 4; }
+
 template <typename T, int D>
 __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const float* __restrict__ beta, T* __restrict__ out, const float* __restrict__ w_far, int H,
     int N) {
   constexpr int NWV = D > 64 ? D / 64 : 1;
+  constexpr int kAhead = ahead_steps<D>();
   constexpr int ROWS = D >= 64 ? 4 : D / 16;  // 16-lane rows holding features
   __shared__ float pk_s[2][D], pq_s[2][D];
   __shared__ float red[2 * 3 * NWV];
@@ -95,31 +123,36 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight(
 #pragma unroll
   for (int c = 0; c < D; ++c) wrow[c] = 0.f;
   float zr = 0.f;
-  // the first step's inputs
-  float xk = 0.f, xq = 0.f, xv = 0.f, bt = 0.f, xo = 0.f;
-  if (N > 0) {
-    if (act) {
-      xk = ld_elem<T>(k + base + r);
-      xq = ld_elem<T>(q + base + r);
-      xv = ld_elem<T>(v + base + r);
-      xo = ld_elem<T>(out + base + r);
-    }
-    bt = beta[(size_t)bh * N];
-  }
-  for (int i = 0; i < N; ++i) {
-    const int par = i & 1;
-    // prefetch step i + 1 (row i + 1 of out is not written before step i + 1)
-    float nk = 0.f, nq = 0.f, nv = 0.f, nb = 0.f, no = 0.f;
-    if (i + 1 < N) {
-      const size_t o = base + (size_t)(i + 1) * D + r;
-      if (act) {
-        nk = ld_elem<T>(k + o);
-        nq = ld_elem<T>(q + o);
-        nv = ld_elem<T>(v + o);
-        no = ld_elem<T>(out + o);
-      }
-      nb = beta[(size_t)bh * N + i + 1];
-    }
+  // a step's inputs are loaded kAhead steps before it runs (register ring,
+  // slot t for the steps i = t mod kAhead), so that no step waits on memory
+  // latency, which is longer than a step (row j of out is not written before
+  // step j)
+  // The loads are unconditional (positions past the end and idle lanes read a
+  // valid element that is then ignored), so that every path issues the same
+  // loads and each step waits only for its own.
+  const int rl = act ? r : 0;
+  float rk[kAhead], rq[kAhead], rv[kAhead], ro[kAhead], rb[kAhead];
+  auto fetch = [&](int j, int t) {
+    const int jc = j < N ? j : N - 1;
+    const size_t o = base + (size_t)jc * D + rl;
+    rk[t] = ld_elem<T>(k + o);
+    rq[t] = ld_elem<T>(q + o);
+    rv[t] = ld_elem<T>(v + o);
+    ro[t] = ld_elem<T>(out + o);
+    rb[t] = beta[(size_t)bh * N + jc];
+  };
+#pragma unroll
+  for (int t = 0; t < kAhead; ++t) fetch(t, t);
+  for (int i0 = 0; i0 < N; i0 += kAhead)
+#pragma unroll
+  for (int t = 0; t < kAhead; ++t) {
+    const int i = i0 + t;
+    if (i >= N) break;
+    const int par = t & 1;
+    float xk = act ? rk[t] : 0.f, xq = act ? rq[t] : 0.f, xv = act ? rv[t] : 0.f;
+    float xo = act ? ro[t] : 0.f, bt = rb[t];
+    take(xk), take(xq), take(xv), take(xo), take(bt);
+    fetch(i + kAhead, t);
     const float fk = act ? phi_l(xk, 0) : 0.f;
     const float fq = act ? phi_l(xq, 0) : 0.f;
     const float sk = block_sum<NWV, ROWS>(fk, red, 0);
@@ -132,24 +165,14 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight(
     // (one wave: its own LDS writes are seen by its later reads)
     if constexpr (NWV > 1) __syncthreads();
     // u_r = W_r . p(k); W_r += beta (v_r - u_r) p(k); num_r = W_r . p(q)
-    float u = 0.f;
-#pragma unroll
-    for (int c = 0; c < D; ++c) u = fmaf(wrow[c], pk_s[par][c], u);
+    const float u = dot_split<D>(wrow, pk_s[par]);
     const float coef = bt * (xv - u);
-    float num = 0.f;
 #pragma unroll
-    for (int c = 0; c < D; ++c) {
-      wrow[c] = fmaf(coef, pk_s[par][c], wrow[c]);
-      num = fmaf(wrow[c], pq_s[par][c], num);
-    }
+    for (int c = 0; c < D; ++c) wrow[c] = fmaf(coef, pk_s[par][c], wrow[c]);
+    const float num = dot_split<D>(wrow, pq_s[par]);
     zr += pk;
     const float den = block_sum<NWV, ROWS>(act ? zr * pq : 0.f, red + 4 * NWV, par);
     if (act && sf > 0.f) st_elem<T>(out + base + (size_t)i * D + r, xo + sf * (num / den));
-    xk = nk;
-    xq = nq;
-    xv = nv;
-    xo = no;
-    bt = nb;
   }
 }
 
@@ -180,6 +203,7 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
     float* __restrict__ wst, float* __restrict__ zst, float* __restrict__ gfw,
     const float* __restrict__ w_far, int H, int N) {
   constexpr int NWV = D > 64 ? D / 64 : 1;
+  constexpr int kAhead = ahead_steps<D>();
   constexpr int ROWS = D >= 64 ? 4 : D / 16;
   constexpr int LD = D + 1;  // padded rows of the column-sum buffers
   __shared__ float pk_s[2][D], pq_s[2][D];
@@ -190,6 +214,7 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
   const int bh = blockIdx.x, h = bh % H;
   const int r = threadIdx.x;
   const bool act = r < D;
+  const int rl = act ? r : 0;  // the row an idle lane reads (and ignores)
   const size_t base = (size_t)bh * N * D;
   float* ws = wst + (size_t)bh * N * D * D;
   float* zs = zst + (size_t)bh * N * D;
@@ -212,19 +237,33 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
 #pragma unroll
     for (int c = 0; c < D; ++c) wrow[c] = 0.f;
     float zr = 0.f;
-    for (int i = 0; i < N; ++i) {
-      const int par = i & 1;
+    // step i's inputs, loaded kAhead steps earlier (ring slot i mod kAhead)
+    // (unconditional loads: past the end and on idle lanes a valid element
+    // is read and ignored)
+    float rk[kAhead], rv[kAhead], rb[kAhead];
+    auto fetch = [&](int j, int t) {
+      const int jc = j < N ? j : N - 1;
+      const size_t oj = base + (size_t)jc * D + rl;
+      rk[t] = ld_elem<T>(k + oj);
+      rv[t] = ld_elem<T>(v + oj);
+      rb[t] = beta[(size_t)bh * N + jc];
+    };
+#pragma unroll
+    for (int t = 0; t < kAhead; ++t) fetch(t, t);
+    for (int i0 = 0; i0 < N; i0 += kAhead)
+#pragma unroll
+    for (int t = 0; t < kAhead; ++t) {
+      const int i = i0 + t;
+      if (i >= N) break;
+      const int par = t & 1;
       slot = par;
-      const size_t o = base + (size_t)i * D + r;
-      const float xk = act ? ld_elem<T>(k + o) : 0.f;
-      const float xv = act ? ld_elem<T>(v + o) : 0.f;
-      const float bt = beta[(size_t)bh * N + i];
+      float xk = act ? rk[t] : 0.f, xv = act ? rv[t] : 0.f, bt = rb[t];
+      take(xk), take(xv), take(bt);
+      fetch(i + kAhead, t);
       float pk, sk;
       norm_phi(xk, pk_s[par], pk, sk);
       if constexpr (NWV > 1) __syncthreads();
-      float u = 0.f;
-#pragma unroll
-      for (int c = 0; c < D; ++c) u = fmaf(wrow[c], pk_s[par][c], u);
+      const float u = dot_split<D>(wrow, pk_s[par]);
       const float coef = bt * (xv - u);
 #pragma unroll
       for (int c = 0; c < D; ++c) wrow[c] = fmaf(coef, pk_s[par][c], wrow[c]);
@@ -250,35 +289,66 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
   float zsr = 0.f;       // Zs[r]
   float bt_next = 0.f;   // beta_{i+1}
   float acc_gfw = 0.f;   // this thread's share of sum_i g_i . fw_i
-  for (int i = N - 1; i >= 0; --i) {
+  // row r of W_j (of W_0 for j < 0, which the step then ignores)
+  auto ld_row = [&](int j, float* w) {
+    const float* src = ws + ((size_t)(j < 0 ? 0 : j) * D + rl) * D;
+#pragma unroll
+    for (int c = 0; c < D; c += 4) {
+      const float4 a = *reinterpret_cast<const float4*>(src + c);
+      w[c] = a.x; w[c + 1] = a.y; w[c + 2] = a.z; w[c + 3] = a.w;
+    }
+  };
+  // step i's inputs (and the gradients already in place at position i) are
+  // loaded kAhead steps earlier (ring slot (N - 1 - i) mod kAhead); the rows
+  // of W sit in a ring of kRingW slots (slot (N - 1 - i) mod kRingW holds W_i
+  // at step i), refilled as soon as a step is done with its W_i, so W_j is
+  // loaded kRingW - 1 steps before its first use (as many as the registers
+  // allow)
+  constexpr int kRingW = D <= 16 ? 4 : 2;
+  static_assert(kAhead % kRingW == 0, "the W ring's slot must follow the step ring's");
+  float wr[kRingW][D];
+  float rk[kAhead], rq[kAhead], rv[kAhead], rg[kAhead], rb[kAhead], rz[kAhead];
+  float rdq[kAhead], rdk[kAhead], rdv[kAhead];
+  // (unconditional loads: before the start and on idle lanes a valid
+  // element is read and ignored)
+  auto fetch = [&](int j, int t) {
+    const int jc = j < 0 ? 0 : j;
+    const size_t oj = base + (size_t)jc * D + rl;
+    rk[t] = ld_elem<T>(k + oj);
+    rq[t] = ld_elem<T>(q + oj);
+    rv[t] = ld_elem<T>(v + oj);
+    rg[t] = ld_elem<T>(dout + oj);
+    rb[t] = beta[(size_t)bh * N + jc];
+    rz[t] = zs[(size_t)jc * D + rl];
+    rdq[t] = ld_elem<T>(dq + oj);
+    rdk[t] = ld_elem<T>(dk + oj);
+    rdv[t] = ld_elem<T>(dv + oj);
+  };
+#pragma unroll
+  for (int t = 0; t < kRingW; ++t) ld_row(N - 1 - t, wr[t]);
+#pragma unroll
+  for (int t = 0; t < kAhead; ++t) fetch(N - 1 - t, t);
+  for (int i0 = N - 1; i0 >= 0; i0 -= kAhead)
+#pragma unroll
+  for (int t = 0; t < kAhead; ++t) {
+    const int i = i0 - t;
+    if (i < 0) break;
     const int par = i & 1;
     slot = par;
     const size_t o = base + (size_t)i * D + r;
-    const float xk = act ? ld_elem<T>(k + o) : 0.f;
-    const float xq = act ? ld_elem<T>(q + o) : 0.f;
-    const float xv = act ? ld_elem<T>(v + o) : 0.f;
-    const float xg = act ? ld_elem<T>(dout + o) : 0.f;
-    const float bt = beta[(size_t)bh * N + i];
-    float wi[D], wp[D];
-    const float* wsrc = ws + ((size_t)i * D + (act ? r : 0)) * D;
-#pragma unroll
-    for (int c = 0; c < D; c += 4) {
-      const float4 a = *reinterpret_cast<const float4*>(wsrc + c);
-      wi[c] = a.x; wi[c + 1] = a.y; wi[c + 2] = a.z; wi[c + 3] = a.w;
-      if (i > 0) {
-        const float4 b = *reinterpret_cast<const float4*>(wsrc - D * D + c);
-        wp[c] = b.x; wp[c + 1] = b.y; wp[c + 2] = b.z; wp[c + 3] = b.w;
-      } else {
-        wp[c] = wp[c + 1] = wp[c + 2] = wp[c + 3] = 0.f;
-      }
-    }
-    const float zi = act ? zs[(size_t)i * D + r] : 0.f;
+    float xk = act ? rk[t] : 0.f, xq = act ? rq[t] : 0.f, xv = act ? rv[t] : 0.f;
+    float xg = act ? rg[t] : 0.f, zi = act ? rz[t] : 0.f, bt = rb[t];
+    float odq = rdq[t], odk = rdk[t], odv = rdv[t];
+    take(xk), take(xq), take(xv), take(xg), take(zi), take(bt);
+    take(odq), take(odk), take(odv);
+    fetch(i - kAhead, t);
+    const float* wi = wr[t % kRingW];
+    const float* wp = wr[(t + 1) % kRingW];  // W_{i-1} (W_0 at i = 0, where W_{-1} = 0)
+    const float wm = i > 0 ? 1.f : 0.f;
     // G_{i+1} carried back through step i + 1's write (p(k_{i+1}) still in
     // pk_s[par ^ 1], written last iteration)
     if (i + 1 < N) {
-      float gp1 = 0.f;
-#pragma unroll
-      for (int c = 0; c < D; ++c) gp1 = fmaf(grow[c], pk_s[par ^ 1][c], gp1);
+      const float gp1 = dot_split<D>(grow, pk_s[par ^ 1]);
       const float m = bt_next * gp1;
 #pragma unroll
       for (int c = 0; c < D; ++c) grow[c] = fmaf(-m, pk_s[par ^ 1][c], grow[c]);
@@ -291,9 +361,7 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
     slot ^= 1;
     if constexpr (NWV > 1) __syncthreads();
     // n_r, s, fw_r; dn_r, ds
-    float nr = 0.f;
-#pragma unroll
-    for (int c = 0; c < D; ++c) nr = fmaf(wi[c], pq_s[par][c], nr);
+    const float nr = dot_split<D>(wi, pq_s[par]);
     const float s_i = bsum(act ? zi * pq : 0.f, 1);
     const float fw = nr / s_i;
     const float gdot = bsum(act ? xg * fw : 0.f, 2);  // g_i . fw_i
@@ -305,12 +373,9 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
     for (int c = 0; c < D; ++c) grow[c] = fmaf(dn, pq_s[par][c], grow[c]);
     zsr = fmaf(ds, pq, zsr);
     // e_r, gp_r, dv, dbeta
-    float u = 0.f, gp = 0.f;
-#pragma unroll
-    for (int c = 0; c < D; ++c) {
-      u = fmaf(wp[c], pk_s[par][c], u);
-      gp = fmaf(grow[c], pk_s[par][c], gp);
-    }
+    const float u = wm * dot_split<D>(wp, pk_s[par]);
+    const float gp = dot_split<D>(grow, pk_s[par]);
+    const float gpw = wm * gp;
     const float e = act ? xv - u : 0.f;
     slot ^= 1;
     const float db = bsum(e * gp, 1);
@@ -320,16 +385,22 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
 #pragma unroll
       for (int c = 0; c < D; ++c) {
         cb1[r * LD + c] = wi[c] * dn;
-        cb2[r * LD + c] = fmaf(grow[c], e, -wp[c] * gp);
+        cb2[r * LD + c] = fmaf(grow[c], e, -wp[c] * gpw);
       }
     }
     __syncthreads();
     float c1 = 0.f, c2 = 0.f;
     if (act) {
-      for (int rr = 0; rr < D; ++rr) {
-        c1 += cb1[rr * LD + r];
-        c2 += cb2[rr * LD + r];
+      float a0 = 0.f, a1 = 0.f, b0 = 0.f, b1 = 0.f;
+#pragma unroll
+      for (int rr = 0; rr < D; rr += 2) {
+        a0 += cb1[rr * LD + r];
+        a1 += cb1[(rr + 1) * LD + r];
+        b0 += cb2[rr * LD + r];
+        b1 += cb2[(rr + 1) * LD + r];
       }
+      c1 = a0 + a1;
+      c2 = b0 + b1;
     }
     __syncthreads();  // the buffers are rewritten next step
     const float dpq = c1 + ds * zi;
@@ -341,12 +412,14 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
     if (act) {
       const float gq = (xq > 0.f ? 1.f : __expf(xq)) * (dpq - tq) / sq;
       const float gk = (xk > 0.f ? 1.f : __expf(xk)) * (dpk - tk) / sk;
-      st_elem<T>(dq + o, ld_elem<T>(dq + o) + gq);
-      st_elem<T>(dk + o, ld_elem<T>(dk + o) + gk);
-      st_elem<T>(dv + o, ld_elem<T>(dv + o) + bt * gp);
+      st_elem<T>(dq + o, odq + gq);
+      st_elem<T>(dk + o, odk + gk);
+      st_elem<T>(dv + o, odv + bt * gp);
     }
     if (r == 0) dbeta[(size_t)bh * N + i] = db;
     bt_next = bt;
+    // W_i's slot takes W_{i-kRingW}
+    ld_row(i - kRingW, wr[t % kRingW]);
   }
   if (r == 0) gfw[bh] = acc_gfw;
 }
