@@ -7,10 +7,12 @@
 // slice with one thread per row r of W (row r of W and z_r in registers), so
 // a step is two length-d dot products per thread and the rank-one update of
 // its row, plus three sums over the threads (sum of phi(k), sum of phi(q), the
-// denominator), by DPP within the wave.  The next step's
-// q, k, v, beta and output row are loaded while the current one computes (a
-// load issued in the step that needs it would hold up every later load: the
-// memory counter is waited for in order).  The kernel adds
+// denominator), by DPP within the wave; for d = 16 and 32, 64 / d lanes share
+// a row (k_fast_weight_narrow), which fills the wave and needs no LDS.  Each
+// step's q, k, v, beta and output row are loaded a few steps ahead (memory
+// latency is longer than a step, and a load issued in the step that needs it
+// would hold up every later load: the memory counter is waited for in
+// order).  The kernel adds
 // sigmoid(w_far[h]) fw_i to `out`, which already holds the rest of the
 // operator (near field and, for the two-kernel variant, the linear far part).
 #include <hip/hip_runtime.h>
@@ -173,6 +175,108 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight(
     zr += pk;
     const float den = block_sum<NWV, ROWS>(act ? zr * pq : 0.f, red + 4 * NWV, par);
     if (act && sf > 0.f) st_elem<T>(out + base + (size_t)i * D + r, xo + sf * (num / den));
+  }
+}
+
+// Narrow heads (d = 16, 32): 64 / d lanes share a row of W, each holding
+// d / (64 / d) of its columns and the same columns of z, so that the wave has
+// no idle lanes and a step needs no LDS: every lane forms p(k) and p(q) for
+// its own columns (the sums over the features by DPP within the row's
+// lanes), and the three length-d dot products (W_r . p(k), W_r . p(q),
+// z . p(q)) are partial sums over the lane's columns plus the same DPP steps.
+// Lane 0 of each row's group writes that row's output.
+template <int LPR>
+__device__ __forceinline__ float row_sum(float x) {
+  if constexpr (LPR >= 2) x = dpp_add<0xB1>(x);
+  if constexpr (LPR >= 4) x = dpp_add<0x4E>(x);
+  return x;
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(64) void k_fast_weight_narrow(
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
+    const float* __restrict__ beta, T* __restrict__ out, const float* __restrict__ w_far, int H,
+    int N) {
+  static_assert(D == 16 || D == 32, "rows shared by 64 / d lanes");
+  constexpr int LPR = 64 / D;    // lanes per row of W
+  constexpr int CPL = D / LPR;   // columns per lane
+  constexpr int NQ = CPL / 4;    // quads per lane
+  constexpr int kAhead = ahead_steps<D>();
+  typedef typename QuadOf<T>::type quad_t;
+  const int bh = blockIdx.x, h = bh % H;
+  const int lane = threadIdx.x;
+  const int r = lane / LPR, c0 = (lane % LPR) * CPL;
+  const size_t base = (size_t)bh * N * D;
+  const float sf = sigmoidf_exact(w_far[h]);
+  float w[CPL], z[CPL];
+#pragma unroll
+  for (int c = 0; c < CPL; ++c) w[c] = z[c] = 0.f;
+  // inputs kAhead steps ahead in a register ring, as in k_fast_weight
+  quad_t rk[kAhead][NQ], rq[kAhead][NQ];
+  float rv[kAhead], ro[kAhead], rb[kAhead];
+  auto fetch = [&](int j, int t) {
+    const int jc = j < N ? j : N - 1;
+    const size_t o = base + (size_t)jc * D;
+#pragma unroll
+    for (int m = 0; m < NQ; ++m) {
+      rk[t][m] = *reinterpret_cast<const quad_t*>(k + o + c0 + 4 * m);
+      rq[t][m] = *reinterpret_cast<const quad_t*>(q + o + c0 + 4 * m);
+    }
+    rv[t] = ld_elem<T>(v + o + r);
+    ro[t] = ld_elem<T>(out + o + r);
+    rb[t] = beta[(size_t)bh * N + jc];
+  };
+#pragma unroll
+  for (int t = 0; t < kAhead; ++t) fetch(t, t);
+  for (int i0 = 0; i0 < N; i0 += kAhead)
+#pragma unroll
+  for (int t = 0; t < kAhead; ++t) {
+    const int i = i0 + t;
+    if (i >= N) break;
+    float xk[CPL], xq[CPL];
+#pragma unroll
+    for (int m = 0; m < NQ; ++m) {
+      quad_to_f32(rk[t][m], xk + 4 * m);
+      quad_to_f32(rq[t][m], xq + 4 * m);
+    }
+    float xv = rv[t], xo = ro[t], bt = rb[t];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) take(xk[c]), take(xq[c]);
+    take(xv), take(xo), take(bt);
+    fetch(i + kAhead, t);
+    float fk[CPL], fq[CPL];
+    float sk = 0.f, sq = 0.f;
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      fk[c] = phi_l(xk[c], 0);
+      fq[c] = phi_l(xq[c], 0);
+      sk += fk[c];
+      sq += fq[c];
+    }
+    sk = row_sum<LPR>(sk);
+    sq = row_sum<LPR>(sq);
+    // one division per sum, then products (within an ulp or so of the
+    // quotients, and a quarter of the instructions)
+    const float ik = 1.f / sk, iq = 1.f / sq;
+    float pk[CPL], pq[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      pk[c] = fk[c] * ik;
+      pq[c] = fq[c] * iq;
+    }
+    // u_r = W_r . p(k); W_r += beta (v_r - u_r) p(k); num_r = W_r . p(q);
+    // z += p(k); den = z . p(q)
+    const float u = row_sum<LPR>(dot_split<CPL>(w, pk));
+    const float coef = bt * (xv - u);
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) {
+      w[c] = fmaf(coef, pk[c], w[c]);
+      z[c] += pk[c];
+    }
+    const float num = row_sum<LPR>(dot_split<CPL>(w, pq));
+    const float den = row_sum<LPR>(dot_split<CPL>(z, pq));
+    if (lane % LPR == 0 && sf > 0.f)
+      st_elem<T>(out + base + (size_t)i * D + r, xo + sf * (num / den));
   }
 }
 
@@ -465,9 +569,15 @@ hipError_t launch_fw_bwd_t(Launcher& L, const FwBwdArgs& a) {
 
 template <typename T, int D>
 void launch_fw_d(Launcher& L, const FwArgs& a) {
-  L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight<T, D>, dim3(a.B * a.H), dim3(D > 64 ? D : 64), 0,
-    (hipStream_t)a.stream, (const T*)a.q, (const T*)a.k, (const T*)a.v, a.beta, (T*)a.out,
-    a.w_far, a.H, a.N);
+  if constexpr (D <= 32) {
+    L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight_narrow<T, D>, dim3(a.B * a.H), dim3(64), 0,
+      (hipStream_t)a.stream, (const T*)a.q, (const T*)a.k, (const T*)a.v, a.beta, (T*)a.out,
+      a.w_far, a.H, a.N);
+  } else {
+    L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight<T, D>, dim3(a.B * a.H), dim3(D > 64 ? D : 64), 0,
+      (hipStream_t)a.stream, (const T*)a.q, (const T*)a.k, (const T*)a.v, a.beta, (T*)a.out,
+      a.w_far, a.H, a.N);
+  }
 }
 
 template <typename T>

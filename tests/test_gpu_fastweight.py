@@ -46,6 +46,14 @@ def test_fast_weight_widths(d, dtype):
     check_fw(1, 3, 65, d, 0, 0, dtype, 4200 + d)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("d", [16, 32])
+def test_fast_weight_short_and_ragged(d, dtype):
+    # lengths below and between the steps the inputs are loaded ahead
+    for i, n in enumerate((1, 2, 3, 5, 131)):
+        check_fw(3, 2, n, d, 4, i % 2, dtype, 4300 + 10 * d + i)
+
+
 # ------------------------------------------------------------------ backward
 
 def check_fw_backward(B, H, N, d, kw, n_linear, dtype, seed, std=1.0):
