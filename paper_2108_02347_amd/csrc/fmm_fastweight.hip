@@ -336,7 +336,70 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
   };
 
   // ---- forward sweep: W_i and z_i of every step into the workspace
-  {
+  if constexpr (D <= 32) {
+    // narrow heads: 64 / d lanes per row of W, each with d / (64 / d) of its
+    // columns (and the same columns of z), as in k_fast_weight_narrow
+    constexpr int LPR = 64 / D, CPL = D / LPR, NQ = CPL / 4;
+    typedef typename QuadOf<T>::type quad_t;
+    const int rn = r / LPR, c0 = (r % LPR) * CPL;
+    float w[CPL], z[CPL];
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) w[c] = z[c] = 0.f;
+    quad_t rkq[kAhead][NQ];
+    float rv[kAhead], rb[kAhead];
+    auto fetch = [&](int j, int t) {
+      const int jc = j < N ? j : N - 1;
+      const size_t o = base + (size_t)jc * D;
+#pragma unroll
+      for (int m = 0; m < NQ; ++m)
+        rkq[t][m] = *reinterpret_cast<const quad_t*>(k + o + c0 + 4 * m);
+      rv[t] = ld_elem<T>(v + o + rn);
+      rb[t] = beta[(size_t)bh * N + jc];
+    };
+#pragma unroll
+    for (int t = 0; t < kAhead; ++t) fetch(t, t);
+    for (int i0 = 0; i0 < N; i0 += kAhead)
+#pragma unroll
+    for (int t = 0; t < kAhead; ++t) {
+      const int i = i0 + t;
+      if (i >= N) break;
+      float xk[CPL];
+#pragma unroll
+      for (int m = 0; m < NQ; ++m) quad_to_f32(rkq[t][m], xk + 4 * m);
+      float xv = rv[t], bt = rb[t];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) take(xk[c]);
+      take(xv), take(bt);
+      fetch(i + kAhead, t);
+      float fk[CPL], sk = 0.f;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        fk[c] = phi_l(xk[c], 0);
+        sk += fk[c];
+      }
+      const float ik = 1.f / row_sum<LPR>(sk);
+      float pk[CPL];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) pk[c] = fk[c] * ik;
+      const float u = row_sum<LPR>(dot_split<CPL>(w, pk));
+      const float coef = bt * (xv - u);
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        w[c] = fmaf(coef, pk[c], w[c]);
+        z[c] += pk[c];
+      }
+      float* dst = ws + ((size_t)i * D + rn) * D + c0;
+#pragma unroll
+      for (int c = 0; c < CPL; c += 4)
+        *reinterpret_cast<float4*>(dst + c) = make_float4(w[c], w[c + 1], w[c + 2], w[c + 3]);
+      if (rn == 0) {
+#pragma unroll
+        for (int c = 0; c < CPL; c += 4)
+          *reinterpret_cast<float4*>(zs + (size_t)i * D + c0 + c) =
+              make_float4(z[c], z[c + 1], z[c + 2], z[c + 3]);
+      }
+    }
+  } else {
     float wrow[D];
 #pragma unroll
     for (int c = 0; c < D; ++c) wrow[c] = 0.f;
