@@ -312,7 +312,7 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
   constexpr int LD = D + 1;  // padded rows of the column-sum buffers
   __shared__ float pk_s[2][D], pq_s[2][D];
   __shared__ float red[2 * 3 * NWV];
-  extern __shared__ float colbuf[];  // two D x LD buffers
+  extern __shared__ __align__(16) float colbuf[];  // the two column-sum buffers
   float* cb1 = colbuf;
   float* cb2 = colbuf + D * LD;
   const int bh = blockIdx.x, h = bh % H;
@@ -450,12 +450,166 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
   __syncthreads();
 
   // ---- backward sweep
+  float acc_gfw = 0.f;   // this thread's share of sum_i g_i . fw_i
+  if constexpr (D == 16) {
+    // d = 16: the row-wise work (G carried and updated, the row dot products,
+    // the terms of the column sums) with four lanes per row of W, each on
+    // four of its columns; the per-feature work (p at one feature, Zs, the
+    // column sums read back, dq and dk) on lanes 0..15, one feature each.
+    constexpr int LPR = 64 / D, CPL = D / LPR;
+    constexpr int LDN = D + 4;  // padded, 16-byte aligned rows of the column-sum buffers
+    constexpr int kRingW = kAhead;
+    typedef typename QuadOf<T>::type quad_t;
+    static_assert(CPL == 4, "one quad of columns per lane");
+    float* cn1 = colbuf;
+    float* cn2 = colbuf + D * LDN;
+    const int rn = r / LPR, g = r % LPR, c0 = g * CPL;
+    const bool col = r < D;  // the lane of feature r
+    float gr[CPL], pkn[CPL];  // row rn of G, p(k_{i+1}), at the lane's columns
+#pragma unroll
+    for (int c = 0; c < CPL; ++c) gr[c] = pkn[c] = 0.f;
+    float zs_col = 0.f;  // Zs at feature r
+    float bt_next = 0.f;
+    // ring of W rows: slot (N - 1 - i) mod kRingW holds row rn of W_i at the
+    // lane's columns; rows before the first read as W_0 and are ignored
+    float wr[kRingW][CPL];
+    auto ld_wrow = [&](int j, float* w) {
+      const float4 a =
+          *reinterpret_cast<const float4*>(ws + ((size_t)(j < 0 ? 0 : j) * D + rn) * D + c0);
+      w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w;
+    };
+    // step inputs kAhead steps ahead (unconditional loads, as above)
+    quad_t rk[kAhead], rq[kAhead];
+    float4 rz[kAhead];
+    float rv[kAhead], rg[kAhead], rdv[kAhead], rb[kAhead];
+    float rkc[kAhead], rqc[kAhead], rzc[kAhead], rdq[kAhead], rdk[kAhead];
+    auto fetch = [&](int j, int t) {
+      const int jc = j < 0 ? 0 : j;
+      const size_t o = base + (size_t)jc * D;
+      rk[t] = *reinterpret_cast<const quad_t*>(k + o + c0);
+      rq[t] = *reinterpret_cast<const quad_t*>(q + o + c0);
+      rz[t] = *reinterpret_cast<const float4*>(zs + (size_t)jc * D + c0);
+      rv[t] = ld_elem<T>(v + o + rn);
+      rg[t] = ld_elem<T>(dout + o + rn);
+      rdv[t] = ld_elem<T>(dv + o + rn);
+      rkc[t] = ld_elem<T>(k + o + rl);
+      rqc[t] = ld_elem<T>(q + o + rl);
+      rzc[t] = zs[(size_t)jc * D + rl];
+      rdq[t] = ld_elem<T>(dq + o + rl);
+      rdk[t] = ld_elem<T>(dk + o + rl);
+      rb[t] = beta[(size_t)bh * N + jc];
+    };
+#pragma unroll
+    for (int t = 0; t < kRingW; ++t) ld_wrow(N - 1 - t, wr[t]);
+#pragma unroll
+    for (int t = 0; t < kAhead; ++t) fetch(N - 1 - t, t);
+    for (int i0 = N - 1; i0 >= 0; i0 -= kAhead)
+#pragma unroll
+    for (int t = 0; t < kAhead; ++t) {
+      const int i = i0 - t;
+      if (i < 0) break;
+      float xk[CPL], xq[CPL];
+      quad_to_f32(rk[t], xk);
+      quad_to_f32(rq[t], xq);
+      float zi[CPL] = {rz[t].x, rz[t].y, rz[t].z, rz[t].w};
+      float xv = rv[t], xg = rg[t], odv = rdv[t], bt = rb[t];
+      float xkc = rkc[t], xqc = rqc[t], zic = rzc[t], odq = rdq[t], odk = rdk[t];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) take(xk[c]), take(xq[c]), take(zi[c]);
+      take(xv), take(xg), take(odv), take(bt);
+      take(xkc), take(xqc), take(zic), take(odq), take(odk);
+      fetch(i - kAhead, t);
+      const float* wi = wr[t % kRingW];
+      const float* wp = wr[(t + 1) % kRingW];  // W_{i-1} (W_0 at i = 0, ignored)
+      const float wm = i > 0 ? 1.f : 0.f;
+      // G_{i+1} carried back through step i + 1's write
+      if (i + 1 < N) {
+        const float gp1 = row_sum<LPR>(dot_split<CPL>(gr, pkn));
+        const float m = bt_next * gp1;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) gr[c] = fmaf(-m, pkn[c], gr[c]);
+      }
+      // p(k_i), p(q_i) at the lane's columns and at feature r
+      float fk[CPL], fq[CPL], sk = 0.f, sq = 0.f;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        fk[c] = phi_l(xk[c], 0);
+        fq[c] = phi_l(xq[c], 0);
+        sk += fk[c];
+        sq += fq[c];
+      }
+      sk = row_sum<LPR>(sk);
+      sq = row_sum<LPR>(sq);
+      const float ik = 1.f / sk, iq = 1.f / sq;
+      float pk[CPL], pq[CPL];
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        pk[c] = fk[c] * ik;
+        pq[c] = fq[c] * iq;
+      }
+      const float pkc = phi_l(xkc, 0) * ik, pqc = phi_l(xqc, 0) * iq;
+      // n_r, s, fw_r; dn_r, ds
+      const float nr = row_sum<LPR>(dot_split<CPL>(wi, pq));
+      const float s_i = row_sum<LPR>(dot_split<CPL>(zi, pq));
+      const float is = 1.f / s_i;  // (products by reciprocals, as for p)
+      const float fw = nr * is;
+      const float gdot = wave_sum<4>(g == 0 ? xg * fw : 0.f);  // g_i . fw_i
+      acc_gfw += r == 0 ? gdot : 0.f;
+      const float dn = sf * xg * is;
+      const float ds = -sf * gdot * is;
+      // G_i, Zs_i
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) gr[c] = fmaf(dn, pq[c], gr[c]);
+      zs_col = fmaf(ds, pqc, zs_col);
+      // e_r, gp_r, dbeta
+      const float u = wm * row_sum<LPR>(dot_split<CPL>(wp, pk));
+      const float gp = row_sum<LPR>(dot_split<CPL>(gr, pk));
+      const float gpw = wm * gp;
+      const float e = xv - u;
+      const float db = wave_sum<4>(g == 0 ? e * gp : 0.f);
+      // the column sums W_i^T dn and G_i^T e - W_{i-1}^T gp through LDS
+      *reinterpret_cast<float4*>(cn1 + rn * LDN + c0) =
+          make_float4(wi[0] * dn, wi[1] * dn, wi[2] * dn, wi[3] * dn);
+      *reinterpret_cast<float4*>(cn2 + rn * LDN + c0) =
+          make_float4(fmaf(gr[0], e, -wp[0] * gpw), fmaf(gr[1], e, -wp[1] * gpw),
+                      fmaf(gr[2], e, -wp[2] * gpw), fmaf(gr[3], e, -wp[3] * gpw));
+      __syncthreads();
+      float a0 = 0.f, a1 = 0.f, b0 = 0.f, b1 = 0.f;
+      if (col) {
+#pragma unroll
+        for (int rr = 0; rr < D; rr += 2) {
+          a0 += cn1[rr * LDN + r];
+          a1 += cn1[(rr + 1) * LDN + r];
+          b0 += cn2[rr * LDN + r];
+          b1 += cn2[(rr + 1) * LDN + r];
+        }
+      }
+      __syncthreads();  // the buffers are rewritten next step
+      const float dpq = (a0 + a1) + ds * zic;
+      const float dpk = bt * (b0 + b1) + zs_col;
+      const float tq = wave_sum<1>(col ? dpq * pqc : 0.f);
+      const float tk = wave_sum<1>(col ? dpk * pkc : 0.f);
+      const size_t o = base + (size_t)i * D;
+      if (col) {
+        const float gq = (xqc > 0.f ? 1.f : __expf(xqc)) * (dpq - tq) * iq;
+        const float gk = (xkc > 0.f ? 1.f : __expf(xkc)) * (dpk - tk) * ik;
+        st_elem<T>(dq + o + r, odq + gq);
+        st_elem<T>(dk + o + r, odk + gk);
+      }
+      if (g == 0) st_elem<T>(dv + o + rn, odv + bt * gp);
+      if (r == 0) dbeta[(size_t)bh * N + i] = db;
+      bt_next = bt;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) pkn[c] = pk[c];
+      // W_i's slot takes W_{i-kRingW}
+      ld_wrow(i - kRingW, wr[t % kRingW]);
+    }
+  } else {
   float grow[D];
 #pragma unroll
   for (int c = 0; c < D; ++c) grow[c] = 0.f;
   float zsr = 0.f;       // Zs[r]
   float bt_next = 0.f;   // beta_{i+1}
-  float acc_gfw = 0.f;   // this thread's share of sum_i g_i . fw_i
   // row r of W_j (of W_0 for j < 0, which the step then ignores)
   auto ld_row = [&](int j, float* w) {
     const float* src = ws + ((size_t)(j < 0 ? 0 : j) * D + rl) * D;
@@ -588,6 +742,7 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
     // W_i's slot takes W_{i-kRingW}
     ld_row(i - kRingW, wr[t % kRingW]);
   }
+  }
   if (r == 0) gfw[bh] = acc_gfw;
 }
 
@@ -605,7 +760,9 @@ __global__ void k_fw_dw(const float* __restrict__ gfw, const float* __restrict__
 
 template <typename T, int D>
 void launch_fw_bwd_d(Launcher& L, const FwBwdArgs& a) {
-  const size_t lds = (size_t)2 * D * (D + 1) * sizeof(float);
+  // two D x (D + 4) buffers (rows padded by one float, or by four where
+  // they are written as quads)
+  const size_t lds = (size_t)2 * D * (D + 4) * sizeof(float);
   static std::atomic<unsigned long long> lds_set{0};
   if (L.note(lds_limit_once((const void*)k_fast_weight_bwd<T, D>, (int)lds, lds_set)) !=
       hipSuccess)

@@ -117,3 +117,11 @@ def test_fast_weight_backward_short_and_many_slices(dtype):
     check_fw_backward(1, 1, 1, 16, 0, 0, dtype, 4600)
     check_fw_backward(3, 2, 2, 64, 5, 1, dtype, 4610)
     check_fw_backward(8, 8, 33, 32, 8, 1, dtype, 4620)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_fast_weight_backward_narrow_lengths(dtype):
+    # d = 16 (four lanes per row of W): lengths below, at and between the
+    # steps the inputs are loaded ahead
+    for i, n in enumerate((2, 3, 4, 5, 9, 130)):
+        check_fw_backward(2, 3, n, 16, 3, i % 2, dtype, 4700 + i)
