@@ -796,7 +796,9 @@ def main():
     fw_rec = {"shape": "B=16 H=8 N=256 d=16 f32 k=20, fast weight + linear far field, causal",
               "ms_per_call": round(tfw * 1e3, 4),
               "tokens_per_s": round(wl4.B * wl4.N / tfw, 1),
-              "scan_kernel_us": round(ms_fw * 1e3 / n_fw, 3) if n_fw else None,
+              # the normalisation pass and the sequential scan, per call
+              "fast_weight_kernels_us_per_call": round(ms_fw * 1e3 / args.steps, 3)
+              if n_fw else None,
               "backward_ms_per_call": round(tfwb * 1e3, 4)}
     del qf, kf, vf, of, bf
 

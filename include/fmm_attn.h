@@ -308,7 +308,8 @@ int fmm_attn_layer_backward(const void* x, const void* w_qkv, const void* w_out,
  *   n_linear: 0 or 1.
  * Other arguments as fmm_attn_forward_ex (dtype FMM_DTYPE_F32 or _BF16).  The
  * recurrence is sequential in i: its cost grows with N at one step latency
- * per row, not with bandwidth.  Uses the library-owned workspace.
+ * per row, not with bandwidth.  Uses the library-owned workspace (for
+ * d = 16 and 32 it also holds p(k) and p(q) of every row, 2*B*H*N*d floats).
  */
 int fmm_attn_forward_fastweight(const void* q, const void* k, const void* v,
                                 const float* beta, void* out, int B, int H, int N, int d,

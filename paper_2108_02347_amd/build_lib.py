@@ -24,7 +24,7 @@ VARIANTS = [
     # accumulation registers beside the vector registers
     ("fmm_bwd.hip", "fmm_bwd_f32_d128", ["-DFMM_BWD_F32_D128"], False),
 ]
-HEADERS = ["fmm_device.h", "fmm_launch.h", "fmm_oct.h", "fmm_apply.h"]
+HEADERS = ["fmm_device.h", "fmm_launch.h", "fmm_oct.h", "fmm_apply.h", "fmm_fw.h"]
 
 
 def hipcc() -> str:

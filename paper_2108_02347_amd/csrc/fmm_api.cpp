@@ -17,6 +17,7 @@
 
 #include "../../include/fmm_attn.h"
 #include "fmm_launch.h"
+#include "fmm_fw.h"
 
 namespace {
 
@@ -798,8 +799,11 @@ int run_fastweight(const void* q, const void* k, const void* v, const float* bet
   const Plan p = plan_for(B, H, N, d, band_k, 1, 1, dtype);
   if (p.ws_bytes == 0) return FMM_ERR_UNSUPPORTED;
   // the operator's records, then H floats of -inf that remove its linear
-  // far part when n_linear = 0
-  const size_t total = p.ws_bytes + align256((size_t)H * 4);
+  // far part when n_linear = 0, then p(k) and p(q) of every position for the
+  // narrow scan
+  const size_t pre_bytes = fmm::fast_weight_pre_bytes(B, H, N, d);
+  if (pre_bytes > SIZE_MAX / 4) return FMM_ERR_UNSUPPORTED;
+  const size_t total = p.ws_bytes + align256((size_t)H * 4) + align256(pre_bytes);
   fmm::LaunchArgs a = make_args(q, k, v, out, B, H, N, d, band_k, 1, 1, w_near, w_far, dtype,
                                 FMM_FAR_NORM_PER_MAP, nullptr, p, stream);
   fmm::FwArgs f;
@@ -821,7 +825,12 @@ int run_fastweight(const void* q, const void* k, const void* v, const float* bet
     fmm::Launcher dry;
     dry.timer = &t;
     dry.dry = true;
-    if (fmm::launch_forward(a, dry) != hipSuccess || fmm::launch_fast_weight(dry, f) != hipSuccess)
+    // (the dry pass only checks grids: the scratch pointer just selects the
+    // kernels)
+    static float dry_placeholder;
+    if (fmm::launch_forward(a, dry) != hipSuccess ||
+        fmm::launch_fast_weight_pre(dry, f, pre_bytes ? &dry_placeholder : nullptr) !=
+            hipSuccess)
       return dry.err == hipErrorInvalidConfiguration ? FMM_ERR_UNSUPPORTED : FMM_ERR_HIP;
   }
   std::lock_guard<std::mutex> wl(ws_mutex());
@@ -831,6 +840,9 @@ int run_fastweight(const void* q, const void* k, const void* v, const float* bet
   a.ws = (float*)ws;
   float* minus_inf =
       reinterpret_cast<float*>(reinterpret_cast<uintptr_t>(ws) + p.ws_bytes);
+  float* pre = pre_bytes ? reinterpret_cast<float*>(reinterpret_cast<uintptr_t>(ws) + p.ws_bytes +
+                                                    align256((size_t)H * 4))
+                         : nullptr;
   std::lock_guard<std::mutex> g(t.mu);
   fmm::Launcher L;
   L.timer = &t;
@@ -839,7 +851,7 @@ int run_fastweight(const void* q, const void* k, const void* v, const float* bet
     a.w_far = minus_inf;
   }
   if (fmm::launch_forward(a, L) != hipSuccess) return FMM_ERR_HIP;
-  return fmm::launch_fast_weight(L, f) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
+  return fmm::launch_fast_weight_pre(L, f, pre) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
 }
 
 // Backward of the fast-weight operator: the operator's backward at rank 1,

@@ -18,9 +18,11 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <type_traits>
 
 #include "fmm_device.h"
 #include "fmm_launch.h"
+#include "fmm_fw.h"
 
 namespace fmm {
 namespace {
@@ -192,21 +194,24 @@ __device__ __forceinline__ float row_sum(float x) {
   return x;
 }
 
-template <typename T, int D>
+template <typename T, int D, bool PRE>
 __global__ __launch_bounds__(64) void k_fast_weight_narrow(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
-    const float* __restrict__ beta, T* __restrict__ out, const float* __restrict__ w_far, int H,
-    int N) {
+    const float* __restrict__ beta, T* __restrict__ out, const float* __restrict__ w_far,
+    const float* __restrict__ pre, int H, int N) {
   static_assert(D == 16 || D == 32, "rows shared by 64 / d lanes");
   constexpr int LPR = 64 / D;    // lanes per row of W
   constexpr int CPL = D / LPR;   // columns per lane
   constexpr int NQ = CPL / 4;    // quads per lane
   constexpr int kAhead = ahead_steps<D>();
-  typedef typename QuadOf<T>::type quad_t;
+  // PRE: p(k) and p(q) of every position already formed by k_fw_normalise
+  // (pre holds p(k), then p(q), fp32 in the layout of k); else from k and q
+  typedef typename std::conditional<PRE, float4, typename QuadOf<T>::type>::type quad_t;
   const int bh = blockIdx.x, h = bh % H;
   const int lane = threadIdx.x;
   const int r = lane / LPR, c0 = (lane % LPR) * CPL;
   const size_t base = (size_t)bh * N * D;
+  const size_t pq_off = (size_t)gridDim.x * N * D;
   const float sf = sigmoidf_exact(w_far[h]);
   float w[CPL], z[CPL];
 #pragma unroll
@@ -219,8 +224,13 @@ __global__ __launch_bounds__(64) void k_fast_weight_narrow(
     const size_t o = base + (size_t)jc * D;
 #pragma unroll
     for (int m = 0; m < NQ; ++m) {
-      rk[t][m] = *reinterpret_cast<const quad_t*>(k + o + c0 + 4 * m);
-      rq[t][m] = *reinterpret_cast<const quad_t*>(q + o + c0 + 4 * m);
+      if constexpr (PRE) {
+        rk[t][m] = *reinterpret_cast<const float4*>(pre + o + c0 + 4 * m);
+        rq[t][m] = *reinterpret_cast<const float4*>(pre + pq_off + o + c0 + 4 * m);
+      } else {
+        rk[t][m] = *reinterpret_cast<const quad_t*>(k + o + c0 + 4 * m);
+        rq[t][m] = *reinterpret_cast<const quad_t*>(q + o + c0 + 4 * m);
+      }
     }
     rv[t] = ld_elem<T>(v + o + r);
     ro[t] = ld_elem<T>(out + o + r);
@@ -244,25 +254,33 @@ __global__ __launch_bounds__(64) void k_fast_weight_narrow(
     for (int c = 0; c < CPL; ++c) take(xk[c]), take(xq[c]);
     take(xv), take(xo), take(bt);
     fetch(i + kAhead, t);
-    float fk[CPL], fq[CPL];
-    float sk = 0.f, sq = 0.f;
-#pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      fk[c] = phi_l(xk[c], 0);
-      fq[c] = phi_l(xq[c], 0);
-      sk += fk[c];
-      sq += fq[c];
-    }
-    sk = row_sum<LPR>(sk);
-    sq = row_sum<LPR>(sq);
-    // one division per sum, then products (within an ulp or so of the
-    // quotients, and a quarter of the instructions)
-    const float ik = 1.f / sk, iq = 1.f / sq;
     float pk[CPL], pq[CPL];
+    if constexpr (PRE) {
 #pragma unroll
-    for (int c = 0; c < CPL; ++c) {
-      pk[c] = fk[c] * ik;
-      pq[c] = fq[c] * iq;
+      for (int c = 0; c < CPL; ++c) {
+        pk[c] = xk[c];
+        pq[c] = xq[c];
+      }
+    } else {
+      float fk[CPL], fq[CPL];
+      float sk = 0.f, sq = 0.f;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        fk[c] = phi_l(xk[c], 0);
+        fq[c] = phi_l(xq[c], 0);
+        sk += fk[c];
+        sq += fq[c];
+      }
+      sk = row_sum<LPR>(sk);
+      sq = row_sum<LPR>(sq);
+      // one division per sum, then products (within an ulp or so of the
+      // quotients, and a quarter of the instructions)
+      const float ik = 1.f / sk, iq = 1.f / sq;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        pk[c] = fk[c] * ik;
+        pq[c] = fq[c] * iq;
+      }
     }
     // u_r = W_r . p(k); W_r += beta (v_r - u_r) p(k); num_r = W_r . p(q);
     // z += p(k); den = z . p(q)
@@ -277,6 +295,38 @@ __global__ __launch_bounds__(64) void k_fast_weight_narrow(
     const float den = row_sum<LPR>(dot_split<CPL>(z, pq));
     if (lane % LPR == 0 && sf > 0.f)
       st_elem<T>(out + base + (size_t)i * D + r, xo + sf * (num / den));
+  }
+}
+
+// p(k) and p(q) of every position (fp32, in the layout of k), one thread per
+// (slice, position): the normalisation the narrow scan would otherwise redo
+// on its sequential path
+template <typename T, int D>
+__global__ __launch_bounds__(256) void k_fw_normalise(const T* __restrict__ k,
+                                                      const T* __restrict__ q,
+                                                      float* __restrict__ pre, size_t rows) {
+  const size_t row = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= rows) return;
+#pragma unroll
+  for (int which = 0; which < 2; ++which) {
+    const T* x = (which ? q : k) + row * D;
+    float* p = pre + (which ? rows * D : 0) + row * D;
+    float f[D];
+    float s = 0.f;
+#pragma unroll
+    for (int m = 0; m < D / 4; ++m) {
+      quad_to_f32(*reinterpret_cast<const typename QuadOf<T>::type*>(x + 4 * m), f + 4 * m);
+#pragma unroll
+      for (int c = 4 * m; c < 4 * m + 4; ++c) {
+        f[c] = phi_l(f[c], 0);
+        s += f[c];
+      }
+    }
+    const float inv = 1.f / s;
+#pragma unroll
+    for (int c = 0; c < D; c += 4)
+      *reinterpret_cast<float4*>(p + c) =
+          make_float4(f[c] * inv, f[c + 1] * inv, f[c + 2] * inv, f[c + 3] * inv);
   }
 }
 
@@ -788,11 +838,20 @@ hipError_t launch_fw_bwd_t(Launcher& L, const FwBwdArgs& a) {
 }
 
 template <typename T, int D>
-void launch_fw_d(Launcher& L, const FwArgs& a) {
+void launch_fw_d(Launcher& L, const FwArgs& a, float* pre) {
   if constexpr (D <= 32) {
-    L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight_narrow<T, D>, dim3(a.B * a.H), dim3(64), 0,
-      (hipStream_t)a.stream, (const T*)a.q, (const T*)a.k, (const T*)a.v, a.beta, (T*)a.out,
-      a.w_far, a.H, a.N);
+    if (pre) {
+      const size_t rows = (size_t)a.B * a.H * a.N;
+      L(FMM_KERNEL_FAST_WEIGHT, k_fw_normalise<T, D>, dim3((unsigned)((rows + 255) / 256)),
+        dim3(256), 0, (hipStream_t)a.stream, (const T*)a.k, (const T*)a.q, pre, rows);
+      L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight_narrow<T, D, true>, dim3(a.B * a.H), dim3(64), 0,
+        (hipStream_t)a.stream, (const T*)a.q, (const T*)a.k, (const T*)a.v, a.beta, (T*)a.out,
+        a.w_far, (const float*)pre, a.H, a.N);
+    } else {
+      L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight_narrow<T, D, false>, dim3(a.B * a.H), dim3(64), 0,
+        (hipStream_t)a.stream, (const T*)a.q, (const T*)a.k, (const T*)a.v, a.beta, (T*)a.out,
+        a.w_far, (const float*)nullptr, a.H, a.N);
+    }
   } else {
     L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight<T, D>, dim3(a.B * a.H), dim3(D > 64 ? D : 64), 0,
       (hipStream_t)a.stream, (const T*)a.q, (const T*)a.k, (const T*)a.v, a.beta, (T*)a.out,
@@ -801,12 +860,12 @@ void launch_fw_d(Launcher& L, const FwArgs& a) {
 }
 
 template <typename T>
-hipError_t launch_fw_t(Launcher& L, const FwArgs& a) {
+hipError_t launch_fw_t(Launcher& L, const FwArgs& a, float* pre) {
   switch (a.d) {
-    case 16: launch_fw_d<T, 16>(L, a); break;
-    case 32: launch_fw_d<T, 32>(L, a); break;
-    case 64: launch_fw_d<T, 64>(L, a); break;
-    case 128: launch_fw_d<T, 128>(L, a); break;
+    case 16: launch_fw_d<T, 16>(L, a, pre); break;
+    case 32: launch_fw_d<T, 32>(L, a, pre); break;
+    case 64: launch_fw_d<T, 64>(L, a, pre); break;
+    case 128: launch_fw_d<T, 128>(L, a, pre); break;
     default: return L.note(hipErrorInvalidValue);
   }
   return L.err;
@@ -820,7 +879,16 @@ __global__ void k_fill(float* __restrict__ p, int n, float x) {
 }  // namespace
 
 hipError_t launch_fast_weight(Launcher& L, const FwArgs& a) {
-  return a.dtype == FMM_DTYPE_BF16 ? launch_fw_t<bf16_t>(L, a) : launch_fw_t<float>(L, a);
+  return launch_fast_weight_pre(L, a, nullptr);
+}
+
+size_t fast_weight_pre_bytes(int B, int H, int N, int d) {
+  return d <= 32 ? (size_t)2 * B * H * N * d * sizeof(float) : 0;
+}
+
+hipError_t launch_fast_weight_pre(Launcher& L, const FwArgs& a, float* pre) {
+  return a.dtype == FMM_DTYPE_BF16 ? launch_fw_t<bf16_t>(L, a, pre)
+                                   : launch_fw_t<float>(L, a, pre);
 }
 
 hipError_t launch_fast_weight_backward(Launcher& L, const FwBwdArgs& a) {
