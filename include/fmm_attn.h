@@ -328,7 +328,8 @@ int fmm_attn_forward_fastweight(const void* q, const void* k, const void* v,
  * dbeta_i = (v_i - u_i) . G_i p(k_i) and the key and query gradients follow;
  * the near field and the linear part are those of fmm_attn_backward (rank 1,
  * causal).  The states W_i of every step are kept in the library-owned
- * workspace: B*H*N*d*(d+1) floats beside the backward's own.  No output may
+ * workspace: B*H*N*d*(d+1) floats beside the backward's own (and, for d = 16
+ * and 32, 2*B*H*N*(d+1) more).  No output may
  * overlap an input or another output.  Errors as fmm_attn_backward.
  */
 int fmm_attn_backward_fastweight(const void* q, const void* k, const void* v,

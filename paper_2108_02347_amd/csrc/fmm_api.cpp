@@ -894,12 +894,17 @@ int run_backward_fastweight(const void* q, const void* k, const void* v, const f
   // sums, H floats of -inf
   typedef unsigned __int128 u128;
   const u128 wst = (u128)B * H * N * d * d * 4, zst = (u128)B * H * N * d * 4;
+  // then, for d = 16 and 32, p(k), p(q) and their inverse sums of every
+  // position for the narrow sweeps
+  const size_t pre_bytes = fmm::fast_weight_backward_pre_bytes(B, H, N, d);
   const u128 tot = (u128)bp.total + align256((size_t)std::min<u128>(wst, SIZE_MAX / 8)) +
                    align256((size_t)std::min<u128>(zst, SIZE_MAX / 8)) +
-                   align256((size_t)B * H * 4) + align256((size_t)H * 4);
+                   align256((size_t)B * H * 4) + align256((size_t)H * 4) +
+                   align256(std::min<size_t>(pre_bytes, SIZE_MAX / 8));
   if (tot > (u128)(SIZE_MAX / 4)) return FMM_ERR_UNSUPPORTED;
   const size_t off_w = bp.total, off_z = off_w + align256((size_t)wst);
   const size_t off_g = off_z + align256((size_t)zst), off_m = off_g + align256((size_t)B * H * 4);
+  const size_t off_p = off_m + align256((size_t)H * 4);
   fmm::LaunchArgs fa = make_args(q, k, v, dq, B, H, N, d, band_k, 1, 1, w_near, w_far, dtype,
                                  FMM_FAR_NORM_PER_MAP, nullptr, bp.p, stream);
   fmm::BwdArgs ba;
@@ -951,9 +956,11 @@ int run_backward_fastweight(const void* q, const void* k, const void* v, const f
     fmm::Launcher dry;
     dry.timer = &t;
     dry.dry = true;
+    static float dry_placeholder;  // (selects the kernels; the dry pass reads nothing)
     if (fmm::launch_state_only(fa, dry) != hipSuccess ||
         fmm::launch_backward_tail(ba, dry) != hipSuccess ||
-        fmm::launch_fast_weight_backward(dry, fb) != hipSuccess)
+        fmm::launch_fast_weight_backward_pre(dry, fb, pre_bytes ? &dry_placeholder : nullptr) !=
+            hipSuccess)
       return dry.err == hipErrorInvalidConfiguration ? FMM_ERR_UNSUPPORTED : FMM_ERR_HIP;
   }
   std::lock_guard<std::mutex> wl(ws_mutex());
@@ -967,6 +974,7 @@ int run_backward_fastweight(const void* q, const void* k, const void* v, const f
   fb.zst = reinterpret_cast<float*>(w + off_z);
   fb.gfw = reinterpret_cast<float*>(w + off_g);
   float* minus_inf = reinterpret_cast<float*>(w + off_m);
+  float* pre = pre_bytes ? reinterpret_cast<float*>(w + off_p) : nullptr;
   std::lock_guard<std::mutex> g(t.mu);
   fmm::Launcher L;
   L.timer = &t;
@@ -977,7 +985,7 @@ int run_backward_fastweight(const void* q, const void* k, const void* v, const f
   }
   if (fmm::launch_state_only(fa, L) != hipSuccess) return FMM_ERR_HIP;
   if (fmm::launch_backward_tail(ba, L) != hipSuccess) return FMM_ERR_HIP;
-  return fmm::launch_fast_weight_backward(L, fb) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
+  return fmm::launch_fast_weight_backward_pre(L, fb, pre) == hipSuccess ? FMM_OK : FMM_ERR_HIP;
 }
 
 }  // namespace

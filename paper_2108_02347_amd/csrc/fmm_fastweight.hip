@@ -304,7 +304,8 @@ __global__ __launch_bounds__(64) void k_fast_weight_narrow(
 template <typename T, int D>
 __global__ __launch_bounds__(256) void k_fw_normalise(const T* __restrict__ k,
                                                       const T* __restrict__ q,
-                                                      float* __restrict__ pre, size_t rows) {
+                                                      float* __restrict__ pre, size_t rows,
+                                                      float* __restrict__ inv_sums) {
   const size_t row = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (row >= rows) return;
 #pragma unroll
@@ -323,6 +324,7 @@ __global__ __launch_bounds__(256) void k_fw_normalise(const T* __restrict__ k,
       }
     }
     const float inv = 1.f / s;
+    if (inv_sums) inv_sums[which * rows + row] = inv;
 #pragma unroll
     for (int c = 0; c < D; c += 4)
       *reinterpret_cast<float4*>(p + c) =
@@ -349,14 +351,22 @@ __global__ __launch_bounds__(256) void k_fw_normalise(const T* __restrict__ k,
 // adds its dq, dk, dv to the gradients already in place (the near field and
 // the linear part, from the operator's backward); it writes dbeta and, per
 // slice, sum_i g_i . fw_i for dw_far.
-template <typename T, int D>
+// PRE (d <= 32): p(k), p(q) and the inverse sums 1 / sum(phi_1(k)),
+// 1 / sum(phi_1(q)) of every position already formed by k_fw_normalise in
+// `pre` (p(k), p(q), then the two inverse sums); the narrow sweeps read them
+// in place of k and q.
+template <typename T, int D, bool PRE>
 __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const float* __restrict__ beta, const T* __restrict__ dout, T* __restrict__ dq,
     T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ dbeta,
     float* __restrict__ wst, float* __restrict__ zst, float* __restrict__ gfw,
-    const float* __restrict__ w_far, int H, int N) {
+    const float* __restrict__ w_far, const float* __restrict__ pre, int H, int N) {
   constexpr int NWV = D > 64 ? D / 64 : 1;
+  const size_t prow = (size_t)gridDim.x * N;  // rows of pre
+  const float* pre_q = PRE ? pre + prow * D : nullptr;
+  const float* pre_ik = PRE ? pre + 2 * prow * D : nullptr;
+  const float* pre_iq = PRE ? pre + 2 * prow * D + prow : nullptr;
   constexpr int kAhead = ahead_steps<D>();
   constexpr int ROWS = D >= 64 ? 4 : D / 16;
   constexpr int LD = D + 1;  // padded rows of the column-sum buffers
@@ -390,7 +400,7 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
     // narrow heads: 64 / d lanes per row of W, each with d / (64 / d) of its
     // columns (and the same columns of z), as in k_fast_weight_narrow
     constexpr int LPR = 64 / D, CPL = D / LPR, NQ = CPL / 4;
-    typedef typename QuadOf<T>::type quad_t;
+    typedef typename std::conditional<PRE, float4, typename QuadOf<T>::type>::type quad_t;
     const int rn = r / LPR, c0 = (r % LPR) * CPL;
     float w[CPL], z[CPL];
 #pragma unroll
@@ -402,7 +412,8 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
       const size_t o = base + (size_t)jc * D;
 #pragma unroll
       for (int m = 0; m < NQ; ++m)
-        rkq[t][m] = *reinterpret_cast<const quad_t*>(k + o + c0 + 4 * m);
+        rkq[t][m] = PRE ? *reinterpret_cast<const quad_t*>(pre + o + c0 + 4 * m)
+                        : *reinterpret_cast<const quad_t*>(k + o + c0 + 4 * m);
       rv[t] = ld_elem<T>(v + o + rn);
       rb[t] = beta[(size_t)bh * N + jc];
     };
@@ -421,16 +432,21 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
       for (int c = 0; c < CPL; ++c) take(xk[c]);
       take(xv), take(bt);
       fetch(i + kAhead, t);
-      float fk[CPL], sk = 0.f;
-#pragma unroll
-      for (int c = 0; c < CPL; ++c) {
-        fk[c] = phi_l(xk[c], 0);
-        sk += fk[c];
-      }
-      const float ik = 1.f / row_sum<LPR>(sk);
       float pk[CPL];
+      if constexpr (PRE) {
 #pragma unroll
-      for (int c = 0; c < CPL; ++c) pk[c] = fk[c] * ik;
+        for (int c = 0; c < CPL; ++c) pk[c] = xk[c];
+      } else {
+        float fk[CPL], sk = 0.f;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          fk[c] = phi_l(xk[c], 0);
+          sk += fk[c];
+        }
+        const float ik = 1.f / row_sum<LPR>(sk);
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) pk[c] = fk[c] * ik;
+      }
       const float u = row_sum<LPR>(dot_split<CPL>(w, pk));
       const float coef = bt * (xv - u);
 #pragma unroll
@@ -509,7 +525,7 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
     constexpr int LPR = 64 / D, CPL = D / LPR;
     constexpr int LDN = D + 4;  // padded, 16-byte aligned rows of the column-sum buffers
     constexpr int kRingW = kAhead;
-    typedef typename QuadOf<T>::type quad_t;
+    typedef typename std::conditional<PRE, float4, typename QuadOf<T>::type>::type quad_t;
     static_assert(CPL == 4, "one quad of columns per lane");
     float* cn1 = colbuf;
     float* cn2 = colbuf + D * LDN;
@@ -533,17 +549,27 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
     float4 rz[kAhead];
     float rv[kAhead], rg[kAhead], rdv[kAhead], rb[kAhead];
     float rkc[kAhead], rqc[kAhead], rzc[kAhead], rdq[kAhead], rdk[kAhead];
+    float rik[kAhead], riq[kAhead];  // PRE: the row's inverse sums
     auto fetch = [&](int j, int t) {
       const int jc = j < 0 ? 0 : j;
       const size_t o = base + (size_t)jc * D;
-      rk[t] = *reinterpret_cast<const quad_t*>(k + o + c0);
-      rq[t] = *reinterpret_cast<const quad_t*>(q + o + c0);
+      if constexpr (PRE) {
+        rk[t] = *reinterpret_cast<const quad_t*>(pre + o + c0);
+        rq[t] = *reinterpret_cast<const quad_t*>(pre_q + o + c0);
+        rkc[t] = pre[o + rl];
+        rqc[t] = pre_q[o + rl];
+        rik[t] = pre_ik[(size_t)bh * N + jc];
+        riq[t] = pre_iq[(size_t)bh * N + jc];
+      } else {
+        rk[t] = *reinterpret_cast<const quad_t*>(k + o + c0);
+        rq[t] = *reinterpret_cast<const quad_t*>(q + o + c0);
+        rkc[t] = ld_elem<T>(k + o + rl);
+        rqc[t] = ld_elem<T>(q + o + rl);
+      }
       rz[t] = *reinterpret_cast<const float4*>(zs + (size_t)jc * D + c0);
       rv[t] = ld_elem<T>(v + o + rn);
       rg[t] = ld_elem<T>(dout + o + rn);
       rdv[t] = ld_elem<T>(dv + o + rn);
-      rkc[t] = ld_elem<T>(k + o + rl);
-      rqc[t] = ld_elem<T>(q + o + rl);
       rzc[t] = zs[(size_t)jc * D + rl];
       rdq[t] = ld_elem<T>(dq + o + rl);
       rdk[t] = ld_elem<T>(dk + o + rl);
@@ -564,6 +590,12 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
       float zi[CPL] = {rz[t].x, rz[t].y, rz[t].z, rz[t].w};
       float xv = rv[t], xg = rg[t], odv = rdv[t], bt = rb[t];
       float xkc = rkc[t], xqc = rqc[t], zic = rzc[t], odq = rdq[t], odk = rdk[t];
+      float xik = 0.f, xiq = 0.f;
+      if constexpr (PRE) {
+        xik = rik[t];
+        xiq = riq[t];
+        take(xik), take(xiq);
+      }
 #pragma unroll
       for (int c = 0; c < CPL; ++c) take(xk[c]), take(xq[c]), take(zi[c]);
       take(xv), take(xg), take(odv), take(bt);
@@ -580,24 +612,38 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
         for (int c = 0; c < CPL; ++c) gr[c] = fmaf(-m, pkn[c], gr[c]);
       }
       // p(k_i), p(q_i) at the lane's columns and at feature r
-      float fk[CPL], fq[CPL], sk = 0.f, sq = 0.f;
+      float pk[CPL], pq[CPL], ik, iq, pkc, pqc;
+      if constexpr (PRE) {
 #pragma unroll
-      for (int c = 0; c < CPL; ++c) {
-        fk[c] = phi_l(xk[c], 0);
-        fq[c] = phi_l(xq[c], 0);
-        sk += fk[c];
-        sq += fq[c];
-      }
-      sk = row_sum<LPR>(sk);
-      sq = row_sum<LPR>(sq);
-      const float ik = 1.f / sk, iq = 1.f / sq;
-      float pk[CPL], pq[CPL];
+        for (int c = 0; c < CPL; ++c) {
+          pk[c] = xk[c];
+          pq[c] = xq[c];
+        }
+        ik = xik;
+        iq = xiq;
+        pkc = xkc;
+        pqc = xqc;
+      } else {
+        float fk[CPL], fq[CPL], sk = 0.f, sq = 0.f;
 #pragma unroll
-      for (int c = 0; c < CPL; ++c) {
-        pk[c] = fk[c] * ik;
-        pq[c] = fq[c] * iq;
+        for (int c = 0; c < CPL; ++c) {
+          fk[c] = phi_l(xk[c], 0);
+          fq[c] = phi_l(xq[c], 0);
+          sk += fk[c];
+          sq += fq[c];
+        }
+        sk = row_sum<LPR>(sk);
+        sq = row_sum<LPR>(sq);
+        ik = 1.f / sk;
+        iq = 1.f / sq;
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+          pk[c] = fk[c] * ik;
+          pq[c] = fq[c] * iq;
+        }
+        pkc = phi_l(xkc, 0) * ik;
+        pqc = phi_l(xqc, 0) * iq;
       }
-      const float pkc = phi_l(xkc, 0) * ik, pqc = phi_l(xqc, 0) * iq;
       // n_r, s, fw_r; dn_r, ds
       const float nr = row_sum<LPR>(dot_split<CPL>(wi, pq));
       const float s_i = row_sum<LPR>(dot_split<CPL>(zi, pq));
@@ -641,8 +687,9 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
       const float tk = wave_sum<1>(col ? dpk * pkc : 0.f);
       const size_t o = base + (size_t)i * D;
       if (col) {
-        const float gq = (xqc > 0.f ? 1.f : __expf(xqc)) * (dpq - tq) * iq;
-        const float gk = (xkc > 0.f ? 1.f : __expf(xkc)) * (dpk - tk) * ik;
+        // phi_1'(x) / S = min(1, phi_1(x)) / S = min(1 / S, p(x))
+        const float gq = (PRE ? fminf(iq, pqc) : (xqc > 0.f ? 1.f : __expf(xqc)) * iq) * (dpq - tq);
+        const float gk = (PRE ? fminf(ik, pkc) : (xkc > 0.f ? 1.f : __expf(xkc)) * ik) * (dpk - tk);
         st_elem<T>(dq + o + r, odq + gq);
         st_elem<T>(dk + o + r, odk + gk);
       }
@@ -808,30 +855,47 @@ __global__ void k_fw_dw(const float* __restrict__ gfw, const float* __restrict__
   dw_far[h] += c * (1.f - c) * s;
 }
 
-template <typename T, int D>
-void launch_fw_bwd_d(Launcher& L, const FwBwdArgs& a) {
+template <typename T, int D, bool PRE>
+void launch_fw_bwd_k(Launcher& L, const FwBwdArgs& a, float* pre) {
   // two D x (D + 4) buffers (rows padded by one float, or by four where
   // they are written as quads)
   const size_t lds = (size_t)2 * D * (D + 4) * sizeof(float);
   static std::atomic<unsigned long long> lds_set{0};
-  if (L.note(lds_limit_once((const void*)k_fast_weight_bwd<T, D>, (int)lds, lds_set)) !=
+  if (L.note(lds_limit_once((const void*)k_fast_weight_bwd<T, D, PRE>, (int)lds, lds_set)) !=
       hipSuccess)
     return;
-  L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight_bwd<T, D>, dim3(a.B * a.H), dim3(D > 64 ? D : 64), lds,
-    (hipStream_t)a.stream, (const T*)a.q, (const T*)a.k, (const T*)a.v, a.beta,
-    (const T*)a.dout, (T*)a.dq, (T*)a.dk, (T*)a.dv, a.dbeta, a.wst, a.zst, a.gfw, a.w_far, a.H,
-    a.N);
+  L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight_bwd<T, D, PRE>, dim3(a.B * a.H),
+    dim3(D > 64 ? D : 64), lds, (hipStream_t)a.stream, (const T*)a.q, (const T*)a.k,
+    (const T*)a.v, a.beta, (const T*)a.dout, (T*)a.dq, (T*)a.dk, (T*)a.dv, a.dbeta, a.wst, a.zst,
+    a.gfw, a.w_far, (const float*)pre, a.H, a.N);
+}
+
+template <typename T, int D>
+void launch_fw_bwd_d(Launcher& L, const FwBwdArgs& a, float* pre) {
+  if constexpr (D <= 32) {
+    if (pre) {
+      const size_t rows = (size_t)a.B * a.H * a.N;
+      L(FMM_KERNEL_FAST_WEIGHT, k_fw_normalise<T, D>, dim3((unsigned)((rows + 255) / 256)),
+        dim3(256), 0, (hipStream_t)a.stream, (const T*)a.k, (const T*)a.q, pre, rows,
+        pre + 2 * rows * D);
+      launch_fw_bwd_k<T, D, true>(L, a, pre);
+    } else {
+      launch_fw_bwd_k<T, D, false>(L, a, nullptr);
+    }
+  } else {
+    launch_fw_bwd_k<T, D, false>(L, a, nullptr);
+  }
   L(FMM_KERNEL_FAST_WEIGHT, k_fw_dw, dim3((a.H + 63) / 64), dim3(64), 0, (hipStream_t)a.stream,
     (const float*)a.gfw, a.w_far, a.dw_far, a.B, a.H);
 }
 
 template <typename T>
-hipError_t launch_fw_bwd_t(Launcher& L, const FwBwdArgs& a) {
+hipError_t launch_fw_bwd_t(Launcher& L, const FwBwdArgs& a, float* pre) {
   switch (a.d) {
-    case 16: launch_fw_bwd_d<T, 16>(L, a); break;
-    case 32: launch_fw_bwd_d<T, 32>(L, a); break;
-    case 64: launch_fw_bwd_d<T, 64>(L, a); break;
-    case 128: launch_fw_bwd_d<T, 128>(L, a); break;
+    case 16: launch_fw_bwd_d<T, 16>(L, a, pre); break;
+    case 32: launch_fw_bwd_d<T, 32>(L, a, pre); break;
+    case 64: launch_fw_bwd_d<T, 64>(L, a, pre); break;
+    case 128: launch_fw_bwd_d<T, 128>(L, a, pre); break;
     default: return L.note(hipErrorInvalidValue);
   }
   return L.err;
@@ -843,7 +907,8 @@ void launch_fw_d(Launcher& L, const FwArgs& a, float* pre) {
     if (pre) {
       const size_t rows = (size_t)a.B * a.H * a.N;
       L(FMM_KERNEL_FAST_WEIGHT, k_fw_normalise<T, D>, dim3((unsigned)((rows + 255) / 256)),
-        dim3(256), 0, (hipStream_t)a.stream, (const T*)a.k, (const T*)a.q, pre, rows);
+        dim3(256), 0, (hipStream_t)a.stream, (const T*)a.k, (const T*)a.q, pre, rows,
+        (float*)nullptr);
       L(FMM_KERNEL_FAST_WEIGHT, k_fast_weight_narrow<T, D, true>, dim3(a.B * a.H), dim3(64), 0,
         (hipStream_t)a.stream, (const T*)a.q, (const T*)a.k, (const T*)a.v, a.beta, (T*)a.out,
         a.w_far, (const float*)pre, a.H, a.N);
@@ -892,7 +957,16 @@ hipError_t launch_fast_weight_pre(Launcher& L, const FwArgs& a, float* pre) {
 }
 
 hipError_t launch_fast_weight_backward(Launcher& L, const FwBwdArgs& a) {
-  return a.dtype == FMM_DTYPE_BF16 ? launch_fw_bwd_t<bf16_t>(L, a) : launch_fw_bwd_t<float>(L, a);
+  return launch_fast_weight_backward_pre(L, a, nullptr);
+}
+
+size_t fast_weight_backward_pre_bytes(int B, int H, int N, int d) {
+  return d <= 32 ? (size_t)2 * B * H * N * (d + 1) * sizeof(float) : 0;
+}
+
+hipError_t launch_fast_weight_backward_pre(Launcher& L, const FwBwdArgs& a, float* pre) {
+  return a.dtype == FMM_DTYPE_BF16 ? launch_fw_bwd_t<bf16_t>(L, a, pre)
+                                   : launch_fw_bwd_t<float>(L, a, pre);
 }
 
 hipError_t launch_fill(Launcher& L, float* p, int n, float x, void* stream) {
