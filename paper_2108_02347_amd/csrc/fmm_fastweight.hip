@@ -8,7 +8,9 @@
 // a step is two length-d dot products per thread and the rank-one update of
 // its row, plus three sums over the threads (sum of phi(k), sum of phi(q), the
 // denominator), by DPP within the wave; for d = 16 and 32, 64 / d lanes share
-// a row (k_fast_weight_narrow), which fills the wave and needs no LDS.  Each
+// a row (k_fast_weight_narrow), which fills the wave and needs no LDS, and a
+// parallel pass (k_fw_normalise) forms p(k) and p(q) of every position first,
+// so that the sequential step does not normalise.  Each
 // step's q, k, v, beta and output row are loaded a few steps ahead (memory
 // latency is longer than a step, and a load issued in the step that needs it
 // would hold up every later load: the memory counter is waited for in
