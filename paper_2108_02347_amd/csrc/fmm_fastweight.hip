@@ -295,8 +295,10 @@ __global__ __launch_bounds__(64) void k_fast_weight_narrow(
     }
     const float num = row_sum<LPR>(dot_split<CPL>(w, pq));
     const float den = row_sum<LPR>(dot_split<CPL>(z, pq));
+    // (the hardware reciprocal, within an ulp: the division's refinement
+    // would lengthen every step)
     if (lane % LPR == 0 && sf > 0.f)
-      st_elem<T>(out + base + (size_t)i * D + r, xo + sf * (num / den));
+      st_elem<T>(out + base + (size_t)i * D + r, xo + sf * (num * __builtin_amdgcn_rcpf(den)));
   }
 }
 
@@ -649,7 +651,7 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
       // n_r, s, fw_r; dn_r, ds
       const float nr = row_sum<LPR>(dot_split<CPL>(wi, pq));
       const float s_i = row_sum<LPR>(dot_split<CPL>(zi, pq));
-      const float is = 1.f / s_i;  // (products by reciprocals, as for p)
+      const float is = __builtin_amdgcn_rcpf(s_i);  // (the hardware reciprocal, within an ulp)
       const float fw = nr * is;
       const float gdot = wave_sum<4>(g == 0 ? xg * fw : 0.f);  // g_i . fw_i
       acc_gfw += r == 0 ? gdot : 0.f;
