@@ -528,6 +528,7 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
     // column sums read back, dq and dk) on lanes 0..15, one feature each.
     constexpr int LPR = 64 / D, CPL = D / LPR;
     constexpr int LDN = D + 4;  // padded, 16-byte aligned rows of the column-sum buffers
+    static_assert(D * LPR == 64 && D % 8 == 0, "four quarters of the wave, two rows at a time");
     constexpr int kRingW = kAhead;
     typedef typename std::conditional<PRE, float4, typename QuadOf<T>::type>::type quad_t;
     static_assert(CPL == 4, "one quad of columns per lane");
@@ -674,19 +675,29 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
           make_float4(fmaf(gr[0], e, -wp[0] * gpw), fmaf(gr[1], e, -wp[1] * gpw),
                       fmaf(gr[2], e, -wp[2] * gpw), fmaf(gr[3], e, -wp[3] * gpw));
       __syncthreads();
-      float a0 = 0.f, a1 = 0.f, b0 = 0.f, b1 = 0.f;
-      if (col) {
+      // each quarter of the wave sums four rows of feature r mod 16, then the
+      // quarters' sums are added across the wave (lanes 16 and 32 apart)
+      float c1, c2;
+      {
+        const int cc = r % D, r0 = (r / D) * (D / 4);
+        float a0 = 0.f, a1 = 0.f, b0 = 0.f, b1 = 0.f;
 #pragma unroll
-        for (int rr = 0; rr < D; rr += 2) {
-          a0 += cn1[rr * LDN + r];
-          a1 += cn1[(rr + 1) * LDN + r];
-          b0 += cn2[rr * LDN + r];
-          b1 += cn2[(rr + 1) * LDN + r];
+        for (int rr = 0; rr < D / 4; rr += 2) {
+          a0 += cn1[(r0 + rr) * LDN + cc];
+          a1 += cn1[(r0 + rr + 1) * LDN + cc];
+          b0 += cn2[(r0 + rr) * LDN + cc];
+          b1 += cn2[(r0 + rr + 1) * LDN + cc];
         }
+        c1 = a0 + a1;
+        c2 = b0 + b1;
+        c1 += __shfl_xor(c1, 16);
+        c2 += __shfl_xor(c2, 16);
+        c1 += __shfl_xor(c1, 32);
+        c2 += __shfl_xor(c2, 32);
       }
       __syncthreads();  // the buffers are rewritten next step
-      const float dpq = (a0 + a1) + ds * zic;
-      const float dpk = bt * (b0 + b1) + zs_col;
+      const float dpq = c1 + ds * zic;
+      const float dpk = bt * c2 + zs_col;
       const float tq = wave_sum<1>(col ? dpq * pqc : 0.f);
       const float tk = wave_sum<1>(col ? dpk * pkc : 0.f);
       const size_t o = base + (size_t)i * D;
