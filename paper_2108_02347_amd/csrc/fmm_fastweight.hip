@@ -205,7 +205,7 @@ __global__ __launch_bounds__(64) void k_fast_weight_narrow(
   constexpr int LPR = 64 / D;    // lanes per row of W
   constexpr int CPL = D / LPR;   // columns per lane
   constexpr int NQ = CPL / 4;    // quads per lane
-  constexpr int kAhead = ahead_steps<D>();
+  constexpr int kAhead = D <= 16 ? 8 : ahead_steps<D>();  // (d = 16: registers to spare)
   // PRE: p(k) and p(q) of every position already formed by k_fw_normalise
   // (pre holds p(k), then p(q), fp32 in the layout of k); else from k and q
   typedef typename std::conditional<PRE, float4, typename QuadOf<T>::type>::type quad_t;
