@@ -404,13 +404,14 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
     // narrow heads: 64 / d lanes per row of W, each with d / (64 / d) of its
     // columns (and the same columns of z), as in k_fast_weight_narrow
     constexpr int LPR = 64 / D, CPL = D / LPR, NQ = CPL / 4;
+    constexpr int kAheadF = D <= 16 ? 8 : kAhead;  // (d = 16: registers to spare)
     typedef typename std::conditional<PRE, float4, typename QuadOf<T>::type>::type quad_t;
     const int rn = r / LPR, c0 = (r % LPR) * CPL;
     float w[CPL], z[CPL];
 #pragma unroll
     for (int c = 0; c < CPL; ++c) w[c] = z[c] = 0.f;
-    quad_t rkq[kAhead][NQ];
-    float rv[kAhead], rb[kAhead];
+    quad_t rkq[kAheadF][NQ];
+    float rv[kAheadF], rb[kAheadF];
     auto fetch = [&](int j, int t) {
       const int jc = j < N ? j : N - 1;
       const size_t o = base + (size_t)jc * D;
@@ -422,10 +423,10 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
       rb[t] = beta[(size_t)bh * N + jc];
     };
 #pragma unroll
-    for (int t = 0; t < kAhead; ++t) fetch(t, t);
-    for (int i0 = 0; i0 < N; i0 += kAhead)
+    for (int t = 0; t < kAheadF; ++t) fetch(t, t);
+    for (int i0 = 0; i0 < N; i0 += kAheadF)
 #pragma unroll
-    for (int t = 0; t < kAhead; ++t) {
+    for (int t = 0; t < kAheadF; ++t) {
       const int i = i0 + t;
       if (i >= N) break;
       float xk[CPL];
@@ -435,7 +436,7 @@ __global__ __launch_bounds__(D > 64 ? D : 64) void k_fast_weight_bwd(
 #pragma unroll
       for (int c = 0; c < CPL; ++c) take(xk[c]);
       take(xv), take(bt);
-      fetch(i + kAhead, t);
+      fetch(i + kAheadF, t);
       float pk[CPL];
       if constexpr (PRE) {
 #pragma unroll
